@@ -1,0 +1,302 @@
+"""PVConv CPU oracle -- TEST INFRASTRUCTURE ONLY.
+
+Plain fp64 reference of one Point-Voxel Convolution layer and of the PVCNN
+network glue, written from the paper (Liu et al., "Point-Voxel CNN for
+Efficient 3D Deep Learning", Section 4 and Section 5.1 "Models"). The per-step
+arithmetic is in pvconv_oracle.c; this module loads it with ctypes and composes
+the steps in the paper's order. Only tests, the package smoke check and the
+benchmark's CPU-baseline leg may import it; the GPU library never does, and
+nothing here imports the GPU library.
+
+Every function takes and returns numpy arrays. Floating-point inputs are
+upcast to float64 exactly (fp32 and bf16-representable values are exact in
+fp64).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import List, Optional, Sequence
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "pvconv_oracle.c")
+_LIB_PATH = os.path.join(_HERE, "libpvconv_oracle.so")
+_lib = None
+
+_P = ctypes.c_void_p
+_I64 = ctypes.c_int64
+
+
+def build(verbose: bool = False) -> str:
+    """Compile the oracle with gcc (fp64, no FMA contraction, OpenMP)."""
+    cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fopenmp", "-ffp-contract=off",
+           "-Wall", "-Wextra", "-o", _LIB_PATH + ".tmp", _SRC, "-lm"]
+    if verbose:
+        print(" ".join(cmd))
+    subprocess.run(cmd, check=True)
+    os.replace(_LIB_PATH + ".tmp", _LIB_PATH)
+    return _LIB_PATH
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH) or os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC):
+        build()
+    lib = ctypes.CDLL(_LIB_PATH)
+    sig = {
+        "ref_normalize": [_P, _I64, _I64, _P, _P, _P],
+        "ref_voxel_ids": [_P, _I64, _I64, ctypes.c_int, _P],
+        "ref_voxelize": [_P, _P, _I64, _I64, _I64, ctypes.c_int, _P, _P],
+        "ref_conv3d": [_P, _I64, ctypes.c_int, _I64, _I64, _P, _P],
+        "ref_conv3d_at": [_P, _I64, ctypes.c_int, _I64, _I64, _P, _I64, _P, _P],
+        "ref_batchnorm": [_P, _I64, _I64, _P, _P, _P, _P, ctypes.c_double],
+        "ref_devoxelize": [_P, _I64, ctypes.c_int, _I64, _P, _I64, _P],
+        "ref_devoxelize_weights": [_P, _I64, ctypes.c_int, _P, _P],
+        "ref_linear": [_P, _I64, _I64, _I64, _P, _P, _P],
+        "ref_maxpool": [_P, _I64, _I64, _I64, _P],
+    }
+    for name, args in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = ctypes.c_int
+    lib.ref_leaky_relu.argtypes = [_P, _I64, ctypes.c_double]
+    lib.ref_leaky_relu.restype = None
+    lib.ref_relu.argtypes = [_P, _I64]
+    lib.ref_relu.restype = None
+    _lib = lib
+    return lib
+
+
+def _f64(a) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.float64)
+
+
+def _ptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _check(rc: int, what: str):
+    if rc != 0:
+        raise ValueError(f"oracle {what}: invalid input (rc={rc})")
+
+
+# ----------------------------------------------------------------------------
+# single steps (Section 4)
+# ----------------------------------------------------------------------------
+def normalize(coords: np.ndarray):
+    """coords [B][N][3] fp32 -> (centroid [B][3], radius [B], pnorm [B][N][3])."""
+    lib = _load()
+    coords = np.ascontiguousarray(coords, dtype=np.float32)
+    B, N, _ = coords.shape
+    c = np.empty((B, 3))
+    m = np.empty(B)
+    pn = np.empty((B, N, 3))
+    _check(lib.ref_normalize(_ptr(coords), B, N, _ptr(c), _ptr(m), _ptr(pn)), "normalize")
+    return c, m, pn
+
+
+def voxel_ids(pnorm: np.ndarray, R: int) -> np.ndarray:
+    """pnorm [B][N][3] -> ids [B][N] int32 (Eq. 2 indicator, clamped)."""
+    lib = _load()
+    pnorm = _f64(pnorm)
+    B, N, _ = pnorm.shape
+    ids = np.empty((B, N), np.int32)
+    _check(lib.ref_voxel_ids(_ptr(pnorm), B, N, R, _ptr(ids)), "voxel_ids")
+    return ids
+
+
+def voxelize(ids: np.ndarray, feats: np.ndarray, R: int):
+    """ids [B][N], feats [B][N][C] -> (grid [B][R^3][C] fp64, counts [B][R^3] int32)."""
+    lib = _load()
+    ids = np.ascontiguousarray(ids, dtype=np.int32)
+    feats = _f64(feats)
+    B, N, C = feats.shape
+    V = R ** 3
+    grid = np.empty((B, V, C))
+    counts = np.empty((B, V), np.int32)
+    _check(lib.ref_voxelize(_ptr(ids), _ptr(feats), B, N, C, R, _ptr(grid), _ptr(counts)),
+           "voxelize")
+    return grid, counts
+
+
+def conv3d(x: np.ndarray, w: np.ndarray, R: int) -> np.ndarray:
+    """x [B][R^3][Cin], w [Cout][3][3][3][Cin] -> y [B][R^3][Cout] (no BN)."""
+    lib = _load()
+    x = _f64(x)
+    w = _f64(w)
+    B, V, Cin = x.shape
+    assert V == R ** 3 and w.shape[1:] == (3, 3, 3, Cin)
+    Cout = w.shape[0]
+    y = np.empty((B, V, Cout))
+    _check(lib.ref_conv3d(_ptr(x), B, R, Cin, Cout, _ptr(w), _ptr(y)), "conv3d")
+    return y
+
+
+def conv3d_at(x: np.ndarray, w: np.ndarray, R: int, sel: np.ndarray) -> np.ndarray:
+    """The convolution at the selected outputs sel[j] = b*R^3 + voxel -> [n_sel][Cout]."""
+    lib = _load()
+    x = _f64(x)
+    w = _f64(w)
+    B, V, Cin = x.shape
+    Cout = w.shape[0]
+    sel = np.ascontiguousarray(sel, dtype=np.int64)
+    y = np.empty((len(sel), Cout))
+    _check(lib.ref_conv3d_at(_ptr(x), B, R, Cin, Cout, _ptr(w), len(sel), _ptr(sel), _ptr(y)),
+           "conv3d_at")
+    return y
+
+
+def batchnorm(y: np.ndarray, bn) -> np.ndarray:
+    """Running-statistics batch normalisation over the last axis (copy)."""
+    lib = _load()
+    out = _f64(y).copy()
+    C = out.shape[-1]
+    M = out.size // C
+    g, b, mu, var = (_f64(bn.gamma), _f64(bn.beta), _f64(bn.mean), _f64(bn.var))
+    _check(lib.ref_batchnorm(_ptr(out), M, C, _ptr(g), _ptr(b), _ptr(mu), _ptr(var),
+                             float(bn.eps)), "batchnorm")
+    return out
+
+
+def leaky_relu(y: np.ndarray, slope: float) -> np.ndarray:
+    lib = _load()
+    out = _f64(y).copy()
+    lib.ref_leaky_relu(_ptr(out), out.size, slope)
+    return out
+
+
+def relu(y: np.ndarray) -> np.ndarray:
+    lib = _load()
+    out = _f64(y).copy()
+    lib.ref_relu(_ptr(out), out.size)
+    return out
+
+
+def devoxelize(grid: np.ndarray, R: int, pnorm: np.ndarray) -> np.ndarray:
+    """grid [B][R^3][C], pnorm [B][N][3] -> [B][N][C] (trilinear)."""
+    lib = _load()
+    grid = _f64(grid)
+    pnorm = _f64(pnorm)
+    B, V, C = grid.shape
+    N = pnorm.shape[1]
+    out = np.empty((B, N, C))
+    _check(lib.ref_devoxelize(_ptr(grid), B, R, C, _ptr(pnorm), N, _ptr(out)), "devoxelize")
+    return out
+
+
+def devoxelize_weights(pnorm: np.ndarray, R: int):
+    """The 8 cells (linear id within the cloud) and trilinear weights per point."""
+    lib = _load()
+    pn = _f64(pnorm).reshape(-1, 3)
+    cells = np.empty((pn.shape[0], 8), np.int64)
+    wts = np.empty((pn.shape[0], 8))
+    _check(lib.ref_devoxelize_weights(_ptr(pn), pn.shape[0], R, _ptr(cells), _ptr(wts)),
+           "devoxelize_weights")
+    shape = pnorm.shape[:-1] + (8,)
+    return cells.reshape(shape), wts.reshape(shape)
+
+
+def linear(x: np.ndarray, w: np.ndarray, bias: Optional[np.ndarray] = None) -> np.ndarray:
+    """x [..][Cin], w [Cout][Cin] -> x w^T + bias."""
+    lib = _load()
+    x = _f64(x)
+    w = _f64(w)
+    Cin = x.shape[-1]
+    M = x.size // Cin
+    Cout = w.shape[0]
+    y = np.empty(x.shape[:-1] + (Cout,))
+    bias_arr = _f64(bias) if bias is not None else None
+    bp = _ptr(bias_arr) if bias_arr is not None else None
+    _check(lib.ref_linear(_ptr(x), M, Cin, Cout, _ptr(w), bp, _ptr(y)), "linear")
+    return y
+
+
+def maxpool(x: np.ndarray) -> np.ndarray:
+    """x [B][N][C] -> [B][C]."""
+    lib = _load()
+    x = _f64(x)
+    B, N, C = x.shape
+    out = np.empty((B, C))
+    _check(lib.ref_maxpool(_ptr(x), B, N, C, _ptr(out)), "maxpool")
+    return out
+
+
+# ----------------------------------------------------------------------------
+# composition: one PVConv layer (Figure "overview", Sections 4.1-4.3)
+# ----------------------------------------------------------------------------
+def voxel_branch(coords, feats, layer):
+    """Normalise, voxelise, n_convs x (conv + BN + leaky ReLU), devoxelise.
+
+    Returns a dict with every intermediate: centroid, radius, pnorm, ids, grid,
+    counts, conv outputs (list, post-activation) and devox [B][N][Cout]."""
+    c, m, pn = normalize(coords)
+    ids = voxel_ids(pn, layer.R)
+    grid, counts = voxelize(ids, feats, layer.R)
+    h = grid
+    convs = []
+    for w, bn in zip(layer.conv_w, layer.conv_bn):
+        h = leaky_relu(batchnorm(conv3d(h, w, layer.R), bn), layer.slope)
+        convs.append(h)
+    dv = devoxelize(h, layer.R, pn)
+    return dict(centroid=c, radius=m, pnorm=pn, ids=ids, grid=grid, counts=counts,
+                convs=convs, devox=dv)
+
+
+def point_branch(feats, layer):
+    """Section 4.2: h = ReLU(BN(W f (+ b)))."""
+    return relu(batchnorm(linear(feats, layer.mlp_w, layer.mlp_b), layer.mlp_bn))
+
+
+def pvconv_forward(coords, feats, layer, return_parts=False):
+    """Section 4.3: the two branches fused by addition (no activation after it)."""
+    vb = voxel_branch(coords, feats, layer)
+    pb = point_branch(feats, layer)
+    out = vb["devox"] + pb
+    if return_parts:
+        vb["point"] = pb
+        vb["out"] = out
+        return vb
+    return out
+
+
+def shared_mlp(x, lp):
+    """One point-only layer: Linear (+ bias), then BN and ReLU unless final."""
+    y = linear(x, lp.w, lp.b)
+    if lp.bn is not None:
+        y = batchnorm(y, lp.bn)
+    if lp.relu:
+        y = relu(y)
+    return y
+
+
+def network_forward(wl, return_stages=False):
+    """PVCNN segmentation forward (Section 5.1 "Models": PointNet with its
+    per-point MLP layers replaced by PVConv).
+
+    Stages: the PVConv blocks, then the point-only MLPs, each feeding the next;
+    a per-cloud max over the points of the last stage gives the global feature;
+    the head's input is the concatenation of every stage's per-point output and
+    the global feature broadcast to every point; the head is a stack of shared
+    per-point layers ending in logits."""
+    x = wl.feats
+    stages = []
+    for L in wl.layers:
+        x = pvconv_forward(wl.coords, x, L)
+        stages.append(x)
+    for lp in wl.mlps:
+        x = shared_mlp(x, lp)
+        stages.append(x)
+    g = maxpool(x)
+    B, N = wl.B, wl.N
+    cat = np.concatenate(stages + [np.broadcast_to(g[:, None, :], (B, N, g.shape[1]))], axis=2)
+    h = cat
+    for lp in wl.head:
+        h = shared_mlp(h, lp)
+    if return_stages:
+        return h, stages, g
+    return h

@@ -1,0 +1,402 @@
+"""Pins for the CPU oracle: each checks it against something other than itself.
+
+The paper prints no worked example, intermediate values or test vectors, so the
+pins are hand-worked examples of the definitions (tests/golden/), invariants
+that the definitions imply, special cases that reduce to a library routine
+(numpy, torch CPU fp64), and brute force on tiny inputs. Each is chosen so that
+a plausible slip (a dropped term, a wrong sign or index, an axis swap, a
+transposed operand, convolution instead of correlation, a shifted cell centre)
+fails at least one of them.
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+
+pytestmark = pytest.mark.filterwarnings("ignore::DeprecationWarning")
+
+
+def _rng(seed=0):
+    return np.random.default_rng(seed)
+
+
+# ----------------------------------------------------------------------------
+# Normalization (Section 4.1) and voxel indices (Eq. 2)
+# ----------------------------------------------------------------------------
+def test_normalize_worked_example(golden_dir):
+    g = json.load(open(os.path.join(golden_dir, "normalize_two_points.json")))
+    coords = np.array([g["coords"]], np.float32)
+    c, m, pn = oracle.normalize(coords)
+    assert np.array_equal(c[0], g["centroid"])
+    assert m[0] == g["radius"]
+    assert np.array_equal(pn[0], np.array(g["pnorm"]))
+    assert oracle.voxel_ids(pn, g["R"])[0].tolist() == g["ids"]
+
+
+@pytest.mark.parametrize("R", [1, 2, 8, 32, 64])
+def test_single_point_and_coincident_points_map_to_centre(R):
+    # A one-point cloud has zero radius; the reading maps it to (1/2,1/2,1/2).
+    for coords in (np.array([[[0.3, -7.0, 2.5]]], np.float32),
+                   np.full((1, 17, 3), 4.25, np.float32)):
+        c, m, pn = oracle.normalize(coords)
+        assert m[0] == 0.0
+        assert np.all(pn == 0.5)
+        ids = oracle.voxel_ids(pn, R)
+        h = R // 2
+        assert np.all(ids == (h * R + h) * R + h)
+
+
+def test_centroid_is_the_mean_and_radius_the_largest_norm():
+    rng = _rng(1)
+    coords = rng.uniform(-3, 5, size=(3, 1000, 3)).astype(np.float32)
+    c, m, pn = oracle.normalize(coords)
+    mean = coords.astype(np.float64).mean(axis=1)
+    np.testing.assert_allclose(c, mean, rtol=0, atol=1e-13)
+    d = coords.astype(np.float64) - c[:, None, :]
+    np.testing.assert_allclose(m, np.linalg.norm(d, axis=2).max(axis=1), rtol=1e-15)
+
+
+def test_normalized_cloud_is_centred_in_the_half_unit_sphere():
+    rng = _rng(2)
+    coords = (rng.normal(size=(4, 777, 3)) * [3.0, 0.2, 1.0] + [10, -4, 2]).astype(np.float32)
+    _, _, pn = oracle.normalize(coords)
+    # the gravity centre maps to the cube centre ...
+    np.testing.assert_allclose(pn.mean(axis=1), 0.5, atol=1e-12)
+    # ... the furthest point lands on the sphere of radius 1/2, nothing outside it
+    r = np.linalg.norm(pn - 0.5, axis=2)
+    np.testing.assert_allclose(r.max(axis=1), 0.5, rtol=1e-15)
+    assert np.all(pn >= -1e-15) and np.all(pn <= 1 + 1e-15)
+
+
+def test_normalization_is_uniform_not_per_axis():
+    # Rotating the cloud rotates the normalised coordinates about the centre:
+    # this fails for any per-axis (min-max or max-abs) scaling.
+    rng = _rng(3)
+    p = rng.normal(size=(1, 500, 3)) * [2.0, 0.5, 1.0]
+    q = np.linalg.qr(rng.normal(size=(3, 3)))[0]
+    a = p.astype(np.float32)
+    b = (p @ q.T).astype(np.float32)
+    _, _, pa = oracle.normalize(a)
+    _, _, pb = oracle.normalize(b)
+    np.testing.assert_allclose((pa - 0.5) @ q.T, pb - 0.5, atol=2e-7)
+
+
+def test_scaling_by_power_of_two_leaves_ids_bit_identical():
+    wl = synth.make_workload(2, B=2, N=2048)
+    _, _, pn = oracle.normalize(wl.coords)
+    for k in (-3, 1, 5):
+        _, _, pk = oracle.normalize(wl.coords * np.float32(2.0 ** k))
+        assert np.array_equal(pk, pn)
+        assert np.array_equal(oracle.voxel_ids(pk, 32), oracle.voxel_ids(pn, 32))
+
+
+def test_translation_and_scale_invariance_approximately():
+    rng = _rng(4)
+    p = rng.uniform(-1, 1, size=(1, 300, 3))
+    _, _, p0 = oracle.normalize(p.astype(np.float32))
+    _, _, p1 = oracle.normalize((p * 3.7 + [0.5, -2.0, 1.25]).astype(np.float32))
+    np.testing.assert_allclose(p0, p1, atol=1e-6)
+
+
+def test_permuting_points_permutes_ids_exactly():
+    wl = synth.make_workload(5, B=1, N=20000)
+    perm = _rng(5).permutation(wl.N)
+    _, _, pn = oracle.normalize(wl.coords)
+    _, _, pp = oracle.normalize(wl.coords[:, perm])
+    assert np.array_equal(pp, pn[:, perm])
+    assert np.array_equal(oracle.voxel_ids(pp, 64), oracle.voxel_ids(pn, 64)[:, perm])
+
+
+@pytest.mark.parametrize("R", [1, 3, 8, 24, 32])
+def test_each_point_lies_in_its_voxel(R):
+    # Eq. 2: point k belongs to voxel (u,v,w) iff floor(x*r)=u etc.; so x lies
+    # in [u/r, (u+1)/r), except that the top face x = 1 is clamped into u = r-1.
+    rng = _rng(6)
+    coords = rng.uniform(-1, 1, size=(2, 3000, 3)).astype(np.float32)
+    _, _, pn = oracle.normalize(coords)
+    ids = oracle.voxel_ids(pn, R).astype(np.int64)
+    uvw = np.stack([ids // (R * R), (ids // R) % R, ids % R], axis=-1)
+    lo = uvw / R
+    hi = (uvw + 1) / R
+    inside = (pn >= lo) & ((pn < hi) | ((uvw == R - 1) & (pn <= 1 + 1e-15)))
+    inside |= (uvw == 0) & (pn < 0)
+    assert inside.all()
+
+
+def test_boundary_tie_uses_floor_not_round():
+    # x exactly on a cell face belongs to the upper cell; x just below does not.
+    pn = np.array([[[0.25, 0.5, 0.75], [np.nextafter(0.25, 0), 0.5, 0.75]]])
+    ids = oracle.voxel_ids(pn, 4)[0]
+    assert ids.tolist() == [(1 * 4 + 2) * 4 + 3, (0 * 4 + 2) * 4 + 3]
+
+
+def test_non_finite_coordinates_are_rejected():
+    bad = np.zeros((1, 4, 3), np.float32)
+    bad[0, 2, 1] = np.nan
+    with pytest.raises(ValueError):
+        oracle.normalize(bad)
+
+
+# ----------------------------------------------------------------------------
+# Voxelization (Eq. 2)
+# ----------------------------------------------------------------------------
+def _brute_voxelize(ids, feats, R):
+    B, N, C = feats.shape
+    V = R ** 3
+    s = np.zeros((B, V, C))
+    n = np.zeros((B, V), np.int64)
+    for b in range(B):
+        np.add.at(s[b], ids[b], feats[b])
+        n[b] = np.bincount(ids[b], minlength=V)
+    with np.errstate(invalid="ignore", divide="ignore"):
+        g = np.where(n[..., None] > 0, s / np.maximum(n, 1)[..., None], 0.0)
+    return g, n
+
+
+@pytest.mark.parametrize("wl_idx,R", [(1, 8), (2, 32), (5, 64)])
+def test_voxelize_matches_bincount_brute_force(wl_idx, R):
+    wl = synth.make_workload(wl_idx, B=2 if wl_idx != 5 else 1, N=4096)
+    _, _, pn = oracle.normalize(wl.coords)
+    ids = oracle.voxel_ids(pn, R)
+    grid, counts = oracle.voxelize(ids, wl.feats, R)
+    g, n = _brute_voxelize(ids, wl.feats.astype(np.float64), R)
+    assert np.array_equal(counts, n)
+    assert np.all(counts.sum(axis=1) == wl.N)  # counts sum to N per cloud
+    np.testing.assert_allclose(grid, g, rtol=1e-13, atol=1e-14)
+
+
+def test_voxelize_constant_field_is_preserved():
+    wl = synth.make_workload(2, B=2, N=2048)
+    _, _, pn = oracle.normalize(wl.coords)
+    ids = oracle.voxel_ids(pn, 32)
+    kappa = 0.7071
+    grid, counts = oracle.voxelize(ids, np.full((2, 2048, 5), kappa), 32)
+    occ = counts > 0
+    assert np.all(grid[occ] == kappa)  # exact: n*kappa/n in fp64 for these n
+    assert np.all(grid[~occ] == 0.0)
+
+
+def test_all_points_in_one_voxel():
+    rng = _rng(7)
+    feats = rng.normal(size=(1, 50, 3))
+    ids = np.full((1, 50), 123, np.int32)
+    grid, counts = oracle.voxelize(ids, feats, 8)
+    assert counts[0, 123] == 50 and counts.sum() == 50
+    np.testing.assert_allclose(grid[0, 123], feats[0].mean(axis=0), rtol=1e-14)
+    assert np.count_nonzero(grid[0, np.arange(512) != 123]) == 0
+
+
+# ----------------------------------------------------------------------------
+# 3x3x3 convolution (Section 4.1 "Feature Aggregation", Section 3)
+# ----------------------------------------------------------------------------
+def _torch_conv(x, w, R):
+    B, V, Cin = x.shape
+    Cout = w.shape[0]
+    xt = torch.from_numpy(x.reshape(B, R, R, R, Cin)).permute(0, 4, 1, 2, 3).contiguous()
+    wt = torch.from_numpy(np.ascontiguousarray(w.transpose(0, 4, 1, 2, 3)))
+    y = torch.nn.functional.conv3d(xt.double(), wt.double(), padding=1)
+    return y.permute(0, 2, 3, 4, 1).reshape(B, V, Cout).numpy()
+
+
+def test_conv_orientation_worked_example(golden_dir):
+    g = json.load(open(os.path.join(golden_dir, "conv_orientation_r3.json")))
+    x = np.zeros((1, 27, 1))
+    x[0, 13, 0] = 1.0  # centre voxel (1,1,1)
+    w = np.arange(27, dtype=np.float64).reshape(1, 3, 3, 3, 1)
+    y = oracle.conv3d(x, w, 3)
+    assert y[0, :, 0].tolist() == g["output_uvw_row_major"]
+
+
+@pytest.mark.parametrize("R,Cin,Cout,B", [(1, 2, 3, 1), (2, 3, 2, 2), (4, 4, 3, 1), (5, 2, 4, 2),
+                                          (6, 3, 2, 1)])
+def test_conv_matches_torch_conv3d_fp64(R, Cin, Cout, B):
+    rng = _rng(R * 100 + Cin)
+    x = rng.normal(size=(B, R ** 3, Cin))
+    w = rng.normal(size=(Cout, 3, 3, 3, Cin))
+    np.testing.assert_allclose(oracle.conv3d(x, w, R), _torch_conv(x, w, R), rtol=1e-12,
+                               atol=1e-12)
+
+
+def test_conv_matches_shifted_sum_brute_force():
+    # independent brute force: pad with zeros and add the 27 shifted copies
+    rng = _rng(11)
+    R, Cin, Cout = 5, 3, 2
+    x = rng.normal(size=(1, R ** 3, Cin))
+    w = rng.normal(size=(Cout, 3, 3, 3, Cin))
+    xg = np.pad(x.reshape(R, R, R, Cin), ((1, 1), (1, 1), (1, 1), (0, 0)))
+    y = np.zeros((R, R, R, Cout))
+    for a in range(3):
+        for b in range(3):
+            for c in range(3):
+                y += xg[a:a + R, b:b + R, c:c + R] @ w[:, a, b, c, :].T
+    np.testing.assert_allclose(oracle.conv3d(x, w, R)[0], y.reshape(-1, Cout), rtol=1e-12,
+                               atol=1e-12)
+
+
+def test_conv_delta_kernels_identity_shift_and_box():
+    rng = _rng(12)
+    R = 4
+    x = rng.normal(size=(1, R ** 3, 1))
+    xg = x.reshape(R, R, R)
+    w = np.zeros((1, 3, 3, 3, 1))
+    w[0, 1, 1, 1, 0] = 1.0
+    np.testing.assert_array_equal(oracle.conv3d(x, w, R), x)  # centre delta: identity
+    w = np.zeros((1, 3, 3, 3, 1))
+    w[0, 2, 1, 1, 0] = 1.0  # offset (+1, 0, 0): y[u] = x[u+1], zero past the edge
+    y = oracle.conv3d(x, w, R)[0, :, 0].reshape(R, R, R)
+    np.testing.assert_array_equal(y[:-1], xg[1:])
+    np.testing.assert_array_equal(y[-1], 0.0)
+    w = np.zeros((1, 3, 3, 3, 1))
+    w[0, 1, 1, 0, 0] = 1.0  # offset (0, 0, -1): y[..., w] = x[..., w-1]
+    y = oracle.conv3d(x, w, R)[0, :, 0].reshape(R, R, R)
+    np.testing.assert_array_equal(y[:, :, 1:], xg[:, :, :-1])
+    np.testing.assert_array_equal(y[:, :, 0], 0.0)
+    ones = np.ones((1, 3, 3, 3, 1))
+    y = oracle.conv3d(np.ones((1, R ** 3, 1)), ones, R)[0, :, 0].reshape(R, R, R)
+    interior = np.array([2, 3, 3, 2])  # neighbours per axis incl. self at R=4
+    np.testing.assert_array_equal(y, np.einsum("i,j,k->ijk", interior, interior, interior))
+
+
+def test_conv_is_linear_and_sampled_matches_dense():
+    rng = _rng(13)
+    R, Cin, Cout = 6, 4, 5
+    x1, x2 = rng.normal(size=(2, 2, R ** 3, Cin))
+    w = rng.normal(size=(Cout, 3, 3, 3, Cin))
+    y = oracle.conv3d(2.5 * x1 + x2, w, R)
+    np.testing.assert_allclose(y, 2.5 * oracle.conv3d(x1, w, R) + oracle.conv3d(x2, w, R),
+                               rtol=1e-12, atol=1e-12)
+    sel = rng.choice(2 * R ** 3, size=40, replace=False)
+    np.testing.assert_array_equal(oracle.conv3d_at(2.5 * x1 + x2, w, R, sel),
+                                  y.reshape(-1, Cout)[sel])
+
+
+def test_batchnorm_and_activations_closed_form():
+    bn = synth.BNParams(gamma=np.array([2.0, 0.5]), beta=np.array([1.0, -1.0]),
+                        mean=np.array([3.0, -2.0]), var=np.array([4.0, 0.25]), eps=0.0)
+    y = np.array([[3.0, -2.0], [5.0, 0.0], [1.0, -3.0]])
+    z = oracle.batchnorm(y, bn)
+    np.testing.assert_array_equal(z, [[1.0, -1.0], [3.0, 1.0], [-1.0, -2.0]])
+    np.testing.assert_array_equal(oracle.leaky_relu(z, 0.1), [[1.0, -0.1], [3.0, 1.0],
+                                                              [-0.1, -0.2]])
+    np.testing.assert_array_equal(oracle.relu(z), [[1.0, 0.0], [3.0, 1.0], [0.0, 0.0]])
+    # folding into scale and shift agrees with the unfolded form
+    bn = synth.draw_bn(_rng(14), 7)
+    y = _rng(15).normal(size=(11, 7))
+    s = bn.gamma.astype(np.float64) / np.sqrt(bn.var.astype(np.float64) + bn.eps)
+    t = bn.beta - bn.mean.astype(np.float64) * s
+    np.testing.assert_allclose(oracle.batchnorm(y, bn), y * s + t, rtol=1e-12, atol=1e-12)
+
+
+# ----------------------------------------------------------------------------
+# Devoxelization (Section 4.1)
+# ----------------------------------------------------------------------------
+def test_devox_worked_example(golden_dir):
+    g = json.load(open(os.path.join(golden_dir, "devox_r2.json")))
+    R = g["R"]
+    u, v, w = np.meshgrid(range(R), range(R), range(R), indexing="ij")
+    grid = (100 * u + 10 * v + w).reshape(1, R ** 3, 1).astype(np.float64)
+    out = oracle.devoxelize(grid, R, np.array([g["points"]]))
+    np.testing.assert_allclose(out[0, :, 0], g["values"], rtol=1e-15)
+
+
+def test_devox_weights_sum_to_one_and_constant_is_preserved():
+    rng = _rng(16)
+    pn = rng.uniform(-0.01, 1.01, size=(2, 500, 3))
+    for R in (1, 2, 7, 32):
+        _, wts = oracle.devoxelize_weights(pn, R)
+        np.testing.assert_allclose(wts.sum(axis=-1), 1.0, atol=1e-15)
+        assert np.all(wts >= 0)
+        out = oracle.devoxelize(np.full((2, R ** 3, 3), -1.25), R, pn)
+        np.testing.assert_allclose(out, -1.25, rtol=1e-15)
+
+
+def test_devox_reproduces_affine_field_and_cell_centres():
+    # V at cell (u,v,w) = a . centre + b with centre = ((u,v,w) + 1/2) / R.
+    # Trilinear interpolation reproduces it exactly for points whose cell
+    # coordinate is not clamped, i.e. inside [1/(2R), 1 - 1/(2R)]^3.
+    R = 8
+    a = np.array([1.5, -2.0, 0.25])
+    u, v, w = np.meshgrid(range(R), range(R), range(R), indexing="ij")
+    cen = (np.stack([u, v, w], -1) + 0.5) / R
+    grid = (cen @ a + 0.3).reshape(1, R ** 3, 1)
+    rng = _rng(17)
+    pn = rng.uniform(0.5 / R, 1 - 0.5 / R, size=(1, 400, 3))
+    out = oracle.devoxelize(grid, R, pn)
+    np.testing.assert_allclose(out[0, :, 0], pn[0] @ a + 0.3, rtol=1e-13, atol=1e-13)
+    # a point at a cell centre returns that cell's value
+    pc = cen.reshape(1, -1, 3)
+    np.testing.assert_allclose(oracle.devoxelize(grid, R, pc)[0, :, 0], grid[0, :, 0],
+                               rtol=1e-14, atol=1e-14)
+
+
+def test_voxelize_then_devoxelize_preserves_constant_where_corners_occupied():
+    wl = synth.make_workload(2, B=2, N=2048)
+    R = 16
+    _, _, pn = oracle.normalize(wl.coords)
+    ids = oracle.voxel_ids(pn, R)
+    kappa = 2.5
+    grid, counts = oracle.voxelize(ids, np.full((2, 2048, 1), kappa), R)
+    out = oracle.devoxelize(grid, R, pn)[..., 0]
+    cells, wts = oracle.devoxelize_weights(pn, R)
+    occupied = np.take_along_axis(counts[:, None, :].repeat(2048, 1), cells, axis=2) > 0
+    full = (occupied | (wts == 0)).all(axis=2)
+    assert full.sum() > 100
+    np.testing.assert_allclose(out[full], kappa, rtol=1e-14)
+    # elsewhere empty corners contribute zero: the value is kappa times the
+    # occupied corners' weight
+    occ_w = (wts * occupied).sum(axis=2)
+    np.testing.assert_allclose(out, kappa * occ_w, rtol=1e-13, atol=1e-15)
+
+
+def test_lone_point_gets_an_eighth_at_even_R():
+    # one point -> centre (1/2,1/2,1/2) -> cell coordinate R/2 - 1/2: all 8
+    # corners weigh 1/8 and only one of them is occupied
+    for R in (2, 8, 32):
+        _, _, pn = oracle.normalize(np.array([[[1.0, 2.0, 3.0]]], np.float32))
+        grid, _ = oracle.voxelize(oracle.voxel_ids(pn, R), np.array([[[4.0]]]), R)
+        assert oracle.devoxelize(grid, R, pn)[0, 0, 0] == 0.5
+
+
+# ----------------------------------------------------------------------------
+# Point branch, fusion, max-pool (Sections 4.2, 4.3, 5.1)
+# ----------------------------------------------------------------------------
+def test_linear_matches_numpy_matmul():
+    rng = _rng(18)
+    x = rng.normal(size=(3, 50, 7))
+    w = rng.normal(size=(5, 7))
+    b = rng.normal(size=5)
+    np.testing.assert_allclose(oracle.linear(x, w, b), np.matmul(x, w.T) + b, rtol=1e-13,
+                               atol=1e-13)
+    np.testing.assert_allclose(oracle.linear(x, w), np.matmul(x, w.T), rtol=1e-13, atol=1e-13)
+
+
+def test_maxpool_matches_numpy():
+    x = _rng(19).normal(size=(3, 40, 6))
+    np.testing.assert_array_equal(oracle.maxpool(x), x.max(axis=1))
+
+
+def test_layer_is_the_sum_of_its_branches():
+    wl = synth.make_workload(1, N=256)
+    L = wl.layers[0]
+    parts = oracle.pvconv_forward(wl.coords, wl.feats, L, return_parts=True)
+    assert np.array_equal(parts["out"], parts["devox"] + parts["point"])
+    # point branch against numpy: ReLU(BN(W f))
+    bn = L.mlp_bn
+    s = bn.gamma.astype(np.float64) / np.sqrt(bn.var.astype(np.float64) + bn.eps)
+    ref = np.maximum((wl.feats.astype(np.float64) @ L.mlp_w.T.astype(np.float64) - bn.mean) * s
+                     + bn.beta, 0)
+    np.testing.assert_allclose(parts["point"], ref, rtol=1e-12, atol=1e-12)
+    # with zero conv weights the voxel branch is constant: LReLU(BN(0)) per channel
+    L0 = synth.PVConvParams(L.cin, L.cout, L.R, [np.zeros_like(L.conv_w[0])], L.conv_bn,
+                            L.mlp_w, L.mlp_bn)
+    p0 = oracle.pvconv_forward(wl.coords, wl.feats, L0, return_parts=True)
+    cb = L.conv_bn[0]
+    z = cb.beta - cb.mean.astype(np.float64) * cb.gamma / np.sqrt(cb.var.astype(np.float64) +
+                                                                  cb.eps)
+    z = np.where(z < 0, 0.1 * z, z)
+    np.testing.assert_allclose(p0["devox"], np.broadcast_to(z, p0["devox"].shape), rtol=1e-12)
