@@ -1,0 +1,209 @@
+/*
+ * pvconv.h -- C ABI of the MI355X (gfx950) Point-Voxel Convolution forward.
+ *
+ * Implements the PVConv layer of Liu, Tang, Lin, Han, "Point-Voxel CNN for
+ * Efficient 3D Deep Learning" (NeurIPS 2019), Section 4: a voxel branch
+ * (normalise -> voxelise -> 3x3x3 convolutions with batch normalisation and a
+ * leaky rectifier -> trilinear devoxelise) and a point branch (a shared
+ * per-point MLP), fused by addition. Every step runs as a HIP kernel on the
+ * GPU; nothing here computes on the host.
+ *
+ * Conventions shared by every entry point
+ *  - Array pointers are DEVICE pointers owned by the caller. The library keeps
+ *    no device memory and no state between calls; scratch space is passed in
+ *    as `workspace` where an entry point needs it.
+ *  - `stream` is a hipStream_t (NULL = the null stream). Every call only
+ *    enqueues work on it: it never synchronises and never allocates.
+ *  - Layouts are row-major, channels innermost ("channels last"):
+ *      point arrays  [B][N][C], row k of cloud b at (b*N + k) * ld
+ *      voxel grids   [B][R][R][R][C], voxel (u,v,w) at ((u*R + v)*R + w),
+ *                    u indexes the x axis (slowest), w the z axis (fastest)
+ *      conv weights  [C_out][3][3][3][C_in], index (du+1, dv+1, dw+1) holds
+ *                    the weight of the neighbour at offset (du, dv, dw)
+ *      linear weights [C_out][C_in]
+ *    `*_ld` arguments are row strides in elements (0 means "= number of
+ *    channels"); they let a caller read or write a column slice of a wider
+ *    array, e.g. a concatenation buffer.
+ *  - PVCONV_BF16 arrays hold raw bfloat16 bits (uint16). bf16 compute means
+ *    bf16 operands with fp32 accumulation.
+ *  - Arguments are validated on the host before anything is enqueued: an
+ *    invalid argument returns PVCONV_EINVAL (or PVCONV_ENOTSUP /
+ *    PVCONV_EWORKSPACE) and enqueues nothing. A failed launch returns
+ *    PVCONV_EHIP. Device faults surface at the caller's next synchronisation.
+ *  - Coordinates must be finite. Non-finite coordinates are a precondition
+ *    violation: results are then unspecified, but every index is clamped, so
+ *    no access leaves its array.
+ */
+#ifndef PVCONV_H
+#define PVCONV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    PVCONV_OK = 0,
+    PVCONV_EINVAL = 1,     /* bad size, NULL required pointer, misaligned pointer */
+    PVCONV_ENOTSUP = 2,    /* valid but unsupported combination (e.g. dtype) */
+    PVCONV_EWORKSPACE = 3, /* workspace NULL or smaller than the queried size */
+    PVCONV_EHIP = 4        /* the HIP runtime reported an error at launch */
+} pvconv_status;
+
+typedef enum { PVCONV_F32 = 0, PVCONV_BF16 = 1 } pvconv_dtype;
+
+typedef enum { PVCONV_ACT_NONE = 0, PVCONV_ACT_RELU = 1, PVCONV_ACT_LEAKY = 2 } pvconv_act;
+
+/* Batch normalisation in inference form (running statistics), Section 4.1
+ * "Feature Aggregation": y = gamma * (x - mean) / sqrt(var + eps) + beta.
+ * Each pointer is a device array of C floats. A NULL pvconv_bn pointer, or
+ * gamma == NULL, means identity. */
+typedef struct {
+    const float* gamma;
+    const float* beta;
+    const float* mean;
+    const float* var;
+    float eps;
+} pvconv_bn;
+
+/* Limits checked by every entry point. */
+#define PVCONV_MAX_R 128
+#define PVCONV_MAX_CONV_CHANNELS 1024
+#define PVCONV_MAX_MLP_CHANNELS 16384
+#define PVCONV_MAX_CONVS 4
+
+/* Human-readable name of a status code (static string). */
+const char* pvconv_status_string(pvconv_status s);
+
+/* ------------------------------------------------------------------------- */
+/* Voxelisation: Section 4.1 "Normalization" and "Voxelization" (Eq. 2).     */
+/*                                                                           */
+/* Per cloud b: the coordinates are centred at their mean (the "gravity      */
+/* center"), divided by the largest centred norm, then scaled by 1/2 and     */
+/* shifted by 1/2 into [0,1]^3 (norm_coords). A cloud whose points all       */
+/* coincide maps to (1/2,1/2,1/2). Point k falls in voxel                    */
+/* (floor(x*R), floor(y*R), floor(z*R)), clamped to [0, R-1]; vox_id is       */
+/* (u*R + v)*R + w. The grid holds, per voxel, the mean of the features of   */
+/* its points (Eq. 2) and 0 for an empty voxel; counts holds N_{u,v,w}.       */
+/* The mean is taken in the order-free arithmetic described in the design    */
+/* notes: the centroid is an int64 fixed-point sum, normalisation is IEEE    */
+/* fp64 without contraction, feature sums accumulate in fp64.                */
+/*                                                                           */
+/*  coords       [B][N][3] fp32                                              */
+/*  feats        [B][N][C] (feat_dt), row stride feat_ld                     */
+/*  grid         out [B][R^3][C] (grid_dt), every element written            */
+/*  counts       out [B][R^3] int32                                          */
+/*  vox_id       out [B][N] int32, or NULL                                   */
+/*  norm_coords  out [B][N][3] fp32 (the fp64 values rounded), or NULL       */
+/*  workspace    >= pvconv_voxelize_workspace_size(B, N, R) bytes, 256-byte  */
+/*               aligned; contents on entry are ignored                      */
+/* Sizes: B >= 0, N >= 0 (N = 0 gives an all-zero grid), 1 <= R <= 128,      */
+/* 1 <= C. feats, grid need 16-byte alignment when C*elem and feat_ld*elem   */
+/* are multiples of 16 (otherwise a slower element-wise path is taken).      */
+/* ------------------------------------------------------------------------- */
+size_t pvconv_voxelize_workspace_size(int B, int N, int R);
+pvconv_status pvconv_voxelize(const float* coords, const void* feats, pvconv_dtype feat_dt,
+                              int feat_ld, int B, int N, int C, int R, void* grid,
+                              pvconv_dtype grid_dt, int32_t* counts, int32_t* vox_id,
+                              float* norm_coords, void* workspace, size_t workspace_bytes,
+                              void* stream);
+
+/* ------------------------------------------------------------------------- */
+/* 3x3x3 convolution + batch norm + activation: Section 4.1 "Feature         */
+/* Aggregation", with the fixed-offset kernel of Section 3 (Eq. 1; each axis */
+/* offset in {0, +-1}).                                                      */
+/*                                                                           */
+/*  y[b,u,v,w,o] = act( BN_o( bias_o + sum_{du,dv,dw in {-1,0,1}}            */
+/*                 sum_i W[o][du+1][dv+1][dw+1][i] * x[b,u+du,v+dv,w+dw,i] ) ) */
+/* with x = 0 outside the grid (zero padding 1, stride 1).                   */
+/*  x       [B][R^3][Cin], dtype dt                                          */
+/*  weight  [Cout][3][3][3][Cin], dtype dt                                   */
+/*  bias    [Cout] fp32 or NULL; bn may be NULL                              */
+/*  act     NONE / RELU / LEAKY (negative slope `slope`)                     */
+/*  y       out [B][R^3][Cout], dtype out_dt                                 */
+/* dt = BF16: MFMA implicit GEMM, bf16 x bf16 -> fp32; needs Cout % 32 == 0. */
+/* dt = F32: fp32 FMA. 1 <= Cin, Cout <= 1024, 1 <= R <= 128. x and y must   */
+/* not overlap.                                                              */
+/* ------------------------------------------------------------------------- */
+pvconv_status pvconv_conv3d(const void* x, int B, int R, int Cin, int Cout, const void* weight,
+                            const float* bias, const pvconv_bn* bn, pvconv_act act, float slope,
+                            pvconv_dtype dt, void* y, pvconv_dtype out_dt, void* stream);
+
+/* ------------------------------------------------------------------------- */
+/* Trilinear devoxelisation: Section 4.1 "Devoxelization".                   */
+/*                                                                           */
+/* Voxel (u,v,w)'s value sits at its cell centre ((u+1/2)/R, ...). Per axis  */
+/* t = clamp(R*x - 1/2, 0, R-1), i0 = floor(t), i1 = min(i0+1, R-1),         */
+/* weights (1 - (t - i0), t - i0); out = sum over the 8 cells of the product */
+/* of the three axis weights times the cell's features.                      */
+/*  grid         [B][R^3][C] (grid_dt)                                       */
+/*  norm_coords  [B][N][3] fp32 in [0,1] (as written by pvconv_voxelize)     */
+/*  out          out [B][N][C] fp32                                          */
+/* ------------------------------------------------------------------------- */
+pvconv_status pvconv_devoxelize(const void* grid, int B, int R, int C, pvconv_dtype grid_dt,
+                                const float* norm_coords, int N, float* out, void* stream);
+
+/* ------------------------------------------------------------------------- */
+/* Shared per-point MLP layer with fused epilogue: Section 4.2 (point-based  */
+/* feature transformation) and Section 4.3 (fusion by addition).             */
+/*                                                                           */
+/*  out[m,o] = act( BN_o( sum_i W[o][i] * x[m,i] + bias_o + cloud_bias[m/P,o] ) ) */
+/*             + residual[m,o]                                               */
+/* where P = points_per_cloud. Rows m = 0..M-1.                              */
+/*  x           [M][Cin] (x_dt), row stride x_ld                             */
+/*  weight      [Cout][Cin] (compute_dt: BF16 -> MFMA, F32 -> fp32 FMA)      */
+/*  bias        [Cout] fp32 or NULL; bn may be NULL                          */
+/*  cloud_bias  [M/P][Cout] fp32 or NULL (a per-cloud row, e.g. the          */
+/*              projection of a broadcast global feature)                    */
+/*  residual    [M][Cout] fp32 (row stride residual_ld) or NULL; added after */
+/*              the activation                                               */
+/*  out         out [M][Cout] (out_dt), row stride out_ld                    */
+/* 1 <= Cin, Cout <= 16384. out must not overlap x.                          */
+/* ------------------------------------------------------------------------- */
+pvconv_status pvconv_point_mlp(const void* x, pvconv_dtype x_dt, int x_ld, int M, int Cin,
+                               int Cout, const void* weight, pvconv_dtype compute_dt,
+                               const float* bias, const pvconv_bn* bn, pvconv_act act,
+                               float slope, const float* cloud_bias, int points_per_cloud,
+                               const float* residual, int residual_ld, void* out,
+                               pvconv_dtype out_dt, int out_ld, void* stream);
+
+/* ------------------------------------------------------------------------- */
+/* Per-cloud max over the points (the PointNet global feature that PVCNN     */
+/* keeps, Section 5.1 "Models"): out[b][c] = max_k x[b][k][c].               */
+/*  x    [B][N][C] (dt), row stride x_ld;  out [B][C] fp32.  N >= 1.         */
+/* ------------------------------------------------------------------------- */
+pvconv_status pvconv_maxpool(const void* x, pvconv_dtype dt, int x_ld, int B, int N, int C,
+                             float* out, void* stream);
+
+/* ------------------------------------------------------------------------- */
+/* One whole PVConv layer: Section 4, Figure "overview".                     */
+/*                                                                           */
+/* out = devoxelise( [conv + BN + leaky]^n_convs ( voxelise(coords, feats) ) ) */
+/*       + ReLU( BN( W_mlp feats + b_mlp ) )                                 */
+/* All weights are in compute_dt (BF16 or F32); grids are kept in            */
+/* compute_dt. out is [B][N][cout] (out_dt) with row stride out_ld.          */
+/* ------------------------------------------------------------------------- */
+typedef struct {
+    int cin, cout, R, n_convs;                 /* 1 <= n_convs <= PVCONV_MAX_CONVS */
+    const void* conv_w[PVCONV_MAX_CONVS];      /* conv i: [cout][3][3][3][i ? cout : cin] */
+    pvconv_bn conv_bn[PVCONV_MAX_CONVS];
+    float conv_slope;                          /* leaky slope of the voxel branch */
+    const void* mlp_w;                         /* [cout][cin] */
+    const float* mlp_b;                        /* [cout] or NULL */
+    pvconv_bn mlp_bn;
+    pvconv_dtype compute_dt;
+} pvconv_layer;
+
+size_t pvconv_forward_workspace_size(int B, int N, const pvconv_layer* L);
+pvconv_status pvconv_forward(const float* coords, const void* feats, pvconv_dtype feat_dt,
+                             int feat_ld, int B, int N, const pvconv_layer* L, void* out,
+                             pvconv_dtype out_dt, int out_ld, void* workspace,
+                             size_t workspace_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PVCONV_H */

@@ -1,0 +1,261 @@
+"""Thin Python binding of libpvconv (include/pvconv.h).
+
+Argument marshalling only: every function allocates its outputs (and any
+workspace) as torch tensors on the input's device, passes raw device pointers,
+sizes and the current torch stream to the C ABI, and raises on a non-OK
+status. All computation happens in the library's HIP kernels. There is no
+fallback: if libpvconv.so is missing the import fails.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libpvconv.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(
+        f"{LIB_PATH} is missing: build the HIP library first "
+        "(python -m paper_1907_03739_amd.build, or __graft_entry__.build())")
+
+_lib = ctypes.CDLL(LIB_PATH)
+
+F32, BF16 = 0, 1
+ACT = {"none": 0, "relu": 1, "leaky": 2}
+MAX_CONVS = 4
+
+_VP = ctypes.c_void_p
+_I = ctypes.c_int
+_SZ = ctypes.c_size_t
+_F = ctypes.c_float
+
+
+class BN(ctypes.Structure):
+    _fields_ = [("gamma", _VP), ("beta", _VP), ("mean", _VP), ("var", _VP), ("eps", _F)]
+
+
+class Layer(ctypes.Structure):
+    _fields_ = [("cin", _I), ("cout", _I), ("R", _I), ("n_convs", _I),
+                ("conv_w", _VP * MAX_CONVS), ("conv_bn", BN * MAX_CONVS),
+                ("conv_slope", _F), ("mlp_w", _VP), ("mlp_b", _VP), ("mlp_bn", BN),
+                ("compute_dt", _I)]
+
+
+_SIGS = {
+    "pvconv_voxelize_workspace_size": ([_I, _I, _I], _SZ),
+    "pvconv_voxelize": ([_VP, _VP, _I, _I, _I, _I, _I, _I, _VP, _I, _VP, _VP, _VP, _VP, _SZ, _VP],
+                        _I),
+    "pvconv_conv3d": ([_VP, _I, _I, _I, _I, _VP, _VP, _VP, _I, _F, _I, _VP, _I, _VP], _I),
+    "pvconv_devoxelize": ([_VP, _I, _I, _I, _I, _VP, _I, _VP, _VP], _I),
+    "pvconv_point_mlp": ([_VP, _I, _I, _I, _I, _I, _VP, _I, _VP, _VP, _I, _F, _VP, _I, _VP, _I,
+                          _VP, _I, _I, _VP], _I),
+    "pvconv_maxpool": ([_VP, _I, _I, _I, _I, _I, _VP, _VP], _I),
+    "pvconv_forward_workspace_size": ([_I, _I, ctypes.POINTER(Layer)], _SZ),
+    "pvconv_forward": ([_VP, _VP, _I, _I, _I, _I, ctypes.POINTER(Layer), _VP, _I, _I, _VP, _SZ,
+                        _VP], _I),
+    "pvconv_status_string": ([_I], ctypes.c_char_p),
+}
+for _name, (_args, _res) in _SIGS.items():
+    _fn = getattr(_lib, _name)
+    _fn.argtypes = _args
+    _fn.restype = _res
+
+EXPORTED = tuple(_SIGS)
+
+
+class PVConvError(RuntimeError):
+    def __init__(self, fn, status):
+        msg = _lib.pvconv_status_string(status).decode()
+        super().__init__(f"{fn}: status {status} ({msg})")
+        self.status = status
+
+
+def _check(fn, status):
+    if status != 0:
+        raise PVConvError(fn, status)
+
+
+def _dt(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype == torch.bfloat16:
+        return BF16
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _torch_dt(d) -> torch.dtype:
+    if d in (F32, torch.float32, "f32"):
+        return torch.float32
+    if d in (BF16, torch.bfloat16, "bf16"):
+        return torch.bfloat16
+    raise TypeError(f"unsupported dtype {d}")
+
+
+def _p(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(t: torch.Tensor):
+    return ctypes.c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
+
+
+def _rows(t: torch.Tensor, nrows: int, ncols: int) -> int:
+    """Row stride (elements) of a [.., rows, cols] view whose rows are evenly
+    spaced and whose channels are contiguous."""
+    if t.shape[-1] != ncols:
+        raise ValueError("channel count mismatch")
+    if t.numel() == 0:
+        return ncols
+    if t.stride(-1) != 1:
+        raise ValueError("channels must be the innermost, contiguous dimension")
+    ld = t.stride(-2) if t.dim() >= 2 else ncols
+    if t.dim() == 3 and t.shape[0] > 1 and t.stride(0) != t.shape[1] * ld:
+        raise ValueError("rows must be evenly spaced across clouds")
+    return ld
+
+
+def _bn_struct(bn) -> BN:
+    if bn is None:
+        return BN()
+    g, b, m, v, eps = bn
+    return BN(g.data_ptr(), b.data_ptr(), m.data_ptr(), v.data_ptr(), float(eps))
+
+
+# ----------------------------------------------------------------------------
+# entry points (same names as the C ABI)
+# ----------------------------------------------------------------------------
+def pvconv_voxelize(coords: torch.Tensor, feats: torch.Tensor, R: int,
+                    grid_dtype=torch.float32, want_ids=True, want_norm=True):
+    """coords [B][N][3] f32, feats [B][N][C] -> (grid [B][R^3][C], counts [B][R^3],
+    vox_id [B][N] or None, norm_coords [B][N][3] or None)."""
+    B, N, _ = coords.shape
+    C = feats.shape[-1]
+    dev = coords.device
+    ld = _rows(feats, N, C)
+    grid = torch.empty((B, R ** 3, C), dtype=_torch_dt(grid_dtype), device=dev)
+    counts = torch.empty((B, R ** 3), dtype=torch.int32, device=dev)
+    ids = torch.empty((B, N), dtype=torch.int32, device=dev) if want_ids else None
+    pn = torch.empty((B, N, 3), dtype=torch.float32, device=dev) if want_norm else None
+    wsb = _lib.pvconv_voxelize_workspace_size(B, N, R)
+    ws = torch.empty(max(wsb, 256), dtype=torch.uint8, device=dev)
+    _check("pvconv_voxelize", _lib.pvconv_voxelize(
+        _p(coords), _p(feats), _dt(feats), ld, B, N, C, R, _p(grid), _dt(grid), _p(counts),
+        _p(ids), _p(pn), _p(ws), wsb, _stream(coords)))
+    return grid, counts, ids, pn
+
+
+def pvconv_conv3d(x: torch.Tensor, weight: torch.Tensor, R: int, bn=None,
+                  bias: Optional[torch.Tensor] = None, act="leaky", slope=0.1,
+                  out_dtype=None):
+    """x [B][R^3][Cin], weight [Cout][3][3][3][Cin] (same dtype) -> y [B][R^3][Cout]."""
+    B, V, Cin = x.shape
+    Cout = weight.shape[0]
+    if V != R ** 3 or tuple(weight.shape[1:]) != (3, 3, 3, Cin):
+        raise ValueError("shape mismatch")
+    y = torch.empty((B, V, Cout), dtype=_torch_dt(out_dtype or x.dtype), device=x.device)
+    bns = _bn_struct(bn)
+    _check("pvconv_conv3d", _lib.pvconv_conv3d(
+        _p(x.contiguous()), B, R, Cin, Cout, _p(weight.contiguous()), _p(bias),
+        ctypes.byref(bns) if bn is not None else None, ACT[act], slope, _dt(x), _p(y), _dt(y),
+        _stream(x)))
+    return y
+
+
+def pvconv_devoxelize(grid: torch.Tensor, R: int, norm_coords: torch.Tensor):
+    """grid [B][R^3][C], norm_coords [B][N][3] f32 -> [B][N][C] f32."""
+    B, V, C = grid.shape
+    N = norm_coords.shape[1]
+    out = torch.empty((B, N, C), dtype=torch.float32, device=grid.device)
+    _check("pvconv_devoxelize", _lib.pvconv_devoxelize(
+        _p(grid.contiguous()), B, R, C, _dt(grid), _p(norm_coords.contiguous()), N, _p(out),
+        _stream(grid)))
+    return out
+
+
+def pvconv_point_mlp(x: torch.Tensor, weight: torch.Tensor, bias=None, bn=None, act="relu",
+                     slope=0.0, cloud_bias=None, points_per_cloud=1, residual=None,
+                     out: Optional[torch.Tensor] = None, out_dtype=torch.float32):
+    """x [..][Cin] (rows evenly strided), weight [Cout][Cin] -> [..][Cout]."""
+    Cin = x.shape[-1]
+    Cout = weight.shape[0]
+    M = 1
+    for d in x.shape[:-1]:
+        M *= int(d)
+    x_ld = _rows(x, M, Cin)
+    if out is None:
+        out = torch.empty(tuple(x.shape[:-1]) + (Cout,), dtype=_torch_dt(out_dtype),
+                          device=x.device)
+    out_ld = _rows(out, M, Cout)
+    res_ld = _rows(residual, M, Cout) if residual is not None else 0
+    bns = _bn_struct(bn)
+    _check("pvconv_point_mlp", _lib.pvconv_point_mlp(
+        _p(x), _dt(x), x_ld, M, Cin, Cout, _p(weight.contiguous()), _dt(weight), _p(bias),
+        ctypes.byref(bns) if bn is not None else None, ACT[act], slope, _p(cloud_bias),
+        points_per_cloud, _p(residual), res_ld, _p(out), _dt(out), out_ld, _stream(x)))
+    return out
+
+
+def pvconv_maxpool(x: torch.Tensor):
+    """x [B][N][C] (rows evenly strided) -> [B][C] f32."""
+    B, N, C = x.shape
+    ld = _rows(x, N, C)
+    out = torch.empty((B, C), dtype=torch.float32, device=x.device)
+    _check("pvconv_maxpool", _lib.pvconv_maxpool(_p(x), _dt(x), ld, B, N, C, _p(out),
+                                                 _stream(x)))
+    return out
+
+
+class DeviceLayer:
+    """Device copies of one PVConv layer's parameters plus the C struct that
+    points at them. Weights are stored in the compute dtype."""
+
+    def __init__(self, params, device, compute_dtype=torch.bfloat16):
+        self.params = params
+        dt = _torch_dt(compute_dtype)
+        f = lambda a: torch.as_tensor(a, dtype=torch.float32).to(device)
+        self.conv_w = [f(w).to(dt).contiguous() for w in params.conv_w]
+        self.conv_bn = [(f(b.gamma), f(b.beta), f(b.mean), f(b.var), b.eps)
+                        for b in params.conv_bn]
+        self.mlp_w = f(params.mlp_w).to(dt).contiguous()
+        self.mlp_b = f(params.mlp_b) if params.mlp_b is not None else None
+        mb = params.mlp_bn
+        self.mlp_bn = (f(mb.gamma), f(mb.beta), f(mb.mean), f(mb.var), mb.eps)
+        L = Layer()
+        L.cin, L.cout, L.R, L.n_convs = params.cin, params.cout, params.R, params.n_convs
+        for i, (w, bn) in enumerate(zip(self.conv_w, self.conv_bn)):
+            L.conv_w[i] = w.data_ptr()
+            L.conv_bn[i] = _bn_struct(bn)
+        L.conv_slope = params.slope
+        L.mlp_w = self.mlp_w.data_ptr()
+        L.mlp_b = self.mlp_b.data_ptr() if self.mlp_b is not None else None
+        L.mlp_bn = _bn_struct(self.mlp_bn)
+        L.compute_dt = _dt(self.mlp_w)
+        self.struct = L
+        self.dtype = dt
+
+
+def pvconv_forward_workspace_size(B: int, N: int, layer: DeviceLayer) -> int:
+    return _lib.pvconv_forward_workspace_size(B, N, ctypes.byref(layer.struct))
+
+
+def pvconv_forward(coords: torch.Tensor, feats: torch.Tensor, layer: DeviceLayer,
+                   out: Optional[torch.Tensor] = None, out_dtype=torch.float32,
+                   workspace: Optional[torch.Tensor] = None):
+    """One PVConv layer: coords [B][N][3] f32, feats [B][N][cin] -> [B][N][cout]."""
+    B, N, _ = coords.shape
+    cin, cout = layer.params.cin, layer.params.cout
+    f_ld = _rows(feats, N, cin)
+    if out is None:
+        out = torch.empty((B, N, cout), dtype=_torch_dt(out_dtype), device=coords.device)
+    o_ld = _rows(out, N, cout)
+    need = pvconv_forward_workspace_size(B, N, layer)
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=coords.device)
+    _check("pvconv_forward", _lib.pvconv_forward(
+        _p(coords), _p(feats), _dt(feats), f_ld, B, N, ctypes.byref(layer.struct), _p(out),
+        _dt(out), o_ld, _p(workspace), workspace.numel(), _stream(coords)))
+    return out

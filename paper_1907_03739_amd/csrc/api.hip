@@ -1,0 +1,240 @@
+// C ABI of libpvconv: argument validation on the host, then launches on the
+// caller's stream. Nothing is enqueued when validation fails.
+#include "pv_common.h"
+
+namespace {
+
+inline bool dtype_ok(pvconv_dtype d) { return d == PVCONV_F32 || d == PVCONV_BF16; }
+inline size_t esize(pvconv_dtype d) { return d == PVCONV_BF16 ? 2 : 4; }
+inline bool act_ok(pvconv_act a) {
+    return a == PVCONV_ACT_NONE || a == PVCONV_ACT_RELU || a == PVCONV_ACT_LEAKY;
+}
+inline bool bn_ok(const pvconv_bn* bn) {
+    if (!bn || !bn->gamma) return true;
+    return bn->beta && bn->mean && bn->var && bn->eps >= 0.f;
+}
+inline hipStream_t as_stream(void* s) { return (hipStream_t)s; }
+
+// Elements must fit the int32 voxel ids and list offsets the kernels use.
+inline bool sizes_fit(long long B, long long N) { return B * N <= (1LL << 30); }
+
+struct ForwardWs {
+    void* vox_ws;
+    int32_t* counts;
+    int32_t* ids;
+    float* pnorm;
+    void* grid_a;
+    void* grid_b;
+    float* devox;
+    size_t total;
+};
+
+ForwardWs carve_forward(void* base, int B, int N, const pvconv_layer* L) {
+    const size_t V = (size_t)L->R * L->R * L->R;
+    const size_t es = esize(L->compute_dt);
+    const int cmax = L->cin > L->cout ? L->cin : L->cout;
+    size_t off = 0;
+    ForwardWs w;
+    char* p = (char*)base;
+    auto take = [&](size_t bytes) {
+        void* q = p ? p + off : nullptr;
+        off += pv_align256(bytes);
+        return q;
+    };
+    w.vox_ws = take(pv_voxelize_ws_bytes(B, N, L->R));
+    w.counts = (int32_t*)take((size_t)B * V * 4);
+    w.ids = (int32_t*)take((size_t)B * N * 4);
+    w.pnorm = (float*)take((size_t)B * N * 12);
+    w.grid_a = take((size_t)B * V * cmax * es);
+    w.grid_b = take((size_t)B * V * L->cout * es);
+    w.devox = (float*)take((size_t)B * N * L->cout * 4);
+    w.total = off;
+    return w;
+}
+
+pvconv_status check_layer(const pvconv_layer* L) {
+    if (!L) return PVCONV_EINVAL;
+    if (L->cin < 1 || L->cout < 1 || L->cin > PVCONV_MAX_CONV_CHANNELS ||
+        L->cout > PVCONV_MAX_CONV_CHANNELS || L->R < 1 || L->R > PVCONV_MAX_R ||
+        L->n_convs < 1 || L->n_convs > PVCONV_MAX_CONVS)
+        return PVCONV_EINVAL;
+    if (!dtype_ok(L->compute_dt)) return PVCONV_EINVAL;
+    if (L->compute_dt == PVCONV_BF16 && L->cout % 32 != 0) return PVCONV_ENOTSUP;
+    for (int i = 0; i < L->n_convs; i++)
+        if (!L->conv_w[i] || !bn_ok(&L->conv_bn[i])) return PVCONV_EINVAL;
+    if (!L->mlp_w || !bn_ok(&L->mlp_bn)) return PVCONV_EINVAL;
+    return PVCONV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* pvconv_status_string(pvconv_status s) {
+    switch (s) {
+        case PVCONV_OK: return "ok";
+        case PVCONV_EINVAL: return "invalid argument";
+        case PVCONV_ENOTSUP: return "unsupported argument combination";
+        case PVCONV_EWORKSPACE: return "workspace missing or too small";
+        case PVCONV_EHIP: return "HIP launch error";
+    }
+    return "unknown status";
+}
+
+size_t pvconv_voxelize_workspace_size(int B, int N, int R) {
+    if (B < 0 || N < 0 || R < 1 || R > PVCONV_MAX_R) return 0;
+    return pv_voxelize_ws_bytes(B, N, R);
+}
+
+pvconv_status pvconv_voxelize(const float* coords, const void* feats, pvconv_dtype feat_dt,
+                              int feat_ld, int B, int N, int C, int R, void* grid,
+                              pvconv_dtype grid_dt, int32_t* counts, int32_t* vox_id,
+                              float* norm_coords, void* workspace, size_t workspace_bytes,
+                              void* stream) {
+    if (B < 0 || N < 0 || C < 1 || R < 1 || R > PVCONV_MAX_R || !sizes_fit(B, N))
+        return PVCONV_EINVAL;
+    if (!dtype_ok(feat_dt) || !dtype_ok(grid_dt)) return PVCONV_EINVAL;
+    if (feat_ld == 0) feat_ld = C;
+    if (feat_ld < C) return PVCONV_EINVAL;
+    if (B == 0) return PVCONV_OK;
+    if (!grid || !counts || (N > 0 && (!coords || !feats))) return PVCONV_EINVAL;
+    if (((uintptr_t)coords & 3) || ((uintptr_t)counts & 3) || ((uintptr_t)vox_id & 3) ||
+        ((uintptr_t)norm_coords & 3) || ((uintptr_t)feats & (esize(feat_dt) - 1)) ||
+        ((uintptr_t)grid & (esize(grid_dt) - 1)))
+        return PVCONV_EINVAL;
+    if (!workspace || ((uintptr_t)workspace & 255) ||
+        workspace_bytes < pv_voxelize_ws_bytes(B, N, R))
+        return PVCONV_EWORKSPACE;
+    return pv_launch_voxelize(coords, feats, feat_dt == PVCONV_BF16, feat_ld, B, N, C, R, grid,
+                              grid_dt == PVCONV_BF16, counts, vox_id, norm_coords, workspace,
+                              as_stream(stream));
+}
+
+pvconv_status pvconv_conv3d(const void* x, int B, int R, int Cin, int Cout, const void* weight,
+                            const float* bias, const pvconv_bn* bn, pvconv_act act, float slope,
+                            pvconv_dtype dt, void* y, pvconv_dtype out_dt, void* stream) {
+    if (B < 0 || R < 1 || R > PVCONV_MAX_R || Cin < 1 || Cout < 1 ||
+        Cin > PVCONV_MAX_CONV_CHANNELS || Cout > PVCONV_MAX_CONV_CHANNELS)
+        return PVCONV_EINVAL;
+    if (!dtype_ok(dt) || !dtype_ok(out_dt) || !act_ok(act) || !bn_ok(bn)) return PVCONV_EINVAL;
+    if (B == 0) return PVCONV_OK;
+    if (!x || !weight || !y) return PVCONV_EINVAL;
+    if (((uintptr_t)x & (esize(dt) - 1)) || ((uintptr_t)weight & (esize(dt) - 1)) ||
+        ((uintptr_t)y & (esize(out_dt) - 1)) || ((uintptr_t)bias & 3))
+        return PVCONV_EINVAL;
+    if (dt == PVCONV_BF16 && Cout % 32 != 0) return PVCONV_ENOTSUP;
+    if (x == y) return PVCONV_EINVAL;
+    return pv_launch_conv3d(x, B, R, Cin, Cout, weight, pv_make_fold(bn, bias), act, slope,
+                            dt == PVCONV_BF16, y, out_dt == PVCONV_BF16, as_stream(stream));
+}
+
+pvconv_status pvconv_devoxelize(const void* grid, int B, int R, int C, pvconv_dtype grid_dt,
+                                const float* norm_coords, int N, float* out, void* stream) {
+    if (B < 0 || N < 0 || R < 1 || R > PVCONV_MAX_R || C < 1 || !sizes_fit(B, N))
+        return PVCONV_EINVAL;
+    if (!dtype_ok(grid_dt)) return PVCONV_EINVAL;
+    if (B == 0 || N == 0) return PVCONV_OK;
+    if (!grid || !norm_coords || !out) return PVCONV_EINVAL;
+    if (((uintptr_t)grid & (esize(grid_dt) - 1)) || ((uintptr_t)norm_coords & 3) ||
+        ((uintptr_t)out & 3))
+        return PVCONV_EINVAL;
+    return pv_launch_devoxelize(grid, B, R, C, grid_dt == PVCONV_BF16, norm_coords, N, out,
+                                as_stream(stream));
+}
+
+pvconv_status pvconv_point_mlp(const void* x, pvconv_dtype x_dt, int x_ld, int M, int Cin,
+                               int Cout, const void* weight, pvconv_dtype compute_dt,
+                               const float* bias, const pvconv_bn* bn, pvconv_act act,
+                               float slope, const float* cloud_bias, int points_per_cloud,
+                               const float* residual, int residual_ld, void* out,
+                               pvconv_dtype out_dt, int out_ld, void* stream) {
+    if (M < 0 || Cin < 1 || Cout < 1 || Cin > PVCONV_MAX_MLP_CHANNELS ||
+        Cout > PVCONV_MAX_MLP_CHANNELS || M > (1 << 30))
+        return PVCONV_EINVAL;
+    if (!dtype_ok(x_dt) || !dtype_ok(compute_dt) || !dtype_ok(out_dt) || !act_ok(act) ||
+        !bn_ok(bn))
+        return PVCONV_EINVAL;
+    if (x_ld == 0) x_ld = Cin;
+    if (out_ld == 0) out_ld = Cout;
+    if (residual_ld == 0) residual_ld = Cout;
+    if (x_ld < Cin || out_ld < Cout || residual_ld < Cout) return PVCONV_EINVAL;
+    if (cloud_bias && points_per_cloud < 1) return PVCONV_EINVAL;
+    if (M == 0) return PVCONV_OK;
+    if (!x || !weight || !out) return PVCONV_EINVAL;
+    if (((uintptr_t)x & (esize(x_dt) - 1)) || ((uintptr_t)weight & (esize(compute_dt) - 1)) ||
+        ((uintptr_t)out & (esize(out_dt) - 1)) || ((uintptr_t)bias & 3) ||
+        ((uintptr_t)cloud_bias & 3) || ((uintptr_t)residual & 3))
+        return PVCONV_EINVAL;
+    if (x == out) return PVCONV_EINVAL;
+    return pv_launch_point_mlp(x, x_dt == PVCONV_BF16, x_ld, M, Cin, Cout, weight,
+                               compute_dt == PVCONV_BF16, pv_make_fold(bn, bias), act, slope,
+                               cloud_bias, cloud_bias ? points_per_cloud : 1, residual,
+                               residual_ld, out, out_dt == PVCONV_BF16, out_ld,
+                               as_stream(stream));
+}
+
+pvconv_status pvconv_maxpool(const void* x, pvconv_dtype dt, int x_ld, int B, int N, int C,
+                             float* out, void* stream) {
+    if (B < 0 || N < 1 || C < 1 || !dtype_ok(dt) || !sizes_fit(B, N)) return PVCONV_EINVAL;
+    if (x_ld == 0) x_ld = C;
+    if (x_ld < C) return PVCONV_EINVAL;
+    if (B == 0) return PVCONV_OK;
+    if (!x || !out || ((uintptr_t)x & (esize(dt) - 1)) || ((uintptr_t)out & 3))
+        return PVCONV_EINVAL;
+    return pv_launch_maxpool(x, dt == PVCONV_BF16, x_ld, B, N, C, out, as_stream(stream));
+}
+
+size_t pvconv_forward_workspace_size(int B, int N, const pvconv_layer* L) {
+    if (B < 0 || N < 0 || check_layer(L) != PVCONV_OK) return 0;
+    return carve_forward(nullptr, B, N, L).total;
+}
+
+pvconv_status pvconv_forward(const float* coords, const void* feats, pvconv_dtype feat_dt,
+                             int feat_ld, int B, int N, const pvconv_layer* L, void* out,
+                             pvconv_dtype out_dt, int out_ld, void* workspace,
+                             size_t workspace_bytes, void* stream) {
+    pvconv_status st = check_layer(L);
+    if (st != PVCONV_OK) return st;
+    if (B < 0 || N < 0 || !sizes_fit(B, N) || !dtype_ok(feat_dt) || !dtype_ok(out_dt))
+        return PVCONV_EINVAL;
+    if (feat_ld == 0) feat_ld = L->cin;
+    if (out_ld == 0) out_ld = L->cout;
+    if (feat_ld < L->cin || out_ld < L->cout) return PVCONV_EINVAL;
+    if (B == 0 || N == 0) return PVCONV_OK;
+    if (!coords || !feats || !out) return PVCONV_EINVAL;
+    if (((uintptr_t)coords & 3) || ((uintptr_t)feats & (esize(feat_dt) - 1)) ||
+        ((uintptr_t)out & (esize(out_dt) - 1)))
+        return PVCONV_EINVAL;
+    const size_t need = carve_forward(nullptr, B, N, L).total;
+    if (!workspace || ((uintptr_t)workspace & 255) || workspace_bytes < need)
+        return PVCONV_EWORKSPACE;
+    ForwardWs w = carve_forward(workspace, B, N, L);
+    hipStream_t s = as_stream(stream);
+    const bool bf = L->compute_dt == PVCONV_BF16;
+    const int R = L->R;
+
+    st = pv_launch_voxelize(coords, feats, feat_dt == PVCONV_BF16, feat_ld, B, N, L->cin, R,
+                            w.grid_a, bf, w.counts, w.ids, w.pnorm, w.vox_ws, s);
+    if (st != PVCONV_OK) return st;
+    void* src = w.grid_a;
+    void* dst = w.grid_b;
+    int cin = L->cin;
+    for (int i = 0; i < L->n_convs; i++) {
+        st = pv_launch_conv3d(src, B, R, cin, L->cout, L->conv_w[i],
+                              pv_make_fold(&L->conv_bn[i], nullptr), PVCONV_ACT_LEAKY,
+                              L->conv_slope, bf, dst, bf, s);
+        if (st != PVCONV_OK) return st;
+        void* t = src;
+        src = dst;
+        dst = t;
+        cin = L->cout;
+    }
+    st = pv_launch_devoxelize(src, B, R, L->cout, bf, w.pnorm, N, w.devox, s);
+    if (st != PVCONV_OK) return st;
+    return pv_launch_point_mlp(feats, feat_dt == PVCONV_BF16, feat_ld, B * N, L->cin, L->cout,
+                               L->mlp_w, bf, pv_make_fold(&L->mlp_bn, L->mlp_b), PVCONV_ACT_RELU,
+                               0.f, nullptr, 1, w.devox, L->cout, out, out_dt == PVCONV_BF16,
+                               out_ld, s);
+}
+
+}  // extern "C"

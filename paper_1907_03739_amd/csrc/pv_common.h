@@ -1,0 +1,92 @@
+// Internal helpers shared by the gfx950 kernels of libpvconv.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "pvconv.h"
+
+typedef __attribute__((__vector_size__(8 * sizeof(short)))) short pv_bf16x8;
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float pv_f32x16;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float pv_f32x4;
+
+// bfloat16 <-> float on raw bits. Rounding is to nearest, ties to even; NaN
+// stays NaN.
+__device__ __forceinline__ float pv_bf16_to_f32(uint16_t h) {
+    return __uint_as_float(((uint32_t)h) << 16);
+}
+__device__ __forceinline__ uint16_t pv_f32_to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+__device__ __forceinline__ uint32_t pv_pack_bf16x2(float lo, float hi) {
+    return (uint32_t)pv_f32_to_bf16(lo) | ((uint32_t)pv_f32_to_bf16(hi) << 16);
+}
+
+// Folded inference batch norm for one channel: y = x * scale + shift.
+struct PvBnFold {
+    const float* gamma;
+    const float* beta;
+    const float* mean;
+    const float* var;
+    const float* bias;  // linear/conv bias folded in, may be NULL
+    float eps;
+};
+
+__device__ __forceinline__ void pv_bn_coeffs(const PvBnFold& bn, int c, float& scale,
+                                             float& shift) {
+    float b = bn.bias ? bn.bias[c] : 0.f;
+    if (bn.gamma) {
+        scale = bn.gamma[c] / sqrtf(bn.var[c] + bn.eps);
+        shift = bn.beta[c] + (b - bn.mean[c]) * scale;
+    } else {
+        scale = 1.f;
+        shift = b;
+    }
+}
+
+__device__ __forceinline__ float pv_activate(float v, int act, float slope) {
+    if (act == PVCONV_ACT_RELU) return v > 0.f ? v : 0.f;
+    if (act == PVCONV_ACT_LEAKY) return v >= 0.f ? v : v * slope;
+    return v;
+}
+
+static inline PvBnFold pv_make_fold(const pvconv_bn* bn, const float* bias) {
+    PvBnFold f;
+    f.gamma = (bn && bn->gamma) ? bn->gamma : nullptr;
+    f.beta = f.gamma ? bn->beta : nullptr;
+    f.mean = f.gamma ? bn->mean : nullptr;
+    f.var = f.gamma ? bn->var : nullptr;
+    f.eps = f.gamma ? bn->eps : 0.f;
+    f.bias = bias;
+    return f;
+}
+
+static inline pvconv_status pv_launch_status() {
+    return hipGetLastError() == hipSuccess ? PVCONV_OK : PVCONV_EHIP;
+}
+
+static inline bool pv_aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+static inline size_t pv_align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// ---- internal launchers (arguments already validated) ---------------------
+size_t pv_voxelize_ws_bytes(int B, int N, int R);
+pvconv_status pv_launch_voxelize(const float* coords, const void* feats, bool feat_bf16,
+                                 int feat_ld, int B, int N, int C, int R, void* grid,
+                                 bool grid_bf16, int32_t* counts, int32_t* vox_id,
+                                 float* norm_coords, void* ws, hipStream_t s);
+pvconv_status pv_launch_conv3d(const void* x, int B, int R, int Cin, int Cout, const void* w,
+                               const PvBnFold& bn, int act, float slope, bool bf16, void* y,
+                               bool out_bf16, hipStream_t s);
+pvconv_status pv_launch_devoxelize(const void* grid, int B, int R, int C, bool grid_bf16,
+                                   const float* pn, int N, float* out, hipStream_t s);
+pvconv_status pv_launch_point_mlp(const void* x, bool x_bf16, int x_ld, int M, int Cin,
+                                  int Cout, const void* w, bool bf16, const PvBnFold& bn,
+                                  int act, float slope, const float* cloud_bias, int ppc,
+                                  const float* residual, int res_ld, void* out, bool out_bf16,
+                                  int out_ld, hipStream_t s);
+pvconv_status pv_launch_maxpool(const void* x, bool bf16, int x_ld, int B, int N, int C,
+                                float* out, hipStream_t s);

@@ -1,0 +1,194 @@
+"""The C ABI library loads, exports every symbol include/pvconv.h declares,
+and rejects invalid arguments on the host before anything is enqueued.
+
+These run without a GPU: every call here fails validation (or has nothing to
+do) before the library touches the HIP runtime.
+"""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_1907_03739_amd import binding as b
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "pvconv.h")
+L = b._lib
+OK, EINVAL, ENOTSUP, EWS = 0, 1, 2, 3
+FAKE = ctypes.c_void_p(0x100000)    # never dereferenced: validation fails first
+FAKE_ODD = ctypes.c_void_p(0x100001)
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(pvconv_\w+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    names = declared_functions()
+    assert len(names) == 9
+    out = subprocess.run(["nm", "-D", "--defined-only", b.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (pvconv_\w+)", out))
+    assert set(names) <= exported, set(names) - exported
+    assert set(names) == set(b.EXPORTED)
+
+
+def test_status_strings():
+    for s in range(5):
+        assert L.pvconv_status_string(s)
+    assert L.pvconv_status_string(99) == b"unknown status"
+
+
+def test_workspace_queries():
+    assert L.pvconv_voxelize_workspace_size(16, 2048, 32) > 16 * 2048 * 4
+    assert L.pvconv_voxelize_workspace_size(1, 65536, 64) > 65536 * 8 * 4
+    assert L.pvconv_voxelize_workspace_size(-1, 10, 8) == 0
+    assert L.pvconv_voxelize_workspace_size(1, 10, 0) == 0
+    assert L.pvconv_voxelize_workspace_size(1, 10, 129) == 0
+    lay = _layer()
+    need = L.pvconv_forward_workspace_size(16, 2048, ctypes.byref(lay))
+    # at least: two bf16 grids of 128 channels + the fp32 devox buffer
+    assert need >= 2 * 16 * 32 ** 3 * 128 * 2 + 16 * 2048 * 128 * 4
+    lay.n_convs = 0
+    assert L.pvconv_forward_workspace_size(16, 2048, ctypes.byref(lay)) == 0
+
+
+def _vox(**kw):
+    a = dict(coords=FAKE, feats=FAKE, feat_dt=0, feat_ld=0, B=2, N=100, C=8, R=8, grid=FAKE,
+             grid_dt=1, counts=FAKE, vox_id=None, norm=None, ws=FAKE, wsb=1 << 30, s=None)
+    a.update(kw)
+    return L.pvconv_voxelize(a["coords"], a["feats"], a["feat_dt"], a["feat_ld"], a["B"], a["N"],
+                             a["C"], a["R"], a["grid"], a["grid_dt"], a["counts"], a["vox_id"],
+                             a["norm"], a["ws"], a["wsb"], a["s"])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(B=-1), EINVAL), (dict(N=-5), EINVAL), (dict(C=0), EINVAL), (dict(R=0), EINVAL),
+    (dict(R=129), EINVAL), (dict(feat_dt=7), EINVAL), (dict(grid_dt=-1), EINVAL),
+    (dict(feat_ld=4), EINVAL), (dict(grid=None), EINVAL), (dict(counts=None), EINVAL),
+    (dict(coords=None), EINVAL), (dict(feats=None), EINVAL), (dict(coords=FAKE_ODD), EINVAL),
+    (dict(grid=FAKE_ODD), EINVAL), (dict(ws=None), EWS), (dict(wsb=16), EWS),
+    (dict(ws=ctypes.c_void_p(0x100010)), EWS), (dict(B=0), OK),
+])
+def test_voxelize_rejects(kw, status):
+    assert _vox(**kw) == status
+
+
+def _conv(**kw):
+    a = dict(x=FAKE, B=1, R=8, Cin=16, Cout=64, w=FAKE, bias=None, bn=None, act=2, slope=0.1,
+             dt=1, y=ctypes.c_void_p(0x200000), out_dt=1, s=None)
+    a.update(kw)
+    return L.pvconv_conv3d(a["x"], a["B"], a["R"], a["Cin"], a["Cout"], a["w"], a["bias"],
+                           a["bn"], a["act"], a["slope"], a["dt"], a["y"], a["out_dt"], a["s"])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(B=-1), EINVAL), (dict(R=0), EINVAL), (dict(R=200), EINVAL), (dict(Cin=0), EINVAL),
+    (dict(Cout=2000), EINVAL), (dict(act=5), EINVAL), (dict(dt=3), EINVAL), (dict(x=None), EINVAL),
+    (dict(w=None), EINVAL), (dict(y=None), EINVAL), (dict(x=FAKE_ODD), EINVAL),
+    (dict(y=FAKE), EINVAL), (dict(Cout=48), ENOTSUP), (dict(B=0), OK),
+])
+def test_conv3d_rejects(kw, status):
+    assert _conv(**kw) == status
+
+
+def test_conv3d_rejects_incomplete_batchnorm():
+    bn = b.BN(0x300000, None, 0x300100, 0x300200, 1e-5)
+    assert _conv(bn=ctypes.byref(bn)) == EINVAL
+    bn = b.BN(0x300000, 0x300100, 0x300200, 0x300300, -1.0)
+    assert _conv(bn=ctypes.byref(bn)) == EINVAL
+
+
+def _devox(**kw):
+    a = dict(grid=FAKE, B=2, R=8, C=16, dt=1, pn=FAKE, N=10, out=FAKE, s=None)
+    a.update(kw)
+    return L.pvconv_devoxelize(a["grid"], a["B"], a["R"], a["C"], a["dt"], a["pn"], a["N"],
+                               a["out"], a["s"])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(B=-1), EINVAL), (dict(N=-1), EINVAL), (dict(R=0), EINVAL), (dict(C=0), EINVAL),
+    (dict(dt=9), EINVAL), (dict(grid=None), EINVAL), (dict(pn=None), EINVAL),
+    (dict(out=None), EINVAL), (dict(pn=FAKE_ODD), EINVAL), (dict(N=0), OK), (dict(B=0), OK),
+])
+def test_devoxelize_rejects(kw, status):
+    assert _devox(**kw) == status
+
+
+def _mlp(**kw):
+    a = dict(x=FAKE, x_dt=0, x_ld=0, M=100, Cin=64, Cout=128, w=FAKE, dt=1, bias=None, bn=None,
+             act=1, slope=0.0, cb=None, ppc=1, res=None, res_ld=0, out=ctypes.c_void_p(0x200000),
+             out_dt=0, out_ld=0, s=None)
+    a.update(kw)
+    return L.pvconv_point_mlp(a["x"], a["x_dt"], a["x_ld"], a["M"], a["Cin"], a["Cout"], a["w"],
+                              a["dt"], a["bias"], a["bn"], a["act"], a["slope"], a["cb"],
+                              a["ppc"], a["res"], a["res_ld"], a["out"], a["out_dt"],
+                              a["out_ld"], a["s"])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(M=-1), EINVAL), (dict(Cin=0), EINVAL), (dict(Cout=0), EINVAL),
+    (dict(Cin=20000), EINVAL), (dict(x_ld=10), EINVAL), (dict(out_ld=100), EINVAL),
+    (dict(res=FAKE, res_ld=5), EINVAL), (dict(cb=FAKE, ppc=0), EINVAL), (dict(x=None), EINVAL),
+    (dict(w=None), EINVAL), (dict(out=None), EINVAL), (dict(x_dt=5), EINVAL),
+    (dict(act=-1), EINVAL), (dict(out=FAKE), EINVAL), (dict(x=FAKE_ODD), EINVAL),
+    (dict(M=0), OK),
+])
+def test_point_mlp_rejects(kw, status):
+    assert _mlp(**kw) == status
+
+
+@pytest.mark.parametrize("args,status", [
+    ((FAKE, 1, 0, 2, 0, 8, FAKE, None), EINVAL),    # N = 0
+    ((FAKE, 1, 4, 2, 5, 8, FAKE, None), EINVAL),    # ld < C
+    ((None, 1, 0, 2, 5, 8, FAKE, None), EINVAL),
+    ((FAKE, 1, 0, 2, 5, 8, None, None), EINVAL),
+    ((FAKE, 2, 0, 2, 5, 8, FAKE, None), EINVAL),    # bad dtype
+    ((FAKE, 1, 0, 0, 5, 8, FAKE, None), OK),        # B = 0
+])
+def test_maxpool_rejects(args, status):
+    assert L.pvconv_maxpool(*args) == status
+
+
+def _layer():
+    lay = b.Layer()
+    lay.cin, lay.cout, lay.R, lay.n_convs = 64, 128, 32, 2
+    lay.conv_w[0] = lay.conv_w[1] = 0x100000
+    lay.mlp_w = 0x100000
+    lay.conv_slope = 0.1
+    lay.compute_dt = 1
+    return lay
+
+
+def _fwd(lay, **kw):
+    a = dict(coords=FAKE, feats=FAKE, fdt=0, fld=0, B=2, N=100, out=FAKE, odt=0, old=0, ws=FAKE,
+             wsb=1 << 40, s=None)
+    a.update(kw)
+    return L.pvconv_forward(a["coords"], a["feats"], a["fdt"], a["fld"], a["B"], a["N"],
+                            ctypes.byref(lay), a["out"], a["odt"], a["old"], a["ws"], a["wsb"],
+                            a["s"])
+
+
+def test_forward_rejects():
+    lay = _layer()
+    assert _fwd(lay, ws=None) == EWS
+    assert _fwd(lay, wsb=1024) == EWS
+    assert _fwd(lay, coords=None) == EINVAL
+    assert _fwd(lay, fld=3) == EINVAL
+    assert _fwd(lay, B=0) == OK
+    for field, val, status in [("n_convs", 0, EINVAL), ("n_convs", 5, EINVAL), ("R", 0, EINVAL),
+                               ("cout", 48, ENOTSUP), ("compute_dt", 4, EINVAL),
+                               ("cin", 0, EINVAL)]:
+        lay = _layer()
+        setattr(lay, field, val)
+        assert _fwd(lay) == status, field
+    lay = _layer()
+    lay.conv_w[1] = None
+    assert _fwd(lay) == EINVAL
+    lay = _layer()
+    lay.mlp_w = None
+    assert _fwd(lay) == EINVAL

@@ -1,0 +1,418 @@
+"""GPU parity: every C-ABI entry point against the fp64 CPU oracle on the same
+seeded inputs. Tolerances are explained in tests/_helpers.py.
+
+Sizes: the workloads' own shapes with the batch reduced so that the oracle
+finishes in seconds (they still span many tiles and a ragged tail), the full
+part-segmentation and stress sizes where the oracle is cheap (voxelisation,
+the whole stress layer), and sampled outputs at full size where it is not
+(the part-segmentation convolutions and layer).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from paper_1907_03739_amd import binding as pv
+from _helpers import (assert_bf16_chain, assert_bf16_step, assert_dot_f32, assert_rel,
+                            bf16_round, bn_scale, dev, dev_bn, host)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True)
+def _gpu_case(request):
+    assert torch.cuda.is_available(), "GPU tests need an MI355X"
+    print(f"\n[gpu case] {request.node.nodeid}", flush=True)
+    yield
+    torch.cuda.synchronize()
+
+
+def test_device_is_gfx950():
+    assert "gfx950" in torch.cuda.get_device_properties(0).gcnArchName
+
+
+# ----------------------------------------------------------------------------
+# voxelisation
+# ----------------------------------------------------------------------------
+def _cloud(wl_idx, B, N, C, seed=0, feat_scale=1.0):
+    wl = synth.make_workload(wl_idx, B=B, N=N)
+    f = np.random.default_rng(seed).normal(size=(B, N, C)).astype(np.float32) * feat_scale
+    return wl.coords, f
+
+
+def _oracle_vox(coords, feats, R):
+    _, _, pn = oracle.normalize(coords)
+    ids = oracle.voxel_ids(pn, R)
+    grid, counts = oracle.voxelize(ids, feats, R)
+    return pn, ids, grid, counts
+
+
+VOX_CASES = [
+    # workload, B, N, R, C, feat dtype, grid dtype
+    (1, 1, 1024, 8, 16, "f32", "f32"),        # single-layer fp32 shape
+    (2, 2, 2048, 32, 64, "f32", "f32"),       # part-seg shape, fused path
+    (2, 2, 2048, 32, 64, "f32", "bf16"),
+    (2, 16, 2048, 32, 64, "f32", "bf16"),     # part-seg full size
+    (3, 2, 2048, 32, 3, "f32", "bf16"),       # 3 channels: element-wise path
+    (4, 2, 4096, 16, 9, "f32", "bf16"),       # scene-seg shape, 9 channels
+    (5, 1, 65536, 64, 64, "f32", "bf16"),     # stress size: split path, 8 partitions
+    (2, 1, 20000, 32, 64, "f32", "f32"),      # split path with a single partition
+    (2, 2, 2048, 24, 32, "bf16", "f32"),      # R not a power of two, bf16 features
+    (1, 3, 1000, 1, 8, "f32", "f32"),         # R = 1: one voxel holds every point
+]
+
+
+@pytest.mark.parametrize("case", VOX_CASES, ids=lambda c: "wl{}_B{}_N{}_R{}_C{}_{}_{}".format(*c))
+def test_voxelize_matches_oracle(case):
+    wl_idx, B, N, R, C, fdt, gdt = case
+    coords, feats = _cloud(wl_idx, B, N, C)
+    if fdt == "bf16":
+        feats = synth.round_to_bf16(feats)
+    pn, ids, grid, counts = _oracle_vox(coords, feats, R)
+    g, c, i, p = pv.pvconv_voxelize(dev(coords), dev(feats, getattr(torch, "bfloat16" if fdt ==
+                                    "bf16" else "float32")), R,
+                                    grid_dtype=torch.bfloat16 if gdt == "bf16" else torch.float32)
+    assert np.array_equal(i.cpu().numpy(), ids)
+    assert np.array_equal(c.cpu().numpy(), counts)
+    assert np.array_equal(p.cpu().numpy(), pn.astype(np.float32))
+    if gdt == "f32":
+        assert_rel(host(g), grid, 1e-5, "voxel grid fp32")
+    else:
+        assert_bf16_step(host(g), grid, "voxel grid bf16")
+
+
+def test_voxelize_strided_features_and_optional_outputs():
+    coords, wide = _cloud(2, 2, 2048, 96)
+    feats = wide[:, :, 16:80]
+    pn, ids, grid, counts = _oracle_vox(coords, feats, 32)
+    wide_d = dev(wide)
+    g, c, i, p = pv.pvconv_voxelize(dev(coords), wide_d[:, :, 16:80], 32, want_ids=False,
+                                    want_norm=False)
+    assert i is None and p is None
+    assert np.array_equal(c.cpu().numpy(), counts)
+    assert_rel(host(g), grid, 1e-5)
+
+
+def test_voxelize_single_point_and_coincident_clouds():
+    rng = np.random.default_rng(3)
+    for N in (1, 37):
+        coords = np.repeat(rng.normal(size=(4, 1, 3)).astype(np.float32), N, axis=1)
+        feats = rng.normal(size=(4, N, 8)).astype(np.float32)
+        pn, ids, grid, counts = _oracle_vox(coords, feats, 8)
+        g, c, i, p = pv.pvconv_voxelize(dev(coords), dev(feats), 8)
+        assert np.all(i.cpu().numpy() == (4 * 8 + 4) * 8 + 4)
+        assert np.array_equal(c.cpu().numpy(), counts)
+        assert np.all(p.cpu().numpy() == 0.5)
+        assert_rel(host(g), grid, 1e-5)
+
+
+def test_voxelize_empty_clouds_give_zero_grids():
+    coords = torch.empty((2, 0, 3), device="cuda")
+    feats = torch.empty((2, 0, 16), device="cuda")
+    g, c, i, p = pv.pvconv_voxelize(coords, feats, 8)
+    assert g.shape == (2, 512, 16) and torch.all(g == 0) and torch.all(c == 0)
+    g, c, _, _ = pv.pvconv_voxelize(torch.empty((0, 5, 3), device="cuda"),
+                                    torch.empty((0, 5, 16), device="cuda"), 8)
+    assert g.numel() == 0
+
+
+def test_voxelize_is_deterministic_and_permutation_equivariant():
+    coords, feats = _cloud(5, 1, 65536, 64)
+    g1, c1, i1, p1 = pv.pvconv_voxelize(dev(coords), dev(feats), 64)
+    g2, c2, i2, p2 = pv.pvconv_voxelize(dev(coords), dev(feats), 64)
+    assert torch.equal(i1, i2) and torch.equal(c1, c2) and torch.equal(g1, g2)
+    perm = np.random.default_rng(4).permutation(65536)
+    g3, c3, i3, p3 = pv.pvconv_voxelize(dev(coords[:, perm]), dev(feats[:, perm]), 64)
+    assert np.array_equal(i3.cpu().numpy(), i1.cpu().numpy()[:, perm])
+    assert torch.equal(c3, c1)
+    assert_rel(host(g3), host(g1), 1e-6, "permuted grid")
+
+
+# ----------------------------------------------------------------------------
+# convolution
+# ----------------------------------------------------------------------------
+def _sparse_grid(rng, B, R, C, occupied=0.3):
+    x = rng.normal(size=(B, R ** 3, C))
+    x *= rng.random(size=(B, R ** 3, 1)) < occupied
+    return bf16_round(x)
+
+
+def _oracle_conv(x, w, bn, R, act="leaky", slope=0.1):
+    y = oracle.batchnorm(oracle.conv3d(x, w, R), bn)
+    return oracle.leaky_relu(y, slope) if act == "leaky" else oracle.relu(y)
+
+
+CONV_CASES = [
+    # B, R, Cin, Cout, out dtype
+    (2, 32, 64, 128, "bf16"),      # part-seg conv 1 (batch reduced)
+    (1, 32, 128, 128, "bf16"),     # part-seg conv 2
+    (1, 64, 64, 64, "bf16"),       # stress conv
+    (2, 16, 128, 128, "bf16"),     # R=16 blocks
+    (2, 32, 3, 64, "bf16"),        # 3 input channels (element-wise loads)
+    (2, 32, 9, 64, "f32"),         # 9 input channels, fp32 out
+    (1, 13, 32, 32, "bf16"),       # ragged R, 32-channel tiles
+    (1, 7, 40, 96, "f32"),         # Cin not a multiple of 32, Cout = 3 x 32
+    (3, 1, 16, 64, "bf16"),        # R = 1
+]
+
+
+@pytest.mark.parametrize("case", CONV_CASES, ids=lambda c: "B{}_R{}_{}to{}_{}".format(*c))
+def test_conv3d_bf16_matches_oracle(case):
+    B, R, Cin, Cout, odt = case
+    rng = np.random.default_rng(R * 1000 + Cin)
+    x = _sparse_grid(rng, B, R, Cin)
+    w = synth.kaiming_normal(rng, (Cout, 3, 3, 3, Cin), 27 * Cin, bf16=True)
+    bn = synth.draw_bn(rng, Cout)
+    ref = _oracle_conv(x, w, bn, R)
+    y = pv.pvconv_conv3d(dev(x, torch.bfloat16), dev(w, torch.bfloat16), R, bn=dev_bn(bn),
+                         out_dtype=torch.bfloat16 if odt == "bf16" else torch.float32)
+    assert_bf16_step(host(y), ref, f"conv {case}")
+
+
+def test_conv3d_bias_and_activations():
+    rng = np.random.default_rng(7)
+    B, R, Cin, Cout = 1, 16, 32, 64
+    x = _sparse_grid(rng, B, R, Cin)
+    w = synth.kaiming_normal(rng, (Cout, 3, 3, 3, Cin), 27 * Cin, bf16=True)
+    bias = rng.normal(size=Cout).astype(np.float32)
+    raw = oracle.conv3d(x, w, R) + bias
+    y = pv.pvconv_conv3d(dev(x, torch.bfloat16), dev(w, torch.bfloat16), R, bias=dev(bias),
+                         act="none", out_dtype=torch.float32)
+    assert_bf16_step(host(y), raw, "conv + bias, no BN, no activation")
+    y = pv.pvconv_conv3d(dev(x, torch.bfloat16), dev(w, torch.bfloat16), R, bias=dev(bias),
+                         act="relu", out_dtype=torch.float32)
+    assert_bf16_step(host(y), oracle.relu(raw), "conv + bias + ReLU")
+
+
+@pytest.mark.parametrize("B,R,Cin,Cout", [(1, 8, 16, 32), (2, 9, 5, 7), (1, 1, 3, 4)])
+def test_conv3d_f32_matches_oracle(B, R, Cin, Cout):
+    rng = np.random.default_rng(R + Cin)
+    x = rng.normal(size=(B, R ** 3, Cin)).astype(np.float32).astype(np.float64)
+    w = synth.kaiming_normal(rng, (Cout, 3, 3, 3, Cin), 27 * Cin, bf16=False)
+    bn = synth.draw_bn(rng, Cout)
+    ref = _oracle_conv(x, w, bn, R)
+    mag = oracle.conv3d(np.abs(x), np.abs(w), R) * bn_scale(bn) + np.abs(
+        bn.mean * bn_scale(bn)) + np.abs(bn.beta)
+    y = pv.pvconv_conv3d(dev(x), dev(w), R, bn=dev_bn(bn), out_dtype=torch.float32)
+    assert_dot_f32(host(y), ref, mag, "conv fp32")
+
+
+def test_conv3d_full_size_part_seg_sampled():
+    # part-seg conv 1 at full batch (16 clouds, R=32, 64 -> 128) in the launch
+    # configuration the benchmark uses; the oracle evaluates 600 sampled outputs,
+    # a third of them on the grid's faces.
+    rng = np.random.default_rng(11)
+    B, R, Cin, Cout = 16, 32, 64, 128
+    x = _sparse_grid(rng, B, R, Cin, occupied=0.06)
+    w = synth.kaiming_normal(rng, (Cout, 3, 3, 3, Cin), 27 * Cin, bf16=True)
+    bn = synth.draw_bn(rng, Cout)
+    y = host(pv.pvconv_conv3d(dev(x, torch.bfloat16), dev(w, torch.bfloat16), R, bn=dev_bn(bn)))
+    sel = rng.choice(B * R ** 3, size=400, replace=False)
+    face = rng.integers(0, R, size=(200, 3))
+    face[np.arange(200), rng.integers(0, 3, 200)] = rng.choice([0, R - 1], 200)
+    sel = np.concatenate([sel, rng.integers(0, B, 200) * R ** 3 +
+                          (face[:, 0] * R + face[:, 1]) * R + face[:, 2]])
+    ref = oracle.leaky_relu(oracle.batchnorm(oracle.conv3d_at(x, w, R, sel), bn), 0.1)
+    assert_bf16_step(y.reshape(-1, Cout)[sel], ref, "full-size conv samples")
+
+
+# ----------------------------------------------------------------------------
+# devoxelisation
+# ----------------------------------------------------------------------------
+@pytest.mark.parametrize("wl_idx,B,N,R,C,gdt", [
+    (2, 2, 2048, 32, 128, "bf16"), (5, 1, 65536, 64, 64, "bf16"), (1, 1, 1024, 8, 32, "f32"),
+    (4, 2, 4096, 16, 64, "bf16"), (2, 2, 999, 24, 3, "f32"), (2, 16, 2048, 32, 128, "bf16"),
+])
+def test_devoxelize_matches_oracle(wl_idx, B, N, R, C, gdt):
+    rng = np.random.default_rng(R * 7 + C)
+    wl = synth.make_workload(wl_idx, B=B, N=N)
+    _, _, pn = oracle.normalize(wl.coords)
+    pn32 = pn.astype(np.float32)
+    G = rng.normal(size=(B, R ** 3, C))
+    if gdt == "bf16":
+        G = bf16_round(G)
+    ref = oracle.devoxelize(G, R, pn32)
+    mag = oracle.devoxelize(np.abs(G), R, pn32)
+    out = pv.pvconv_devoxelize(dev(G, torch.bfloat16 if gdt == "bf16" else torch.float32), R,
+                               dev(pn32))
+    assert_dot_f32(host(out), ref, mag, "devoxelize")
+
+
+# ----------------------------------------------------------------------------
+# point MLP with fused epilogue
+# ----------------------------------------------------------------------------
+MLP_CASES = [
+    # M, Cin, Cout, x dtype, bias, bn, act, residual, cloud bias (points per cloud)
+    (4096, 64, 128, "bf16", False, True, "relu", True, 0),
+    (32768, 64, 128, "bf16", False, True, "relu", True, 0),   # part-seg point branch, full
+    (1000, 3, 64, "bf16", False, True, "relu", False, 0),
+    (1000, 9, 64, "bf16", True, True, "leaky", True, 0),
+    (777, 128, 50, "bf16", True, False, "none", False, 0),    # logits layer
+    (4100, 256, 13, "bf16", True, False, "none", False, 0),
+    (2048, 512, 256, "bf16", False, True, "relu", False, 512),
+    (65536, 64, 64, "bf16", False, True, "relu", True, 0),    # stress point branch, full
+]
+
+
+@pytest.mark.parametrize("case", MLP_CASES, ids=lambda c: "M{}_{}to{}_{}_{}".format(*c[:4], c[6]))
+def test_point_mlp_bf16_matches_oracle(case):
+    M, Cin, Cout, xdt, use_b, use_bn, act, use_res, ppc = case
+    rng = np.random.default_rng(M + Cin)
+    x = bf16_round(rng.normal(size=(M, Cin)))
+    w = synth.kaiming_normal(rng, (Cout, Cin), Cin, bf16=True)
+    bias = rng.normal(size=Cout).astype(np.float32) if use_b else None
+    bn = synth.draw_bn(rng, Cout) if use_bn else None
+    res = rng.normal(size=(M, Cout)).astype(np.float32) if use_res else None
+    cb = rng.normal(size=(M // ppc, Cout)).astype(np.float32) if ppc else None
+    y = oracle.linear(x, w, bias)
+    if cb is not None:
+        y = y + np.repeat(cb, ppc, axis=0)
+    if bn is not None:
+        y = oracle.batchnorm(y, bn)
+    y = {"relu": oracle.relu, "leaky": lambda a: oracle.leaky_relu(a, 0.2),
+         "none": lambda a: a}[act](y)
+    if res is not None:
+        y = y + res
+    out = pv.pvconv_point_mlp(dev(x, torch.bfloat16), dev(w, torch.bfloat16),
+                              bias=dev(bias) if use_b else None,
+                              bn=dev_bn(bn) if use_bn else None, act=act, slope=0.2,
+                              cloud_bias=dev(cb) if ppc else None, points_per_cloud=max(ppc, 1),
+                              residual=dev(res) if use_res else None)
+    assert_bf16_step(host(out), y, f"point mlp {case}")
+
+
+def test_point_mlp_fp32_inputs_strided_rows_and_bf16_out():
+    rng = np.random.default_rng(21)
+    M, Cin, Cout = 3000, 64, 128
+    wide = rng.normal(size=(M, 200)).astype(np.float32)
+    w = synth.kaiming_normal(rng, (Cout, Cin), Cin, bf16=True)
+    bn = synth.draw_bn(rng, Cout)
+    # fp32 inputs are rounded to bf16 by the kernel: the oracle takes the same rounded values
+    ref = oracle.relu(oracle.batchnorm(oracle.linear(bf16_round(wide[:, 40:104]), w), bn))
+    dst = torch.zeros((M, 300), dtype=torch.bfloat16, device="cuda")
+    xd = dev(wide)
+    pv.pvconv_point_mlp(xd[:, 40:104], dev(w, torch.bfloat16), bn=dev_bn(bn),
+                        out=dst[:, 100:228])
+    got = host(dst)
+    assert_bf16_step(got[:, 100:228], ref, "strided mlp")
+    assert np.all(got[:, :100] == 0) and np.all(got[:, 228:] == 0)
+
+
+@pytest.mark.parametrize("M,Cin,Cout", [(1024, 16, 32), (333, 7, 5)])
+def test_point_mlp_f32_matches_oracle(M, Cin, Cout):
+    rng = np.random.default_rng(M)
+    x = rng.normal(size=(M, Cin)).astype(np.float32).astype(np.float64)
+    w = synth.kaiming_normal(rng, (Cout, Cin), Cin, bf16=False)
+    bn = synth.draw_bn(rng, Cout)
+    res = rng.normal(size=(M, Cout)).astype(np.float32)
+    ref = oracle.relu(oracle.batchnorm(oracle.linear(x, w), bn)) + res
+    mag = np.abs(x) @ np.abs(w.T) * bn_scale(bn) + np.abs(bn.mean * bn_scale(bn)) + \
+        np.abs(bn.beta) + np.abs(res)
+    out = pv.pvconv_point_mlp(dev(x), dev(w), bn=dev_bn(bn), residual=dev(res))
+    assert_dot_f32(host(out), ref, mag, "mlp fp32")
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_maxpool_matches_oracle(dt):
+    rng = np.random.default_rng(5)
+    x = rng.normal(size=(8, 2048, 2600)).astype(np.float32).astype(np.float64)
+    if dt == "bf16":
+        x = bf16_round(x)
+    ref = oracle.maxpool(x[:, :, 300:2348])
+    xd = dev(x, torch.bfloat16 if dt == "bf16" else torch.float32)
+    out = pv.pvconv_maxpool(xd[:, :, 300:2348])
+    assert np.array_equal(host(out), ref)
+
+
+# ----------------------------------------------------------------------------
+# whole layer
+# ----------------------------------------------------------------------------
+def _run_layer(wl, L, dtype):
+    layer = pv.DeviceLayer(L, "cuda", dtype)
+    return host(pv.pvconv_forward(dev(wl.coords), dev(wl.feats), layer))
+
+
+def test_forward_fp32_single_layer_full_size():
+    wl = synth.make_workload(1)
+    ref = oracle.pvconv_forward(wl.coords, wl.feats, wl.layers[0])
+    got = _run_layer(wl, wl.layers[0], torch.float32)
+    rms = np.sqrt(np.mean(ref ** 2))
+    assert_dot_f32(got, ref, np.full_like(ref, rms), "fp32 layer")
+
+
+@pytest.mark.parametrize("wl_idx,B", [(2, 2), (5, 1)])
+def test_forward_bf16_layer(wl_idx, B):
+    wl = synth.make_workload(wl_idx, B=B)
+    ref = oracle.pvconv_forward(wl.coords, wl.feats, wl.layers[0])
+    got = _run_layer(wl, wl.layers[0], torch.bfloat16)
+    assert_bf16_chain(got, ref, f"layer wl{wl_idx}")
+
+
+def test_forward_scene_first_block_nine_channels():
+    wl = synth.make_workload(4, B=2)
+    L = wl.layers[0]
+    ref = oracle.pvconv_forward(wl.coords, wl.feats, L)
+    assert_bf16_chain(_run_layer(wl, L, torch.bfloat16), ref, "scene block 1")
+
+
+def _oracle_layer_at(coords, feats, L, pts):
+    """The layer's output at selected points (b, k), computing each
+    convolution only at the voxels those points depend on."""
+    clouds = sorted({b for b, _ in pts})
+    loc = {b: i for i, b in enumerate(clouds)}
+    R, V = L.R, L.R ** 3
+    _, _, pn = oracle.normalize(coords[clouds])
+    grid, _ = oracle.voxelize(oracle.voxel_ids(pn, R), feats[clouds], R)
+    sel_pn = np.stack([pn[loc[b], k] for b, k in pts])
+    cells, _ = oracle.devoxelize_weights(sel_pn, R)
+    need = [set() for _ in range(L.n_convs)]
+    for (b, _), cs in zip(pts, cells):
+        need[-1].update(loc[b] * V + int(c) for c in cs)
+    for i in range(L.n_convs - 1, 0, -1):   # conv i reads conv i-1 at the 27 neighbours
+        for s in need[i]:
+            lb, r = divmod(s, V)
+            u, v, w = r // (R * R), (r // R) % R, r % R
+            for du in (-1, 0, 1):
+                for dv in (-1, 0, 1):
+                    for dw in (-1, 0, 1):
+                        a, bb, c = u + du, v + dv, w + dw
+                        if 0 <= a < R and 0 <= bb < R and 0 <= c < R:
+                            need[i - 1].add(lb * V + (a * R + bb) * R + c)
+    h = grid
+    for i, (wt, bn) in enumerate(zip(L.conv_w, L.conv_bn)):
+        sel = np.array(sorted(need[i]), np.int64)
+        y = oracle.leaky_relu(oracle.batchnorm(oracle.conv3d_at(h, wt, R, sel), bn), L.slope)
+        h = np.zeros((len(clouds), V, L.cout))
+        h.reshape(-1, L.cout)[sel] = y
+    out = []
+    for j, (b, k) in enumerate(pts):
+        dvx = oracle.devoxelize(h[loc[b]][None], R, sel_pn[j][None, None])[0, 0]
+        pt = oracle.point_branch(feats[b, k][None], L)[0]
+        out.append(dvx + pt)
+    return np.array(out)
+
+
+def test_forward_part_seg_full_size_sampled():
+    wl = synth.make_workload(2)
+    L = wl.layers[0]
+    got = _run_layer(wl, L, torch.bfloat16)
+    rng = np.random.default_rng(9)
+    pts = [(int(b), int(k)) for b in (3, 11) for k in rng.choice(wl.N, 24, replace=False)]
+    ref = _oracle_layer_at(wl.coords, wl.feats, L, pts)
+    sub = np.stack([got[b, k] for b, k in pts])
+    # the chain tolerance's RMS floor uses the whole sampled block
+    assert_bf16_chain(sub, ref, "part-seg layer, sampled points")
+
+
+def test_forward_on_a_side_stream_and_repeatable():
+    wl = synth.make_workload(2, B=2)
+    layer = pv.DeviceLayer(wl.layers[0], "cuda", torch.bfloat16)
+    c, f = dev(wl.coords), dev(wl.feats)
+    a = pv.pvconv_forward(c, f, layer)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        b = pv.pvconv_forward(c, f, layer)
+    s.synchronize()
+    assert torch.equal(a, b)
