@@ -1,0 +1,247 @@
+#!/usr/bin/env python3
+"""Benchmark of the PVConv forward (one layer) on one MI355X.
+
+A step is one call of pvconv_forward on the whole batch: normalisation and
+voxelisation, the two 3x3x3 convolutions with batch norm and leaky ReLU,
+trilinear devoxelisation and the point-branch MLP whose epilogue adds the two
+branches (Section 4 of the PVCNN paper). Inputs (coordinates, features,
+weights) are resident in device memory before the timed region starts.
+
+Default workload: the part-segmentation-scale layer, 16 clouds x 2048 points,
+64 -> 128 channels, R = 32, bf16 operands with fp32 accumulation.
+
+Printed: ONE JSON line with the headline throughput (points/s), ms per layer,
+the roofline of the dominant kernel (the convolution, MFMA-bound), per-step
+timings of the same chain, and the CPU oracle timed on a bounded sample of the
+same workload (which also checks the GPU output on that sample).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "PVConv fwd points/sec + ms/layer (N=2048,R=32,C=64→128); % HBM/MFMA peak"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_F32_TFLOPS = 157.3     # MI355X fp32 vector
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", type=int, default=2, choices=(1, 2, 5),
+                    help="single-layer workload: 1 fp32 R=8, 2 part-seg R=32, 5 stress R=64")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="lower bound of CPU work for the oracle baseline sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+def conv_flops(B, R, cin, cout):
+    return 2.0 * 27 * cin * cout * B * R ** 3
+
+
+def distinct_corners(pn, R):
+    """Number of distinct (cloud, cell) pairs the trilinear gather touches,
+    from the normalised coordinates the GPU wrote (for the algorithmic byte
+    count of devoxelisation)."""
+    import numpy as np
+    B = pn.shape[0]
+    t = np.clip(pn.astype(np.float64) * R - 0.5, 0.0, R - 1)
+    i0 = np.floor(t).astype(np.int64)
+    i1 = np.minimum(i0 + 1, R - 1)
+    total = 0
+    for b in range(B):
+        cells = []
+        for a in (i0[b], i1[b]):
+            for e in (i0[b], i1[b]):
+                for g in (i0[b], i1[b]):
+                    cells.append((a[:, 0] * R + e[:, 1]) * R + g[:, 2])
+        total += np.unique(np.concatenate(cells)).size
+    return total
+
+
+def cpu_baseline(wl, gpu_out, seconds):
+    """The oracle on the first clouds of the same workload, one at a time,
+    until at least `seconds` of CPU work; also compares the GPU output on
+    those clouds against it (the bf16 chain bound of the parity tests)."""
+    import numpy as np
+    import oracle
+    L = wl.layers[0]
+    oracle.pvconv_forward(wl.coords[:1, :8], wl.feats[:1, :8], L)  # load the library
+    cores = int(os.environ.get("OMP_NUM_THREADS") or len(os.sched_getaffinity(0)))
+    done, worst, t_total = 0, 0.0, 0.0
+    for b in range(wl.B):
+        t0 = time.perf_counter()
+        ref = oracle.pvconv_forward(wl.coords[b:b + 1], wl.feats[b:b + 1], L)[0]
+        t_total += time.perf_counter() - t0
+        rms = float(np.sqrt(np.mean(ref ** 2)))
+        worst = max(worst, float(np.max(np.abs(gpu_out[b] - ref) / (np.abs(ref) + rms))))
+        done += 1
+        if t_total >= seconds:
+            break
+    tol = 2e-2 if wl.dtype == "bf16" else 1e-5
+    return ({"value": done * wl.N / t_total, "unit": "points/s", "cores": cores,
+             "kind": "oracle",
+             "sample": f"first {done} of {wl.B} clouds ({done * wl.N} points), one cloud per "
+                       f"oracle call, fp64, {t_total:.1f} s"},
+            {"clouds": done, "max_err": worst, "bound": tol, "ok": worst <= tol})
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py runs on exactly one GPU: the PVConv forward here is a single-GPU "
+              "build (the batch would shard by cloud across GPUs, which is not built). "
+              "Use --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_1907_03739_amd import binding as pv
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    wl = synth.make_workload(args.workload)
+    L = wl.layers[0]
+    bf16 = wl.dtype == "bf16"
+    cdt = torch.bfloat16 if bf16 else torch.float32
+    B, N, R, cin, cout = wl.B, wl.N, L.R, L.cin, L.cout
+    layer = pv.DeviceLayer(L, dev, cdt)
+    coords = torch.as_tensor(wl.coords).to(dev)
+    feats = torch.as_tensor(wl.feats).to(dev)
+    out = torch.empty((B, N, cout), dtype=torch.float32, device=dev)
+    ws = torch.empty(max(pv.pvconv_forward_workspace_size(B, N, layer), 256), dtype=torch.uint8,
+                     device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    # ---- headline: K whole-layer steps -----------------------------------
+    for _ in range(args.warmup):
+        pv.pvconv_forward(coords, feats, layer, out=out, workspace=ws)
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    t0 = time.perf_counter()
+    ev[0].record(stream)
+    for i in range(args.steps):
+        pv.pvconv_forward(coords, feats, layer, out=out, workspace=ws)
+        ev[i + 1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    step_ms = [ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)]
+    ms_per_step = wall * 1e3 / args.steps
+    gpu_out = out.double().cpu().numpy()
+
+    # ---- per-step breakdown: the same chain as separate C-ABI calls, with
+    # events between them on the stream the kernels run on ----------------
+    names = ["voxelize"] + [f"conv{i + 1}" for i in range(L.n_convs)] + ["devoxelize",
+                                                                         "point_mlp"]
+    per = {n: [] for n in names}
+
+    def chain(record):
+        marks = [torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)]
+        marks[0].record(stream)
+        g, _, _, pn = pv.pvconv_voxelize(coords, feats, R, grid_dtype=cdt, want_ids=True)
+        marks[1].record(stream)
+        h = g
+        for i in range(L.n_convs):
+            h = pv.pvconv_conv3d(h, layer.conv_w[i], R, bn=layer.conv_bn[i], act="leaky",
+                                 slope=L.slope, out_dtype=cdt)
+            marks[2 + i].record(stream)
+        dv = pv.pvconv_devoxelize(h, R, pn)
+        marks[2 + L.n_convs].record(stream)
+        pv.pvconv_point_mlp(feats, layer.mlp_w, bias=layer.mlp_b, bn=layer.mlp_bn, act="relu",
+                            residual=dv, out=out)
+        marks[3 + L.n_convs].record(stream)
+        if record is not None:
+            record.append(marks)
+        return pn
+
+    for _ in range(max(2, args.warmup // 2)):
+        chain(None)
+    torch.cuda.synchronize()
+    recs = []
+    for _ in range(args.steps):
+        pn = chain(recs)
+    torch.cuda.synchronize()
+    for marks in recs:
+        for j, n in enumerate(names):
+            per[n].append(marks[j].elapsed_time(marks[j + 1]))
+    pn_host = pn.cpu().numpy()
+
+    # ---- algorithmic work per step ---------------------------------------
+    s_g = 2 if bf16 else 4
+    V = R ** 3
+    work = {
+        "voxelize": ("GB/s", B * N * (12 + 4 * cin + 4) + B * V * (cin * s_g + 4)),
+        "devoxelize": ("GB/s", B * N * (12 + 4 * cout) + distinct_corners(pn_host, R) * cout * s_g),
+        "point_mlp": ("GB/s", B * N * (4 * cin + 8 * cout)),
+    }
+    c = cin
+    for i in range(L.n_convs):
+        work[f"conv{i + 1}"] = ("TFLOP/s", conv_flops(B, R, c, cout))
+        c = cout
+    kernels = {}
+    for n in names:
+        unit, amount = work[n]
+        ms = statistics.mean(per[n])
+        if unit == "GB/s":
+            rate, peak = amount / (ms * 1e-3) / 1e9, PEAK_HBM_GBS
+        else:
+            rate = amount / (ms * 1e-3) / 1e12
+            peak = PEAK_BF16_TFLOPS if bf16 else PEAK_F32_TFLOPS
+        kernels[n] = {"ms": round(ms, 4), "ms_min": round(min(per[n]), 4),
+                      "achieved": round(rate, 2), "unit": unit, "frac": round(rate / peak, 4),
+                      "algorithmic": amount}
+
+    # dominant kernel: the convolution (one kernel, L.n_convs launches per step)
+    conv_names = [f"conv{i + 1}" for i in range(L.n_convs)]
+    conv_ms = statistics.mean([kernels[n]["ms"] for n in conv_names])
+    conv_work = statistics.mean([work[n][1] for n in conv_names])
+    conv_peak = PEAK_BF16_TFLOPS if bf16 else PEAK_F32_TFLOPS
+    achieved = conv_work / (conv_ms * 1e-3) / 1e12
+    roofline = {"bound": "mfma" if bf16 else "alu", "achieved": round(achieved, 2),
+                "peak": conv_peak, "unit": "TFLOP/s", "frac": round(achieved / conv_peak, 4),
+                "traffic": None, "kernel": "pv_conv3d_bf16_kernel" if bf16 else
+                "pv_conv3d_f32_kernel", "flop_per_launch": conv_work,
+                "avg_launch_ms": round(conv_ms, 4)}
+
+    line = {
+        "metric": METRIC, "value": round(B * N / (ms_per_step * 1e-3), 1), "unit": "points/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16" if bf16 else "f32", "data": "synthetic",
+        "config": {"workload": wl.name, "B": B, "N": N, "R": R, "cin": cin, "cout": cout,
+                   "n_convs": L.n_convs, "points_per_step": B * N},
+        "ms_per_layer": round(ms_per_step, 4),
+        "ms_per_step_events": {"median": round(statistics.median(step_ms), 4),
+                               "min": round(min(step_ms), 4)},
+        "roofline": roofline,
+        "kernels": kernels,
+        "inputs_sha256": wl.sha256(),
+    }
+    if not args.no_cpu_baseline:
+        cb, parity = cpu_baseline(wl, gpu_out, args.cpu_seconds)
+        line["cpu_baseline"] = cb
+        line["parity_sample"] = parity
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

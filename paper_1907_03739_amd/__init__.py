@@ -3,8 +3,23 @@
 The computation lives in libpvconv.so (HIP kernels behind the C ABI declared in
 include/pvconv.h); `binding` marshals torch tensors into those calls and
 `network` chains them into the PVCNN segmentation networks.
+
+The binding is imported on first use of one of its names, so that the build
+module stays importable before libpvconv.so exists. Using any entry point
+without the library raises ImportError: there is no fallback.
 """
-from .binding import (  # noqa: F401
-    BF16, F32, DeviceLayer, PVConvError, pvconv_conv3d, pvconv_devoxelize, pvconv_forward,
-    pvconv_forward_workspace_size, pvconv_maxpool, pvconv_point_mlp, pvconv_voxelize,
+import importlib
+
+_BINDING_NAMES = (
+    "BF16", "F32", "DeviceLayer", "PVConvError", "pvconv_conv3d", "pvconv_devoxelize",
+    "pvconv_forward", "pvconv_forward_workspace_size", "pvconv_maxpool", "pvconv_point_mlp",
+    "pvconv_voxelize",
 )
+
+__all__ = list(_BINDING_NAMES)
+
+
+def __getattr__(name):
+    if name in _BINDING_NAMES:
+        return getattr(importlib.import_module(".binding", __name__), name)
+    raise AttributeError(f"module {__name__!r} has no attribute {name!r}")
