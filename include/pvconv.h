@@ -124,12 +124,16 @@ pvconv_status pvconv_voxelize(const float* coords, const void* feats, pvconv_dty
 /*  act     NONE / RELU / LEAKY (negative slope `slope`)                     */
 /*  y       out [B][R^3][Cout], dtype out_dt                                 */
 /* dt = BF16: MFMA implicit GEMM, bf16 x bf16 -> fp32; needs Cout % 32 == 0. */
-/* dt = F32: fp32 FMA. 1 <= Cin, Cout <= 1024, 1 <= R <= 128. x and y must   */
-/* not overlap.                                                              */
+/* It first repacks the weights into the MFMA fragment order inside          */
+/* `workspace` (>= pvconv_conv3d_workspace_size bytes, 256-byte aligned;     */
+/* contents on entry ignored). dt = F32: fp32 FMA, no workspace (may be      */
+/* NULL). 1 <= Cin, Cout <= 1024, 1 <= R <= 128. x and y must not overlap.   */
 /* ------------------------------------------------------------------------- */
+size_t pvconv_conv3d_workspace_size(int Cin, int Cout, pvconv_dtype dt);
 pvconv_status pvconv_conv3d(const void* x, int B, int R, int Cin, int Cout, const void* weight,
                             const float* bias, const pvconv_bn* bn, pvconv_act act, float slope,
-                            pvconv_dtype dt, void* y, pvconv_dtype out_dt, void* stream);
+                            pvconv_dtype dt, void* y, pvconv_dtype out_dt, void* workspace,
+                            size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------- */
 /* Trilinear devoxelisation: Section 4.1 "Devoxelization".                   */

@@ -49,7 +49,9 @@ _SIGS = {
     "pvconv_voxelize_workspace_size": ([_I, _I, _I], _SZ),
     "pvconv_voxelize": ([_VP, _VP, _I, _I, _I, _I, _I, _I, _VP, _I, _VP, _VP, _VP, _VP, _SZ, _VP],
                         _I),
-    "pvconv_conv3d": ([_VP, _I, _I, _I, _I, _VP, _VP, _VP, _I, _F, _I, _VP, _I, _VP], _I),
+    "pvconv_conv3d_workspace_size": ([_I, _I, _I], _SZ),
+    "pvconv_conv3d": ([_VP, _I, _I, _I, _I, _VP, _VP, _VP, _I, _F, _I, _VP, _I, _VP, _SZ, _VP],
+                      _I),
     "pvconv_devoxelize": ([_VP, _I, _I, _I, _I, _VP, _I, _VP, _VP], _I),
     "pvconv_point_mlp": ([_VP, _I, _I, _I, _I, _I, _VP, _I, _VP, _VP, _I, _F, _VP, _I, _VP, _I,
                           _VP, _I, _I, _VP], _I),
@@ -150,18 +152,23 @@ def pvconv_voxelize(coords: torch.Tensor, feats: torch.Tensor, R: int,
 
 def pvconv_conv3d(x: torch.Tensor, weight: torch.Tensor, R: int, bn=None,
                   bias: Optional[torch.Tensor] = None, act="leaky", slope=0.1,
-                  out_dtype=None):
+                  out_dtype=None, out: Optional[torch.Tensor] = None,
+                  workspace: Optional[torch.Tensor] = None):
     """x [B][R^3][Cin], weight [Cout][3][3][3][Cin] (same dtype) -> y [B][R^3][Cout]."""
     B, V, Cin = x.shape
     Cout = weight.shape[0]
     if V != R ** 3 or tuple(weight.shape[1:]) != (3, 3, 3, Cin):
         raise ValueError("shape mismatch")
-    y = torch.empty((B, V, Cout), dtype=_torch_dt(out_dtype or x.dtype), device=x.device)
+    y = out if out is not None else torch.empty(
+        (B, V, Cout), dtype=_torch_dt(out_dtype or x.dtype), device=x.device)
+    need = _lib.pvconv_conv3d_workspace_size(Cin, Cout, _dt(x))
+    if need and (workspace is None or workspace.numel() < need):
+        workspace = torch.empty(need, dtype=torch.uint8, device=x.device)
     bns = _bn_struct(bn)
     _check("pvconv_conv3d", _lib.pvconv_conv3d(
         _p(x.contiguous()), B, R, Cin, Cout, _p(weight.contiguous()), _p(bias),
         ctypes.byref(bns) if bn is not None else None, ACT[act], slope, _dt(x), _p(y), _dt(y),
-        _stream(x)))
+        _p(workspace) if need else None, workspace.numel() if need else 0, _stream(x)))
     return y
 
 

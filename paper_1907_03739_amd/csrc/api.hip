@@ -19,6 +19,7 @@ inline hipStream_t as_stream(void* s) { return (hipStream_t)s; }
 inline bool sizes_fit(long long B, long long N) { return B * N <= (1LL << 30); }
 
 struct ForwardWs {
+    void* conv_ws[PVCONV_MAX_CONVS];
     void* vox_ws;
     int32_t* counts;
     int32_t* ids;
@@ -41,6 +42,10 @@ ForwardWs carve_forward(void* base, int B, int N, const pvconv_layer* L) {
         off += pv_align256(bytes);
         return q;
     };
+    for (int i = 0; i < PVCONV_MAX_CONVS; i++)
+        w.conv_ws[i] = i < L->n_convs ? take(pv_conv3d_ws_bytes(i ? L->cout : L->cin, L->cout,
+                                                                L->compute_dt == PVCONV_BF16))
+                                      : nullptr;
     w.vox_ws = take(pv_voxelize_ws_bytes(B, N, L->R));
     w.counts = (int32_t*)take((size_t)B * V * 4);
     w.ids = (int32_t*)take((size_t)B * N * 4);
@@ -110,9 +115,17 @@ pvconv_status pvconv_voxelize(const float* coords, const void* feats, pvconv_dty
                               as_stream(stream));
 }
 
+size_t pvconv_conv3d_workspace_size(int Cin, int Cout, pvconv_dtype dt) {
+    if (Cin < 1 || Cout < 1 || Cin > PVCONV_MAX_CONV_CHANNELS || Cout > PVCONV_MAX_CONV_CHANNELS ||
+        !dtype_ok(dt))
+        return 0;
+    return pv_conv3d_ws_bytes(Cin, Cout, dt == PVCONV_BF16);
+}
+
 pvconv_status pvconv_conv3d(const void* x, int B, int R, int Cin, int Cout, const void* weight,
                             const float* bias, const pvconv_bn* bn, pvconv_act act, float slope,
-                            pvconv_dtype dt, void* y, pvconv_dtype out_dt, void* stream) {
+                            pvconv_dtype dt, void* y, pvconv_dtype out_dt, void* workspace,
+                            size_t workspace_bytes, void* stream) {
     if (B < 0 || R < 1 || R > PVCONV_MAX_R || Cin < 1 || Cout < 1 ||
         Cin > PVCONV_MAX_CONV_CHANNELS || Cout > PVCONV_MAX_CONV_CHANNELS)
         return PVCONV_EINVAL;
@@ -124,8 +137,12 @@ pvconv_status pvconv_conv3d(const void* x, int B, int R, int Cin, int Cout, cons
         return PVCONV_EINVAL;
     if (dt == PVCONV_BF16 && Cout % 32 != 0) return PVCONV_ENOTSUP;
     if (x == y) return PVCONV_EINVAL;
+    const size_t need = pv_conv3d_ws_bytes(Cin, Cout, dt == PVCONV_BF16);
+    if (need && (!workspace || ((uintptr_t)workspace & 255) || workspace_bytes < need))
+        return PVCONV_EWORKSPACE;
     return pv_launch_conv3d(x, B, R, Cin, Cout, weight, pv_make_fold(bn, bias), act, slope,
-                            dt == PVCONV_BF16, y, out_dt == PVCONV_BF16, as_stream(stream));
+                            dt == PVCONV_BF16, y, out_dt == PVCONV_BF16, workspace,
+                            as_stream(stream));
 }
 
 pvconv_status pvconv_devoxelize(const void* grid, int B, int R, int C, pvconv_dtype grid_dt,
@@ -222,7 +239,7 @@ pvconv_status pvconv_forward(const float* coords, const void* feats, pvconv_dtyp
     for (int i = 0; i < L->n_convs; i++) {
         st = pv_launch_conv3d(src, B, R, cin, L->cout, L->conv_w[i],
                               pv_make_fold(&L->conv_bn[i], nullptr), PVCONV_ACT_LEAKY,
-                              L->conv_slope, bf, dst, bf, s);
+                              L->conv_slope, bf, dst, bf, w.conv_ws[i], s);
         if (st != PVCONV_OK) return st;
         void* t = src;
         src = dst;

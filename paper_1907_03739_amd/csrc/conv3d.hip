@@ -2,166 +2,296 @@
 // (Section 4.1 "Feature Aggregation"; fixed-offset kernel of Section 3, Eq. 1).
 //
 // bf16 path: implicit GEMM on the MFMA units. M = output voxels, N = output
-// channels, K = 27 taps x input channels. A workgroup owns a 4x8x8 brick of
-// output voxels and NT output channels. For each chunk of 32 input channels it
-// stages the brick's 6x10x10 halo in LDS once (zero-filled outside the grid),
-// then walks the 27 taps: each tap's A operand is the halo shifted by the tap
-// offset, read straight from LDS, and the tap's NT x 32 weight slice is
-// double-buffered through LDS. Each of the 4 waves computes one u-slice of the
-// brick (64 voxels = two 32-row MFMA blocks) against all NT channels with
-// v_mfma_f32_32x32x16_bf16, so every A fragment feeds NT/32 MFMAs and every B
-// fragment two. The epilogue folds bias + batch norm into one scale/shift per
-// channel, applies the activation and stores bf16 or fp32.
+// channels, K = 27 taps x input channels.
+//
+//  * One 256-thread workgroup per CU owns an 8x8x8 brick of output voxels and
+//    32*NB output channels. Each wave computes two u-slices of the brick (128
+//    voxels) against all 32*NB channels with v_mfma_f32_32x32x16_bf16: A =
+//    weights (rows = output channels), B = voxels (columns), 4 x NB
+//    accumulator blocks, so every voxel fragment feeds NB MFMAs and every
+//    weight fragment four.
+//  * The input is consumed in chunks of 16 channels (one MFMA k step). A
+//    chunk's 10x10x10 halo (zero outside the grid) sits in LDS at 48 bytes per
+//    voxel (32 bytes of data) and 640 bytes per 10-voxel row: with that
+//    padding the 16-byte fragment reads of every tap hit distinct banks. The
+//    next chunk's halo is fetched into the other of two buffers during the
+//    first taps of the current chunk.
+//  * The 27 taps of a chunk are unrolled, so every LDS fragment address is a
+//    per-lane base plus an immediate. Weights come pre-packed in fragment
+//    order (pv_pack_conv_weights_kernel): each fragment load is one coalesced
+//    1 KB buffer load, issued one tap ahead into registers. The only barrier
+//    is one per chunk.
+//  * The epilogue folds bias + batch norm into one scale/shift per channel,
+//    applies the activation and stores 4 consecutive channels per lane.
 //
 // fp32 path: one thread per (voxel, output channel), plain FMA loop.
 #include "pv_common.h"
 
 namespace {
 
-constexpr int kBU = 4, kBV = 8, kBW = 8;     // output brick (u, v, w)
-constexpr int kHU = kBU + 2, kHV = kBV + 2, kHW = kBW + 2;
-constexpr int kHaloVox = kHU * kHV * kHW;    // 600
-constexpr int kKC = 32;                      // input channels per K chunk
-constexpr int kRow = kKC + 8;                // LDS row pitch in bf16 (80 B: conflict-free b128 reads)
+constexpr int kBrick = 8;                          // output brick edge (u, v, w)
+constexpr int kHalo = kBrick + 2;                  // halo edge
+constexpr int kHaloVox = kHalo * kHalo * kHalo;    // 1000
+constexpr int kKC = 16;                            // input channels per chunk
+constexpr int kVoxPitch = 48;                      // LDS bytes per halo voxel
+constexpr int kRowPitch = 640;                     // LDS bytes per 10-voxel row
+constexpr int kHaloBytes = kHalo * kHalo * kRowPitch;  // 64000 per buffer
 constexpr int kThreads = 256;
+constexpr int kPieces = kHaloVox * 2;              // 16-byte pieces per chunk halo
+constexpr int kSets = (kPieces + kThreads - 1) / kThreads;  // 8 pieces per thread
+constexpr int kTaps = 27;
+constexpr int kOOB = 0x40000000;                   // byte offset always out of range
 
 __device__ __forceinline__ uint4 pack8(const uint16_t* e) {
     return make_uint4((uint32_t)e[0] | ((uint32_t)e[1] << 16), (uint32_t)e[2] | ((uint32_t)e[3] << 16),
                       (uint32_t)e[4] | ((uint32_t)e[5] << 16), (uint32_t)e[6] | ((uint32_t)e[7] << 16));
 }
 
-template <int NT, bool VEC>
-__global__ __launch_bounds__(kThreads, 2) void pv_conv3d_bf16_kernel(
-    const uint16_t* __restrict__ x, const uint16_t* __restrict__ w, PvBnFold bn, int act,
-    float slope, void* __restrict__ y, int out_bf16, int R, int Cin, int Cout, int nbu, int nbv,
-    int nbw) {
-    __shared__ __attribute__((aligned(16))) uint16_t halo[kHaloVox * kRow];
-    __shared__ __attribute__((aligned(16))) uint16_t wbuf[2][NT * kRow];
+__device__ __forceinline__ pv_bf16x8 as_frag(uint4 v) {
+    pv_bf16x8 r;
+    __builtin_memcpy(&r, &v, 16);
+    return r;
+}
+
+// Raw buffer loads: an offset at or past the resource's size reads as zero,
+// which provides the conv's zero padding (and zero channels past C_in)
+// without branches or selects on the loaded value.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
+                                             0x00020000);
+}
+
+__device__ __forceinline__ uint4 bload16(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+    const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+    uint4 u;
+    __builtin_memcpy(&u, &v, 16);
+    return u;
+}
+
+// 8 bf16 channels one by one: channel i at voff + 2i if i < valid, else zero.
+__device__ __forceinline__ uint4 bload8_elems(__amdgpu_buffer_rsrc_t r, int voff, int soff,
+                                              int valid) {
+    uint16_t e[8];
+#pragma unroll
+    for (int i = 0; i < 8; i++)
+        e[i] = __builtin_amdgcn_raw_buffer_load_b16(r, i < valid ? voff + 2 * i : kOOB, soff, 0);
+    return pack8(e);
+}
+
+template <int NB, bool VEC>
+__global__ __launch_bounds__(kThreads, 1) void pv_conv3d_bf16_kernel(
+    const uint16_t* __restrict__ x, const uint16_t* __restrict__ wpk, PvBnFold bn, int act,
+    float slope, void* __restrict__ y, int out_bf16, int vec_out, int R, int Cin, int Cout,
+    int nbr, int nblocks) {
+    __shared__ __attribute__((aligned(16))) char lds[2 * kHaloBytes];
+    __shared__ float bn_tab[2][NB * 32];  // folded scale and shift per output channel
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    // Blocks are dispatched round-robin over the 8 XCDs; give each XCD a
+    // contiguous range of bricks so that neighbouring halos share its L2.
     int bid = blockIdx.x;
-    const int nblk_n = Cout / NT;
-    const int nt = bid % nblk_n;
-    bid /= nblk_n;
-    const int bw = bid % nbw;
-    bid /= nbw;
-    const int bv = bid % nbv;
-    bid /= nbv;
-    const int bu = bid % nbu;
-    const int b = bid / nbu;
-    const int u0 = bu * kBU, v0 = bv * kBV, w0 = bw * kBW, n0 = nt * NT;
+    if ((nblocks & 7) == 0) bid = (bid & 7) * (nblocks >> 3) + (bid >> 3);
+    constexpr int NT = NB * 32;
+    const int ntiles = Cout / NT;
+    const int nt = bid % ntiles;
+    bid /= ntiles;
+    const int bw = bid % nbr;
+    bid /= nbr;
+    const int bv = bid % nbr;
+    bid /= nbr;
+    const int bu = bid % nbr;
+    const int b = bid / nbr;
+    const int u0 = bu * kBrick, v0 = bv * kBrick, w0 = bw * kBrick, n0 = nt * NT;
     const size_t cloud = (size_t)b * R * R * R;
+    const int nch = (Cin + kKC - 1) / kKC;
 
-    constexpr int NB = NT / 32;
-    pv_f32x16 acc[2][NB];
-    for (int i = 0; i < 2; i++)
+    const int r32 = lane & 31, khalf = lane >> 5;
+    // LDS byte address of this lane's B fragment (voxel column r32 of block
+    // mb, channels khalf*8 .. +7) at tap offset (0,0,0) in buffer 0: block mb
+    // covers u = 2*wave + mb/2 and v rows (mb&1)*4 .. +3, eight w each.
+    int bbase[4];
+#pragma unroll
+    for (int mb = 0; mb < 4; mb++) {
+        const int ul = 2 * wave + (mb >> 1), vl = (mb & 1) * 4 + (r32 >> 3), wl = r32 & 7;
+        bbase[mb] = (ul * kHalo + vl) * kRowPitch + wl * kVoxPitch + khalf * 16;
+    }
+
+    // Halo pieces of this thread: piece p = set*256 + tid is voxel p/2 (as
+    // (hu,hv,hw) of the 10x10x10 halo), channels (p%2)*8 .. +7 of the chunk.
+    // Threads past the last piece repeat voxel 999 (same value, same slot).
+    // goff: byte offset into the input resource (kOOB outside the grid);
+    // loff: LDS byte offset in buffer 0.
+    const int ulo = max(u0 - 1, 0), uhi = min(u0 + kBrick + 1, R);
+    const size_t slab = (size_t)R * R * Cin;  // elements per u-slab
+    const __amdgpu_buffer_rsrc_t xr =
+        make_rsrc(x + cloud * Cin + ulo * slab, (uint32_t)((uhi - ulo) * slab * 2));
+    const int pq = tid & 1;
+    int goff[kSets], loff[kSets];
+#pragma unroll
+    for (int set = 0; set < kSets; set++) {
+        const int h = min(set * (kThreads / 2) + (tid >> 1), kHaloVox - 1);
+        const int hu = h / (kHalo * kHalo), hv = (h / kHalo) % kHalo, hw = h % kHalo;
+        const int gu = u0 + hu - 1, gv = v0 + hv - 1, gw = w0 + hw - 1;
+        const bool in = gu >= 0 && gu < R && gv >= 0 && gv < R && gw >= 0 && gw < R;
+        goff[set] = in ? ((((gu - ulo) * R + gv) * R + gw) * Cin + pq * 8) * 2 : kOOB;
+        loff[set] = (hu * kHalo + hv) * kRowPitch + hw * kVoxPitch + pq * 16;
+    }
+    // Piece of set `set` for the chunk starting at channel cc: pieces whose
+    // channels lie past Cin read as zero.
+    auto halo_load = [&](int set, int cc) -> uint4 {
+        if (VEC) return bload16(xr, cc + pq * 8 < Cin ? goff[set] : kOOB, cc * 2);
+        return bload8_elems(xr, goff[set], cc * 2, Cin - cc - pq * 8);
+    };
+
+    // Packed weights: for chunk c, tap t and 32-channel output group g the 64
+    // lanes' fragments are 1 KB at ((c*27 + t)*G + g)*1024.
+    const int G = Cout / 32;
+    const __amdgpu_buffer_rsrc_t wr = make_rsrc(wpk, (uint32_t)((size_t)nch * kTaps * G * 1024));
+    const int wlane = lane * 16;
+    auto load_w = [&](int c, int tap, pv_bf16x8 (&wf)[NB]) {
+        const int cc = c < nch ? c : nch - 1;  // past the end: reload, never used
+#pragma unroll
+        for (int nb = 0; nb < NB; nb++)
+            wf[nb] = as_frag(bload16(wr, wlane, ((cc * kTaps + tap) * G + nt * NB + nb) * 1024));
+    };
+
+    pv_f32x16 acc[4][NB];
+#pragma unroll
+    for (int i = 0; i < 4; i++)
+#pragma unroll
         for (int j = 0; j < NB; j++)
+#pragma unroll
             for (int e = 0; e < 16; e++) acc[i][j][e] = 0.f;
 
-    // Weight slice (tap, cc) -> registers: NT rows x 32 channels = NT*4 chunks
-    // of 16 B; each thread owns NT*4/256 chunks.
-    constexpr int WCHUNKS = NT * 4;
-    constexpr int WCH = (WCHUNKS + kThreads - 1) / kThreads;
-    uint4 wreg[WCH];
-    auto load_w = [&](int tap, int cc) {
-        for (int i = 0; i < WCH; i++) {
-            const int ch = tid + i * kThreads;
-            if (ch >= WCHUNKS) break;
-            const int n = ch >> 2, q = ch & 3;
-            const int c = cc + q * 8;
-            const uint16_t* src = w + ((size_t)(n0 + n) * 27 + tap) * Cin + c;
-            uint4 v = make_uint4(0, 0, 0, 0);
-            if (VEC) {
-                if (c < Cin) v = *(const uint4*)src;
-            } else {
-                uint16_t e[8];
-                for (int t = 0; t < 8; t++) e[t] = (c + t < Cin) ? src[t] : (uint16_t)0;
-                v = pack8(e);
-            }
-            wreg[i] = v;
-        }
-    };
-    auto store_w = [&](int buf) {
-        for (int i = 0; i < WCH; i++) {
-            const int ch = tid + i * kThreads;
-            if (ch >= WCHUNKS) break;
-            const int n = ch >> 2, q = ch & 3;
-            *(uint4*)&wbuf[buf][n * kRow + q * 8] = wreg[i];
-        }
-    };
+    if (tid < NT) {
+        float sc, sh;
+        pv_bn_coeffs(bn, n0 + tid, sc, sh);
+        bn_tab[0][tid] = sc;
+        bn_tab[1][tid] = sh;
+    }
+    // Chunk 0's halo, the weights of taps 0 and 1.
+#pragma unroll
+    for (int set = 0; set < kSets; set++) *(uint4*)(lds + loff[set]) = halo_load(set, 0);
+    pv_bf16x8 wf[3][NB];
+    load_w(0, 0, wf[0]);
+    load_w(0, 1, wf[1]);
+    __syncthreads();
 
-    // A-fragment row of this lane: voxel (lv, lw) inside the wave's u-slice.
-    const int r32 = lane & 31, khalf = (lane >> 5) * 8;
-
-    for (int cc = 0; cc < Cin; cc += kKC) {
-        __syncthreads();  // previous chunk's readers are done with halo / wbuf
-        for (int idx = tid; idx < kHaloVox * 4; idx += kThreads) {
-            const int hv = idx >> 2, q = idx & 3;
-            const int hu = hv / (kHV * kHW), rem = hv - hu * (kHV * kHW);
-            const int hvv = rem / kHW, hw = rem - hvv * kHW;
-            const int gu = u0 + hu - 1, gv = v0 + hvv - 1, gw = w0 + hw - 1;
-            const int c = cc + q * 8;
-            uint4 v = make_uint4(0, 0, 0, 0);
-            if (gu >= 0 && gu < R && gv >= 0 && gv < R && gw >= 0 && gw < R && c < Cin) {
-                const uint16_t* src = x + (cloud + ((size_t)gu * R + gv) * R + gw) * Cin + c;
-                if (VEC) {
-                    v = *(const uint4*)src;
-                } else {
-                    uint16_t e[8];
-                    for (int t = 0; t < 8; t++) e[t] = (c + t < Cin) ? src[t] : (uint16_t)0;
-                    v = pack8(e);
-                }
+    // Chunk c sits in LDS buffer c%2: 27 taps, unrolled. Tap t computes with
+    // weight set t%3 (27 = 9 x 3, so the ring realigns at every chunk) while
+    // tap t+2's weights load into set (t+2)%3, and with B fragments bf[t%2]
+    // while tap t+1's are read from LDS into the other set. Piece set s of the
+    // next chunk's halo is loaded at tap s into hr[s%4] and stored to the
+    // other LDS buffer at tap s+4. One loop body for every chunk keeps the
+    // accumulators in the same registers throughout.
+    constexpr int kHaloLag = 4;
+    for (int c = 0; c < nch; c++) {
+        const int cur_off = (c & 1) * kHaloBytes, nxt_off = kHaloBytes - cur_off;
+        int rb[4];
+#pragma unroll
+        for (int mb = 0; mb < 4; mb++) rb[mb] = bbase[mb] + cur_off;
+        const int cn = (c + 1 < nch ? c + 1 : c) * kKC;  // last chunk reloads itself
+        pv_bf16x8 bf[2][4];
+        uint4 hr[kHaloLag];
+#pragma unroll
+        for (int mb = 0; mb < 4; mb++) bf[0][mb] = *(const pv_bf16x8*)(lds + rb[mb]);
+#pragma unroll
+        for (int t = 0; t < kTaps; t++) {
+            const int cur = t & 1, nxt = cur ^ 1;
+            if (t + 2 < kTaps)
+                load_w(c, t + 2, wf[(t + 2) % 3]);
+            else
+                load_w(c + 1, t + 2 - kTaps, wf[(t + 2) % 3]);
+            if (t >= kHaloLag && t < kSets + kHaloLag)
+                *(uint4*)(lds + loff[t - kHaloLag] + nxt_off) = hr[(t - kHaloLag) % kHaloLag];
+            if (t < kSets) hr[t % kHaloLag] = halo_load(t, cn);
+            if (t + 1 < kTaps) {
+                const int tn = t + 1;
+                const int toff = (tn / 9) * kHalo * kRowPitch + ((tn / 3) % 3) * kRowPitch +
+                                 (tn % 3) * kVoxPitch;
+#pragma unroll
+                for (int mb = 0; mb < 4; mb++)
+                    bf[nxt][mb] = *(const pv_bf16x8*)(lds + rb[mb] + toff);
             }
-            *(uint4*)&halo[hv * kRow + q * 8] = v;
-        }
-        load_w(0, cc);
-        store_w(0);
-        __syncthreads();
-        const int ksteps = (Cin - cc) >= kKC ? 2 : ((Cin - cc) + 15) / 16;
-        for (int tap = 0; tap < 27; ++tap) {
-            if (tap + 1 < 27) load_w(tap + 1, cc);
-            const int du = tap / 9, dv = (tap / 3) % 3, dw = tap % 3;  // offset + 1
-            const uint16_t* wb = wbuf[tap & 1];
-            for (int ks = 0; ks < ksteps; ++ks) {
-                pv_bf16x8 a[2], bb[NB];
-                for (int mb = 0; mb < 2; mb++) {
-                    const int lv = mb * 4 + (r32 >> 3), lw = r32 & 7;
-                    const int h = ((wave + du) * kHV + (lv + dv)) * kHW + (lw + dw);
-                    a[mb] = *(const pv_bf16x8*)&halo[h * kRow + ks * 16 + khalf];
-                }
+#pragma unroll
+            for (int mb = 0; mb < 4; mb++)
+#pragma unroll
                 for (int nb = 0; nb < NB; nb++)
-                    bb[nb] = *(const pv_bf16x8*)&wb[(nb * 32 + r32) * kRow + ks * 16 + khalf];
-                for (int mb = 0; mb < 2; mb++)
-                    for (int nb = 0; nb < NB; nb++)
-                        acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[mb], bb[nb],
-                                                                             acc[mb][nb], 0, 0, 0);
-            }
-            if (tap + 1 < 27) store_w((tap + 1) & 1);
-            __syncthreads();
+                    acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                        wf[t % 3][nb], bf[cur][mb], acc[mb][nb], 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
         }
+        __syncthreads();  // chunk done: next halo complete, this buffer free
     }
 
-    // Epilogue. Lane holds column n = r32 of each 32x32 block and rows
-    // 8*(e/4) + 4*(lane/32) + e%4 for e = 0..15.
-    const int u = u0 + wave;
+    // Epilogue. Block (mb, nb) holds D[n][voxel]: lane has voxel column r32
+    // of the block and output channels 8*j + 4*khalf + i (e = 4*j + i), i.e.
+    // four consecutive channels per j, stored as one 8- or 16-byte vector
+    // when the output is aligned for it.
+#pragma clang loop unroll(full)
     for (int nb = 0; nb < NB; nb++) {
-        const int n = n0 + nb * 32 + r32;
-        float scale, shift;
-        pv_bn_coeffs(bn, n, scale, shift);
-        for (int mb = 0; mb < 2; mb++) {
-            for (int e = 0; e < 16; e++) {
-                const int row = 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-                const int v = v0 + mb * 4 + (row >> 3), ww = w0 + (row & 7);
+#pragma clang loop unroll(full)
+        for (int j = 0; j < 4; j++) {
+            const int nl = nb * 32 + 8 * j + 4 * khalf;  // channel within the tile
+            const float4 sc = *(const float4*)&bn_tab[0][nl];
+            const float4 sh = *(const float4*)&bn_tab[1][nl];
+            const size_t n = (size_t)n0 + nl;
+#pragma clang loop unroll(full)
+            for (int mb = 0; mb < 4; mb++) {
+                const int u = u0 + 2 * wave + (mb >> 1);
+                const int v = v0 + (mb & 1) * 4 + (r32 >> 3), ww = w0 + (r32 & 7);
                 if (u >= R || v >= R || ww >= R) continue;
-                const float val = pv_activate(acc[mb][nb][e] * scale + shift, act, slope);
                 const size_t o = (cloud + ((size_t)u * R + v) * R + ww) * Cout + n;
-                if (out_bf16)
-                    ((uint16_t*)y)[o] = pv_f32_to_bf16(val);
-                else
-                    ((float*)y)[o] = val;
+                float r[4];
+                r[0] = pv_activate(acc[mb][nb][4 * j + 0] * sc.x + sh.x, act, slope);
+                r[1] = pv_activate(acc[mb][nb][4 * j + 1] * sc.y + sh.y, act, slope);
+                r[2] = pv_activate(acc[mb][nb][4 * j + 2] * sc.z + sh.z, act, slope);
+                r[3] = pv_activate(acc[mb][nb][4 * j + 3] * sc.w + sh.w, act, slope);
+                if (out_bf16) {
+                    uint16_t* d = (uint16_t*)y + o;
+                    if (vec_out) {
+                        *(uint2*)d = make_uint2(pv_pack_bf16x2(r[0], r[1]), pv_pack_bf16x2(r[2], r[3]));
+                    } else {
+#pragma clang loop unroll(full)
+                        for (int i = 0; i < 4; i++) d[i] = pv_f32_to_bf16(r[i]);
+                    }
+                } else {
+                    float* d = (float*)y + o;
+                    if (vec_out) {
+                        *(float4*)d = make_float4(r[0], r[1], r[2], r[3]);
+                    } else {
+#pragma clang loop unroll(full)
+                        for (int i = 0; i < 4; i++) d[i] = r[i];
+                    }
+                }
             }
         }
     }
+}
+
+// Repack bf16 weights [Cout][27][Cin] into the fragment order the MFMA conv
+// reads: 16-byte element ((c*27 + t)*G + g)*64 + lane holds the 8 channels
+// k = c*16 + (lane/32)*8 .. +7 of output channel g*32 + lane%32 at tap t
+// (zero past Cin), G = Cout/32. One thread per element.
+__global__ __launch_bounds__(256) void pv_pack_conv_weights_kernel(const uint16_t* __restrict__ w,
+                                                                   uint4* __restrict__ packed,
+                                                                   int Cin, int Cout, int total) {
+    const int i = blockIdx.x * 256 + threadIdx.x;
+    if (i >= total) return;
+    const int G = Cout / 32;
+    const int lane = i & 63;
+    int r = i >> 6;
+    const int g = r % G;
+    r /= G;
+    const int t = r % kTaps;
+    const int c = r / kTaps;
+    const int n = g * 32 + (lane & 31);
+    const int k = c * kKC + (lane >> 5) * 8;
+    const uint16_t* src = w + ((size_t)n * kTaps + t) * Cin;
+    uint16_t e[8];
+#pragma unroll
+    for (int j = 0; j < 8; j++) e[j] = k + j < Cin ? src[k + j] : (uint16_t)0;
+    packed[i] = pack8(e);
 }
 
 __global__ __launch_bounds__(256) void pv_conv3d_f32_kernel(const float* __restrict__ x,
@@ -194,36 +324,47 @@ __global__ __launch_bounds__(256) void pv_conv3d_f32_kernel(const float* __restr
         ((float*)y)[i] = val;
 }
 
-template <int NT>
+template <int NB>
 void launch_bf16(const void* x, int B, int R, int Cin, int Cout, const void* w,
                  const PvBnFold& bn, int act, float slope, void* y, bool out_bf16, bool vec,
                  hipStream_t s) {
-    const int nbu = (R + kBU - 1) / kBU, nbv = (R + kBV - 1) / kBV, nbw = (R + kBW - 1) / kBW;
-    const size_t blocks = (size_t)B * nbu * nbv * nbw * (Cout / NT);
+    const int nbr = (R + kBrick - 1) / kBrick;
+    const size_t blocks = (size_t)B * nbr * nbr * nbr * (Cout / (NB * 32));
+    const bool vec_out = pv_aligned16(y);
     if (vec)
-        hipLaunchKernelGGL((pv_conv3d_bf16_kernel<NT, true>), dim3((unsigned)blocks),
+        hipLaunchKernelGGL((pv_conv3d_bf16_kernel<NB, true>), dim3((unsigned)blocks),
                            dim3(kThreads), 0, s, (const uint16_t*)x, (const uint16_t*)w, bn, act,
-                           slope, y, (int)out_bf16, R, Cin, Cout, nbu, nbv, nbw);
+                           slope, y, (int)out_bf16, (int)vec_out, R, Cin, Cout, nbr, (int)blocks);
     else
-        hipLaunchKernelGGL((pv_conv3d_bf16_kernel<NT, false>), dim3((unsigned)blocks),
+        hipLaunchKernelGGL((pv_conv3d_bf16_kernel<NB, false>), dim3((unsigned)blocks),
                            dim3(kThreads), 0, s, (const uint16_t*)x, (const uint16_t*)w, bn, act,
-                           slope, y, (int)out_bf16, R, Cin, Cout, nbu, nbv, nbw);
+                           slope, y, (int)out_bf16, (int)vec_out, R, Cin, Cout, nbr, (int)blocks);
 }
 
 }  // namespace
 
+size_t pv_conv3d_ws_bytes(int Cin, int Cout, bool bf16) {
+    if (!bf16) return 0;
+    const size_t nch = (size_t)(Cin + kKC - 1) / kKC;
+    return nch * kKC * kTaps * (size_t)Cout * 2;
+}
+
 pvconv_status pv_launch_conv3d(const void* x, int B, int R, int Cin, int Cout, const void* w,
                                const PvBnFold& bn, int act, float slope, bool bf16, void* y,
-                               bool out_bf16, hipStream_t s) {
+                               bool out_bf16, void* ws, hipStream_t s) {
     if (B == 0) return PVCONV_OK;
     if (bf16) {
-        const bool vec = (Cin % 8 == 0) && pv_aligned16(x) && pv_aligned16(w);
+        const int total = (int)(pv_conv3d_ws_bytes(Cin, Cout, true) / 16);
+        hipLaunchKernelGGL(pv_pack_conv_weights_kernel, dim3((total + 255) / 256), dim3(256), 0,
+                           s, (const uint16_t*)w, (uint4*)ws, Cin, Cout, total);
+        w = ws;
+        const bool vec = (Cin % 8 == 0) && pv_aligned16(x);
         if (Cout % 128 == 0)
-            launch_bf16<128>(x, B, R, Cin, Cout, w, bn, act, slope, y, out_bf16, vec, s);
+            launch_bf16<4>(x, B, R, Cin, Cout, w, bn, act, slope, y, out_bf16, vec, s);
         else if (Cout % 64 == 0)
-            launch_bf16<64>(x, B, R, Cin, Cout, w, bn, act, slope, y, out_bf16, vec, s);
+            launch_bf16<2>(x, B, R, Cin, Cout, w, bn, act, slope, y, out_bf16, vec, s);
         else
-            launch_bf16<32>(x, B, R, Cin, Cout, w, bn, act, slope, y, out_bf16, vec, s);
+            launch_bf16<1>(x, B, R, Cin, Cout, w, bn, act, slope, y, out_bf16, vec, s);
     } else {
         const size_t total = (size_t)B * R * R * R * Cout;
         hipLaunchKernelGGL(pv_conv3d_f32_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256),

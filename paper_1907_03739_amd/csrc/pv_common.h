@@ -78,9 +78,10 @@ pvconv_status pv_launch_voxelize(const float* coords, const void* feats, bool fe
                                  int feat_ld, int B, int N, int C, int R, void* grid,
                                  bool grid_bf16, int32_t* counts, int32_t* vox_id,
                                  float* norm_coords, void* ws, hipStream_t s);
+size_t pv_conv3d_ws_bytes(int Cin, int Cout, bool bf16);
 pvconv_status pv_launch_conv3d(const void* x, int B, int R, int Cin, int Cout, const void* w,
                                const PvBnFold& bn, int act, float slope, bool bf16, void* y,
-                               bool out_bf16, hipStream_t s);
+                               bool out_bf16, void* ws, hipStream_t s);
 pvconv_status pv_launch_devoxelize(const void* grid, int B, int R, int C, bool grid_bf16,
                                    const float* pn, int N, float* out, hipStream_t s);
 pvconv_status pv_launch_point_mlp(const void* x, bool x_bf16, int x_ld, int M, int Cin,

@@ -29,7 +29,7 @@ def declared_functions():
 
 def test_library_exports_every_declared_symbol():
     names = declared_functions()
-    assert len(names) == 9
+    assert len(names) == 10
     out = subprocess.run(["nm", "-D", "--defined-only", b.LIB_PATH], capture_output=True,
                          text=True, check=True).stdout
     exported = set(re.findall(r"\bT (pvconv_\w+)", out))
@@ -41,6 +41,14 @@ def test_status_strings():
     for s in range(5):
         assert L.pvconv_status_string(s)
     assert L.pvconv_status_string(99) == b"unknown status"
+
+
+def test_conv_workspace_query():
+    # bf16: the packed weights, channels padded to 16; fp32 needs none
+    assert L.pvconv_conv3d_workspace_size(128, 128, 1) == 128 * 27 * 128 * 2
+    assert L.pvconv_conv3d_workspace_size(3, 64, 1) == 64 * 27 * 16 * 2
+    assert L.pvconv_conv3d_workspace_size(16, 32, 0) == 0
+    assert L.pvconv_conv3d_workspace_size(0, 32, 1) == 0
 
 
 def test_workspace_queries():
@@ -80,10 +88,12 @@ def test_voxelize_rejects(kw, status):
 
 def _conv(**kw):
     a = dict(x=FAKE, B=1, R=8, Cin=16, Cout=64, w=FAKE, bias=None, bn=None, act=2, slope=0.1,
-             dt=1, y=ctypes.c_void_p(0x200000), out_dt=1, s=None)
+             dt=1, y=ctypes.c_void_p(0x200000), out_dt=1, ws=ctypes.c_void_p(0x400000),
+             wsb=1 << 30, s=None)
     a.update(kw)
     return L.pvconv_conv3d(a["x"], a["B"], a["R"], a["Cin"], a["Cout"], a["w"], a["bias"],
-                           a["bn"], a["act"], a["slope"], a["dt"], a["y"], a["out_dt"], a["s"])
+                           a["bn"], a["act"], a["slope"], a["dt"], a["y"], a["out_dt"], a["ws"],
+                           a["wsb"], a["s"])
 
 
 @pytest.mark.parametrize("kw,status", [
@@ -91,6 +101,7 @@ def _conv(**kw):
     (dict(Cout=2000), EINVAL), (dict(act=5), EINVAL), (dict(dt=3), EINVAL), (dict(x=None), EINVAL),
     (dict(w=None), EINVAL), (dict(y=None), EINVAL), (dict(x=FAKE_ODD), EINVAL),
     (dict(y=FAKE), EINVAL), (dict(Cout=48), ENOTSUP), (dict(B=0), OK),
+    (dict(ws=None), EWS), (dict(wsb=100), EWS), (dict(ws=ctypes.c_void_p(0x400010)), EWS),
 ])
 def test_conv3d_rejects(kw, status):
     assert _conv(**kw) == status
