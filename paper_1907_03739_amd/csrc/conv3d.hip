@@ -41,6 +41,12 @@ constexpr int kPieces = kHaloVox * 2;              // 16-byte pieces per chunk h
 constexpr int kSets = (kPieces + kThreads - 1) / kThreads;  // 8 pieces per thread
 constexpr int kTaps = 27;
 constexpr int kOOB = 0x40000000;                   // byte offset always out of range
+// Epilogue staging: the output tile goes through LDS as [512 voxels][PW
+// channels] rows of up to 256 bytes, padded by 16 bytes, then out with
+// coalesced 16-byte stores.
+constexpr int kStageRow = 256 + 16;
+constexpr int kStageBytes = kBrick * kBrick * kBrick * kStageRow;  // 139264
+constexpr int kLdsBytes = kStageBytes > 2 * kHaloBytes ? kStageBytes : 2 * kHaloBytes;
 
 __device__ __forceinline__ uint4 pack8(const uint16_t* e) {
     return make_uint4((uint32_t)e[0] | ((uint32_t)e[1] << 16), (uint32_t)e[2] | ((uint32_t)e[3] << 16),
@@ -83,7 +89,7 @@ __global__ __launch_bounds__(kThreads, 1) void pv_conv3d_bf16_kernel(
     const uint16_t* __restrict__ x, const uint16_t* __restrict__ wpk, PvBnFold bn, int act,
     float slope, void* __restrict__ y, int out_bf16, int vec_out, int R, int Cin, int Cout,
     int nbr, int nblocks) {
-    __shared__ __attribute__((aligned(16))) char lds[2 * kHaloBytes];
+    __shared__ __attribute__((aligned(16))) char lds[kLdsBytes];
     __shared__ float bn_tab[2][NB * 32];  // folded scale and shift per output channel
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -225,47 +231,66 @@ __global__ __launch_bounds__(kThreads, 1) void pv_conv3d_bf16_kernel(
     }
 
     // Epilogue. Block (mb, nb) holds D[n][voxel]: lane has voxel column r32
-    // of the block and output channels 8*j + 4*khalf + i (e = 4*j + i), i.e.
-    // four consecutive channels per j, stored as one 8- or 16-byte vector
-    // when the output is aligned for it.
+    // of the block and output channels 8*j + 4*khalf + i (e = 4*j + i). The
+    // tile is staged in LDS in passes of PW channels (256 bytes per voxel),
+    // then each thread copies 16-byte pieces out, so every store instruction
+    // writes whole contiguous rows.
+    constexpr int PW_BF16 = NT < 128 ? NT : 128, PW_F32 = NT < 64 ? NT : 64;
+    const int esz = out_bf16 ? 2 : 4;
+    const int PW = out_bf16 ? PW_BF16 : PW_F32;
+    const int rowb = PW * esz;            // bytes of one voxel's pass row
+    const int pieces = rowb / 16;         // 16-byte pieces per voxel row
+    const size_t yrow = (size_t)Cout * esz;
+    for (int pass = 0; pass * PW < NT; pass++) {
 #pragma clang loop unroll(full)
-    for (int nb = 0; nb < NB; nb++) {
+        for (int nb = 0; nb < NB; nb++) {
 #pragma clang loop unroll(full)
-        for (int j = 0; j < 4; j++) {
-            const int nl = nb * 32 + 8 * j + 4 * khalf;  // channel within the tile
-            const float4 sc = *(const float4*)&bn_tab[0][nl];
-            const float4 sh = *(const float4*)&bn_tab[1][nl];
-            const size_t n = (size_t)n0 + nl;
+            for (int j = 0; j < 4; j++) {
+                const int nl = nb * 32 + 8 * j + 4 * khalf;  // channel within the tile
+                if (nl < pass * PW || nl >= (pass + 1) * PW) continue;
+                const float4 sc = *(const float4*)&bn_tab[0][nl];
+                const float4 sh = *(const float4*)&bn_tab[1][nl];
+                const int cb = (nl - pass * PW) * esz;       // byte offset in the row
 #pragma clang loop unroll(full)
-            for (int mb = 0; mb < 4; mb++) {
-                const int u = u0 + 2 * wave + (mb >> 1);
-                const int v = v0 + (mb & 1) * 4 + (r32 >> 3), ww = w0 + (r32 & 7);
-                if (u >= R || v >= R || ww >= R) continue;
-                const size_t o = (cloud + ((size_t)u * R + v) * R + ww) * Cout + n;
-                float r[4];
-                r[0] = pv_activate(acc[mb][nb][4 * j + 0] * sc.x + sh.x, act, slope);
-                r[1] = pv_activate(acc[mb][nb][4 * j + 1] * sc.y + sh.y, act, slope);
-                r[2] = pv_activate(acc[mb][nb][4 * j + 2] * sc.z + sh.z, act, slope);
-                r[3] = pv_activate(acc[mb][nb][4 * j + 3] * sc.w + sh.w, act, slope);
-                if (out_bf16) {
-                    uint16_t* d = (uint16_t*)y + o;
-                    if (vec_out) {
+                for (int mb = 0; mb < 4; mb++) {
+                    const int vox = (2 * wave + (mb >> 1)) * 64 + ((mb & 1) * 4 + (r32 >> 3)) * 8 +
+                                    (r32 & 7);
+                    float r[4];
+                    r[0] = pv_activate(acc[mb][nb][4 * j + 0] * sc.x + sh.x, act, slope);
+                    r[1] = pv_activate(acc[mb][nb][4 * j + 1] * sc.y + sh.y, act, slope);
+                    r[2] = pv_activate(acc[mb][nb][4 * j + 2] * sc.z + sh.z, act, slope);
+                    r[3] = pv_activate(acc[mb][nb][4 * j + 3] * sc.w + sh.w, act, slope);
+                    char* d = lds + vox * kStageRow + cb;
+                    if (out_bf16)
                         *(uint2*)d = make_uint2(pv_pack_bf16x2(r[0], r[1]), pv_pack_bf16x2(r[2], r[3]));
-                    } else {
-#pragma clang loop unroll(full)
-                        for (int i = 0; i < 4; i++) d[i] = pv_f32_to_bf16(r[i]);
-                    }
-                } else {
-                    float* d = (float*)y + o;
-                    if (vec_out) {
+                    else
                         *(float4*)d = make_float4(r[0], r[1], r[2], r[3]);
-                    } else {
-#pragma clang loop unroll(full)
-                        for (int i = 0; i < 4; i++) d[i] = r[i];
-                    }
+                }
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+        __syncthreads();
+        // copy out: piece k of voxel vox (k < pieces)
+        const size_t col = ((size_t)n0 + pass * PW) * esz;
+        for (int i = tid; i < 512 * pieces; i += kThreads) {
+            const int vox = i / pieces, k = i - vox * pieces;
+            const int u = u0 + (vox >> 6), v = v0 + ((vox >> 3) & 7), ww = w0 + (vox & 7);
+            if (u >= R || v >= R || ww >= R) continue;
+            const uint4 val = *(const uint4*)(lds + vox * kStageRow + k * 16);
+            char* dst = (char*)y + (cloud + ((size_t)u * R + v) * R + ww) * yrow + col + k * 16;
+            if (vec_out) {
+                *(uint4*)dst = val;
+            } else {
+                const uint32_t q[4] = {val.x, val.y, val.z, val.w};
+                for (int e = 0; e < 16 / esz; e++) {
+                    if (out_bf16)
+                        ((uint16_t*)dst)[e] = (uint16_t)(q[e >> 1] >> ((e & 1) * 16));
+                    else
+                        ((uint32_t*)dst)[e] = q[e];
                 }
             }
         }
+        __syncthreads();
     }
 }
 

@@ -10,19 +10,24 @@ typedef __attribute__((__vector_size__(8 * sizeof(short)))) short pv_bf16x8;
 typedef __attribute__((__vector_size__(16 * sizeof(float)))) float pv_f32x16;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float pv_f32x4;
 
-// bfloat16 <-> float on raw bits. Rounding is to nearest, ties to even; NaN
-// stays NaN.
+// bfloat16 <-> float on raw bits. float -> bf16 uses gfx950's conversion
+// instruction (round to nearest, ties to even; NaN stays NaN), no branches.
 __device__ __forceinline__ float pv_bf16_to_f32(uint16_t h) {
     return __uint_as_float(((uint32_t)h) << 16);
 }
 __device__ __forceinline__ uint16_t pv_f32_to_bf16(float f) {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return (uint16_t)(u >> 16);
+    const __bf16 h = (__bf16)f;
+    uint16_t u;
+    __builtin_memcpy(&u, &h, 2);
+    return u;
 }
 __device__ __forceinline__ uint32_t pv_pack_bf16x2(float lo, float hi) {
-    return (uint32_t)pv_f32_to_bf16(lo) | ((uint32_t)pv_f32_to_bf16(hi) << 16);
+    typedef float pv_f2 __attribute__((ext_vector_type(2)));
+    typedef __bf16 pv_b2 __attribute__((ext_vector_type(2)));
+    const pv_b2 v = __builtin_convertvector((pv_f2){lo, hi}, pv_b2);
+    uint32_t u;
+    __builtin_memcpy(&u, &v, 4);
+    return u;
 }
 
 // Folded inference batch norm for one channel: y = x * scale + shift.
@@ -47,10 +52,11 @@ __device__ __forceinline__ void pv_bn_coeffs(const PvBnFold& bn, int c, float& s
     }
 }
 
+// Activation as x >= 0 ? x : x * neg, with neg = 1 (none), 0 (ReLU) or the
+// leaky slope: one compare, one multiply, one select, no branches.
 __device__ __forceinline__ float pv_activate(float v, int act, float slope) {
-    if (act == PVCONV_ACT_RELU) return v > 0.f ? v : 0.f;
-    if (act == PVCONV_ACT_LEAKY) return v >= 0.f ? v : v * slope;
-    return v;
+    const float neg = act == PVCONV_ACT_LEAKY ? slope : (act == PVCONV_ACT_RELU ? 0.f : 1.f);
+    return v >= 0.f ? v : v * neg;
 }
 
 static inline PvBnFold pv_make_fold(const pvconv_bn* bn, const float* bias) {
