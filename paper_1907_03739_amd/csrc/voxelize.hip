@@ -3,26 +3,34 @@
 //
 // Data flow for one call (B clouds, N points, grid R^3, C channels):
 //   1. normalise: per-cloud centroid (int64 fixed point, order-free), largest
-//      centred norm, normalised coordinates and voxel ids.
-//   2. bucket: per cloud, an LDS histogram over (a partition of) the voxels,
-//      written out as `counts`, scanned, and used to scatter point indices
-//      into a list sorted by voxel; each 256-voxel tile records its slice.
-//   3. fill: one workgroup per 256-voxel tile writes the tile's whole slice
-//      of the dense grid once, coalesced: the mean of the voxel's features
-//      (fp64 sums) or zeros.
-// Small problems (R^3 <= 32768 and N <= 16384) fuse 1 and 2 into a single
-// workgroup per cloud; larger ones split normalisation over many workgroups
-// (four short launches that pass partial results through the workspace) and
-// bucket one 32768-voxel partition per workgroup.
+//      centred norm, then every point's normalised coordinates and voxel id.
+//      Clouds of up to 4096 points: one kernel, whose 256-point slices each
+//      recompute the cloud's parameters from registers. Larger clouds: four
+//      short kernels (abs-max, fixed-point sum, radius, points) that pass
+//      per-workgroup partial results through the workspace.
+//      The same launch zeroes the whole grid with streaming 16-byte stores
+//      (extra workgroups), so the empty voxels (most of the grid) cost one
+//      pure write stream.
+//   2. tile fill: one workgroup per (cloud, tile of TV voxels) collects the
+//      points that fall in its tile, counting-sorts them by voxel in LDS,
+//      writes the tile's counts and overwrites the rows of its occupied
+//      voxels with the mean of their features (fp64 sums). Voxels holding
+//      many points are summed by a whole wave with the points split across
+//      lanes, so a heavily collided cloud costs a few extra rounds of loads.
+// No global atomics; each occupied row is written twice (zero, then mean),
+// every other element once.
+#include <algorithm>
+
 #include "pv_common.h"
 
 namespace {
 
-constexpr int kPart = 32768;        // voxels per LDS histogram (128 KiB of int32)
-constexpr int kTile = 256;          // voxels per fill workgroup
-constexpr int kSmallMaxN = 16384;   // largest N for the fused per-cloud path
-constexpr int kNormPts = 2048;      // points per workgroup, split normalisation
+constexpr int kNormPts = 1024;      // points per workgroup, large-cloud normalisation
 constexpr int kNormThreads = 256;
+constexpr int kSmallMaxN = 4096;    // largest cloud normalised by one kernel
+constexpr int kTileThreads = 256;
+constexpr int kHeavy = 32;          // voxels with more points are summed by a whole wave
+constexpr int kMaxCap = 8192;       // tile points kept in LDS at once
 
 // ---------------------------------------------------------------------------
 // Normalisation arithmetic. IEEE fp64, round to nearest even, no contraction,
@@ -74,10 +82,19 @@ __device__ __forceinline__ int normalise_point(const float* p, const double* c, 
         double d = (double)p[a] - c[a];
         double unit = (M2 == 0.0) ? 0.0 : d / m;
         double x = unit * 0.5 + 0.5;
-        if (pn_out) pn_out[a] = (float)x;
+        pn_out[a] = (float)x;
         uvw[a] = voxel_axis(x, R);
     }
     return (uvw[0] * R + uvw[1]) * R + uvw[2];
+}
+
+__device__ __forceinline__ void write_point(int32_t* vox_id, float* norm_coords, size_t k, int id,
+                                            const float* pn) {
+    vox_id[k] = id;
+    float* o = norm_coords + k * 3;
+    o[0] = pn[0];
+    o[1] = pn[1];
+    o[2] = pn[2];
 }
 
 // ---------------------------------------------------------------------------
@@ -89,23 +106,31 @@ __device__ __forceinline__ T wave_reduce(T v, Op op) {
     return v;
 }
 
-template <int NT, typename T, typename Op>
-__device__ T block_reduce(T v, Op op, T* lds /* NT/64 entries */) {
-    v = wave_reduce(v, op);
-    const int w = threadIdx.x >> 6;
-    __syncthreads();
-    if ((threadIdx.x & 63) == 0) lds[w] = v;
-    __syncthreads();
-    T r = lds[0];
-    for (int i = 1; i < NT / 64; i++) r = op(r, lds[i]);
-    return r;
-}
-
 struct MaxF { __device__ float operator()(float a, float b) const { return fmaxf(a, b); } };
 struct MaxD { __device__ double operator()(double a, double b) const { return fmax(a, b); } };
 struct AddL {
     __device__ long long operator()(long long a, long long b) const { return a + b; }
 };
+
+// K values reduced together over an NT-thread workgroup; every thread gets
+// the results. lds holds K * NT/64 entries.
+template <int NT, int K, typename T, typename Op>
+__device__ void block_reduce_k(T (&v)[K], Op op, T* lds) {
+#pragma unroll
+    for (int i = 0; i < K; i++) v[i] = wave_reduce(v[i], op);
+    const int w = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0)
+#pragma unroll
+        for (int i = 0; i < K; i++) lds[i * (NT / 64) + w] = v[i];
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < K; i++) {
+        T r = lds[i * (NT / 64)];
+        for (int j = 1; j < NT / 64; j++) r = op(r, lds[i * (NT / 64) + j]);
+        v[i] = r;
+    }
+    __syncthreads();
+}
 
 // Exclusive scan of one int per thread over the workgroup; also returns the total.
 template <int NT>
@@ -126,114 +151,99 @@ __device__ int block_exclusive_scan(int v, int* lds /* NT/64 */, int& total) {
         if (i < w) before += s;
         total += s;
     }
+    __syncthreads();
     return before + incl - v;
 }
 
-// Per-cloud normalisation parameters, computed by one workgroup of NT threads
-// over all N points of the cloud.
-template <int NT>
-__device__ void cloud_params(const float* p, int N, double* c, double& M2, double& m,
-                             float* redf, long long* redl, double* redd) {
-    float A[3] = {0.f, 0.f, 0.f};
-    for (int k = threadIdx.x; k < N; k += NT)
-        for (int a = 0; a < 3; a++) A[a] = fmaxf(A[a], fabsf(p[3 * k + a]));
-    int S[3];
-    for (int a = 0; a < 3; a++) {
-        A[a] = block_reduce<NT>(A[a], MaxF(), redf);
-        S[a] = fixed_scale(A[a], N);
-    }
-    long long q[3] = {0, 0, 0};
-    for (int k = threadIdx.x; k < N; k += NT)
-        for (int a = 0; a < 3; a++)
-            if (A[a] > 0.f) q[a] += fixed_term(p[3 * k + a], S[a]);
-    for (int a = 0; a < 3; a++) {
-        q[a] = block_reduce<NT>(q[a], AddL(), redl);
-        c[a] = centroid_from_sum(q[a], S[a], A[a], N);
-    }
-    double mx = 0.0;
-    for (int k = threadIdx.x; k < N; k += NT) mx = fmax(mx, sq_dist(p + 3 * k, c));
-    M2 = block_reduce<NT>(mx, MaxD(), redd);
-    m = sqrt(M2);
+// ---------------------------------------------------------------------------
+// Normalisation, clouds of up to kSmallMaxN points: grid (slices, clouds) of
+// 256-thread workgroups. Every workgroup holds its cloud's points in
+// registers (PPT per thread), computes the normalisation parameters with
+// three workgroup reductions (the three axes reduced together) and writes
+// the voxel id and normalised coordinates of its own slice of 256 points.
+// The parameters are order-free, so all slices of a cloud agree bit for bit.
+// ---------------------------------------------------------------------------
+// Zero fill of the whole grid (16-byte stores, grid-stride over `zero_blocks`
+// workgroups). The tile kernel then writes the rows of occupied voxels.
+__device__ __forceinline__ void zero_fill_role(uint4* grid16, size_t n16, int zb, int zero_blocks) {
+    for (size_t i = (size_t)zb * 256 + threadIdx.x; i < n16; i += (size_t)zero_blocks * 256)
+        grid16[i] = make_uint4(0, 0, 0, 0);
 }
 
-// Histogram scan + tile ranges + scatter, shared by the two bucket kernels.
-// hist[0..nv) holds the counts of voxels [v_begin, v_begin + nv) on entry.
-template <int NT>
-__device__ void scan_and_ranges(int* hist, int nv, int v_begin, int* scan_lds, int2* tile_range,
-                                int tile_first) {
-    const int seg = (nv + NT - 1) / NT;
-    const int s0 = min(nv, (int)threadIdx.x * seg), s1 = min(nv, s0 + seg);
-    int local = 0;
-    for (int i = s0; i < s1; i++) local += hist[i];
-    int total;
-    int run = block_exclusive_scan<NT>(local, scan_lds, total);
-    for (int i = s0; i < s1; i++) {
-        int h = hist[i];
-        hist[i] = run;
-        run += h;
-    }
-    __syncthreads();
-    const int ntiles = (nv + kTile - 1) / kTile;
-    for (int t = threadIdx.x; t < ntiles; t += NT) {
-        int lo = hist[t * kTile];
-        int hi = (t + 1) * kTile < nv ? hist[(t + 1) * kTile] : total;
-        tile_range[tile_first + t] = make_int2(lo, hi);
-    }
-    __syncthreads();
-    (void)v_begin;
-}
-
-// ---------------------------------------------------------------------------
-// Fused path: one workgroup per cloud does normalisation and bucketing.
-// ---------------------------------------------------------------------------
-__global__ __launch_bounds__(1024) void pv_voxelize_bucket_small_kernel(
-    const float* __restrict__ coords, int N, int R, int32_t* __restrict__ vox_id,
-    float* __restrict__ norm_coords, int32_t* __restrict__ counts, int32_t* __restrict__ list,
-    int2* __restrict__ tile_range) {
-    constexpr int NT = 1024;
-    __shared__ int hist[kPart];
-    __shared__ float redf[NT / 64];
-    __shared__ long long redl[NT / 64];
+template <int PPT>
+__device__ void ids_role(const float* __restrict__ coords, int N, int R, int slice, int b,
+                         int32_t* __restrict__ vox_id, float* __restrict__ norm_coords) {
+    constexpr int NT = 256;
+    __shared__ float redf[3 * NT / 64];
+    __shared__ long long redl[3 * NT / 64];
     __shared__ double redd[NT / 64];
-    __shared__ int scan_lds[NT / 64];
-
-    const int b = blockIdx.x;
-    const int V = R * R * R;
-    const int tiles = (V + kTile - 1) / kTile;
     const float* p = coords + (size_t)b * N * 3;
-    for (int i = threadIdx.x; i < V; i += NT) hist[i] = 0;
-
-    double c[3], M2, m;
-    cloud_params<NT>(p, N, c, M2, m, redf, redl, redd);
-
-    int32_t* ids = vox_id + (size_t)b * N;
-    for (int k = threadIdx.x; k < N; k += NT) {
-        float pn[3];
-        int id = normalise_point(p + 3 * k, c, M2, m, R, pn);
-        if (norm_coords) {
-            float* o = norm_coords + ((size_t)b * N + k) * 3;
-            o[0] = pn[0];
-            o[1] = pn[1];
-            o[2] = pn[2];
-        }
-        ids[k] = id;
-        atomicAdd(&hist[id], 1);
+    float x[PPT][3];
+#pragma unroll
+    for (int i = 0; i < PPT; i++) {
+        const int k = threadIdx.x + i * NT;
+#pragma unroll
+        for (int a = 0; a < 3; a++) x[i][a] = k < N ? p[3 * k + a] : 0.f;
     }
-    __syncthreads();
-    int32_t* cnt = counts + (size_t)b * V;
-    for (int i = threadIdx.x; i < V; i += NT) cnt[i] = hist[i];
-    __syncthreads();
-    scan_and_ranges<NT>(hist, V, 0, scan_lds, tile_range, b * tiles);
-    int32_t* lst = list + (size_t)b * N;
-    for (int k = threadIdx.x; k < N; k += NT) {  // same points as above: own writes
-        int pos = atomicAdd(&hist[ids[k]], 1);
-        lst[pos] = k;
+    float A[3] = {0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < PPT; i++)
+#pragma unroll
+        for (int a = 0; a < 3; a++) A[a] = fmaxf(A[a], fabsf(x[i][a]));
+    block_reduce_k<NT>(A, MaxF(), redf);
+    int S[3];
+    long long q[3] = {0, 0, 0};
+#pragma unroll
+    for (int a = 0; a < 3; a++) {
+        S[a] = fixed_scale(A[a], N);
+#pragma unroll
+        for (int i = 0; i < PPT; i++)
+            if (A[a] > 0.f && threadIdx.x + i * NT < N) q[a] += fixed_term(x[i][a], S[a]);
+    }
+    block_reduce_k<NT>(q, AddL(), redl);
+    double c[3];
+#pragma unroll
+    for (int a = 0; a < 3; a++) c[a] = centroid_from_sum(q[a], S[a], A[a], N);
+    double mx[1] = {0.0};
+#pragma unroll
+    for (int i = 0; i < PPT; i++)
+        if (threadIdx.x + i * NT < N) mx[0] = fmax(mx[0], sq_dist(x[i], c));
+    block_reduce_k<NT>(mx, MaxD(), redd);
+    const double M2 = mx[0];
+    const double m = sqrt(M2);
+    // this workgroup's slice: points slice*256 + tid, i.e. register row `slice`
+#pragma unroll
+    for (int i = 0; i < PPT; i++) {
+        const int k = threadIdx.x + i * NT;
+        if (i != slice || k >= N) continue;
+        float pn[3];
+        const int id = normalise_point(x[i], c, M2, m, R, pn);
+        write_point(vox_id, norm_coords, (size_t)b * N + k, id, pn);
     }
 }
 
+// One launch, two roles: the first B * slices workgroups normalise (slice
+// blockIdx % slices of cloud blockIdx / slices), the rest zero the grid.
+template <int PPT>
+__global__ __launch_bounds__(256) void pv_voxel_ids_kernel(const float* __restrict__ coords,
+                                                           int N, int R, int slices, int nid,
+                                                           int32_t* __restrict__ vox_id,
+                                                           float* __restrict__ norm_coords,
+                                                           uint4* __restrict__ grid16, size_t n16) {
+    const int bid = blockIdx.x;
+    if (bid >= nid) {
+        zero_fill_role(grid16, n16, bid - nid, gridDim.x - nid);
+        return;
+    }
+    ids_role<PPT>(coords, N, R, bid % slices, bid / slices, vox_id, norm_coords);
+}
+
 // ---------------------------------------------------------------------------
-// Split path. Partial results per (cloud, workgroup g) pass between launches:
-//   pA [B][G][3] float, pQ [B][G][3] int64, pM [B][G] double.
+// Normalisation, larger clouds: four kernels over G = ceil(N / kNormPts)
+// workgroups per cloud, each step combining the previous step's G partials
+// (read in parallel, one per thread) before working on its own points.
+// Partials: pA [B][G][3] abs-max, pQ [B][G][3] fixed-point sums, pM [B][G]
+// largest squared distance.
 // ---------------------------------------------------------------------------
 struct SplitWs {
     float* pA;
@@ -242,47 +252,53 @@ struct SplitWs {
     int G;
 };
 
+__device__ void combine_absmax(const SplitWs& ws, int b, float* redf, float (&A)[3]) {
+    A[0] = A[1] = A[2] = 0.f;
+    for (int g = threadIdx.x; g < ws.G; g += kNormThreads)
+        for (int a = 0; a < 3; a++) A[a] = fmaxf(A[a], ws.pA[((size_t)b * ws.G + g) * 3 + a]);
+    block_reduce_k<kNormThreads>(A, MaxF(), redf);
+}
+
+__device__ void combine_centroid(const SplitWs& ws, int b, int N, float* redf, long long* redl,
+                                 double (&c)[3]) {
+    float A[3];
+    combine_absmax(ws, b, redf, A);
+    long long q[3] = {0, 0, 0};
+    for (int g = threadIdx.x; g < ws.G; g += kNormThreads)
+        for (int a = 0; a < 3; a++) q[a] += ws.pQ[((size_t)b * ws.G + g) * 3 + a];
+    block_reduce_k<kNormThreads>(q, AddL(), redl);
+    for (int a = 0; a < 3; a++) c[a] = centroid_from_sum(q[a], fixed_scale(A[a], N), A[a], N);
+}
+
+// Grid (G * B + zero workgroups): the first G * B compute abs-max partials,
+// the rest zero the grid.
 __global__ __launch_bounds__(kNormThreads) void pv_norm_absmax_kernel(const float* coords, int N,
-                                                                      SplitWs ws) {
-    __shared__ float redf[kNormThreads / 64];
-    const int g = blockIdx.x, b = blockIdx.y;
+                                                                      SplitWs ws, int B,
+                                                                      uint4* grid16, size_t n16) {
+    __shared__ float redf[3 * kNormThreads / 64];
+    const int nid = ws.G * B;
+    if ((int)blockIdx.x >= nid) {
+        zero_fill_role(grid16, n16, blockIdx.x - nid, gridDim.x - nid);
+        return;
+    }
+    const int g = blockIdx.x % ws.G, b = blockIdx.x / ws.G;
     const float* p = coords + (size_t)b * N * 3;
     const int k0 = g * kNormPts, k1 = min(N, k0 + kNormPts);
     float A[3] = {0.f, 0.f, 0.f};
     for (int k = k0 + threadIdx.x; k < k1; k += kNormThreads)
         for (int a = 0; a < 3; a++) A[a] = fmaxf(A[a], fabsf(p[3 * k + a]));
-    for (int a = 0; a < 3; a++) {
-        float r = block_reduce<kNormThreads>(A[a], MaxF(), redf);
-        if (threadIdx.x == 0) ws.pA[((size_t)b * ws.G + g) * 3 + a] = r;
-    }
-}
-
-// Reduce the G partials of cloud b (every workgroup does it; G is small).
-__device__ void split_absmax(const SplitWs& ws, int b, float* A) {
-    for (int a = 0; a < 3; a++) {
-        float r = 0.f;
-        for (int g = 0; g < ws.G; g++) r = fmaxf(r, ws.pA[((size_t)b * ws.G + g) * 3 + a]);
-        A[a] = r;
-    }
-}
-
-__device__ void split_centroid(const SplitWs& ws, int b, int N, double* c) {
-    float A[3];
-    split_absmax(ws, b, A);
-    for (int a = 0; a < 3; a++) {
-        long long q = 0;
-        for (int g = 0; g < ws.G; g++) q += ws.pQ[((size_t)b * ws.G + g) * 3 + a];
-        c[a] = centroid_from_sum(q, fixed_scale(A[a], N), A[a], N);
-    }
+    block_reduce_k<kNormThreads>(A, MaxF(), redf);
+    if (threadIdx.x < 3) ws.pA[((size_t)b * ws.G + g) * 3 + threadIdx.x] = A[threadIdx.x];
 }
 
 __global__ __launch_bounds__(kNormThreads) void pv_norm_sum_kernel(const float* coords, int N,
                                                                    SplitWs ws) {
-    __shared__ long long redl[kNormThreads / 64];
+    __shared__ float redf[3 * kNormThreads / 64];
+    __shared__ long long redl[3 * kNormThreads / 64];
     const int g = blockIdx.x, b = blockIdx.y;
     const float* p = coords + (size_t)b * N * 3;
     float A[3];
-    split_absmax(ws, b, A);
+    combine_absmax(ws, b, redf, A);
     int S[3];
     for (int a = 0; a < 3; a++) S[a] = fixed_scale(A[a], N);
     const int k0 = g * kNormPts, k1 = min(N, k0 + kNormPts);
@@ -290,100 +306,69 @@ __global__ __launch_bounds__(kNormThreads) void pv_norm_sum_kernel(const float* 
     for (int k = k0 + threadIdx.x; k < k1; k += kNormThreads)
         for (int a = 0; a < 3; a++)
             if (A[a] > 0.f) q[a] += fixed_term(p[3 * k + a], S[a]);
-    for (int a = 0; a < 3; a++) {
-        long long r = block_reduce<kNormThreads>(q[a], AddL(), redl);
-        if (threadIdx.x == 0) ws.pQ[((size_t)b * ws.G + g) * 3 + a] = r;
-    }
+    block_reduce_k<kNormThreads>(q, AddL(), redl);
+    if (threadIdx.x < 3) ws.pQ[((size_t)b * ws.G + g) * 3 + threadIdx.x] = q[threadIdx.x];
 }
 
 __global__ __launch_bounds__(kNormThreads) void pv_norm_radius_kernel(const float* coords, int N,
                                                                       SplitWs ws) {
+    __shared__ float redf[3 * kNormThreads / 64];
+    __shared__ long long redl[3 * kNormThreads / 64];
     __shared__ double redd[kNormThreads / 64];
     const int g = blockIdx.x, b = blockIdx.y;
     const float* p = coords + (size_t)b * N * 3;
     double c[3];
-    split_centroid(ws, b, N, c);
+    combine_centroid(ws, b, N, redf, redl, c);
     const int k0 = g * kNormPts, k1 = min(N, k0 + kNormPts);
-    double mx = 0.0;
-    for (int k = k0 + threadIdx.x; k < k1; k += kNormThreads) mx = fmax(mx, sq_dist(p + 3 * k, c));
-    double r = block_reduce<kNormThreads>(mx, MaxD(), redd);
-    if (threadIdx.x == 0) ws.pM[(size_t)b * ws.G + g] = r;
+    double mx[1] = {0.0};
+    for (int k = k0 + threadIdx.x; k < k1; k += kNormThreads)
+        mx[0] = fmax(mx[0], sq_dist(p + 3 * k, c));
+    block_reduce_k<kNormThreads>(mx, MaxD(), redd);
+    if (threadIdx.x == 0) ws.pM[(size_t)b * ws.G + g] = mx[0];
 }
 
 __global__ __launch_bounds__(kNormThreads) void pv_norm_points_kernel(
     const float* coords, int N, int R, SplitWs ws, int32_t* __restrict__ vox_id,
     float* __restrict__ norm_coords) {
+    __shared__ float redf[3 * kNormThreads / 64];
+    __shared__ long long redl[3 * kNormThreads / 64];
+    __shared__ double redd[kNormThreads / 64];
     const int g = blockIdx.x, b = blockIdx.y;
     const float* p = coords + (size_t)b * N * 3;
     double c[3];
-    split_centroid(ws, b, N, c);
-    double M2 = 0.0;
-    for (int i = 0; i < ws.G; i++) M2 = fmax(M2, ws.pM[(size_t)b * ws.G + i]);
+    combine_centroid(ws, b, N, redf, redl, c);
+    double mx[1] = {0.0};
+    for (int i = threadIdx.x; i < ws.G; i += kNormThreads)
+        mx[0] = fmax(mx[0], ws.pM[(size_t)b * ws.G + i]);
+    block_reduce_k<kNormThreads>(mx, MaxD(), redd);
+    const double M2 = mx[0];
     const double m = sqrt(M2);
     const int k0 = g * kNormPts, k1 = min(N, k0 + kNormPts);
     for (int k = k0 + threadIdx.x; k < k1; k += kNormThreads) {
         float pn[3];
-        int id = normalise_point(p + 3 * k, c, M2, m, R, pn);
-        if (norm_coords) {
-            float* o = norm_coords + ((size_t)b * N + k) * 3;
-            o[0] = pn[0];
-            o[1] = pn[1];
-            o[2] = pn[2];
-        }
-        vox_id[(size_t)b * N + k] = id;
-    }
-}
-
-// One workgroup per (partition p, cloud b): histogram of the points whose voxel
-// lies in [p*kPart, p*kPart + nv), counts out, scan, tile ranges, scatter into
-// the partition's own list region list[(b*P + p)*N ...].
-__global__ __launch_bounds__(1024) void pv_bucket_partition_kernel(
-    const int32_t* __restrict__ vox_id, int N, int R, int P, int32_t* __restrict__ counts,
-    int32_t* __restrict__ list, int2* __restrict__ tile_range) {
-    constexpr int NT = 1024;
-    __shared__ int hist[kPart];
-    __shared__ int scan_lds[NT / 64];
-    const int p = blockIdx.x, b = blockIdx.y;
-    const int V = R * R * R;
-    const int tiles = (V + kTile - 1) / kTile;
-    const int v0 = p * kPart, nv = min(kPart, V - v0);
-    for (int i = threadIdx.x; i < nv; i += NT) hist[i] = 0;
-    __syncthreads();
-    const int32_t* ids = vox_id + (size_t)b * N;
-    for (int k = threadIdx.x; k < N; k += NT) {
-        int r = ids[k] - v0;
-        if (r >= 0 && r < nv) atomicAdd(&hist[r], 1);
-    }
-    __syncthreads();
-    int32_t* cnt = counts + (size_t)b * V + v0;
-    for (int i = threadIdx.x; i < nv; i += NT) cnt[i] = hist[i];
-    __syncthreads();
-    scan_and_ranges<NT>(hist, nv, v0, scan_lds, tile_range, b * tiles + v0 / kTile);
-    int32_t* lst = list + ((size_t)b * P + p) * N;
-    for (int k = threadIdx.x; k < N; k += NT) {
-        int r = ids[k] - v0;
-        if (r >= 0 && r < nv) lst[atomicAdd(&hist[r], 1)] = k;
+        const int id = normalise_point(p + 3 * k, c, M2, m, R, pn);
+        write_point(vox_id, norm_coords, (size_t)b * N + k, id, pn);
     }
 }
 
 // ---------------------------------------------------------------------------
-// Fill: one workgroup per 256-voxel tile writes the tile's grid rows once.
+// Feature rows: 8 channels at a time (16 or 32 bytes) or one channel.
 // ---------------------------------------------------------------------------
 template <typename FT>
-__device__ __forceinline__ void load8(const FT* src, double* acc);
+__device__ __forceinline__ void load8f(const FT* src, float* v);
 template <>
-__device__ __forceinline__ void load8<float>(const float* src, double* acc) {
-    float4 a = *(const float4*)src, b = *(const float4*)(src + 4);
-    acc[0] += a.x; acc[1] += a.y; acc[2] += a.z; acc[3] += a.w;
-    acc[4] += b.x; acc[5] += b.y; acc[6] += b.z; acc[7] += b.w;
+__device__ __forceinline__ void load8f<float>(const float* src, float* v) {
+    const float4 a = *(const float4*)src, b = *(const float4*)(src + 4);
+    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+    v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
 }
 template <>
-__device__ __forceinline__ void load8<uint16_t>(const uint16_t* src, double* acc) {
-    uint4 a = *(const uint4*)src;
-    uint32_t w[4] = {a.x, a.y, a.z, a.w};
+__device__ __forceinline__ void load8f<uint16_t>(const uint16_t* src, float* v) {
+    const uint4 a = *(const uint4*)src;
+    const uint32_t w[4] = {a.x, a.y, a.z, a.w};
     for (int i = 0; i < 4; i++) {
-        acc[2 * i] += pv_bf16_to_f32((uint16_t)(w[i] & 0xffffu));
-        acc[2 * i + 1] += pv_bf16_to_f32((uint16_t)(w[i] >> 16));
+        v[2 * i] = pv_bf16_to_f32((uint16_t)(w[i] & 0xffffu));
+        v[2 * i + 1] = pv_bf16_to_f32((uint16_t)(w[i] >> 16));
     }
 }
 template <typename GT>
@@ -398,7 +383,6 @@ __device__ __forceinline__ void store8<uint16_t>(uint16_t* dst, const float* v) 
     *(uint4*)dst = make_uint4(pv_pack_bf16x2(v[0], v[1]), pv_pack_bf16x2(v[2], v[3]),
                               pv_pack_bf16x2(v[4], v[5]), pv_pack_bf16x2(v[6], v[7]));
 }
-
 template <typename FT>
 __device__ __forceinline__ float load1(const FT* p);
 template <>
@@ -412,110 +396,429 @@ __device__ __forceinline__ void store1<float>(float* p, float v) { *p = v; }
 template <>
 __device__ __forceinline__ void store1<uint16_t>(uint16_t* p, float v) { *p = pv_f32_to_bf16(v); }
 
-template <typename FT, typename GT, bool VEC>
-__global__ __launch_bounds__(256) void pv_voxel_fill_kernel(
-    const FT* __restrict__ feats, int feat_ld, int N, int C, int R, int P,
-    const int32_t* __restrict__ counts, const int32_t* __restrict__ list,
-    const int2* __restrict__ tile_range, GT* __restrict__ grid) {
-    constexpr int NT = 256;
-    __shared__ int cnt[kTile];
-    __shared__ int off[kTile];
-    __shared__ int scan_lds[NT / 64];
-    const int t = blockIdx.x, b = blockIdx.y;
-    const int V = R * R * R;
-    const int tiles = (V + kTile - 1) / kTile;
-    const int v0 = t * kTile, nv = min(kTile, V - v0);
-    const int2 rg = tile_range[(size_t)b * tiles + t];
-    GT* out = grid + ((size_t)b * V + v0) * C;
-
-    if (rg.x == rg.y) {  // no point in this tile: zeros only
-        if (VEC) {
-            const int chunks = nv * C * (int)sizeof(GT) / 16;
-            uint4* o = (uint4*)out;
-            for (int i = threadIdx.x; i < chunks; i += NT) o[i] = make_uint4(0, 0, 0, 0);
-        } else {
-            for (int i = threadIdx.x; i < nv * C; i += NT) out[i] = (GT)0;
-        }
-        return;
+// Sum of 8 channels over the points list[j0], list[j0 + step], ... (< j1) in
+// that order, fp64, with eight points' loads in flight at a time.
+template <typename FT>
+__device__ __forceinline__ void sum8(const FT* fb, int feat_ld, int col, const int* list, int j0,
+                                     int j1, int step, double* acc) {
+    constexpr int U = 8;
+    int j = j0;
+    for (; j + (U - 1) * step < j1; j += U * step) {
+        float f[U][8];
+#pragma unroll
+        for (int u = 0; u < U; u++) load8f<FT>(fb + (size_t)list[j + u * step] * feat_ld + col, f[u]);
+#pragma unroll
+        for (int u = 0; u < U; u++)
+#pragma unroll
+            for (int i = 0; i < 8; i++) acc[i] += (double)f[u][i];
     }
-    int n = threadIdx.x < nv ? counts[(size_t)b * V + v0 + threadIdx.x] : 0;
-    int total;
-    int ex = block_exclusive_scan<NT>(n, scan_lds, total);
-    cnt[threadIdx.x] = n;
-    off[threadIdx.x] = rg.x + ex;
-    __syncthreads();
+    for (; j < j1; j += step) {
+        float f[8];
+        load8f<FT>(fb + (size_t)list[j] * feat_ld + col, f);
+#pragma unroll
+        for (int i = 0; i < 8; i++) acc[i] += (double)f[i];
+    }
+}
 
-    const int p = v0 / kPart;
-    const int32_t* lst = list + ((size_t)b * P + p) * N;
-    const FT* fb = feats + (size_t)b * N * feat_ld;
+// ---------------------------------------------------------------------------
+// Tile fill: one workgroup per (tile t of TV voxels, cloud b).
+//
+// Dynamic LDS: hist[TV] points per voxel, start[TV+1] exclusive prefix,
+// cur[TV] scatter cursors, heavy[TV] heavy-voxel list, kbuf[CAP] and
+// rbuf[CAP] the tile's points (index, voxel) as found, list[CAP] the points
+// sorted by voxel, then a region used either as the fp32 feature stage (the
+// tile's points' features, when they fit) or as red[256][8] doubles for the
+// heavy-voxel reduction (also the fp64 accumulators of a voxel holding more
+// than CAP points).
+// ---------------------------------------------------------------------------
+constexpr int kRedBytes = kTileThreads * 8 * (int)sizeof(double);  // 16 KB
+
+struct TileLds {
+    int* hist;
+    int* start;
+    int* cur;
+    int* heavy;
+    int* kbuf;
+    int* rbuf;
+    int* list;
+    double* red;
+    float* stage;
+};
+
+size_t tile_lds_bytes(int TV, int CAP, int stage_bytes) {
+    return (size_t)(4 * TV + 1) * 4 + (size_t)3 * CAP * 4 + 16 /* align */ +
+           (size_t)(stage_bytes > kRedBytes ? stage_bytes : kRedBytes);
+}
+
+__device__ inline TileLds tile_lds(char* smem, int TV, int CAP) {
+    TileLds L;
+    int* p = (int*)smem;
+    L.hist = p;
+    L.start = p + TV;
+    L.cur = L.start + TV + 1;
+    L.heavy = L.cur + TV;
+    L.kbuf = L.heavy + TV;
+    L.rbuf = L.kbuf + CAP;
+    L.list = L.rbuf + CAP;
+    uintptr_t r = (uintptr_t)(L.list + CAP);
+    L.red = (double*)((r + 15) & ~(uintptr_t)15);
+    L.stage = (float*)L.red;
+    return L;
+}
+
+// Means of voxels [lo, hi) of the tile from list (voxel vi's points at
+// list[start[vi] - base .. start[vi+1] - base)), written to out (the tile's
+// grid rows).
+//  * staged (VEC, the segment's features fit the stage): every point's
+//    features are first copied to LDS with independent loads, then each
+//    (voxel, 8-channel group) item sums from LDS and the grid rows stream out;
+//  * otherwise (VEC): voxels of up to kHeavy points are summed straight from
+//    global memory; heavier voxels are then taken one at a time by the whole
+//    workgroup, the points split across threads;
+//  * not VEC: one (voxel, channel) item per thread, straight from memory.
+template <typename FT, typename GT, bool VEC>
+__device__ void tile_fill_range(const TileLds& L, int lo, int hi, int base, const FT* fb,
+                                int feat_ld, int C, GT* out, int* s_nheavy, int stage_bytes) {
+    constexpr int NT = kTileThreads;
+    if (threadIdx.x == 0) *s_nheavy = 0;
+    __syncthreads();
     if (VEC) {
         const int gpv = C / 8;  // 8-channel groups per voxel
-        for (int item = threadIdx.x; item < nv * gpv; item += NT) {
-            const int vi = item / gpv, cg = item - vi * gpv;
-            const int nk = cnt[vi];
+        const int items = (hi - lo) * gpv;
+        const int npts = L.start[hi] - L.start[lo];
+        if ((size_t)npts * C * 4 <= (size_t)stage_bytes) {
+            // stage: row j (list order) = the features of point list[j]
+            const int pieces = npts * gpv;
+            for (int i0 = threadIdx.x; i0 < pieces; i0 += 4 * NT) {
+                float f[4][8];
+#pragma unroll
+                for (int u = 0; u < 4; u++) {
+                    const int i = i0 + u * NT;
+                    if (i < pieces) {
+                        const int j = i / gpv, cg = i - j * gpv;
+                        load8f<FT>(fb + (size_t)L.list[j] * feat_ld + cg * 8, f[u]);
+                    }
+                }
+#pragma unroll
+                for (int u = 0; u < 4; u++) {
+                    const int i = i0 + u * NT;
+                    if (i < pieces) {
+                        float* d = L.stage + (size_t)i * 8;
+                        *(float4*)d = make_float4(f[u][0], f[u][1], f[u][2], f[u][3]);
+                        *(float4*)(d + 4) = make_float4(f[u][4], f[u][5], f[u][6], f[u][7]);
+                    }
+                }
+            }
+            __syncthreads();
+            for (int item = threadIdx.x; item < items; item += NT) {
+                const int vi = lo + item / gpv, cg = item % gpv;
+                const int nk = L.hist[vi];
+                if (nk == 0) continue;  // empty voxel: its row is already zero
+                float mean[8];
+                {
+                    double acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+                    const int j0 = L.start[vi] - base;
+                    for (int j = j0; j < j0 + nk; j++) {
+                        const float* src = L.stage + ((size_t)j * gpv + cg) * 8;
+                        const float4 x0 = *(const float4*)src, x1 = *(const float4*)(src + 4);
+                        acc[0] += x0.x; acc[1] += x0.y; acc[2] += x0.z; acc[3] += x0.w;
+                        acc[4] += x1.x; acc[5] += x1.y; acc[6] += x1.z; acc[7] += x1.w;
+                    }
+#pragma unroll
+                    for (int i = 0; i < 8; i++) mean[i] = (float)(acc[i] / (double)nk);
+                }
+                store8<GT>(out + (size_t)vi * C + cg * 8, mean);
+            }
+            __syncthreads();
+            return;
+        }
+        for (int item = threadIdx.x; item < items; item += NT) {
+            const int vi = lo + item / gpv, cg = item % gpv;
+            const int nk = L.hist[vi];
+            if (nk == 0) continue;  // empty voxel: its row is already zero
             float mean[8];
-            if (nk == 0) {
-                for (int i = 0; i < 8; i++) mean[i] = 0.f;
-            } else {
+            if (nk > kHeavy) {
+                if (cg == 0) L.heavy[atomicAdd(s_nheavy, 1)] = vi;
+                continue;
+            }
+            {
                 double acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-                const int j0 = off[vi];
-                for (int j = j0; j < j0 + nk; j++)
-                    load8<FT>(fb + (size_t)lst[j] * feat_ld + cg * 8, acc);
+                const int j0 = L.start[vi] - base;
+                sum8<FT>(fb, feat_ld, cg * 8, L.list, j0, j0 + nk, 1, acc);
+#pragma unroll
                 for (int i = 0; i < 8; i++) mean[i] = (float)(acc[i] / (double)nk);
             }
             store8<GT>(out + (size_t)vi * C + cg * 8, mean);
         }
-    } else {
-        for (int item = threadIdx.x; item < nv * C; item += NT) {
-            const int vi = item / C, c = item - vi * C;
-            const int nk = cnt[vi];
-            float mean = 0.f;
-            if (nk > 0) {
-                double acc = 0.0;
-                const int j0 = off[vi];
-                for (int j = j0; j < j0 + nk; j++)
-                    acc += (double)load1<FT>(fb + (size_t)lst[j] * feat_ld + c);
-                mean = (float)(acc / (double)nk);
+        __syncthreads();
+        // Heavy voxels: one per wave, four at a time. For channel groups cg0 ..
+        // cg0+ng-1, lane = sub * ng + (cg - cg0) sums points j = sub, sub+S,
+        // ... (S = 64 / ng subsets); the S partial sums are then combined in
+        // subset order through LDS.
+        const int nheavy = *s_nheavy;
+        const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+        double* red = L.red + (size_t)wave * 64 * 8;
+        for (int r0 = 0; r0 < nheavy; r0 += NT / 64) {
+            const int hidx = r0 + wave;
+            const bool active = hidx < nheavy;
+            const int vi = active ? L.heavy[hidx] : 0;
+            const int nk = active ? L.hist[vi] : 0;
+            const int j0 = active ? L.start[vi] - base : 0;
+            for (int cg0 = 0; cg0 < gpv; cg0 += 64) {
+                const int ng = min(64, gpv - cg0);
+                const int S = 64 / ng;
+                const int sub = lane / ng, cl = lane % ng;
+                double acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+                if (active && sub < S)
+                    sum8<FT>(fb, feat_ld, (cg0 + cl) * 8, L.list, j0 + sub, j0 + nk, S, acc);
+                if (sub < S)
+#pragma unroll
+                    for (int i = 0; i < 8; i++) red[(sub * ng + cl) * 8 + i] = acc[i];
+                __syncthreads();
+                if (active && lane < ng) {
+                    double tot[8];
+#pragma unroll
+                    for (int i = 0; i < 8; i++) tot[i] = red[lane * 8 + i];
+                    for (int s2 = 1; s2 < S; s2++)
+#pragma unroll
+                        for (int i = 0; i < 8; i++) tot[i] += red[(s2 * ng + lane) * 8 + i];
+                    float mean[8];
+#pragma unroll
+                    for (int i = 0; i < 8; i++) mean[i] = (float)(tot[i] / (double)nk);
+                    store8<GT>(out + (size_t)vi * C + (cg0 + lane) * 8, mean);
+                }
+                __syncthreads();
             }
-            store1<GT>(out + (size_t)vi * C + c, mean);
+        }
+    } else {
+        const int items = (hi - lo) * C;
+        for (int item = threadIdx.x; item < items; item += NT) {
+            const int vi = lo + item / C, ch = item % C;
+            const int nk = L.hist[vi];
+            if (nk == 0) continue;  // empty voxel: its row is already zero
+            double acc = 0.0;
+            const int j0 = L.start[vi] - base;
+            for (int j = j0; j < j0 + nk; j++)
+                acc += (double)load1<FT>(fb + (size_t)L.list[j] * feat_ld + ch);
+            store1<GT>(out + (size_t)vi * C + ch, (float)(acc / (double)nk));
+        }
+    }
+    __syncthreads();
+}
+
+// The tile's points among ids[0 .. N): count per voxel and keep (index,
+// voxel) while they fit. Reads 16 ids per thread per round when the array
+// is 16-byte aligned.
+__device__ __forceinline__ void tile_collect_one(const TileLds& L, int k, int r, int nv, int CAP,
+                                                 int* s_ntile) {
+    if (r >= 0 && r < nv) {
+        atomicAdd(&L.hist[r], 1);
+        const int slot = atomicAdd(s_ntile, 1);
+        if (slot < CAP) {
+            L.kbuf[slot] = k;
+            L.rbuf[slot] = r;
         }
     }
 }
 
-template <typename FT, typename GT>
-void launch_fill(const void* feats, int feat_ld, int B, int N, int C, int R, int P,
-                 const int32_t* counts, const int32_t* list, const int2* tr, void* grid,
-                 bool vec, hipStream_t s) {
+template <typename FT, typename GT, bool VEC>
+__global__ __launch_bounds__(kTileThreads) void pv_voxel_tile_kernel(
+    const int32_t* __restrict__ vox_id, const FT* __restrict__ feats, int feat_ld, int N, int C,
+    int R, int TV, int CAP, int stage_bytes, GT* __restrict__ grid, int32_t* __restrict__ counts) {
+    constexpr int NT = kTileThreads;
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    __shared__ int scan_lds[NT / 64];
+    __shared__ int s_ntile, s_nheavy;
+    const TileLds L = tile_lds(smem, TV, CAP);
+
+    const int t = blockIdx.x, b = blockIdx.y;
     const int V = R * R * R;
-    dim3 g((V + kTile - 1) / kTile, B);
-    if (vec)
-        hipLaunchKernelGGL((pv_voxel_fill_kernel<FT, GT, true>), g, dim3(256), 0, s,
-                           (const FT*)feats, feat_ld, N, C, R, P, counts, list, tr, (GT*)grid);
-    else
-        hipLaunchKernelGGL((pv_voxel_fill_kernel<FT, GT, false>), g, dim3(256), 0, s,
-                           (const FT*)feats, feat_ld, N, C, R, P, counts, list, tr, (GT*)grid);
+    const int v0 = t * TV, nv = min(TV, V - v0);
+    const int32_t* ids = vox_id + (size_t)b * N;
+    const FT* fb = feats + (size_t)b * N * feat_ld;
+    GT* out = grid + ((size_t)b * V + v0) * C;
+
+    for (int i = threadIdx.x; i < TV; i += NT) L.hist[i] = 0;
+    if (threadIdx.x == 0) s_ntile = 0;
+    __syncthreads();
+    // 1. the tile's points
+    int k0 = 0;
+    if (((uintptr_t)ids & 15) == 0) {
+        const int n16 = N / 16 * 16;  // rounds of 4 int4 loads per thread
+        for (int kb = threadIdx.x * 4; kb < n16; kb += NT * 16) {
+            int4 q[4];
+#pragma unroll
+            for (int u = 0; u < 4; u++) {
+                const int k = kb + u * NT * 4;
+                q[u] = k < n16 ? *(const int4*)(ids + k) : make_int4(-1 - v0, 0, 0, 0);
+            }
+#pragma unroll
+            for (int u = 0; u < 4; u++) {
+                const int k = kb + u * NT * 4;
+                if (k < n16) {
+                    tile_collect_one(L, k, q[u].x - v0, nv, CAP, &s_ntile);
+                    tile_collect_one(L, k + 1, q[u].y - v0, nv, CAP, &s_ntile);
+                    tile_collect_one(L, k + 2, q[u].z - v0, nv, CAP, &s_ntile);
+                    tile_collect_one(L, k + 3, q[u].w - v0, nv, CAP, &s_ntile);
+                }
+            }
+        }
+        k0 = n16;
+    }
+    for (int k = k0 + threadIdx.x; k < N; k += NT) tile_collect_one(L, k, ids[k] - v0, nv, CAP, &s_ntile);
+    __syncthreads();
+    // 2. counts out; exclusive prefix over the tile's voxels
+    int32_t* cnt = counts + (size_t)b * V + v0;
+    for (int i = threadIdx.x; i < nv; i += NT) cnt[i] = L.hist[i];
+    {
+        const int seg = (TV + NT - 1) / NT;
+        const int s0 = min(TV, (int)threadIdx.x * seg), s1 = min(TV, s0 + seg);
+        int local = 0;
+        for (int i = s0; i < s1; i++) local += L.hist[i];
+        int total;
+        int run = block_exclusive_scan<NT>(local, scan_lds, total);
+        for (int i = s0; i < s1; i++) {
+            L.start[i] = run;
+            run += L.hist[i];
+        }
+        if (threadIdx.x == 0) L.start[TV] = total;
+    }
+    __syncthreads();
+    const int total = L.start[TV];
+    if (total <= CAP) {
+        // 3. counting sort of the kept points by voxel, then the fill
+        for (int i = threadIdx.x; i < nv; i += NT) L.cur[i] = L.start[i];
+        __syncthreads();
+        for (int s = threadIdx.x; s < total; s += NT)
+            L.list[atomicAdd(&L.cur[L.rbuf[s]], 1)] = L.kbuf[s];
+        __syncthreads();
+        tile_fill_range<FT, GT, VEC>(L, 0, nv, 0, fb, feat_ld, C, out, &s_nheavy, stage_bytes);
+        return;
+    }
+    // More points than fit: voxel segments of at most CAP points, each
+    // gathered by scanning the ids again. A single voxel beyond CAP points is
+    // summed by the whole workgroup with LDS fp64 atomics.
+    int lo = 0;
+    while (lo < nv) {
+        if (L.start[lo + 1] - L.start[lo] > CAP) {
+            const int nk = L.start[lo + 1] - L.start[lo];
+            double* hacc = L.red;  // C <= 1024 doubles fit in red[] (16 KB)
+            for (int ch = threadIdx.x; ch < C; ch += NT) hacc[ch] = 0.0;
+            __syncthreads();
+            for (int k = threadIdx.x; k < N; k += NT)
+                if (ids[k] == v0 + lo)
+                    for (int ch = 0; ch < C; ch++)
+                        atomicAdd(&hacc[ch], (double)load1<FT>(fb + (size_t)k * feat_ld + ch));
+            __syncthreads();
+            for (int ch = threadIdx.x; ch < C; ch += NT)
+                store1<GT>(out + (size_t)lo * C + ch, (float)(hacc[ch] / (double)nk));
+            __syncthreads();
+            lo++;
+            continue;
+        }
+        // largest hi with start[hi] - start[lo] <= CAP (binary search)
+        int a = lo + 1, z = nv;
+        while (a < z) {
+            const int mid = (a + z + 1) >> 1;
+            if (L.start[mid] - L.start[lo] <= CAP)
+                a = mid;
+            else
+                z = mid - 1;
+        }
+        const int hi = a, base = L.start[lo];
+        for (int i = lo + threadIdx.x; i < hi; i += NT) L.cur[i] = L.start[i] - base;
+        __syncthreads();
+        for (int k = threadIdx.x; k < N; k += NT) {
+            const int r = ids[k] - v0;
+            if (r >= lo && r < hi) L.list[atomicAdd(&L.cur[r], 1)] = k;
+        }
+        __syncthreads();
+        tile_fill_range<FT, GT, VEC>(L, lo, hi, base, fb, feat_ld, C, out, &s_nheavy, stage_bytes);
+        lo = hi;
+    }
+}
+
+// Tile size: small clouds (every tile scans all N ids, cheap) aim for about
+// 2048 workgroups so each tile's points fit the feature stage; large clouds
+// aim for 256 (one per CU) to bound the id scans.
+int tile_voxels(int B, int V, int N) {
+    const long long want = N <= kSmallMaxN ? 2048 : 256;
+    int tv = 1024;
+    while (tv > 128 && (long long)B * ((V + tv - 1) / tv) < want) tv >>= 1;
+    return tv;
+}
+
+constexpr int kStageBytes = 48 * 1024;
+constexpr size_t kLdsMax = 160 * 1024;  // gfx950 LDS per workgroup
+
+// LDS budget of the tile kernel. Small clouds: room for 256 points and a
+// 32 KB feature stage (tiles beyond either take the segmented or unstaged
+// path, rare for small clouds), so several workgroups fit per CU. Large clouds: capacity for kMaxCap points and as much of the
+// stage as the 160 KB LDS leaves. Dynamic LDS beyond 64 KB has to be granted
+// per kernel; when that fails both shrink to what 64 KB holds (tiles with
+// more points then take the unstaged or segmented paths).
+template <typename K>
+void tile_budget(K kernel, int TV, int N, int& cap, int& stage) {
+    const bool small_cloud = N <= kSmallMaxN;
+    const int want = small_cloud ? 256 : kMaxCap;
+    cap = N < want ? (N > 0 ? N : 1) : want;
+    if (small_cloud) {
+        stage = 32 * 1024;
+    } else {
+        const size_t rest = tile_lds_bytes(TV, cap, 0) - kRedBytes;
+        stage = (int)std::min<size_t>(kStageBytes, kLdsMax - rest) & ~15;
+        if (stage < kRedBytes) stage = 0;
+    }
+    const size_t small = 65536;
+    if (tile_lds_bytes(TV, cap, stage) <= small) return;
+    if (hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)tile_lds_bytes(TV, cap, stage)) == hipSuccess)
+        return;
+    (void)hipGetLastError();
+    stage = 0;
+    while (cap > 1 && tile_lds_bytes(TV, cap, stage) > small) cap >>= 1;
+}
+
+template <typename FT, typename GT>
+void launch_tiles(const int32_t* ids, const void* feats, int feat_ld, int B, int N, int C, int R,
+                  void* grid, int32_t* counts, bool vec, hipStream_t s) {
+    const int V = R * R * R;
+    const int TV = tile_voxels(B, V, N);
+    dim3 g((V + TV - 1) / TV, B);
+    int cap, stage;
+    if (vec) {
+        auto k = pv_voxel_tile_kernel<FT, GT, true>;
+        tile_budget(k, TV, N, cap, stage);
+        hipLaunchKernelGGL(k, g, dim3(kTileThreads), tile_lds_bytes(TV, cap, stage), s, ids,
+                           (const FT*)feats, feat_ld, N, C, R, TV, cap, stage, (GT*)grid, counts);
+    } else {
+        auto k = pv_voxel_tile_kernel<FT, GT, false>;
+        tile_budget(k, TV, N, cap, stage);
+        hipLaunchKernelGGL(k, g, dim3(kTileThreads), tile_lds_bytes(TV, cap, stage), s, ids,
+                           (const FT*)feats, feat_ld, N, C, R, TV, cap, 0, (GT*)grid, counts);
+    }
+}
+
+// Zero fill byte by byte, for grids the 16-byte path cannot cover.
+__global__ __launch_bounds__(256) void pv_zero_elems_kernel(char* __restrict__ p, size_t n) {
+    for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (size_t)gridDim.x * 256)
+        p[i] = 0;
 }
 
 struct VoxWs {
-    int32_t* list;
-    int2* tile_range;
     int32_t* ids;
+    float* pnorm;
     SplitWs split;
 };
 
-VoxWs carve_ws(void* ws, int B, int N, int R) {
-    const int V = R * R * R;
-    const int P = (V + kPart - 1) / kPart;
-    const int tiles = (V + kTile - 1) / kTile;
+VoxWs carve_ws(void* ws, int B, int N) {
     const int G = (N + kNormPts - 1) / kNormPts;
     char* p = (char*)ws;
     VoxWs w;
-    w.list = (int32_t*)p;
-    p += pv_align256((size_t)B * P * N * sizeof(int32_t));
-    w.tile_range = (int2*)p;
-    p += pv_align256((size_t)B * tiles * sizeof(int2));
     w.ids = (int32_t*)p;
     p += pv_align256((size_t)B * N * sizeof(int32_t));
+    w.pnorm = (float*)p;
+    p += pv_align256((size_t)B * N * 3 * sizeof(float));
     w.split.G = G;
     w.split.pA = (float*)p;
     p += pv_align256((size_t)B * G * 3 * sizeof(float));
@@ -528,13 +831,10 @@ VoxWs carve_ws(void* ws, int B, int N, int R) {
 }  // namespace
 
 size_t pv_voxelize_ws_bytes(int B, int N, int R) {
-    const int V = R * R * R;
-    const int P = (V + kPart - 1) / kPart;
-    const int tiles = (V + kTile - 1) / kTile;
+    (void)R;
     const int G = (N + kNormPts - 1) / kNormPts;
-    return pv_align256((size_t)B * P * N * sizeof(int32_t)) +
-           pv_align256((size_t)B * tiles * sizeof(int2)) +
-           pv_align256((size_t)B * N * sizeof(int32_t)) +
+    return pv_align256((size_t)B * N * sizeof(int32_t)) +
+           pv_align256((size_t)B * N * 3 * sizeof(float)) +
            pv_align256((size_t)B * G * 3 * sizeof(float)) +
            pv_align256((size_t)B * G * 3 * sizeof(long long)) +
            pv_align256((size_t)B * G * sizeof(double));
@@ -545,50 +845,59 @@ pvconv_status pv_launch_voxelize(const float* coords, const void* feats, bool fe
                                  bool grid_bf16, int32_t* counts, int32_t* vox_id,
                                  float* norm_coords, void* ws, hipStream_t s) {
     if (B == 0) return PVCONV_OK;
-    const int V = R * R * R;
-    const int P = (V + kPart - 1) / kPart;
-    VoxWs w = carve_ws(ws, B, N, R);
+    VoxWs w = carve_ws(ws, B, N);
     int32_t* ids = vox_id ? vox_id : w.ids;
-    if (N > 0) {
-        if (V <= kPart && N <= kSmallMaxN) {
-            hipLaunchKernelGGL(pv_voxelize_bucket_small_kernel, dim3(B), dim3(1024), 0, s, coords,
-                               N, R, ids, norm_coords, counts, w.list, w.tile_range);
-        } else {
-            dim3 g(w.split.G, B);
-            hipLaunchKernelGGL(pv_norm_absmax_kernel, g, dim3(kNormThreads), 0, s, coords, N,
-                               w.split);
-            hipLaunchKernelGGL(pv_norm_sum_kernel, g, dim3(kNormThreads), 0, s, coords, N,
-                               w.split);
-            hipLaunchKernelGGL(pv_norm_radius_kernel, g, dim3(kNormThreads), 0, s, coords, N,
-                               w.split);
-            hipLaunchKernelGGL(pv_norm_points_kernel, g, dim3(kNormThreads), 0, s, coords, N, R,
-                               w.split, ids, norm_coords);
-            hipLaunchKernelGGL(pv_bucket_partition_kernel, dim3(P, B), dim3(1024), 0, s, ids, N,
-                               R, P, counts, w.list, w.tile_range);
+    float* pn = norm_coords ? norm_coords : w.pnorm;
+    // zero the grid (16-byte stores) alongside the normalisation
+    const size_t gbytes = (size_t)B * R * R * R * C * (grid_bf16 ? 2 : 4);
+    const size_t n16 = gbytes / 16;
+    const int zero_blocks = (int)std::min<size_t>(2048, (n16 + 4095) / 4096);
+    uint4* grid16 = (uint4*)grid;
+    const bool grid_ok = pv_aligned16(grid) && gbytes % 16 == 0;
+    if (N <= kSmallMaxN) {
+        const int slices = (N + 255) / 256;
+        const int nid = slices * B;
+        const int zb = grid_ok ? zero_blocks : 0;
+        if (nid + zb > 0) {
+            const dim3 gi(nid + zb);
+            if (N <= 1024)
+                hipLaunchKernelGGL(pv_voxel_ids_kernel<4>, gi, dim3(256), 0, s, coords, N, R,
+                                   slices, nid, ids, pn, grid16, n16);
+            else if (N <= 2048)
+                hipLaunchKernelGGL(pv_voxel_ids_kernel<8>, gi, dim3(256), 0, s, coords, N, R,
+                                   slices, nid, ids, pn, grid16, n16);
+            else
+                hipLaunchKernelGGL(pv_voxel_ids_kernel<16>, gi, dim3(256), 0, s, coords, N, R,
+                                   slices, nid, ids, pn, grid16, n16);
         }
     } else {
-        // No points: every tile is empty. The fill kernel writes zeros; counts
-        // are zeroed here with the same kind of plain store kernel.
-        hipLaunchKernelGGL(pv_bucket_partition_kernel, dim3(P, B), dim3(1024), 0, s, ids, 0, R,
-                           P, counts, w.list, w.tile_range);
+        const int nid = w.split.G * B;
+        const int zb = grid_ok ? zero_blocks : 0;
+        dim3 g(w.split.G, B);
+        hipLaunchKernelGGL(pv_norm_absmax_kernel, dim3(nid + zb), dim3(kNormThreads), 0, s,
+                           coords, N, w.split, B, grid16, n16);
+        hipLaunchKernelGGL(pv_norm_sum_kernel, g, dim3(kNormThreads), 0, s, coords, N, w.split);
+        hipLaunchKernelGGL(pv_norm_radius_kernel, g, dim3(kNormThreads), 0, s, coords, N, w.split);
+        hipLaunchKernelGGL(pv_norm_points_kernel, g, dim3(kNormThreads), 0, s, coords, N, R,
+                           w.split, ids, pn);
+    }
+    if (!grid_ok) {
+        // a grid that 16-byte stores cannot cover: the plain element kernel
+        hipLaunchKernelGGL(pv_zero_elems_kernel, dim3(1024), dim3(256), 0, s, (char*)grid, gbytes);
     }
     const size_t esz_f = feat_bf16 ? 2 : 4, esz_g = grid_bf16 ? 2 : 4;
     const bool vec = (C % 8 == 0) && pv_aligned16(feats) && pv_aligned16(grid) &&
                      ((size_t)feat_ld * esz_f) % 16 == 0 && ((size_t)C * esz_g) % 16 == 0;
     if (feat_bf16) {
         if (grid_bf16)
-            launch_fill<uint16_t, uint16_t>(feats, feat_ld, B, N, C, R, P, counts, w.list,
-                                            w.tile_range, grid, vec, s);
+            launch_tiles<uint16_t, uint16_t>(ids, feats, feat_ld, B, N, C, R, grid, counts, vec, s);
         else
-            launch_fill<uint16_t, float>(feats, feat_ld, B, N, C, R, P, counts, w.list,
-                                         w.tile_range, grid, vec, s);
+            launch_tiles<uint16_t, float>(ids, feats, feat_ld, B, N, C, R, grid, counts, vec, s);
     } else {
         if (grid_bf16)
-            launch_fill<float, uint16_t>(feats, feat_ld, B, N, C, R, P, counts, w.list,
-                                         w.tile_range, grid, vec, s);
+            launch_tiles<float, uint16_t>(ids, feats, feat_ld, B, N, C, R, grid, counts, vec, s);
         else
-            launch_fill<float, float>(feats, feat_ld, B, N, C, R, P, counts, w.list,
-                                      w.tile_range, grid, vec, s);
+            launch_tiles<float, float>(ids, feats, feat_ld, B, N, C, R, grid, counts, vec, s);
     }
     return pv_launch_status();
 }

@@ -107,6 +107,24 @@ def test_voxelize_single_point_and_coincident_clouds():
         assert_rel(host(g), grid, 1e-5)
 
 
+@pytest.mark.parametrize("N,spread", [(60000, 1.0), (9000, 0.0), (40000, 0.02)],
+                         ids=["tile_overflow", "one_voxel_beyond_capacity", "dense_cluster"])
+def test_voxelize_crowded_tiles(N, spread):
+    # More points in one tile than the LDS keeps (segmented path), every point
+    # in one voxel (whole-workgroup path), and one tight cluster (heavy voxels).
+    rng = np.random.default_rng(N)
+    R = 8
+    coords = (rng.uniform(-1, 1, size=(1, N, 3)) * spread).astype(np.float32)
+    coords[0, 0] = [1.0, 1.0, 1.0]   # fixes the radius so the cluster stays central
+    coords[0, 1] = [-1.0, -1.0, -1.0]
+    feats = rng.normal(size=(1, N, 16)).astype(np.float32)
+    pn, ids, grid, counts = _oracle_vox(coords, feats, R)
+    g, c, i, p = pv.pvconv_voxelize(dev(coords), dev(feats), R)
+    assert np.array_equal(i.cpu().numpy(), ids)
+    assert np.array_equal(c.cpu().numpy(), counts)
+    assert_rel(host(g), grid, 1e-5, "crowded voxel grid")
+
+
 def test_voxelize_empty_clouds_give_zero_grids():
     coords = torch.empty((2, 0, 3), device="cuda")
     feats = torch.empty((2, 0, 16), device="cuda")
