@@ -270,6 +270,9 @@ MLP_CASES = [
     (4100, 256, 13, "bf16", True, False, "none", False, 0),
     (2048, 512, 256, "bf16", False, True, "relu", False, 512),
     (65536, 64, 64, "bf16", False, True, "relu", True, 0),    # stress point branch, full
+    (777, 96, 100, "bf16", True, True, "leaky", True, 0),     # ragged K chunk, N and M tails
+    (1500, 40, 36, "bf16", False, True, "relu", True, 500),   # ragged K step, 3 clouds
+    (2500, 128, 260, "f32", True, True, "relu", True, 0),     # fp32 rows, 3 channel blocks
 ]
 
 
@@ -277,7 +280,9 @@ MLP_CASES = [
 def test_point_mlp_bf16_matches_oracle(case):
     M, Cin, Cout, xdt, use_b, use_bn, act, use_res, ppc = case
     rng = np.random.default_rng(M + Cin)
-    x = bf16_round(rng.normal(size=(M, Cin)))
+    x = rng.normal(size=(M, Cin)).astype(np.float32)
+    x_in = dev(x) if xdt == "f32" else dev(bf16_round(x), torch.bfloat16)
+    x = bf16_round(x)  # fp32 rows are rounded to bf16 by the kernel
     w = synth.kaiming_normal(rng, (Cout, Cin), Cin, bf16=True)
     bias = rng.normal(size=Cout).astype(np.float32) if use_b else None
     bn = synth.draw_bn(rng, Cout) if use_bn else None
@@ -292,7 +297,7 @@ def test_point_mlp_bf16_matches_oracle(case):
          "none": lambda a: a}[act](y)
     if res is not None:
         y = y + res
-    out = pv.pvconv_point_mlp(dev(x, torch.bfloat16), dev(w, torch.bfloat16),
+    out = pv.pvconv_point_mlp(x_in, dev(w, torch.bfloat16),
                               bias=dev(bias) if use_b else None,
                               bn=dev_bn(bn) if use_bn else None, act=act, slope=0.2,
                               cloud_bias=dev(cb) if ppc else None, points_per_cloud=max(ppc, 1),
