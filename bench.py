@@ -1,11 +1,14 @@
 #!/usr/bin/env python3
-"""Benchmark of the PVConv forward (one layer) on one MI355X.
+"""Benchmark of the PVConv forward on one MI355X.
 
-A step is one call of pvconv_forward on the whole batch: normalisation and
-voxelisation, the two 3x3x3 convolutions with batch norm and leaky ReLU,
-trilinear devoxelisation and the point-branch MLP whose epilogue adds the two
-branches (Section 4 of the PVCNN paper). Inputs (coordinates, features,
-weights) are resident in device memory before the timed region starts.
+Layer workloads (1, 2, 5): a step is one call of pvconv_forward on the whole
+batch: normalisation and voxelisation, the 3x3x3 convolutions with batch norm
+and leaky ReLU, trilinear devoxelisation and the point-branch MLP whose
+epilogue adds the two branches (Section 4 of the PVCNN paper).
+Network workloads (3, 4): a step is one forward of the PVCNN segmentation
+network (Section 5.1): PVConv blocks, point MLPs, max-pool, head.
+Inputs (coordinates, features, weights) are resident in device memory before
+the timed region starts.
 
 Default workload: the part-segmentation-scale layer, 16 clouds x 2048 points,
 64 -> 128 channels, R = 32, bf16 operands with fp32 accumulation.
@@ -39,8 +42,9 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", type=int, default=2, choices=(1, 2, 5),
-                    help="single-layer workload: 1 fp32 R=8, 2 part-seg R=32, 5 stress R=64")
+    ap.add_argument("--workload", type=int, default=2, choices=(1, 2, 3, 4, 5),
+                    help="1 fp32 layer R=8, 2 part-seg layer R=32, 3 part-seg network, "
+                         "4 scene-seg network, 5 stress layer R=64")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="lower bound of CPU work for the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -98,6 +102,131 @@ def cpu_baseline(wl, gpu_out, seconds):
             {"clouds": done, "max_err": worst, "bound": tol, "ok": worst <= tol})
 
 
+def network_flops(wl):
+    """MFMA flops of one network forward, per step name."""
+    B, N = wl.B, wl.N
+    fl = {}
+    for i, L in enumerate(wl.layers):
+        c, f = L.cin, 0.0
+        for _ in range(L.n_convs):
+            f += conv_flops(B, L.R, c, L.cout)
+            c = L.cout
+        fl[f"pvconv{i + 1}"] = f + 2.0 * B * N * L.cin * L.cout
+    for j, lp in enumerate(wl.mlps):
+        fl[f"mlp{j + 1}"] = 2.0 * B * N * lp.w.shape[0] * lp.w.shape[1]
+    cg = wl.mlps[-1].w.shape[0] if wl.mlps else wl.layers[-1].cout
+    h0 = wl.head[0].w
+    fl["global"] = 2.0 * B * cg * h0.shape[0]
+    fl["head"] = 2.0 * B * N * (h0.shape[0] * (h0.shape[1] - cg)) + sum(
+        2.0 * B * N * lp.w.shape[0] * lp.w.shape[1] for lp in wl.head[1:])
+    return fl
+
+
+def bench_network(args, wl, dev):
+    """A step is one whole segmentation-network forward (PVConv blocks, point
+    MLPs, max-pool, head) on the batch."""
+    import numpy as np
+    import torch
+    from paper_1907_03739_amd.network import DeviceNetwork
+
+    B, N = wl.B, wl.N
+    net = DeviceNetwork(wl.layers, wl.mlps, wl.head, B, N, dev)
+    coords = torch.as_tensor(wl.coords).to(dev)
+    feats = torch.as_tensor(wl.feats).to(dev)
+    stream = torch.cuda.current_stream(dev)
+    for _ in range(args.warmup):
+        net.forward(coords, feats)
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    t0 = time.perf_counter()
+    ev[0].record(stream)
+    for i in range(args.steps):
+        net.forward(coords, feats)
+        ev[i + 1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    step_ms = [ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)]
+    ms_per_step = wall * 1e3 / args.steps
+    gpu_out = net.logits.double().cpu().numpy()
+
+    names = net.steps()
+    per = {n: [] for n in names}
+    for _ in range(args.steps):
+        marks = []
+
+        def mark(name, marks=marks):
+            e = torch.cuda.Event(enable_timing=True)
+            e.record(stream)
+            marks.append(e)
+
+        net.forward_timed(coords, feats, mark)
+        torch.cuda.synchronize()
+        for j, n in enumerate(names):
+            per[n].append(marks[j].elapsed_time(marks[j + 1]))
+    fl = network_flops(wl)
+    kernels = {}
+    for n in names:
+        ms = statistics.mean(per[n])
+        rate = fl[n] / (ms * 1e-3) / 1e12
+        kernels[n] = {"ms": round(ms, 4), "ms_min": round(min(per[n]), 4),
+                      "achieved": round(rate, 2), "unit": "TFLOP/s",
+                      "frac": round(rate / PEAK_BF16_TFLOPS, 4), "algorithmic": fl[n]}
+    dom = max(names, key=lambda n: kernels[n]["ms"])
+    roofline = {"bound": "mfma", "achieved": kernels[dom]["achieved"], "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s", "frac": kernels[dom]["frac"], "traffic": None,
+                "kernel": f"network step {dom}", "flop_per_launch": fl[dom],
+                "avg_launch_ms": kernels[dom]["ms"]}
+    total_fl = sum(fl.values())
+    line = {
+        "metric": METRIC, "value": round(B * N / (ms_per_step * 1e-3), 1), "unit": "points/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": wl.name, "B": B, "N": N,
+                   "blocks": [[L.cin, L.cout, L.R] for L in wl.layers],
+                   "mlps": [int(m.w.shape[0]) for m in wl.mlps],
+                   "head": [int(h.w.shape[0]) for h in wl.head], "points_per_step": B * N},
+        "ms_per_step_events": {"median": round(statistics.median(step_ms), 4),
+                               "min": round(min(step_ms), 4)},
+        "network_tflops": round(total_fl / (ms_per_step * 1e-3) / 1e12, 2),
+        "roofline": roofline,
+        "kernels": kernels,
+        "inputs_sha256": wl.sha256(),
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        cores = int(os.environ.get("OMP_NUM_THREADS") or len(os.sched_getaffinity(0)))
+        done, worst, t_total = 0, 0.0, 0.0
+        for b in range(B):
+            one = synth_one(wl, b)
+            t1 = time.perf_counter()
+            ref = oracle.network_forward(one, stage_dtype="bf16")[0]
+            t_total += time.perf_counter() - t1
+            rms = float(np.sqrt(np.mean(ref ** 2)))
+            worst = max(worst, float(np.max(np.abs(gpu_out[b] - ref) / (np.abs(ref) + rms))))
+            done += 1
+            if t_total >= args.cpu_seconds:
+                break
+        line["cpu_baseline"] = {
+            "value": done * N / t_total, "unit": "points/s", "cores": cores, "kind": "oracle",
+            "sample": f"first {done} of {B} clouds ({done * N} points), one cloud per oracle "
+                      f"call, fp64 with bf16 stage storage, {t_total:.1f} s"}
+        # end-to-end bound of the network parity tests: sqrt(S) x the chain bound
+        stages = len(wl.layers) + len(wl.mlps) + len(wl.head) - 1
+        bound = 2e-2 * stages ** 0.5
+        line["parity_sample"] = {"clouds": done, "max_err": worst, "bound": round(bound, 4),
+                                 "ok": worst <= bound}
+    print(json.dumps(line), flush=True)
+
+
+def synth_one(wl, b):
+    """Workload wl restricted to its cloud b (the networks are per cloud)."""
+    import copy
+    one = copy.copy(wl)
+    one.B, one.coords, one.feats = 1, wl.coords[b:b + 1], wl.feats[b:b + 1]
+    return one
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -120,6 +249,8 @@ def main():
     torch.cuda.set_device(dev)
 
     wl = synth.make_workload(args.workload)
+    if wl.is_network:
+        return bench_network(args, wl, dev)
     L = wl.layers[0]
     bf16 = wl.dtype == "bf16"
     cdt = torch.bfloat16 if bf16 else torch.float32

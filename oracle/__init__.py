@@ -274,7 +274,22 @@ def shared_mlp(x, lp):
     return y
 
 
-def network_forward(wl, return_stages=False):
+def round_bf16(a) -> np.ndarray:
+    """Each value rounded to the nearest bfloat16 (8 significant bits, fp32's
+    exponent range; round to nearest, ties to even), returned as float64.
+
+    This is the storage precision of the networks' activations ("bf16 weights
+    and activations", the configuration of Section 5.1's networks used here).
+    For x = m 2^e with m in [0.5, 1) the bf16 grid spacing near x is
+    2^(e-8), and 2^-133 below the normal range."""
+    x = _f64(a)
+    _, e = np.frexp(x)
+    q = np.ldexp(1.0, np.maximum(e - 8, -133))
+    r = np.rint(x / q) * q          # x / q is exact: q is a power of two
+    return np.where(np.isfinite(x), r, x)
+
+
+def network_forward(wl, return_stages=False, stage_dtype="f64"):
     """PVCNN segmentation forward (Section 5.1 "Models": PointNet with its
     per-point MLP layers replaced by PVConv).
 
@@ -282,21 +297,31 @@ def network_forward(wl, return_stages=False):
     a per-cloud max over the points of the last stage gives the global feature;
     the head's input is the concatenation of every stage's per-point output and
     the global feature broadcast to every point; the head is a stack of shared
-    per-point layers ending in logits."""
+    per-point layers ending in logits.
+
+    stage_dtype "f64" keeps every value in fp64; "bf16" stores each stage's
+    output and each hidden head layer's output in bf16 (round_bf16) before the
+    next step reads it, as a network with bf16 activations does. The logits
+    are never rounded."""
+    if stage_dtype not in ("f64", "bf16"):
+        raise ValueError("stage_dtype must be 'f64' or 'bf16'")
+    store = round_bf16 if stage_dtype == "bf16" else (lambda v: v)
     x = wl.feats
     stages = []
     for L in wl.layers:
-        x = pvconv_forward(wl.coords, x, L)
+        x = store(pvconv_forward(wl.coords, x, L))
         stages.append(x)
     for lp in wl.mlps:
-        x = shared_mlp(x, lp)
+        x = store(shared_mlp(x, lp))
         stages.append(x)
     g = maxpool(x)
     B, N = wl.B, wl.N
     cat = np.concatenate(stages + [np.broadcast_to(g[:, None, :], (B, N, g.shape[1]))], axis=2)
     h = cat
-    for lp in wl.head:
+    for k, lp in enumerate(wl.head):
         h = shared_mlp(h, lp)
+        if k + 1 < len(wl.head):
+            h = store(h)
     if return_stages:
         return h, stages, g
     return h

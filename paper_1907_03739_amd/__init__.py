@@ -16,10 +16,12 @@ _BINDING_NAMES = (
     "pvconv_voxelize",
 )
 
-__all__ = list(_BINDING_NAMES)
+__all__ = list(_BINDING_NAMES) + ["DeviceNetwork"]
 
 
 def __getattr__(name):
     if name in _BINDING_NAMES:
         return getattr(importlib.import_module(".binding", __name__), name)
+    if name == "DeviceNetwork":
+        return importlib.import_module(".network", __name__).DeviceNetwork
     raise AttributeError(f"module {__name__!r} has no attribute {name!r}")

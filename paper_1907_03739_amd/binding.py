@@ -206,11 +206,14 @@ def pvconv_point_mlp(x: torch.Tensor, weight: torch.Tensor, bias=None, bn=None, 
     return out
 
 
-def pvconv_maxpool(x: torch.Tensor):
+def pvconv_maxpool(x: torch.Tensor, out: Optional[torch.Tensor] = None):
     """x [B][N][C] (rows evenly strided) -> [B][C] f32."""
     B, N, C = x.shape
     ld = _rows(x, N, C)
-    out = torch.empty((B, C), dtype=torch.float32, device=x.device)
+    if out is None:
+        out = torch.empty((B, C), dtype=torch.float32, device=x.device)
+    elif tuple(out.shape) != (B, C) or out.dtype != torch.float32 or not out.is_contiguous():
+        raise ValueError("out must be a contiguous [B][C] float32 tensor")
     _check("pvconv_maxpool", _lib.pvconv_maxpool(_p(x), _dt(x), ld, B, N, C, _p(out),
                                                  _stream(x)))
     return out

@@ -76,4 +76,7 @@ def assert_bf16_step(gpu, ref, what="bf16"):
 def assert_bf16_chain(gpu, ref, what="bf16 chain"):
     d = np.abs(gpu - ref)
     rms = float(np.sqrt(np.mean(ref ** 2))) if ref.size else 0.0
+    if d.size:
+        print(f"[{what}] max |d|/(|ref|+rms) = {float(np.max(d / (np.abs(ref) + rms))):.3g}",
+              flush=True)
     _report(d, 2e-2 * (np.abs(ref) + rms), what)

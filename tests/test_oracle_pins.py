@@ -400,3 +400,81 @@ def test_layer_is_the_sum_of_its_branches():
                                                                   cb.eps)
     z = np.where(z < 0, 0.1 * z, z)
     np.testing.assert_allclose(p0["devox"], np.broadcast_to(z, p0["devox"].shape), rtol=1e-12)
+
+
+# ----------------------------------------------------------------------------
+# Network glue (Section 5.1 "Models") and bf16 storage of activations
+# ----------------------------------------------------------------------------
+def test_round_bf16_matches_torch_and_breaks_ties_to_even():
+    rng = _rng(20)
+    x = np.concatenate([rng.normal(size=4000) * 10.0 ** rng.integers(-30, 30, size=4000),
+                        rng.normal(size=200) * 2.0 ** -128]).astype(np.float32)
+    ref = torch.from_numpy(x).to(torch.bfloat16).to(torch.float64).numpy()
+    np.testing.assert_array_equal(oracle.round_bf16(x), ref)
+    one = 1.0
+    cases = {one + 2 ** -8: one,                       # tie, even neighbour below
+             one + 3 * 2 ** -8: one + 2 ** -6,          # tie, even neighbour above
+             -(one + 2 ** -8): -one,
+             one + 2 ** -8 + 2 ** -30: one + 2 ** -7,   # just past the tie
+             0.0: 0.0, 3.0: 3.0}
+    for v, want in cases.items():
+        assert oracle.round_bf16(np.array([v]))[0] == want, v
+    assert np.isnan(oracle.round_bf16(np.array([np.nan]))[0])
+
+
+@pytest.mark.parametrize("idx", [3, 4])
+def test_network_clouds_are_independent(idx):
+    wl = synth.make_workload(idx, B=2, N=96)
+    full = oracle.network_forward(wl)
+    for b in range(2):
+        one = synth.make_workload(idx, B=2, N=96)
+        one.B, one.coords, one.feats = 1, wl.coords[b:b + 1], wl.feats[b:b + 1]
+        np.testing.assert_array_equal(oracle.network_forward(one)[0], full[b])
+
+
+def test_network_global_feature_is_broadcast_last():
+    """With the head's stage columns zeroed, the first head layer sees only
+    the pooled global feature: every point of a cloud gets the same logits,
+    equal to the head applied to g alone."""
+    wl = synth.make_workload(3, B=2, N=80)
+    h0 = wl.head[0]
+    cg = wl.mlps[-1].w.shape[0]
+    w = h0.w.copy()
+    w[:, :-cg] = 0.0
+    wl.head = [synth.LinearParams(w=w, b=h0.b, bn=h0.bn, relu=h0.relu)] + wl.head[1:]
+    out, stages, g = oracle.network_forward(wl, return_stages=True)
+    np.testing.assert_allclose(out, np.broadcast_to(out[:, :1], out.shape), rtol=0, atol=1e-12)
+    np.testing.assert_array_equal(g, stages[-1].max(axis=1))
+    h = g
+    for lp in [synth.LinearParams(w=w[:, -cg:], b=h0.b, bn=h0.bn, relu=h0.relu)] + wl.head[1:]:
+        h = oracle.shared_mlp(h, lp)
+    np.testing.assert_allclose(out[:, 0], h, rtol=1e-12, atol=1e-12)
+
+
+def test_network_concat_order_follows_the_stages():
+    """A head whose first layer is the identity on one stage-column range
+    (then no BN/activation) returns exactly that stage's output."""
+    wl = synth.make_workload(4, B=1, N=64)
+    widths = [L.cout for L in wl.layers] + [m.w.shape[0] for m in wl.mlps]
+    total = sum(widths) + widths[-1]
+    k = 1                                   # the second PVConv block
+    off = sum(widths[:k])
+    w = np.zeros((widths[k], total))
+    w[np.arange(widths[k]), off + np.arange(widths[k])] = 1.0
+    wl.head = [synth.LinearParams(w=w, b=None, bn=None, relu=False)]
+    out, stages, _ = oracle.network_forward(wl, return_stages=True)
+    np.testing.assert_array_equal(out, stages[k])
+
+
+def test_network_bf16_storage_rounds_every_stage():
+    wl = synth.make_workload(4, B=1, N=64)
+    out16, st16, g16 = oracle.network_forward(wl, return_stages=True, stage_dtype="bf16")
+    out64 = oracle.network_forward(wl)
+    for s in st16:
+        np.testing.assert_array_equal(oracle.round_bf16(s), s)
+    np.testing.assert_array_equal(oracle.round_bf16(g16), g16)
+    rms = np.sqrt(np.mean(out64 ** 2))
+    assert np.max(np.abs(out16 - out64)) < 0.05 * rms   # bf16 storage, not a different net
+    assert np.max(np.abs(out16 - out64)) > 0.0
+    with pytest.raises(ValueError):
+        oracle.network_forward(wl, stage_dtype="f16")
