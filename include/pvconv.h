@@ -177,6 +177,8 @@ pvconv_status pvconv_point_mlp(const void* x, pvconv_dtype x_dt, int x_ld, int M
 /* Per-cloud max over the points (the PointNet global feature that PVCNN     */
 /* keeps, Section 5.1 "Models"): out[b][c] = max_k x[b][k][c].               */
 /*  x    [B][N][C] (dt), row stride x_ld;  out [B][C] fp32.  N >= 1.         */
+/* Exact and order-free (deterministic). NaN inputs are a precondition       */
+/* violation: the result for their channel is unspecified.                   */
 /* ------------------------------------------------------------------------- */
 pvconv_status pvconv_maxpool(const void* x, pvconv_dtype dt, int x_ld, int B, int N, int C,
                              float* out, void* stream);

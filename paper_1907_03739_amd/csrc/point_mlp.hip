@@ -228,6 +228,186 @@ __global__ __launch_bounds__(kWaves * 64) void pv_point_mlp_tile_kernel(
         }
 }
 
+// ---- wide layers: LDS-tiled MFMA GEMM ------------------------------------
+// For K >= 128 and C_out >= 128 the layer is MFMA-bound, so operands are
+// shared through LDS: a 256-thread workgroup owns a TN x TM (channels x
+// points) output tile, stages K in chunks of kGK = 64 (weights and point rows
+// as bf16, 128 bytes of data per row padded to kGPitch = 144 so that the
+// 16-byte fragment reads of 16 consecutive rows hit distinct banks), double
+// buffered: the next chunk's global loads are in flight while the current
+// chunk feeds the MFMAs, one barrier per chunk. Each wave computes
+// (NB*32) x (MB*32) of the tile with the weights as the A operand, so the
+// epilogue holds 4 consecutive channels of one point per lane.
+constexpr int kGK = 64;
+constexpr int kGPitch = 144;
+
+template <int NB, int MB, int WN, int WM>
+struct GemmShape {
+    static constexpr int TN = WN * NB * 32;   // output channels per workgroup
+    static constexpr int TM = WM * MB * 32;   // points per workgroup
+    static constexpr int ROWS = TN + TM;      // staged rows per chunk
+    static constexpr int PIECES = ROWS * 8 / 256;  // 16-byte pieces per thread per chunk
+    static constexpr int LDS = 2 * ROWS * kGPitch;
+    static_assert(WN * WM == 4, "four waves");
+    static_assert(ROWS % 32 == 0, "rows come in groups of 32 per piece set");
+};
+
+__device__ __forceinline__ uint4 piece_bf16(const uint16_t* p) { return *(const uint4*)p; }
+__device__ __forceinline__ uint4 piece_bf16(const float* p) {
+    const float4 a = *(const float4*)p, b = *(const float4*)(p + 4);
+    return uint4{pv_pack_bf16x2(a.x, a.y), pv_pack_bf16x2(a.z, a.w), pv_pack_bf16x2(b.x, b.y),
+                 pv_pack_bf16x2(b.z, b.w)};
+}
+
+// Requirements (checked by the launcher): Cin % 8 == 0, Cout % 4 == 0, x and
+// weight rows 16-byte aligned, residual / cloud rows 16-byte aligned, output
+// rows 16-byte (fp32) or 8-byte (bf16) aligned.
+template <int NB, int MB, int WN, int WM, typename XT>
+__global__ __launch_bounds__(256, 1) void pv_point_mlp_lds_kernel(
+    const XT* __restrict__ x, int x_ld, int M, int Cin, int Cout, const uint16_t* __restrict__ w,
+    PvBnFold bn, int act, float slope, const float* __restrict__ cloud_bias, int ppc,
+    const float* __restrict__ residual, int res_ld, void* __restrict__ out, int out_bf16,
+    int out_ld, int ntn, int nblocks) {
+    typedef GemmShape<NB, MB, WN, WM> S;
+    __shared__ __attribute__((aligned(16))) char lds[S::LDS];
+    __shared__ float4 tab[2][S::TN / 4];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    // Consecutive tiles (same point rows, neighbouring channel tiles) go to
+    // the same XCD, so the point rows are fetched into one L2.
+    int bid = blockIdx.x;
+    if ((nblocks & 7) == 0) bid = (bid & 7) * (nblocks >> 3) + (bid >> 3);
+    const int n0 = (bid % ntn) * S::TN, m0 = (bid / ntn) * S::TM;
+
+    if (tid < S::TN) {
+        const int c = min(n0 + tid, Cout - 1);
+        float sc, sh;
+        pv_bn_coeffs(bn, c, sc, sh);
+        ((float*)tab[0])[tid] = sc;
+        ((float*)tab[1])[tid] = sh;
+    }
+
+    // Staging: piece i*256 + tid is row i*32 + tid/8 of the chunk (weight
+    // rows first, then point rows), bytes (tid%8)*16 .. +15 of its 128.
+    // Rows past M or C_out are clamped onto the last valid row (their results
+    // are never stored); columns past C_in stage as zero.
+    const int part = tid & 7;
+    const uint16_t* wsrc = w + part * 8;
+    const XT* xsrc = x + part * 8;
+    uint4 stage[S::PIECES];
+    auto stage_load = [&](int k0) {
+        const bool ok = k0 + part * 8 < Cin;
+        const int k = ok ? k0 : 0;
+#pragma unroll
+        for (int i = 0; i < S::PIECES; i++) {
+            const int row = i * 32 + (tid >> 3);
+            uint4 v;
+            if (row < S::TN)   // resolved at compile time (TN is a multiple of 32)
+                v = piece_bf16(wsrc + (size_t)min(n0 + row, Cout - 1) * Cin + k);
+            else
+                v = piece_bf16(xsrc + (size_t)min(m0 + row - S::TN, M - 1) * x_ld + k);
+            stage[i] = ok ? v : uint4{0u, 0u, 0u, 0u};
+        }
+    };
+    auto stage_store = [&](int buf) {
+        char* base = lds + buf * (S::ROWS * kGPitch) + (tid >> 3) * kGPitch + part * 16;
+#pragma unroll
+        for (int i = 0; i < S::PIECES; i++) *(uint4*)(base + i * 32 * kGPitch) = stage[i];
+    };
+
+    const int wn = wave % WN, wm = wave / WN;
+    const int r32 = lane & 31, khalf = lane >> 5;
+    const int a_off = (wn * NB * 32 + r32) * kGPitch + khalf * 16;
+    const int b_off = (S::TN + wm * MB * 32 + r32) * kGPitch + khalf * 16;
+
+    pv_f32x16 acc[MB][NB];
+#pragma unroll
+    for (int i = 0; i < MB; i++)
+#pragma unroll
+        for (int j = 0; j < NB; j++)
+#pragma unroll
+            for (int e = 0; e < 16; e++) acc[i][j][e] = 0.f;
+
+    const int nch = (Cin + kGK - 1) / kGK;
+    stage_load(0);
+    stage_store(0);
+    __syncthreads();
+    for (int c = 0; c < nch; c++) {
+        if (c + 1 < nch) stage_load((c + 1) * kGK);
+        const char* buf = lds + (c & 1) * (S::ROWS * kGPitch);
+#pragma unroll
+        for (int ks = 0; ks < kGK / 16; ks++) {
+            pv_bf16x8 a[NB], b[MB];
+#pragma unroll
+            for (int nb = 0; nb < NB; nb++)
+                a[nb] = *(const pv_bf16x8*)(buf + a_off + nb * 32 * kGPitch + ks * 32);
+#pragma unroll
+            for (int mb = 0; mb < MB; mb++)
+                b[mb] = *(const pv_bf16x8*)(buf + b_off + mb * 32 * kGPitch + ks * 32);
+#pragma unroll
+            for (int mb = 0; mb < MB; mb++)
+#pragma unroll
+                for (int nb = 0; nb < NB; nb++)
+                    acc[mb][nb] =
+                        __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[nb], b[mb], acc[mb][nb], 0, 0, 0);
+        }
+        if (c + 1 < nch) stage_store((c + 1) & 1);
+        __syncthreads();
+    }
+
+    // Epilogue, one 32-point block (mb) at a time. acc[mb][nb][4g + j] is
+    // channel wn*NB*32 + nb*32 + 8g + 4*khalf + j of the tile at point
+    // wm*MB*32 + mb*32 + r32. The per-cloud and residual rows of block mb+1
+    // are loaded before block mb is stored: one counter tracks loads and
+    // stores alike, so a load issued after a store would wait for it.
+    const float neg = act == PVCONV_ACT_LEAKY ? slope : (act == PVCONV_ACT_RELU ? 0.f : 1.f);
+    float4 ext[2][2][NB][4];   // [set][cloud row, residual][nb][g]
+    auto load_ext = [&](int mb, float4 (&e)[2][NB][4]) {
+        const int m = min(m0 + wm * MB * 32 + mb * 32 + r32, M - 1);
+        const float* cbr = cloud_bias ? cloud_bias + (size_t)(m / ppc) * Cout : nullptr;
+        const float* rr = residual ? residual + (size_t)m * res_ld : nullptr;
+#pragma unroll
+        for (int nb = 0; nb < NB; nb++)
+#pragma unroll
+            for (int g = 0; g < 4; g++) {
+                const int n = min(n0 + wn * NB * 32 + nb * 32 + g * 8 + 4 * khalf, Cout - 4);
+                e[0][nb][g] = cbr ? *(const float4*)(cbr + n) : float4{0.f, 0.f, 0.f, 0.f};
+                e[1][nb][g] = rr ? *(const float4*)(rr + n) : float4{0.f, 0.f, 0.f, 0.f};
+            }
+    };
+    load_ext(0, ext[0]);
+#pragma unroll
+    for (int mb = 0; mb < MB; mb++) {
+        if (mb + 1 < MB) load_ext(mb + 1, ext[(mb + 1) & 1]);
+        const int m = m0 + wm * MB * 32 + mb * 32 + r32;
+        const size_t orow = (size_t)min(m, M - 1) * out_ld;
+#pragma unroll
+        for (int nb = 0; nb < NB; nb++)
+#pragma unroll
+            for (int g = 0; g < 4; g++) {
+                const int nl = wn * NB * 32 + nb * 32 + g * 8 + 4 * khalf;
+                const float4 sc = tab[0][nl >> 2], sh = tab[1][nl >> 2];
+                const float4 cb = ext[mb & 1][0][nb][g], rs = ext[mb & 1][1][nb][g];
+                float v[4] = {(acc[mb][nb][4 * g] + cb.x) * sc.x + sh.x,
+                              (acc[mb][nb][4 * g + 1] + cb.y) * sc.y + sh.y,
+                              (acc[mb][nb][4 * g + 2] + cb.z) * sc.z + sh.z,
+                              (acc[mb][nb][4 * g + 3] + cb.w) * sc.w + sh.w};
+#pragma unroll
+                for (int j = 0; j < 4; j++) v[j] = v[j] >= 0.f ? v[j] : v[j] * neg;
+                v[0] += rs.x;
+                v[1] += rs.y;
+                v[2] += rs.z;
+                v[3] += rs.w;
+                if (m >= M || n0 + nl >= Cout) continue;
+                if (out_bf16)
+                    *(uint2*)((uint16_t*)out + orow + n0 + nl) =
+                        uint2{pv_pack_bf16x2(v[0], v[1]), pv_pack_bf16x2(v[2], v[3])};
+                else
+                    *(float4*)((float*)out + orow + n0 + nl) = float4{v[0], v[1], v[2], v[3]};
+            }
+    }
+}
+
 // Scalar-epilogue kernel for shapes the tile kernel cannot take (odd channel
 // counts or unaligned rows): one wave per 32 points x (32*NB) channels with
 // the points as the A operand.
@@ -290,6 +470,22 @@ __device__ __forceinline__ float ld1<float>(const float* p) { return *p; }
 template <>
 __device__ __forceinline__ float ld1<uint16_t>(const uint16_t* p) { return pv_bf16_to_f32(*p); }
 
+// 8 consecutive values as fp32 (no rounding): the max-pool's loads.
+__device__ __forceinline__ void load8_raw(const float* p, float (&v)[8]) {
+    const float4 a = *(const float4*)p, b = *(const float4*)(p + 4);
+    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+    v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+}
+__device__ __forceinline__ void load8_raw(const uint16_t* p, float (&v)[8]) {
+    const uint4 a = *(const uint4*)p;
+    const uint32_t u[4] = {a.x, a.y, a.z, a.w};
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+        v[2 * i] = __uint_as_float(u[i] << 16);
+        v[2 * i + 1] = __uint_as_float(u[i] & 0xffff0000u);
+    }
+}
+
 template <typename XT>
 __global__ __launch_bounds__(256) void pv_point_mlp_f32_kernel(
     const XT* __restrict__ x, int x_ld, int M, int Cin, int Cout, const float* __restrict__ w,
@@ -335,22 +531,168 @@ void launch_mfma(const void* x, int x_ld, int M, int Cin, int Cout, const void* 
                            cb, ppc, res, res_ld, out, (int)out_bf16, out_ld);
 }
 
+// ---- small-M path --------------------------------------------------------
+// Fewer rows than one tile workgroup covers (e.g. one row per cloud): one wave
+// per output element, the lanes splitting K, then a wave-wide sum. bf16
+// operands (fp32 rows rounded to bf16) with fp32 accumulation, like the MFMA
+// path.
+template <int NB, int MB, int WN, int WM, typename XT>
+void launch_lds(const void* x, int x_ld, int M, int Cin, int Cout, const void* w,
+                const PvBnFold& bn, int act, float slope, const float* cb, int ppc,
+                const float* res, int res_ld, void* out, bool out_bf16, int out_ld,
+                hipStream_t s) {
+    typedef GemmShape<NB, MB, WN, WM> S;
+    const int ntn = (Cout + S::TN - 1) / S::TN;
+    const int nblocks = ntn * ((M + S::TM - 1) / S::TM);
+    hipLaunchKernelGGL((pv_point_mlp_lds_kernel<NB, MB, WN, WM, XT>), dim3(nblocks), dim3(256), 0,
+                       s, (const XT*)x, x_ld, M, Cin, Cout, (const uint16_t*)w, bn, act, slope, cb,
+                       ppc, res, res_ld, out, (int)out_bf16, out_ld, ntn, nblocks);
+}
+
 template <typename XT>
-__global__ __launch_bounds__(256) void pv_maxpool_kernel(const XT* __restrict__ x, int x_ld,
-                                                         int N, int C, float* __restrict__ out) {
-    __shared__ float part[4][64];
-    const int c = blockIdx.x * 64 + (threadIdx.x & 63);
-    const int slice = threadIdx.x >> 6;
-    const int b = blockIdx.y;
-    float m = -INFINITY;
-    if (c < C)
-        for (int k = slice; k < N; k += 4) m = fmaxf(m, ld1<XT>(x + ((size_t)b * N + k) * x_ld + c));
-    part[slice][threadIdx.x & 63] = m;
-    __syncthreads();
-    if (slice == 0 && c < C) {
-        for (int i = 1; i < 4; i++) m = fmaxf(m, part[i][threadIdx.x]);
-        out[(size_t)b * C + c] = m;
+__device__ __forceinline__ void load8_f32(const XT* p, float (&v)[8]);
+template <>
+__device__ __forceinline__ void load8_f32<float>(const float* p, float (&v)[8]) {
+    const float4 a = *(const float4*)p, b = *(const float4*)(p + 4);
+    v[0] = pv_bf16_to_f32(pv_f32_to_bf16(a.x)); v[1] = pv_bf16_to_f32(pv_f32_to_bf16(a.y));
+    v[2] = pv_bf16_to_f32(pv_f32_to_bf16(a.z)); v[3] = pv_bf16_to_f32(pv_f32_to_bf16(a.w));
+    v[4] = pv_bf16_to_f32(pv_f32_to_bf16(b.x)); v[5] = pv_bf16_to_f32(pv_f32_to_bf16(b.y));
+    v[6] = pv_bf16_to_f32(pv_f32_to_bf16(b.z)); v[7] = pv_bf16_to_f32(pv_f32_to_bf16(b.w));
+}
+template <>
+__device__ __forceinline__ void load8_f32<uint16_t>(const uint16_t* p, float (&v)[8]) {
+    const uint4 a = *(const uint4*)p;
+    const uint32_t u[4] = {a.x, a.y, a.z, a.w};
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+        v[2 * i] = __uint_as_float(u[i] << 16);
+        v[2 * i + 1] = __uint_as_float(u[i] & 0xffff0000u);
     }
+}
+template <typename XT>
+__device__ __forceinline__ float ldb(const XT* p);
+template <>
+__device__ __forceinline__ float ldb<float>(const float* p) {
+    return pv_bf16_to_f32(pv_f32_to_bf16(*p));
+}
+template <>
+__device__ __forceinline__ float ldb<uint16_t>(const uint16_t* p) { return pv_bf16_to_f32(*p); }
+
+template <typename XT, bool VEC>
+__global__ __launch_bounds__(256) void pv_point_mlp_rows_kernel(
+    const XT* __restrict__ x, int x_ld, int M, int Cin, int Cout, const uint16_t* __restrict__ w,
+    PvBnFold bn, int act, float slope, const float* __restrict__ cloud_bias, int ppc,
+    const float* __restrict__ residual, int res_ld, void* __restrict__ out, int out_bf16,
+    int out_ld) {
+    const int lane = threadIdx.x & 63;
+    const long e = (long)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (e >= (long)M * Cout) return;
+    const int m = (int)(e / Cout), n = (int)(e % Cout);
+    const XT* xr = x + (size_t)m * x_ld;
+    const uint16_t* wr = w + (size_t)n * Cin;
+    float s = 0.f;
+    if (VEC) {
+#pragma unroll 2
+        for (int k = lane * 8; k < Cin; k += 512) {
+            float a[8], b[8];
+            load8_f32<XT>(xr + k, a);
+            load8_f32<uint16_t>(wr + k, b);
+#pragma unroll
+            for (int j = 0; j < 8; j++) s += a[j] * b[j];
+        }
+    } else {
+#pragma unroll 4
+        for (int k = lane; k < Cin; k += 64) s += ldb<XT>(xr + k) * pv_bf16_to_f32(wr[k]);
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
+    if (lane != 0) return;
+    if (cloud_bias) s += cloud_bias[(size_t)(m / ppc) * Cout + n];
+    float sc, sh;
+    pv_bn_coeffs(bn, n, sc, sh);
+    float v = pv_activate(s * sc + sh, act, slope);
+    if (residual) v += residual[(size_t)m * res_ld + n];
+    if (out_bf16)
+        ((uint16_t*)out)[(size_t)m * out_ld + n] = pv_f32_to_bf16(v);
+    else
+        ((float*)out)[(size_t)m * out_ld + n] = v;
+}
+
+// ---- per-cloud max-pool -------------------------------------------------
+// out starts at -inf (fill kernel); each block takes a slice of kPoolPts
+// points of one cloud and a range of channels, reduces in registers (and
+// across its four waves in LDS), then merges into out with integer atomics:
+// for a non-negative float the int ordering is the float ordering, for a
+// negative one the unsigned ordering is reversed, so atomicMax on int and
+// atomicMin on unsigned give the float max in any order, bit-exactly.
+constexpr int kPoolPts = 128;
+
+__device__ __forceinline__ void atomic_max_f32(float* a, float v) {
+    if (__float_as_int(v) >= 0)
+        atomicMax((int*)a, __float_as_int(v));
+    else
+        atomicMin((unsigned int*)a, __float_as_uint(v));
+}
+
+__global__ __launch_bounds__(256) void pv_fill_f32_kernel(float* __restrict__ p, int n, float v) {
+    const int i = blockIdx.x * 256 + threadIdx.x;
+    if (i < n) p[i] = v;
+}
+
+// VEC: C % 8 == 0 and 16-byte rows; a lane owns 8 consecutive channels, a
+// wave 512, and the block's four waves split the slice's points.
+template <typename XT>
+__global__ __launch_bounds__(256) void pv_maxpool_vec_kernel(const XT* __restrict__ x, int x_ld,
+                                                             int N, int C,
+                                                             float* __restrict__ out) {
+    __shared__ float part[4][512];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int b = blockIdx.y;
+    const int p0 = blockIdx.z * kPoolPts, p1 = min(p0 + kPoolPts, N);
+    const int cb = blockIdx.x * 512, c0 = cb + lane * 8;
+    float m[8];
+#pragma unroll
+    for (int j = 0; j < 8; j++) m[j] = -INFINITY;
+    if (c0 < C) {
+        const XT* base = x + (size_t)b * N * x_ld + c0;
+        for (int p = p0 + wave; p < p1; p += 16) {
+            // four rows in flight; past the slice, a row repeats (max is idempotent)
+            float v[4][8];
+#pragma unroll
+            for (int u = 0; u < 4; u++) {
+                const int row = p + 4 * u < p1 ? p + 4 * u : p;
+                load8_raw(base + (size_t)row * x_ld, v[u]);
+            }
+#pragma unroll
+            for (int u = 0; u < 4; u++)
+#pragma unroll
+                for (int j = 0; j < 8; j++) m[j] = fmaxf(m[j], v[u][j]);
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < 8; j++) part[wave][lane * 8 + j] = m[j];
+    __syncthreads();
+    for (int i = threadIdx.x; i < 512; i += 256) {
+        const int c = cb + i;
+        if (c >= C) continue;
+        const float r = fmaxf(fmaxf(part[0][i], part[1][i]), fmaxf(part[2][i], part[3][i]));
+        atomic_max_f32(out + (size_t)b * C + c, r);
+    }
+}
+
+template <typename XT>
+__global__ __launch_bounds__(256) void pv_maxpool_scalar_kernel(const XT* __restrict__ x,
+                                                                int x_ld, int N, int C,
+                                                                float* __restrict__ out) {
+    const int c = blockIdx.x * 256 + threadIdx.x;
+    const int b = blockIdx.y;
+    const int p0 = blockIdx.z * kPoolPts, p1 = min(p0 + kPoolPts, N);
+    if (c >= C) return;
+    const XT* base = x + (size_t)b * N * x_ld + c;
+    float m = -INFINITY;
+#pragma unroll 4
+    for (int p = p0; p < p1; p++) m = fmaxf(m, ld1<XT>(base + (size_t)p * x_ld));
+    atomic_max_f32(out + (size_t)b * C + c, m);
 }
 
 }  // namespace
@@ -361,6 +703,23 @@ pvconv_status pv_launch_point_mlp(const void* x, bool x_bf16, int x_ld, int M, i
                                   const float* res, int res_ld, void* out, bool out_bf16,
                                   int out_ld, hipStream_t s) {
     if (M == 0) return PVCONV_OK;
+    if (bf16 && M < kWaves * 32) {
+        const size_t esz = x_bf16 ? 2 : 4;
+        const bool vec = Cin % 8 == 0 && pv_aligned16(x) && pv_aligned16(w) &&
+                         ((size_t)x_ld * esz) % 16 == 0;
+        const unsigned blocks = (unsigned)(((long)M * Cout + 3) / 4);
+#define PV_ROWS(XT, V)                                                                         \
+    hipLaunchKernelGGL((pv_point_mlp_rows_kernel<XT, V>), dim3(blocks), dim3(256), 0, s,       \
+                       (const XT*)x, x_ld, M, Cin, Cout, (const uint16_t*)w, bn, act, slope, cb, \
+                       ppc, res, res_ld, out, (int)out_bf16, out_ld)
+        if (x_bf16) {
+            if (vec) PV_ROWS(uint16_t, true); else PV_ROWS(uint16_t, false);
+        } else {
+            if (vec) PV_ROWS(float, true); else PV_ROWS(float, false);
+        }
+#undef PV_ROWS
+        return pv_launch_status();
+    }
     if (bf16) {
         const size_t esz = x_bf16 ? 2 : 4;
         const bool vec = Cin % 8 == 0 && pv_aligned16(x) && pv_aligned16(w) &&
@@ -369,6 +728,16 @@ pvconv_status pv_launch_point_mlp(const void* x, bool x_bf16, int x_ld, int M, i
             vec && Cout % 4 == 0 && (!res || (pv_aligned16(res) && res_ld % 4 == 0)) &&
             (!cb || pv_aligned16(cb)) && out_ld % 4 == 0 &&
             ((uintptr_t)out & (out_bf16 ? 7u : 15u)) == 0;
+        // wide layers: LDS-tiled GEMM, 128-channel x 256-point tiles
+        if (tile && Cin >= 128 && Cout >= 128) {
+            if (x_bf16)
+                launch_lds<4, 2, 1, 4, uint16_t>(x, x_ld, M, Cin, Cout, w, bn, act, slope, cb, ppc,
+                                                 res, res_ld, out, out_bf16, out_ld, s);
+            else
+                launch_lds<4, 2, 1, 4, float>(x, x_ld, M, Cin, Cout, w, bn, act, slope, cb, ppc,
+                                              res, res_ld, out, out_bf16, out_ld, s);
+            return pv_launch_status();
+        }
         if (x_bf16) {
             if (Cout > 64)
                 launch_mfma<4, uint16_t>(x, x_ld, M, Cin, Cout, w, vec, tile, bn, act, slope, cb,
@@ -402,12 +771,28 @@ pvconv_status pv_launch_point_mlp(const void* x, bool x_bf16, int x_ld, int M, i
 pvconv_status pv_launch_maxpool(const void* x, bool bf16, int x_ld, int B, int N, int C,
                                 float* out, hipStream_t s) {
     if (B == 0) return PVCONV_OK;
-    dim3 g((C + 63) / 64, B);
-    if (bf16)
-        hipLaunchKernelGGL(pv_maxpool_kernel<uint16_t>, g, dim3(256), 0, s, (const uint16_t*)x,
-                           x_ld, N, C, out);
-    else
-        hipLaunchKernelGGL(pv_maxpool_kernel<float>, g, dim3(256), 0, s, (const float*)x, x_ld,
-                           N, C, out);
+    const int n = B * C;
+    hipLaunchKernelGGL(pv_fill_f32_kernel, dim3((n + 255) / 256), dim3(256), 0, s, out, n,
+                       -INFINITY);
+    const unsigned slices = (unsigned)((N + kPoolPts - 1) / kPoolPts);
+    const size_t esz = bf16 ? 2 : 4;
+    const bool vec = C % 8 == 0 && pv_aligned16(x) && ((size_t)x_ld * esz) % 16 == 0;
+    if (vec) {
+        dim3 g((C + 511) / 512, B, slices);
+        if (bf16)
+            hipLaunchKernelGGL(pv_maxpool_vec_kernel<uint16_t>, g, dim3(256), 0, s,
+                               (const uint16_t*)x, x_ld, N, C, out);
+        else
+            hipLaunchKernelGGL(pv_maxpool_vec_kernel<float>, g, dim3(256), 0, s, (const float*)x,
+                               x_ld, N, C, out);
+    } else {
+        dim3 g((C + 255) / 256, B, slices);
+        if (bf16)
+            hipLaunchKernelGGL(pv_maxpool_scalar_kernel<uint16_t>, g, dim3(256), 0, s,
+                               (const uint16_t*)x, x_ld, N, C, out);
+        else
+            hipLaunchKernelGGL(pv_maxpool_scalar_kernel<float>, g, dim3(256), 0, s,
+                               (const float*)x, x_ld, N, C, out);
+    }
     return pv_launch_status();
 }

@@ -273,6 +273,12 @@ MLP_CASES = [
     (777, 96, 100, "bf16", True, True, "leaky", True, 0),     # ragged K chunk, N and M tails
     (1500, 40, 36, "bf16", False, True, "relu", True, 500),   # ragged K step, 3 clouds
     (2500, 128, 260, "f32", True, True, "relu", True, 0),     # fp32 rows, 3 channel blocks
+    (3000, 200, 136, "bf16", True, True, "leaky", True, 0),   # wide: ragged K chunk and tiles
+    (16384, 512, 2048, "bf16", False, True, "relu", False, 0),  # wide: part-seg MLP 512->2048
+    (4100, 2880, 256, "bf16", False, True, "relu", False, 2050),  # wide: head with cloud rows
+    (8, 2048, 256, "f32", False, False, "none", False, 0),    # one row per cloud (global)
+    (100, 72, 36, "bf16", True, True, "leaky", True, 50),     # few rows, 2 clouds
+    (37, 9, 5, "bf16", True, True, "relu", True, 0),          # few rows, odd widths
 ]
 
 
@@ -336,16 +342,26 @@ def test_point_mlp_f32_matches_oracle(M, Cin, Cout):
     assert_dot_f32(host(out), ref, mag, "mlp fp32")
 
 
-@pytest.mark.parametrize("dt", ["f32", "bf16"])
-def test_maxpool_matches_oracle(dt):
-    rng = np.random.default_rng(5)
-    x = rng.normal(size=(8, 2048, 2600)).astype(np.float32).astype(np.float64)
+@pytest.mark.parametrize("dt,off,C,N,shift", [
+    ("f32", 300, 2048, 2048, 0.0),    # 16-byte rows: vector path
+    ("bf16", 304, 2048, 2048, 0.0),
+    ("bf16", 300, 2048, 2048, 0.0),   # unaligned rows: scalar path
+    ("bf16", 8, 520, 333, 0.0),       # partial channel group, ragged point slice
+    ("f32", 0, 13, 1000, 0.0),
+    ("f32", 16, 1024, 700, -50.0),    # all negative
+    ("bf16", 0, 64, 1, 0.0),          # one point
+])
+def test_maxpool_matches_oracle(dt, off, C, N, shift):
+    rng = np.random.default_rng(5 + C + N)
+    x = (rng.normal(size=(8, N, off + C + 7)) + shift).astype(np.float32).astype(np.float64)
     if dt == "bf16":
         x = bf16_round(x)
-    ref = oracle.maxpool(x[:, :, 300:2348])
+    ref = oracle.maxpool(x[:, :, off:off + C])
     xd = dev(x, torch.bfloat16 if dt == "bf16" else torch.float32)
-    out = pv.pvconv_maxpool(xd[:, :, 300:2348])
+    out = pv.pvconv_maxpool(xd[:, :, off:off + C])
     assert np.array_equal(host(out), ref)
+    again = pv.pvconv_maxpool(xd[:, :, off:off + C], out=out)   # reused output starts over
+    assert np.array_equal(host(again), ref)
 
 
 # ----------------------------------------------------------------------------
