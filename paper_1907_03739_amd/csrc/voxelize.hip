@@ -8,17 +8,17 @@
 //      recompute the cloud's parameters from registers. Larger clouds: four
 //      short kernels (abs-max, fixed-point sum, radius, points) that pass
 //      per-workgroup partial results through the workspace.
-//      The same launch zeroes the whole grid with streaming 16-byte stores
-//      (extra workgroups), so the empty voxels (most of the grid) cost one
-//      pure write stream.
 //   2. tile fill: one workgroup per (cloud, tile of TV voxels) collects the
 //      points that fall in its tile, counting-sorts them by voxel in LDS,
-//      writes the tile's counts and overwrites the rows of its occupied
-//      voxels with the mean of their features (fp64 sums). Voxels holding
+//      writes the tile's counts, zero rows for its empty voxels and, for the
+//      occupied ones, the mean of their features (fp64 sums). Voxels holding
 //      many points are summed by a whole wave with the points split across
 //      lanes, so a heavily collided cloud costs a few extra rounds of loads.
-// No global atomics; each occupied row is written twice (zero, then mean),
-// every other element once.
+//      Barriers order LDS only, so the grid rows stream out while the
+//      workgroup works on.
+// No global atomics; with 16-byte grid rows every grid element is written
+// once. Otherwise the normalisation launch first zeroes the grid (extra
+// workgroups) and the tile fill overwrites the occupied rows.
 #include <algorithm>
 
 #include "pv_common.h"
@@ -28,7 +28,6 @@ namespace {
 constexpr int kNormPts = 1024;      // points per workgroup, large-cloud normalisation
 constexpr int kNormThreads = 256;
 constexpr int kSmallMaxN = 4096;    // largest cloud normalised by one kernel
-constexpr int kTileThreads = 256;
 constexpr int kHeavy = 32;          // voxels with more points are summed by a whole wave
 constexpr int kMaxCap = 8192;       // tile points kept in LDS at once
 
@@ -98,6 +97,19 @@ __device__ __forceinline__ void write_point(int32_t* vox_id, float* norm_coords,
 }
 
 // ---------------------------------------------------------------------------
+// Workgroup barrier for LDS data only. Every barrier in this file hands LDS
+// data between threads; no thread reads global memory another thread of the
+// workgroup wrote. So the barrier orders LDS accesses alone and does not wait
+// for outstanding global stores (which __syncthreads() would), letting grid
+// rows stream out while the workgroup carries on.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// ---------------------------------------------------------------------------
 // Workgroup reductions and scans (wave64).
 // ---------------------------------------------------------------------------
 template <typename T, typename Op>
@@ -122,14 +134,14 @@ __device__ void block_reduce_k(T (&v)[K], Op op, T* lds) {
     if ((threadIdx.x & 63) == 0)
 #pragma unroll
         for (int i = 0; i < K; i++) lds[i * (NT / 64) + w] = v[i];
-    __syncthreads();
+    lds_barrier();
 #pragma unroll
     for (int i = 0; i < K; i++) {
         T r = lds[i * (NT / 64)];
         for (int j = 1; j < NT / 64; j++) r = op(r, lds[i * (NT / 64) + j]);
         v[i] = r;
     }
-    __syncthreads();
+    lds_barrier();
 }
 
 // Exclusive scan of one int per thread over the workgroup; also returns the total.
@@ -141,9 +153,9 @@ __device__ int block_exclusive_scan(int v, int* lds /* NT/64 */, int& total) {
         int t = __shfl_up(incl, o, 64);
         if (lane >= o) incl += t;
     }
-    __syncthreads();
+    lds_barrier();
     if (lane == 63) lds[w] = incl;
-    __syncthreads();
+    lds_barrier();
     int before = 0;
     total = 0;
     for (int i = 0; i < NT / 64; i++) {
@@ -151,7 +163,7 @@ __device__ int block_exclusive_scan(int v, int* lds /* NT/64 */, int& total) {
         if (i < w) before += s;
         total += s;
     }
-    __syncthreads();
+    lds_barrier();
     return before + incl - v;
 }
 
@@ -431,7 +443,8 @@ __device__ __forceinline__ void sum8(const FT* fb, int feat_ld, int col, const i
 // heavy-voxel reduction (also the fp64 accumulators of a voxel holding more
 // than CAP points).
 // ---------------------------------------------------------------------------
-constexpr int kRedBytes = kTileThreads * 8 * (int)sizeof(double);  // 16 KB
+// heavy-voxel reduction buffer: 8 doubles per thread
+constexpr int red_bytes(int NT) { return NT * 8 * (int)sizeof(double); }
 
 struct TileLds {
     int* hist;
@@ -445,9 +458,9 @@ struct TileLds {
     float* stage;
 };
 
-size_t tile_lds_bytes(int TV, int CAP, int stage_bytes) {
+size_t tile_lds_bytes(int NT, int TV, int CAP, int stage_bytes) {
     return (size_t)(4 * TV + 1) * 4 + (size_t)3 * CAP * 4 + 16 /* align */ +
-           (size_t)(stage_bytes > kRedBytes ? stage_bytes : kRedBytes);
+           (size_t)(stage_bytes > red_bytes(NT) ? stage_bytes : red_bytes(NT));
 }
 
 __device__ inline TileLds tile_lds(char* smem, int TV, int CAP) {
@@ -476,12 +489,15 @@ __device__ inline TileLds tile_lds(char* smem, int TV, int CAP) {
 //    global memory; heavier voxels are then taken one at a time by the whole
 //    workgroup, the points split across threads;
 //  * not VEC: one (voxel, channel) item per thread, straight from memory.
-template <typename FT, typename GT, bool VEC>
+// last: no LDS reuse follows, so the closing barriers are skipped.
+// side(): other stores of the workgroup (the empty rows), issued once this
+// range's first feature loads are in flight so that they queue behind them.
+template <int NT, typename FT, typename GT, bool VEC, typename Side>
 __device__ void tile_fill_range(const TileLds& L, int lo, int hi, int base, const FT* fb,
-                                int feat_ld, int C, GT* out, int* s_nheavy, int stage_bytes) {
-    constexpr int NT = kTileThreads;
+                                int feat_ld, int C, GT* out, int* s_nheavy, int stage_bytes,
+                                bool last, Side side) {
     if (threadIdx.x == 0) *s_nheavy = 0;
-    __syncthreads();
+    lds_barrier();
     if (VEC) {
         const int gpv = C / 8;  // 8-channel groups per voxel
         const int items = (hi - lo) * gpv;
@@ -489,6 +505,7 @@ __device__ void tile_fill_range(const TileLds& L, int lo, int hi, int base, cons
         if ((size_t)npts * C * 4 <= (size_t)stage_bytes) {
             // stage: row j (list order) = the features of point list[j]
             const int pieces = npts * gpv;
+            bool sided = false;
             for (int i0 = threadIdx.x; i0 < pieces; i0 += 4 * NT) {
                 float f[4][8];
 #pragma unroll
@@ -498,6 +515,10 @@ __device__ void tile_fill_range(const TileLds& L, int lo, int hi, int base, cons
                         const int j = i / gpv, cg = i - j * gpv;
                         load8f<FT>(fb + (size_t)L.list[j] * feat_ld + cg * 8, f[u]);
                     }
+                }
+                if (!sided) {
+                    side();
+                    sided = true;
                 }
 #pragma unroll
                 for (int u = 0; u < 4; u++) {
@@ -509,7 +530,8 @@ __device__ void tile_fill_range(const TileLds& L, int lo, int hi, int base, cons
                     }
                 }
             }
-            __syncthreads();
+            if (!sided) side();
+            lds_barrier();
             for (int item = threadIdx.x; item < items; item += NT) {
                 const int vi = lo + item / gpv, cg = item % gpv;
                 const int nk = L.hist[vi];
@@ -529,28 +551,41 @@ __device__ void tile_fill_range(const TileLds& L, int lo, int hi, int base, cons
                 }
                 store8<GT>(out + (size_t)vi * C + cg * 8, mean);
             }
-            __syncthreads();
+            if (!last) lds_barrier();
             return;
         }
-        for (int item = threadIdx.x; item < items; item += NT) {
-            const int vi = lo + item / gpv, cg = item % gpv;
+        // Occupied voxels: light ones listed in occ (L.cur, free once the
+        // points are sorted) so that the (voxel, channel group) items are
+        // spread evenly over the threads, heavy ones for the wave loop.
+        __shared__ int s_nocc;
+        int* occ = L.cur;
+        if (threadIdx.x == 0) s_nocc = 0;
+        lds_barrier();
+        for (int vi = lo + threadIdx.x; vi < hi; vi += NT) {
             const int nk = L.hist[vi];
-            if (nk == 0) continue;  // empty voxel: its row is already zero
+            if (nk == 0) continue;  // empty voxel: a zero row
+            if (nk > kHeavy)
+                L.heavy[atomicAdd(s_nheavy, 1)] = vi;
+            else
+                occ[atomicAdd(&s_nocc, 1)] = vi;
+        }
+        lds_barrier();
+        const int nocc = s_nocc;
+        for (int item = threadIdx.x; item < nocc * gpv; item += NT) {
+            const int vi = occ[item / gpv], cg = item % gpv;
+            const int nk = L.hist[vi];
+            double acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+            const int j0 = L.start[vi] - base;
+            sum8<FT>(fb, feat_ld, cg * 8, L.list, j0, j0 + nk, 1, acc);
             float mean[8];
-            if (nk > kHeavy) {
-                if (cg == 0) L.heavy[atomicAdd(s_nheavy, 1)] = vi;
-                continue;
-            }
-            {
-                double acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-                const int j0 = L.start[vi] - base;
-                sum8<FT>(fb, feat_ld, cg * 8, L.list, j0, j0 + nk, 1, acc);
 #pragma unroll
-                for (int i = 0; i < 8; i++) mean[i] = (float)(acc[i] / (double)nk);
-            }
+            for (int i = 0; i < 8; i++) mean[i] = (float)(acc[i] / (double)nk);
             store8<GT>(out + (size_t)vi * C + cg * 8, mean);
         }
-        __syncthreads();
+        // after this thread's gathers: loads issued after the zero stores
+        // would wait for them (one counter tracks both, in issue order)
+        side();
+        lds_barrier();
         // Heavy voxels: one per wave, four at a time. For channel groups cg0 ..
         // cg0+ng-1, lane = sub * ng + (cg - cg0) sums points j = sub, sub+S,
         // ... (S = 64 / ng subsets); the S partial sums are then combined in
@@ -574,7 +609,7 @@ __device__ void tile_fill_range(const TileLds& L, int lo, int hi, int base, cons
                 if (sub < S)
 #pragma unroll
                     for (int i = 0; i < 8; i++) red[(sub * ng + cl) * 8 + i] = acc[i];
-                __syncthreads();
+                lds_barrier();
                 if (active && lane < ng) {
                     double tot[8];
 #pragma unroll
@@ -587,10 +622,11 @@ __device__ void tile_fill_range(const TileLds& L, int lo, int hi, int base, cons
                     for (int i = 0; i < 8; i++) mean[i] = (float)(tot[i] / (double)nk);
                     store8<GT>(out + (size_t)vi * C + (cg0 + lane) * 8, mean);
                 }
-                __syncthreads();
+                lds_barrier();
             }
         }
     } else {
+        side();
         const int items = (hi - lo) * C;
         for (int item = threadIdx.x; item < items; item += NT) {
             const int vi = lo + item / C, ch = item % C;
@@ -603,7 +639,7 @@ __device__ void tile_fill_range(const TileLds& L, int lo, int hi, int base, cons
             store1<GT>(out + (size_t)vi * C + ch, (float)(acc / (double)nk));
         }
     }
-    __syncthreads();
+    if (!last) lds_barrier();
 }
 
 // The tile's points among ids[0 .. N): count per voxel and keep (index,
@@ -621,11 +657,11 @@ __device__ __forceinline__ void tile_collect_one(const TileLds& L, int k, int r,
     }
 }
 
-template <typename FT, typename GT, bool VEC>
-__global__ __launch_bounds__(kTileThreads) void pv_voxel_tile_kernel(
+template <int NT, typename FT, typename GT, bool VEC>
+__global__ __launch_bounds__(NT) void pv_voxel_tile_kernel(
     const int32_t* __restrict__ vox_id, const FT* __restrict__ feats, int feat_ld, int N, int C,
-    int R, int TV, int CAP, int stage_bytes, GT* __restrict__ grid, int32_t* __restrict__ counts) {
-    constexpr int NT = kTileThreads;
+    int R, int TV, int CAP, int stage_bytes, int zero_rows, GT* __restrict__ grid,
+    int32_t* __restrict__ counts) {
     extern __shared__ __attribute__((aligned(16))) char smem[];
     __shared__ int scan_lds[NT / 64];
     __shared__ int s_ntile, s_nheavy;
@@ -640,7 +676,7 @@ __global__ __launch_bounds__(kTileThreads) void pv_voxel_tile_kernel(
 
     for (int i = threadIdx.x; i < TV; i += NT) L.hist[i] = 0;
     if (threadIdx.x == 0) s_ntile = 0;
-    __syncthreads();
+    lds_barrier();
     // 1. the tile's points
     int k0 = 0;
     if (((uintptr_t)ids & 15) == 0) {
@@ -666,10 +702,20 @@ __global__ __launch_bounds__(kTileThreads) void pv_voxel_tile_kernel(
         k0 = n16;
     }
     for (int k = k0 + threadIdx.x; k < N; k += NT) tile_collect_one(L, k, ids[k] - v0, nv, CAP, &s_ntile);
-    __syncthreads();
+    lds_barrier();
     // 2. counts out; exclusive prefix over the tile's voxels
     int32_t* cnt = counts + (size_t)b * V + v0;
     for (int i = threadIdx.x; i < nv; i += NT) cnt[i] = L.hist[i];
+    // The tile's empty voxels: zero rows (16-byte stores), streaming out
+    // while the occupied voxels are gathered.
+    auto zero_empty_rows = [&]() {
+        if (!VEC || !zero_rows) return;
+        const int pr = C * (int)sizeof(GT) / 16;  // 16-byte pieces per row
+        uint4* o16 = (uint4*)out;
+        for (int i = threadIdx.x; i < nv * pr; i += NT)
+            if (L.hist[i / pr] == 0) o16[i] = make_uint4(0u, 0u, 0u, 0u);
+    };
+    auto nothing = []() {};
     {
         const int seg = (TV + NT - 1) / NT;
         const int s0 = min(TV, (int)threadIdx.x * seg), s1 = min(TV, s0 + seg);
@@ -683,18 +729,20 @@ __global__ __launch_bounds__(kTileThreads) void pv_voxel_tile_kernel(
         }
         if (threadIdx.x == 0) L.start[TV] = total;
     }
-    __syncthreads();
+    lds_barrier();
     const int total = L.start[TV];
     if (total <= CAP) {
         // 3. counting sort of the kept points by voxel, then the fill
         for (int i = threadIdx.x; i < nv; i += NT) L.cur[i] = L.start[i];
-        __syncthreads();
+        lds_barrier();
         for (int s = threadIdx.x; s < total; s += NT)
             L.list[atomicAdd(&L.cur[L.rbuf[s]], 1)] = L.kbuf[s];
-        __syncthreads();
-        tile_fill_range<FT, GT, VEC>(L, 0, nv, 0, fb, feat_ld, C, out, &s_nheavy, stage_bytes);
+        lds_barrier();
+        tile_fill_range<NT, FT, GT, VEC>(L, 0, nv, 0, fb, feat_ld, C, out, &s_nheavy, stage_bytes,
+                                         true, zero_empty_rows);
         return;
     }
+    zero_empty_rows();
     // More points than fit: voxel segments of at most CAP points, each
     // gathered by scanning the ids again. A single voxel beyond CAP points is
     // summed by the whole workgroup with LDS fp64 atomics.
@@ -704,15 +752,15 @@ __global__ __launch_bounds__(kTileThreads) void pv_voxel_tile_kernel(
             const int nk = L.start[lo + 1] - L.start[lo];
             double* hacc = L.red;  // C <= 1024 doubles fit in red[] (16 KB)
             for (int ch = threadIdx.x; ch < C; ch += NT) hacc[ch] = 0.0;
-            __syncthreads();
+            lds_barrier();
             for (int k = threadIdx.x; k < N; k += NT)
                 if (ids[k] == v0 + lo)
                     for (int ch = 0; ch < C; ch++)
                         atomicAdd(&hacc[ch], (double)load1<FT>(fb + (size_t)k * feat_ld + ch));
-            __syncthreads();
+            lds_barrier();
             for (int ch = threadIdx.x; ch < C; ch += NT)
                 store1<GT>(out + (size_t)lo * C + ch, (float)(hacc[ch] / (double)nk));
-            __syncthreads();
+            lds_barrier();
             lo++;
             continue;
         }
@@ -727,13 +775,14 @@ __global__ __launch_bounds__(kTileThreads) void pv_voxel_tile_kernel(
         }
         const int hi = a, base = L.start[lo];
         for (int i = lo + threadIdx.x; i < hi; i += NT) L.cur[i] = L.start[i] - base;
-        __syncthreads();
+        lds_barrier();
         for (int k = threadIdx.x; k < N; k += NT) {
             const int r = ids[k] - v0;
             if (r >= lo && r < hi) L.list[atomicAdd(&L.cur[r], 1)] = k;
         }
-        __syncthreads();
-        tile_fill_range<FT, GT, VEC>(L, lo, hi, base, fb, feat_ld, C, out, &s_nheavy, stage_bytes);
+        lds_barrier();
+        tile_fill_range<NT, FT, GT, VEC>(L, lo, hi, base, fb, feat_ld, C, out, &s_nheavy, stage_bytes,
+                                         false, nothing);
         lo = hi;
     }
 }
@@ -741,62 +790,85 @@ __global__ __launch_bounds__(kTileThreads) void pv_voxel_tile_kernel(
 // Tile size: small clouds (every tile scans all N ids, cheap) aim for about
 // 2048 workgroups so each tile's points fit the feature stage; large clouds
 // aim for 256 (one per CU) to bound the id scans.
-int tile_voxels(int B, int V, int N) {
-    const long long want = N <= kSmallMaxN ? 2048 : 256;
+// Tile shape. Small clouds (every tile scans all N ids, cheap): about 2048
+// tiles of 128 threads and no feature stage (each (voxel, channel group) sums
+// straight from memory), about 15 KB of LDS, so that eight workgroups fit per
+// CU and every tile is resident at once. Large clouds: about 256 tiles (one
+// per CU) of 256 threads to bound the id scans.
+struct TileShape {
+    int nt, tv;
+};
+TileShape tile_shape(int B, int V, int N) {
+    const bool small_cloud = N <= kSmallMaxN;
+    const long long want = small_cloud ? 2048 : 256;
     int tv = 1024;
     while (tv > 128 && (long long)B * ((V + tv - 1) / tv) < want) tv >>= 1;
-    return tv;
+    return TileShape{small_cloud ? 128 : 256, tv};
 }
 
 constexpr int kStageBytes = 48 * 1024;
 constexpr size_t kLdsMax = 160 * 1024;  // gfx950 LDS per workgroup
 
-// LDS budget of the tile kernel. Small clouds: room for 256 points and a
-// 32 KB feature stage (tiles beyond either take the segmented or unstaged
-// path, rare for small clouds), so several workgroups fit per CU. Large clouds: capacity for kMaxCap points and as much of the
-// stage as the 160 KB LDS leaves. Dynamic LDS beyond 64 KB has to be granted
-// per kernel; when that fails both shrink to what 64 KB holds (tiles with
-// more points then take the unstaged or segmented paths).
+// LDS budget of the tile kernel. Small clouds: room for 256 points, no
+// feature stage (tiles with more points take the segmented path, rare for
+// small clouds). Large clouds: capacity
+// for kMaxCap points and as much of the stage as the 160 KB LDS leaves.
+// Dynamic LDS beyond 64 KB has to be granted per kernel; when that fails
+// both shrink to what 64 KB holds (tiles with more points then take the
+// unstaged or segmented paths).
 template <typename K>
-void tile_budget(K kernel, int TV, int N, int& cap, int& stage) {
+void tile_budget(K kernel, int NT, int TV, int N, int& cap, int& stage) {
     const bool small_cloud = N <= kSmallMaxN;
     const int want = small_cloud ? 256 : kMaxCap;
     cap = N < want ? (N > 0 ? N : 1) : want;
     if (small_cloud) {
-        stage = 32 * 1024;
+        stage = 0;
     } else {
-        const size_t rest = tile_lds_bytes(TV, cap, 0) - kRedBytes;
+        const size_t rest = tile_lds_bytes(NT, TV, cap, 0) - red_bytes(NT);
         stage = (int)std::min<size_t>(kStageBytes, kLdsMax - rest) & ~15;
-        if (stage < kRedBytes) stage = 0;
+        if (stage < red_bytes(NT)) stage = 0;
     }
     const size_t small = 65536;
-    if (tile_lds_bytes(TV, cap, stage) <= small) return;
+    if (tile_lds_bytes(NT, TV, cap, stage) <= small) return;
     if (hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)tile_lds_bytes(TV, cap, stage)) == hipSuccess)
+                            (int)tile_lds_bytes(NT, TV, cap, stage)) == hipSuccess)
         return;
     (void)hipGetLastError();
     stage = 0;
-    while (cap > 1 && tile_lds_bytes(TV, cap, stage) > small) cap >>= 1;
+    while (cap > 1 && tile_lds_bytes(NT, TV, cap, stage) > small) cap >>= 1;
+}
+
+template <int NT, typename FT, typename GT>
+void launch_tiles_nt(const int32_t* ids, const void* feats, int feat_ld, int B, int N, int C,
+                     int R, int TV, void* grid, int32_t* counts, bool vec, bool zero_rows,
+                     hipStream_t s) {
+    const int V = R * R * R;
+    dim3 g((V + TV - 1) / TV, B);
+    int cap, stage;
+    if (vec) {
+        auto k = pv_voxel_tile_kernel<NT, FT, GT, true>;
+        tile_budget(k, NT, TV, N, cap, stage);
+        hipLaunchKernelGGL(k, g, dim3(NT), tile_lds_bytes(NT, TV, cap, stage), s, ids,
+                           (const FT*)feats, feat_ld, N, C, R, TV, cap, stage, (int)zero_rows,
+                           (GT*)grid, counts);
+    } else {
+        auto k = pv_voxel_tile_kernel<NT, FT, GT, false>;
+        tile_budget(k, NT, TV, N, cap, stage);
+        hipLaunchKernelGGL(k, g, dim3(NT), tile_lds_bytes(NT, TV, cap, stage), s, ids,
+                           (const FT*)feats, feat_ld, N, C, R, TV, cap, 0, 0, (GT*)grid, counts);
+    }
 }
 
 template <typename FT, typename GT>
 void launch_tiles(const int32_t* ids, const void* feats, int feat_ld, int B, int N, int C, int R,
-                  void* grid, int32_t* counts, bool vec, hipStream_t s) {
-    const int V = R * R * R;
-    const int TV = tile_voxels(B, V, N);
-    dim3 g((V + TV - 1) / TV, B);
-    int cap, stage;
-    if (vec) {
-        auto k = pv_voxel_tile_kernel<FT, GT, true>;
-        tile_budget(k, TV, N, cap, stage);
-        hipLaunchKernelGGL(k, g, dim3(kTileThreads), tile_lds_bytes(TV, cap, stage), s, ids,
-                           (const FT*)feats, feat_ld, N, C, R, TV, cap, stage, (GT*)grid, counts);
-    } else {
-        auto k = pv_voxel_tile_kernel<FT, GT, false>;
-        tile_budget(k, TV, N, cap, stage);
-        hipLaunchKernelGGL(k, g, dim3(kTileThreads), tile_lds_bytes(TV, cap, stage), s, ids,
-                           (const FT*)feats, feat_ld, N, C, R, TV, cap, 0, (GT*)grid, counts);
-    }
+                  void* grid, int32_t* counts, bool vec, bool zero_rows, hipStream_t s) {
+    const TileShape t = tile_shape(B, R * R * R, N);
+    if (t.nt == 128)
+        launch_tiles_nt<128, FT, GT>(ids, feats, feat_ld, B, N, C, R, t.tv, grid, counts, vec,
+                                     zero_rows, s);
+    else
+        launch_tiles_nt<256, FT, GT>(ids, feats, feat_ld, B, N, C, R, t.tv, grid, counts, vec,
+                                     zero_rows, s);
 }
 
 // Zero fill byte by byte, for grids the 16-byte path cannot cover.
@@ -848,16 +920,21 @@ pvconv_status pv_launch_voxelize(const float* coords, const void* feats, bool fe
     VoxWs w = carve_ws(ws, B, N);
     int32_t* ids = vox_id ? vox_id : w.ids;
     float* pn = norm_coords ? norm_coords : w.pnorm;
-    // zero the grid (16-byte stores) alongside the normalisation
-    const size_t gbytes = (size_t)B * R * R * R * C * (grid_bf16 ? 2 : 4);
+    // Rows of empty voxels are zero. With 16-byte rows the tile kernel writes
+    // them itself (each grid row is then written exactly once); otherwise the
+    // grid is zeroed first, alongside the normalisation, and the tile kernel
+    // overwrites the occupied rows.
+    const size_t esz_f = feat_bf16 ? 2 : 4, esz_g = grid_bf16 ? 2 : 4;
+    const bool vec = (C % 8 == 0) && pv_aligned16(feats) && pv_aligned16(grid) &&
+                     ((size_t)feat_ld * esz_f) % 16 == 0 && ((size_t)C * esz_g) % 16 == 0;
+    const size_t gbytes = (size_t)B * R * R * R * C * esz_g;
     const size_t n16 = gbytes / 16;
-    const int zero_blocks = (int)std::min<size_t>(2048, (n16 + 4095) / 4096);
-    uint4* grid16 = (uint4*)grid;
     const bool grid_ok = pv_aligned16(grid) && gbytes % 16 == 0;
+    const int zb = (grid_ok && !vec) ? (int)std::min<size_t>(2048, (n16 + 4095) / 4096) : 0;
+    uint4* grid16 = (uint4*)grid;
     if (N <= kSmallMaxN) {
         const int slices = (N + 255) / 256;
         const int nid = slices * B;
-        const int zb = grid_ok ? zero_blocks : 0;
         if (nid + zb > 0) {
             const dim3 gi(nid + zb);
             if (N <= 1024)
@@ -872,7 +949,6 @@ pvconv_status pv_launch_voxelize(const float* coords, const void* feats, bool fe
         }
     } else {
         const int nid = w.split.G * B;
-        const int zb = grid_ok ? zero_blocks : 0;
         dim3 g(w.split.G, B);
         hipLaunchKernelGGL(pv_norm_absmax_kernel, dim3(nid + zb), dim3(kNormThreads), 0, s,
                            coords, N, w.split, B, grid16, n16);
@@ -885,19 +961,19 @@ pvconv_status pv_launch_voxelize(const float* coords, const void* feats, bool fe
         // a grid that 16-byte stores cannot cover: the plain element kernel
         hipLaunchKernelGGL(pv_zero_elems_kernel, dim3(1024), dim3(256), 0, s, (char*)grid, gbytes);
     }
-    const size_t esz_f = feat_bf16 ? 2 : 4, esz_g = grid_bf16 ? 2 : 4;
-    const bool vec = (C % 8 == 0) && pv_aligned16(feats) && pv_aligned16(grid) &&
-                     ((size_t)feat_ld * esz_f) % 16 == 0 && ((size_t)C * esz_g) % 16 == 0;
     if (feat_bf16) {
         if (grid_bf16)
-            launch_tiles<uint16_t, uint16_t>(ids, feats, feat_ld, B, N, C, R, grid, counts, vec, s);
+            launch_tiles<uint16_t, uint16_t>(ids, feats, feat_ld, B, N, C, R, grid, counts, vec,
+                                             vec, s);
         else
-            launch_tiles<uint16_t, float>(ids, feats, feat_ld, B, N, C, R, grid, counts, vec, s);
+            launch_tiles<uint16_t, float>(ids, feats, feat_ld, B, N, C, R, grid, counts, vec, vec,
+                                          s);
     } else {
         if (grid_bf16)
-            launch_tiles<float, uint16_t>(ids, feats, feat_ld, B, N, C, R, grid, counts, vec, s);
+            launch_tiles<float, uint16_t>(ids, feats, feat_ld, B, N, C, R, grid, counts, vec, vec,
+                                          s);
         else
-            launch_tiles<float, float>(ids, feats, feat_ld, B, N, C, R, grid, counts, vec, s);
+            launch_tiles<float, float>(ids, feats, feat_ld, B, N, C, R, grid, counts, vec, vec, s);
     }
     return pv_launch_status();
 }
