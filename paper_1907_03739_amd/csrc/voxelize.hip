@@ -29,7 +29,7 @@ constexpr int kNormPts = 1024;      // points per workgroup, large-cloud normali
 constexpr int kNormThreads = 256;
 constexpr int kSmallMaxN = 4096;    // largest cloud normalised by one kernel
 constexpr int kHeavy = 32;          // voxels with more points are summed by a whole wave
-constexpr int kMaxCap = 8192;       // tile points kept in LDS at once
+constexpr int kMaxCap = 4096;       // tile points kept in LDS at once
 
 // ---------------------------------------------------------------------------
 // Normalisation arithmetic. IEEE fp64, round to nearest even, no contraction,
@@ -262,6 +262,17 @@ struct SplitWs {
     long long* pQ;
     double* pM;
     int G;
+    // points bucketed by tile: tcount [B][T] points per tile, tcursor [B][T]
+    // fill cursors, tstart [B][T] bucket offsets, bk / br [B][N] point index
+    // and voxel within the tile, in tile order (within a tile in no
+    // particular order)
+    int* tcount;
+    int* tcursor;
+    int* tstart;
+    int* bk;
+    int* br;
+    int T;
+    int TV;
 };
 
 __device__ void combine_absmax(const SplitWs& ws, int b, float* redf, float (&A)[3]) {
@@ -293,6 +304,9 @@ __global__ __launch_bounds__(kNormThreads) void pv_norm_absmax_kernel(const floa
         zero_fill_role(grid16, n16, blockIdx.x - nid, gridDim.x - nid);
         return;
     }
+    if (blockIdx.x == 0)  // the tile counters start at zero (used two launches later)
+        for (int i = threadIdx.x; i < 2 * B * ws.T; i += kNormThreads)
+            (i < B * ws.T ? ws.tcount : ws.tcursor)[i % (B * ws.T)] = 0;
     const int g = blockIdx.x % ws.G, b = blockIdx.x / ws.G;
     const float* p = coords + (size_t)b * N * 3;
     const int k0 = g * kNormPts, k1 = min(N, k0 + kNormPts);
@@ -356,10 +370,72 @@ __global__ __launch_bounds__(kNormThreads) void pv_norm_points_kernel(
     const double M2 = mx[0];
     const double m = sqrt(M2);
     const int k0 = g * kNormPts, k1 = min(N, k0 + kNormPts);
+    // points per tile of this slice, LDS first, then one global add per tile
+    extern __shared__ int thist[];  // [T]
+    for (int t = threadIdx.x; t < ws.T; t += kNormThreads) thist[t] = 0;
+    lds_barrier();
     for (int k = k0 + threadIdx.x; k < k1; k += kNormThreads) {
         float pn[3];
         const int id = normalise_point(p + 3 * k, c, M2, m, R, pn);
         write_point(vox_id, norm_coords, (size_t)b * N + k, id, pn);
+        atomicAdd(&thist[id / ws.TV], 1);
+    }
+    lds_barrier();
+    for (int t = threadIdx.x; t < ws.T; t += kNormThreads)
+        if (thist[t]) atomicAdd(&ws.tcount[(size_t)b * ws.T + t], thist[t]);
+}
+
+// Scatter of each point into its tile's bucket: grid (G, B), the same slices
+// as pv_norm_points_kernel. Each workgroup takes the exclusive prefix of the
+// cloud's tile counts, ranks its points per tile in LDS, reserves a range of
+// every tile's bucket with one global add and writes (point, voxel in tile).
+__global__ __launch_bounds__(kNormThreads) void pv_bucket_kernel(const int32_t* __restrict__ ids,
+                                                                 int N, SplitWs ws) {
+    constexpr int NT = kNormThreads;
+    constexpr int PPT = kNormPts / NT;
+    extern __shared__ int bl[];  // pre[T], hist[T]
+    __shared__ int scan_lds[NT / 64];
+    int* pre = bl;
+    int* hist = bl + ws.T;
+    const int g = blockIdx.x, b = blockIdx.y;
+    const int* tc = ws.tcount + (size_t)b * ws.T;
+    {
+        const int seg = (ws.T + NT - 1) / NT;
+        const int s0 = min(ws.T, (int)threadIdx.x * seg), s1 = min(ws.T, s0 + seg);
+        int local = 0;
+        for (int t = s0; t < s1; t++) local += tc[t];
+        int total;
+        int run = block_exclusive_scan<NT>(local, scan_lds, total);
+        for (int t = s0; t < s1; t++) {
+            pre[t] = run;
+            if (g == 0) ws.tstart[(size_t)b * ws.T + t] = run;
+            run += tc[t];
+        }
+        for (int t = threadIdx.x; t < ws.T; t += NT) hist[t] = 0;
+    }
+    lds_barrier();
+    const int k0 = g * kNormPts;
+    int tile[PPT], rank[PPT], vid[PPT];
+#pragma unroll
+    for (int i = 0; i < PPT; i++) {
+        const int k = k0 + i * NT + threadIdx.x;
+        tile[i] = -1;
+        if (k < N) {
+            vid[i] = ids[(size_t)b * N + k];
+            tile[i] = vid[i] / ws.TV;
+            rank[i] = atomicAdd(&hist[tile[i]], 1);
+        }
+    }
+    lds_barrier();
+    for (int t = threadIdx.x; t < ws.T; t += NT)
+        if (hist[t]) pre[t] += atomicAdd(&ws.tcursor[(size_t)b * ws.T + t], hist[t]);
+    lds_barrier();
+#pragma unroll
+    for (int i = 0; i < PPT; i++) {
+        if (tile[i] < 0) continue;
+        const size_t pos = (size_t)b * N + pre[tile[i]] + rank[i];
+        ws.bk[pos] = k0 + i * NT + threadIdx.x;
+        ws.br[pos] = vid[i] - tile[i] * ws.TV;
     }
 }
 
@@ -661,13 +737,17 @@ template <int NT, typename FT, typename GT, bool VEC>
 __global__ __launch_bounds__(NT) void pv_voxel_tile_kernel(
     const int32_t* __restrict__ vox_id, const FT* __restrict__ feats, int feat_ld, int N, int C,
     int R, int TV, int CAP, int stage_bytes, int zero_rows, GT* __restrict__ grid,
-    int32_t* __restrict__ counts) {
+    int32_t* __restrict__ counts, const int* __restrict__ bk, const int* __restrict__ br,
+    const int* __restrict__ tcount, const int* __restrict__ tstart, int T) {
     extern __shared__ __attribute__((aligned(16))) char smem[];
     __shared__ int scan_lds[NT / 64];
     __shared__ int s_ntile, s_nheavy;
     const TileLds L = tile_lds(smem, TV, CAP);
 
     const int t = blockIdx.x, b = blockIdx.y;
+    const bool bucketed = bk != nullptr;
+    const int bstart = bucketed ? tstart[(size_t)b * T + t] : 0;
+    const int btotal = bucketed ? tcount[(size_t)b * T + t] : 0;
     const int V = R * R * R;
     const int v0 = t * TV, nv = min(TV, V - v0);
     const int32_t* ids = vox_id + (size_t)b * N;
@@ -677,31 +757,56 @@ __global__ __launch_bounds__(NT) void pv_voxel_tile_kernel(
     for (int i = threadIdx.x; i < TV; i += NT) L.hist[i] = 0;
     if (threadIdx.x == 0) s_ntile = 0;
     lds_barrier();
-    // 1. the tile's points
-    int k0 = 0;
-    if (((uintptr_t)ids & 15) == 0) {
-        const int n16 = N / 16 * 16;  // rounds of 4 int4 loads per thread
-        for (int kb = threadIdx.x * 4; kb < n16; kb += NT * 16) {
-            int4 q[4];
+    // 1. the tile's points: its bucket when the points were bucketed by tile
+    // (large clouds), else a scan of all the cloud's ids
+    const int* kb = bucketed ? bk + (size_t)b * N + bstart : nullptr;
+    const int* rb = bucketed ? br + (size_t)b * N + bstart : nullptr;
+    // every point of the tile (bucketed) or of the cloud, as (index, voxel - v0)
+    auto each_point = [&](auto fn) {
+        if (bucketed)
+            for (int j = threadIdx.x; j < btotal; j += NT) fn(kb[j], rb[j]);
+        else
+            for (int k = threadIdx.x; k < N; k += NT) fn(k, ids[k] - v0);
+    };
+    if (bucketed) {
+        for (int j0 = threadIdx.x; j0 < btotal; j0 += 4 * NT) {
+            int kk[4], rr[4];
 #pragma unroll
             for (int u = 0; u < 4; u++) {
-                const int k = kb + u * NT * 4;
-                q[u] = k < n16 ? *(const int4*)(ids + k) : make_int4(-1 - v0, 0, 0, 0);
+                const int j = j0 + u * NT;
+                kk[u] = j < btotal ? kb[j] : 0;
+                rr[u] = j < btotal ? rb[j] : -1;
             }
 #pragma unroll
-            for (int u = 0; u < 4; u++) {
-                const int k = kb + u * NT * 4;
-                if (k < n16) {
-                    tile_collect_one(L, k, q[u].x - v0, nv, CAP, &s_ntile);
-                    tile_collect_one(L, k + 1, q[u].y - v0, nv, CAP, &s_ntile);
-                    tile_collect_one(L, k + 2, q[u].z - v0, nv, CAP, &s_ntile);
-                    tile_collect_one(L, k + 3, q[u].w - v0, nv, CAP, &s_ntile);
+            for (int u = 0; u < 4; u++) tile_collect_one(L, kk[u], rr[u], nv, CAP, &s_ntile);
+        }
+    } else {
+        int k0 = 0;
+        if (((uintptr_t)ids & 15) == 0) {
+            const int n16 = N / 16 * 16;  // rounds of 4 int4 loads per thread
+            for (int kq = threadIdx.x * 4; kq < n16; kq += NT * 16) {
+                int4 q[4];
+#pragma unroll
+                for (int u = 0; u < 4; u++) {
+                    const int k = kq + u * NT * 4;
+                    q[u] = k < n16 ? *(const int4*)(ids + k) : make_int4(-1 - v0, 0, 0, 0);
+                }
+#pragma unroll
+                for (int u = 0; u < 4; u++) {
+                    const int k = kq + u * NT * 4;
+                    if (k < n16) {
+                        tile_collect_one(L, k, q[u].x - v0, nv, CAP, &s_ntile);
+                        tile_collect_one(L, k + 1, q[u].y - v0, nv, CAP, &s_ntile);
+                        tile_collect_one(L, k + 2, q[u].z - v0, nv, CAP, &s_ntile);
+                        tile_collect_one(L, k + 3, q[u].w - v0, nv, CAP, &s_ntile);
+                    }
                 }
             }
+            k0 = n16;
         }
-        k0 = n16;
+        for (int k = k0 + threadIdx.x; k < N; k += NT)
+            tile_collect_one(L, k, ids[k] - v0, nv, CAP, &s_ntile);
     }
-    for (int k = k0 + threadIdx.x; k < N; k += NT) tile_collect_one(L, k, ids[k] - v0, nv, CAP, &s_ntile);
     lds_barrier();
     // 2. counts out; exclusive prefix over the tile's voxels
     int32_t* cnt = counts + (size_t)b * V + v0;
@@ -753,10 +858,11 @@ __global__ __launch_bounds__(NT) void pv_voxel_tile_kernel(
             double* hacc = L.red;  // C <= 1024 doubles fit in red[] (16 KB)
             for (int ch = threadIdx.x; ch < C; ch += NT) hacc[ch] = 0.0;
             lds_barrier();
-            for (int k = threadIdx.x; k < N; k += NT)
-                if (ids[k] == v0 + lo)
+            each_point([&](int k, int r) {
+                if (r == lo)
                     for (int ch = 0; ch < C; ch++)
                         atomicAdd(&hacc[ch], (double)load1<FT>(fb + (size_t)k * feat_ld + ch));
+            });
             lds_barrier();
             for (int ch = threadIdx.x; ch < C; ch += NT)
                 store1<GT>(out + (size_t)lo * C + ch, (float)(hacc[ch] / (double)nk));
@@ -776,10 +882,9 @@ __global__ __launch_bounds__(NT) void pv_voxel_tile_kernel(
         const int hi = a, base = L.start[lo];
         for (int i = lo + threadIdx.x; i < hi; i += NT) L.cur[i] = L.start[i] - base;
         lds_barrier();
-        for (int k = threadIdx.x; k < N; k += NT) {
-            const int r = ids[k] - v0;
+        each_point([&](int k, int r) {
             if (r >= lo && r < hi) L.list[atomicAdd(&L.cur[r], 1)] = k;
-        }
+        });
         lds_barrier();
         tile_fill_range<NT, FT, GT, VEC>(L, lo, hi, base, fb, feat_ld, C, out, &s_nheavy, stage_bytes,
                                          false, nothing);
@@ -791,43 +896,33 @@ __global__ __launch_bounds__(NT) void pv_voxel_tile_kernel(
 // 2048 workgroups so each tile's points fit the feature stage; large clouds
 // aim for 256 (one per CU) to bound the id scans.
 // Tile shape. Small clouds (every tile scans all N ids, cheap): about 2048
-// tiles of 128 threads and no feature stage (each (voxel, channel group) sums
-// straight from memory), about 15 KB of LDS, so that eight workgroups fit per
-// CU and every tile is resident at once. Large clouds: about 256 tiles (one
-// per CU) of 256 threads to bound the id scans.
+// tiles of 128 threads, about 15 KB of LDS, so that eight workgroups fit per
+// CU and every tile is resident at once. Large clouds (points bucketed by
+// tile beforehand): about 1024 tiles of 256 threads, so that a dense cluster
+// spreads over several workgroups.
 struct TileShape {
     int nt, tv;
 };
 TileShape tile_shape(int B, int V, int N) {
     const bool small_cloud = N <= kSmallMaxN;
-    const long long want = small_cloud ? 2048 : 256;
+    const long long want = small_cloud ? 2048 : 1024;
     int tv = 1024;
     while (tv > 128 && (long long)B * ((V + tv - 1) / tv) < want) tv >>= 1;
     return TileShape{small_cloud ? 128 : 256, tv};
 }
 
-constexpr int kStageBytes = 48 * 1024;
-constexpr size_t kLdsMax = 160 * 1024;  // gfx950 LDS per workgroup
 
-// LDS budget of the tile kernel. Small clouds: room for 256 points, no
-// feature stage (tiles with more points take the segmented path, rare for
-// small clouds). Large clouds: capacity
-// for kMaxCap points and as much of the stage as the 160 KB LDS leaves.
-// Dynamic LDS beyond 64 KB has to be granted per kernel; when that fails
-// both shrink to what 64 KB holds (tiles with more points then take the
-// unstaged or segmented paths).
+// LDS budget of the tile kernel: room for 256 (small clouds) or kMaxCap
+// (large clouds) points and no feature stage (each (voxel, channel group)
+// sums straight from memory); tiles with more points take the segmented
+// path. Dynamic LDS beyond 64 KB has to be granted per kernel; when that
+// fails the capacity shrinks to what 64 KB holds.
 template <typename K>
 void tile_budget(K kernel, int NT, int TV, int N, int& cap, int& stage) {
     const bool small_cloud = N <= kSmallMaxN;
     const int want = small_cloud ? 256 : kMaxCap;
     cap = N < want ? (N > 0 ? N : 1) : want;
-    if (small_cloud) {
-        stage = 0;
-    } else {
-        const size_t rest = tile_lds_bytes(NT, TV, cap, 0) - red_bytes(NT);
-        stage = (int)std::min<size_t>(kStageBytes, kLdsMax - rest) & ~15;
-        if (stage < red_bytes(NT)) stage = 0;
-    }
+    stage = 0;
     const size_t small = 65536;
     if (tile_lds_bytes(NT, TV, cap, stage) <= small) return;
     if (hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -838,10 +933,20 @@ void tile_budget(K kernel, int NT, int TV, int N, int& cap, int& stage) {
     while (cap > 1 && tile_lds_bytes(NT, TV, cap, stage) > small) cap >>= 1;
 }
 
+// Tiles' point sources: the points bucketed by tile (large clouds) or none
+// (each tile scans all ids).
+struct Buckets {
+    const int* bk;
+    const int* br;
+    const int* tcount;
+    const int* tstart;
+    int T;
+};
+
 template <int NT, typename FT, typename GT>
 void launch_tiles_nt(const int32_t* ids, const void* feats, int feat_ld, int B, int N, int C,
                      int R, int TV, void* grid, int32_t* counts, bool vec, bool zero_rows,
-                     hipStream_t s) {
+                     const Buckets& bu, hipStream_t s) {
     const int V = R * R * R;
     dim3 g((V + TV - 1) / TV, B);
     int cap, stage;
@@ -850,25 +955,27 @@ void launch_tiles_nt(const int32_t* ids, const void* feats, int feat_ld, int B, 
         tile_budget(k, NT, TV, N, cap, stage);
         hipLaunchKernelGGL(k, g, dim3(NT), tile_lds_bytes(NT, TV, cap, stage), s, ids,
                            (const FT*)feats, feat_ld, N, C, R, TV, cap, stage, (int)zero_rows,
-                           (GT*)grid, counts);
+                           (GT*)grid, counts, bu.bk, bu.br, bu.tcount, bu.tstart, bu.T);
     } else {
         auto k = pv_voxel_tile_kernel<NT, FT, GT, false>;
         tile_budget(k, NT, TV, N, cap, stage);
         hipLaunchKernelGGL(k, g, dim3(NT), tile_lds_bytes(NT, TV, cap, stage), s, ids,
-                           (const FT*)feats, feat_ld, N, C, R, TV, cap, 0, 0, (GT*)grid, counts);
+                           (const FT*)feats, feat_ld, N, C, R, TV, cap, 0, 0, (GT*)grid, counts,
+                           bu.bk, bu.br, bu.tcount, bu.tstart, bu.T);
     }
 }
 
 template <typename FT, typename GT>
 void launch_tiles(const int32_t* ids, const void* feats, int feat_ld, int B, int N, int C, int R,
-                  void* grid, int32_t* counts, bool vec, bool zero_rows, hipStream_t s) {
+                  void* grid, int32_t* counts, bool vec, bool zero_rows, const Buckets& bu,
+                  hipStream_t s) {
     const TileShape t = tile_shape(B, R * R * R, N);
     if (t.nt == 128)
         launch_tiles_nt<128, FT, GT>(ids, feats, feat_ld, B, N, C, R, t.tv, grid, counts, vec,
-                                     zero_rows, s);
+                                     zero_rows, bu, s);
     else
         launch_tiles_nt<256, FT, GT>(ids, feats, feat_ld, B, N, C, R, t.tv, grid, counts, vec,
-                                     zero_rows, s);
+                                     zero_rows, bu, s);
 }
 
 // Zero fill byte by byte, for grids the 16-byte path cannot cover.
@@ -883,33 +990,44 @@ struct VoxWs {
     SplitWs split;
 };
 
-VoxWs carve_ws(void* ws, int B, int N) {
+// Workspace: ids [B][N], normalised coordinates [B][N][3], the split
+// normalisation's partials and, for large clouds, the tile buckets.
+VoxWs carve_ws(void* ws, int B, int N, int R, size_t* bytes) {
     const int G = (N + kNormPts - 1) / kNormPts;
-    char* p = (char*)ws;
+    const int V = R * R * R;
+    const TileShape ts = tile_shape(B, V, N);
+    const bool large = N > kSmallMaxN;
+    size_t off = 0;
     VoxWs w;
-    w.ids = (int32_t*)p;
-    p += pv_align256((size_t)B * N * sizeof(int32_t));
-    w.pnorm = (float*)p;
-    p += pv_align256((size_t)B * N * 3 * sizeof(float));
+    auto take = [&](size_t n) {
+        void* q = ws ? (void*)((char*)ws + off) : nullptr;
+        off += pv_align256(n);
+        return q;
+    };
+    w.ids = (int32_t*)take((size_t)B * N * sizeof(int32_t));
+    w.pnorm = (float*)take((size_t)B * N * 3 * sizeof(float));
     w.split.G = G;
-    w.split.pA = (float*)p;
-    p += pv_align256((size_t)B * G * 3 * sizeof(float));
-    w.split.pQ = (long long*)p;
-    p += pv_align256((size_t)B * G * 3 * sizeof(long long));
-    w.split.pM = (double*)p;
+    w.split.pA = (float*)take((size_t)B * G * 3 * sizeof(float));
+    w.split.pQ = (long long*)take((size_t)B * G * 3 * sizeof(long long));
+    w.split.pM = (double*)take((size_t)B * G * sizeof(double));
+    w.split.TV = ts.tv;
+    w.split.T = large ? (V + ts.tv - 1) / ts.tv : 0;
+    const size_t nt = (size_t)B * w.split.T;
+    w.split.tcount = (int*)take(nt * sizeof(int));
+    w.split.tcursor = (int*)take(nt * sizeof(int));
+    w.split.tstart = (int*)take(nt * sizeof(int));
+    w.split.bk = (int*)take(large ? (size_t)B * N * sizeof(int) : 0);
+    w.split.br = (int*)take(large ? (size_t)B * N * sizeof(int) : 0);
+    if (bytes) *bytes = off;
     return w;
 }
 
 }  // namespace
 
 size_t pv_voxelize_ws_bytes(int B, int N, int R) {
-    (void)R;
-    const int G = (N + kNormPts - 1) / kNormPts;
-    return pv_align256((size_t)B * N * sizeof(int32_t)) +
-           pv_align256((size_t)B * N * 3 * sizeof(float)) +
-           pv_align256((size_t)B * G * 3 * sizeof(float)) +
-           pv_align256((size_t)B * G * 3 * sizeof(long long)) +
-           pv_align256((size_t)B * G * sizeof(double));
+    size_t bytes = 0;
+    carve_ws(nullptr, B, N, R, &bytes);
+    return bytes;
 }
 
 pvconv_status pv_launch_voxelize(const float* coords, const void* feats, bool feat_bf16,
@@ -917,7 +1035,7 @@ pvconv_status pv_launch_voxelize(const float* coords, const void* feats, bool fe
                                  bool grid_bf16, int32_t* counts, int32_t* vox_id,
                                  float* norm_coords, void* ws, hipStream_t s) {
     if (B == 0) return PVCONV_OK;
-    VoxWs w = carve_ws(ws, B, N);
+    VoxWs w = carve_ws(ws, B, N, R, nullptr);
     int32_t* ids = vox_id ? vox_id : w.ids;
     float* pn = norm_coords ? norm_coords : w.pnorm;
     // Rows of empty voxels are zero. With 16-byte rows the tile kernel writes
@@ -954,9 +1072,15 @@ pvconv_status pv_launch_voxelize(const float* coords, const void* feats, bool fe
                            coords, N, w.split, B, grid16, n16);
         hipLaunchKernelGGL(pv_norm_sum_kernel, g, dim3(kNormThreads), 0, s, coords, N, w.split);
         hipLaunchKernelGGL(pv_norm_radius_kernel, g, dim3(kNormThreads), 0, s, coords, N, w.split);
-        hipLaunchKernelGGL(pv_norm_points_kernel, g, dim3(kNormThreads), 0, s, coords, N, R,
-                           w.split, ids, pn);
+        hipLaunchKernelGGL(pv_norm_points_kernel, g, dim3(kNormThreads),
+                           (size_t)w.split.T * sizeof(int), s, coords, N, R, w.split, ids, pn);
+        hipLaunchKernelGGL(pv_bucket_kernel, g, dim3(kNormThreads),
+                           (size_t)2 * w.split.T * sizeof(int), s, ids, N, w.split);
     }
+    const Buckets bu = N > kSmallMaxN
+                           ? Buckets{w.split.bk, w.split.br, w.split.tcount, w.split.tstart,
+                                     w.split.T}
+                           : Buckets{nullptr, nullptr, nullptr, nullptr, 0};
     if (!grid_ok) {
         // a grid that 16-byte stores cannot cover: the plain element kernel
         hipLaunchKernelGGL(pv_zero_elems_kernel, dim3(1024), dim3(256), 0, s, (char*)grid, gbytes);
@@ -964,16 +1088,17 @@ pvconv_status pv_launch_voxelize(const float* coords, const void* feats, bool fe
     if (feat_bf16) {
         if (grid_bf16)
             launch_tiles<uint16_t, uint16_t>(ids, feats, feat_ld, B, N, C, R, grid, counts, vec,
-                                             vec, s);
+                                             vec, bu, s);
         else
             launch_tiles<uint16_t, float>(ids, feats, feat_ld, B, N, C, R, grid, counts, vec, vec,
-                                          s);
+                                          bu, s);
     } else {
         if (grid_bf16)
             launch_tiles<float, uint16_t>(ids, feats, feat_ld, B, N, C, R, grid, counts, vec, vec,
-                                          s);
+                                          bu, s);
         else
-            launch_tiles<float, float>(ids, feats, feat_ld, B, N, C, R, grid, counts, vec, vec, s);
+            launch_tiles<float, float>(ids, feats, feat_ld, B, N, C, R, grid, counts, vec, vec, bu,
+                                       s);
     }
     return pv_launch_status();
 }
