@@ -4,12 +4,16 @@
 // bf16 path: implicit GEMM on the MFMA units. M = output voxels, N = output
 // channels, K = 27 taps x input channels.
 //
-//  * One 256-thread workgroup per CU owns an 8x8x8 brick of output voxels and
-//    32*NB output channels. Each wave computes two u-slices of the brick (128
-//    voxels) against all 32*NB channels with v_mfma_f32_32x32x16_bf16: A =
-//    weights (rows = output channels), B = voxels (columns), 4 x NB
-//    accumulator blocks, so every voxel fragment feeds NB MFMAs and every
-//    weight fragment four.
+//  * One workgroup per CU owns an 8x8x8 brick of output voxels and 32*NB
+//    output channels. Its waves form 4 voxel groups x WCH channel groups:
+//    each wave computes two u-slices of the brick (128 voxels) against
+//    32*NB/WCH channels with v_mfma_f32_32x32x16_bf16: A = weights (rows =
+//    output channels), B = voxels (columns), 4 x NB/WCH accumulator blocks,
+//    so every voxel fragment feeds NB/WCH MFMAs and every weight fragment
+//    four. WCH = 2 (eight waves, two per SIMD, so that one wave's waits
+//    overlap the other's MFMAs) measures faster for 64 input channels;
+//    WCH = 1 (four waves, one per SIMD, all 256 accumulator registers) for
+//    wider inputs.
 //  * The input is consumed in chunks of 16 channels (one MFMA k step). A
 //    chunk's 10x10x10 halo (zero outside the grid) sits in LDS at 48 bytes per
 //    voxel (32 bytes of data) and 640 bytes per 10-voxel row: with that
@@ -19,10 +23,11 @@
 //  * The 27 taps of a chunk are unrolled, so every LDS fragment address is a
 //    per-lane base plus an immediate. Weights come pre-packed in fragment
 //    order (pv_pack_conv_weights_kernel): each fragment load is one coalesced
-//    1 KB buffer load, issued one tap ahead into registers. The only barrier
+//    1 KB buffer load, issued two taps ahead into registers. The only barrier
 //    is one per chunk.
-//  * The epilogue folds bias + batch norm into one scale/shift per channel,
-//    applies the activation and stores 4 consecutive channels per lane.
+//  * The epilogue folds bias + batch norm into one scale/shift per channel
+//    (a table in LDS), applies the activation and stages the tile through
+//    LDS so that every store instruction writes whole contiguous rows.
 //
 // fp32 path: one thread per (voxel, output channel), plain FMA loop.
 #include "pv_common.h"
@@ -36,9 +41,7 @@ constexpr int kKC = 16;                            // input channels per chunk
 constexpr int kVoxPitch = 48;                      // LDS bytes per halo voxel
 constexpr int kRowPitch = 640;                     // LDS bytes per 10-voxel row
 constexpr int kHaloBytes = kHalo * kHalo * kRowPitch;  // 64000 per buffer
-constexpr int kThreads = 256;
 constexpr int kPieces = kHaloVox * 2;              // 16-byte pieces per chunk halo
-constexpr int kSets = (kPieces + kThreads - 1) / kThreads;  // 8 pieces per thread
 constexpr int kTaps = 27;
 constexpr int kOOB = 0x40000000;                   // byte offset always out of range
 // Epilogue staging: the output tile goes through LDS as [512 voxels][PW
@@ -84,8 +87,10 @@ __device__ __forceinline__ uint4 bload8_elems(__amdgpu_buffer_rsrc_t r, int voff
     return pack8(e);
 }
 
-template <int NB, bool VEC>
-__global__ __launch_bounds__(kThreads, 1) void pv_conv3d_bf16_kernel(
+// WCH channel groups of waves: 1 (four waves, 256 threads) or 2 (eight
+// waves, two per SIMD).
+template <int NB, int WCH, bool VEC>
+__global__ __launch_bounds__(256 * WCH, 1) void pv_conv3d_bf16_kernel(
     const uint16_t* __restrict__ x, const uint16_t* __restrict__ wpk, PvBnFold bn, int act,
     float slope, void* __restrict__ y, int out_bf16, int vec_out, int R, int Cin, int Cout,
     int nbr, int nblocks) {
@@ -98,6 +103,12 @@ __global__ __launch_bounds__(kThreads, 1) void pv_conv3d_bf16_kernel(
     int bid = blockIdx.x;
     if ((nblocks & 7) == 0) bid = (bid & 7) * (nblocks >> 3) + (bid >> 3);
     constexpr int NT = NB * 32;
+    // Waves = 4 voxel groups x WCH channel groups: each wave owns two u-slices
+    // of the brick (4 blocks of 32 voxels) and NBW blocks of 32 channels.
+    static_assert(NB % WCH == 0, "channel groups split the tile evenly");
+    constexpr int NTH = 256 * WCH, NBW = NB / WCH;
+    constexpr int kSets = (kPieces + NTH - 1) / NTH;  // halo pieces per thread
+    const int wv = wave / WCH, wc = wave % WCH;
     const int ntiles = Cout / NT;
     const int nt = bid % ntiles;
     bid /= ntiles;
@@ -118,11 +129,11 @@ __global__ __launch_bounds__(kThreads, 1) void pv_conv3d_bf16_kernel(
     int bbase[4];
 #pragma unroll
     for (int mb = 0; mb < 4; mb++) {
-        const int ul = 2 * wave + (mb >> 1), vl = (mb & 1) * 4 + (r32 >> 3), wl = r32 & 7;
+        const int ul = 2 * wv + (mb >> 1), vl = (mb & 1) * 4 + (r32 >> 3), wl = r32 & 7;
         bbase[mb] = (ul * kHalo + vl) * kRowPitch + wl * kVoxPitch + khalf * 16;
     }
 
-    // Halo pieces of this thread: piece p = set*256 + tid is voxel p/2 (as
+    // Halo pieces of this thread: piece p = set*NTH + tid is voxel p/2 (as
     // (hu,hv,hw) of the 10x10x10 halo), channels (p%2)*8 .. +7 of the chunk.
     // Threads past the last piece repeat voxel 999 (same value, same slot).
     // goff: byte offset into the input resource (kOOB outside the grid);
@@ -135,7 +146,7 @@ __global__ __launch_bounds__(kThreads, 1) void pv_conv3d_bf16_kernel(
     int goff[kSets], loff[kSets];
 #pragma unroll
     for (int set = 0; set < kSets; set++) {
-        const int h = min(set * (kThreads / 2) + (tid >> 1), kHaloVox - 1);
+        const int h = min(set * (NTH / 2) + (tid >> 1), kHaloVox - 1);
         const int hu = h / (kHalo * kHalo), hv = (h / kHalo) % kHalo, hw = h % kHalo;
         const int gu = u0 + hu - 1, gv = v0 + hv - 1, gw = w0 + hw - 1;
         const bool in = gu >= 0 && gu < R && gv >= 0 && gv < R && gw >= 0 && gw < R;
@@ -154,18 +165,19 @@ __global__ __launch_bounds__(kThreads, 1) void pv_conv3d_bf16_kernel(
     const int G = Cout / 32;
     const __amdgpu_buffer_rsrc_t wr = make_rsrc(wpk, (uint32_t)((size_t)nch * kTaps * G * 1024));
     const int wlane = lane * 16;
-    auto load_w = [&](int c, int tap, pv_bf16x8 (&wf)[NB]) {
+    auto load_w = [&](int c, int tap, pv_bf16x8 (&wf)[NBW]) {
         const int cc = c < nch ? c : nch - 1;  // past the end: reload, never used
 #pragma unroll
-        for (int nb = 0; nb < NB; nb++)
-            wf[nb] = as_frag(bload16(wr, wlane, ((cc * kTaps + tap) * G + nt * NB + nb) * 1024));
+        for (int nb = 0; nb < NBW; nb++)
+            wf[nb] = as_frag(bload16(wr, wlane,
+                                     ((cc * kTaps + tap) * G + nt * NB + wc * NBW + nb) * 1024));
     };
 
-    pv_f32x16 acc[4][NB];
+    pv_f32x16 acc[4][NBW];
 #pragma unroll
     for (int i = 0; i < 4; i++)
 #pragma unroll
-        for (int j = 0; j < NB; j++)
+        for (int j = 0; j < NBW; j++)
 #pragma unroll
             for (int e = 0; e < 16; e++) acc[i][j][e] = 0.f;
 
@@ -178,7 +190,7 @@ __global__ __launch_bounds__(kThreads, 1) void pv_conv3d_bf16_kernel(
     // Chunk 0's halo, the weights of taps 0 and 1.
 #pragma unroll
     for (int set = 0; set < kSets; set++) *(uint4*)(lds + loff[set]) = halo_load(set, 0);
-    pv_bf16x8 wf[3][NB];
+    pv_bf16x8 wf[3][NBW];
     load_w(0, 0, wf[0]);
     load_w(0, 1, wf[1]);
     __syncthreads();
@@ -222,7 +234,7 @@ __global__ __launch_bounds__(kThreads, 1) void pv_conv3d_bf16_kernel(
 #pragma unroll
             for (int mb = 0; mb < 4; mb++)
 #pragma unroll
-                for (int nb = 0; nb < NB; nb++)
+                for (int nb = 0; nb < NBW; nb++)
                     acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
                         wf[t % 3][nb], bf[cur][mb], acc[mb][nb], 0, 0, 0);
             __builtin_amdgcn_sched_barrier(0);
@@ -243,17 +255,17 @@ __global__ __launch_bounds__(kThreads, 1) void pv_conv3d_bf16_kernel(
     const size_t yrow = (size_t)Cout * esz;
     for (int pass = 0; pass * PW < NT; pass++) {
 #pragma clang loop unroll(full)
-        for (int nb = 0; nb < NB; nb++) {
+        for (int nb = 0; nb < NBW; nb++) {
 #pragma clang loop unroll(full)
             for (int j = 0; j < 4; j++) {
-                const int nl = nb * 32 + 8 * j + 4 * khalf;  // channel within the tile
+                const int nl = (wc * NBW + nb) * 32 + 8 * j + 4 * khalf;  // channel in the tile
                 if (nl < pass * PW || nl >= (pass + 1) * PW) continue;
                 const float4 sc = *(const float4*)&bn_tab[0][nl];
                 const float4 sh = *(const float4*)&bn_tab[1][nl];
                 const int cb = (nl - pass * PW) * esz;       // byte offset in the row
 #pragma clang loop unroll(full)
                 for (int mb = 0; mb < 4; mb++) {
-                    const int vox = (2 * wave + (mb >> 1)) * 64 + ((mb & 1) * 4 + (r32 >> 3)) * 8 +
+                    const int vox = (2 * wv + (mb >> 1)) * 64 + ((mb & 1) * 4 + (r32 >> 3)) * 8 +
                                     (r32 & 7);
                     float r[4];
                     r[0] = pv_activate(acc[mb][nb][4 * j + 0] * sc.x + sh.x, act, slope);
@@ -272,7 +284,7 @@ __global__ __launch_bounds__(kThreads, 1) void pv_conv3d_bf16_kernel(
         __syncthreads();
         // copy out: piece k of voxel vox (k < pieces)
         const size_t col = ((size_t)n0 + pass * PW) * esz;
-        for (int i = tid; i < 512 * pieces; i += kThreads) {
+        for (int i = tid; i < 512 * pieces; i += NTH) {
             const int vox = i / pieces, k = i - vox * pieces;
             const int u = u0 + (vox >> 6), v = v0 + ((vox >> 3) & 7), ww = w0 + (vox & 7);
             if (u >= R || v >= R || ww >= R) continue;
@@ -300,7 +312,8 @@ __global__ __launch_bounds__(kThreads, 1) void pv_conv3d_bf16_kernel(
 // (zero past Cin), G = Cout/32. One thread per element.
 __global__ __launch_bounds__(256) void pv_pack_conv_weights_kernel(const uint16_t* __restrict__ w,
                                                                    uint4* __restrict__ packed,
-                                                                   int Cin, int Cout, int total) {
+                                                                   int Cin, int Cout, int total,
+                                                                   int vec) {
     const int i = blockIdx.x * 256 + threadIdx.x;
     if (i >= total) return;
     const int G = Cout / 32;
@@ -313,6 +326,10 @@ __global__ __launch_bounds__(256) void pv_pack_conv_weights_kernel(const uint16_
     const int n = g * 32 + (lane & 31);
     const int k = c * kKC + (lane >> 5) * 8;
     const uint16_t* src = w + ((size_t)n * kTaps + t) * Cin;
+    if (vec) {  // Cin % 8 == 0 and 16-byte aligned rows: one load
+        packed[i] = k < Cin ? *(const uint4*)(src + k) : make_uint4(0u, 0u, 0u, 0u);
+        return;
+    }
     uint16_t e[8];
 #pragma unroll
     for (int j = 0; j < 8; j++) e[j] = k + j < Cin ? src[k + j] : (uint16_t)0;
@@ -349,7 +366,7 @@ __global__ __launch_bounds__(256) void pv_conv3d_f32_kernel(const float* __restr
         ((float*)y)[i] = val;
 }
 
-template <int NB>
+template <int NB, int WCH>
 void launch_bf16(const void* x, int B, int R, int Cin, int Cout, const void* w,
                  const PvBnFold& bn, int act, float slope, void* y, bool out_bf16, bool vec,
                  hipStream_t s) {
@@ -357,13 +374,15 @@ void launch_bf16(const void* x, int B, int R, int Cin, int Cout, const void* w,
     const size_t blocks = (size_t)B * nbr * nbr * nbr * (Cout / (NB * 32));
     const bool vec_out = pv_aligned16(y);
     if (vec)
-        hipLaunchKernelGGL((pv_conv3d_bf16_kernel<NB, true>), dim3((unsigned)blocks),
-                           dim3(kThreads), 0, s, (const uint16_t*)x, (const uint16_t*)w, bn, act,
-                           slope, y, (int)out_bf16, (int)vec_out, R, Cin, Cout, nbr, (int)blocks);
+        hipLaunchKernelGGL((pv_conv3d_bf16_kernel<NB, WCH, true>), dim3((unsigned)blocks),
+                           dim3(256 * WCH), 0, s, (const uint16_t*)x, (const uint16_t*)w, bn,
+                           act, slope, y, (int)out_bf16, (int)vec_out, R, Cin, Cout, nbr,
+                           (int)blocks);
     else
-        hipLaunchKernelGGL((pv_conv3d_bf16_kernel<NB, false>), dim3((unsigned)blocks),
-                           dim3(kThreads), 0, s, (const uint16_t*)x, (const uint16_t*)w, bn, act,
-                           slope, y, (int)out_bf16, (int)vec_out, R, Cin, Cout, nbr, (int)blocks);
+        hipLaunchKernelGGL((pv_conv3d_bf16_kernel<NB, WCH, false>), dim3((unsigned)blocks),
+                           dim3(256 * WCH), 0, s, (const uint16_t*)x, (const uint16_t*)w, bn,
+                           act, slope, y, (int)out_bf16, (int)vec_out, R, Cin, Cout, nbr,
+                           (int)blocks);
 }
 
 }  // namespace
@@ -381,15 +400,24 @@ pvconv_status pv_launch_conv3d(const void* x, int B, int R, int Cin, int Cout, c
     if (bf16) {
         const int total = (int)(pv_conv3d_ws_bytes(Cin, Cout, true) / 16);
         hipLaunchKernelGGL(pv_pack_conv_weights_kernel, dim3((total + 255) / 256), dim3(256), 0,
-                           s, (const uint16_t*)w, (uint4*)ws, Cin, Cout, total);
+                           s, (const uint16_t*)w, (uint4*)ws, Cin, Cout, total,
+                           (int)(Cin % 8 == 0 && pv_aligned16(w)));
         w = ws;
         const bool vec = (Cin % 8 == 0) && pv_aligned16(x);
-        if (Cout % 128 == 0)
-            launch_bf16<4>(x, B, R, Cin, Cout, w, bn, act, slope, y, out_bf16, vec, s);
-        else if (Cout % 64 == 0)
-            launch_bf16<2>(x, B, R, Cin, Cout, w, bn, act, slope, y, out_bf16, vec, s);
-        else
-            launch_bf16<1>(x, B, R, Cin, Cout, w, bn, act, slope, y, out_bf16, vec, s);
+        const bool two = Cin <= 64;  // eight waves for narrow inputs
+        if (Cout % 128 == 0) {
+            if (two)
+                launch_bf16<4, 2>(x, B, R, Cin, Cout, w, bn, act, slope, y, out_bf16, vec, s);
+            else
+                launch_bf16<4, 1>(x, B, R, Cin, Cout, w, bn, act, slope, y, out_bf16, vec, s);
+        } else if (Cout % 64 == 0) {
+            if (two)
+                launch_bf16<2, 2>(x, B, R, Cin, Cout, w, bn, act, slope, y, out_bf16, vec, s);
+            else
+                launch_bf16<2, 1>(x, B, R, Cin, Cout, w, bn, act, slope, y, out_bf16, vec, s);
+        } else {
+            launch_bf16<1, 1>(x, B, R, Cin, Cout, w, bn, act, slope, y, out_bf16, vec, s);
+        }
     } else {
         const size_t total = (size_t)B * R * R * R * Cout;
         hipLaunchKernelGGL(pv_conv3d_f32_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256),
