@@ -5,7 +5,8 @@
 // one contiguous C-channel row (16 B per lane for bf16, 32 B for fp32) and the
 // point's output row is written contiguously. Corner indices and weights are
 // recomputed per lane from the normalised coordinates (cell centres at
-// (i + 1/2) / R, border cells replicated).
+// (i + 1/2) / R, border cells replicated). Each XCD takes a contiguous range
+// of points (a few clouds), so that its L2 holds the rows those clouds touch.
 #include "pv_common.h"
 
 namespace {
@@ -60,7 +61,13 @@ __global__ __launch_bounds__(256) void pv_devoxelize_kernel(const GT* __restrict
                                                             const float* __restrict__ pn,
                                                             float* __restrict__ out, int N, int R,
                                                             int C, size_t items) {
-    const size_t item = (size_t)blockIdx.x * 256 + threadIdx.x;
+    // Workgroups are dispatched round-robin over the 8 XCDs; give each XCD a
+    // contiguous range of them (a few clouds), so that the corner rows
+    // neighbouring points share are fetched once into that XCD's L2 instead
+    // of into all eight.
+    size_t bid = blockIdx.x;
+    if ((gridDim.x & 7) == 0) bid = (bid & 7) * (gridDim.x >> 3) + (bid >> 3);
+    const size_t item = bid * 256 + threadIdx.x;
     if (item >= items) return;
     const int per_point = VEC ? C / 8 : C;
     const size_t point = item / per_point;
