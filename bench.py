@@ -319,46 +319,68 @@ def main():
     ms_per_step = wall * 1e3 / args.steps
     gpu_out = out.double().cpu().numpy()
 
-    # ---- per-step breakdown: the same chain as separate C-ABI calls, with
-    # events between them on the stream the kernels run on ----------------
+    # ---- per-step breakdown: the same chain as separate C-ABI calls. Each
+    # call is timed as the average of REPS back-to-back launches captured in a
+    # HIP graph (so that host submission cannot leave the GPU idle between
+    # them), replayed `steps // REPS` times between HIP events on the stream
+    # the kernels run on. Buffers are allocated once, outside the timing. -----
     names = ["voxelize"] + [f"conv{i + 1}" for i in range(L.n_convs)] + ["devoxelize",
                                                                          "point_mlp"]
-    per = {n: [] for n in names}
+    V = R ** 3
+    grid = torch.empty((B, V, cin), dtype=cdt, device=dev)
+    counts = torch.empty((B, V), dtype=torch.int32, device=dev)
+    ids = torch.empty((B, N), dtype=torch.int32, device=dev)
+    pn = torch.empty((B, N, 3), dtype=torch.float32, device=dev)
+    vws = torch.empty(max(pv._lib.pvconv_voxelize_workspace_size(B, N, R), 256),
+                      dtype=torch.uint8, device=dev)
+    hs = [torch.empty((B, V, cout), dtype=cdt, device=dev) for _ in range(L.n_convs)]
+    cws = torch.empty(max(pv._lib.pvconv_conv3d_workspace_size(max(cin, cout), cout,
+                                                               1 if bf16 else 0), 256),
+                      dtype=torch.uint8, device=dev)
+    dv = torch.empty((B, N, cout), dtype=torch.float32, device=dev)
 
-    def chain(record):
-        marks = [torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)]
-        marks[0].record(stream)
-        g, _, _, pn = pv.pvconv_voxelize(coords, feats, R, grid_dtype=cdt, want_ids=True)
-        marks[1].record(stream)
-        h = g
-        for i in range(L.n_convs):
-            h = pv.pvconv_conv3d(h, layer.conv_w[i], R, bn=layer.conv_bn[i], act="leaky",
-                                 slope=L.slope, out_dtype=cdt)
-            marks[2 + i].record(stream)
-        dv = pv.pvconv_devoxelize(h, R, pn)
-        marks[2 + L.n_convs].record(stream)
-        pv.pvconv_point_mlp(feats, layer.mlp_w, bias=layer.mlp_b, bn=layer.mlp_bn, act="relu",
-                            residual=dv, out=out)
-        marks[3 + L.n_convs].record(stream)
-        if record is not None:
-            record.append(marks)
-        return pn
+    def step_fn(name):
+        if name == "voxelize":
+            return lambda: pv.pvconv_voxelize(coords, feats, R, grid_dtype=cdt, grid=grid,
+                                              counts=counts, ids=ids, norm=pn, workspace=vws)
+        if name.startswith("conv"):
+            i = int(name[4:]) - 1
+            src = grid if i == 0 else hs[i - 1]
+            return lambda: pv.pvconv_conv3d(src, layer.conv_w[i], R, bn=layer.conv_bn[i],
+                                            act="leaky", slope=L.slope, out=hs[i],
+                                            workspace=cws)
+        if name == "devoxelize":
+            return lambda: pv.pvconv_devoxelize(hs[-1], R, pn, out=dv)
+        return lambda: pv.pvconv_point_mlp(feats, layer.mlp_w, bias=layer.mlp_b, bn=layer.mlp_bn,
+                                           act="relu", residual=dv, out=out)
 
-    for _ in range(max(2, args.warmup // 2)):
-        chain(None)
+    for n in names:  # one eager pass fills every intermediate
+        step_fn(n)()
     torch.cuda.synchronize()
-    recs = []
-    for _ in range(args.steps):
-        pn = chain(recs)
-    torch.cuda.synchronize()
-    for marks in recs:
-        for j, n in enumerate(names):
-            per[n].append(marks[j].elapsed_time(marks[j + 1]))
+    REPS = 10
+    per = {}
+    for n in names:
+        fn = step_fn(n)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(REPS):
+                fn()
+        g.replay()
+        torch.cuda.synchronize()
+        times = []
+        for _ in range(max(1, args.steps // REPS)):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            g.replay()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            times.append(e0.elapsed_time(e1) / REPS)
+        per[n] = times
+        del g
     pn_host = pn.cpu().numpy()
 
     # ---- algorithmic work per step ---------------------------------------
     s_g = 2 if bf16 else 4
-    V = R ** 3
     work = {
         "voxelize": ("GB/s", B * N * (12 + 4 * cin + 4) + B * V * (cin * s_g + 4)),
         "devoxelize": ("GB/s", B * N * (12 + 4 * cout) + distinct_corners(pn_host, R) * cout * s_g),

@@ -130,20 +130,32 @@ def _bn_struct(bn) -> BN:
 # ----------------------------------------------------------------------------
 # entry points (same names as the C ABI)
 # ----------------------------------------------------------------------------
+def _out(t: Optional[torch.Tensor], shape, dtype, device, what):
+    """A caller-given output (checked) or a new one."""
+    if t is None:
+        return torch.empty(shape, dtype=dtype, device=device)
+    if tuple(t.shape) != tuple(shape) or t.dtype != dtype or not t.is_contiguous():
+        raise ValueError(f"{what} must be a contiguous {tuple(shape)} {dtype} tensor")
+    return t
+
+
 def pvconv_voxelize(coords: torch.Tensor, feats: torch.Tensor, R: int,
-                    grid_dtype=torch.float32, want_ids=True, want_norm=True):
+                    grid_dtype=torch.float32, want_ids=True, want_norm=True, grid=None,
+                    counts=None, ids=None, norm=None, workspace=None):
     """coords [B][N][3] f32, feats [B][N][C] -> (grid [B][R^3][C], counts [B][R^3],
-    vox_id [B][N] or None, norm_coords [B][N][3] or None)."""
+    vox_id [B][N] or None, norm_coords [B][N][3] or None). Outputs and the
+    workspace may be passed in (then nothing is allocated)."""
     B, N, _ = coords.shape
     C = feats.shape[-1]
     dev = coords.device
     ld = _rows(feats, N, C)
-    grid = torch.empty((B, R ** 3, C), dtype=_torch_dt(grid_dtype), device=dev)
-    counts = torch.empty((B, R ** 3), dtype=torch.int32, device=dev)
-    ids = torch.empty((B, N), dtype=torch.int32, device=dev) if want_ids else None
-    pn = torch.empty((B, N, 3), dtype=torch.float32, device=dev) if want_norm else None
+    grid = _out(grid, (B, R ** 3, C), _torch_dt(grid_dtype), dev, "grid")
+    counts = _out(counts, (B, R ** 3), torch.int32, dev, "counts")
+    ids = _out(ids, (B, N), torch.int32, dev, "ids") if want_ids else None
+    pn = _out(norm, (B, N, 3), torch.float32, dev, "norm") if want_norm else None
     wsb = _lib.pvconv_voxelize_workspace_size(B, N, R)
-    ws = torch.empty(max(wsb, 256), dtype=torch.uint8, device=dev)
+    ws = workspace if workspace is not None and workspace.numel() >= wsb else \
+        torch.empty(max(wsb, 256), dtype=torch.uint8, device=dev)
     _check("pvconv_voxelize", _lib.pvconv_voxelize(
         _p(coords), _p(feats), _dt(feats), ld, B, N, C, R, _p(grid), _dt(grid), _p(counts),
         _p(ids), _p(pn), _p(ws), wsb, _stream(coords)))
@@ -172,11 +184,11 @@ def pvconv_conv3d(x: torch.Tensor, weight: torch.Tensor, R: int, bn=None,
     return y
 
 
-def pvconv_devoxelize(grid: torch.Tensor, R: int, norm_coords: torch.Tensor):
+def pvconv_devoxelize(grid: torch.Tensor, R: int, norm_coords: torch.Tensor, out=None):
     """grid [B][R^3][C], norm_coords [B][N][3] f32 -> [B][N][C] f32."""
     B, V, C = grid.shape
     N = norm_coords.shape[1]
-    out = torch.empty((B, N, C), dtype=torch.float32, device=grid.device)
+    out = _out(out, (B, N, C), torch.float32, grid.device, "out")
     _check("pvconv_devoxelize", _lib.pvconv_devoxelize(
         _p(grid.contiguous()), B, R, C, _dt(grid), _p(norm_coords.contiguous()), N, _p(out),
         _stream(grid)))

@@ -20,6 +20,8 @@
 // once. Otherwise the normalisation launch first zeroes the grid (extra
 // workgroups) and the tile fill overwrites the occupied rows.
 #include <algorithm>
+#include <mutex>
+#include <unordered_map>
 
 #include "pv_common.h"
 
@@ -646,21 +648,31 @@ __device__ void tile_fill_range(const TileLds& L, int lo, int hi, int base, cons
                 occ[atomicAdd(&s_nocc, 1)] = vi;
         }
         lds_barrier();
+        // The first item's first point is loaded before side() issues the
+        // zero rows: one counter tracks loads and stores in issue order, so a
+        // load issued after the stores would wait for them.
         const int nocc = s_nocc;
+        bool sided = false;
         for (int item = threadIdx.x; item < nocc * gpv; item += NT) {
             const int vi = occ[item / gpv], cg = item % gpv;
             const int nk = L.hist[vi];
-            double acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
             const int j0 = L.start[vi] - base;
-            sum8<FT>(fb, feat_ld, cg * 8, L.list, j0, j0 + nk, 1, acc);
+            float f0[8];
+            load8f<FT>(fb + (size_t)L.list[j0] * feat_ld + cg * 8, f0);
+            if (!sided) {
+                side();
+                sided = true;
+            }
+            double acc[8];
+#pragma unroll
+            for (int i = 0; i < 8; i++) acc[i] = (double)f0[i];
+            sum8<FT>(fb, feat_ld, cg * 8, L.list, j0 + 1, j0 + nk, 1, acc);
             float mean[8];
 #pragma unroll
             for (int i = 0; i < 8; i++) mean[i] = (float)(acc[i] / (double)nk);
             store8<GT>(out + (size_t)vi * C + cg * 8, mean);
         }
-        // after this thread's gathers: loads issued after the zero stores
-        // would wait for them (one counter tracks both, in issue order)
-        side();
+        if (!sided) side();
         lds_barrier();
         // Heavy voxels: one per wave, four at a time. For channel groups cg0 ..
         // cg0+ng-1, lane = sub * ng + (cg - cg0) sums points j = sub, sub+S,
@@ -924,10 +936,24 @@ void tile_budget(K kernel, int NT, int TV, int N, int& cap, int& stage) {
     cap = N < want ? (N > 0 ? N : 1) : want;
     stage = 0;
     const size_t small = 65536;
-    if (tile_lds_bytes(NT, TV, cap, stage) <= small) return;
+    const size_t want_bytes = tile_lds_bytes(NT, TV, cap, stage);
+    if (want_bytes <= small) return;
+    // the grant is per kernel and lasts for the process: ask once per kernel
+    // and size (a launch being captured into a graph then makes no other call)
+    static std::mutex mu;
+    static std::unordered_map<const void*, size_t> granted;
+    {
+        std::lock_guard<std::mutex> lock(mu);
+        auto it = granted.find((const void*)kernel);
+        if (it != granted.end() && want_bytes <= it->second) return;
+    }
     if (hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)tile_lds_bytes(NT, TV, cap, stage)) == hipSuccess)
+                            (int)want_bytes) == hipSuccess) {
+        std::lock_guard<std::mutex> lock(mu);
+        size_t& g = granted[(const void*)kernel];
+        g = std::max(g, want_bytes);
         return;
+    }
     (void)hipGetLastError();
     stage = 0;
     while (cap > 1 && tile_lds_bytes(NT, TV, cap, stage) > small) cap >>= 1;
