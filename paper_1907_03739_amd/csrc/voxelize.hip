@@ -487,11 +487,10 @@ template <>
 __device__ __forceinline__ void store1<uint16_t>(uint16_t* p, float v) { *p = pv_f32_to_bf16(v); }
 
 // Sum of 8 channels over the points list[j0], list[j0 + step], ... (< j1) in
-// that order, fp64, with eight points' loads in flight at a time.
-template <typename FT>
+// that order, fp64, with U points' loads in flight at a time.
+template <typename FT, int U = 8>
 __device__ __forceinline__ void sum8(const FT* fb, int feat_ld, int col, const int* list, int j0,
                                      int j1, int step, double* acc) {
-    constexpr int U = 8;
     int j = j0;
     for (; j + (U - 1) * step < j1; j += U * step) {
         float f[U][8];
@@ -648,29 +647,45 @@ __device__ void tile_fill_range(const TileLds& L, int lo, int hi, int base, cons
                 occ[atomicAdd(&s_nocc, 1)] = vi;
         }
         lds_barrier();
-        // The first item's first point is loaded before side() issues the
-        // zero rows: one counter tracks loads and stores in issue order, so a
-        // load issued after the stores would wait for them.
-        const int nocc = s_nocc;
+        // Items go in batches of IB per thread: the first point of every item
+        // of a batch is loaded at once (most occupied voxels hold one or two
+        // points), then the zero rows go out (side()), then each item adds
+        // its remaining points. One counter tracks loads and stores in issue
+        // order, so loads issued after side()'s stores would wait for them.
+        constexpr int IB = 4;
+        const int nocc = s_nocc, nitems = nocc * gpv;
         bool sided = false;
-        for (int item = threadIdx.x; item < nocc * gpv; item += NT) {
-            const int vi = occ[item / gpv], cg = item % gpv;
-            const int nk = L.hist[vi];
-            const int j0 = L.start[vi] - base;
-            float f0[8];
-            load8f<FT>(fb + (size_t)L.list[j0] * feat_ld + cg * 8, f0);
+        for (int i0 = threadIdx.x; i0 < nitems; i0 += IB * NT) {
+            float f0[IB][8];
+            int vis[IB], cgs[IB], nks[IB], j0s[IB];
+#pragma unroll
+            for (int q = 0; q < IB; q++) {
+                const int item = i0 + q * NT;
+                nks[q] = 0;
+                if (item < nitems) {
+                    vis[q] = occ[item / gpv];
+                    cgs[q] = item % gpv;
+                    nks[q] = L.hist[vis[q]];
+                    j0s[q] = L.start[vis[q]] - base;
+                    load8f<FT>(fb + (size_t)L.list[j0s[q]] * feat_ld + cgs[q] * 8, f0[q]);
+                }
+            }
             if (!sided) {
                 side();
                 sided = true;
             }
-            double acc[8];
 #pragma unroll
-            for (int i = 0; i < 8; i++) acc[i] = (double)f0[i];
-            sum8<FT>(fb, feat_ld, cg * 8, L.list, j0 + 1, j0 + nk, 1, acc);
-            float mean[8];
+            for (int q = 0; q < IB; q++) {
+                if (nks[q] == 0) continue;
+                double acc[8];
 #pragma unroll
-            for (int i = 0; i < 8; i++) mean[i] = (float)(acc[i] / (double)nk);
-            store8<GT>(out + (size_t)vi * C + cg * 8, mean);
+                for (int i = 0; i < 8; i++) acc[i] = (double)f0[q][i];
+                sum8<FT, 4>(fb, feat_ld, cgs[q] * 8, L.list, j0s[q] + 1, j0s[q] + nks[q], 1, acc);
+                float mean[8];
+#pragma unroll
+                for (int i = 0; i < 8; i++) mean[i] = (float)(acc[i] / (double)nks[q]);
+                store8<GT>(out + (size_t)vis[q] * C + cgs[q] * 8, mean);
+            }
         }
         if (!sided) side();
         lds_barrier();
