@@ -40,8 +40,9 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 def parse():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=100,
+                    help="untimed steps first (the clock settles under load within ~50 ms)")
     ap.add_argument("--workload", type=int, default=2, choices=(1, 2, 3, 4, 5),
                     help="1 fp32 layer R=8, 2 part-seg layer R=32, 3 part-seg network, "
                          "4 scene-seg network, 5 stress layer R=64")

@@ -404,13 +404,17 @@ pvconv_status pv_launch_conv3d(const void* x, int B, int R, int Cin, int Cout, c
                            (int)(Cin % 8 == 0 && pv_aligned16(w)));
         w = ws;
         const bool vec = (Cin % 8 == 0) && pv_aligned16(x);
+        // Channel tile: the widest (most reuse of each halo) that still gives
+        // about one workgroup per CU; small grids (R = 16) take narrow tiles.
+        const int nbr = (R + kBrick - 1) / kBrick;
+        const long bricks = (long)B * nbr * nbr * nbr;
         const bool two = Cin <= 64;  // eight waves for narrow inputs
-        if (Cout % 128 == 0) {
+        if (Cout % 128 == 0 && bricks * (Cout / 128) >= 256) {
             if (two)
                 launch_bf16<4, 2>(x, B, R, Cin, Cout, w, bn, act, slope, y, out_bf16, vec, s);
             else
                 launch_bf16<4, 1>(x, B, R, Cin, Cout, w, bn, act, slope, y, out_bf16, vec, s);
-        } else if (Cout % 64 == 0) {
+        } else if (Cout % 64 == 0 && bricks * (Cout / 64) >= 256) {
             if (two)
                 launch_bf16<2, 2>(x, B, R, Cin, Cout, w, bn, act, slope, y, out_bf16, vec, s);
             else
