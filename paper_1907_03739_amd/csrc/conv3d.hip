@@ -29,7 +29,7 @@
 //    (a table in LDS), applies the activation and stages the tile through
 //    LDS so that every store instruction writes whole contiguous rows.
 //
-// fp32 path: one thread per (voxel, output channel), plain FMA loop.
+// fp32 path: four lanes per (voxel, output channel), plain FMA loops.
 #include "pv_common.h"
 
 namespace {
@@ -336,27 +336,49 @@ __global__ __launch_bounds__(256) void pv_pack_conv_weights_kernel(const uint16_
     packed[i] = pack8(e);
 }
 
+// fp32 path: four consecutive lanes per output (voxel, channel), each
+// summing the taps tap = part, part + 4, ... over all input channels (16
+// bytes at a time when the rows allow), then a 4-lane sum.
+template <bool V4>
 __global__ __launch_bounds__(256) void pv_conv3d_f32_kernel(const float* __restrict__ x,
                                                             const float* __restrict__ w,
                                                             PvBnFold bn, int act, float slope,
                                                             void* __restrict__ y, int out_bf16,
                                                             int B, int R, int Cin, int Cout) {
     const size_t V = (size_t)R * R * R;
-    const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
-    if (i >= (size_t)B * V * Cout) return;
-    const int o = (int)(i % Cout);
-    const size_t vox = i / Cout;
+    const size_t t = (size_t)blockIdx.x * 256 + threadIdx.x;
+    const size_t i = t >> 2;  // output element
+    const int part = (int)(t & 3);
+    const bool live = i < (size_t)B * V * Cout;
+    const size_t ic = live ? i : 0;  // dead lanes still join the 4-lane sum
+    const int o = (int)(ic % Cout);
+    const size_t vox = ic / Cout;
     const size_t b = vox / V;
     const int r = (int)(vox % V);
     const int u = r / (R * R), v = (r / R) % R, ww = r % R;
     float s = 0.f;
-    for (int tap = 0; tap < 27; tap++) {
-        const int nu = u + tap / 9 - 1, nv = v + (tap / 3) % 3 - 1, nw = ww + tap % 3 - 1;
-        if (nu < 0 || nu >= R || nv < 0 || nv >= R || nw < 0 || nw >= R) continue;
-        const float* xi = x + (b * V + ((size_t)nu * R + nv) * R + nw) * Cin;
-        const float* wk = w + ((size_t)o * 27 + tap) * Cin;
-        for (int c = 0; c < Cin; c++) s += wk[c] * xi[c];
+    if (live) {
+        for (int tap = part; tap < 27; tap += 4) {
+            const int nu = u + tap / 9 - 1, nv = v + (tap / 3) % 3 - 1, nw = ww + tap % 3 - 1;
+            if (nu < 0 || nu >= R || nv < 0 || nv >= R || nw < 0 || nw >= R) continue;
+            const float* xi = x + (b * V + ((size_t)nu * R + nv) * R + nw) * Cin;
+            const float* wk = w + ((size_t)o * 27 + tap) * Cin;
+            if (V4) {
+                for (int c = 0; c < Cin; c += 4) {
+                    const float4 a = *(const float4*)(xi + c), q = *(const float4*)(wk + c);
+                    s += q.x * a.x;
+                    s += q.y * a.y;
+                    s += q.z * a.z;
+                    s += q.w * a.w;
+                }
+            } else {
+                for (int c = 0; c < Cin; c++) s += wk[c] * xi[c];
+            }
+        }
     }
+    s += __shfl_xor(s, 1, 64);
+    s += __shfl_xor(s, 2, 64);
+    if (!live || part != 0) return;
     float scale, shift;
     pv_bn_coeffs(bn, o, scale, shift);
     const float val = pv_activate(s * scale + shift, act, slope);
@@ -424,9 +446,15 @@ pvconv_status pv_launch_conv3d(const void* x, int B, int R, int Cin, int Cout, c
         }
     } else {
         const size_t total = (size_t)B * R * R * R * Cout;
-        hipLaunchKernelGGL(pv_conv3d_f32_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256),
-                           0, s, (const float*)x, (const float*)w, bn, act, slope, y,
-                           (int)out_bf16, B, R, Cin, Cout);
+        const unsigned blocks = (unsigned)((4 * total + 255) / 256);
+        if (Cin % 4 == 0 && pv_aligned16(x) && pv_aligned16(w))
+            hipLaunchKernelGGL(pv_conv3d_f32_kernel<true>, dim3(blocks), dim3(256), 0, s,
+                               (const float*)x, (const float*)w, bn, act, slope, y, (int)out_bf16,
+                               B, R, Cin, Cout);
+        else
+            hipLaunchKernelGGL(pv_conv3d_f32_kernel<false>, dim3(blocks), dim3(256), 0, s,
+                               (const float*)x, (const float*)w, bn, act, slope, y, (int)out_bf16,
+                               B, R, Cin, Cout);
     }
     return pv_launch_status();
 }
