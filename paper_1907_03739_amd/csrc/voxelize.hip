@@ -184,21 +184,17 @@ __device__ __forceinline__ void zero_fill_role(uint4* grid16, size_t n16, int zb
         grid16[i] = make_uint4(0, 0, 0, 0);
 }
 
-template <int PPT>
-__device__ void ids_role(const float* __restrict__ coords, int N, int R, int slice, int b,
-                         int32_t* __restrict__ vox_id, float* __restrict__ norm_coords) {
-    constexpr int NT = 256;
+// A cloud's normalisation parameters (centroid c, largest squared centred
+// norm M2, m = sqrt(M2)) from its N points, held PPT per thread (point
+// threadIdx.x + i*NT in x[i]) by an NT-thread workgroup. Every reduction is
+// order-free, so every workgroup that calls this for a cloud gets the same
+// bits.
+template <int PPT, int NT>
+__device__ void cloud_params(const float (&x)[PPT][3], int N, double (&c)[3], double& M2,
+                             double& m) {
     __shared__ float redf[3 * NT / 64];
     __shared__ long long redl[3 * NT / 64];
     __shared__ double redd[NT / 64];
-    const float* p = coords + (size_t)b * N * 3;
-    float x[PPT][3];
-#pragma unroll
-    for (int i = 0; i < PPT; i++) {
-        const int k = threadIdx.x + i * NT;
-#pragma unroll
-        for (int a = 0; a < 3; a++) x[i][a] = k < N ? p[3 * k + a] : 0.f;
-    }
     float A[3] = {0.f, 0.f, 0.f};
 #pragma unroll
     for (int i = 0; i < PPT; i++)
@@ -215,7 +211,6 @@ __device__ void ids_role(const float* __restrict__ coords, int N, int R, int sli
             if (A[a] > 0.f && threadIdx.x + i * NT < N) q[a] += fixed_term(x[i][a], S[a]);
     }
     block_reduce_k<NT>(q, AddL(), redl);
-    double c[3];
 #pragma unroll
     for (int a = 0; a < 3; a++) c[a] = centroid_from_sum(q[a], S[a], A[a], N);
     double mx[1] = {0.0};
@@ -223,8 +218,30 @@ __device__ void ids_role(const float* __restrict__ coords, int N, int R, int sli
     for (int i = 0; i < PPT; i++)
         if (threadIdx.x + i * NT < N) mx[0] = fmax(mx[0], sq_dist(x[i], c));
     block_reduce_k<NT>(mx, MaxD(), redd);
-    const double M2 = mx[0];
-    const double m = sqrt(M2);
+    M2 = mx[0];
+    m = sqrt(M2);
+}
+
+// The cloud's N points into registers, PPT per thread (zero past N).
+template <int PPT, int NT>
+__device__ __forceinline__ void load_cloud(const float* __restrict__ p, int N,
+                                           float (&x)[PPT][3]) {
+#pragma unroll
+    for (int i = 0; i < PPT; i++) {
+        const int k = threadIdx.x + i * NT;
+#pragma unroll
+        for (int a = 0; a < 3; a++) x[i][a] = k < N ? p[3 * k + a] : 0.f;
+    }
+}
+
+template <int PPT>
+__device__ void ids_role(const float* __restrict__ coords, int N, int R, int slice, int b,
+                         int32_t* __restrict__ vox_id, float* __restrict__ norm_coords) {
+    constexpr int NT = 256;
+    float x[PPT][3];
+    load_cloud<PPT, NT>(coords + (size_t)b * N * 3, N, x);
+    double c[3], M2, m;
+    cloud_params<PPT, NT>(x, N, c, M2, m);
     // this workgroup's slice: points slice*256 + tid, i.e. register row `slice`
 #pragma unroll
     for (int i = 0; i < PPT; i++) {
@@ -760,6 +777,98 @@ __device__ __forceinline__ void tile_collect_one(const TileLds& L, int k, int r,
     }
 }
 
+// The rest of a tile once its points are collected (L.hist, L.kbuf/rbuf):
+// counts out, prefix over the voxels, counting sort, zero rows (zero_rows),
+// means. each_point(fn) calls fn(point, voxel - v0) for every point of the
+// cloud that may lie in the tile (for the segmented passes, when the tile
+// holds more than CAP points).
+template <int NT, typename FT, typename GT, bool VEC, typename EachPoint>
+__device__ void tile_finish(const TileLds& L, int TV, int nv, int CAP, int32_t* cnt, GT* out,
+                            const FT* fb, int feat_ld, int C, bool zero_rows, int stage_bytes,
+                            int* scan_lds, int* s_nheavy, EachPoint each_point) {
+    // 2. counts out; exclusive prefix over the tile's voxels
+    for (int i = threadIdx.x; i < nv; i += NT) cnt[i] = L.hist[i];
+    // The tile's empty voxels: zero rows (16-byte stores), streaming out
+    // while the occupied voxels are gathered.
+    auto zero_empty_rows = [&]() {
+        if (!VEC || !zero_rows) return;
+        const int pr = C * (int)sizeof(GT) / 16;  // 16-byte pieces per row
+        uint4* o16 = (uint4*)out;
+        for (int i = threadIdx.x; i < nv * pr; i += NT)
+            if (L.hist[i / pr] == 0) o16[i] = make_uint4(0u, 0u, 0u, 0u);
+    };
+    auto nothing = []() {};
+    {
+        const int seg = (TV + NT - 1) / NT;
+        const int s0 = min(TV, (int)threadIdx.x * seg), s1 = min(TV, s0 + seg);
+        int local = 0;
+        for (int i = s0; i < s1; i++) local += L.hist[i];
+        int total;
+        int run = block_exclusive_scan<NT>(local, scan_lds, total);
+        for (int i = s0; i < s1; i++) {
+            L.start[i] = run;
+            run += L.hist[i];
+        }
+        if (threadIdx.x == 0) L.start[TV] = total;
+    }
+    lds_barrier();
+    const int total = L.start[TV];
+    if (total <= CAP) {
+        // 3. counting sort of the kept points by voxel, then the fill
+        for (int i = threadIdx.x; i < nv; i += NT) L.cur[i] = L.start[i];
+        lds_barrier();
+        for (int s = threadIdx.x; s < total; s += NT)
+            L.list[atomicAdd(&L.cur[L.rbuf[s]], 1)] = L.kbuf[s];
+        lds_barrier();
+        tile_fill_range<NT, FT, GT, VEC>(L, 0, nv, 0, fb, feat_ld, C, out, s_nheavy, stage_bytes,
+                                         true, zero_empty_rows);
+        return;
+    }
+    zero_empty_rows();
+    // More points than fit: voxel segments of at most CAP points, each
+    // gathered by scanning the ids again. A single voxel beyond CAP points is
+    // summed by the whole workgroup with LDS fp64 atomics.
+    int lo = 0;
+    while (lo < nv) {
+        if (L.start[lo + 1] - L.start[lo] > CAP) {
+            const int nk = L.start[lo + 1] - L.start[lo];
+            double* hacc = L.red;  // C <= 1024 doubles fit in red[] (16 KB)
+            for (int ch = threadIdx.x; ch < C; ch += NT) hacc[ch] = 0.0;
+            lds_barrier();
+            each_point([&](int k, int r) {
+                if (r == lo)
+                    for (int ch = 0; ch < C; ch++)
+                        atomicAdd(&hacc[ch], (double)load1<FT>(fb + (size_t)k * feat_ld + ch));
+            });
+            lds_barrier();
+            for (int ch = threadIdx.x; ch < C; ch += NT)
+                store1<GT>(out + (size_t)lo * C + ch, (float)(hacc[ch] / (double)nk));
+            lds_barrier();
+            lo++;
+            continue;
+        }
+        // largest hi with start[hi] - start[lo] <= CAP (binary search)
+        int a = lo + 1, z = nv;
+        while (a < z) {
+            const int mid = (a + z + 1) >> 1;
+            if (L.start[mid] - L.start[lo] <= CAP)
+                a = mid;
+            else
+                z = mid - 1;
+        }
+        const int hi = a, base = L.start[lo];
+        for (int i = lo + threadIdx.x; i < hi; i += NT) L.cur[i] = L.start[i] - base;
+        lds_barrier();
+        each_point([&](int k, int r) {
+            if (r >= lo && r < hi) L.list[atomicAdd(&L.cur[r], 1)] = k;
+        });
+        lds_barrier();
+        tile_fill_range<NT, FT, GT, VEC>(L, lo, hi, base, fb, feat_ld, C, out, s_nheavy, stage_bytes,
+                                         false, nothing);
+        lo = hi;
+    }
+}
+
 template <int NT, typename FT, typename GT, bool VEC>
 __global__ __launch_bounds__(NT) void pv_voxel_tile_kernel(
     const int32_t* __restrict__ vox_id, const FT* __restrict__ feats, int feat_ld, int N, int C,
@@ -835,88 +944,8 @@ __global__ __launch_bounds__(NT) void pv_voxel_tile_kernel(
             tile_collect_one(L, k, ids[k] - v0, nv, CAP, &s_ntile);
     }
     lds_barrier();
-    // 2. counts out; exclusive prefix over the tile's voxels
-    int32_t* cnt = counts + (size_t)b * V + v0;
-    for (int i = threadIdx.x; i < nv; i += NT) cnt[i] = L.hist[i];
-    // The tile's empty voxels: zero rows (16-byte stores), streaming out
-    // while the occupied voxels are gathered.
-    auto zero_empty_rows = [&]() {
-        if (!VEC || !zero_rows) return;
-        const int pr = C * (int)sizeof(GT) / 16;  // 16-byte pieces per row
-        uint4* o16 = (uint4*)out;
-        for (int i = threadIdx.x; i < nv * pr; i += NT)
-            if (L.hist[i / pr] == 0) o16[i] = make_uint4(0u, 0u, 0u, 0u);
-    };
-    auto nothing = []() {};
-    {
-        const int seg = (TV + NT - 1) / NT;
-        const int s0 = min(TV, (int)threadIdx.x * seg), s1 = min(TV, s0 + seg);
-        int local = 0;
-        for (int i = s0; i < s1; i++) local += L.hist[i];
-        int total;
-        int run = block_exclusive_scan<NT>(local, scan_lds, total);
-        for (int i = s0; i < s1; i++) {
-            L.start[i] = run;
-            run += L.hist[i];
-        }
-        if (threadIdx.x == 0) L.start[TV] = total;
-    }
-    lds_barrier();
-    const int total = L.start[TV];
-    if (total <= CAP) {
-        // 3. counting sort of the kept points by voxel, then the fill
-        for (int i = threadIdx.x; i < nv; i += NT) L.cur[i] = L.start[i];
-        lds_barrier();
-        for (int s = threadIdx.x; s < total; s += NT)
-            L.list[atomicAdd(&L.cur[L.rbuf[s]], 1)] = L.kbuf[s];
-        lds_barrier();
-        tile_fill_range<NT, FT, GT, VEC>(L, 0, nv, 0, fb, feat_ld, C, out, &s_nheavy, stage_bytes,
-                                         true, zero_empty_rows);
-        return;
-    }
-    zero_empty_rows();
-    // More points than fit: voxel segments of at most CAP points, each
-    // gathered by scanning the ids again. A single voxel beyond CAP points is
-    // summed by the whole workgroup with LDS fp64 atomics.
-    int lo = 0;
-    while (lo < nv) {
-        if (L.start[lo + 1] - L.start[lo] > CAP) {
-            const int nk = L.start[lo + 1] - L.start[lo];
-            double* hacc = L.red;  // C <= 1024 doubles fit in red[] (16 KB)
-            for (int ch = threadIdx.x; ch < C; ch += NT) hacc[ch] = 0.0;
-            lds_barrier();
-            each_point([&](int k, int r) {
-                if (r == lo)
-                    for (int ch = 0; ch < C; ch++)
-                        atomicAdd(&hacc[ch], (double)load1<FT>(fb + (size_t)k * feat_ld + ch));
-            });
-            lds_barrier();
-            for (int ch = threadIdx.x; ch < C; ch += NT)
-                store1<GT>(out + (size_t)lo * C + ch, (float)(hacc[ch] / (double)nk));
-            lds_barrier();
-            lo++;
-            continue;
-        }
-        // largest hi with start[hi] - start[lo] <= CAP (binary search)
-        int a = lo + 1, z = nv;
-        while (a < z) {
-            const int mid = (a + z + 1) >> 1;
-            if (L.start[mid] - L.start[lo] <= CAP)
-                a = mid;
-            else
-                z = mid - 1;
-        }
-        const int hi = a, base = L.start[lo];
-        for (int i = lo + threadIdx.x; i < hi; i += NT) L.cur[i] = L.start[i] - base;
-        lds_barrier();
-        each_point([&](int k, int r) {
-            if (r >= lo && r < hi) L.list[atomicAdd(&L.cur[r], 1)] = k;
-        });
-        lds_barrier();
-        tile_fill_range<NT, FT, GT, VEC>(L, lo, hi, base, fb, feat_ld, C, out, &s_nheavy, stage_bytes,
-                                         false, nothing);
-        lo = hi;
-    }
+    tile_finish<NT, FT, GT, VEC>(L, TV, nv, CAP, counts + (size_t)b * V + v0, out, fb, feat_ld, C,
+                                 zero_rows != 0, stage_bytes, scan_lds, &s_nheavy, each_point);
 }
 
 // Tile size: small clouds (every tile scans all N ids, cheap) aim for about
