@@ -15,8 +15,11 @@ Default workload: the part-segmentation-scale layer, 16 clouds x 2048 points,
 
 Printed: ONE JSON line with the headline throughput (points/s), ms per layer,
 the roofline of the dominant kernel (the convolution, MFMA-bound), per-step
-timings of the same chain, and the CPU oracle timed on a bounded sample of the
-same workload (which also checks the GPU output on that sample).
+timings of the same chain (back to back, and cold: after a 512 MiB write that
+evicts the caches), the device's measured peaks (a dense bf16 MFMA loop and a
+16-byte copy) as a second denominator next to the published ones, and the CPU
+oracle timed on a bounded sample of the same workload (which also checks the
+GPU output on that sample).
 """
 from __future__ import annotations
 
@@ -49,6 +52,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="lower bound of CPU work for the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-peaks", action="store_true",
+                    help="skip the measured-peak probes (MFMA loop, copy)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only copy a MIB-MiB buffer 3 times (a plain copy kernel of known "
                          "size, to calibrate the HBM byte counters) and exit")
@@ -87,6 +92,62 @@ def copy_probe(mib):
         b.copy_(a)
     torch.cuda.synchronize()
     print(f"copied {mib} MiB x 3", flush=True)
+
+
+PEAK_LIB = os.path.join(ROOT, "paper_1907_03739_amd", "libpvpeak.so")
+
+
+def measured_peaks(stream):
+    """The device's measured peaks: dense bf16 MFMA (v_mfma_f32_32x32x16_bf16
+    on random operands, three waves per SIMD, ~16 ms per launch after ~0.1 s
+    of the same load) and HBM (a 16-byte copy of 1 GiB, read + write bytes);
+    best of five launches each."""
+    import ctypes
+    import torch
+    lib = ctypes.CDLL(PEAK_LIB)
+    lib.pv_peak_mfma.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
+    lib.pv_peak_mfma_flop.restype = ctypes.c_double
+    lib.pv_peak_mfma_flop.argtypes = [ctypes.c_int, ctypes.c_int]
+    lib.pv_peak_copy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
+                                 ctypes.c_void_p]
+    h = ctypes.c_void_p(stream.cuda_stream)
+
+    def best(launch, warm, reps):
+        for _ in range(warm):
+            launch()
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            launch()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1) * 1e-3)
+        return min(ts)
+
+    blocks = 3 * torch.cuda.get_device_properties(stream.device).multi_processor_count
+    iters = 100000
+    out = torch.empty(blocks * 256, dtype=torch.float32, device=stream.device)
+
+    def mfma():
+        if lib.pv_peak_mfma(blocks, iters, ctypes.c_void_p(out.data_ptr()), h) != 0:
+            raise RuntimeError("MFMA probe launch failed")
+    t_mfma = best(mfma, 6, 5)
+    n = 1 << 30
+    src = torch.ones(n // 4, dtype=torch.float32, device=stream.device)
+    dst = torch.empty_like(src)
+
+    def copy():
+        if lib.pv_peak_copy(ctypes.c_void_p(src.data_ptr()), ctypes.c_void_p(dst.data_ptr()),
+                            n // 16, h) != 0:
+            raise RuntimeError("copy probe launch failed")
+    t_copy = best(copy, 3, 5)
+    del src, dst, out
+    return {"mfma_bf16_tflops": round(lib.pv_peak_mfma_flop(blocks, iters) / t_mfma / 1e12, 1),
+            "hbm_copy_gbs": round(2 * n / t_copy / 1e9, 1),
+            "how": f"MFMA loop {blocks} workgroups x 4 waves, {iters} rounds of 4 "
+                   f"32x32x16 bf16 MFMAs; streaming 16-byte copy of 1 GiB (2 GiB moved); "
+                   f"best of 5 launches"}
 
 
 def conv_flops(B, R, cin, cout):
@@ -214,6 +275,10 @@ def bench_network(args, wl, dev):
                 "unit": "TFLOP/s", "frac": kernels[dom]["frac"], "traffic": None,
                 "kernel": f"network step {dom}", "flop_per_launch": fl[dom],
                 "avg_launch_ms": kernels[dom]["ms"]}
+    peaks = None if args.no_peaks else measured_peaks(stream)
+    if peaks:
+        roofline["frac_measured_peak"] = round(kernels[dom]["achieved"] /
+                                               peaks["mfma_bf16_tflops"], 4)
     total_fl = sum(fl.values())
     line = {
         "metric": METRIC, "value": round(B * N / (ms_per_step * 1e-3), 1), "unit": "points/s",
@@ -229,6 +294,7 @@ def bench_network(args, wl, dev):
         "network_tflops": round(total_fl / (ms_per_step * 1e-3) / 1e12, 2),
         "roofline": roofline,
         "kernels": kernels,
+        "peaks_measured": peaks,
         "inputs_sha256": wl.sha256(),
     }
     if not args.no_cpu_baseline:
@@ -378,7 +444,49 @@ def main():
             times.append(e0.elapsed_time(e1) / REPS)
         per[n] = times
         del g
+
+    # ---- the same calls cold: each after a 512 MiB write that evicts the
+    # L2s and the 256 MB Infinity Cache. A graph of REPS (flush, call) pairs
+    # against a graph of REPS flushes alone; the difference per pair is the
+    # call's time from cold caches. ---------------------------------------
+    scratch = torch.empty(512 << 18, dtype=torch.float32, device=dev)
+    COLD = 10
+
+    def timed(graph):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        graph.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1)
+
+    g0 = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g0):
+        for _ in range(COLD):
+            scratch.fill_(1.0)
+    g0.replay()
+    torch.cuda.synchronize()
+    cold = {}
+    for n in names:
+        fn = step_fn(n)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(COLD):
+                scratch.fill_(1.0)
+                fn()
+        g.replay()
+        torch.cuda.synchronize()
+        diffs = []
+        for _ in range(max(1, args.steps // COLD)):
+            t_flush = timed(g0)
+            t_both = timed(g)
+            diffs.append((t_both - t_flush) / COLD)
+        cold[n] = diffs
+        del g
+    del g0, scratch
     pn_host = pn.cpu().numpy()
+
+    peaks = None if args.no_peaks else measured_peaks(stream)
 
     # ---- algorithmic work per step ---------------------------------------
     s_g = 2 if bf16 else 4
@@ -400,9 +508,18 @@ def main():
         else:
             rate = amount / (ms * 1e-3) / 1e12
             peak = PEAK_BF16_TFLOPS if bf16 else PEAK_F32_TFLOPS
+        ms_cold = statistics.median(cold[n])
+        rate_cold = amount / (ms_cold * 1e-3) / (1e9 if unit == "GB/s" else 1e12)
         kernels[n] = {"ms": round(ms, 4), "ms_min": round(min(per[n]), 4),
                       "achieved": round(rate, 2), "unit": unit, "frac": round(rate / peak, 4),
-                      "algorithmic": amount}
+                      "ms_cold": round(ms_cold, 4), "achieved_cold": round(rate_cold, 2),
+                      "frac_cold": round(rate_cold / peak, 4), "algorithmic": amount}
+        if peaks:
+            mp = peaks["hbm_copy_gbs"] if unit == "GB/s" else (
+                peaks["mfma_bf16_tflops"] if bf16 else None)
+            if mp:
+                kernels[n]["frac_measured_peak"] = round(rate / mp, 4)
+                kernels[n]["frac_cold_measured_peak"] = round(rate_cold / mp, 4)
 
     # dominant kernel: the convolution (one kernel, L.n_convs launches per step)
     conv_names = [f"conv{i + 1}" for i in range(L.n_convs)]
@@ -416,6 +533,8 @@ def main():
                 "kernel": "pv_conv3d_bf16_kernel" if bf16 else
                 "pv_conv3d_f32_kernel", "flop_per_launch": conv_work,
                 "avg_launch_ms": round(conv_ms, 4)}
+    if peaks and bf16:
+        roofline["frac_measured_peak"] = round(achieved / peaks["mfma_bf16_tflops"], 4)
 
     line = {
         "metric": METRIC, "value": round(B * N / (ms_per_step * 1e-3), 1), "unit": "points/s",
@@ -429,6 +548,7 @@ def main():
                                "min": round(min(step_ms), 4)},
         "roofline": roofline,
         "kernels": kernels,
+        "peaks_measured": peaks,
         "inputs_sha256": wl.sha256(),
     }
     if not args.no_cpu_baseline:

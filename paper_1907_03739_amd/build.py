@@ -1,4 +1,5 @@
-"""Build libpvconv.so (HIP, gfx950) in-tree with hipcc.
+"""Build libpvconv.so (HIP, gfx950) in-tree with hipcc, and libpvpeak.so (the
+measured-peak probes the benchmark uses, csrc/peak/).
 
 Usage: python -m paper_1907_03739_amd.build [--verbose]
 """
@@ -16,6 +17,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libpvconv.so")
+PEAK_LIB = os.path.join(PKG, "libpvpeak.so")
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
@@ -28,6 +30,10 @@ FLAGS = [f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-Wall",
 
 def sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")))
+
+
+def peak_sources():
+    return sorted(glob.glob(os.path.join(CSRC, "peak", "*.hip")))
 
 
 def _compile(src, verbose):
@@ -45,20 +51,27 @@ def _compile(src, verbose):
     return obj
 
 
-def build(verbose: bool = False) -> str:
-    """Compile every csrc/*.hip for gfx950 and link libpvconv.so (always rebuilds)."""
-    os.makedirs(BUILD, exist_ok=True)
-    srcs = sources()
-    with concurrent.futures.ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
-        objs = list(ex.map(lambda s: _compile(s, verbose), srcs))
-    tmp = LIB + ".tmp"
+def _link(objs, lib, verbose):
+    tmp = lib + ".tmp"
     cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stdout}{r.stderr}")
-    os.replace(tmp, LIB)
+    os.replace(tmp, lib)
+
+
+def build(verbose: bool = False) -> str:
+    """Compile every csrc/*.hip for gfx950 and link libpvconv.so, and the probes
+    of csrc/peak/ into libpvpeak.so (always rebuilds)."""
+    os.makedirs(BUILD, exist_ok=True)
+    srcs, peak = sources(), peak_sources()
+    with concurrent.futures.ThreadPoolExecutor(max_workers=min(8, len(srcs) + len(peak))) as ex:
+        objs = list(ex.map(lambda s: _compile(s, verbose), srcs + peak))
+    _link(objs[:len(srcs)], LIB, verbose)
+    if peak:
+        _link(objs[len(srcs):], PEAK_LIB, verbose)
     return LIB
 
 

@@ -125,6 +125,39 @@ def test_voxelize_crowded_tiles(N, spread):
     assert_rel(host(g), grid, 1e-5, "crowded voxel grid")
 
 
+@pytest.mark.parametrize("N,R,C,gdt", [(2048, 32, 64, torch.bfloat16), (3000, 7, 16, torch.float32),
+                                        (20000, 31, 32, torch.bfloat16), (1, 5, 8, torch.float32)],
+                         ids=["ids_launch", "odd_R", "split_path", "one_point"])
+def test_voxelize_writes_every_row_of_a_dirty_grid(N, R, C, gdt):
+    # Empty rows are written by two kernels (the rows of voxels outside the
+    # normalisation ball by the normalisation launch, the rest by the tile
+    # kernel): with the grid filled with NaN beforehand every row must come
+    # out right. Half the points lie on a sphere, so after normalisation they
+    # sit on the ball's surface, the other half inside it.
+    rng = np.random.default_rng(N + R)
+    B = 2
+    d = rng.normal(size=(B, N, 3))
+    d /= np.linalg.norm(d, axis=2, keepdims=True)
+    d[:, N // 2:] *= rng.uniform(0, 1, size=(B, N - N // 2, 1))
+    coords = (d * 3.0 + rng.normal(size=(B, 1, 3))).astype(np.float32)
+    feats = rng.normal(size=(B, N, C)).astype(np.float32)
+    if gdt == torch.bfloat16:
+        feats = synth.round_to_bf16(feats)
+    pn, ids, grid, counts = _oracle_vox(coords, feats, R)
+    g = torch.full((B, R ** 3, C), float("nan"), dtype=gdt, device="cuda")
+    cnt = torch.full((B, R ** 3), -7, dtype=torch.int32, device="cuda")
+    g, c, i, p = pv.pvconv_voxelize(dev(coords), dev(feats), R, grid_dtype=gdt, grid=g, counts=cnt)
+    assert np.array_equal(i.cpu().numpy(), ids)
+    assert np.array_equal(c.cpu().numpy(), counts)
+    got = host(g)
+    assert not np.isnan(got).any()
+    assert np.all(got[counts == 0] == 0)
+    if gdt == torch.float32:
+        assert_rel(got, grid, 1e-5, "voxel grid fp32")
+    else:
+        assert_bf16_step(got, grid, "voxel grid bf16")
+
+
 def test_voxelize_empty_clouds_give_zero_grids():
     coords = torch.empty((2, 0, 3), device="cuda")
     feats = torch.empty((2, 0, 16), device="cuda")
