@@ -32,6 +32,7 @@ constexpr int kNormThreads = 256;
 constexpr int kSmallMaxN = 4096;    // largest cloud normalised by one kernel
 constexpr int kHeavy = 32;          // voxels with more points are summed by a whole wave
 constexpr int kMaxCap = 4096;       // tile points kept in LDS at once
+constexpr int kCUs = 256;           // compute units of an MI355X
 
 // ---------------------------------------------------------------------------
 // Normalisation arithmetic. IEEE fp64, round to nearest even, no contraction,
@@ -948,14 +949,12 @@ __global__ __launch_bounds__(NT) void pv_voxel_tile_kernel(
                                  zero_rows != 0, stage_bytes, scan_lds, &s_nheavy, each_point);
 }
 
-// Tile size: small clouds (every tile scans all N ids, cheap) aim for about
-// 2048 workgroups so each tile's points fit the feature stage; large clouds
-// aim for 256 (one per CU) to bound the id scans.
 // Tile shape. Small clouds (every tile scans all N ids, cheap): about 2048
-// tiles of 128 threads, about 15 KB of LDS, so that eight workgroups fit per
-// CU and every tile is resident at once. Large clouds (points bucketed by
-// tile beforehand): about 1024 tiles of 256 threads, so that a dense cluster
-// spreads over several workgroups.
+// tiles of 128 threads, about 18 KB of LDS, so that eight workgroups fit per
+// CU and every tile is resident at once; coarse grids go down to 32 voxels
+// per tile to get there. Large clouds (points bucketed by tile beforehand):
+// about 1024 tiles of 256 threads, so that a dense cluster spreads over
+// several workgroups.
 struct TileShape {
     int nt, tv;
 };
@@ -963,20 +962,29 @@ TileShape tile_shape(int B, int V, int N) {
     const bool small_cloud = N <= kSmallMaxN;
     const long long want = small_cloud ? 2048 : 1024;
     int tv = 1024;
-    while (tv > 128 && (long long)B * ((V + tv - 1) / tv) < want) tv >>= 1;
+    while (tv > 32 && (long long)B * ((V + tv - 1) / tv) < want) tv >>= 1;
     return TileShape{small_cloud ? 128 : 256, tv};
 }
 
 
-// LDS budget of the tile kernel: room for 256 (small clouds) or kMaxCap
-// (large clouds) points and no feature stage (each (voxel, channel group)
-// sums straight from memory); tiles with more points take the segmented
-// path. Dynamic LDS beyond 64 KB has to be granted per kernel; when that
-// fails the capacity shrinks to what 64 KB holds.
+// LDS budget of the tile kernel: no feature stage (each (voxel, channel
+// group) sums straight from memory) and room for the tile's points, tiles
+// with more points taking the segmented path. Large clouds: kMaxCap points.
+// Small clouds: as many as keep every tile of the grid resident at once (the
+// 160 KB of a CU shared by its tiles, less 2 KB of slack), at least 256, at
+// most kMaxCap (coarse grids, with many points per tile, have few tiles).
+// Dynamic LDS beyond 64 KB has to be granted per kernel; when that fails the
+// capacity shrinks to what 64 KB holds.
 template <typename K>
-void tile_budget(K kernel, int NT, int TV, int N, int& cap, int& stage) {
+void tile_budget(K kernel, int NT, int TV, int N, long tiles, int& cap, int& stage) {
     const bool small_cloud = N <= kSmallMaxN;
-    const int want = small_cloud ? 256 : kMaxCap;
+    int want = kMaxCap;
+    if (small_cloud) {
+        const long per_cu = std::max(1L, (tiles + kCUs - 1) / kCUs);
+        const long budget = std::min<long>(65536, 160 * 1024 / per_cu - 2048);
+        const long fit = (budget - (long)tile_lds_bytes(NT, TV, 0, 0)) / 12;
+        want = (int)std::max(256L, std::min<long>(kMaxCap, fit));
+    }
     cap = N < want ? (N > 0 ? N : 1) : want;
     stage = 0;
     const size_t small = 65536;
@@ -1022,13 +1030,13 @@ void launch_tiles_nt(const int32_t* ids, const void* feats, int feat_ld, int B, 
     int cap, stage;
     if (vec) {
         auto k = pv_voxel_tile_kernel<NT, FT, GT, true>;
-        tile_budget(k, NT, TV, N, cap, stage);
+        tile_budget(k, NT, TV, N, (long)g.x * g.y, cap, stage);
         hipLaunchKernelGGL(k, g, dim3(NT), tile_lds_bytes(NT, TV, cap, stage), s, ids,
                            (const FT*)feats, feat_ld, N, C, R, TV, cap, stage, (int)zero_rows,
                            (GT*)grid, counts, bu.bk, bu.br, bu.tcount, bu.tstart, bu.T);
     } else {
         auto k = pv_voxel_tile_kernel<NT, FT, GT, false>;
-        tile_budget(k, NT, TV, N, cap, stage);
+        tile_budget(k, NT, TV, N, (long)g.x * g.y, cap, stage);
         hipLaunchKernelGGL(k, g, dim3(NT), tile_lds_bytes(NT, TV, cap, stage), s, ids,
                            (const FT*)feats, feat_ld, N, C, R, TV, cap, 0, 0, (GT*)grid, counts,
                            bu.bk, bu.br, bu.tcount, bu.tstart, bu.T);
