@@ -262,7 +262,9 @@ __device__ __forceinline__ uint4 piece_bf16(const float* p) {
 // Requirements (checked by the launcher): Cin % 8 == 0, Cout % 4 == 0, x and
 // weight rows 16-byte aligned, residual / cloud rows 16-byte aligned, output
 // rows 16-byte (fp32) or 8-byte (bf16) aligned.
-template <int NB, int MB, int WN, int WM, typename XT>
+// EXT: a per-cloud row or a residual is given (else neither is read, and
+// the registers that prefetch them are not needed).
+template <int NB, int MB, int WN, int WM, typename XT, bool EXT>
 __global__ __launch_bounds__(256, 1) void pv_point_mlp_lds_kernel(
     const XT* __restrict__ x, int x_ld, int M, int Cin, int Cout, const uint16_t* __restrict__ w,
     PvBnFold bn, int act, float slope, const float* __restrict__ cloud_bias, int ppc,
@@ -294,6 +296,9 @@ __global__ __launch_bounds__(256, 1) void pv_point_mlp_lds_kernel(
     const int part = tid & 7;
     const uint16_t* wsrc = w + part * 8;
     const XT* xsrc = x + part * 8;
+    // The columns past C_in are zeroed when the chunk is stored to LDS, not
+    // when it is loaded: a select right after the load would make the wave
+    // wait for the load there, before the MFMAs it is meant to overlap.
     uint4 stage[S::PIECES];
     auto stage_load = [&](int k0) {
         const bool ok = k0 + part * 8 < Cin;
@@ -306,13 +311,15 @@ __global__ __launch_bounds__(256, 1) void pv_point_mlp_lds_kernel(
                 v = piece_bf16(wsrc + (size_t)min(n0 + row, Cout - 1) * Cin + k);
             else
                 v = piece_bf16(xsrc + (size_t)min(m0 + row - S::TN, M - 1) * x_ld + k);
-            stage[i] = ok ? v : uint4{0u, 0u, 0u, 0u};
+            stage[i] = v;
         }
     };
-    auto stage_store = [&](int buf) {
+    auto stage_store = [&](int buf, int k0) {
+        const bool ok = k0 + part * 8 < Cin;
         char* base = lds + buf * (S::ROWS * kGPitch) + (tid >> 3) * kGPitch + part * 16;
 #pragma unroll
-        for (int i = 0; i < S::PIECES; i++) *(uint4*)(base + i * 32 * kGPitch) = stage[i];
+        for (int i = 0; i < S::PIECES; i++)
+            *(uint4*)(base + i * 32 * kGPitch) = ok ? stage[i] : uint4{0u, 0u, 0u, 0u};
     };
 
     const int wn = wave % WN, wm = wave / WN;
@@ -330,7 +337,7 @@ __global__ __launch_bounds__(256, 1) void pv_point_mlp_lds_kernel(
 
     const int nch = (Cin + kGK - 1) / kGK;
     stage_load(0);
-    stage_store(0);
+    stage_store(0, 0);
     __syncthreads();
     for (int c = 0; c < nch; c++) {
         if (c + 1 < nch) stage_load((c + 1) * kGK);
@@ -351,43 +358,44 @@ __global__ __launch_bounds__(256, 1) void pv_point_mlp_lds_kernel(
                     acc[mb][nb] =
                         __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[nb], b[mb], acc[mb][nb], 0, 0, 0);
         }
-        if (c + 1 < nch) stage_store((c + 1) & 1);
+        if (c + 1 < nch) stage_store((c + 1) & 1, (c + 1) * kGK);
+
         __syncthreads();
     }
 
-    // Epilogue, one 32-point block (mb) at a time. acc[mb][nb][4g + j] is
-    // channel wn*NB*32 + nb*32 + 8g + 4*khalf + j of the tile at point
-    // wm*MB*32 + mb*32 + r32. The per-cloud and residual rows of block mb+1
-    // are loaded before block mb is stored: one counter tracks loads and
-    // stores alike, so a load issued after a store would wait for it.
+    // Epilogue, one (32-point block mb, 32-channel block nb) at a time.
+    // acc[mb][nb][4g + j] is channel wn*NB*32 + nb*32 + 8g + 4*khalf + j of
+    // the tile at point wm*MB*32 + mb*32 + r32. The per-cloud and residual
+    // rows of the next block are loaded before this block is stored: one
+    // counter tracks loads and stores alike, so a load issued after a store
+    // would wait for it.
     const float neg = act == PVCONV_ACT_LEAKY ? slope : (act == PVCONV_ACT_RELU ? 0.f : 1.f);
-    float4 ext[2][2][NB][4];   // [set][cloud row, residual][nb][g]
-    auto load_ext = [&](int mb, float4 (&e)[2][NB][4]) {
+    float4 ext[2][2][4];   // [set][cloud row, residual][g]
+    auto load_ext = [&](int mb, int nb, float4 (&e)[2][4]) {
         const int m = min(m0 + wm * MB * 32 + mb * 32 + r32, M - 1);
-        const float* cbr = cloud_bias ? cloud_bias + (size_t)(m / ppc) * Cout : nullptr;
-        const float* rr = residual ? residual + (size_t)m * res_ld : nullptr;
+        const float* cbr = EXT && cloud_bias ? cloud_bias + (size_t)(m / ppc) * Cout : nullptr;
+        const float* rr = EXT && residual ? residual + (size_t)m * res_ld : nullptr;
 #pragma unroll
-        for (int nb = 0; nb < NB; nb++)
-#pragma unroll
-            for (int g = 0; g < 4; g++) {
-                const int n = min(n0 + wn * NB * 32 + nb * 32 + g * 8 + 4 * khalf, Cout - 4);
-                e[0][nb][g] = cbr ? *(const float4*)(cbr + n) : float4{0.f, 0.f, 0.f, 0.f};
-                e[1][nb][g] = rr ? *(const float4*)(rr + n) : float4{0.f, 0.f, 0.f, 0.f};
-            }
+        for (int g = 0; g < 4; g++) {
+            const int n = min(n0 + wn * NB * 32 + nb * 32 + g * 8 + 4 * khalf, Cout - 4);
+            e[0][g] = cbr ? *(const float4*)(cbr + n) : float4{0.f, 0.f, 0.f, 0.f};
+            e[1][g] = rr ? *(const float4*)(rr + n) : float4{0.f, 0.f, 0.f, 0.f};
+        }
     };
-    load_ext(0, ext[0]);
+    load_ext(0, 0, ext[0]);
 #pragma unroll
     for (int mb = 0; mb < MB; mb++) {
-        if (mb + 1 < MB) load_ext(mb + 1, ext[(mb + 1) & 1]);
         const int m = m0 + wm * MB * 32 + mb * 32 + r32;
         const size_t orow = (size_t)min(m, M - 1) * out_ld;
 #pragma unroll
-        for (int nb = 0; nb < NB; nb++)
+        for (int nb = 0; nb < NB; nb++) {
+            const int blk = mb * NB + nb;
+            if (blk + 1 < MB * NB) load_ext((blk + 1) / NB, (blk + 1) % NB, ext[(blk + 1) & 1]);
 #pragma unroll
             for (int g = 0; g < 4; g++) {
                 const int nl = wn * NB * 32 + nb * 32 + g * 8 + 4 * khalf;
                 const float4 sc = tab[0][nl >> 2], sh = tab[1][nl >> 2];
-                const float4 cb = ext[mb & 1][0][nb][g], rs = ext[mb & 1][1][nb][g];
+                const float4 cb = ext[blk & 1][0][g], rs = ext[blk & 1][1][g];
                 float v[4] = {(acc[mb][nb][4 * g] + cb.x) * sc.x + sh.x,
                               (acc[mb][nb][4 * g + 1] + cb.y) * sc.y + sh.y,
                               (acc[mb][nb][4 * g + 2] + cb.z) * sc.z + sh.z,
@@ -405,6 +413,7 @@ __global__ __launch_bounds__(256, 1) void pv_point_mlp_lds_kernel(
                 else
                     *(float4*)((float*)out + orow + n0 + nl) = float4{v[0], v[1], v[2], v[3]};
             }
+        }
     }
 }
 
@@ -531,11 +540,6 @@ void launch_mfma(const void* x, int x_ld, int M, int Cin, int Cout, const void* 
                            cb, ppc, res, res_ld, out, (int)out_bf16, out_ld);
 }
 
-// ---- small-M path --------------------------------------------------------
-// Fewer rows than one tile workgroup covers (e.g. one row per cloud): one wave
-// per output element, the lanes splitting K, then a wave-wide sum. bf16
-// operands (fp32 rows rounded to bf16) with fp32 accumulation, like the MFMA
-// path.
 template <int NB, int MB, int WN, int WM, typename XT>
 void launch_lds(const void* x, int x_ld, int M, int Cin, int Cout, const void* w,
                 const PvBnFold& bn, int act, float slope, const float* cb, int ppc,
@@ -544,11 +548,23 @@ void launch_lds(const void* x, int x_ld, int M, int Cin, int Cout, const void* w
     typedef GemmShape<NB, MB, WN, WM> S;
     const int ntn = (Cout + S::TN - 1) / S::TN;
     const int nblocks = ntn * ((M + S::TM - 1) / S::TM);
-    hipLaunchKernelGGL((pv_point_mlp_lds_kernel<NB, MB, WN, WM, XT>), dim3(nblocks), dim3(256), 0,
-                       s, (const XT*)x, x_ld, M, Cin, Cout, (const uint16_t*)w, bn, act, slope, cb,
-                       ppc, res, res_ld, out, (int)out_bf16, out_ld, ntn, nblocks);
+    if (cb || res)
+        hipLaunchKernelGGL((pv_point_mlp_lds_kernel<NB, MB, WN, WM, XT, true>), dim3(nblocks),
+                           dim3(256), 0, s, (const XT*)x, x_ld, M, Cin, Cout, (const uint16_t*)w,
+                           bn, act, slope, cb, ppc, res, res_ld, out, (int)out_bf16, out_ld, ntn,
+                           nblocks);
+    else
+        hipLaunchKernelGGL((pv_point_mlp_lds_kernel<NB, MB, WN, WM, XT, false>), dim3(nblocks),
+                           dim3(256), 0, s, (const XT*)x, x_ld, M, Cin, Cout, (const uint16_t*)w,
+                           bn, act, slope, cb, ppc, res, res_ld, out, (int)out_bf16, out_ld, ntn,
+                           nblocks);
 }
 
+// ---- small-M path --------------------------------------------------------
+// Fewer rows than one tile workgroup covers (e.g. one row per cloud): one wave
+// per output element, the lanes splitting K, then a wave-wide sum. bf16
+// operands (fp32 rows rounded to bf16) with fp32 accumulation, like the MFMA
+// path.
 template <typename XT>
 __device__ __forceinline__ void load8_f32(const XT* p, float (&v)[8]);
 template <>
@@ -728,7 +744,18 @@ pvconv_status pv_launch_point_mlp(const void* x, bool x_bf16, int x_ld, int M, i
             vec && Cout % 4 == 0 && (!res || (pv_aligned16(res) && res_ld % 4 == 0)) &&
             (!cb || pv_aligned16(cb)) && out_ld % 4 == 0 &&
             ((uintptr_t)out & (out_bf16 ? 7u : 15u)) == 0;
-        // wide layers: LDS-tiled GEMM, 128-channel x 256-point tiles
+        // wide layers: LDS-tiled GEMM, 256 x 256 (channels x points) tiles
+        // when they still give a workgroup per CU, else 128 x 256
+        const long big_tiles = (long)((Cout + 255) / 256) * ((M + 255) / 256);
+        if (tile && Cin >= 128 && Cout >= 256 && big_tiles >= 256) {
+            if (x_bf16)
+                launch_lds<4, 4, 2, 2, uint16_t>(x, x_ld, M, Cin, Cout, w, bn, act, slope, cb, ppc,
+                                                 res, res_ld, out, out_bf16, out_ld, s);
+            else
+                launch_lds<4, 4, 2, 2, float>(x, x_ld, M, Cin, Cout, w, bn, act, slope, cb, ppc,
+                                              res, res_ld, out, out_bf16, out_ld, s);
+            return pv_launch_status();
+        }
         if (tile && Cin >= 128 && Cout >= 128) {
             if (x_bf16)
                 launch_lds<4, 2, 1, 4, uint16_t>(x, x_ld, M, Cin, Cout, w, bn, act, slope, cb, ppc,

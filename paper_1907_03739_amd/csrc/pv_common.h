@@ -12,6 +12,16 @@ typedef __attribute__((__vector_size__(4 * sizeof(float)))) float pv_f32x4;
 
 // bfloat16 <-> float on raw bits. float -> bf16 uses gfx950's conversion
 // instruction (round to nearest, ties to even; NaN stays NaN), no branches.
+// Workgroup barrier for LDS data only: orders the LDS accesses around it
+// and, unlike __syncthreads(), does not wait for outstanding global loads
+// and stores, so loads issued for later work stay in flight across it. Only
+// for barriers that hand LDS data between threads.
+__device__ __forceinline__ void pv_lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 __device__ __forceinline__ float pv_bf16_to_f32(uint16_t h) {
     return __uint_as_float(((uint32_t)h) << 16);
 }

@@ -127,13 +127,14 @@ def test_voxelize_crowded_tiles(N, spread):
 
 @pytest.mark.parametrize("N,R,C,gdt", [(2048, 32, 64, torch.bfloat16), (3000, 7, 16, torch.float32),
                                         (20000, 31, 32, torch.bfloat16), (1, 5, 8, torch.float32)],
-                         ids=["ids_launch", "odd_R", "split_path", "one_point"])
+                         ids=["vec_rows", "odd_R", "split_path", "one_point"])
 def test_voxelize_writes_every_row_of_a_dirty_grid(N, R, C, gdt):
-    # Empty rows are written by two kernels (the rows of voxels outside the
-    # normalisation ball by the normalisation launch, the rest by the tile
-    # kernel): with the grid filled with NaN beforehand every row must come
-    # out right. Half the points lie on a sphere, so after normalisation they
-    # sit on the ball's surface, the other half inside it.
+    # Every grid row is written by the kernels (empty rows as zeros by the
+    # tile kernel, or by the normalisation launch for rows that are not
+    # 16-byte vectors): with the grid filled with NaN beforehand every row
+    # must come out right. Half the points lie on a sphere, so after
+    # normalisation they sit on the ball's surface (the cells on the grid's
+    # edge), the other half inside it.
     rng = np.random.default_rng(N + R)
     B = 2
     d = rng.normal(size=(B, N, 3))
@@ -313,6 +314,8 @@ MLP_CASES = [
     (3000, 200, 136, "bf16", True, True, "leaky", True, 0),   # wide: ragged K chunk and tiles
     (16384, 512, 2048, "bf16", False, True, "relu", False, 0),  # wide: part-seg MLP 512->2048
     (4100, 2880, 256, "bf16", False, True, "relu", False, 2050),  # wide: head with cloud rows
+    (65600, 160, 264, "bf16", True, True, "leaky", True, 0),  # 256x256 tiles: ragged M, N, K
+    (65536, 128, 256, "f32", False, True, "relu", True, 2048),  # 256x256 tiles: cloud rows
     (8, 2048, 256, "f32", False, False, "none", False, 0),    # one row per cloud (global)
     (100, 72, 36, "bf16", True, True, "leaky", True, 50),     # few rows, 2 clouds
     (37, 9, 5, "bf16", True, True, "relu", True, 0),          # few rows, odd widths
