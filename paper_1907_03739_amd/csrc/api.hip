@@ -233,13 +233,20 @@ pvconv_status pvconv_forward(const float* coords, const void* feats, pvconv_dtyp
     st = pv_launch_voxelize(coords, feats, feat_dt == PVCONV_BF16, feat_ld, B, N, L->cin, R,
                             w.grid_a, bf, w.counts, w.ids, w.pnorm, w.vox_ws, s);
     if (st != PVCONV_OK) return st;
+    // bf16: the weights of all the convolutions repacked in one launch
+    if (bf) {
+        PvPackJobs jobs{};
+        for (int i = 0; i < L->n_convs; i++)
+            pv_pack_job(jobs, L->conv_w[i], i ? L->cout : L->cin, L->cout, w.conv_ws[i]);
+        pv_launch_pack_conv_weights(jobs, s);
+    }
     void* src = w.grid_a;
     void* dst = w.grid_b;
     int cin = L->cin;
     for (int i = 0; i < L->n_convs; i++) {
         st = pv_launch_conv3d(src, B, R, cin, L->cout, L->conv_w[i],
                               pv_make_fold(&L->conv_bn[i], nullptr), PVCONV_ACT_LEAKY,
-                              L->conv_slope, bf, dst, bf, w.conv_ws[i], s);
+                              L->conv_slope, bf, dst, bf, w.conv_ws[i], s, /*packed=*/bf);
         if (st != PVCONV_OK) return st;
         void* t = src;
         src = dst;

@@ -247,76 +247,89 @@ __global__ __launch_bounds__(256 * WCH, 1) void pv_conv3d_bf16_kernel(
     // tile is staged in LDS in passes of PW channels (256 bytes per voxel),
     // then each thread copies 16-byte pieces out, so every store instruction
     // writes whole contiguous rows.
-    constexpr int PW_BF16 = NT < 128 ? NT : 128, PW_F32 = NT < 64 ? NT : 64;
-    const int esz = out_bf16 ? 2 : 4;
-    const int PW = out_bf16 ? PW_BF16 : PW_F32;
-    const int rowb = PW * esz;            // bytes of one voxel's pass row
-    const int pieces = rowb / 16;         // 16-byte pieces per voxel row
-    const size_t yrow = (size_t)Cout * esz;
-    for (int pass = 0; pass * PW < NT; pass++) {
-#pragma clang loop unroll(full)
-        for (int nb = 0; nb < NBW; nb++) {
-#pragma clang loop unroll(full)
-            for (int j = 0; j < 4; j++) {
-                const int nl = (wc * NBW + nb) * 32 + 8 * j + 4 * khalf;  // channel in the tile
-                if (nl < pass * PW || nl >= (pass + 1) * PW) continue;
-                const float4 sc = *(const float4*)&bn_tab[0][nl];
-                const float4 sh = *(const float4*)&bn_tab[1][nl];
-                const int cb = (nl - pass * PW) * esz;       // byte offset in the row
-#pragma clang loop unroll(full)
-                for (int mb = 0; mb < 4; mb++) {
-                    const int vox = (2 * wv + (mb >> 1)) * 64 + ((mb & 1) * 4 + (r32 >> 3)) * 8 +
-                                    (r32 & 7);
-                    float r[4];
-                    r[0] = pv_activate(acc[mb][nb][4 * j + 0] * sc.x + sh.x, act, slope);
-                    r[1] = pv_activate(acc[mb][nb][4 * j + 1] * sc.y + sh.y, act, slope);
-                    r[2] = pv_activate(acc[mb][nb][4 * j + 2] * sc.z + sh.z, act, slope);
-                    r[3] = pv_activate(acc[mb][nb][4 * j + 3] * sc.w + sh.w, act, slope);
-                    char* d = lds + vox * kStageRow + cb;
-                    if (out_bf16)
-                        *(uint2*)d = make_uint2(pv_pack_bf16x2(r[0], r[1]), pv_pack_bf16x2(r[2], r[3]));
-                    else
-                        *(float4*)d = make_float4(r[0], r[1], r[2], r[3]);
-                }
-                __builtin_amdgcn_sched_barrier(0);
-            }
-        }
-        __syncthreads();
-        // copy out: piece k of voxel vox (k < pieces)
-        const size_t col = ((size_t)n0 + pass * PW) * esz;
-        for (int i = tid; i < 512 * pieces; i += NTH) {
-            const int vox = i / pieces, k = i - vox * pieces;
-            const int u = u0 + (vox >> 6), v = v0 + ((vox >> 3) & 7), ww = w0 + (vox & 7);
-            if (u >= R || v >= R || ww >= R) continue;
-            const uint4 val = *(const uint4*)(lds + vox * kStageRow + k * 16);
-            char* dst = (char*)y + (cloud + ((size_t)u * R + v) * R + ww) * yrow + col + k * 16;
-            if (vec_out) {
-                *(uint4*)dst = val;
-            } else {
-                const uint32_t q[4] = {val.x, val.y, val.z, val.w};
-                for (int e = 0; e < 16 / esz; e++) {
-                    if (out_bf16)
-                        ((uint16_t*)dst)[e] = (uint16_t)(q[e >> 1] >> ((e & 1) * 16));
-                    else
-                        ((uint32_t*)dst)[e] = q[e];
+    // The output type is a compile-time branch of the epilogue (one straight
+    // copy per type), so that the per-element code carries no type tests.
+    const float neg = act == PVCONV_ACT_LEAKY ? slope : (act == PVCONV_ACT_RELU ? 0.f : 1.f);
+    auto epilogue = [&](auto out_type) {
+        constexpr bool OBF = decltype(out_type)::value;
+        constexpr int esz = OBF ? 2 : 4;
+        constexpr int PW = OBF ? (NT < 128 ? NT : 128) : (NT < 64 ? NT : 64);
+        constexpr int pieces = PW * esz / 16;  // 16-byte pieces per voxel row
+        const size_t yrow = (size_t)Cout * esz;
+#pragma unroll
+        for (int pass = 0; pass * PW < NT; pass++) {
+#pragma unroll
+            for (int nb = 0; nb < NBW; nb++) {
+#pragma unroll
+                for (int j = 0; j < 4; j++) {
+                    const int nl = (wc * NBW + nb) * 32 + 8 * j + 4 * khalf;  // channel in the tile
+                    if (nl < pass * PW || nl >= (pass + 1) * PW) continue;
+                    const float4 sc = *(const float4*)&bn_tab[0][nl];
+                    const float4 sh = *(const float4*)&bn_tab[1][nl];
+                    const int cb = (nl - pass * PW) * esz;  // byte offset in the row
+#pragma unroll
+                    for (int mb = 0; mb < 4; mb++) {
+                        const int vox = (2 * wv + (mb >> 1)) * 64 +
+                                        ((mb & 1) * 4 + (r32 >> 3)) * 8 + (r32 & 7);
+                        float r[4] = {acc[mb][nb][4 * j + 0] * sc.x + sh.x,
+                                      acc[mb][nb][4 * j + 1] * sc.y + sh.y,
+                                      acc[mb][nb][4 * j + 2] * sc.z + sh.z,
+                                      acc[mb][nb][4 * j + 3] * sc.w + sh.w};
+#pragma unroll
+                        for (int e = 0; e < 4; e++) r[e] = r[e] >= 0.f ? r[e] : r[e] * neg;
+                        char* d = lds + vox * kStageRow + cb;
+                        if constexpr (OBF)
+                            *(uint2*)d = make_uint2(pv_pack_bf16x2(r[0], r[1]),
+                                                    pv_pack_bf16x2(r[2], r[3]));
+                        else
+                            *(float4*)d = make_float4(r[0], r[1], r[2], r[3]);
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
                 }
             }
+            pv_lds_barrier();
+            // copy out: piece k of voxel vox (k < pieces)
+            const size_t col = ((size_t)n0 + pass * PW) * esz;
+            for (int i = tid; i < 512 * pieces; i += NTH) {
+                const int vox = i / pieces, k = i % pieces;
+                const int u = u0 + (vox >> 6), v = v0 + ((vox >> 3) & 7), ww = w0 + (vox & 7);
+                if (u >= R || v >= R || ww >= R) continue;
+                const uint4 val = *(const uint4*)(lds + vox * kStageRow + k * 16);
+                char* dst = (char*)y + (cloud + ((size_t)u * R + v) * R + ww) * yrow + col + k * 16;
+                if (vec_out) {
+                    *(uint4*)dst = val;
+                } else {
+                    const uint32_t q[4] = {val.x, val.y, val.z, val.w};
+                    for (int e = 0; e < 16 / esz; e++) {
+                        if constexpr (OBF)
+                            ((uint16_t*)dst)[e] = (uint16_t)(q[e >> 1] >> ((e & 1) * 16));
+                        else
+                            ((uint32_t*)dst)[e] = q[e];
+                    }
+                }
+            }
+            pv_lds_barrier();
         }
-        __syncthreads();
-    }
+    };
+    if (out_bf16)
+        epilogue(std::integral_constant<bool, true>{});
+    else
+        epilogue(std::integral_constant<bool, false>{});
 }
 
 // Repack bf16 weights [Cout][27][Cin] into the fragment order the MFMA conv
 // reads: 16-byte element ((c*27 + t)*G + g)*64 + lane holds the 8 channels
 // k = c*16 + (lane/32)*8 .. +7 of output channel g*32 + lane%32 at tap t
-// (zero past Cin), G = Cout/32. One thread per element.
-__global__ __launch_bounds__(256) void pv_pack_conv_weights_kernel(const uint16_t* __restrict__ w,
-                                                                   uint4* __restrict__ packed,
-                                                                   int Cin, int Cout, int total,
-                                                                   int vec) {
-    const int i = blockIdx.x * 256 + threadIdx.x;
-    if (i >= total) return;
-    const int G = Cout / 32;
+// (zero past Cin), G = Cout/32. One thread per element; one launch packs the
+// weights of all the convolutions of a layer (the blocks of job q follow those of
+// jobs 0 .. q-1).
+__global__ __launch_bounds__(256) void pv_pack_conv_weights_kernel(PvPackJobs jobs) {
+    int blk = blockIdx.x, q = 0;
+    while (q + 1 < jobs.n && blk >= jobs.job[q].blocks) blk -= jobs.job[q++].blocks;
+    const PvPackJob& J = jobs.job[q];
+    const int i = blk * 256 + threadIdx.x;
+    if (i >= J.total) return;
+    const int G = J.Cout / 32;
     const int lane = i & 63;
     int r = i >> 6;
     const int g = r % G;
@@ -325,15 +338,15 @@ __global__ __launch_bounds__(256) void pv_pack_conv_weights_kernel(const uint16_
     const int c = r / kTaps;
     const int n = g * 32 + (lane & 31);
     const int k = c * kKC + (lane >> 5) * 8;
-    const uint16_t* src = w + ((size_t)n * kTaps + t) * Cin;
-    if (vec) {  // Cin % 8 == 0 and 16-byte aligned rows: one load
-        packed[i] = k < Cin ? *(const uint4*)(src + k) : make_uint4(0u, 0u, 0u, 0u);
+    const uint16_t* src = J.w + ((size_t)n * kTaps + t) * J.Cin;
+    if (J.vec) {  // Cin % 8 == 0 and 16-byte aligned rows: one load
+        J.packed[i] = k < J.Cin ? *(const uint4*)(src + k) : make_uint4(0u, 0u, 0u, 0u);
         return;
     }
     uint16_t e[8];
 #pragma unroll
-    for (int j = 0; j < 8; j++) e[j] = k + j < Cin ? src[k + j] : (uint16_t)0;
-    packed[i] = pack8(e);
+    for (int j = 0; j < 8; j++) e[j] = k + j < J.Cin ? src[k + j] : (uint16_t)0;
+    J.packed[i] = pack8(e);
 }
 
 // fp32 path: four consecutive lanes per output (voxel, channel), each
@@ -415,15 +428,34 @@ size_t pv_conv3d_ws_bytes(int Cin, int Cout, bool bf16) {
     return nch * kKC * kTaps * (size_t)Cout * 2;
 }
 
+void pv_pack_job(PvPackJobs& jobs, const void* w, int Cin, int Cout, void* packed) {
+    PvPackJob& J = jobs.job[jobs.n++];
+    J.w = (const uint16_t*)w;
+    J.packed = (uint4*)packed;
+    J.Cin = Cin;
+    J.Cout = Cout;
+    J.total = (int)(pv_conv3d_ws_bytes(Cin, Cout, true) / 16);
+    J.vec = (int)(Cin % 8 == 0 && pv_aligned16(w));
+    J.blocks = (J.total + 255) / 256;
+}
+
+void pv_launch_pack_conv_weights(const PvPackJobs& jobs, hipStream_t s) {
+    int blocks = 0;
+    for (int q = 0; q < jobs.n; q++) blocks += jobs.job[q].blocks;
+    if (blocks > 0)
+        hipLaunchKernelGGL(pv_pack_conv_weights_kernel, dim3(blocks), dim3(256), 0, s, jobs);
+}
+
 pvconv_status pv_launch_conv3d(const void* x, int B, int R, int Cin, int Cout, const void* w,
                                const PvBnFold& bn, int act, float slope, bool bf16, void* y,
-                               bool out_bf16, void* ws, hipStream_t s) {
+                               bool out_bf16, void* ws, hipStream_t s, bool packed) {
     if (B == 0) return PVCONV_OK;
     if (bf16) {
-        const int total = (int)(pv_conv3d_ws_bytes(Cin, Cout, true) / 16);
-        hipLaunchKernelGGL(pv_pack_conv_weights_kernel, dim3((total + 255) / 256), dim3(256), 0,
-                           s, (const uint16_t*)w, (uint4*)ws, Cin, Cout, total,
-                           (int)(Cin % 8 == 0 && pv_aligned16(w)));
+        if (!packed) {
+            PvPackJobs jobs{};
+            pv_pack_job(jobs, w, Cin, Cout, ws);
+            pv_launch_pack_conv_weights(jobs, s);
+        }
         w = ws;
         const bool vec = (Cin % 8 == 0) && pv_aligned16(x);
         // Channel tile: the widest (most reuse of each halo) that still gives

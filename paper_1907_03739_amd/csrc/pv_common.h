@@ -95,9 +95,24 @@ pvconv_status pv_launch_voxelize(const float* coords, const void* feats, bool fe
                                  bool grid_bf16, int32_t* counts, int32_t* vox_id,
                                  float* norm_coords, void* ws, hipStream_t s);
 size_t pv_conv3d_ws_bytes(int Cin, int Cout, bool bf16);
+// bf16 conv weights [Cout][27][Cin] repacked into the MFMA fragment order
+// (into a workspace of pv_conv3d_ws_bytes), the convolutions of a layer in one
+// launch
+struct PvPackJob {
+    const uint16_t* w;
+    uint4* packed;
+    int Cin, Cout, total, vec, blocks;
+};
+struct PvPackJobs {
+    PvPackJob job[PVCONV_MAX_CONVS];
+    int n;
+};
+void pv_pack_job(PvPackJobs& jobs, const void* w, int Cin, int Cout, void* packed);
+void pv_launch_pack_conv_weights(const PvPackJobs& jobs, hipStream_t s);
+// packed: the bf16 weights are already repacked in ws (w is then unused)
 pvconv_status pv_launch_conv3d(const void* x, int B, int R, int Cin, int Cout, const void* w,
                                const PvBnFold& bn, int act, float slope, bool bf16, void* y,
-                               bool out_bf16, void* ws, hipStream_t s);
+                               bool out_bf16, void* ws, hipStream_t s, bool packed = false);
 pvconv_status pv_launch_devoxelize(const void* grid, int B, int R, int C, bool grid_bf16,
                                    const float* pn, int N, float* out, hipStream_t s);
 pvconv_status pv_launch_point_mlp(const void* x, bool x_bf16, int x_ld, int M, int Cin,
