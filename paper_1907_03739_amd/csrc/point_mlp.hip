@@ -11,7 +11,9 @@
 // holding four consecutive output channels of one point; the epilogue adds
 // bias and the per-cloud row, applies the folded batch norm (from a table in
 // LDS) and the activation, adds the residual and writes 16-byte (8-byte for
-// bf16) vectors. Shapes that rule out vector access take the scalar kernel.
+// bf16) vectors. Shapes that rule out vector access load value by value
+// (ragged or unaligned C_in) or read and write channel by channel (ragged
+// C_out or unaligned rows).
 #include "pv_common.h"
 
 namespace {
@@ -87,10 +89,12 @@ struct RawOf<uint16_t> {
     typedef uint4 T;
 };
 
-// Requirements (checked by the launcher): Cin % 8 == 0, Cout % 4 == 0, x rows
-// and weight rows 16-byte aligned, residual / cloud rows 16-byte aligned,
-// output rows 16-byte (fp32) or 8-byte (bf16) aligned.
-template <int NB, typename XT>
+// VEC (checked by the launcher): Cin % 8 == 0, x rows and weight rows
+// 16-byte aligned; else every operand value is loaded on its own, with zero
+// past Cin. C4 (checked by the launcher): Cout % 4 == 0, residual / cloud
+// rows 16-byte aligned, output rows 16-byte (fp32) or 8-byte (bf16) aligned;
+// else the epilogue reads and writes channel by channel.
+template <int NB, typename XT, bool VEC, bool C4>
 __global__ __launch_bounds__(kWaves * 64) void pv_point_mlp_tile_kernel(
     const XT* __restrict__ x, int x_ld, int M, int Cin, int Cout, const uint16_t* __restrict__ w,
     PvBnFold bn, int act, float slope, const float* __restrict__ cloud_bias, int ppc,
@@ -121,14 +125,22 @@ __global__ __launch_bounds__(kWaves * 64) void pv_point_mlp_tile_kernel(
     for (int nb = 0; nb < NB; nb++)
         wr[nb] = w + (size_t)min(n0 + nb * 32 + r32, Cout - 1) * Cin + 8 * h;
 
-    // Column offsets of this lane's four-channel groups, clamped into the
+    // Column offsets of this lane's four-channel groups. C4: clamped into the
     // valid columns so that every load below is unconditional (one batch,
-    // no branches between loads); clamped groups are never stored.
+    // no branches between loads); clamped groups are never stored. Else
+    // unclamped, each channel checked against Cout.
     int coff[NB][4];
 #pragma unroll
     for (int nb = 0; nb < NB; nb++)
 #pragma unroll
-        for (int g = 0; g < 4; g++) coff[nb][g] = n0 + min(nb * 32 + g * 8 + 4 * h, ncols - 4);
+        for (int g = 0; g < 4; g++)
+            coff[nb][g] = n0 + (C4 ? min(nb * 32 + g * 8 + 4 * h, ncols - 4) : nb * 32 + g * 8 + 4 * h);
+    // four channels from row p at column c (C4: one 16-byte load)
+    auto row4 = [&](const float* p, int c) -> float4 {
+        if constexpr (C4) return *(const float4*)(p + c);
+        return float4{c < Cout ? p[c] : 0.f, c + 1 < Cout ? p[c + 1] : 0.f,
+                      c + 2 < Cout ? p[c + 2] : 0.f, c + 3 < Cout ? p[c + 3] : 0.f};
+    };
 
     // The residual rows go in flight first: they are consumed last.
     float4 res[NB][4];
@@ -137,7 +149,7 @@ __global__ __launch_bounds__(kWaves * 64) void pv_point_mlp_tile_kernel(
 #pragma unroll
         for (int nb = 0; nb < NB; nb++)
 #pragma unroll
-            for (int g = 0; g < 4; g++) res[nb][g] = *(const float4*)(rr + coff[nb][g]);
+            for (int g = 0; g < 4; g++) res[nb][g] = row4(rr, coff[nb][g]);
     } else {
 #pragma unroll
         for (int nb = 0; nb < NB; nb++)
@@ -152,7 +164,28 @@ __global__ __launch_bounds__(kWaves * 64) void pv_point_mlp_tile_kernel(
         for (int e = 0; e < 16; e++) acc[nb][e] = 0.f;
 
     typedef typename RawOf<XT>::T XRaw;
-    for (int k0 = 0; k0 < Cin; k0 += 64) {
+    if constexpr (!VEC) {
+        for (int k0 = 0; k0 < Cin; k0 += 64) {
+            pv_bf16x8 xg[4], wg[4][NB];
+#pragma unroll
+            for (int ks = 0; ks < 4; ks++) {
+                const int k = k0 + ks * 16 + 8 * h;   // this lane's 8 values of the step
+                const int valid = max(0, min(8, Cin - k));
+                xg[ks] = load_a8<XT>(x + (size_t)m * x_ld + k, false, valid);
+#pragma unroll
+                for (int nb = 0; nb < NB; nb++)
+                    wg[ks][nb] = load_a8<uint16_t>(
+                        w + (size_t)min(n0 + nb * 32 + r32, Cout - 1) * Cin + k, false, valid);
+            }
+#pragma unroll
+            for (int ks = 0; ks < 4; ks++)
+#pragma unroll
+                for (int nb = 0; nb < NB; nb++)
+                    acc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wg[ks][nb], xg[ks], acc[nb],
+                                                                      0, 0, 0);
+        }
+    }
+    for (int k0 = 0; VEC && k0 < Cin; k0 += 64) {
         XRaw xf[4];
         uint4 wf[4][NB];
         bool kv[4];
@@ -185,7 +218,7 @@ __global__ __launch_bounds__(kWaves * 64) void pv_point_mlp_tile_kernel(
 #pragma unroll
         for (int nb = 0; nb < NB; nb++)
 #pragma unroll
-            for (int g = 0; g < 4; g++) cb[nb][g] = *(const float4*)(cbr + coff[nb][g]);
+            for (int g = 0; g < 4; g++) cb[nb][g] = row4(cbr, coff[nb][g]);
 #pragma unroll
         for (int nb = 0; nb < NB; nb++)
 #pragma unroll
@@ -220,11 +253,20 @@ __global__ __launch_bounds__(kWaves * 64) void pv_point_mlp_tile_kernel(
         for (int g = 0; g < 4; g++) {
             if (nb * 32 + g * 8 + 4 * h >= ncols) continue;
             const float4 v = res[nb][g];
-            if (out_bf16)
+            if constexpr (!C4) {
+                const float e[4] = {v.x, v.y, v.z, v.w};
+                for (int j = 0; j < 4 && coff[nb][g] + j < Cout; j++) {
+                    if (out_bf16)
+                        ((uint16_t*)out)[orow + coff[nb][g] + j] = pv_f32_to_bf16(e[j]);
+                    else
+                        ((float*)out)[orow + coff[nb][g] + j] = e[j];
+                }
+            } else if (out_bf16) {
                 *(uint2*)((uint16_t*)out + orow + coff[nb][g]) =
                     uint2{pv_pack_bf16x2(v.x, v.y), pv_pack_bf16x2(v.z, v.w)};
-            else
+            } else {
                 *(float4*)((float*)out + orow + coff[nb][g]) = v;
+            }
         }
 }
 
@@ -417,61 +459,6 @@ __global__ __launch_bounds__(256, 1) void pv_point_mlp_lds_kernel(
     }
 }
 
-// Scalar-epilogue kernel for shapes the tile kernel cannot take (odd channel
-// counts or unaligned rows): one wave per 32 points x (32*NB) channels with
-// the points as the A operand.
-template <int NB, bool VEC, typename XT>
-__global__ __launch_bounds__(kWaves * 64) void pv_point_mlp_bf16_kernel(
-    const XT* __restrict__ x, int x_ld, int M, int Cin, int Cout, const uint16_t* __restrict__ w,
-    PvBnFold bn, int act, float slope, const float* __restrict__ cloud_bias, int ppc,
-    const float* __restrict__ residual, int res_ld, void* __restrict__ out, int out_bf16,
-    int out_ld) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int m0 = (blockIdx.x * kWaves + wave) * 32;
-    const int n0 = blockIdx.y * (NB * 32);
-    if (m0 >= M) return;
-    const int r32 = lane & 31, khalf = (lane >> 5) * 8;
-    const int m = m0 + r32;
-    const bool mrow = m < M;
-    const XT* xr = x + (size_t)(mrow ? m : 0) * x_ld;
-
-    pv_f32x16 acc[NB];
-    for (int j = 0; j < NB; j++)
-        for (int e = 0; e < 16; e++) acc[j][e] = 0.f;
-
-    for (int k0 = 0; k0 < Cin; k0 += 16) {
-        const int k = k0 + khalf;
-        const int valid = mrow ? max(0, min(8, Cin - k)) : 0;
-        const pv_bf16x8 a = load_a8<XT>(xr + k, VEC && valid == 8, valid);
-        for (int nb = 0; nb < NB; nb++) {
-            const int n = n0 + nb * 32 + r32;
-            const int wv = n < Cout ? max(0, min(8, Cin - k)) : 0;
-            const pv_bf16x8 bfr =
-                load_a8<uint16_t>(w + (size_t)(n < Cout ? n : 0) * Cin + k, VEC && wv == 8, wv);
-            acc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bfr, acc[nb], 0, 0, 0);
-        }
-    }
-
-    for (int nb = 0; nb < NB; nb++) {
-        const int n = n0 + nb * 32 + r32;
-        if (n >= Cout) continue;
-        float scale, shift;
-        pv_bn_coeffs(bn, n, scale, shift);
-        for (int e = 0; e < 16; e++) {
-            const int mm = m0 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-            if (mm >= M) continue;
-            float v = acc[nb][e];
-            if (cloud_bias) v += cloud_bias[(size_t)(mm / ppc) * Cout + n];
-            v = pv_activate(v * scale + shift, act, slope);
-            if (residual) v += residual[(size_t)mm * res_ld + n];
-            if (out_bf16)
-                ((uint16_t*)out)[(size_t)mm * out_ld + n] = pv_f32_to_bf16(v);
-            else
-                ((float*)out)[(size_t)mm * out_ld + n] = v;
-        }
-    }
-}
-
 template <typename XT>
 __device__ __forceinline__ float ld1(const XT* p);
 template <>
@@ -522,22 +509,20 @@ __global__ __launch_bounds__(256) void pv_point_mlp_f32_kernel(
 
 template <int NB, typename XT>
 void launch_mfma(const void* x, int x_ld, int M, int Cin, int Cout, const void* w, bool vec,
-                 bool tile, const PvBnFold& bn, int act, float slope, const float* cb, int ppc,
+                 bool c4, const PvBnFold& bn, int act, float slope, const float* cb, int ppc,
                  const float* res, int res_ld, void* out, bool out_bf16, int out_ld,
                  hipStream_t s) {
     dim3 g((M + kWaves * 32 - 1) / (kWaves * 32), (Cout + NB * 32 - 1) / (NB * 32));
-    if (tile)
-        hipLaunchKernelGGL((pv_point_mlp_tile_kernel<NB, XT>), g, dim3(kWaves * 64), 0, s,
-                           (const XT*)x, x_ld, M, Cin, Cout, (const uint16_t*)w, bn, act, slope,
-                           cb, ppc, res, res_ld, out, (int)out_bf16, out_ld);
-    else if (vec)
-        hipLaunchKernelGGL((pv_point_mlp_bf16_kernel<NB, true, XT>), g, dim3(kWaves * 64), 0, s,
-                           (const XT*)x, x_ld, M, Cin, Cout, (const uint16_t*)w, bn, act, slope,
-                           cb, ppc, res, res_ld, out, (int)out_bf16, out_ld);
-    else
-        hipLaunchKernelGGL((pv_point_mlp_bf16_kernel<NB, false, XT>), g, dim3(kWaves * 64), 0, s,
-                           (const XT*)x, x_ld, M, Cin, Cout, (const uint16_t*)w, bn, act, slope,
-                           cb, ppc, res, res_ld, out, (int)out_bf16, out_ld);
+#define PV_TILE(V, C)                                                                         \
+    hipLaunchKernelGGL((pv_point_mlp_tile_kernel<NB, XT, V, C>), g, dim3(kWaves * 64), 0, s, \
+                       (const XT*)x, x_ld, M, Cin, Cout, (const uint16_t*)w, bn, act, slope,   \
+                       cb, ppc, res, res_ld, out, (int)out_bf16, out_ld)
+    if (vec) {
+        if (c4) PV_TILE(true, true); else PV_TILE(true, false);
+    } else {
+        if (c4) PV_TILE(false, true); else PV_TILE(false, false);
+    }
+#undef PV_TILE
 }
 
 template <int NB, int MB, int WN, int WM, typename XT>
@@ -740,10 +725,12 @@ pvconv_status pv_launch_point_mlp(const void* x, bool x_bf16, int x_ld, int M, i
         const size_t esz = x_bf16 ? 2 : 4;
         const bool vec = Cin % 8 == 0 && pv_aligned16(x) && pv_aligned16(w) &&
                          ((size_t)x_ld * esz) % 16 == 0;
-        const bool tile =
-            vec && Cout % 4 == 0 && (!res || (pv_aligned16(res) && res_ld % 4 == 0)) &&
-            (!cb || pv_aligned16(cb)) && out_ld % 4 == 0 &&
-            ((uintptr_t)out & (out_bf16 ? 7u : 15u)) == 0;
+        // c4: four-channel groups of the residual, cloud and output rows are
+        // whole aligned vectors
+        const bool c4 = Cout % 4 == 0 && (!res || (pv_aligned16(res) && res_ld % 4 == 0)) &&
+                        (!cb || pv_aligned16(cb)) && out_ld % 4 == 0 &&
+                        ((uintptr_t)out & (out_bf16 ? 7u : 15u)) == 0;
+        const bool tile = vec && c4;
         // wide layers: LDS-tiled GEMM, 256 x 256 (channels x points) tiles
         // when they still give a workgroup per CU, else 128 x 256
         const long big_tiles = (long)((Cout + 255) / 256) * ((M + 255) / 256);
@@ -767,17 +754,17 @@ pvconv_status pv_launch_point_mlp(const void* x, bool x_bf16, int x_ld, int M, i
         }
         if (x_bf16) {
             if (Cout > 64)
-                launch_mfma<4, uint16_t>(x, x_ld, M, Cin, Cout, w, vec, tile, bn, act, slope, cb,
+                launch_mfma<4, uint16_t>(x, x_ld, M, Cin, Cout, w, vec, c4, bn, act, slope, cb,
                                          ppc, res, res_ld, out, out_bf16, out_ld, s);
             else
-                launch_mfma<2, uint16_t>(x, x_ld, M, Cin, Cout, w, vec, tile, bn, act, slope, cb,
+                launch_mfma<2, uint16_t>(x, x_ld, M, Cin, Cout, w, vec, c4, bn, act, slope, cb,
                                          ppc, res, res_ld, out, out_bf16, out_ld, s);
         } else {
             if (Cout > 64)
-                launch_mfma<4, float>(x, x_ld, M, Cin, Cout, w, vec, tile, bn, act, slope, cb,
+                launch_mfma<4, float>(x, x_ld, M, Cin, Cout, w, vec, c4, bn, act, slope, cb,
                                       ppc, res, res_ld, out, out_bf16, out_ld, s);
             else
-                launch_mfma<2, float>(x, x_ld, M, Cin, Cout, w, vec, tile, bn, act, slope, cb,
+                launch_mfma<2, float>(x, x_ld, M, Cin, Cout, w, vec, c4, bn, act, slope, cb,
                                       ppc, res, res_ld, out, out_bf16, out_ld, s);
         }
     } else {
