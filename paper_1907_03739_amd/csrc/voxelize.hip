@@ -31,6 +31,9 @@ constexpr int kNormPts = 1024;      // points per workgroup, large-cloud normali
 constexpr int kNormThreads = 256;
 constexpr int kSmallMaxN = 4096;    // largest cloud normalised by one kernel
 constexpr int kHeavy = 32;          // voxels with more points are summed by a whole wave
+constexpr int kExport = 32;         // large clouds: voxels with more points go to the heavy-voxel kernel
+constexpr int kChunk = 256;         // points per work item of the heavy-voxel kernel
+constexpr int kHeavyMaxC = 128;     // ... for up to this many channels (its sums' workspace)
 constexpr int kMaxCap = 4096;       // tile points kept in LDS at once
 constexpr int kCUs = 256;           // compute units of an MI355X
 
@@ -293,6 +296,12 @@ struct SplitWs {
     int* br;
     int T;
     int TV;
+    // heavy-voxel queue: hq[0] entries, then (cloud, voxel, bucket offset,
+    // points) per voxel; room for hmax voxels. hpart [chunks][C] fp64 sums of
+    // each chunk of kChunk points (room for C <= kHeavyMaxC).
+    int* hq;
+    int hmax;
+    double* hpart;
 };
 
 __device__ void combine_absmax(const SplitWs& ws, int b, float* redf, float (&A)[3]) {
@@ -324,9 +333,11 @@ __global__ __launch_bounds__(kNormThreads) void pv_norm_absmax_kernel(const floa
         zero_fill_role(grid16, n16, blockIdx.x - nid, gridDim.x - nid);
         return;
     }
-    if (blockIdx.x == 0)  // the tile counters start at zero (used two launches later)
+    if (blockIdx.x == 0) {  // the tile counters start at zero (used two launches later)
         for (int i = threadIdx.x; i < 2 * B * ws.T; i += kNormThreads)
             (i < B * ws.T ? ws.tcount : ws.tcursor)[i % (B * ws.T)] = 0;
+        if (threadIdx.x == 0 && ws.hq) ws.hq[0] = 0;
+    }
     const int g = blockIdx.x % ws.G, b = blockIdx.x / ws.G;
     const float* p = coords + (size_t)b * N * 3;
     const int k0 = g * kNormPts, k1 = min(N, k0 + kNormPts);
@@ -574,6 +585,17 @@ __device__ inline TileLds tile_lds(char* smem, int TV, int CAP) {
     return L;
 }
 
+// Where a tile hands its heaviest voxels (more than kExport points) to the
+// heavy-voxel kernel instead of summing them itself: their sorted point
+// lists go back to the tile's bucket (global, from bstart), one queue entry
+// each. hq == nullptr: no export.
+struct HeavyOut {
+    int* hq;
+    int* bucket;   // the tile's bucket: point indices, from the tile's first
+    int b, vox0;   // cloud, first voxel of the tile
+    int bstart;    // bucket offset of the tile within the cloud
+};
+
 // Means of voxels [lo, hi) of the tile from list (voxel vi's points at
 // list[start[vi] - base .. start[vi+1] - base)), written to out (the tile's
 // grid rows).
@@ -590,7 +612,7 @@ __device__ inline TileLds tile_lds(char* smem, int TV, int CAP) {
 template <int NT, typename FT, typename GT, bool VEC, typename Side>
 __device__ void tile_fill_range(const TileLds& L, int lo, int hi, int base, const FT* fb,
                                 int feat_ld, int C, GT* out, int* s_nheavy, int stage_bytes,
-                                bool last, Side side) {
+                                bool last, Side side, const HeavyOut& ho) {
     if (threadIdx.x == 0) *s_nheavy = 0;
     lds_barrier();
     if (VEC) {
@@ -652,19 +674,43 @@ __device__ void tile_fill_range(const TileLds& L, int lo, int hi, int base, cons
         // Occupied voxels: light ones listed in occ (L.cur, free once the
         // points are sorted) so that the (voxel, channel group) items are
         // spread evenly over the threads, heavy ones for the wave loop.
-        __shared__ int s_nocc;
+        // exported voxels are listed from heavy[hi - lo - 1] down
+        __shared__ int s_nocc, s_nexp;
         int* occ = L.cur;
-        if (threadIdx.x == 0) s_nocc = 0;
+        if (threadIdx.x == 0) s_nocc = s_nexp = 0;
         lds_barrier();
         for (int vi = lo + threadIdx.x; vi < hi; vi += NT) {
             const int nk = L.hist[vi];
             if (nk == 0) continue;  // empty voxel: a zero row
-            if (nk > kHeavy)
+            if (ho.hq && nk > kExport)
+                L.heavy[hi - lo - 1 - atomicAdd(&s_nexp, 1)] = vi;
+            else if (nk > kHeavy)
                 L.heavy[atomicAdd(s_nheavy, 1)] = vi;
             else
                 occ[atomicAdd(&s_nocc, 1)] = vi;
         }
         lds_barrier();
+        // Exported voxels: the sorted point list back to the bucket (at the
+        // voxel's offset in the tile) and a queue entry.
+        const int nexp = s_nexp;
+        if (nexp > 0) {
+            __shared__ int s_slot0;
+            if (threadIdx.x == 0) s_slot0 = atomicAdd(ho.hq, nexp);
+            lds_barrier();
+            for (int e = 0; e < nexp; e++) {
+                const int vi = L.heavy[hi - lo - 1 - e], q = s_slot0 + e;
+                const int nk = L.hist[vi], j0 = L.start[vi] - base;
+                for (int j = threadIdx.x; j < nk; j += NT)
+                    ho.bucket[L.start[vi] + j] = L.list[j0 + j];
+                if (threadIdx.x == 0) {
+                    int* ent = ho.hq + 1 + 4 * q;
+                    ent[0] = ho.b;
+                    ent[1] = ho.vox0 + vi;
+                    ent[2] = ho.bstart + L.start[vi];
+                    ent[3] = nk;
+                }
+            }
+        }
         // Items go in batches of IB per thread: the first point of every item
         // of a batch is loaded at once (most occupied voxels hold one or two
         // points), then the zero rows go out (side()), then each item adds
@@ -786,7 +832,8 @@ __device__ __forceinline__ void tile_collect_one(const TileLds& L, int k, int r,
 template <int NT, typename FT, typename GT, bool VEC, typename EachPoint>
 __device__ void tile_finish(const TileLds& L, int TV, int nv, int CAP, int32_t* cnt, GT* out,
                             const FT* fb, int feat_ld, int C, bool zero_rows, int stage_bytes,
-                            int* scan_lds, int* s_nheavy, EachPoint each_point) {
+                            int* scan_lds, int* s_nheavy, EachPoint each_point,
+                            const HeavyOut& ho) {
     // 2. counts out; exclusive prefix over the tile's voxels
     for (int i = threadIdx.x; i < nv; i += NT) cnt[i] = L.hist[i];
     // The tile's empty voxels: zero rows (16-byte stores), streaming out
@@ -822,7 +869,7 @@ __device__ void tile_finish(const TileLds& L, int TV, int nv, int CAP, int32_t* 
             L.list[atomicAdd(&L.cur[L.rbuf[s]], 1)] = L.kbuf[s];
         lds_barrier();
         tile_fill_range<NT, FT, GT, VEC>(L, 0, nv, 0, fb, feat_ld, C, out, s_nheavy, stage_bytes,
-                                         true, zero_empty_rows);
+                                         true, zero_empty_rows, ho);
         return;
     }
     zero_empty_rows();
@@ -864,8 +911,10 @@ __device__ void tile_finish(const TileLds& L, int TV, int nv, int CAP, int32_t* 
             if (r >= lo && r < hi) L.list[atomicAdd(&L.cur[r], 1)] = k;
         });
         lds_barrier();
+        // (the later segments scan the bucket again: nothing is exported)
         tile_fill_range<NT, FT, GT, VEC>(L, lo, hi, base, fb, feat_ld, C, out, s_nheavy, stage_bytes,
-                                         false, nothing);
+                                         false, nothing,
+                                         HeavyOut{nullptr, nullptr, 0, 0, 0});
         lo = hi;
     }
 }
@@ -874,8 +923,8 @@ template <int NT, typename FT, typename GT, bool VEC>
 __global__ __launch_bounds__(NT) void pv_voxel_tile_kernel(
     const int32_t* __restrict__ vox_id, const FT* __restrict__ feats, int feat_ld, int N, int C,
     int R, int TV, int CAP, int stage_bytes, int zero_rows, GT* __restrict__ grid,
-    int32_t* __restrict__ counts, const int* __restrict__ bk, const int* __restrict__ br,
-    const int* __restrict__ tcount, const int* __restrict__ tstart, int T) {
+    int32_t* __restrict__ counts, int* bk, const int* __restrict__ br,
+    const int* __restrict__ tcount, const int* __restrict__ tstart, int T, int* hq) {
     extern __shared__ __attribute__((aligned(16))) char smem[];
     __shared__ int scan_lds[NT / 64];
     __shared__ int s_ntile, s_nheavy;
@@ -945,8 +994,10 @@ __global__ __launch_bounds__(NT) void pv_voxel_tile_kernel(
             tile_collect_one(L, k, ids[k] - v0, nv, CAP, &s_ntile);
     }
     lds_barrier();
+    const HeavyOut ho{bucketed ? hq : nullptr, bucketed ? bk + (size_t)b * N + bstart : nullptr, b,
+                      v0, bstart};
     tile_finish<NT, FT, GT, VEC>(L, TV, nv, CAP, counts + (size_t)b * V + v0, out, fb, feat_ld, C,
-                                 zero_rows != 0, stage_bytes, scan_lds, &s_nheavy, each_point);
+                                 zero_rows != 0, stage_bytes, scan_lds, &s_nheavy, each_point, ho);
 }
 
 // Tile shape. Small clouds (every tile scans all N ids, cheap): about 2048
@@ -1014,11 +1065,12 @@ void tile_budget(K kernel, int NT, int TV, int N, long tiles, int& cap, int& sta
 // Tiles' point sources: the points bucketed by tile (large clouds) or none
 // (each tile scans all ids).
 struct Buckets {
-    const int* bk;
+    int* bk;
     const int* br;
     const int* tcount;
     const int* tstart;
     int T;
+    int* hq;  // heavy-voxel queue (nullptr: none)
 };
 
 template <int NT, typename FT, typename GT>
@@ -1033,13 +1085,122 @@ void launch_tiles_nt(const int32_t* ids, const void* feats, int feat_ld, int B, 
         tile_budget(k, NT, TV, N, (long)g.x * g.y, cap, stage);
         hipLaunchKernelGGL(k, g, dim3(NT), tile_lds_bytes(NT, TV, cap, stage), s, ids,
                            (const FT*)feats, feat_ld, N, C, R, TV, cap, stage, (int)zero_rows,
-                           (GT*)grid, counts, bu.bk, bu.br, bu.tcount, bu.tstart, bu.T);
+                           (GT*)grid, counts, bu.bk, bu.br, bu.tcount, bu.tstart, bu.T, bu.hq);
     } else {
         auto k = pv_voxel_tile_kernel<NT, FT, GT, false>;
         tile_budget(k, NT, TV, N, (long)g.x * g.y, cap, stage);
         hipLaunchKernelGGL(k, g, dim3(NT), tile_lds_bytes(NT, TV, cap, stage), s, ids,
                            (const FT*)feats, feat_ld, N, C, R, TV, cap, 0, 0, (GT*)grid, counts,
-                           bu.bk, bu.br, bu.tcount, bu.tstart, bu.T);
+                           bu.bk, bu.br, bu.tcount, bu.tstart, bu.T, bu.hq);
+    }
+}
+
+// Heavy voxels handed over by the tiles (large clouds, more than kExport
+// points each), cut into chunks of kChunk points, chunk c of the queue order
+// taken by workgroup c % gridDim.x. The queue is read in windows of 256
+// entries: an exclusive scan of the entries' chunk counts gives each chunk
+// its voxel. In a chunk, thread sub * ng + (cg - cg0) sums points sub,
+// sub + S, ... (S = 256 / ng subsets of the voxel's ng channel groups); the
+// partials are combined in subset order through LDS and written as the
+// chunk's fp64 sums. No workgroup waits for another: the next kernel
+// combines each voxel's chunks.
+__device__ __forceinline__ int heavy_window(const int* hq, int nq, int w0, int* s_pre, int* s_scan) {
+    const int ent = w0 + (int)threadIdx.x;
+    const int nch = ent < nq ? (hq[1 + 4 * ent + 3] + kChunk - 1) / kChunk : 0;
+    int total;
+    const int pre = block_exclusive_scan<256>(nch, s_scan, total);
+    s_pre[threadIdx.x] = pre;
+    lds_barrier();
+    return total;
+}
+
+template <typename FT>
+__global__ __launch_bounds__(256) void pv_voxel_heavy_kernel(
+    const FT* __restrict__ feats, int feat_ld, int N, int C, const int* __restrict__ bk,
+    const int* __restrict__ hq, double* __restrict__ hpart) {
+    __shared__ double red[256 * 8];
+    __shared__ int s_pre[256], s_scan[4];
+    const int nq = hq[0];
+    const int gpv = C / 8, t = threadIdx.x, G = gridDim.x;
+    int chunk_base = 0;
+    for (int w0 = 0; w0 < nq; w0 += 256) {
+        const int total = heavy_window(hq, nq, w0, s_pre, s_scan);
+        int local = (int)(((long)blockIdx.x - chunk_base) % G);
+        if (local < 0) local += G;
+        for (; local < total; local += G) {
+            // the window entry holding chunk `local`: last e with s_pre[e] <= local
+            int lo = 0, hi = min(256, nq - w0) - 1;
+            while (lo < hi) {
+                const int mid = (lo + hi + 1) >> 1;
+                if (s_pre[mid] <= local) lo = mid; else hi = mid - 1;
+            }
+            const int* e = hq + 1 + 4 * (w0 + lo);
+            const int b = e[0], off = e[2], nk = e[3];
+            const int p0 = (local - s_pre[lo]) * kChunk, p1 = min(nk, p0 + kChunk);
+            const FT* fb = feats + (size_t)b * N * feat_ld;
+            const int* list = bk + (size_t)b * N + off;
+            double* dst = hpart + (size_t)(chunk_base + local) * C;
+            for (int cg0 = 0; cg0 < gpv; cg0 += 256) {
+                const int ng = min(256, gpv - cg0);
+                const int S = 256 / ng;
+                const int sub = t / ng, cl = t % ng;
+                if (sub < S) {
+                    double acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+                    sum8<FT>(fb, feat_ld, (cg0 + cl) * 8, list, p0 + sub, p1, S, acc);
+#pragma unroll
+                    for (int i = 0; i < 8; i++) red[(sub * ng + cl) * 8 + i] = acc[i];
+                }
+                lds_barrier();
+                if (t < ng) {
+                    double tot[8];
+#pragma unroll
+                    for (int i = 0; i < 8; i++) tot[i] = red[t * 8 + i];
+                    for (int s2 = 1; s2 < S; s2++)
+#pragma unroll
+                        for (int i = 0; i < 8; i++) tot[i] += red[(s2 * ng + t) * 8 + i];
+#pragma unroll
+                    for (int i = 0; i < 8; i++) dst[(cg0 + t) * 8 + i] = tot[i];
+                }
+                lds_barrier();
+            }
+        }
+        chunk_base += total;
+    }
+}
+
+// The queued voxels' means: voxel q of the queue (workgroup q % gridDim.x)
+// adds its chunks' sums in chunk order and writes its grid row.
+template <typename GT>
+__global__ __launch_bounds__(256) void pv_voxel_heavy_mean_kernel(int C, int R,
+                                                                 const int* __restrict__ hq,
+                                                                 const double* __restrict__ hpart,
+                                                                 GT* __restrict__ grid) {
+    __shared__ int s_pre[256], s_scan[4];
+    const int nq = hq[0];
+    const int V = R * R * R, gpv = C / 8, G = gridDim.x;
+    int chunk_base = 0;
+    for (int w0 = 0; w0 < nq; w0 += 256) {
+        const int total = heavy_window(hq, nq, w0, s_pre, s_scan);
+        for (int e = (int)blockIdx.x - w0 % G; e < min(256, nq - w0); e += G) {
+            if (e < 0) continue;
+            const int* ent = hq + 1 + 4 * (w0 + e);
+            const int b = ent[0], vox = ent[1], nk = ent[3];
+            const int nch = (nk + kChunk - 1) / kChunk;
+            const double* src = hpart + (size_t)(chunk_base + s_pre[e]) * C;
+            GT* out = grid + ((size_t)b * V + vox) * C;
+            for (int cg = threadIdx.x; cg < gpv; cg += 256) {
+                double tot[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+                for (int k = 0; k < nch; k++)
+#pragma unroll
+                    for (int i = 0; i < 8; i++) tot[i] += src[(size_t)k * C + cg * 8 + i];
+                float mean[8];
+#pragma unroll
+                for (int i = 0; i < 8; i++) mean[i] = (float)(tot[i] / (double)nk);
+                store8<GT>(out + cg * 8, mean);
+            }
+        }
+        chunk_base += total;
+        lds_barrier();
     }
 }
 
@@ -1096,6 +1257,12 @@ VoxWs carve_ws(void* ws, int B, int N, int R, size_t* bytes) {
     w.split.tstart = (int*)take(nt * sizeof(int));
     w.split.bk = (int*)take(large ? (size_t)B * N * sizeof(int) : 0);
     w.split.br = (int*)take(large ? (size_t)B * N * sizeof(int) : 0);
+    // a voxel goes to the queue with more than kExport points
+    w.split.hmax = large ? B * (N / (kExport + 1)) : 0;
+    w.split.hq = (int*)take(large ? (1 + 4 * (size_t)w.split.hmax) * sizeof(int) : 0);
+    // chunks: at most one per kChunk queued points plus one per voxel
+    const size_t hchunks = large ? (size_t)w.split.hmax + (size_t)B * N / kChunk : 0;
+    w.split.hpart = (double*)take(hchunks * kHeavyMaxC * sizeof(double));
     if (bytes) *bytes = off;
     return w;
 }
@@ -1157,12 +1324,25 @@ pvconv_status pv_launch_voxelize(const float* coords, const void* feats, bool fe
     }
     const Buckets bu = N > kSmallMaxN
                            ? Buckets{w.split.bk, w.split.br, w.split.tcount, w.split.tstart,
-                                     w.split.T}
-                           : Buckets{nullptr, nullptr, nullptr, nullptr, 0};
+                                     w.split.T, vec && C <= kHeavyMaxC ? w.split.hq : nullptr}
+                           : Buckets{nullptr, nullptr, nullptr, nullptr, 0, nullptr};
     if (!grid_ok) {
         // a grid that 16-byte stores cannot cover: the plain element kernel
         hipLaunchKernelGGL(pv_zero_elems_kernel, dim3(1024), dim3(256), 0, s, (char*)grid, gbytes);
     }
+    // heavy voxels queued by the tiles (large clouds, 16-byte rows)
+    const int hgrid = std::min(256, w.split.hmax);
+    auto heavy = [&](auto ft, auto gt) {
+        typedef decltype(ft) FT;
+        typedef decltype(gt) GT;
+        if (bu.hq && hgrid > 0) {
+            hipLaunchKernelGGL((pv_voxel_heavy_kernel<FT>), dim3(hgrid), dim3(256), 0, s,
+                               (const FT*)feats, feat_ld, N, C, w.split.bk, w.split.hq,
+                               w.split.hpart);
+            hipLaunchKernelGGL((pv_voxel_heavy_mean_kernel<GT>), dim3(hgrid), dim3(256), 0, s, C,
+                               R, w.split.hq, w.split.hpart, (GT*)grid);
+        }
+    };
     if (feat_bf16) {
         if (grid_bf16)
             launch_tiles<uint16_t, uint16_t>(ids, feats, feat_ld, B, N, C, R, grid, counts, vec,
@@ -1177,6 +1357,11 @@ pvconv_status pv_launch_voxelize(const float* coords, const void* feats, bool fe
         else
             launch_tiles<float, float>(ids, feats, feat_ld, B, N, C, R, grid, counts, vec, vec, bu,
                                        s);
+    }
+    if (feat_bf16) {
+        if (grid_bf16) heavy(uint16_t{}, uint16_t{}); else heavy(uint16_t{}, float{});
+    } else {
+        if (grid_bf16) heavy(float{}, uint16_t{}); else heavy(float{}, float{});
     }
     return pv_launch_status();
 }

@@ -125,6 +125,37 @@ def test_voxelize_crowded_tiles(N, spread):
     assert_rel(host(g), grid, 1e-5, "crowded voxel grid")
 
 
+@pytest.mark.parametrize("C,fdt,gdt", [(128, "bf16", torch.bfloat16), (24, "f32", torch.float32),
+                                       (136, "f32", torch.bfloat16)],
+                         ids=["C128_bf16", "C24_f32", "C136_wider_than_the_queue_sums"])
+def test_voxelize_clustered_large_clouds(C, fdt, gdt):
+    # Large clouds whose dense voxels (more than 32 points) are handed to the
+    # heavy-voxel kernels in chunks of 256 points (up to 128 channels), or
+    # summed in their tile (wider rows); two clouds, a voxel of ~3000 points.
+    rng = np.random.default_rng(C)
+    B, N, R = 2, 12000, 16
+    centers = rng.uniform(-0.6, 0.6, size=(B, 6, 1, 3))
+    pts = centers + rng.normal(size=(B, 6, N // 6, 3)) * rng.uniform(0.005, 0.05, size=(B, 6, 1, 1))
+    coords = pts.reshape(B, N, 3).astype(np.float32)
+    coords[:, :3000] = coords[:, :1]          # one voxel of 3000 points per cloud
+    coords[:, -1] = [1.5, 1.5, 1.5]           # spread the grid
+    feats = rng.normal(size=(B, N, C)).astype(np.float32)
+    if fdt == "bf16":
+        feats = synth.round_to_bf16(feats)
+    pn, ids, grid, counts = _oracle_vox(coords, feats, R)
+    assert counts.max() >= 3000
+    g = torch.full((B, R ** 3, C), float("nan"), dtype=gdt, device="cuda")
+    g, c, i, p = pv.pvconv_voxelize(dev(coords), dev(feats, torch.bfloat16 if fdt == "bf16" else
+                                                      torch.float32), R, grid_dtype=gdt, grid=g)
+    assert np.array_equal(i.cpu().numpy(), ids)
+    assert np.array_equal(c.cpu().numpy(), counts)
+    got = host(g)
+    if gdt == torch.float32:
+        assert_rel(got, grid, 1e-5, "clustered grid fp32")
+    else:
+        assert_bf16_step(got, grid, "clustered grid bf16")
+
+
 @pytest.mark.parametrize("N,R,C,gdt", [(2048, 32, 64, torch.bfloat16), (3000, 7, 16, torch.float32),
                                         (20000, 31, 32, torch.bfloat16), (1, 5, 8, torch.float32)],
                          ids=["vec_rows", "odd_R", "split_path", "one_point"])
