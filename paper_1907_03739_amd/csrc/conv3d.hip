@@ -10,10 +10,10 @@
 //    32*NB/WCH channels with v_mfma_f32_32x32x16_bf16: A = weights (rows =
 //    output channels), B = voxels (columns), 4 x NB/WCH accumulator blocks,
 //    so every voxel fragment feeds NB/WCH MFMAs and every weight fragment
-//    four. WCH = 2 (eight waves, two per SIMD, so that one wave's waits
-//    overlap the other's MFMAs) measures faster for 64 input channels;
-//    WCH = 1 (four waves, one per SIMD, all 256 accumulator registers) for
-//    wider inputs.
+//    four. WCH = 1 (four waves, one per SIMD, all 256 accumulator registers
+//    for a 128-channel tile) measures fastest for 128-channel tiles; WCH = 2
+//    (eight waves, two per SIMD, so that one wave's waits overlap the
+//    other's MFMAs) for 64-channel tiles of 64 or fewer input channels.
 //  * The input is consumed in chunks of 16 channels (one MFMA k step). A
 //    chunk's 10x10x10 halo (zero outside the grid) sits in LDS at 48 bytes per
 //    voxel (32 bytes of data) and 640 bytes per 10-voxel row: with that
@@ -462,12 +462,12 @@ pvconv_status pv_launch_conv3d(const void* x, int B, int R, int Cin, int Cout, c
         // about one workgroup per CU; small grids (R = 16) take narrow tiles.
         const int nbr = (R + kBrick - 1) / kBrick;
         const long bricks = (long)B * nbr * nbr * nbr;
-        const bool two = Cin <= 64;  // eight waves for narrow inputs
+        // Waves: four (one per SIMD, 128 channels each) for 128-channel tiles;
+        // eight (two channel groups) for 64-channel tiles of narrow inputs,
+        // where a wave's 64 channels would leave its MFMAs too few per load.
+        const bool two = Cin <= 64;
         if (Cout % 128 == 0 && bricks * (Cout / 128) >= 256) {
-            if (two)
-                launch_bf16<4, 2>(x, B, R, Cin, Cout, w, bn, act, slope, y, out_bf16, vec, s);
-            else
-                launch_bf16<4, 1>(x, B, R, Cin, Cout, w, bn, act, slope, y, out_bf16, vec, s);
+            launch_bf16<4, 1>(x, B, R, Cin, Cout, w, bn, act, slope, y, out_bf16, vec, s);
         } else if (Cout % 64 == 0 && bricks * (Cout / 64) >= 256) {
             if (two)
                 launch_bf16<2, 2>(x, B, R, Cin, Cout, w, bn, act, slope, y, out_bf16, vec, s);
