@@ -290,6 +290,31 @@ __global__ __launch_bounds__(256 * WCH, 1) void pv_conv3d_bf16_kernel(
             pv_lds_barrier();
             // copy out: piece k of voxel vox (k < pieces)
             const size_t col = ((size_t)n0 + pass * PW) * esz;
+            if (vec_out && u0 + kBrick <= R && v0 + kBrick <= R && w0 + kBrick <= R) {
+                // the whole brick inside the grid: batches of UC pieces per
+                // thread, every LDS read of a batch issued before its stores
+                constexpr int kIt = 512 * pieces / NTH, UC = kIt < 4 ? kIt : 4;
+                static_assert(kIt % UC == 0, "copy-out batches divide the pieces");
+#pragma unroll 1
+                for (int i0 = 0; i0 < kIt; i0 += UC) {
+                    uint4 val[UC];
+#pragma unroll
+                    for (int q = 0; q < UC; q++) {
+                        const int i = tid + (i0 + q) * NTH, vox = i / pieces, k = i % pieces;
+                        val[q] = *(const uint4*)(lds + vox * kStageRow + k * 16);
+                    }
+#pragma unroll
+                    for (int q = 0; q < UC; q++) {
+                        const int i = tid + (i0 + q) * NTH, vox = i / pieces, k = i % pieces;
+                        const int u = u0 + (vox >> 6), v = v0 + ((vox >> 3) & 7),
+                                  ww = w0 + (vox & 7);
+                        *(uint4*)((char*)y + (cloud + ((size_t)u * R + v) * R + ww) * yrow + col +
+                                  k * 16) = val[q];
+                    }
+                }
+                pv_lds_barrier();
+                continue;
+            }
             for (int i = tid; i < 512 * pieces; i += NTH) {
                 const int vox = i / pieces, k = i % pieces;
                 const int u = u0 + (vox >> 6), v = v0 + ((vox >> 3) & 7), ww = w0 + (vox & 7);
