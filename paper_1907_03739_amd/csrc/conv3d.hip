@@ -11,9 +11,13 @@
 //    output channels), B = voxels (columns), 4 x NB/WCH accumulator blocks,
 //    so every voxel fragment feeds NB/WCH MFMAs and every weight fragment
 //    four. WCH = 1 (four waves, one per SIMD, all 256 accumulator registers
-//    for a 128-channel tile) measures fastest for 128-channel tiles; WCH = 2
-//    (eight waves, two per SIMD, so that one wave's waits overlap the
-//    other's MFMAs) for 64-channel tiles of 64 or fewer input channels.
+//    for a 128-channel tile) measures fastest for 128-channel tiles of wide
+//    inputs; WCH = 2 (eight waves, two per SIMD, so that one wave's waits
+//    overlap the other's MFMAs) for 64-channel tiles of narrow inputs on
+//    small grids. Narrow inputs on grids with enough tiles take 64-channel
+//    tiles single-buffered (SB): 64 KB of LDS and at most 128 accumulator
+//    registers per wave, so two workgroups share a CU and one's prologue and
+//    epilogue overlap the other's MFMAs.
 //  * The input is consumed in chunks of 16 channels (one MFMA k step). A
 //    chunk's 10x10x10 halo (zero outside the grid) sits in LDS at 48 bytes per
 //    voxel (32 bytes of data) and 640 bytes per 10-voxel row: with that
@@ -50,6 +54,10 @@ constexpr int kOOB = 0x40000000;                   // byte offset always out of 
 constexpr int kStageRow = 256 + 16;
 constexpr int kStageBytes = kBrick * kBrick * kBrick * kStageRow;  // 139264
 constexpr int kLdsBytes = kStageBytes > 2 * kHaloBytes ? kStageBytes : 2 * kHaloBytes;
+// Single-buffered variant (two workgroups per CU): one halo buffer, the
+// epilogue staged through it in passes of 32 bf16 (16 fp32) channels.
+constexpr int kStageRowSB = 64 + 16;
+static_assert(512 * kStageRowSB <= kHaloBytes, "single-buffer stage fits the halo buffer");
 
 __device__ __forceinline__ uint4 pack8(const uint16_t* e) {
     return make_uint4((uint32_t)e[0] | ((uint32_t)e[1] << 16), (uint32_t)e[2] | ((uint32_t)e[3] << 16),
@@ -88,13 +96,16 @@ __device__ __forceinline__ uint4 bload8_elems(__amdgpu_buffer_rsrc_t r, int voff
 }
 
 // WCH channel groups of waves: 1 (four waves, 256 threads) or 2 (eight
-// waves, two per SIMD).
-template <int NB, int WCH, bool VEC>
-__global__ __launch_bounds__(256 * WCH, 1) void pv_conv3d_bf16_kernel(
+// waves, two per SIMD). SB: one halo buffer (the next chunk's halo waits in
+// registers until the current chunk is done) and at most 128 accumulator
+// registers, so that two workgroups share a CU and one's prologue and
+// epilogue overlap the other's MFMAs.
+template <int NB, int WCH, bool VEC, bool SB = false>
+__global__ __launch_bounds__(256 * WCH, SB ? 2 : 1) void pv_conv3d_bf16_kernel(
     const uint16_t* __restrict__ x, const uint16_t* __restrict__ wpk, PvBnFold bn, int act,
     float slope, void* __restrict__ y, int out_bf16, int vec_out, int R, int Cin, int Cout,
     int nbr, int nblocks) {
-    __shared__ __attribute__((aligned(16))) char lds[kLdsBytes];
+    __shared__ __attribute__((aligned(16))) char lds[SB ? kHaloBytes : kLdsBytes];
     __shared__ float bn_tab[2][NB * 32];  // folded scale and shift per output channel
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -203,7 +214,49 @@ __global__ __launch_bounds__(256 * WCH, 1) void pv_conv3d_bf16_kernel(
     // other LDS buffer at tap s+4. One loop body for every chunk keeps the
     // accumulators in the same registers throughout.
     constexpr int kHaloLag = 4;
-    for (int c = 0; c < nch; c++) {
+    if constexpr (SB) {
+        // One buffer: piece set s of the next chunk's halo is loaded at tap s
+        // into hr[s] and stored once every wave is done with the chunk.
+        uint4 hr[kSets];
+        for (int c = 0; c < nch; c++) {
+            const bool more = c + 1 < nch;
+            const int cn = (more ? c + 1 : c) * kKC;
+            pv_bf16x8 bf[2][4];
+#pragma unroll
+            for (int mb = 0; mb < 4; mb++) bf[0][mb] = *(const pv_bf16x8*)(lds + bbase[mb]);
+#pragma unroll
+            for (int t = 0; t < kTaps; t++) {
+                const int cur = t & 1, nxt = cur ^ 1;
+                if (t + 2 < kTaps)
+                    load_w(c, t + 2, wf[(t + 2) % 3]);
+                else
+                    load_w(c + 1, t + 2 - kTaps, wf[(t + 2) % 3]);
+                if (t < kSets && more) hr[t] = halo_load(t, cn);
+                if (t + 1 < kTaps) {
+                    const int tn = t + 1;
+                    const int toff = (tn / 9) * kHalo * kRowPitch + ((tn / 3) % 3) * kRowPitch +
+                                     (tn % 3) * kVoxPitch;
+#pragma unroll
+                    for (int mb = 0; mb < 4; mb++)
+                        bf[nxt][mb] = *(const pv_bf16x8*)(lds + bbase[mb] + toff);
+                }
+#pragma unroll
+                for (int mb = 0; mb < 4; mb++)
+#pragma unroll
+                    for (int nb = 0; nb < NBW; nb++)
+                        acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                            wf[t % 3][nb], bf[cur][mb], acc[mb][nb], 0, 0, 0);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            pv_lds_barrier();  // every wave is done reading the chunk
+            if (more) {
+#pragma unroll
+                for (int set = 0; set < kSets; set++) *(uint4*)(lds + loff[set]) = hr[set];
+                __syncthreads();  // the next chunk's halo is in place
+            }
+        }
+    }
+    for (int c = 0; !SB && c < nch; c++) {
         const int cur_off = (c & 1) * kHaloBytes, nxt_off = kHaloBytes - cur_off;
         int rb[4];
 #pragma unroll
@@ -253,7 +306,9 @@ __global__ __launch_bounds__(256 * WCH, 1) void pv_conv3d_bf16_kernel(
     auto epilogue = [&](auto out_type) {
         constexpr bool OBF = decltype(out_type)::value;
         constexpr int esz = OBF ? 2 : 4;
-        constexpr int PW = OBF ? (NT < 128 ? NT : 128) : (NT < 64 ? NT : 64);
+        constexpr int PW = SB ? (OBF ? (NT < 32 ? NT : 32) : (NT < 16 ? NT : 16))
+                              : (OBF ? (NT < 128 ? NT : 128) : (NT < 64 ? NT : 64));
+        constexpr int kRow = SB ? kStageRowSB : kStageRow;  // LDS bytes per staged voxel
         constexpr int pieces = PW * esz / 16;  // 16-byte pieces per voxel row
         const size_t yrow = (size_t)Cout * esz;
 #pragma unroll
@@ -277,7 +332,7 @@ __global__ __launch_bounds__(256 * WCH, 1) void pv_conv3d_bf16_kernel(
                                       acc[mb][nb][4 * j + 3] * sc.w + sh.w};
 #pragma unroll
                         for (int e = 0; e < 4; e++) r[e] = r[e] >= 0.f ? r[e] : r[e] * neg;
-                        char* d = lds + vox * kStageRow + cb;
+                        char* d = lds + vox * kRow + cb;
                         if constexpr (OBF)
                             *(uint2*)d = make_uint2(pv_pack_bf16x2(r[0], r[1]),
                                                     pv_pack_bf16x2(r[2], r[3]));
@@ -301,7 +356,7 @@ __global__ __launch_bounds__(256 * WCH, 1) void pv_conv3d_bf16_kernel(
 #pragma unroll
                     for (int q = 0; q < UC; q++) {
                         const int i = tid + (i0 + q) * NTH, vox = i / pieces, k = i % pieces;
-                        val[q] = *(const uint4*)(lds + vox * kStageRow + k * 16);
+                        val[q] = *(const uint4*)(lds + vox * kRow + k * 16);
                     }
 #pragma unroll
                     for (int q = 0; q < UC; q++) {
@@ -319,7 +374,7 @@ __global__ __launch_bounds__(256 * WCH, 1) void pv_conv3d_bf16_kernel(
                 const int vox = i / pieces, k = i % pieces;
                 const int u = u0 + (vox >> 6), v = v0 + ((vox >> 3) & 7), ww = w0 + (vox & 7);
                 if (u >= R || v >= R || ww >= R) continue;
-                const uint4 val = *(const uint4*)(lds + vox * kStageRow + k * 16);
+                const uint4 val = *(const uint4*)(lds + vox * kRow + k * 16);
                 char* dst = (char*)y + (cloud + ((size_t)u * R + v) * R + ww) * yrow + col + k * 16;
                 if (vec_out) {
                     *(uint4*)dst = val;
@@ -426,7 +481,7 @@ __global__ __launch_bounds__(256) void pv_conv3d_f32_kernel(const float* __restr
         ((float*)y)[i] = val;
 }
 
-template <int NB, int WCH>
+template <int NB, int WCH, bool SB = false>
 void launch_bf16(const void* x, int B, int R, int Cin, int Cout, const void* w,
                  const PvBnFold& bn, int act, float slope, void* y, bool out_bf16, bool vec,
                  hipStream_t s) {
@@ -434,12 +489,12 @@ void launch_bf16(const void* x, int B, int R, int Cin, int Cout, const void* w,
     const size_t blocks = (size_t)B * nbr * nbr * nbr * (Cout / (NB * 32));
     const bool vec_out = pv_aligned16(y);
     if (vec)
-        hipLaunchKernelGGL((pv_conv3d_bf16_kernel<NB, WCH, true>), dim3((unsigned)blocks),
+        hipLaunchKernelGGL((pv_conv3d_bf16_kernel<NB, WCH, true, SB>), dim3((unsigned)blocks),
                            dim3(256 * WCH), 0, s, (const uint16_t*)x, (const uint16_t*)w, bn,
                            act, slope, y, (int)out_bf16, (int)vec_out, R, Cin, Cout, nbr,
                            (int)blocks);
     else
-        hipLaunchKernelGGL((pv_conv3d_bf16_kernel<NB, WCH, false>), dim3((unsigned)blocks),
+        hipLaunchKernelGGL((pv_conv3d_bf16_kernel<NB, WCH, false, SB>), dim3((unsigned)blocks),
                            dim3(256 * WCH), 0, s, (const uint16_t*)x, (const uint16_t*)w, bn,
                            act, slope, y, (int)out_bf16, (int)vec_out, R, Cin, Cout, nbr,
                            (int)blocks);
@@ -487,11 +542,17 @@ pvconv_status pv_launch_conv3d(const void* x, int B, int R, int Cin, int Cout, c
         // about one workgroup per CU; small grids (R = 16) take narrow tiles.
         const int nbr = (R + kBrick - 1) / kBrick;
         const long bricks = (long)B * nbr * nbr * nbr;
-        // Waves: four (one per SIMD, 128 channels each) for 128-channel tiles;
-        // eight (two channel groups) for 64-channel tiles of narrow inputs,
-        // where a wave's 64 channels would leave its MFMAs too few per load.
+        // Narrow inputs (at most 64 channels, so at most four chunks, where a
+        // workgroup's prologue and epilogue weigh most) with enough tiles for
+        // two workgroups per CU: 64-channel tiles, single-buffered, two per
+        // CU (11 % faster at 64->128 and 64->64 than one 128-channel
+        // workgroup per CU). Otherwise four waves (one per SIMD, 128 channels
+        // each) for 128-channel tiles; eight (two channel groups) for
+        // 64-channel tiles of narrow inputs.
         const bool two = Cin <= 64;
-        if (Cout % 128 == 0 && bricks * (Cout / 128) >= 256) {
+        if (Cin <= 64 && Cout % 64 == 0 && bricks * (Cout / 64) >= 512) {
+            launch_bf16<2, 1, true>(x, B, R, Cin, Cout, w, bn, act, slope, y, out_bf16, vec, s);
+        } else if (Cout % 128 == 0 && bricks * (Cout / 128) >= 256) {
             launch_bf16<4, 1>(x, B, R, Cin, Cout, w, bn, act, slope, y, out_bf16, vec, s);
         } else if (Cout % 64 == 0 && bricks * (Cout / 64) >= 256) {
             if (two)
