@@ -54,10 +54,11 @@ constexpr int kOOB = 0x40000000;                   // byte offset always out of 
 constexpr int kStageRow = 256 + 16;
 constexpr int kStageBytes = kBrick * kBrick * kBrick * kStageRow;  // 139264
 constexpr int kLdsBytes = kStageBytes > 2 * kHaloBytes ? kStageBytes : 2 * kHaloBytes;
-// Single-buffered variant (two workgroups per CU): one halo buffer, the
-// epilogue staged through it in passes of 32 bf16 (16 fp32) channels.
-constexpr int kStageRowSB = 64 + 16;
-static_assert(512 * kStageRowSB <= kHaloBytes, "single-buffer stage fits the halo buffer");
+// Single-buffered variant (two workgroups per CU): one halo buffer; the
+// epilogue stages the 64-channel tile through LDS in one pass (bf16: whole
+// 128-byte halves of the output rows) or two (fp32).
+constexpr int kStageRowSB = 128 + 16;
+constexpr int kLdsBytesSB = 512 * kStageRowSB > kHaloBytes ? 512 * kStageRowSB : kHaloBytes;
 
 __device__ __forceinline__ uint4 pack8(const uint16_t* e) {
     return make_uint4((uint32_t)e[0] | ((uint32_t)e[1] << 16), (uint32_t)e[2] | ((uint32_t)e[3] << 16),
@@ -105,7 +106,7 @@ __global__ __launch_bounds__(256 * WCH, SB ? 2 : 1) void pv_conv3d_bf16_kernel(
     const uint16_t* __restrict__ x, const uint16_t* __restrict__ wpk, PvBnFold bn, int act,
     float slope, void* __restrict__ y, int out_bf16, int vec_out, int R, int Cin, int Cout,
     int nbr, int nblocks) {
-    __shared__ __attribute__((aligned(16))) char lds[SB ? kHaloBytes : kLdsBytes];
+    __shared__ __attribute__((aligned(16))) char lds[SB ? kLdsBytesSB : kLdsBytes];
     __shared__ float bn_tab[2][NB * 32];  // folded scale and shift per output channel
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -306,7 +307,7 @@ __global__ __launch_bounds__(256 * WCH, SB ? 2 : 1) void pv_conv3d_bf16_kernel(
     auto epilogue = [&](auto out_type) {
         constexpr bool OBF = decltype(out_type)::value;
         constexpr int esz = OBF ? 2 : 4;
-        constexpr int PW = SB ? (OBF ? (NT < 32 ? NT : 32) : (NT < 16 ? NT : 16))
+        constexpr int PW = SB ? (OBF ? (NT < 64 ? NT : 64) : (NT < 32 ? NT : 32))
                               : (OBF ? (NT < 128 ? NT : 128) : (NT < 64 ? NT : 64));
         constexpr int kRow = SB ? kStageRowSB : kStageRow;  // LDS bytes per staged voxel
         constexpr int pieces = PW * esz / 16;  // 16-byte pieces per voxel row

@@ -281,14 +281,15 @@ def test_conv3d_f32_matches_oracle(B, R, Cin, Cout):
     assert_dot_f32(host(y), ref, mag, "conv fp32")
 
 
-@pytest.mark.parametrize("B,R,Cin,Cout", [
-    (16, 32, 64, 128),    # part-seg conv 1: 64-channel tiles, two workgroups per CU
-    (16, 32, 128, 128),   # part-seg conv 2: 128-channel tiles, four waves
-    (4, 32, 128, 64),     # 64-channel tiles, four waves
-    (8, 32, 9, 64),       # scene-seg first conv: two workgroups per CU, value loads
-    (1, 64, 64, 64),      # stress conv: two workgroups per CU
+@pytest.mark.parametrize("B,R,Cin,Cout,odt", [
+    (16, 32, 64, 128, "bf16"),    # part-seg conv 1: 64-channel tiles, two workgroups per CU
+    (16, 32, 128, 128, "bf16"),   # part-seg conv 2: 128-channel tiles, four waves
+    (4, 32, 128, 64, "bf16"),     # 64-channel tiles, four waves
+    (8, 32, 9, 64, "bf16"),       # scene-seg first conv: two workgroups per CU, value loads
+    (1, 64, 64, 64, "bf16"),      # stress conv: two workgroups per CU
+    (8, 32, 16, 64, "f32"),       # two workgroups per CU, fp32 output (two staging passes)
 ])
-def test_conv3d_full_size_sampled(B, R, Cin, Cout):
+def test_conv3d_full_size_sampled(B, R, Cin, Cout, odt):
     # full batch in the launch configuration the benchmark uses (the channel
     # tile and wave count depend on the grid size); the oracle evaluates 600
     # sampled outputs, a third of them on the grid's faces.
@@ -296,7 +297,8 @@ def test_conv3d_full_size_sampled(B, R, Cin, Cout):
     x = _sparse_grid(rng, B, R, Cin, occupied=0.06 if Cin <= 64 else 0.5)
     w = synth.kaiming_normal(rng, (Cout, 3, 3, 3, Cin), 27 * Cin, bf16=True)
     bn = synth.draw_bn(rng, Cout)
-    y = host(pv.pvconv_conv3d(dev(x, torch.bfloat16), dev(w, torch.bfloat16), R, bn=dev_bn(bn)))
+    y = host(pv.pvconv_conv3d(dev(x, torch.bfloat16), dev(w, torch.bfloat16), R, bn=dev_bn(bn),
+                              out_dtype=torch.float32 if odt == "f32" else None))
     sel = rng.choice(B * R ** 3, size=400, replace=False)
     face = rng.integers(0, R, size=(200, 3))
     face[np.arange(200), rng.integers(0, 3, 200)] = rng.choice([0, R - 1], 200)
