@@ -14,10 +14,10 @@
 //    for a 128-channel tile) measures fastest for 128-channel tiles of wide
 //    inputs; WCH = 2 (eight waves, two per SIMD, so that one wave's waits
 //    overlap the other's MFMAs) for 64-channel tiles of narrow inputs on
-//    small grids. Narrow inputs on grids with enough tiles take 64-channel
-//    tiles single-buffered (SB): 64 KB of LDS and at most 128 accumulator
-//    registers per wave, so two workgroups share a CU and one's prologue and
-//    epilogue overlap the other's MFMAs.
+//    small grids. Inputs of up to 128 channels on grids with enough tiles
+//    take 64-channel tiles single-buffered (SB): 72 KB of LDS and at most
+//    128 accumulator registers per wave, so two workgroups share a CU and
+//    one's prologue and epilogue overlap the other's MFMAs.
 //  * The input is consumed in chunks of 16 channels (one MFMA k step). A
 //    chunk's 10x10x10 halo (zero outside the grid) sits in LDS at 48 bytes per
 //    voxel (32 bytes of data) and 640 bytes per 10-voxel row: with that
@@ -253,7 +253,8 @@ __global__ __launch_bounds__(256 * WCH, SB ? 2 : 1) void pv_conv3d_bf16_kernel(
             if (more) {
 #pragma unroll
                 for (int set = 0; set < kSets; set++) *(uint4*)(lds + loff[set]) = hr[set];
-                __syncthreads();  // the next chunk's halo is in place
+                pv_lds_barrier();  // the next chunk's halo is in place (its loads are
+                                   // done: the stores above used them)
             }
         }
     }
@@ -543,15 +544,15 @@ pvconv_status pv_launch_conv3d(const void* x, int B, int R, int Cin, int Cout, c
         // about one workgroup per CU; small grids (R = 16) take narrow tiles.
         const int nbr = (R + kBrick - 1) / kBrick;
         const long bricks = (long)B * nbr * nbr * nbr;
-        // Narrow inputs (at most 64 channels, so at most four chunks, where a
-        // workgroup's prologue and epilogue weigh most) with enough tiles for
-        // two workgroups per CU: 64-channel tiles, single-buffered, two per
-        // CU (11 % faster at 64->128 and 64->64 than one 128-channel
+        // Inputs of up to 128 channels with enough tiles for two workgroups
+        // per CU: 64-channel tiles, single-buffered, two per CU (one's
+        // prologue and epilogue overlap the other's MFMAs: 11 % faster at
+        // 64->128 and 64->64, 2.5 % at 128->128, than one 128-channel
         // workgroup per CU). Otherwise four waves (one per SIMD, 128 channels
         // each) for 128-channel tiles; eight (two channel groups) for
         // 64-channel tiles of narrow inputs.
         const bool two = Cin <= 64;
-        if (Cin <= 64 && Cout % 64 == 0 && bricks * (Cout / 64) >= 512) {
+        if (Cin <= 128 && Cout % 64 == 0 && bricks * (Cout / 64) >= 512) {
             launch_bf16<2, 1, true>(x, B, R, Cin, Cout, w, bn, act, slope, y, out_bf16, vec, s);
         } else if (Cout % 128 == 0 && bricks * (Cout / 128) >= 256) {
             launch_bf16<4, 1>(x, B, R, Cin, Cout, w, bn, act, slope, y, out_bf16, vec, s);

@@ -283,7 +283,8 @@ def test_conv3d_f32_matches_oracle(B, R, Cin, Cout):
 
 @pytest.mark.parametrize("B,R,Cin,Cout,odt", [
     (16, 32, 64, 128, "bf16"),    # part-seg conv 1: 64-channel tiles, two workgroups per CU
-    (16, 32, 128, 128, "bf16"),   # part-seg conv 2: 128-channel tiles, four waves
+    (16, 32, 128, 128, "bf16"),   # part-seg conv 2: 64-channel tiles, two workgroups per CU
+    (4, 32, 192, 128, "bf16"),    # wide input: 128-channel tiles, four waves, double-buffered
     (4, 32, 128, 64, "bf16"),     # 64-channel tiles, four waves
     (8, 32, 9, 64, "bf16"),       # scene-seg first conv: two workgroups per CU, value loads
     (1, 64, 64, 64, "bf16"),      # stress conv: two workgroups per CU
