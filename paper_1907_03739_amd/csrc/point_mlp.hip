@@ -732,7 +732,7 @@ pvconv_status pv_launch_point_mlp(const void* x, bool x_bf16, int x_ld, int M, i
                         ((uintptr_t)out & (out_bf16 ? 7u : 15u)) == 0;
         const bool tile = vec && c4;
         // wide layers: LDS-tiled GEMM, 256 x 256 (channels x points) tiles
-        // when they still give a workgroup per CU, else 128 x 256
+        // when they still give a workgroup per CU, else 128 x 256 or 128 x 128
         const long big_tiles = (long)((Cout + 255) / 256) * ((M + 255) / 256);
         if (tile && Cin >= 128 && Cout >= 256 && big_tiles >= 256) {
             if (x_bf16)
@@ -743,8 +743,21 @@ pvconv_status pv_launch_point_mlp(const void* x, bool x_bf16, int x_ld, int M, i
                                               res, res_ld, out, out_bf16, out_ld, s);
             return pv_launch_status();
         }
+        // 128 x 128 tiles where 128 x 256 would leave CUs idle (e.g. the head's
+        // 256-wide first layer: 34 % faster)
+        const long mid_tiles = (long)((Cout + 127) / 128) * ((M + 255) / 256);
+        if (tile && Cin >= 128 && Cout >= 128 && mid_tiles < 256) {
+            if (x_bf16)
+                launch_lds<4, 1, 1, 4, uint16_t>(x, x_ld, M, Cin, Cout, w, bn, act, slope, cb, ppc,
+                                                 res, res_ld, out, out_bf16, out_ld, s);
+            else
+                launch_lds<4, 1, 1, 4, float>(x, x_ld, M, Cin, Cout, w, bn, act, slope, cb, ppc,
+                                              res, res_ld, out, out_bf16, out_ld, s);
+            return pv_launch_status();
+        }
         if (tile && Cin >= 128 && Cout >= 128) {
             if (x_bf16)
+
                 launch_lds<4, 2, 1, 4, uint16_t>(x, x_ld, M, Cin, Cout, w, bn, act, slope, cb, ppc,
                                                  res, res_ld, out, out_bf16, out_ld, s);
             else
