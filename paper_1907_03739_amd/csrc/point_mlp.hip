@@ -288,10 +288,12 @@ struct GemmShape {
     static constexpr int TN = WN * NB * 32;   // output channels per workgroup
     static constexpr int TM = WM * MB * 32;   // points per workgroup
     static constexpr int ROWS = TN + TM;      // staged rows per chunk
-    static constexpr int PIECES = ROWS * 8 / 256;  // 16-byte pieces per thread per chunk
+    static constexpr int NTHR = 64 * WN * WM; // threads (four or eight waves)
+    static constexpr int RSET = NTHR / 8;     // rows per piece set (8 threads per row)
+    static constexpr int PIECES = ROWS * 8 / NTHR;  // 16-byte pieces per thread per chunk
     static constexpr int LDS = 2 * ROWS * kGPitch;
-    static_assert(WN * WM == 4, "four waves");
-    static_assert(ROWS % 32 == 0, "rows come in groups of 32 per piece set");
+    static_assert(WN * WM == 4 || WN * WM == 8, "four or eight waves");
+    static_assert(ROWS % RSET == 0 && TN % RSET == 0, "whole piece sets, weights apart");
 };
 
 __device__ __forceinline__ uint4 piece_bf16(const uint16_t* p) { return *(const uint4*)p; }
@@ -307,7 +309,7 @@ __device__ __forceinline__ uint4 piece_bf16(const float* p) {
 // EXT: a per-cloud row or a residual is given (else neither is read, and
 // the registers that prefetch them are not needed).
 template <int NB, int MB, int WN, int WM, typename XT, bool EXT>
-__global__ __launch_bounds__(256, 1) void pv_point_mlp_lds_kernel(
+__global__ __launch_bounds__(64 * WN * WM, 1) void pv_point_mlp_lds_kernel(
     const XT* __restrict__ x, int x_ld, int M, int Cin, int Cout, const uint16_t* __restrict__ w,
     PvBnFold bn, int act, float slope, const float* __restrict__ cloud_bias, int ppc,
     const float* __restrict__ residual, int res_ld, void* __restrict__ out, int out_bf16,
@@ -331,7 +333,7 @@ __global__ __launch_bounds__(256, 1) void pv_point_mlp_lds_kernel(
         ((float*)tab[1])[tid] = sh;
     }
 
-    // Staging: piece i*256 + tid is row i*32 + tid/8 of the chunk (weight
+    // Staging: piece i*NTHR + tid is row i*RSET + tid/8 of the chunk (weight
     // rows first, then point rows), bytes (tid%8)*16 .. +15 of its 128.
     // Rows past M or C_out are clamped onto the last valid row (their results
     // are never stored); columns past C_in stage as zero.
@@ -347,9 +349,9 @@ __global__ __launch_bounds__(256, 1) void pv_point_mlp_lds_kernel(
         const int k = ok ? k0 : 0;
 #pragma unroll
         for (int i = 0; i < S::PIECES; i++) {
-            const int row = i * 32 + (tid >> 3);
+            const int row = i * S::RSET + (tid >> 3);
             uint4 v;
-            if (row < S::TN)   // resolved at compile time (TN is a multiple of 32)
+            if (i * S::RSET < S::TN)   // resolved at compile time (TN: whole piece sets)
                 v = piece_bf16(wsrc + (size_t)min(n0 + row, Cout - 1) * Cin + k);
             else
                 v = piece_bf16(xsrc + (size_t)min(m0 + row - S::TN, M - 1) * x_ld + k);
@@ -361,7 +363,7 @@ __global__ __launch_bounds__(256, 1) void pv_point_mlp_lds_kernel(
         char* base = lds + buf * (S::ROWS * kGPitch) + (tid >> 3) * kGPitch + part * 16;
 #pragma unroll
         for (int i = 0; i < S::PIECES; i++)
-            *(uint4*)(base + i * 32 * kGPitch) = ok ? stage[i] : uint4{0u, 0u, 0u, 0u};
+            *(uint4*)(base + i * S::RSET * kGPitch) = ok ? stage[i] : uint4{0u, 0u, 0u, 0u};
     };
 
     const int wn = wave % WN, wm = wave / WN;
@@ -535,12 +537,12 @@ void launch_lds(const void* x, int x_ld, int M, int Cin, int Cout, const void* w
     const int nblocks = ntn * ((M + S::TM - 1) / S::TM);
     if (cb || res)
         hipLaunchKernelGGL((pv_point_mlp_lds_kernel<NB, MB, WN, WM, XT, true>), dim3(nblocks),
-                           dim3(256), 0, s, (const XT*)x, x_ld, M, Cin, Cout, (const uint16_t*)w,
+                           dim3(S::NTHR), 0, s, (const XT*)x, x_ld, M, Cin, Cout, (const uint16_t*)w,
                            bn, act, slope, cb, ppc, res, res_ld, out, (int)out_bf16, out_ld, ntn,
                            nblocks);
     else
         hipLaunchKernelGGL((pv_point_mlp_lds_kernel<NB, MB, WN, WM, XT, false>), dim3(nblocks),
-                           dim3(256), 0, s, (const XT*)x, x_ld, M, Cin, Cout, (const uint16_t*)w,
+                           dim3(S::NTHR), 0, s, (const XT*)x, x_ld, M, Cin, Cout, (const uint16_t*)w,
                            bn, act, slope, cb, ppc, res, res_ld, out, (int)out_bf16, out_ld, ntn,
                            nblocks);
 }
@@ -731,15 +733,16 @@ pvconv_status pv_launch_point_mlp(const void* x, bool x_bf16, int x_ld, int M, i
                         (!cb || pv_aligned16(cb)) && out_ld % 4 == 0 &&
                         ((uintptr_t)out & (out_bf16 ? 7u : 15u)) == 0;
         const bool tile = vec && c4;
-        // wide layers: LDS-tiled GEMM, 256 x 256 (channels x points) tiles
-        // when they still give a workgroup per CU, else 128 x 256 or 128 x 128
+        // wide layers: LDS-tiled GEMM, 256 x 256 (channels x points) tiles of
+        // eight waves (two per SIMD, 128 x 64 each) when they still give a
+        // workgroup per CU, else four-wave 128 x 256 or 128 x 128 tiles
         const long big_tiles = (long)((Cout + 255) / 256) * ((M + 255) / 256);
         if (tile && Cin >= 128 && Cout >= 256 && big_tiles >= 256) {
             if (x_bf16)
-                launch_lds<4, 4, 2, 2, uint16_t>(x, x_ld, M, Cin, Cout, w, bn, act, slope, cb, ppc,
+                launch_lds<4, 2, 2, 4, uint16_t>(x, x_ld, M, Cin, Cout, w, bn, act, slope, cb, ppc,
                                                  res, res_ld, out, out_bf16, out_ld, s);
             else
-                launch_lds<4, 4, 2, 2, float>(x, x_ld, M, Cin, Cout, w, bn, act, slope, cb, ppc,
+                launch_lds<4, 2, 2, 4, float>(x, x_ld, M, Cin, Cout, w, bn, act, slope, cb, ppc,
                                               res, res_ld, out, out_bf16, out_ld, s);
             return pv_launch_status();
         }
