@@ -735,7 +735,8 @@ pvconv_status pv_launch_point_mlp(const void* x, bool x_bf16, int x_ld, int M, i
         const bool tile = vec && c4;
         // wide layers: LDS-tiled GEMM, 256 x 256 (channels x points) tiles of
         // eight waves (two per SIMD, 128 x 64 each) when they still give a
-        // workgroup per CU, else four-wave 128 x 256 or 128 x 128 tiles
+        // workgroup per CU, else eight-wave 128 x 256 (128 x 32 each) or
+        // four-wave 128 x 128 tiles
         const long big_tiles = (long)((Cout + 255) / 256) * ((M + 255) / 256);
         if (tile && Cin >= 128 && Cout >= 256 && big_tiles >= 256) {
             if (x_bf16)
@@ -761,10 +762,10 @@ pvconv_status pv_launch_point_mlp(const void* x, bool x_bf16, int x_ld, int M, i
         if (tile && Cin >= 128 && Cout >= 128) {
             if (x_bf16)
 
-                launch_lds<4, 2, 1, 4, uint16_t>(x, x_ld, M, Cin, Cout, w, bn, act, slope, cb, ppc,
+                launch_lds<4, 1, 1, 8, uint16_t>(x, x_ld, M, Cin, Cout, w, bn, act, slope, cb, ppc,
                                                  res, res_ld, out, out_bf16, out_ld, s);
             else
-                launch_lds<4, 2, 1, 4, float>(x, x_ld, M, Cin, Cout, w, bn, act, slope, cb, ppc,
+                launch_lds<4, 1, 1, 8, float>(x, x_ld, M, Cin, Cout, w, bn, act, slope, cb, ppc,
                                               res, res_ld, out, out_bf16, out_ld, s);
             return pv_launch_status();
         }
