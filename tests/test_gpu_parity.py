@@ -289,6 +289,7 @@ def test_conv3d_f32_matches_oracle(B, R, Cin, Cout):
     (8, 32, 9, 64, "bf16"),       # scene-seg first conv: two workgroups per CU, value loads
     (1, 64, 64, 64, "bf16"),      # stress conv: two workgroups per CU
     (8, 32, 16, 64, "f32"),       # two workgroups per CU, fp32 output (two staging passes)
+    (2, 60, 64, 64, "bf16"),      # two workgroups per CU, ragged bricks on the far faces
 ])
 def test_conv3d_full_size_sampled(B, R, Cin, Cout, odt):
     # full batch in the launch configuration the benchmark uses (the channel
