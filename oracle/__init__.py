@@ -57,6 +57,7 @@ def _load():
         "ref_batchnorm": [_P, _I64, _I64, _P, _P, _P, _P, ctypes.c_double],
         "ref_devoxelize": [_P, _I64, ctypes.c_int, _I64, _P, _I64, _P],
         "ref_devoxelize_weights": [_P, _I64, ctypes.c_int, _P, _P],
+        "ref_devoxelize_nearest": [_P, _I64, ctypes.c_int, _I64, _P, _I64, _P],
         "ref_linear": [_P, _I64, _I64, _I64, _P, _P, _P],
         "ref_maxpool": [_P, _I64, _I64, _I64, _P],
     }
@@ -189,6 +190,20 @@ def devoxelize(grid: np.ndarray, R: int, pnorm: np.ndarray) -> np.ndarray:
     return out
 
 
+def devoxelize_nearest(grid: np.ndarray, R: int, ids: np.ndarray) -> np.ndarray:
+    """grid [B][R^3][C], ids [B][N] -> [B][N][C]: each point takes the row of
+    the voxel it falls into (Section 4.1 "Devoxelization", nearest neighbour)."""
+    lib = _load()
+    grid = _f64(grid)
+    ids = np.ascontiguousarray(ids, dtype=np.int32)
+    B, V, C = grid.shape
+    N = ids.shape[1]
+    out = np.empty((B, N, C))
+    _check(lib.ref_devoxelize_nearest(_ptr(grid), B, R, C, _ptr(ids), N, _ptr(out)),
+           "devoxelize_nearest")
+    return out
+
+
 def devoxelize_weights(pnorm: np.ndarray, R: int):
     """The 8 cells (linear id within the cloud) and trilinear weights per point."""
     lib = _load()
@@ -230,7 +245,8 @@ def maxpool(x: np.ndarray) -> np.ndarray:
 # composition: one PVConv layer (Figure "overview", Sections 4.1-4.3)
 # ----------------------------------------------------------------------------
 def voxel_branch(coords, feats, layer):
-    """Normalise, voxelise, n_convs x (conv + BN + leaky ReLU), devoxelise.
+    """Normalise, voxelise, n_convs x (conv + BN + leaky ReLU), devoxelise
+    (trilinear, or nearest neighbour when layer.devox == "nearest").
 
     Returns a dict with every intermediate: centroid, radius, pnorm, ids, grid,
     counts, conv outputs (list, post-activation) and devox [B][N][Cout]."""
@@ -242,7 +258,10 @@ def voxel_branch(coords, feats, layer):
     for w, bn in zip(layer.conv_w, layer.conv_bn):
         h = leaky_relu(batchnorm(conv3d(h, w, layer.R), bn), layer.slope)
         convs.append(h)
-    dv = devoxelize(h, layer.R, pn)
+    if getattr(layer, "devox", "trilinear") == "nearest":
+        dv = devoxelize_nearest(h, layer.R, ids)
+    else:
+        dv = devoxelize(h, layer.R, pn)
     return dict(centroid=c, radius=m, pnorm=pn, ids=ids, grid=grid, counts=counts,
                 convs=convs, devox=dv)
 

@@ -20,10 +20,13 @@
  *   ref_leaky_relu     Section 4.1 "Feature Aggregation" (leaky rectifier)
  *   ref_relu           Section 4.2 (point-branch MLP nonlinearity)
  *   ref_devoxelize     Section 4.1 "Devoxelization" (trilinear interpolation)
+ *   ref_devoxelize_nearest  Section 4.1 "Devoxelization", the nearest-neighbour
+ *                      mapping the section sets against trilinear (the
+ *                      devoxelisation row of the ablation table)
  *   ref_linear         Section 4.2 "Point-Based Feature Transformation"
  *   ref_maxpool        Section 5.1 "Models" (PointNet backbone global feature)
  * Fusion by addition (Section 4.3) and the composition of the steps live in
- * oracle/pvconv_oracle.py.
+ * oracle/__init__.py.
  *
  * Readings where the paper is silent (each also listed in the design notes):
  *  - the "gravity center" is the arithmetic mean of the coordinates, summed in
@@ -286,6 +289,26 @@ int ref_devoxelize(const double* grid, int64_t B, int R, int64_t C, const double
                         const double* cell = grid + (b * V + (iu[a] * R + iv[e]) * R + iw[g]) * C;
                         for (int64_t c = 0; c < C; c++) o[c] += wt * cell[c];
                     }
+        }
+    return PV_ORACLE_OK;
+}
+
+/* Nearest-neighbour devoxelisation: every point takes the features of the
+ * voxel it falls into, i.e. the voxel of its Eq. 2 index, so that all points
+ * of one voxel share one feature vector.
+ * grid [B][R^3][C], ids [B][N] (voxel index within the cloud) -> out [B][N][C].
+ * An index outside [0, R^3) is invalid input. */
+int ref_devoxelize_nearest(const double* grid, int64_t B, int R, int64_t C,
+                           const int32_t* ids, int64_t N, double* out) {
+    if (R < 1) return PV_ORACLE_EINVAL;
+    int64_t V = (int64_t)R * R * R;
+    for (int64_t k = 0; k < B * N; k++)
+        if (ids[k] < 0 || ids[k] >= V) return PV_ORACLE_EINVAL;
+    for (int64_t b = 0; b < B; b++)
+        for (int64_t k = 0; k < N; k++) {
+            const double* row = grid + (b * V + ids[b * N + k]) * C;
+            double* o = out + (b * N + k) * C;
+            for (int64_t c = 0; c < C; c++) o[c] = row[c];
         }
     return PV_ORACLE_OK;
 }

@@ -242,6 +242,7 @@ class PVConvParams:
     mlp_bn: BNParams
     mlp_b: Optional[np.ndarray] = None
     slope: float = LEAKY_SLOPE
+    devox: str = "trilinear"   # or "nearest"
 
     @property
     def n_convs(self):

@@ -362,6 +362,72 @@ def test_lone_point_gets_an_eighth_at_even_R():
         assert oracle.devoxelize(grid, R, pn)[0, 0, 0] == 0.5
 
 
+def test_nearest_devox_of_voxelize_is_the_voxel_mean_by_brute_force():
+    # Section 4.1 "Devoxelization", nearest neighbour: each point gets the
+    # features of the grid cell it falls into, so after voxelisation (no
+    # convolution) every point reads the mean over the points sharing its cell.
+    # The expectation groups points by their cell with a Python dict.
+    wl = synth.make_workload(2, B=2, N=600)
+    rng = _rng(30)
+    feats = rng.normal(size=(2, 600, 5))
+    for R in (4, 13, 32):
+        _, _, pn = oracle.normalize(wl.coords)
+        ids = oracle.voxel_ids(pn, R)
+        grid, _ = oracle.voxelize(ids, feats, R)
+        out = oracle.devoxelize_nearest(grid, R, ids)
+        for b in range(2):
+            groups = {}
+            for k in range(600):
+                groups.setdefault(int(ids[b, k]), []).append(k)
+            for cell, members in groups.items():
+                mean = feats[b, members].mean(axis=0)
+                np.testing.assert_allclose(out[b, members], np.broadcast_to(mean, (len(members), 5)),
+                                           rtol=1e-13, atol=1e-13)
+                # the paper's stated property: one cell, one shared feature
+                assert (out[b, members] == out[b, members[0]]).all()
+
+
+def test_nearest_devox_reads_the_cell_of_each_index_and_matches_trilinear_at_centres():
+    # a grid whose row is its own (u, v, w) digits: the output names the cell
+    R = 6
+    u, v, w = np.meshgrid(range(R), range(R), range(R), indexing="ij")
+    grid = (100 * u + 10 * v + w).reshape(1, R ** 3, 1).astype(np.float64)
+    ids = np.array([[0, 1, R, R * R, R ** 3 - 1, (2 * R + 3) * R + 5]], np.int32)
+    out = oracle.devoxelize_nearest(grid, R, ids)[0, :, 0]
+    np.testing.assert_array_equal(out, [0, 1, 10, 100, 555, 235])
+    # at a cell centre trilinear weights collapse onto that cell, and the
+    # centre's Eq. 2 index is that cell: the two mappings agree there
+    rng = _rng(31)
+    g = rng.normal(size=(1, R ** 3, 3))
+    cen = ((np.stack([u, v, w], -1) + 0.5) / R).reshape(1, -1, 3)
+    cid = oracle.voxel_ids(cen, R)
+    np.testing.assert_array_equal(cid[0], np.arange(R ** 3))
+    np.testing.assert_allclose(oracle.devoxelize_nearest(g, R, cid), oracle.devoxelize(g, R, cen),
+                               rtol=1e-14, atol=1e-14)
+
+
+def test_nearest_devox_rejects_indices_outside_the_grid():
+    grid = np.zeros((1, 8, 2))
+    for bad in (-1, 8):
+        with pytest.raises(ValueError):
+            oracle.devoxelize_nearest(grid, 2, np.array([[0, bad]], np.int32))
+
+
+def test_layer_with_nearest_devox_differs_only_in_the_voxel_branch_mapping():
+    wl = synth.make_workload(1, N=300)
+    L = wl.layers[0]
+    Ln = synth.PVConvParams(L.cin, L.cout, L.R, L.conv_w, L.conv_bn, L.mlp_w, L.mlp_bn,
+                            devox="nearest")
+    pt = oracle.pvconv_forward(wl.coords, wl.feats, L, return_parts=True)
+    pn_ = oracle.pvconv_forward(wl.coords, wl.feats, Ln, return_parts=True)
+    np.testing.assert_array_equal(pt["point"], pn_["point"])
+    np.testing.assert_array_equal(pt["convs"][-1], pn_["convs"][-1])
+    h = pt["convs"][-1]
+    ref = np.stack([h[b, pt["ids"][b]] for b in range(h.shape[0])])
+    np.testing.assert_array_equal(pn_["devox"], ref)
+    assert np.array_equal(pn_["out"], pn_["devox"] + pn_["point"])
+
+
 # ----------------------------------------------------------------------------
 # Point branch, fusion, max-pool (Sections 4.2, 4.3, 5.1)
 # ----------------------------------------------------------------------------
