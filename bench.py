@@ -54,6 +54,11 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-peaks", action="store_true",
                     help="skip the measured-peak probes (MFMA loop, copy)")
+    ap.add_argument("--variants", action="store_true",
+                    help="instead of the headline: the layer variants the paper discusses "
+                         "(R 16/24/32, one to three convolutions, channel widths, nearest-"
+                         "neighbour devoxelisation) on the part-seg layer's clouds, one JSON "
+                         "line each")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only copy a MIB-MiB buffer 3 times (a plain copy kernel of known "
                          "size, to calibrate the HBM byte counters) and exit")
@@ -323,6 +328,77 @@ def bench_network(args, wl, dev):
     print(json.dumps(line), flush=True)
 
 
+# Layer variants on the default workload's clouds (16 x 2048 points): the
+# resolution sweep of the resolution table (R = 16, 24, 32), the number of
+# convolutions per PVConv of the ablation table (1, 2, 3), narrower layers
+# (the width multipliers of the scene-segmentation table; bf16 MFMA needs
+# C_out % 32 == 0, so 0.25 x (64 -> 128) is the narrowest) and the
+# nearest-neighbour devoxelisation the ablation compares with trilinear.
+VARIANTS = [
+    # name, R, n_convs, width, devox
+    ("base", 32, 2, 1.0, "trilinear"),
+    ("R16", 16, 2, 1.0, "trilinear"),
+    ("R24", 24, 2, 1.0, "trilinear"),
+    ("convs1", 32, 1, 1.0, "trilinear"),
+    ("convs3", 32, 3, 1.0, "trilinear"),
+    ("width0.5", 32, 2, 0.5, "trilinear"),
+    ("width0.25", 32, 2, 0.25, "trilinear"),
+    ("nearest", 32, 2, 1.0, "nearest"),
+    ("R16_width0.25", 16, 2, 0.25, "trilinear"),
+]
+
+
+def bench_variants(args, dev):
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_1907_03739_amd import binding as pv
+
+    wl = synth.make_workload(2)
+    B, N = wl.B, wl.N
+    coords = torch.as_tensor(wl.coords).to(dev)
+    stream = torch.cuda.current_stream(dev)
+    REPS = 10
+    for name, R, n_convs, width, devox in VARIANTS:
+        cin, cout = int(64 * width), int(128 * width)
+        rng = np.random.default_rng(7000 + R + 10 * n_convs + int(100 * width))
+        L = synth.draw_pvconv(rng, cin, cout, R, n_convs, bf16=True)
+        L.devox = devox
+        layer = pv.DeviceLayer(L, dev, torch.bfloat16)
+        feats = torch.as_tensor(wl.feats[..., :cin]).to(dev).contiguous()
+        out = torch.empty((B, N, cout), dtype=torch.float32, device=dev)
+        ws = torch.empty(max(pv.pvconv_forward_workspace_size(B, N, layer), 256),
+                         dtype=torch.uint8, device=dev)
+        fn = lambda: pv.pvconv_forward(coords, feats, layer, out=out, workspace=ws)
+        for _ in range(max(1, args.warmup // 5)):
+            fn()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(REPS):
+                fn()
+        g.replay()
+        torch.cuda.synchronize()
+        times = []
+        for _ in range(max(3, args.steps // REPS)):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            g.replay()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            times.append(e0.elapsed_time(e1) / REPS)
+        del g
+        ms = statistics.median(times)
+        flops = sum(conv_flops(B, R, cin if i == 0 else cout, cout) for i in range(n_convs))
+        print(json.dumps({
+            "variant": name, "R": R, "n_convs": n_convs, "cin": cin, "cout": cout,
+            "devox": devox, "B": B, "N": N, "ms_per_layer": round(ms, 4),
+            "ms_min": round(min(times), 4), "points_per_s": round(B * N / (ms * 1e-3), 1),
+            "conv_tflop_per_layer": round(flops / 1e12, 4), "dtype": "bf16",
+            "data": "synthetic"}), flush=True)
+
+
 def synth_one(wl, b):
     """Workload wl restricted to its cloud b (the networks are per cloud)."""
     import copy
@@ -355,6 +431,8 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
 
+    if args.variants:
+        return bench_variants(args, dev)
     wl = synth.make_workload(args.workload)
     if wl.is_network:
         return bench_network(args, wl, dev)

@@ -150,6 +150,25 @@ pvconv_status pvconv_devoxelize(const void* grid, int B, int R, int C, pvconv_dt
                                 const float* norm_coords, int N, float* out, void* stream);
 
 /* ------------------------------------------------------------------------- */
+/* Nearest-neighbour devoxelisation: the alternative to trilinear            */
+/* interpolation that Section 4.1 "Devoxelization" describes (every point    */
+/* takes the features of the grid cell it falls into; the devoxelisation     */
+/* row of the ablation table compares the two).                              */
+/*                                                                           */
+/*  out[b][k][c] = grid[b][vox_id[b][k]][c], in fp32 (exact for both grid    */
+/*  dtypes).                                                                 */
+/*  grid    [B][R^3][C] (grid_dt)                                            */
+/*  vox_id  [B][N] int32 voxel index within the cloud, as pvconv_voxelize    */
+/*          writes it; an index outside [0, R^3) is a precondition violation */
+/*          (it is clamped into the grid: memory-safe, result unspecified)   */
+/*  out     out [B][N][C] fp32                                               */
+/* 1 <= R <= 128, 1 <= C. Same alignment rules as pvconv_devoxelize.         */
+/* ------------------------------------------------------------------------- */
+pvconv_status pvconv_devoxelize_nearest(const void* grid, int B, int R, int C,
+                                        pvconv_dtype grid_dt, const int32_t* vox_id, int N,
+                                        float* out, void* stream);
+
+/* ------------------------------------------------------------------------- */
 /* Shared per-point MLP layer with fused epilogue: Section 4.2 (point-based  */
 /* feature transformation) and Section 4.3 (fusion by addition).             */
 /*                                                                           */
@@ -183,11 +202,17 @@ pvconv_status pvconv_point_mlp(const void* x, pvconv_dtype x_dt, int x_ld, int M
 pvconv_status pvconv_maxpool(const void* x, pvconv_dtype dt, int x_ld, int B, int N, int C,
                              float* out, void* stream);
 
+/* Devoxelisation of a layer (Section 4.1 "Devoxelization"). */
+typedef enum { PVCONV_DEVOX_TRILINEAR = 0, PVCONV_DEVOX_NEAREST = 1 } pvconv_devox;
+
 /* ------------------------------------------------------------------------- */
 /* One whole PVConv layer: Section 4, Figure "overview".                     */
 /*                                                                           */
 /* out = devoxelise( [conv + BN + leaky]^n_convs ( voxelise(coords, feats) ) ) */
 /*       + ReLU( BN( W_mlp feats + b_mlp ) )                                 */
+/* devoxelise is trilinear (pvconv_devoxelize) or, with devox =              */
+/* PVCONV_DEVOX_NEAREST, nearest neighbour (pvconv_devoxelize_nearest). A     */
+/* zero-initialised struct selects trilinear.                                */
 /* All weights are in compute_dt (BF16 or F32); grids are kept in            */
 /* compute_dt. out is [B][N][cout] (out_dt) with row stride out_ld.          */
 /* ------------------------------------------------------------------------- */
@@ -200,6 +225,7 @@ typedef struct {
     const float* mlp_b;                        /* [cout] or NULL */
     pvconv_bn mlp_bn;
     pvconv_dtype compute_dt;
+    pvconv_devox devox;
 } pvconv_layer;
 
 size_t pvconv_forward_workspace_size(int B, int N, const pvconv_layer* L);

@@ -42,7 +42,9 @@ class Layer(ctypes.Structure):
     _fields_ = [("cin", _I), ("cout", _I), ("R", _I), ("n_convs", _I),
                 ("conv_w", _VP * MAX_CONVS), ("conv_bn", BN * MAX_CONVS),
                 ("conv_slope", _F), ("mlp_w", _VP), ("mlp_b", _VP), ("mlp_bn", BN),
-                ("compute_dt", _I)]
+                ("compute_dt", _I), ("devox", _I)]
+
+DEVOX = {"trilinear": 0, "nearest": 1}
 
 
 _SIGS = {
@@ -53,6 +55,7 @@ _SIGS = {
     "pvconv_conv3d": ([_VP, _I, _I, _I, _I, _VP, _VP, _VP, _I, _F, _I, _VP, _I, _VP, _SZ, _VP],
                       _I),
     "pvconv_devoxelize": ([_VP, _I, _I, _I, _I, _VP, _I, _VP, _VP], _I),
+    "pvconv_devoxelize_nearest": ([_VP, _I, _I, _I, _I, _VP, _I, _VP, _VP], _I),
     "pvconv_point_mlp": ([_VP, _I, _I, _I, _I, _I, _VP, _I, _VP, _VP, _I, _F, _VP, _I, _VP, _I,
                           _VP, _I, _I, _VP], _I),
     "pvconv_maxpool": ([_VP, _I, _I, _I, _I, _I, _VP, _VP], _I),
@@ -195,6 +198,20 @@ def pvconv_devoxelize(grid: torch.Tensor, R: int, norm_coords: torch.Tensor, out
     return out
 
 
+def pvconv_devoxelize_nearest(grid: torch.Tensor, R: int, vox_id: torch.Tensor, out=None):
+    """grid [B][R^3][C], vox_id [B][N] int32 -> [B][N][C] f32 (each point takes
+    the row of its voxel)."""
+    B, V, C = grid.shape
+    N = vox_id.shape[1]
+    if vox_id.dtype != torch.int32:
+        raise TypeError("vox_id must be int32")
+    out = _out(out, (B, N, C), torch.float32, grid.device, "out")
+    _check("pvconv_devoxelize_nearest", _lib.pvconv_devoxelize_nearest(
+        _p(grid.contiguous()), B, R, C, _dt(grid), _p(vox_id.contiguous()), N, _p(out),
+        _stream(grid)))
+    return out
+
+
 def pvconv_point_mlp(x: torch.Tensor, weight: torch.Tensor, bias=None, bn=None, act="relu",
                      slope=0.0, cloud_bias=None, points_per_cloud=1, residual=None,
                      out: Optional[torch.Tensor] = None, out_dtype=torch.float32):
@@ -256,6 +273,7 @@ class DeviceLayer:
         L.mlp_b = self.mlp_b.data_ptr() if self.mlp_b is not None else None
         L.mlp_bn = _bn_struct(self.mlp_bn)
         L.compute_dt = _dt(self.mlp_w)
+        L.devox = DEVOX[getattr(params, "devox", "trilinear")]
         self.struct = L
         self.dtype = dt
 

@@ -68,6 +68,8 @@ pvconv_status check_layer(const pvconv_layer* L) {
     for (int i = 0; i < L->n_convs; i++)
         if (!L->conv_w[i] || !bn_ok(&L->conv_bn[i])) return PVCONV_EINVAL;
     if (!L->mlp_w || !bn_ok(&L->mlp_bn)) return PVCONV_EINVAL;
+    if (L->devox != PVCONV_DEVOX_TRILINEAR && L->devox != PVCONV_DEVOX_NEAREST)
+        return PVCONV_EINVAL;
     return PVCONV_OK;
 }
 
@@ -157,6 +159,21 @@ pvconv_status pvconv_devoxelize(const void* grid, int B, int R, int C, pvconv_dt
         return PVCONV_EINVAL;
     return pv_launch_devoxelize(grid, B, R, C, grid_dt == PVCONV_BF16, norm_coords, N, out,
                                 as_stream(stream));
+}
+
+pvconv_status pvconv_devoxelize_nearest(const void* grid, int B, int R, int C,
+                                        pvconv_dtype grid_dt, const int32_t* vox_id, int N,
+                                        float* out, void* stream) {
+    if (B < 0 || N < 0 || R < 1 || R > PVCONV_MAX_R || C < 1 || !sizes_fit(B, N))
+        return PVCONV_EINVAL;
+    if (!dtype_ok(grid_dt)) return PVCONV_EINVAL;
+    if (B == 0 || N == 0) return PVCONV_OK;
+    if (!grid || !vox_id || !out) return PVCONV_EINVAL;
+    if (((uintptr_t)grid & (esize(grid_dt) - 1)) || ((uintptr_t)vox_id & 3) ||
+        ((uintptr_t)out & 3))
+        return PVCONV_EINVAL;
+    return pv_launch_devoxelize_nearest(grid, B, R, C, grid_dt == PVCONV_BF16, vox_id, N, out,
+                                        as_stream(stream));
 }
 
 pvconv_status pvconv_point_mlp(const void* x, pvconv_dtype x_dt, int x_ld, int M, int Cin,
@@ -253,7 +270,9 @@ pvconv_status pvconv_forward(const float* coords, const void* feats, pvconv_dtyp
         dst = t;
         cin = L->cout;
     }
-    st = pv_launch_devoxelize(src, B, R, L->cout, bf, w.pnorm, N, w.devox, s);
+    st = L->devox == PVCONV_DEVOX_NEAREST
+             ? pv_launch_devoxelize_nearest(src, B, R, L->cout, bf, w.ids, N, w.devox, s)
+             : pv_launch_devoxelize(src, B, R, L->cout, bf, w.pnorm, N, w.devox, s);
     if (st != PVCONV_OK) return st;
     return pv_launch_point_mlp(feats, feat_dt == PVCONV_BF16, feat_ld, B * N, L->cin, L->cout,
                                L->mlp_w, bf, pv_make_fold(&L->mlp_bn, L->mlp_b), PVCONV_ACT_RELU,

@@ -115,6 +115,9 @@ pvconv_status pv_launch_conv3d(const void* x, int B, int R, int Cin, int Cout, c
                                bool out_bf16, void* ws, hipStream_t s, bool packed = false);
 pvconv_status pv_launch_devoxelize(const void* grid, int B, int R, int C, bool grid_bf16,
                                    const float* pn, int N, float* out, hipStream_t s);
+pvconv_status pv_launch_devoxelize_nearest(const void* grid, int B, int R, int C, bool grid_bf16,
+                                           const int32_t* ids, int N, float* out,
+                                           hipStream_t s);
 pvconv_status pv_launch_point_mlp(const void* x, bool x_bf16, int x_ld, int M, int Cin,
                                   int Cout, const void* w, bool bf16, const PvBnFold& bn,
                                   int act, float slope, const float* cloud_bias, int ppc,

@@ -29,7 +29,7 @@ def declared_functions():
 
 def test_library_exports_every_declared_symbol():
     names = declared_functions()
-    assert len(names) == 10
+    assert len(names) == 11
     out = subprocess.run(["nm", "-D", "--defined-only", b.LIB_PATH], capture_output=True,
                          text=True, check=True).stdout
     exported = set(re.findall(r"\bT (pvconv_\w+)", out))
@@ -131,6 +131,23 @@ def test_devoxelize_rejects(kw, status):
     assert _devox(**kw) == status
 
 
+def _devox_nn(**kw):
+    a = dict(grid=FAKE, B=2, R=8, C=16, dt=1, ids=FAKE, N=10, out=FAKE, s=None)
+    a.update(kw)
+    return L.pvconv_devoxelize_nearest(a["grid"], a["B"], a["R"], a["C"], a["dt"], a["ids"],
+                                       a["N"], a["out"], a["s"])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(B=-1), EINVAL), (dict(N=-1), EINVAL), (dict(R=0), EINVAL), (dict(R=129), EINVAL),
+    (dict(C=0), EINVAL), (dict(dt=9), EINVAL), (dict(grid=None), EINVAL),
+    (dict(ids=None), EINVAL), (dict(out=None), EINVAL), (dict(ids=FAKE_ODD), EINVAL),
+    (dict(grid=FAKE_ODD), EINVAL), (dict(N=0), OK), (dict(B=0), OK),
+])
+def test_devoxelize_nearest_rejects(kw, status):
+    assert _devox_nn(**kw) == status
+
+
 def _mlp(**kw):
     a = dict(x=FAKE, x_dt=0, x_ld=0, M=100, Cin=64, Cout=128, w=FAKE, dt=1, bias=None, bn=None,
              act=1, slope=0.0, cb=None, ppc=1, res=None, res_ld=0, out=ctypes.c_void_p(0x200000),
@@ -194,7 +211,7 @@ def test_forward_rejects():
     assert _fwd(lay, B=0) == OK
     for field, val, status in [("n_convs", 0, EINVAL), ("n_convs", 5, EINVAL), ("R", 0, EINVAL),
                                ("cout", 48, ENOTSUP), ("compute_dt", 4, EINVAL),
-                               ("cin", 0, EINVAL)]:
+                               ("cin", 0, EINVAL), ("devox", 2, EINVAL), ("devox", -1, EINVAL)]:
         lay = _layer()
         setattr(lay, field, val)
         assert _fwd(lay) == status, field

@@ -7,6 +7,8 @@ part-segmentation and stress sizes where the oracle is cheap (voxelisation,
 the whole stress layer), and sampled outputs at full size where it is not
 (the part-segmentation convolutions and layer).
 """
+import dataclasses
+
 import numpy as np
 import pytest
 import torch
@@ -332,6 +334,27 @@ def test_devoxelize_matches_oracle(wl_idx, B, N, R, C, gdt):
     assert_dot_f32(host(out), ref, mag, "devoxelize")
 
 
+@pytest.mark.parametrize("wl_idx,B,N,R,C,gdt", [
+    (2, 16, 2048, 32, 128, "bf16"), (5, 1, 65536, 64, 64, "bf16"), (1, 1, 1024, 8, 32, "f32"),
+    (2, 3, 999, 24, 20, "bf16"), (2, 2, 777, 7, 3, "f32"), (4, 2, 4096, 16, 9, "bf16"),
+])
+def test_devoxelize_nearest_matches_oracle(wl_idx, B, N, R, C, gdt):
+    # a copy of the voxel's row: bit-exact against the oracle
+    rng = np.random.default_rng(R * 11 + C)
+    wl = synth.make_workload(wl_idx, B=B, N=N)
+    _, _, pn = oracle.normalize(wl.coords)
+    ids = oracle.voxel_ids(pn, R)
+    ids[:, :5] = [0, R ** 3 - 1, R - 1, R * R, R ** 3 // 2]   # grid corners and middle
+    G = rng.normal(size=(B, R ** 3, C)).astype(np.float32).astype(np.float64)
+    if gdt == "bf16":
+        G = bf16_round(G)
+    ref = oracle.devoxelize_nearest(G, R, ids)
+    out = pv.pvconv_devoxelize_nearest(
+        dev(G, torch.bfloat16 if gdt == "bf16" else torch.float32), R,
+        torch.as_tensor(ids, dtype=torch.int32).cuda())
+    assert np.array_equal(host(out), ref)
+
+
 # ----------------------------------------------------------------------------
 # point MLP with fused epilogue
 # ----------------------------------------------------------------------------
@@ -463,6 +486,21 @@ def test_forward_bf16_layer(wl_idx, B):
     ref = oracle.pvconv_forward(wl.coords, wl.feats, wl.layers[0])
     got = _run_layer(wl, wl.layers[0], torch.bfloat16)
     assert_bf16_chain(got, ref, f"layer wl{wl_idx}")
+
+
+@pytest.mark.parametrize("wl_idx,B", [(2, 2), (1, 1)])
+def test_forward_nearest_devox_layer(wl_idx, B):
+    # the layer with the nearest-neighbour mapping (Section 4.1 "Devoxelization")
+    wl = synth.make_workload(wl_idx, B=B)
+    L = dataclasses.replace(wl.layers[0], devox="nearest")
+    ref = oracle.pvconv_forward(wl.coords, wl.feats, L)
+    if wl_idx == 1:
+        got = _run_layer(wl, L, torch.float32)
+        rms = np.sqrt(np.mean(ref ** 2))
+        assert_dot_f32(got, ref, np.full_like(ref, rms), "fp32 layer, nearest devox")
+    else:
+        got = _run_layer(wl, L, torch.bfloat16)
+        assert_bf16_chain(got, ref, "bf16 layer, nearest devox")
 
 
 def test_forward_scene_first_block_nine_channels():
