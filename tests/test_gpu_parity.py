@@ -503,6 +503,26 @@ def test_forward_nearest_devox_layer(wl_idx, B):
         assert_bf16_chain(got, ref, "bf16 layer, nearest devox")
 
 
+@pytest.mark.parametrize("R,n_convs,width,devox", [
+    (24, 2, 1.0, "trilinear"), (32, 1, 1.0, "trilinear"), (32, 3, 1.0, "trilinear"),
+    (32, 2, 0.25, "trilinear"), (16, 3, 0.5, "nearest"), (24, 2, 0.5, "nearest"),
+])
+def test_forward_layer_variants(R, n_convs, width, devox):
+    # the variants the paper's resolution and ablation tables vary: R (24 is
+    # not a power of two), one to three convolutions, narrower channels, and
+    # the devoxelisation mapping; two part-seg clouds each
+    wl = synth.make_workload(2, B=2)
+    cin, cout = int(64 * width), int(128 * width)
+    L = synth.draw_pvconv(np.random.default_rng(R + 10 * n_convs), cin, cout, R, n_convs,
+                          bf16=True)
+    L.devox = devox
+    feats = np.ascontiguousarray(wl.feats[..., :cin])
+    ref = oracle.pvconv_forward(wl.coords, feats, L)
+    layer = pv.DeviceLayer(L, "cuda", torch.bfloat16)
+    got = host(pv.pvconv_forward(dev(wl.coords), dev(feats), layer))
+    assert_bf16_chain(got, ref, f"layer R{R} x{n_convs} {cin}->{cout} {devox}")
+
+
 def test_forward_scene_first_block_nine_channels():
     wl = synth.make_workload(4, B=2)
     L = wl.layers[0]
