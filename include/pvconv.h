@@ -111,6 +111,22 @@ pvconv_status pvconv_voxelize(const float* coords, const void* feats, pvconv_dty
                               void* stream);
 
 /* ------------------------------------------------------------------------- */
+/* Voxelisation from given voxel indices: Eq. 2 (Section 4.1                 */
+/* "Voxelization") with the indices of an earlier pvconv_voxelize of the     */
+/* same coordinates and the same R. Every layer that voxelises the same      */
+/* points at the same resolution has the same indices (the normalisation     */
+/* depends on the coordinates only), so they are computed once per R.        */
+/*  vox_id  [B][N] int32 in [0, R^3) (an index outside is invalid input: the */
+/*          point is dropped; memory-safe)                                   */
+/*  other arguments, outputs and the workspace as for pvconv_voxelize        */
+/*  (workspace >= pvconv_voxelize_workspace_size(B, N, R))                   */
+/* ------------------------------------------------------------------------- */
+pvconv_status pvconv_voxelize_from_ids(const int32_t* vox_id, const void* feats,
+                                       pvconv_dtype feat_dt, int feat_ld, int B, int N, int C,
+                                       int R, void* grid, pvconv_dtype grid_dt, int32_t* counts,
+                                       void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------- */
 /* 3x3x3 convolution + batch norm + activation: Section 4.1 "Feature         */
 /* Aggregation", with the fixed-offset kernel of Section 3 (Eq. 1; each axis */
 /* offset in {0, +-1}).                                                      */
@@ -233,6 +249,21 @@ pvconv_status pvconv_forward(const float* coords, const void* feats, pvconv_dtyp
                              int feat_ld, int B, int N, const pvconv_layer* L, void* out,
                              pvconv_dtype out_dt, int out_ld, void* workspace,
                              size_t workspace_bytes, void* stream);
+
+/* The same layer, sharing its normalisation with other layers of the same    */
+/* points (Section 4.1 "Normalization" depends on the coordinates only, and  */
+/* the voxel indices on the coordinates and R):                              */
+/*  ids_given = 0: vox_id [B][N] int32 and norm_coords [B][N][3] fp32 are    */
+/*    outputs (each may be NULL), as pvconv_voxelize writes them;            */
+/*  ids_given = 1: both are inputs (non-NULL) from such a call with the same */
+/*    coordinates and the same R; the normalisation is skipped and coords    */
+/*    is not read (may be NULL).                                             */
+/* pvconv_forward(...) is pvconv_forward_ex(..., NULL, NULL, 0, ...).         */
+pvconv_status pvconv_forward_ex(const float* coords, const void* feats, pvconv_dtype feat_dt,
+                                int feat_ld, int B, int N, const pvconv_layer* L,
+                                int32_t* vox_id, float* norm_coords, int ids_given, void* out,
+                                pvconv_dtype out_dt, int out_ld, void* workspace,
+                                size_t workspace_bytes, void* stream);
 
 #ifdef __cplusplus
 }

@@ -51,6 +51,8 @@ _SIGS = {
     "pvconv_voxelize_workspace_size": ([_I, _I, _I], _SZ),
     "pvconv_voxelize": ([_VP, _VP, _I, _I, _I, _I, _I, _I, _VP, _I, _VP, _VP, _VP, _VP, _SZ, _VP],
                         _I),
+    "pvconv_voxelize_from_ids": ([_VP, _VP, _I, _I, _I, _I, _I, _I, _VP, _I, _VP, _VP, _SZ,
+                                  _VP], _I),
     "pvconv_conv3d_workspace_size": ([_I, _I, _I], _SZ),
     "pvconv_conv3d": ([_VP, _I, _I, _I, _I, _VP, _VP, _VP, _I, _F, _I, _VP, _I, _VP, _SZ, _VP],
                       _I),
@@ -62,6 +64,8 @@ _SIGS = {
     "pvconv_forward_workspace_size": ([_I, _I, ctypes.POINTER(Layer)], _SZ),
     "pvconv_forward": ([_VP, _VP, _I, _I, _I, _I, ctypes.POINTER(Layer), _VP, _I, _I, _VP, _SZ,
                         _VP], _I),
+    "pvconv_forward_ex": ([_VP, _VP, _I, _I, _I, _I, ctypes.POINTER(Layer), _VP, _VP, _I, _VP,
+                           _I, _I, _VP, _SZ, _VP], _I),
     "pvconv_status_string": ([_I], ctypes.c_char_p),
 }
 for _name, (_args, _res) in _SIGS.items():
@@ -163,6 +167,27 @@ def pvconv_voxelize(coords: torch.Tensor, feats: torch.Tensor, R: int,
         _p(coords), _p(feats), _dt(feats), ld, B, N, C, R, _p(grid), _dt(grid), _p(counts),
         _p(ids), _p(pn), _p(ws), wsb, _stream(coords)))
     return grid, counts, ids, pn
+
+
+def pvconv_voxelize_from_ids(vox_id: torch.Tensor, feats: torch.Tensor, R: int,
+                             grid_dtype=torch.float32, grid=None, counts=None, workspace=None):
+    """vox_id [B][N] int32 (from pvconv_voxelize at the same R), feats [B][N][C]
+    -> (grid [B][R^3][C], counts [B][R^3])."""
+    B, N = vox_id.shape
+    C = feats.shape[-1]
+    dev = feats.device
+    if vox_id.dtype != torch.int32 or not vox_id.is_contiguous():
+        raise TypeError("vox_id must be a contiguous int32 tensor")
+    ld = _rows(feats, N, C)
+    grid = _out(grid, (B, R ** 3, C), _torch_dt(grid_dtype), dev, "grid")
+    counts = _out(counts, (B, R ** 3), torch.int32, dev, "counts")
+    wsb = _lib.pvconv_voxelize_workspace_size(B, N, R)
+    ws = workspace if workspace is not None and workspace.numel() >= wsb else \
+        torch.empty(max(wsb, 256), dtype=torch.uint8, device=dev)
+    _check("pvconv_voxelize_from_ids", _lib.pvconv_voxelize_from_ids(
+        _p(vox_id), _p(feats), _dt(feats), ld, B, N, C, R, _p(grid), _dt(grid), _p(counts),
+        _p(ws), wsb, _stream(feats)))
+    return grid, counts
 
 
 def pvconv_conv3d(x: torch.Tensor, weight: torch.Tensor, R: int, bn=None,
@@ -284,18 +309,30 @@ def pvconv_forward_workspace_size(B: int, N: int, layer: DeviceLayer) -> int:
 
 def pvconv_forward(coords: torch.Tensor, feats: torch.Tensor, layer: DeviceLayer,
                    out: Optional[torch.Tensor] = None, out_dtype=torch.float32,
-                   workspace: Optional[torch.Tensor] = None):
-    """One PVConv layer: coords [B][N][3] f32, feats [B][N][cin] -> [B][N][cout]."""
-    B, N, _ = coords.shape
+                   workspace: Optional[torch.Tensor] = None,
+                   vox_id: Optional[torch.Tensor] = None, norm: Optional[torch.Tensor] = None,
+                   ids_given: bool = False):
+    """One PVConv layer: coords [B][N][3] f32, feats [B][N][cin] -> [B][N][cout].
+
+    vox_id [B][N] int32 and norm [B][N][3] f32: written by the call (outputs),
+    or with ids_given=True read instead of normalising again (from an earlier
+    call on the same coordinates at the same R; coords is then not read)."""
+    B, N = feats.shape[0], feats.shape[1]
     cin, cout = layer.params.cin, layer.params.cout
     f_ld = _rows(feats, N, cin)
     if out is None:
-        out = torch.empty((B, N, cout), dtype=_torch_dt(out_dtype), device=coords.device)
+        out = torch.empty((B, N, cout), dtype=_torch_dt(out_dtype), device=feats.device)
     o_ld = _rows(out, N, cout)
     need = pvconv_forward_workspace_size(B, N, layer)
     if workspace is None or workspace.numel() < need:
-        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=coords.device)
-    _check("pvconv_forward", _lib.pvconv_forward(
-        _p(coords), _p(feats), _dt(feats), f_ld, B, N, ctypes.byref(layer.struct), _p(out),
-        _dt(out), o_ld, _p(workspace), workspace.numel(), _stream(coords)))
+        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=feats.device)
+    for t, shape, dt in ((vox_id, (B, N), torch.int32), (norm, (B, N, 3), torch.float32)):
+        if t is not None and (tuple(t.shape) != shape or t.dtype != dt or not t.is_contiguous()):
+            raise ValueError(f"expected a contiguous {shape} {dt} tensor")
+    if ids_given and (vox_id is None or norm is None):
+        raise ValueError("ids_given needs vox_id and norm")
+    _check("pvconv_forward_ex", _lib.pvconv_forward_ex(
+        _p(coords), _p(feats), _dt(feats), f_ld, B, N, ctypes.byref(layer.struct), _p(vox_id),
+        _p(norm), int(ids_given), _p(out), _dt(out), o_ld, _p(workspace), workspace.numel(),
+        _stream(feats)))
     return out

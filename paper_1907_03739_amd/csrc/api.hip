@@ -117,6 +117,28 @@ pvconv_status pvconv_voxelize(const float* coords, const void* feats, pvconv_dty
                               as_stream(stream));
 }
 
+pvconv_status pvconv_voxelize_from_ids(const int32_t* vox_id, const void* feats,
+                                       pvconv_dtype feat_dt, int feat_ld, int B, int N, int C,
+                                       int R, void* grid, pvconv_dtype grid_dt, int32_t* counts,
+                                       void* workspace, size_t workspace_bytes, void* stream) {
+    if (B < 0 || N < 0 || C < 1 || R < 1 || R > PVCONV_MAX_R || !sizes_fit(B, N))
+        return PVCONV_EINVAL;
+    if (!dtype_ok(feat_dt) || !dtype_ok(grid_dt)) return PVCONV_EINVAL;
+    if (feat_ld == 0) feat_ld = C;
+    if (feat_ld < C) return PVCONV_EINVAL;
+    if (B == 0) return PVCONV_OK;
+    if (!grid || !counts || (N > 0 && (!vox_id || !feats))) return PVCONV_EINVAL;
+    if (((uintptr_t)vox_id & 3) || ((uintptr_t)counts & 3) ||
+        ((uintptr_t)feats & (esize(feat_dt) - 1)) || ((uintptr_t)grid & (esize(grid_dt) - 1)))
+        return PVCONV_EINVAL;
+    if (!workspace || ((uintptr_t)workspace & 255) ||
+        workspace_bytes < pv_voxelize_ws_bytes(B, N, R))
+        return PVCONV_EWORKSPACE;
+    return pv_launch_voxelize_from_ids(vox_id, feats, feat_dt == PVCONV_BF16, feat_ld, B, N, C,
+                                       R, grid, grid_dt == PVCONV_BF16, counts, workspace,
+                                       as_stream(stream));
+}
+
 size_t pvconv_conv3d_workspace_size(int Cin, int Cout, pvconv_dtype dt) {
     if (Cin < 1 || Cout < 1 || Cin > PVCONV_MAX_CONV_CHANNELS || Cout > PVCONV_MAX_CONV_CHANNELS ||
         !dtype_ok(dt))
@@ -227,6 +249,15 @@ pvconv_status pvconv_forward(const float* coords, const void* feats, pvconv_dtyp
                              int feat_ld, int B, int N, const pvconv_layer* L, void* out,
                              pvconv_dtype out_dt, int out_ld, void* workspace,
                              size_t workspace_bytes, void* stream) {
+    return pvconv_forward_ex(coords, feats, feat_dt, feat_ld, B, N, L, nullptr, nullptr, 0, out,
+                             out_dt, out_ld, workspace, workspace_bytes, stream);
+}
+
+pvconv_status pvconv_forward_ex(const float* coords, const void* feats, pvconv_dtype feat_dt,
+                                int feat_ld, int B, int N, const pvconv_layer* L,
+                                int32_t* vox_id, float* norm_coords, int ids_given, void* out,
+                                pvconv_dtype out_dt, int out_ld, void* workspace,
+                                size_t workspace_bytes, void* stream) {
     pvconv_status st = check_layer(L);
     if (st != PVCONV_OK) return st;
     if (B < 0 || N < 0 || !sizes_fit(B, N) || !dtype_ok(feat_dt) || !dtype_ok(out_dt))
@@ -234,10 +265,13 @@ pvconv_status pvconv_forward(const float* coords, const void* feats, pvconv_dtyp
     if (feat_ld == 0) feat_ld = L->cin;
     if (out_ld == 0) out_ld = L->cout;
     if (feat_ld < L->cin || out_ld < L->cout) return PVCONV_EINVAL;
+    if (ids_given != 0 && ids_given != 1) return PVCONV_EINVAL;
     if (B == 0 || N == 0) return PVCONV_OK;
-    if (!coords || !feats || !out) return PVCONV_EINVAL;
+    if ((!ids_given && !coords) || (ids_given && (!vox_id || !norm_coords)) || !feats || !out)
+        return PVCONV_EINVAL;
     if (((uintptr_t)coords & 3) || ((uintptr_t)feats & (esize(feat_dt) - 1)) ||
-        ((uintptr_t)out & (esize(out_dt) - 1)))
+        ((uintptr_t)out & (esize(out_dt) - 1)) || ((uintptr_t)vox_id & 3) ||
+        ((uintptr_t)norm_coords & 3))
         return PVCONV_EINVAL;
     const size_t need = carve_forward(nullptr, B, N, L).total;
     if (!workspace || ((uintptr_t)workspace & 255) || workspace_bytes < need)
@@ -247,8 +281,14 @@ pvconv_status pvconv_forward(const float* coords, const void* feats, pvconv_dtyp
     const bool bf = L->compute_dt == PVCONV_BF16;
     const int R = L->R;
 
-    st = pv_launch_voxelize(coords, feats, feat_dt == PVCONV_BF16, feat_ld, B, N, L->cin, R,
-                            w.grid_a, bf, w.counts, w.ids, w.pnorm, w.vox_ws, s);
+    int32_t* ids = vox_id ? vox_id : w.ids;
+    const float* pnorm = norm_coords ? norm_coords : w.pnorm;
+    st = ids_given ? pv_launch_voxelize_from_ids(ids, feats, feat_dt == PVCONV_BF16, feat_ld, B,
+                                                 N, L->cin, R, w.grid_a, bf, w.counts, w.vox_ws,
+                                                 s)
+                   : pv_launch_voxelize(coords, feats, feat_dt == PVCONV_BF16, feat_ld, B, N,
+                                        L->cin, R, w.grid_a, bf, w.counts, ids,
+                                        norm_coords ? norm_coords : w.pnorm, w.vox_ws, s);
     if (st != PVCONV_OK) return st;
     // bf16: the weights of all the convolutions repacked in one launch
     if (bf) {
@@ -271,8 +311,8 @@ pvconv_status pvconv_forward(const float* coords, const void* feats, pvconv_dtyp
         cin = L->cout;
     }
     st = L->devox == PVCONV_DEVOX_NEAREST
-             ? pv_launch_devoxelize_nearest(src, B, R, L->cout, bf, w.ids, N, w.devox, s)
-             : pv_launch_devoxelize(src, B, R, L->cout, bf, w.pnorm, N, w.devox, s);
+             ? pv_launch_devoxelize_nearest(src, B, R, L->cout, bf, ids, N, w.devox, s)
+             : pv_launch_devoxelize(src, B, R, L->cout, bf, pnorm, N, w.devox, s);
     if (st != PVCONV_OK) return st;
     return pv_launch_point_mlp(feats, feat_dt == PVCONV_BF16, feat_ld, B * N, L->cin, L->cout,
                                L->mlp_w, bf, pv_make_fold(&L->mlp_bn, L->mlp_b), PVCONV_ACT_RELU,

@@ -94,6 +94,11 @@ pvconv_status pv_launch_voxelize(const float* coords, const void* feats, bool fe
                                  int feat_ld, int B, int N, int C, int R, void* grid,
                                  bool grid_bf16, int32_t* counts, int32_t* vox_id,
                                  float* norm_coords, void* ws, hipStream_t s);
+// the same with the voxel indices given (no normalisation)
+pvconv_status pv_launch_voxelize_from_ids(const int32_t* ids, const void* feats, bool feat_bf16,
+                                          int feat_ld, int B, int N, int C, int R, void* grid,
+                                          bool grid_bf16, int32_t* counts, void* ws,
+                                          hipStream_t s);
 size_t pv_conv3d_ws_bytes(int Cin, int Cout, bool bf16);
 // bf16 conv weights [Cout][27][Cin] repacked into the MFMA fragment order
 // (into a workspace of pv_conv3d_ws_bytes), the convolutions of a layer in one

@@ -416,6 +416,40 @@ __global__ __launch_bounds__(kNormThreads) void pv_norm_points_kernel(
         if (thist[t]) atomicAdd(&ws.tcount[(size_t)b * ws.T + t], thist[t]);
 }
 
+// Given voxel indices: the tile counters and the heavy-voxel queue of large
+// clouds start at zero (workgroup 0 of the first launch, for B > 0; the other
+// workgroups zero the grid when the tile kernel writes only occupied rows),
+// then points per tile, LDS first, one global add per tile (second launch,
+// grid (G, B)). Indices outside the grid are dropped here and in the bucket
+// scatter alike.
+__global__ __launch_bounds__(kNormThreads) void pv_tile_reset_kernel(SplitWs ws, int B,
+                                                                     uint4* grid16, size_t n16) {
+    if (blockIdx.x > 0) {
+        zero_fill_role(grid16, n16, blockIdx.x - 1, gridDim.x - 1);
+        return;
+    }
+    if (B == 0) return;  // small clouds: nothing is bucketed, only the grid is zeroed
+    for (int i = threadIdx.x; i < 2 * B * ws.T; i += kNormThreads)
+        (i < B * ws.T ? ws.tcount : ws.tcursor)[i % (B * ws.T)] = 0;
+    if (threadIdx.x == 0 && ws.hq) ws.hq[0] = 0;
+}
+
+__global__ __launch_bounds__(kNormThreads) void pv_tile_count_kernel(
+    const int32_t* __restrict__ ids, int N, SplitWs ws) {
+    extern __shared__ int thist[];  // [T]
+    const int g = blockIdx.x, b = blockIdx.y;
+    for (int t = threadIdx.x; t < ws.T; t += kNormThreads) thist[t] = 0;
+    lds_barrier();
+    const int k0 = g * kNormPts, k1 = min(N, k0 + kNormPts);
+    for (int k = k0 + threadIdx.x; k < k1; k += kNormThreads) {
+        const int id = ids[(size_t)b * N + k];
+        if (id >= 0 && id / ws.TV < ws.T) atomicAdd(&thist[id / ws.TV], 1);
+    }
+    lds_barrier();
+    for (int t = threadIdx.x; t < ws.T; t += kNormThreads)
+        if (thist[t]) atomicAdd(&ws.tcount[(size_t)b * ws.T + t], thist[t]);
+}
+
 // Scatter of each point into its tile's bucket: grid (G, B), the same slices
 // as pv_norm_points_kernel. Each workgroup takes the exclusive prefix of the
 // cloud's tile counts, ranks its points per tile in LDS, reserves a range of
@@ -453,8 +487,11 @@ __global__ __launch_bounds__(kNormThreads) void pv_bucket_kernel(const int32_t* 
         tile[i] = -1;
         if (k < N) {
             vid[i] = ids[(size_t)b * N + k];
-            tile[i] = vid[i] / ws.TV;
-            rank[i] = atomicAdd(&hist[tile[i]], 1);
+            // an index outside the grid (given indices: invalid input) is dropped
+            if (vid[i] >= 0 && vid[i] / ws.TV < ws.T) {
+                tile[i] = vid[i] / ws.TV;
+                rank[i] = atomicAdd(&hist[tile[i]], 1);
+            }
         }
     }
     lds_barrier();
@@ -711,16 +748,16 @@ __device__ void tile_fill_range(const TileLds& L, int lo, int hi, int base, cons
                 }
             }
         }
-        // Items go in batches of IB per thread: the first point of every item
-        // of a batch is loaded at once (most occupied voxels hold one or two
-        // points), then the zero rows go out (side()), then each item adds
+        // Items go in batches of IB per thread: the first two points of every
+        // item of a batch are loaded at once (most occupied voxels hold one or
+        // two points), then the zero rows go out (side()), then each item adds
         // its remaining points. One counter tracks loads and stores in issue
         // order, so loads issued after side()'s stores would wait for them.
-        constexpr int IB = 4;
+        constexpr int IB = 2;
         const int nocc = s_nocc, nitems = nocc * gpv;
         bool sided = false;
         for (int i0 = threadIdx.x; i0 < nitems; i0 += IB * NT) {
-            float f0[IB][8];
+            float f0[IB][8], f1[IB][8];
             int vis[IB], cgs[IB], nks[IB], j0s[IB];
 #pragma unroll
             for (int q = 0; q < IB; q++) {
@@ -732,6 +769,8 @@ __device__ void tile_fill_range(const TileLds& L, int lo, int hi, int base, cons
                     nks[q] = L.hist[vis[q]];
                     j0s[q] = L.start[vis[q]] - base;
                     load8f<FT>(fb + (size_t)L.list[j0s[q]] * feat_ld + cgs[q] * 8, f0[q]);
+                    if (nks[q] > 1)
+                        load8f<FT>(fb + (size_t)L.list[j0s[q] + 1] * feat_ld + cgs[q] * 8, f1[q]);
                 }
             }
             if (!sided) {
@@ -744,7 +783,11 @@ __device__ void tile_fill_range(const TileLds& L, int lo, int hi, int base, cons
                 double acc[8];
 #pragma unroll
                 for (int i = 0; i < 8; i++) acc[i] = (double)f0[q][i];
-                sum8<FT, 4>(fb, feat_ld, cgs[q] * 8, L.list, j0s[q] + 1, j0s[q] + nks[q], 1, acc);
+                if (nks[q] > 1)
+#pragma unroll
+                    for (int i = 0; i < 8; i++) acc[i] += (double)f1[q][i];
+                sum8<FT, 4>(fb, feat_ld, cgs[q] * 8, L.list, j0s[q] + 2, j0s[q] + nks[q], 1, acc);
+
                 float mean[8];
 #pragma unroll
                 for (int i = 0; i < 8; i++) mean[i] = (float)(acc[i] / (double)nks[q]);
@@ -1275,60 +1318,46 @@ size_t pv_voxelize_ws_bytes(int B, int N, int R) {
     return bytes;
 }
 
-pvconv_status pv_launch_voxelize(const float* coords, const void* feats, bool feat_bf16,
-                                 int feat_ld, int B, int N, int C, int R, void* grid,
-                                 bool grid_bf16, int32_t* counts, int32_t* vox_id,
-                                 float* norm_coords, void* ws, hipStream_t s) {
-    if (B == 0) return PVCONV_OK;
-    VoxWs w = carve_ws(ws, B, N, R, nullptr);
-    int32_t* ids = vox_id ? vox_id : w.ids;
-    float* pn = norm_coords ? norm_coords : w.pnorm;
-    // Rows of empty voxels are zero. With 16-byte rows the tile kernel writes
-    // them itself (each grid row is then written exactly once); otherwise the
-    // grid is zeroed first, alongside the normalisation, and the tile kernel
-    // overwrites the occupied rows.
+namespace {
+
+// How a voxelisation call writes the grid: 16-byte rows (vec: the tile kernel
+// writes every row, zero rows for empty voxels) or not (the grid is zeroed
+// first, by zb workgroups of the first launch, or element by element when
+// 16-byte stores cannot cover it).
+struct GridPlan {
+    bool vec, grid_ok;
+    size_t gbytes, n16;
+    int zb;
+};
+
+GridPlan grid_plan(const void* feats, bool feat_bf16, int feat_ld, int B, int C, int R,
+                   const void* grid, bool grid_bf16) {
+    GridPlan g;
     const size_t esz_f = feat_bf16 ? 2 : 4, esz_g = grid_bf16 ? 2 : 4;
-    const bool vec = (C % 8 == 0) && pv_aligned16(feats) && pv_aligned16(grid) &&
-                     ((size_t)feat_ld * esz_f) % 16 == 0 && ((size_t)C * esz_g) % 16 == 0;
-    const size_t gbytes = (size_t)B * R * R * R * C * esz_g;
-    const size_t n16 = gbytes / 16;
-    const bool grid_ok = pv_aligned16(grid) && gbytes % 16 == 0;
-    const int zb = (grid_ok && !vec) ? (int)std::min<size_t>(2048, (n16 + 4095) / 4096) : 0;
-    uint4* grid16 = (uint4*)grid;
-    if (N <= kSmallMaxN) {
-        const int slices = (N + 255) / 256;
-        const int nid = slices * B;
-        if (nid + zb > 0) {
-            const dim3 gi(nid + zb);
-            if (N <= 1024)
-                hipLaunchKernelGGL(pv_voxel_ids_kernel<4>, gi, dim3(256), 0, s, coords, N, R,
-                                   slices, nid, ids, pn, grid16, n16);
-            else if (N <= 2048)
-                hipLaunchKernelGGL(pv_voxel_ids_kernel<8>, gi, dim3(256), 0, s, coords, N, R,
-                                   slices, nid, ids, pn, grid16, n16);
-            else
-                hipLaunchKernelGGL(pv_voxel_ids_kernel<16>, gi, dim3(256), 0, s, coords, N, R,
-                                   slices, nid, ids, pn, grid16, n16);
-        }
-    } else {
-        const int nid = w.split.G * B;
-        dim3 g(w.split.G, B);
-        hipLaunchKernelGGL(pv_norm_absmax_kernel, dim3(nid + zb), dim3(kNormThreads), 0, s,
-                           coords, N, w.split, B, grid16, n16);
-        hipLaunchKernelGGL(pv_norm_sum_kernel, g, dim3(kNormThreads), 0, s, coords, N, w.split);
-        hipLaunchKernelGGL(pv_norm_radius_kernel, g, dim3(kNormThreads), 0, s, coords, N, w.split);
-        hipLaunchKernelGGL(pv_norm_points_kernel, g, dim3(kNormThreads),
-                           (size_t)w.split.T * sizeof(int), s, coords, N, R, w.split, ids, pn);
-        hipLaunchKernelGGL(pv_bucket_kernel, g, dim3(kNormThreads),
-                           (size_t)2 * w.split.T * sizeof(int), s, ids, N, w.split);
-    }
+    g.vec = (C % 8 == 0) && pv_aligned16(feats) && pv_aligned16(grid) &&
+            ((size_t)feat_ld * esz_f) % 16 == 0 && ((size_t)C * esz_g) % 16 == 0;
+    g.gbytes = (size_t)B * R * R * R * C * esz_g;
+    g.n16 = g.gbytes / 16;
+    g.grid_ok = pv_aligned16(grid) && g.gbytes % 16 == 0;
+    g.zb = (g.grid_ok && !g.vec) ? (int)std::min<size_t>(2048, (g.n16 + 4095) / 4096) : 0;
+    return g;
+}
+
+// Everything after the voxel indices (and, for large clouds, the tile
+// buckets) are known: the tile kernel, then the heavy-voxel kernels.
+pvconv_status voxelize_fill(const int32_t* ids, const void* feats, bool feat_bf16, int feat_ld,
+                            int B, int N, int C, int R, void* grid, bool grid_bf16,
+                            int32_t* counts, const VoxWs& w, const GridPlan& gp,
+                            hipStream_t s) {
+    const bool vec = gp.vec;
     const Buckets bu = N > kSmallMaxN
                            ? Buckets{w.split.bk, w.split.br, w.split.tcount, w.split.tstart,
                                      w.split.T, vec && C <= kHeavyMaxC ? w.split.hq : nullptr}
                            : Buckets{nullptr, nullptr, nullptr, nullptr, 0, nullptr};
-    if (!grid_ok) {
+    if (!gp.grid_ok) {
         // a grid that 16-byte stores cannot cover: the plain element kernel
-        hipLaunchKernelGGL(pv_zero_elems_kernel, dim3(1024), dim3(256), 0, s, (char*)grid, gbytes);
+        hipLaunchKernelGGL(pv_zero_elems_kernel, dim3(1024), dim3(256), 0, s, (char*)grid,
+                           gp.gbytes);
     }
     // heavy voxels queued by the tiles (large clouds, 16-byte rows)
     const int hgrid = std::min(256, w.split.hmax);
@@ -1364,4 +1393,80 @@ pvconv_status pv_launch_voxelize(const float* coords, const void* feats, bool fe
         if (grid_bf16) heavy(float{}, uint16_t{}); else heavy(float{}, float{});
     }
     return pv_launch_status();
+}
+
+}  // namespace
+
+pvconv_status pv_launch_voxelize(const float* coords, const void* feats, bool feat_bf16,
+                                 int feat_ld, int B, int N, int C, int R, void* grid,
+                                 bool grid_bf16, int32_t* counts, int32_t* vox_id,
+                                 float* norm_coords, void* ws, hipStream_t s) {
+    if (B == 0) return PVCONV_OK;
+    VoxWs w = carve_ws(ws, B, N, R, nullptr);
+    int32_t* ids = vox_id ? vox_id : w.ids;
+    float* pn = norm_coords ? norm_coords : w.pnorm;
+    // Rows of empty voxels are zero. With 16-byte rows the tile kernel writes
+    // them itself (each grid row is then written exactly once); otherwise the
+    // grid is zeroed first, alongside the normalisation, and the tile kernel
+    // overwrites the occupied rows.
+    const GridPlan gp = grid_plan(feats, feat_bf16, feat_ld, B, C, R, grid, grid_bf16);
+    const int zb = gp.zb;
+    const size_t n16 = gp.n16;
+    uint4* grid16 = (uint4*)grid;
+    if (N <= kSmallMaxN) {
+        const int slices = (N + 255) / 256;
+        const int nid = slices * B;
+        if (nid + zb > 0) {
+            const dim3 gi(nid + zb);
+            if (N <= 1024)
+                hipLaunchKernelGGL(pv_voxel_ids_kernel<4>, gi, dim3(256), 0, s, coords, N, R,
+                                   slices, nid, ids, pn, grid16, n16);
+            else if (N <= 2048)
+                hipLaunchKernelGGL(pv_voxel_ids_kernel<8>, gi, dim3(256), 0, s, coords, N, R,
+                                   slices, nid, ids, pn, grid16, n16);
+            else
+                hipLaunchKernelGGL(pv_voxel_ids_kernel<16>, gi, dim3(256), 0, s, coords, N, R,
+                                   slices, nid, ids, pn, grid16, n16);
+        }
+    } else {
+        const int nid = w.split.G * B;
+        dim3 g(w.split.G, B);
+        hipLaunchKernelGGL(pv_norm_absmax_kernel, dim3(nid + zb), dim3(kNormThreads), 0, s,
+                           coords, N, w.split, B, grid16, n16);
+        hipLaunchKernelGGL(pv_norm_sum_kernel, g, dim3(kNormThreads), 0, s, coords, N, w.split);
+        hipLaunchKernelGGL(pv_norm_radius_kernel, g, dim3(kNormThreads), 0, s, coords, N, w.split);
+        hipLaunchKernelGGL(pv_norm_points_kernel, g, dim3(kNormThreads),
+                           (size_t)w.split.T * sizeof(int), s, coords, N, R, w.split, ids, pn);
+        hipLaunchKernelGGL(pv_bucket_kernel, g, dim3(kNormThreads),
+                           (size_t)2 * w.split.T * sizeof(int), s, ids, N, w.split);
+    }
+    return voxelize_fill(ids, feats, feat_bf16, feat_ld, B, N, C, R, grid, grid_bf16, counts, w,
+                         gp, s);
+}
+
+pvconv_status pv_launch_voxelize_from_ids(const int32_t* ids, const void* feats, bool feat_bf16,
+                                          int feat_ld, int B, int N, int C, int R, void* grid,
+                                          bool grid_bf16, int32_t* counts, void* ws,
+                                          hipStream_t s) {
+    if (B == 0) return PVCONV_OK;
+    VoxWs w = carve_ws(ws, B, N, R, nullptr);
+    const GridPlan gp = grid_plan(feats, feat_bf16, feat_ld, B, C, R, grid, grid_bf16);
+    uint4* grid16 = (uint4*)grid;
+    if (N <= kSmallMaxN) {
+        // the tiles scan the indices themselves; only a grid without 16-byte
+        // rows needs zeroing first
+        if (gp.zb > 0)
+            hipLaunchKernelGGL(pv_tile_reset_kernel, dim3(1 + gp.zb), dim3(kNormThreads), 0, s,
+                               w.split, 0, grid16, gp.n16);
+    } else {
+        dim3 g(w.split.G, B);
+        hipLaunchKernelGGL(pv_tile_reset_kernel, dim3(1 + gp.zb), dim3(kNormThreads), 0, s,
+                           w.split, B, grid16, gp.n16);
+        hipLaunchKernelGGL(pv_tile_count_kernel, g, dim3(kNormThreads),
+                           (size_t)w.split.T * sizeof(int), s, ids, N, w.split);
+        hipLaunchKernelGGL(pv_bucket_kernel, g, dim3(kNormThreads),
+                           (size_t)2 * w.split.T * sizeof(int), s, ids, N, w.split);
+    }
+    return voxelize_fill(ids, feats, feat_bf16, feat_ld, B, N, C, R, grid, grid_bf16, counts, w,
+                         gp, s);
 }

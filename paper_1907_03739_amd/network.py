@@ -7,7 +7,10 @@ binding; this module only lays out device buffers and orders the calls.
 
 Forward, for B clouds of N points:
   * the PVConv blocks, each feeding the next (Sections 4.1-4.3), then the
-    point-only shared MLPs (Linear + BN + ReLU);
+    point-only shared MLPs (Linear + BN + ReLU). Every block normalises the
+    same coordinates, so the voxel indices are computed once per resolution:
+    a block whose R an earlier block of the same forward used takes that
+    block's indices and normalised coordinates (pvconv_forward_ex);
   * every stage writes its per-point output straight into its column range of
     one [B][N][C_stages] bf16 buffer, so the concatenation the head reads costs
     no copy;
@@ -87,16 +90,35 @@ class DeviceNetwork:
         self.logits = torch.empty((B, N, self.n_classes), **f32)
         ws = max(pv.pvconv_forward_workspace_size(B, N, L) for L in self.blocks)
         self.workspace = torch.empty(max(ws, 256), dtype=torch.uint8, device=device)
+        # voxel indices per resolution, and the normalised coordinates
+        self.ids = {R: torch.empty((B, N), dtype=torch.int32, device=device)
+                    for R in {L.R for L in layers}}
+        self.norm = torch.empty((B, N, 3), **f32)
 
     def stage_view(self, i: int) -> torch.Tensor:
         o, w = self.offsets[i], self.widths[i]
         return self.cat[:, :, o:o + w]
 
     # -- the steps, callable one by one (the tests feed each from the oracle) --
-    def run_block(self, i: int, coords: torch.Tensor, feats: torch.Tensor) -> torch.Tensor:
+    def run_block(self, i: int, coords: torch.Tensor, feats: torch.Tensor,
+                  reuse_ids: bool = False) -> torch.Tensor:
+        """Block i. reuse_ids: take the voxel indices and normalised
+        coordinates an earlier block at the same R wrote for these coords."""
         out = self.stage_view(i)
-        pv.pvconv_forward(coords, feats, self.blocks[i], out=out, workspace=self.workspace)
+        pv.pvconv_forward(coords, feats, self.blocks[i], out=out, workspace=self.workspace,
+                          vox_id=self.ids[self.blocks[i].params.R], norm=self.norm,
+                          ids_given=reuse_ids)
         return out
+
+    def _run_blocks(self, coords, x, marks=None):
+        seen = set()
+        for i, blk in enumerate(self.blocks):
+            if marks:
+                marks(f"pvconv{i + 1}")
+            R = blk.params.R
+            x = self.run_block(i, coords, x, reuse_ids=R in seen)
+            seen.add(R)
+        return x
 
     def run_mlp(self, j: int, x: torch.Tensor) -> torch.Tensor:
         m = self.mlps[j]
@@ -125,9 +147,7 @@ class DeviceNetwork:
     def forward(self, coords: torch.Tensor, feats: torch.Tensor) -> torch.Tensor:
         """coords [B][N][3] f32, feats [B][N][C_in] (f32 or bf16) -> logits
         [B][N][n_classes] f32 (a view of a buffer reused by the next call)."""
-        x = feats
-        for i in range(len(self.blocks)):
-            x = self.run_block(i, coords, x)
+        x = self._run_blocks(coords, feats)
         for j in range(len(self.mlps)):
             x = self.run_mlp(j, x)
         self.run_global(x)
@@ -141,10 +161,7 @@ class DeviceNetwork:
     def forward_timed(self, coords, feats, marks: Callable[[Optional[str]], None]):
         """forward() with marks(name) called before each step and marks(None)
         after the last; used to place timing events between the steps."""
-        x = feats
-        for i in range(len(self.blocks)):
-            marks(f"pvconv{i + 1}")
-            x = self.run_block(i, coords, x)
+        x = self._run_blocks(coords, feats, marks)
         for j in range(len(self.mlps)):
             marks(f"mlp{j + 1}")
             x = self.run_mlp(j, x)

@@ -29,7 +29,7 @@ def declared_functions():
 
 def test_library_exports_every_declared_symbol():
     names = declared_functions()
-    assert len(names) == 11
+    assert len(names) == 13
     out = subprocess.run(["nm", "-D", "--defined-only", b.LIB_PATH], capture_output=True,
                          text=True, check=True).stdout
     exported = set(re.findall(r"\bT (pvconv_\w+)", out))
@@ -148,6 +148,26 @@ def test_devoxelize_nearest_rejects(kw, status):
     assert _devox_nn(**kw) == status
 
 
+def _vfi(**kw):
+    a = dict(ids=FAKE, feats=FAKE, fdt=0, ld=0, B=2, N=100, C=16, R=8, grid=FAKE, gdt=1,
+             counts=FAKE, ws=ctypes.c_void_p(0x400000), wsb=1 << 40, s=None)
+    a.update(kw)
+    return L.pvconv_voxelize_from_ids(a["ids"], a["feats"], a["fdt"], a["ld"], a["B"], a["N"],
+                                      a["C"], a["R"], a["grid"], a["gdt"], a["counts"], a["ws"],
+                                      a["wsb"], a["s"])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(B=-1), EINVAL), (dict(N=-1), EINVAL), (dict(C=0), EINVAL), (dict(R=0), EINVAL),
+    (dict(R=129), EINVAL), (dict(fdt=7), EINVAL), (dict(gdt=7), EINVAL), (dict(ld=8), EINVAL),
+    (dict(ids=None), EINVAL), (dict(feats=None), EINVAL), (dict(grid=None), EINVAL),
+    (dict(counts=None), EINVAL), (dict(ids=FAKE_ODD), EINVAL), (dict(ws=None), EWS),
+    (dict(wsb=16), EWS), (dict(ws=ctypes.c_void_p(0x400010)), EWS), (dict(B=0), OK),
+])
+def test_voxelize_from_ids_rejects(kw, status):
+    assert _vfi(**kw) == status
+
+
 def _mlp(**kw):
     a = dict(x=FAKE, x_dt=0, x_ld=0, M=100, Cin=64, Cout=128, w=FAKE, dt=1, bias=None, bn=None,
              act=1, slope=0.0, cb=None, ppc=1, res=None, res_ld=0, out=ctypes.c_void_p(0x200000),
@@ -200,6 +220,27 @@ def _fwd(lay, **kw):
     return L.pvconv_forward(a["coords"], a["feats"], a["fdt"], a["fld"], a["B"], a["N"],
                             ctypes.byref(lay), a["out"], a["odt"], a["old"], a["ws"], a["wsb"],
                             a["s"])
+
+
+def _fwd_ex(lay, **kw):
+    a = dict(coords=FAKE, feats=FAKE, fdt=0, fld=0, B=2, N=100, ids=FAKE, norm=FAKE, given=1,
+             out=FAKE, odt=0, old=0, ws=FAKE, wsb=1 << 40, s=None)
+    a.update(kw)
+    return L.pvconv_forward_ex(a["coords"], a["feats"], a["fdt"], a["fld"], a["B"], a["N"],
+                               ctypes.byref(lay), a["ids"], a["norm"], a["given"], a["out"],
+                               a["odt"], a["old"], a["ws"], a["wsb"], a["s"])
+
+
+def test_forward_ex_rejects():
+    lay = _layer()
+    assert _fwd_ex(lay, given=2) == EINVAL
+    assert _fwd_ex(lay, given=-1) == EINVAL
+    assert _fwd_ex(lay, ids=None) == EINVAL           # given indices missing
+    assert _fwd_ex(lay, norm=None) == EINVAL
+    assert _fwd_ex(lay, given=0, coords=None) == EINVAL
+    assert _fwd_ex(lay, ids=FAKE_ODD) == EINVAL
+    assert _fwd_ex(lay, ws=None) == EWS
+    assert _fwd_ex(lay, B=0) == OK
 
 
 def test_forward_rejects():

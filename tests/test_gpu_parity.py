@@ -84,6 +84,60 @@ def test_voxelize_matches_oracle(case):
         assert_bf16_step(host(g), grid, "voxel grid bf16")
 
 
+@pytest.mark.parametrize("wl_idx,B,N,R,C,gdt", [
+    (2, 4, 2048, 32, 64, "bf16"),    # small clouds, 16-byte rows
+    (2, 2, 2048, 16, 20, "f32"),     # small clouds, grid zeroed first
+    (5, 1, 65536, 64, 64, "bf16"),   # large cloud: tile counts and buckets from the indices
+    (5, 1, 65536, 32, 20, "f32"),    # large cloud, grid zeroed first
+])
+def test_voxelize_from_given_ids(wl_idx, B, N, R, C, gdt):
+    # Eq. 2 with the indices of an earlier call (the cross-layer reuse of the
+    # normalisation): the same grid and counts, over a grid left dirty
+    coords, feats = _cloud(wl_idx, B, N, C, seed=7)
+    gt = torch.bfloat16 if gdt == "bf16" else torch.float32
+    pn, ids, grid, counts = _oracle_vox(coords, feats, R)
+    ids_d = torch.as_tensor(ids, dtype=torch.int32).cuda()
+    g0 = torch.full((B, R ** 3, C), float("nan"), dtype=gt, device="cuda")
+    c0 = torch.full((B, R ** 3), -7, dtype=torch.int32, device="cuda")
+    g, c = pv.pvconv_voxelize_from_ids(ids_d, dev(feats), R, grid_dtype=gt, grid=g0, counts=c0)
+    assert np.array_equal(c.cpu().numpy(), counts)
+    if gdt == "f32":
+        assert_rel(host(g), grid, 1e-5, "voxel grid fp32, given ids")
+    else:
+        assert_bf16_step(host(g), grid, "voxel grid bf16, given ids")
+    # indices outside the grid drop their points (invalid input, memory-safe)
+    bad = ids.copy()
+    bad[:, ::97] = -1
+    bad[:, 1::89] = R ** 3 + 5
+    keep = (bad >= 0) & (bad < R ** 3)
+    gk, ck = pv.pvconv_voxelize_from_ids(torch.as_tensor(bad, dtype=torch.int32).cuda(),
+                                         dev(feats), R, grid_dtype=gt)
+    for b in range(B):
+        gb, cb = oracle.voxelize(ids[b:b + 1, keep[b]], feats[b:b + 1, keep[b]], R)
+        assert np.array_equal(ck.cpu().numpy()[b], cb[0])
+        if gdt == "f32":
+            assert_rel(host(gk)[b], gb[0], 1e-5, "dropped indices")
+        else:
+            assert_bf16_step(host(gk)[b], gb[0], "dropped indices")
+
+
+def test_forward_reusing_the_indices_of_an_earlier_layer():
+    wl = synth.make_workload(2, B=2)
+    L = wl.layers[0]
+    layer = pv.DeviceLayer(L, "cuda", torch.bfloat16)
+    coords, feats = dev(wl.coords), dev(wl.feats)
+    ids = torch.empty((2, wl.N), dtype=torch.int32, device="cuda")
+    norm = torch.empty((2, wl.N, 3), dtype=torch.float32, device="cuda")
+    first = host(pv.pvconv_forward(coords, feats, layer, vox_id=ids, norm=norm))
+    _, _, pn = oracle.normalize(wl.coords)
+    assert np.array_equal(ids.cpu().numpy(), oracle.voxel_ids(pn, L.R))
+    assert np.array_equal(norm.cpu().numpy(), pn.astype(np.float32))
+    again = host(pv.pvconv_forward(None, feats, layer, vox_id=ids, norm=norm, ids_given=True))
+    np.testing.assert_allclose(again, first, rtol=1e-6, atol=1e-6)
+    ref = oracle.pvconv_forward(wl.coords, wl.feats, L)
+    assert_bf16_chain(again, ref, "layer from given indices")
+
+
 def test_voxelize_strided_features_and_optional_outputs():
     coords, wide = _cloud(2, 2, 2048, 96)
     feats = wide[:, :, 16:80]
