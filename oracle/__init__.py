@@ -58,6 +58,11 @@ def _load():
         "ref_devoxelize": [_P, _I64, ctypes.c_int, _I64, _P, _I64, _P],
         "ref_devoxelize_weights": [_P, _I64, ctypes.c_int, _P, _P],
         "ref_devoxelize_nearest": [_P, _I64, ctypes.c_int, _I64, _P, _I64, _P],
+        "ref_voxelize_backward": [_P, _P, _P, _I64, _I64, _I64, ctypes.c_int, _P],
+        "ref_devoxelize_backward": [_P, _P, _I64, _I64, _I64, ctypes.c_int, _P],
+        "ref_devoxelize_nearest_backward": [_P, _P, _I64, _I64, _I64, ctypes.c_int, _P],
+        "ref_conv3d_backward_data": [_P, _I64, ctypes.c_int, _I64, _I64, _P, _P],
+        "ref_conv3d_backward_weight": [_P, _P, _I64, ctypes.c_int, _I64, _I64, _P],
         "ref_linear": [_P, _I64, _I64, _I64, _P, _P, _P],
         "ref_maxpool": [_P, _I64, _I64, _I64, _P],
     }
@@ -214,6 +219,92 @@ def devoxelize_weights(pnorm: np.ndarray, R: int):
            "devoxelize_weights")
     shape = pnorm.shape[:-1] + (8,)
     return cells.reshape(shape), wts.reshape(shape)
+
+
+# ----------------------------------------------------------------------------
+# backward: gradients of the steps with respect to their inputs (and of the
+# convolution with respect to its weights), the adjoints of the forward maps
+# ----------------------------------------------------------------------------
+def voxelize_backward(dgrid: np.ndarray, ids: np.ndarray, counts: np.ndarray,
+                      R: int) -> np.ndarray:
+    """dL/dV [B][R^3][C] -> dL/df [B][N][C] (Eq. 2's average, transposed)."""
+    lib = _load()
+    dgrid = _f64(dgrid)
+    ids = np.ascontiguousarray(ids, dtype=np.int32)
+    counts = np.ascontiguousarray(counts, dtype=np.int32)
+    B, V, C = dgrid.shape
+    N = ids.shape[1]
+    out = np.empty((B, N, C))
+    _check(lib.ref_voxelize_backward(_ptr(dgrid), _ptr(ids), _ptr(counts), B, N, C, R,
+                                     _ptr(out)), "voxelize_backward")
+    return out
+
+
+def devoxelize_backward(dout: np.ndarray, R: int, pnorm: np.ndarray) -> np.ndarray:
+    """dL/dout [B][N][C] -> dL/dV [B][R^3][C] (trilinear weights, transposed)."""
+    lib = _load()
+    dout = _f64(dout)
+    pnorm = _f64(pnorm)
+    B, N, C = dout.shape
+    out = np.empty((B, R ** 3, C))
+    _check(lib.ref_devoxelize_backward(_ptr(dout), _ptr(pnorm), B, N, C, R, _ptr(out)),
+           "devoxelize_backward")
+    return out
+
+
+def devoxelize_nearest_backward(dout: np.ndarray, R: int, ids: np.ndarray) -> np.ndarray:
+    """dL/dout [B][N][C] -> dL/dV [B][R^3][C] (each point's gradient to its cell)."""
+    lib = _load()
+    dout = _f64(dout)
+    ids = np.ascontiguousarray(ids, dtype=np.int32)
+    B, N, C = dout.shape
+    out = np.empty((B, R ** 3, C))
+    _check(lib.ref_devoxelize_nearest_backward(_ptr(dout), _ptr(ids), B, N, C, R, _ptr(out)),
+           "devoxelize_nearest_backward")
+    return out
+
+
+def conv3d_backward_data(dy: np.ndarray, w: np.ndarray, R: int) -> np.ndarray:
+    """dL/dy [B][R^3][Cout], w [Cout][3][3][3][Cin] -> dL/dx [B][R^3][Cin]."""
+    lib = _load()
+    dy = _f64(dy)
+    w = _f64(w)
+    B, V, Cout = dy.shape
+    Cin = w.shape[-1]
+    out = np.empty((B, V, Cin))
+    _check(lib.ref_conv3d_backward_data(_ptr(dy), B, R, Cin, Cout, _ptr(w), _ptr(out)),
+           "conv3d_backward_data")
+    return out
+
+
+def conv3d_backward_weight(dy: np.ndarray, x: np.ndarray, R: int) -> np.ndarray:
+    """dL/dy [B][R^3][Cout], x [B][R^3][Cin] -> dL/dW [Cout][3][3][3][Cin]."""
+    lib = _load()
+    dy = _f64(dy)
+    x = _f64(x)
+    B, V, Cout = dy.shape
+    Cin = x.shape[-1]
+    out = np.empty((Cout, 3, 3, 3, Cin))
+    _check(lib.ref_conv3d_backward_weight(_ptr(dy), _ptr(x), B, R, Cin, Cout, _ptr(out)),
+           "conv3d_backward_weight")
+    return out
+
+
+def act_bn_backward(dy: np.ndarray, y: np.ndarray, bn, act: str, slope: float = 0.1):
+    """y = act(BN(z)) per channel: dL/dz = dL/dy * act'(y) * gamma / sqrt(var + eps).
+    The rectifiers' derivative is read from the sign of y (equal to that of
+    BN(z) for a positive slope): 1 where y > 0, slope (leaky) or 0 (relu)
+    elsewhere. bn None: identity."""
+    dy = _f64(dy)
+    y = _f64(y)
+    if act == "leaky":
+        d = np.where(y > 0, 1.0, slope)
+    elif act == "relu":
+        d = np.where(y > 0, 1.0, 0.0)
+    else:
+        d = np.ones_like(y)
+    scale = 1.0 if bn is None else (_f64(bn.gamma) / np.sqrt(_f64(bn.var) + bn.eps))
+    return dy * d * scale
 
 
 def linear(x: np.ndarray, w: np.ndarray, bias: Optional[np.ndarray] = None) -> np.ndarray:

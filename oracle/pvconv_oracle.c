@@ -24,6 +24,12 @@
  *                      mapping the section sets against trilinear (the
  *                      devoxelisation row of the ablation table)
  *   ref_linear         Section 4.2 "Point-Based Feature Transformation"
+ *   ref_*_backward     gradients of the above with respect to their inputs
+ *                      (and of the convolution with respect to its weights):
+ *                      the layer is differentiable end to end (Section 4.1
+ *                      "Devoxelization" relies on it for trilinear vs
+ *                      nearest); each is the adjoint of the linear map the
+ *                      forward step applies
  *   ref_maxpool        Section 5.1 "Models" (PointNet backbone global feature)
  * Fusion by addition (Section 4.3) and the composition of the steps live in
  * oracle/__init__.py.
@@ -364,6 +370,139 @@ int ref_maxpool(const double* x, int64_t B, int64_t N, int64_t C, double* out) {
                 if (v > m) m = v;
             }
             out[b * C + c] = m;
+        }
+    return PV_ORACLE_OK;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Backward pass: gradients of the steps above. Each forward step is linear  */
+/* in the input it is differentiated by, so each gradient is the adjoint     */
+/* (transpose) of that linear map, written out from its definition.          */
+/* ------------------------------------------------------------------------- */
+
+/* Eq. 2 averages the features of the points in each voxel, so
+ * dL/df[b][k][c] = dL/dV[b][id_k][c] / N[b][id_k].
+ * dgrid [B][R^3][C], ids [B][N], counts [B][R^3] -> dfeats [B][N][C]. */
+int ref_voxelize_backward(const double* dgrid, const int32_t* ids, const int32_t* counts,
+                          int64_t B, int64_t N, int64_t C, int R, double* dfeats) {
+    if (R < 1) return PV_ORACLE_EINVAL;
+    int64_t V = (int64_t)R * R * R;
+    for (int64_t b = 0; b < B; b++)
+        for (int64_t k = 0; k < N; k++) {
+            int64_t id = ids[b * N + k];
+            if (id < 0 || id >= V || counts[b * V + id] < 1) return PV_ORACLE_EINVAL;
+            double n = (double)counts[b * V + id];
+            for (int64_t c = 0; c < C; c++)
+                dfeats[(b * N + k) * C + c] = dgrid[(b * V + id) * C + c] / n;
+        }
+    return PV_ORACLE_OK;
+}
+
+/* Trilinear devoxelisation: out_k = sum over its 8 cells of w(k, cell) V[cell],
+ * so dL/dV[cell] = sum over the points k of w(k, cell) dL/dout_k.
+ * dout [B][N][C], pnorm [B][N][3] -> dgrid [B][R^3][C]. */
+int ref_devoxelize_backward(const double* dout, const double* pnorm, int64_t B, int64_t N,
+                            int64_t C, int R, double* dgrid) {
+    if (R < 1) return PV_ORACLE_EINVAL;
+    int64_t V = (int64_t)R * R * R;
+    memset(dgrid, 0, sizeof(double) * (size_t)(B * V * C));
+    for (int64_t b = 0; b < B; b++)
+        for (int64_t k = 0; k < N; k++) {
+            const double* p = pnorm + (b * N + k) * 3;
+            int64_t iu[2], iv[2], iw[2];
+            double wu[2], wv[2], ww[2];
+            trilinear_axis(p[0], R, &iu[0], &iu[1], &wu[0], &wu[1]);
+            trilinear_axis(p[1], R, &iv[0], &iv[1], &wv[0], &wv[1]);
+            trilinear_axis(p[2], R, &iw[0], &iw[1], &ww[0], &ww[1]);
+            const double* g = dout + (b * N + k) * C;
+            for (int a = 0; a < 2; a++)
+                for (int e = 0; e < 2; e++)
+                    for (int f = 0; f < 2; f++) {
+                        double wt = (wu[a] * wv[e]) * ww[f];
+                        double* cell = dgrid + (b * V + (iu[a] * R + iv[e]) * R + iw[f]) * C;
+                        for (int64_t c = 0; c < C; c++) cell[c] += wt * g[c];
+                    }
+        }
+    return PV_ORACLE_OK;
+}
+
+/* Nearest-neighbour devoxelisation copies V[id_k] to point k, so
+ * dL/dV[cell] = sum of dL/dout_k over the points k with id_k = cell. */
+int ref_devoxelize_nearest_backward(const double* dout, const int32_t* ids, int64_t B,
+                                    int64_t N, int64_t C, int R, double* dgrid) {
+    if (R < 1) return PV_ORACLE_EINVAL;
+    int64_t V = (int64_t)R * R * R;
+    for (int64_t k = 0; k < B * N; k++)
+        if (ids[k] < 0 || ids[k] >= V) return PV_ORACLE_EINVAL;
+    memset(dgrid, 0, sizeof(double) * (size_t)(B * V * C));
+    for (int64_t b = 0; b < B; b++)
+        for (int64_t k = 0; k < N; k++) {
+            double* cell = dgrid + (b * V + ids[b * N + k]) * C;
+            const double* g = dout + (b * N + k) * C;
+            for (int64_t c = 0; c < C; c++) cell[c] += g[c];
+        }
+    return PV_ORACLE_OK;
+}
+
+/* Convolution, gradient with respect to its input. Output voxel p reads
+ * input voxel p + d through W[o][d][i], so
+ * dL/dx[b][q][i] = sum over offsets d and output channels o of
+ *                  W[o][d][i] * dL/dy[b][q - d][o], for q - d inside the grid.
+ * dy [B][R^3][Cout], w [Cout][27][Cin] -> dx [B][R^3][Cin]. */
+int ref_conv3d_backward_data(const double* dy, int64_t B, int R, int64_t Cin, int64_t Cout,
+                             const double* w, double* dx) {
+    if (B < 0 || R < 1 || Cin < 1 || Cout < 1) return PV_ORACLE_EINVAL;
+    int64_t V = (int64_t)R * R * R;
+#pragma omp parallel for collapse(2) schedule(dynamic)
+    for (int64_t b = 0; b < B; b++)
+        for (int64_t u = 0; u < R; u++)
+            for (int64_t v = 0; v < R; v++)
+                for (int64_t ww = 0; ww < R; ww++) {
+                    double* out = dx + (b * V + (u * R + v) * R + ww) * Cin;
+                    for (int64_t i = 0; i < Cin; i++) out[i] = 0.0;
+                    for (int du = -1; du <= 1; du++)
+                        for (int dv = -1; dv <= 1; dv++)
+                            for (int dw = -1; dw <= 1; dw++) {
+                                int64_t pu = u - du, pv = v - dv, pw = ww - dw;
+                                if (pu < 0 || pu >= R || pv < 0 || pv >= R || pw < 0 || pw >= R)
+                                    continue;
+                                int tap = ((du + 1) * 3 + (dv + 1)) * 3 + (dw + 1);
+                                const double* g = dy + (b * V + (pu * R + pv) * R + pw) * Cout;
+                                for (int64_t o = 0; o < Cout; o++) {
+                                    const double* wk = w + (o * 27 + tap) * Cin;
+                                    for (int64_t i = 0; i < Cin; i++) out[i] += wk[i] * g[o];
+                                }
+                            }
+                }
+    return PV_ORACLE_OK;
+}
+
+/* Convolution, gradient with respect to its weights:
+ * dL/dW[o][d][i] = sum over clouds b and output voxels p of
+ *                  dL/dy[b][p][o] * x[b][p + d][i], for p + d inside the grid.
+ * dy [B][R^3][Cout], x [B][R^3][Cin] -> dw [Cout][27][Cin]. */
+int ref_conv3d_backward_weight(const double* dy, const double* x, int64_t B, int R, int64_t Cin,
+                               int64_t Cout, double* dw) {
+    if (B < 0 || R < 1 || Cin < 1 || Cout < 1) return PV_ORACLE_EINVAL;
+    int64_t V = (int64_t)R * R * R;
+#pragma omp parallel for collapse(2) schedule(dynamic)
+    for (int64_t o = 0; o < Cout; o++)
+        for (int tap = 0; tap < 27; tap++) {
+            int du = tap / 9 - 1, dv = (tap / 3) % 3 - 1, dw_ = tap % 3 - 1;
+            double* out = dw + (o * 27 + tap) * Cin;
+            for (int64_t i = 0; i < Cin; i++) out[i] = 0.0;
+            for (int64_t b = 0; b < B; b++)
+                for (int64_t u = 0; u < R; u++)
+                    for (int64_t v = 0; v < R; v++)
+                        for (int64_t ww = 0; ww < R; ww++) {
+                            int64_t nu = u + du, nv = v + dv, nw = ww + dw_;
+                            if (nu < 0 || nu >= R || nv < 0 || nv >= R || nw < 0 || nw >= R)
+                                continue;
+                            double g = dy[(b * V + (u * R + v) * R + ww) * Cout + o];
+                            if (g == 0.0) continue;
+                            const double* xin = x + (b * V + (nu * R + nv) * R + nw) * Cin;
+                            for (int64_t i = 0; i < Cin; i++) out[i] += g * xin[i];
+                        }
         }
     return PV_ORACLE_OK;
 }

@@ -429,6 +429,101 @@ def test_layer_with_nearest_devox_differs_only_in_the_voxel_branch_mapping():
 
 
 # ----------------------------------------------------------------------------
+# Backward: each gradient is pinned by the adjoint identity <dy, f(x)> =
+# <f*(dy), x> of its (linear) forward step, by finite differences, or by torch
+# autograd on the CPU in fp64
+# ----------------------------------------------------------------------------
+def _dot(a, b):
+    return float(np.sum(np.asarray(a, np.float64) * np.asarray(b, np.float64)))
+
+
+def test_voxelize_backward_is_the_adjoint_of_the_average():
+    wl = synth.make_workload(2, B=2, N=500)
+    rng = _rng(40)
+    R, C = 8, 3
+    _, _, pn = oracle.normalize(wl.coords)
+    ids = oracle.voxel_ids(pn, R)
+    f = rng.normal(size=(2, 500, C))
+    grid, counts = oracle.voxelize(ids, f, R)
+    dV = rng.normal(size=grid.shape)
+    df = oracle.voxelize_backward(dV, ids, counts, R)
+    assert abs(_dot(dV, grid) - _dot(df, f)) <= 1e-11 * (abs(_dot(dV, grid)) + 1)
+    # finite difference in one feature (the map is linear: exact up to rounding)
+    for (b, k, c) in [(0, 0, 0), (1, 37, 2), (0, 499, 1)]:
+        e = np.zeros_like(f)
+        e[b, k, c] = 1.0
+        g1, _ = oracle.voxelize(ids, f + e, R)
+        np.testing.assert_allclose(_dot(dV, g1) - _dot(dV, grid), df[b, k, c], rtol=1e-9,
+                                   atol=1e-12)
+
+
+def test_devoxelize_backward_is_the_adjoint_trilinear_and_nearest():
+    rng = _rng(41)
+    B, N, C = 2, 300, 4
+    for R in (1, 5, 8):
+        pn = rng.uniform(-0.02, 1.02, size=(B, N, 3))
+        G = rng.normal(size=(B, R ** 3, C))
+        dout = rng.normal(size=(B, N, C))
+        dG = oracle.devoxelize_backward(dout, R, pn)
+        lhs = _dot(dout, oracle.devoxelize(G, R, pn))
+        assert abs(lhs - _dot(dG, G)) <= 1e-11 * (abs(lhs) + 1)
+        ids = rng.integers(0, R ** 3, size=(B, N)).astype(np.int32)
+        dGn = oracle.devoxelize_nearest_backward(dout, R, ids)
+        lhs = _dot(dout, oracle.devoxelize_nearest(G, R, ids))
+        assert abs(lhs - _dot(dGn, G)) <= 1e-11 * (abs(lhs) + 1)
+        # every point hands each of its cells its trilinear weight: the
+        # gradient of an all-ones output sums to N per cloud
+        np.testing.assert_allclose(oracle.devoxelize_backward(np.ones((B, N, 1)), R, pn)
+                                   .sum(axis=(1, 2)), N, rtol=1e-12)
+
+
+@pytest.mark.parametrize("R,Cin,Cout,B", [(1, 2, 3, 1), (3, 3, 2, 2), (5, 4, 3, 1)])
+def test_conv_backward_matches_torch_autograd_fp64(R, Cin, Cout, B):
+    rng = _rng(42 + R)
+    x = rng.normal(size=(B, R ** 3, Cin))
+    w = rng.normal(size=(Cout, 3, 3, 3, Cin))
+    dy = rng.normal(size=(B, R ** 3, Cout))
+    xt = torch.tensor(x.reshape(B, R, R, R, Cin)).permute(0, 4, 1, 2, 3).requires_grad_(True)
+    wt = torch.tensor(w).permute(0, 4, 1, 2, 3).contiguous().requires_grad_(True)
+    yt = torch.nn.functional.conv3d(xt, wt, padding=1)
+    dyt = torch.tensor(dy.reshape(B, R, R, R, Cout)).permute(0, 4, 1, 2, 3)
+    yt.backward(dyt)
+    dx_ref = xt.grad.permute(0, 2, 3, 4, 1).reshape(B, R ** 3, Cin).numpy()
+    dw_ref = wt.grad.permute(0, 2, 3, 4, 1).numpy()
+    np.testing.assert_allclose(oracle.conv3d_backward_data(dy, w, R), dx_ref, rtol=1e-12,
+                               atol=1e-12)
+    np.testing.assert_allclose(oracle.conv3d_backward_weight(dy, x, R), dw_ref, rtol=1e-12,
+                               atol=1e-12)
+
+
+def test_conv_backward_is_the_adjoint_at_a_realistic_shape():
+    rng = _rng(43)
+    R, Cin, Cout = 6, 5, 7
+    x = rng.normal(size=(2, R ** 3, Cin)) * (rng.random((2, R ** 3, 1)) < 0.3)
+    w = rng.normal(size=(Cout, 3, 3, 3, Cin))
+    dy = rng.normal(size=(2, R ** 3, Cout))
+    y = oracle.conv3d(x, w, R)
+    lhs = _dot(dy, y)
+    assert abs(lhs - _dot(oracle.conv3d_backward_data(dy, w, R), x)) <= 1e-10 * (abs(lhs) + 1)
+    assert abs(lhs - _dot(oracle.conv3d_backward_weight(dy, x, R), w)) <= 1e-10 * (abs(lhs) + 1)
+
+
+def test_act_bn_backward_matches_finite_differences():
+    rng = _rng(44)
+    bn = synth.draw_bn(rng, 6)
+    z = rng.normal(size=(50, 6)) * 2
+    dy = rng.normal(size=(50, 6))
+    h = 1e-6
+    for act, fwd in [("leaky", lambda t: oracle.leaky_relu(oracle.batchnorm(t, bn), 0.1)),
+                     ("relu", lambda t: oracle.relu(oracle.batchnorm(t, bn))),
+                     ("none", lambda t: oracle.batchnorm(t, bn))]:
+        y = fwd(z)
+        dz = oracle.act_bn_backward(dy, y, bn, act, 0.1)
+        fd = (fwd(z + h) - fwd(z - h)) / (2 * h) * dy   # elementwise: one step per entry
+        np.testing.assert_allclose(dz, fd, rtol=1e-6, atol=1e-8)
+
+
+# ----------------------------------------------------------------------------
 # Point branch, fusion, max-pool (Sections 4.2, 4.3, 5.1)
 # ----------------------------------------------------------------------------
 def test_linear_matches_numpy_matmul():
