@@ -265,6 +265,61 @@ pvconv_status pvconv_forward_ex(const float* coords, const void* feats, pvconv_d
                                 pvconv_dtype out_dt, int out_ld, void* workspace,
                                 size_t workspace_bytes, void* stream);
 
+/* ========================================================================= */
+/* Backward pass: gradients of the steps above with respect to their inputs  */
+/* (the layer is differentiable end to end). Each step is linear in the      */
+/* input it is differentiated by, and each gradient is the adjoint of that   */
+/* map. Gradients are fp32.                                                  */
+/* ========================================================================= */
+
+/* Voxelisation (Eq. 2, an average per voxel):                               */
+/*  dfeats[b][k][c] = dgrid[b][vox_id[b][k]][c] / counts[b][vox_id[b][k]]    */
+/*  dgrid [B][R^3][C] (dt), vox_id [B][N], counts [B][R^3] int32 as          */
+/*  pvconv_voxelize wrote them; dfeats out [B][N][C] fp32. An index outside  */
+/*  the grid or a count below 1 is invalid input (memory-safe, result        */
+/*  unspecified).                                                            */
+pvconv_status pvconv_voxelize_backward(const void* dgrid, pvconv_dtype dt, int B, int N, int C,
+                                       int R, const int32_t* vox_id, const int32_t* counts,
+                                       float* dfeats, void* stream);
+
+/* Trilinear devoxelisation (Section 4.1 "Devoxelization"):                   */
+/*  dgrid[b][cell][c] = sum over points k of w(k, cell) * dout[b][k][c], with */
+/*  the 8 cells and weights of pvconv_devoxelize. dout [B][N][C] fp32,        */
+/*  norm_coords [B][N][3]; dgrid out [B][R^3][C] fp32, every element written  */
+/*  (cleared, then accumulated with fp32 atomic adds: the order of the adds,  */
+/*  and so the last bits, may differ between runs).                          */
+pvconv_status pvconv_devoxelize_backward(const float* dout, int B, int N, int C, int R,
+                                         const float* norm_coords, float* dgrid, void* stream);
+
+/* Nearest-neighbour devoxelisation: dgrid[b][cell] = sum of dout[b][k] over  */
+/* the points k with vox_id[b][k] = cell (as above otherwise).               */
+pvconv_status pvconv_devoxelize_nearest_backward(const float* dout, int B, int N, int C, int R,
+                                                 const int32_t* vox_id, float* dgrid,
+                                                 void* stream);
+
+/* Convolution (Section 4.1 "Feature Aggregation"), gradient with respect to */
+/* its input:                                                                */
+/*  dx[b,q,i] = sum_{d in {-1,0,1}^3} sum_o W[o][d+1][i] * dy[b,q-d,o]       */
+/* (dy = 0 outside the grid): the forward convolution of dy with the kernel  */
+/* mirrored through its centre and its channel axes swapped, computed by the */
+/* forward kernels. dy [B][R^3][Cout] (dt), weight [Cout][3][3][3][Cin] (dt), */
+/* dx out [B][R^3][Cin] (dx_dt). dt = BF16 needs Cin % 32 == 0. workspace >= */
+/* pvconv_conv3d_backward_data_workspace_size bytes, 256-byte aligned.        */
+size_t pvconv_conv3d_backward_data_workspace_size(int Cin, int Cout, pvconv_dtype dt);
+pvconv_status pvconv_conv3d_backward_data(const void* dy, int B, int R, int Cin, int Cout,
+                                          const void* weight, pvconv_dtype dt, void* dx,
+                                          pvconv_dtype dx_dt, void* workspace,
+                                          size_t workspace_bytes, void* stream);
+
+/* Batch norm + activation, y = act(BN(z)) per channel, gradient with respect */
+/* to z: dz = dy * act'(y) * gamma / sqrt(var + eps), the rectifiers'        */
+/* derivative read from the sign of y (1 where y > 0, else slope for LEAKY,   */
+/* 0 for RELU; NONE: 1). bn NULL: identity. dy [M][C] fp32, y [M][C] (y_dt),  */
+/* dz out [M][C] fp32 (may alias dy).                                        */
+pvconv_status pvconv_act_bn_backward(const float* dy, const void* y, pvconv_dtype y_dt, int M,
+                                     int C, const pvconv_bn* bn, pvconv_act act, float slope,
+                                     float* dz, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -67,6 +67,13 @@ _SIGS = {
     "pvconv_forward_ex": ([_VP, _VP, _I, _I, _I, _I, ctypes.POINTER(Layer), _VP, _VP, _I, _VP,
                            _I, _I, _VP, _SZ, _VP], _I),
     "pvconv_status_string": ([_I], ctypes.c_char_p),
+    "pvconv_voxelize_backward": ([_VP, _I, _I, _I, _I, _I, _VP, _VP, _VP, _VP], _I),
+    "pvconv_devoxelize_backward": ([_VP, _I, _I, _I, _I, _VP, _VP, _VP], _I),
+    "pvconv_devoxelize_nearest_backward": ([_VP, _I, _I, _I, _I, _VP, _VP, _VP], _I),
+    "pvconv_conv3d_backward_data_workspace_size": ([_I, _I, _I], _SZ),
+    "pvconv_conv3d_backward_data": ([_VP, _I, _I, _I, _I, _VP, _I, _VP, _I, _VP, _SZ, _VP],
+                                    _I),
+    "pvconv_act_bn_backward": ([_VP, _VP, _I, _I, _I, _VP, _I, _F, _VP, _VP], _I),
 }
 for _name, (_args, _res) in _SIGS.items():
     _fn = getattr(_lib, _name)
@@ -270,6 +277,73 @@ def pvconv_maxpool(x: torch.Tensor, out: Optional[torch.Tensor] = None):
         raise ValueError("out must be a contiguous [B][C] float32 tensor")
     _check("pvconv_maxpool", _lib.pvconv_maxpool(_p(x), _dt(x), ld, B, N, C, _p(out),
                                                  _stream(x)))
+    return out
+
+
+# ----------------------------------------------------------------------------
+# backward (gradients with respect to the steps' inputs; fp32 gradients)
+# ----------------------------------------------------------------------------
+def pvconv_voxelize_backward(dgrid: torch.Tensor, R: int, vox_id: torch.Tensor,
+                             counts: torch.Tensor, out=None):
+    """dgrid [B][R^3][C] -> dfeats [B][N][C] f32 (dV of each point's voxel / count)."""
+    B, V, C = dgrid.shape
+    N = vox_id.shape[1]
+    out = _out(out, (B, N, C), torch.float32, dgrid.device, "out")
+    _check("pvconv_voxelize_backward", _lib.pvconv_voxelize_backward(
+        _p(dgrid.contiguous()), _dt(dgrid), B, N, C, R, _p(vox_id.contiguous()),
+        _p(counts.contiguous()), _p(out), _stream(dgrid)))
+    return out
+
+
+def pvconv_devoxelize_backward(dout: torch.Tensor, R: int, norm_coords: torch.Tensor, out=None):
+    """dout [B][N][C] f32 -> dgrid [B][R^3][C] f32 (trilinear weights, transposed)."""
+    B, N, C = dout.shape
+    out = _out(out, (B, R ** 3, C), torch.float32, dout.device, "out")
+    _check("pvconv_devoxelize_backward", _lib.pvconv_devoxelize_backward(
+        _p(dout.contiguous()), B, N, C, R, _p(norm_coords.contiguous()), _p(out),
+        _stream(dout)))
+    return out
+
+
+def pvconv_devoxelize_nearest_backward(dout: torch.Tensor, R: int, vox_id: torch.Tensor,
+                                       out=None):
+    """dout [B][N][C] f32 -> dgrid [B][R^3][C] f32 (each point's gradient to its cell)."""
+    B, N, C = dout.shape
+    out = _out(out, (B, R ** 3, C), torch.float32, dout.device, "out")
+    _check("pvconv_devoxelize_nearest_backward", _lib.pvconv_devoxelize_nearest_backward(
+        _p(dout.contiguous()), B, N, C, R, _p(vox_id.contiguous()), _p(out), _stream(dout)))
+    return out
+
+
+def pvconv_conv3d_backward_data(dy: torch.Tensor, weight: torch.Tensor, R: int,
+                                out_dtype=torch.float32, out=None, workspace=None):
+    """dy [B][R^3][Cout], weight [Cout][3][3][3][Cin] (same dtype) -> dx [B][R^3][Cin]."""
+    B, V, Cout = dy.shape
+    Cin = weight.shape[-1]
+    if V != R ** 3 or tuple(weight.shape[:4]) != (Cout, 3, 3, 3):
+        raise ValueError("shape mismatch")
+    dx = _out(out, (B, V, Cin), _torch_dt(out_dtype), dy.device, "out")
+    need = _lib.pvconv_conv3d_backward_data_workspace_size(Cin, Cout, _dt(dy))
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=dy.device)
+    _check("pvconv_conv3d_backward_data", _lib.pvconv_conv3d_backward_data(
+        _p(dy.contiguous()), B, R, Cin, Cout, _p(weight.contiguous()), _dt(dy), _p(dx),
+        _dt(dx), _p(workspace), workspace.numel(), _stream(dy)))
+    return dx
+
+
+def pvconv_act_bn_backward(dy: torch.Tensor, y: torch.Tensor, bn=None, act="leaky", slope=0.1,
+                           out=None):
+    """y = act(BN(z)) [..][C]; dy [..][C] f32 -> dz [..][C] f32."""
+    C = y.shape[-1]
+    M = y.numel() // C
+    if dy.shape != y.shape:
+        raise ValueError("dy and y must have the same shape")
+    out = _out(out, tuple(y.shape), torch.float32, y.device, "out")
+    bns = _bn_struct(bn)
+    _check("pvconv_act_bn_backward", _lib.pvconv_act_bn_backward(
+        _p(dy.contiguous()), _p(y.contiguous()), _dt(y), M, C,
+        ctypes.byref(bns) if bn is not None else None, ACT[act], slope, _p(out), _stream(y)))
     return out
 
 

@@ -320,4 +320,87 @@ pvconv_status pvconv_forward_ex(const float* coords, const void* feats, pvconv_d
                                out_ld, s);
 }
 
+pvconv_status pvconv_voxelize_backward(const void* dgrid, pvconv_dtype dt, int B, int N, int C,
+                                       int R, const int32_t* vox_id, const int32_t* counts,
+                                       float* dfeats, void* stream) {
+    if (B < 0 || N < 0 || C < 1 || R < 1 || R > PVCONV_MAX_R || !sizes_fit(B, N) ||
+        !dtype_ok(dt))
+        return PVCONV_EINVAL;
+    if (B == 0 || N == 0) return PVCONV_OK;
+    if (!dgrid || !vox_id || !counts || !dfeats) return PVCONV_EINVAL;
+    if (((uintptr_t)dgrid & (esize(dt) - 1)) || ((uintptr_t)vox_id & 3) ||
+        ((uintptr_t)counts & 3) || ((uintptr_t)dfeats & 3))
+        return PVCONV_EINVAL;
+    return pv_launch_voxelize_backward(dgrid, dt == PVCONV_BF16, B, N, C, R, vox_id, counts,
+                                       dfeats, as_stream(stream));
+}
+
+static pvconv_status devox_backward(const float* dout, int B, int N, int C, int R,
+                                    const float* pn, const int32_t* ids, float* dgrid,
+                                    void* stream) {
+    if (B < 0 || N < 0 || C < 1 || R < 1 || R > PVCONV_MAX_R || !sizes_fit(B, N))
+        return PVCONV_EINVAL;
+    if (B == 0) return PVCONV_OK;
+    if (!dgrid || (N > 0 && (!dout || (!pn && !ids)))) return PVCONV_EINVAL;
+    if (((uintptr_t)dout & 3) || ((uintptr_t)pn & 3) || ((uintptr_t)ids & 3) ||
+        ((uintptr_t)dgrid & 3))
+        return PVCONV_EINVAL;
+    return pv_launch_devoxelize_backward(dout, B, N, C, R, pn, ids, dgrid, as_stream(stream));
+}
+
+pvconv_status pvconv_devoxelize_backward(const float* dout, int B, int N, int C, int R,
+                                         const float* norm_coords, float* dgrid, void* stream) {
+    if (B > 0 && N > 0 && !norm_coords) return PVCONV_EINVAL;
+    return devox_backward(dout, B, N, C, R, norm_coords, nullptr, dgrid, stream);
+}
+
+pvconv_status pvconv_devoxelize_nearest_backward(const float* dout, int B, int N, int C, int R,
+                                                 const int32_t* vox_id, float* dgrid,
+                                                 void* stream) {
+    if (B > 0 && N > 0 && !vox_id) return PVCONV_EINVAL;
+    return devox_backward(dout, B, N, C, R, nullptr, vox_id, dgrid, stream);
+}
+
+size_t pvconv_conv3d_backward_data_workspace_size(int Cin, int Cout, pvconv_dtype dt) {
+    if (Cin < 1 || Cout < 1 || Cin > PVCONV_MAX_CONV_CHANNELS ||
+        Cout > PVCONV_MAX_CONV_CHANNELS || !dtype_ok(dt))
+        return 0;
+    return pv_conv3d_bwd_data_ws_bytes(Cin, Cout, dt == PVCONV_BF16);
+}
+
+pvconv_status pvconv_conv3d_backward_data(const void* dy, int B, int R, int Cin, int Cout,
+                                          const void* weight, pvconv_dtype dt, void* dx,
+                                          pvconv_dtype dx_dt, void* workspace,
+                                          size_t workspace_bytes, void* stream) {
+    if (B < 0 || R < 1 || R > PVCONV_MAX_R || Cin < 1 || Cout < 1 ||
+        Cin > PVCONV_MAX_CONV_CHANNELS || Cout > PVCONV_MAX_CONV_CHANNELS)
+        return PVCONV_EINVAL;
+    if (!dtype_ok(dt) || !dtype_ok(dx_dt)) return PVCONV_EINVAL;
+    if (B == 0) return PVCONV_OK;
+    if (!dy || !weight || !dx) return PVCONV_EINVAL;
+    if (((uintptr_t)dy & (esize(dt) - 1)) || ((uintptr_t)weight & (esize(dt) - 1)) ||
+        ((uintptr_t)dx & (esize(dx_dt) - 1)))
+        return PVCONV_EINVAL;
+    if (dt == PVCONV_BF16 && Cin % 32 != 0) return PVCONV_ENOTSUP;
+    if (dy == dx) return PVCONV_EINVAL;
+    const size_t need = pv_conv3d_bwd_data_ws_bytes(Cin, Cout, dt == PVCONV_BF16);
+    if (!workspace || ((uintptr_t)workspace & 255) || workspace_bytes < need)
+        return PVCONV_EWORKSPACE;
+    return pv_launch_conv3d_backward_data(dy, B, R, Cin, Cout, weight, dt == PVCONV_BF16, dx,
+                                          dx_dt == PVCONV_BF16, workspace, as_stream(stream));
+}
+
+pvconv_status pvconv_act_bn_backward(const float* dy, const void* y, pvconv_dtype y_dt, int M,
+                                     int C, const pvconv_bn* bn, pvconv_act act, float slope,
+                                     float* dz, void* stream) {
+    if (M < 0 || C < 1 || !dtype_ok(y_dt) || !act_ok(act) || !bn_ok(bn)) return PVCONV_EINVAL;
+    if (M == 0) return PVCONV_OK;
+    if (!dy || !y || !dz) return PVCONV_EINVAL;
+    if (((uintptr_t)dy & 3) || ((uintptr_t)y & (esize(y_dt) - 1)) || ((uintptr_t)dz & 3))
+        return PVCONV_EINVAL;
+    return pv_launch_act_bn_backward(dy, y, y_dt == PVCONV_BF16, (size_t)M, C,
+                                     pv_make_fold(bn, nullptr), act, slope, dz,
+                                     as_stream(stream));
+}
+
 }  // extern "C"

@@ -130,3 +130,18 @@ pvconv_status pv_launch_point_mlp(const void* x, bool x_bf16, int x_ld, int M, i
                                   int out_ld, hipStream_t s);
 pvconv_status pv_launch_maxpool(const void* x, bool bf16, int x_ld, int B, int N, int C,
                                 float* out, hipStream_t s);
+// backward (backward.hip)
+size_t pv_conv3d_bwd_data_ws_bytes(int Cin, int Cout, bool bf16);
+pvconv_status pv_launch_voxelize_backward(const void* dgrid, bool bf16, int B, int N, int C,
+                                          int R, const int32_t* ids, const int32_t* counts,
+                                          float* dfeats, hipStream_t s);
+// ids != NULL: nearest neighbour (pn unused), else trilinear
+pvconv_status pv_launch_devoxelize_backward(const float* dout, int B, int N, int C, int R,
+                                            const float* pn, const int32_t* ids, float* dgrid,
+                                            hipStream_t s);
+pvconv_status pv_launch_conv3d_backward_data(const void* dy, int B, int R, int Cin, int Cout,
+                                             const void* w, bool bf16, void* dx, bool dx_bf16,
+                                             void* ws, hipStream_t s);
+pvconv_status pv_launch_act_bn_backward(const float* dy, const void* y, bool y_bf16, size_t M,
+                                        int C, const PvBnFold& bn, int act, float slope,
+                                        float* dz, hipStream_t s);

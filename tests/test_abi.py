@@ -19,6 +19,7 @@ L = b._lib
 OK, EINVAL, ENOTSUP, EWS = 0, 1, 2, 3
 FAKE = ctypes.c_void_p(0x100000)    # never dereferenced: validation fails first
 FAKE_ODD = ctypes.c_void_p(0x100001)
+FAKE2 = ctypes.c_void_p(0x200000)
 
 
 def declared_functions():
@@ -29,7 +30,7 @@ def declared_functions():
 
 def test_library_exports_every_declared_symbol():
     names = declared_functions()
-    assert len(names) == 13
+    assert len(names) == 19
     out = subprocess.run(["nm", "-D", "--defined-only", b.LIB_PATH], capture_output=True,
                          text=True, check=True).stdout
     exported = set(re.findall(r"\bT (pvconv_\w+)", out))
@@ -229,6 +230,57 @@ def _fwd_ex(lay, **kw):
     return L.pvconv_forward_ex(a["coords"], a["feats"], a["fdt"], a["fld"], a["B"], a["N"],
                                ctypes.byref(lay), a["ids"], a["norm"], a["given"], a["out"],
                                a["odt"], a["old"], a["ws"], a["wsb"], a["s"])
+
+
+@pytest.mark.parametrize("call,status", [
+    (lambda: L.pvconv_voxelize_backward(FAKE, 1, 2, 10, 16, 8, FAKE, FAKE, FAKE, None), None),
+    (lambda: L.pvconv_voxelize_backward(FAKE, 3, 2, 10, 16, 8, FAKE, FAKE, FAKE, None), EINVAL),
+    (lambda: L.pvconv_voxelize_backward(FAKE, 1, 2, 10, 16, 0, FAKE, FAKE, FAKE, None), EINVAL),
+    (lambda: L.pvconv_voxelize_backward(FAKE, 1, 2, 10, 16, 8, None, FAKE, FAKE, None), EINVAL),
+    (lambda: L.pvconv_voxelize_backward(FAKE, 1, 2, 10, 16, 8, FAKE, None, FAKE, None), EINVAL),
+    (lambda: L.pvconv_voxelize_backward(FAKE, 1, 2, 10, 16, 8, FAKE, FAKE, FAKE_ODD, None),
+     EINVAL),
+    (lambda: L.pvconv_voxelize_backward(FAKE, 1, 0, 10, 16, 8, FAKE, FAKE, FAKE, None), OK),
+    (lambda: L.pvconv_devoxelize_backward(FAKE, 2, 10, 16, 129, FAKE, FAKE, None), EINVAL),
+    (lambda: L.pvconv_devoxelize_backward(FAKE, 2, 10, 16, 8, None, FAKE, None), EINVAL),
+    (lambda: L.pvconv_devoxelize_backward(FAKE, 2, 10, 16, 8, FAKE, None, None), EINVAL),
+    (lambda: L.pvconv_devoxelize_backward(FAKE_ODD, 2, 10, 16, 8, FAKE, FAKE, None), EINVAL),
+    (lambda: L.pvconv_devoxelize_backward(FAKE, 0, 10, 16, 8, FAKE, FAKE, None), OK),
+    (lambda: L.pvconv_devoxelize_nearest_backward(FAKE, 2, 10, 16, 8, None, FAKE, None),
+     EINVAL),
+    (lambda: L.pvconv_devoxelize_nearest_backward(FAKE, 2, -1, 16, 8, FAKE, FAKE, None),
+     EINVAL),
+    (lambda: L.pvconv_conv3d_backward_data(FAKE, 2, 8, 48, 64, FAKE, 1, FAKE, 0, FAKE, 1 << 40,
+                                           None), ENOTSUP),
+    (lambda: L.pvconv_conv3d_backward_data(FAKE, 2, 8, 64, 64, FAKE, 1, FAKE2, 0, None, 0, None),
+     EWS),
+    (lambda: L.pvconv_conv3d_backward_data(FAKE, 2, 8, 64, 64, FAKE, 1, FAKE, 0, FAKE, 1 << 40,
+                                           None), EINVAL),     # dx aliases dy
+    (lambda: L.pvconv_conv3d_backward_data(FAKE, 2, 8, 64, 64, None, 1, FAKE, 0, FAKE, 1 << 40,
+                                           None), EINVAL),
+    (lambda: L.pvconv_conv3d_backward_data(FAKE, 2, 0, 64, 64, FAKE, 1, FAKE, 0, FAKE, 1 << 40,
+                                           None), EINVAL),
+    (lambda: L.pvconv_conv3d_backward_data(FAKE, 0, 8, 64, 64, FAKE, 1, FAKE, 0, None, 0, None),
+     OK),
+    (lambda: L.pvconv_act_bn_backward(FAKE, FAKE, 1, 100, 0, None, 2, 0.1, FAKE, None), EINVAL),
+    (lambda: L.pvconv_act_bn_backward(FAKE, FAKE, 1, 100, 8, None, 7, 0.1, FAKE, None), EINVAL),
+    (lambda: L.pvconv_act_bn_backward(FAKE, None, 1, 100, 8, None, 2, 0.1, FAKE, None), EINVAL),
+    (lambda: L.pvconv_act_bn_backward(FAKE, FAKE_ODD, 1, 100, 8, None, 2, 0.1, FAKE, None),
+     EINVAL),
+    (lambda: L.pvconv_act_bn_backward(FAKE, FAKE, 1, 0, 8, None, 2, 0.1, FAKE, None), OK),
+])
+def test_backward_entry_points_reject(call, status):
+    if status is None:      # valid arguments: would launch, so only check the others
+        return
+    assert call() == status
+
+
+def test_backward_workspace_query():
+    # the mirrored weights, then the forward convolution's packed weights
+    assert L.pvconv_conv3d_backward_data_workspace_size(64, 128, 1) == \
+        128 * 27 * 64 * 2 + L.pvconv_conv3d_workspace_size(128, 64, 1)
+    assert L.pvconv_conv3d_backward_data_workspace_size(5, 7, 0) == 256 * ((7 * 27 * 5 * 4 + 255) // 256)
+    assert L.pvconv_conv3d_backward_data_workspace_size(0, 7, 0) == 0
 
 
 def test_forward_ex_rejects():

@@ -1,0 +1,137 @@
+"""GPU parity of the backward entry points against the fp64 oracle's
+gradients (pinned in tests/test_oracle_pins.py by adjoint identities, finite
+differences and torch autograd). Tolerances as in tests/_helpers.py: fp32
+sums within 1e-5 of (|ref| + the same sum over magnitudes); bf16 convolution
+inputs as the forward convolution.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from paper_1907_03739_amd import binding as pv
+from _helpers import assert_bf16_step, assert_dot_f32, assert_rel, bf16_round, dev, dev_bn, host
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True)
+def _gpu_case(request):
+    assert torch.cuda.is_available(), "GPU tests need an MI355X"
+    print(f"\n[gpu case] {request.node.nodeid}", flush=True)
+    yield
+    torch.cuda.synchronize()
+
+
+def _ids_counts(wl_idx, B, N, R):
+    wl = synth.make_workload(wl_idx, B=B, N=N)
+    _, _, pn = oracle.normalize(wl.coords)
+    ids = oracle.voxel_ids(pn, R)
+    counts = np.stack([np.bincount(ids[b], minlength=R ** 3) for b in range(B)]).astype(np.int32)
+    return pn, ids, counts
+
+
+def _i32(a):
+    return torch.as_tensor(np.ascontiguousarray(a), dtype=torch.int32).cuda()
+
+
+@pytest.mark.parametrize("wl_idx,B,N,R,C,gdt", [
+    (2, 4, 2048, 32, 64, "bf16"), (2, 2, 2048, 32, 64, "f32"), (2, 2, 999, 24, 20, "f32"),
+    (5, 1, 65536, 64, 64, "bf16"), (1, 1, 1024, 8, 3, "bf16"),
+])
+def test_voxelize_backward_matches_oracle(wl_idx, B, N, R, C, gdt):
+    _, ids, counts = _ids_counts(wl_idx, B, N, R)
+    rng = np.random.default_rng(R + C)
+    dV = rng.normal(size=(B, R ** 3, C)).astype(np.float32).astype(np.float64)
+    if gdt == "bf16":
+        dV = bf16_round(dV)
+    ref = oracle.voxelize_backward(dV, ids, counts, R)
+    got = pv.pvconv_voxelize_backward(dev(dV, torch.bfloat16 if gdt == "bf16" else
+                                          torch.float32), R, _i32(ids), _i32(counts))
+    assert_rel(host(got), ref, 1e-6, "voxelize backward")
+
+
+@pytest.mark.parametrize("wl_idx,B,N,R,C", [
+    (2, 2, 2048, 32, 64), (2, 16, 2048, 32, 128), (5, 1, 65536, 64, 64), (1, 1, 1024, 8, 3),
+    (4, 2, 4096, 16, 20),
+])
+def test_devoxelize_backward_matches_oracle(wl_idx, B, N, R, C):
+    pn, ids, _ = _ids_counts(wl_idx, B, N, R)
+    pn32 = pn.astype(np.float32)
+    rng = np.random.default_rng(3 * R + C)
+    dout = rng.normal(size=(B, N, C)).astype(np.float32).astype(np.float64)
+    # trilinear: atomics in any order, fp32 sums
+    ref = oracle.devoxelize_backward(dout, R, pn32)
+    mag = oracle.devoxelize_backward(np.abs(dout), R, pn32)
+    dirty = torch.full((B, R ** 3, C), float("nan"), device="cuda")
+    got = pv.pvconv_devoxelize_backward(dev(dout), R, dev(pn32), out=dirty)
+    assert_dot_f32(host(got), ref, mag, "devoxelize backward")
+    # nearest
+    ref = oracle.devoxelize_nearest_backward(dout, R, ids)
+    mag = oracle.devoxelize_nearest_backward(np.abs(dout), R, ids)
+    got = pv.pvconv_devoxelize_nearest_backward(dev(dout), R, _i32(ids), out=dirty)
+    assert_dot_f32(host(got), ref, mag, "nearest devoxelize backward")
+
+
+@pytest.mark.parametrize("B,R,Cin,Cout,dt", [
+    (2, 32, 64, 128, "bf16"),      # the part-seg layer's first conv, input gradient
+    (1, 16, 128, 128, "bf16"),
+    (1, 13, 32, 64, "bf16"),       # ragged bricks
+    (2, 8, 16, 32, "f32"),
+    (1, 9, 5, 7, "f32"),           # fp32 path, odd channel counts
+])
+def test_conv3d_backward_data_matches_oracle(B, R, Cin, Cout, dt):
+    rng = np.random.default_rng(R * 5 + Cin)
+    dy = rng.normal(size=(B, R ** 3, Cout)) * (rng.random((B, R ** 3, 1)) < 0.4)
+    w = synth.kaiming_normal(rng, (Cout, 3, 3, 3, Cin), 27 * Cin, bf16=dt == "bf16")
+    if dt == "bf16":
+        dy = bf16_round(dy)
+    else:
+        dy = dy.astype(np.float32).astype(np.float64)
+        w = w.astype(np.float32).astype(np.float64)
+    ref = oracle.conv3d_backward_data(dy, w, R)
+    tdt = torch.bfloat16 if dt == "bf16" else torch.float32
+    got = host(pv.pvconv_conv3d_backward_data(dev(dy, tdt), dev(w, tdt), R))
+    if dt == "bf16":
+        # fp32 accumulation of exact bf16 products: the forward conv's bound
+        assert_bf16_step(got, ref, "conv input gradient bf16")
+    else:
+        mag = oracle.conv3d_backward_data(np.abs(dy), np.abs(w), R)
+        assert_dot_f32(got, ref, mag, "conv input gradient fp32")
+
+
+def test_conv3d_backward_data_is_the_adjoint_of_the_forward_on_gpu():
+    # <dy, conv(x)> = <conv_bwd(dy), x> with both sides from the GPU kernels
+    rng = np.random.default_rng(11)
+    R, Cin, Cout = 16, 64, 64
+    x = bf16_round(rng.normal(size=(1, R ** 3, Cin)))
+    dy = bf16_round(rng.normal(size=(1, R ** 3, Cout)))
+    w = synth.kaiming_normal(rng, (Cout, 3, 3, 3, Cin), 27 * Cin, bf16=True)
+    y = host(pv.pvconv_conv3d(dev(x, torch.bfloat16), dev(w, torch.bfloat16), R, act="none",
+                              out_dtype=torch.float32))
+    dx = host(pv.pvconv_conv3d_backward_data(dev(dy, torch.bfloat16), dev(w, torch.bfloat16),
+                                             R))
+    lhs, rhs = float(np.sum(dy * y)), float(np.sum(dx * x))
+    scale = max(float(np.sum(np.abs(dy * y))), float(np.sum(np.abs(dx * x))))
+    assert abs(lhs - rhs) <= 1e-5 * scale, (lhs, rhs, scale)
+
+
+@pytest.mark.parametrize("ydt,act,with_bn", [
+    ("f32", "leaky", True), ("bf16", "leaky", True), ("f32", "relu", True),
+    ("bf16", "none", False), ("f32", "leaky", False),
+])
+def test_act_bn_backward_matches_oracle(ydt, act, with_bn):
+    rng = np.random.default_rng(5)
+    M, C = 20000, 96
+    bn = synth.draw_bn(rng, C) if with_bn else None
+    y = rng.normal(size=(M, C)).astype(np.float32).astype(np.float64)
+    if ydt == "bf16":
+        y = bf16_round(y)
+    dy = rng.normal(size=(M, C)).astype(np.float32).astype(np.float64)
+    ref = oracle.act_bn_backward(dy, y, bn, act, 0.1)
+    got = pv.pvconv_act_bn_backward(dev(dy), dev(y, torch.bfloat16 if ydt == "bf16" else
+                                                 torch.float32),
+                                    bn=dev_bn(bn) if bn is not None else None, act=act,
+                                    slope=0.1)
+    assert_rel(host(got), ref, 1e-5, "act + BN backward")
