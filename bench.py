@@ -59,6 +59,9 @@ def parse():
                          "(R 16/24/32, one to three convolutions, channel widths, nearest-"
                          "neighbour devoxelisation) on the part-seg layer's clouds, one JSON "
                          "line each")
+    ap.add_argument("--backward", action="store_true",
+                    help="instead of the headline: the backward entry points (input "
+                         "gradients) at the part-seg layer's shapes, one JSON line each")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only copy a MIB-MiB buffer 3 times (a plain copy kernel of known "
                          "size, to calibrate the HBM byte counters) and exit")
@@ -399,6 +402,85 @@ def bench_variants(args, dev):
             "data": "synthetic"}), flush=True)
 
 
+def bench_backward(args, dev):
+    """Input gradients of the part-seg layer's steps, in reverse order, each
+    timed as the average of 10 back-to-back calls captured in a graph."""
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_1907_03739_amd import binding as pv
+
+    wl = synth.make_workload(2)
+    L = wl.layers[0]
+    B, N, R, cin, cout = wl.B, wl.N, L.R, L.cin, L.cout
+    V = R ** 3
+    stream = torch.cuda.current_stream(dev)
+    layer = pv.DeviceLayer(L, dev, torch.bfloat16)
+    coords = torch.as_tensor(wl.coords).to(dev)
+    feats = torch.as_tensor(wl.feats).to(dev)
+    grid, counts, ids, pn = pv.pvconv_voxelize(coords, feats, R, grid_dtype=torch.bfloat16)
+    gen = torch.Generator(device=dev).manual_seed(5)
+    dout = torch.randn((B, N, cout), device=dev, generator=gen)
+    dgrid = torch.empty((B, V, cout), dtype=torch.float32, device=dev)
+    y = torch.randn((B, V, cout), device=dev, generator=gen).to(torch.bfloat16)
+    dz = torch.empty((B, V, cout), dtype=torch.float32, device=dev)
+    dy16 = torch.randn((B, V, cout), device=dev, generator=gen).to(torch.bfloat16)
+    dx2 = torch.empty((B, V, cout), dtype=torch.bfloat16, device=dev)
+    dx1 = torch.empty((B, V, cin), dtype=torch.bfloat16, device=dev)
+    dvox = torch.randn((B, V, cin), device=dev, generator=gen).to(torch.bfloat16)
+    dfeats = torch.empty((B, N, cin), dtype=torch.float32, device=dev)
+    wsz = max(pv._lib.pvconv_conv3d_backward_data_workspace_size(c, cout, 1) for c in (cin, cout))
+    ws = torch.empty(wsz, dtype=torch.uint8, device=dev)
+    bn2 = layer.conv_bn[1]
+    s_g = 2
+    steps = [
+        # name, call, unit, algorithmic amount per call
+        ("devoxelize_backward", lambda: pv.pvconv_devoxelize_backward(dout, R, pn, out=dgrid),
+         "GB/s", B * N * (12 + 4 * cout) + B * V * cout * 4),
+        ("act_bn_backward", lambda: pv.pvconv_act_bn_backward(dgrid, y, bn=bn2, out=dz),
+         "GB/s", B * V * cout * (4 + s_g + 4)),
+        ("conv2_backward_data", lambda: pv.pvconv_conv3d_backward_data(
+            dy16, layer.conv_w[1], R, out_dtype=torch.bfloat16, out=dx2, workspace=ws),
+         "TFLOP/s", conv_flops(B, R, cout, cout)),
+        ("conv1_backward_data", lambda: pv.pvconv_conv3d_backward_data(
+            dy16, layer.conv_w[0], R, out_dtype=torch.bfloat16, out=dx1, workspace=ws),
+         "TFLOP/s", conv_flops(B, R, cin, cout)),
+        ("voxelize_backward", lambda: pv.pvconv_voxelize_backward(dvox, R, ids, counts,
+                                                                   out=dfeats),
+         "GB/s", B * N * (4 + 4 + 4 * cin) + int((counts > 0).sum().item()) * cin * s_g),
+    ]
+    REPS = 10
+    for name, fn, unit, amount in steps:
+        fn()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(REPS):
+                fn()
+        g.replay()
+        torch.cuda.synchronize()
+        times = []
+        for _ in range(max(3, args.steps // REPS)):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            g.replay()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            times.append(e0.elapsed_time(e1) / REPS)
+        del g
+        ms = statistics.median(times)
+        if unit == "GB/s":
+            rate, peak = amount / (ms * 1e-3) / 1e9, PEAK_HBM_GBS
+        else:
+            rate, peak = amount / (ms * 1e-3) / 1e12, PEAK_BF16_TFLOPS
+        print(json.dumps({"step": name, "workload": wl.name, "ms": round(ms, 4),
+                          "ms_min": round(min(times), 4), "achieved": round(rate, 2),
+                          "unit": unit, "peak": peak, "frac": round(rate / peak, 4),
+                          "algorithmic": amount, "dtype": "bf16 in, fp32 gradients",
+                          "data": "synthetic"}), flush=True)
+
+
 def synth_one(wl, b):
     """Workload wl restricted to its cloud b (the networks are per cloud)."""
     import copy
@@ -433,6 +515,8 @@ def main():
 
     if args.variants:
         return bench_variants(args, dev)
+    if args.backward:
+        return bench_backward(args, dev)
     wl = synth.make_workload(args.workload)
     if wl.is_network:
         return bench_network(args, wl, dev)
