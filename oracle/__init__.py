@@ -374,6 +374,27 @@ def pvconv_forward(coords, feats, layer, return_parts=False):
     return out
 
 
+def layer_backward_features(coords, feats, layer, dout):
+    """Gradient of one layer's output with respect to its input features
+    (Sections 4.1-4.3 differentiated): the voxel branch back through the
+    devoxelisation, each conv's BN + leaky and input gradient, and the
+    voxelisation; the point branch back through ReLU + BN and the linear map;
+    the fusion adds the two."""
+    parts = pvconv_forward(coords, feats, layer, return_parts=True)
+    R = layer.R
+    if getattr(layer, "devox", "trilinear") == "nearest":
+        g = devoxelize_nearest_backward(dout, R, parts["ids"])
+    else:
+        g = devoxelize_backward(dout, R, parts["pnorm"])
+    for i in range(len(layer.conv_w) - 1, -1, -1):
+        g = act_bn_backward(g, parts["convs"][i], layer.conv_bn[i], "leaky", layer.slope)
+        g = conv3d_backward_data(g, layer.conv_w[i], R)
+    dvox = voxelize_backward(g, parts["ids"], parts["counts"], R)
+    dz = act_bn_backward(dout, parts["point"], layer.mlp_bn, "relu")
+    dpoint = linear(dz, _f64(layer.mlp_w).T.copy())
+    return dvox + dpoint
+
+
 def shared_mlp(x, lp):
     """One point-only layer: Linear (+ bias), then BN and ReLU unless final."""
     y = linear(x, lp.w, lp.b)

@@ -11,7 +11,8 @@ import torch
 import oracle
 import synth
 from paper_1907_03739_amd import binding as pv
-from _helpers import assert_bf16_step, assert_dot_f32, assert_rel, bf16_round, dev, dev_bn, host
+from _helpers import (assert_bf16_chain, assert_bf16_step, assert_dot_f32, assert_rel,
+                      bf16_round, dev, dev_bn, host)
 
 pytestmark = pytest.mark.gpu
 
@@ -135,3 +136,58 @@ def test_act_bn_backward_matches_oracle(ydt, act, with_bn):
                                     bn=dev_bn(bn) if bn is not None else None, act=act,
                                     slope=0.1)
     assert_rel(host(got), ref, 1e-5, "act + BN backward")
+
+
+@pytest.mark.parametrize("wl_idx,B,devox", [(1, 1, "trilinear"), (2, 2, "trilinear"),
+                                            (2, 2, "nearest")])
+def test_layer_feature_gradient_composed_from_the_entry_points(wl_idx, B, devox):
+    # The whole layer's input-feature gradient from the backward entry points
+    # (and the point MLP with the transposed weight). The reference chains the
+    # oracle's backward steps (pinned one by one, and their composition by
+    # finite differences) through the same forward state: the rectifiers'
+    # derivatives are read from the GPU's own activations, since an
+    # activation within rounding of zero may take either side, and the
+    # gradients are rounded to bf16 where the GPU chain stores them in bf16.
+    import dataclasses
+    wl = synth.make_workload(wl_idx, B=B)
+    L = dataclasses.replace(wl.layers[0], devox=devox)
+    bf = wl.dtype == "bf16"
+    cdt = torch.bfloat16 if bf else torch.float32
+    rnd = bf16_round if bf else (lambda a: a.astype(np.float32).astype(np.float64))
+    R = L.R
+    rng = np.random.default_rng(9)
+    dout = rng.normal(size=(B, wl.N, L.cout)).astype(np.float32).astype(np.float64)
+
+    layer = pv.DeviceLayer(L, "cuda", cdt)
+    feats = dev(wl.feats)
+    grid, counts, ids, pn = pv.pvconv_voxelize(dev(wl.coords), feats, R, grid_dtype=cdt)
+    ys, h = [], grid
+    for i in range(L.n_convs):
+        h = pv.pvconv_conv3d(h, layer.conv_w[i], R, bn=layer.conv_bn[i], act="leaky",
+                             slope=L.slope)
+        ys.append(h)
+    hp = pv.pvconv_point_mlp(feats, layer.mlp_w, bias=layer.mlp_b, bn=layer.mlp_bn, act="relu")
+    d = dev(dout)
+    g = (pv.pvconv_devoxelize_nearest_backward(d, R, ids) if devox == "nearest"
+         else pv.pvconv_devoxelize_backward(d, R, pn))
+    for i in range(L.n_convs - 1, -1, -1):
+        g = pv.pvconv_act_bn_backward(g, ys[i], bn=layer.conv_bn[i], act="leaky", slope=L.slope)
+        g = pv.pvconv_conv3d_backward_data(g.to(cdt), layer.conv_w[i], R)
+    dvox = pv.pvconv_voxelize_backward(g.to(cdt), R, ids, counts)
+    dz = pv.pvconv_act_bn_backward(d, hp, bn=layer.mlp_bn, act="relu")
+    wT = torch.as_tensor(L.mlp_w, dtype=torch.float32).t().contiguous().cuda()
+    dpoint = pv.pvconv_point_mlp(dz, wT, act="none")
+    got = host(dvox) + host(dpoint)
+
+    ids_h, counts_h = ids.cpu().numpy(), counts.cpu().numpy()
+    r = (oracle.devoxelize_nearest_backward(dout, R, ids_h) if devox == "nearest"
+         else oracle.devoxelize_backward(dout, R, host(pn)))
+    for i in range(L.n_convs - 1, -1, -1):
+        r = oracle.act_bn_backward(r, host(ys[i]), L.conv_bn[i], "leaky", L.slope)
+        r = oracle.conv3d_backward_data(rnd(r), L.conv_w[i], R)
+    ref = oracle.voxelize_backward(rnd(r), ids_h, counts_h, R)
+    ref = ref + oracle.linear(oracle.act_bn_backward(dout, host(hp), L.mlp_bn, "relu"),
+                              np.ascontiguousarray(np.asarray(L.mlp_w, np.float64).T))
+    # a sum over chains of bf16-stored gradients: the chain bound of the
+    # forward layer tests (relative to |ref| + its rms)
+    assert_bf16_chain(got, ref, f"layer feature gradient ({devox})")

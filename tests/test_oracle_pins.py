@@ -508,6 +508,28 @@ def test_conv_backward_is_the_adjoint_at_a_realistic_shape():
     assert abs(lhs - _dot(oracle.conv3d_backward_weight(dy, x, R), w)) <= 1e-10 * (abs(lhs) + 1)
 
 
+def test_layer_feature_gradient_matches_finite_differences():
+    # the layer is piecewise linear in its features: central differences of
+    # the pinned forward give the directional derivative exactly away from the
+    # rectifiers' kinks
+    wl = synth.make_workload(1, N=200)
+    L = wl.layers[0]
+    rng = _rng(45)
+    feats = wl.feats.astype(np.float64)
+    dout = rng.normal(size=(1, 200, L.cout))
+    for devox in ("trilinear", "nearest"):
+        Ld = synth.PVConvParams(L.cin, L.cout, L.R, L.conv_w, L.conv_bn, L.mlp_w, L.mlp_bn,
+                                devox=devox)
+        df = oracle.layer_backward_features(wl.coords, feats, Ld, dout)
+        h = 1e-6
+        for _ in range(4):
+            e = rng.normal(size=feats.shape)
+            fp = oracle.pvconv_forward(wl.coords, feats + h * e, Ld)
+            fm = oracle.pvconv_forward(wl.coords, feats - h * e, Ld)
+            fd = _dot(dout, fp - fm) / (2 * h)
+            np.testing.assert_allclose(_dot(df, e), fd, rtol=1e-6)
+
+
 def test_act_bn_backward_matches_finite_differences():
     rng = _rng(44)
     bn = synth.draw_bn(rng, 6)
