@@ -209,10 +209,11 @@ __device__ __forceinline__ void load4<uint16_t>(const uint16_t* p, float* v) {
     v[3] = pv_bf16_to_f32((uint16_t)(a.y >> 16));
 }
 
+// dz may alias dy (each element is read, then written, by one thread).
 template <typename YT, bool V4>
 __global__ __launch_bounds__(256) void pv_act_bn_backward_kernel(
-    const float* __restrict__ dy, const YT* __restrict__ y, PvBnFold bn, float neg,
-    float* __restrict__ dz, int C, size_t n) {
+    const float* dy, const YT* __restrict__ y, PvBnFold bn, float neg, float* dz, int C,
+    size_t n) {
     const size_t stride = (size_t)gridDim.x * 256;
     constexpr int E = V4 ? 4 : 1;
     for (size_t j = ((size_t)blockIdx.x * 256 + threadIdx.x) * E; j < n; j += stride * E) {
