@@ -60,8 +60,9 @@ def parse():
                          "neighbour devoxelisation) on the part-seg layer's clouds, one JSON "
                          "line each")
     ap.add_argument("--backward", action="store_true",
-                    help="instead of the headline: the backward entry points (input "
-                         "gradients) at the part-seg layer's shapes, one JSON line each")
+                    help="instead of the headline: the backward entry points (input and "
+                         "conv weight gradients) at the part-seg layer's shapes, one JSON "
+                         "line each")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only copy a MIB-MiB buffer 3 times (a plain copy kernel of known "
                          "size, to calibrate the HBM byte counters) and exit")
@@ -403,8 +404,9 @@ def bench_variants(args, dev):
 
 
 def bench_backward(args, dev):
-    """Input gradients of the part-seg layer's steps, in reverse order, each
-    timed as the average of 10 back-to-back calls captured in a graph."""
+    """Gradients of the part-seg layer's steps (inputs, and the convolutions'
+    weights), in reverse order, each timed as the average of 10 back-to-back
+    calls captured in a graph."""
     import numpy as np
     import torch
 
@@ -433,6 +435,10 @@ def bench_backward(args, dev):
     wsz = max(pv._lib.pvconv_conv3d_backward_data_workspace_size(c, cout, 1) for c in (cin, cout))
     ws = torch.empty(wsz, dtype=torch.uint8, device=dev)
     bn2 = layer.conv_bn[1]
+    dw1 = torch.empty((cout, 3, 3, 3, cin), dtype=torch.float32, device=dev)
+    dw2 = torch.empty((cout, 3, 3, 3, cout), dtype=torch.float32, device=dev)
+    wws = torch.empty(max(pv._lib.pvconv_conv3d_backward_weight_workspace_size(B, R, c, cout)
+                          for c in (cin, cout)), dtype=torch.uint8, device=dev)
     s_g = 2
     steps = [
         # name, call, unit, algorithmic amount per call
@@ -446,6 +452,10 @@ def bench_backward(args, dev):
         ("conv1_backward_data", lambda: pv.pvconv_conv3d_backward_data(
             dy16, layer.conv_w[0], R, out_dtype=torch.bfloat16, out=dx1, workspace=ws),
          "TFLOP/s", conv_flops(B, R, cin, cout)),
+        ("conv2_backward_weight", lambda: pv.pvconv_conv3d_backward_weight(
+            dy16, y, R, out=dw2, workspace=wws), "TFLOP/s", conv_flops(B, R, cout, cout)),
+        ("conv1_backward_weight", lambda: pv.pvconv_conv3d_backward_weight(
+            dy16, grid, R, out=dw1, workspace=wws), "TFLOP/s", conv_flops(B, R, cin, cout)),
         ("voxelize_backward", lambda: pv.pvconv_voxelize_backward(dvox, R, ids, counts,
                                                                    out=dfeats),
          "GB/s", B * N * (4 + 4 + 4 * cin) + int((counts > 0).sum().item()) * cin * s_g),

@@ -311,6 +311,21 @@ pvconv_status pvconv_conv3d_backward_data(const void* dy, int B, int R, int Cin,
                                           pvconv_dtype dx_dt, void* workspace,
                                           size_t workspace_bytes, void* stream);
 
+/* Convolution, gradient with respect to its weights:                       */
+/*  dw[o][d+1][i] = sum_b sum_p dy[b,p,o] * x[b,p+d,i]  (x = 0 outside)       */
+/* an MFMA implicit GEMM over the voxels, split over bricks of the grid; the */
+/* splits' partial sums (in the workspace) are added in a fixed order, so    */
+/* the result is deterministic. dy [B][R^3][Cout] and x [B][R^3][Cin] (the   */
+/* convolution's input) in BF16, 16-byte aligned; dw out [Cout][3][3][3][Cin] */
+/* fp32. Needs Cout % 64 == 0 and Cin % 16 == 0 (else PVCONV_ENOTSUP).       */
+/* workspace >= pvconv_conv3d_backward_weight_workspace_size bytes, 256-byte */
+/* aligned.                                                                  */
+size_t pvconv_conv3d_backward_weight_workspace_size(int B, int R, int Cin, int Cout);
+pvconv_status pvconv_conv3d_backward_weight(const void* dy, const void* x, pvconv_dtype dt,
+                                            int B, int R, int Cin, int Cout, float* dw,
+                                            void* workspace, size_t workspace_bytes,
+                                            void* stream);
+
 /* Batch norm + activation, y = act(BN(z)) per channel, gradient with respect */
 /* to z: dz = dy * act'(y) * gamma / sqrt(var + eps), the rectifiers'        */
 /* derivative read from the sign of y (1 where y > 0, else slope for LEAKY,   */

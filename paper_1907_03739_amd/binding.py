@@ -74,6 +74,8 @@ _SIGS = {
     "pvconv_conv3d_backward_data": ([_VP, _I, _I, _I, _I, _VP, _I, _VP, _I, _VP, _SZ, _VP],
                                     _I),
     "pvconv_act_bn_backward": ([_VP, _VP, _I, _I, _I, _VP, _I, _F, _VP, _VP], _I),
+    "pvconv_conv3d_backward_weight_workspace_size": ([_I, _I, _I, _I], _SZ),
+    "pvconv_conv3d_backward_weight": ([_VP, _VP, _I, _I, _I, _I, _I, _VP, _VP, _SZ, _VP], _I),
 }
 for _name, (_args, _res) in _SIGS.items():
     _fn = getattr(_lib, _name)
@@ -330,6 +332,23 @@ def pvconv_conv3d_backward_data(dy: torch.Tensor, weight: torch.Tensor, R: int,
         _p(dy.contiguous()), B, R, Cin, Cout, _p(weight.contiguous()), _dt(dy), _p(dx),
         _dt(dx), _p(workspace), workspace.numel(), _stream(dy)))
     return dx
+
+
+def pvconv_conv3d_backward_weight(dy: torch.Tensor, x: torch.Tensor, R: int, out=None,
+                                  workspace=None):
+    """dy [B][R^3][Cout], x [B][R^3][Cin] (bf16) -> dW [Cout][3][3][3][Cin] f32."""
+    B, V, Cout = dy.shape
+    Cin = x.shape[-1]
+    if V != R ** 3 or tuple(x.shape[:2]) != (B, V):
+        raise ValueError("shape mismatch")
+    dw = _out(out, (Cout, 3, 3, 3, Cin), torch.float32, dy.device, "out")
+    need = _lib.pvconv_conv3d_backward_weight_workspace_size(B, R, Cin, Cout)
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=dy.device)
+    _check("pvconv_conv3d_backward_weight", _lib.pvconv_conv3d_backward_weight(
+        _p(dy.contiguous()), _p(x.contiguous()), _dt(dy), B, R, Cin, Cout, _p(dw),
+        _p(workspace), workspace.numel(), _stream(dy)))
+    return dw
 
 
 def pvconv_act_bn_backward(dy: torch.Tensor, y: torch.Tensor, bn=None, act="leaky", slope=0.1,

@@ -390,6 +390,31 @@ pvconv_status pvconv_conv3d_backward_data(const void* dy, int B, int R, int Cin,
                                           dx_dt == PVCONV_BF16, workspace, as_stream(stream));
 }
 
+size_t pvconv_conv3d_backward_weight_workspace_size(int B, int R, int Cin, int Cout) {
+    if (B < 0 || R < 1 || R > PVCONV_MAX_R || Cin < 1 || Cout < 1 ||
+        Cin > PVCONV_MAX_CONV_CHANNELS || Cout > PVCONV_MAX_CONV_CHANNELS)
+        return 0;
+    return pv_conv3d_wgrad_ws_bytes(B, R, Cin, Cout);
+}
+
+pvconv_status pvconv_conv3d_backward_weight(const void* dy, const void* x, pvconv_dtype dt,
+                                            int B, int R, int Cin, int Cout, float* dw,
+                                            void* workspace, size_t workspace_bytes,
+                                            void* stream) {
+    if (B < 0 || R < 1 || R > PVCONV_MAX_R || Cin < 1 || Cout < 1 ||
+        Cin > PVCONV_MAX_CONV_CHANNELS || Cout > PVCONV_MAX_CONV_CHANNELS || !dtype_ok(dt) ||
+        !sizes_fit(B, (long long)R * R * R))
+        return PVCONV_EINVAL;
+    if (dt != PVCONV_BF16 || Cout % 64 != 0 || Cin % 16 != 0) return PVCONV_ENOTSUP;
+    if (!dw || (B > 0 && (!dy || !x))) return PVCONV_EINVAL;
+    if (!pv_aligned16(dy) || !pv_aligned16(x) || ((uintptr_t)dw & 3)) return PVCONV_EINVAL;
+    const size_t need = pv_conv3d_wgrad_ws_bytes(B, R, Cin, Cout);
+    if (need && (!workspace || ((uintptr_t)workspace & 255) || workspace_bytes < need))
+        return PVCONV_EWORKSPACE;
+    return pv_launch_conv3d_backward_weight(dy, x, B, R, Cin, Cout, dw, workspace,
+                                            as_stream(stream));
+}
+
 pvconv_status pvconv_act_bn_backward(const float* dy, const void* y, pvconv_dtype y_dt, int M,
                                      int C, const pvconv_bn* bn, pvconv_act act, float slope,
                                      float* dz, void* stream) {

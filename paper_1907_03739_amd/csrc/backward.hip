@@ -239,6 +239,186 @@ __global__ __launch_bounds__(256) void pv_act_bn_backward_kernel(
     }
 }
 
+// ---------------------------------------------------------------------------
+// Convolution weight gradient on the MFMA units:
+//   dW[o][t][i] = sum over clouds b and output voxels p of dy[b][p][o] * x[b][p + d_t][i]
+// an implicit GEMM with M = output channels, N = (tap, input channel) and
+// K = voxels. A workgroup (four waves) owns 64 output channels x one chunk of
+// 16 input channels x all 27 taps for a contiguous range of 8x8x8 bricks (a
+// split of the voxel sum); each split writes its partial sums, and a second
+// kernel adds the splits in split order. Per brick:
+//  * dy of the brick, transposed in LDS to [64 o][512 p]: an A fragment (8
+//    consecutive voxels, one w-row, of one channel) is one 16-byte read;
+//  * x of the brick's 10x10x10 halo for the 16 channels, transposed to
+//    [s][16 i][10][10][8] for s = 0, 1, 2: copy s holds the halo's w-window
+//    s .. s+7, so the B fragment of a tap with w-offset dw (a w-row of 8
+//    voxels shifted by dw) is one aligned 16-byte read of copy dw + 1.
+// The GEMM's columns pair the taps: column n of tap pair q is tap 2q + n/16,
+// input channel n % 16 (tap 27 of the last pair is padding, zero). Every wave
+// owns both 32-channel blocks of the 64 and tap pairs w, w+4, w+8, w+12 (<14).
+// Voxels outside the grid (ragged bricks, the halo's border) read as zero.
+constexpr int kWgO = 64;                              // output channels per workgroup
+constexpr int kWgPairs = 14;                          // tap pairs, 27 taps + 1 padding
+constexpr int kDyPitch = 512 * 2 + 16;                // bytes per transposed dy row
+constexpr int kDyBytes = kWgO * kDyPitch;             // 66560
+constexpr int kXtBytes = 3 * 16 * 10 * 10 * 8 * 2;    // 76800
+constexpr int kWgradLds = kDyBytes + kXtBytes;        // 143360
+
+__global__ __launch_bounds__(256, 1) void pv_conv3d_wgrad_kernel(
+    const uint16_t* __restrict__ dy, const uint16_t* __restrict__ x, float* __restrict__ part,
+    int R, int Cin, int Cout, int nbr, int nbricks, int per_split) {
+    __shared__ __attribute__((aligned(16))) char lds[kWgradLds];
+    char* ldy = lds;
+    char* lxt = lds + kDyBytes;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int r32 = lane & 31, khalf = lane >> 5;
+    const int split = blockIdx.x, o0 = blockIdx.y * kWgO, i0 = blockIdx.z * 16;
+    const int b0 = split * per_split, b1 = min(nbricks, b0 + per_split);
+    const size_t V = (size_t)R * R * R;
+
+    pv_f32x16 acc[2][4];
+#pragma unroll
+    for (int ob = 0; ob < 2; ob++)
+#pragma unroll
+        for (int qi = 0; qi < 4; qi++)
+#pragma unroll
+            for (int j = 0; j < 16; j++) acc[ob][qi][j] = 0.f;
+    // this lane's columns: tap pair q = wave + 4 qi, tap 2q + (r32 >> 4), channel r32 & 15
+    int boff[4];   // LDS byte offset of the B fragment at (pu, pv) = (0, 0), or -1
+#pragma unroll
+    for (int qi = 0; qi < 4; qi++) {
+        const int q = wave + 4 * qi, tap = 2 * q + (r32 >> 4);
+        if (q >= kWgPairs || tap >= 27) {
+            boff[qi] = -1;
+            continue;
+        }
+        const int du = tap / 9 - 1, dv = (tap / 3) % 3 - 1, dw = tap % 3 - 1;
+        boff[qi] = (((((dw + 1) * 16 + (r32 & 15)) * 10 + (du + 1)) * 10 + (dv + 1)) * 8) * 2;
+    }
+
+    for (int brick = b0; brick < b1; brick++) {
+        int rest = brick;
+        const int bw = rest % nbr;
+        rest /= nbr;
+        const int bv = rest % nbr;
+        rest /= nbr;
+        const int bu = rest % nbr;
+        const int b = rest / nbr;
+        const int u0 = bu * 8, v0 = bv * 8, w0 = bw * 8;
+        const uint16_t* dyb = dy + (size_t)b * V * Cout + o0;
+        const uint16_t* xb = x + (size_t)b * V * Cin + i0;
+        // dy of voxels p = 2 tid, 2 tid + 1 (one w-row pair), all 64 channels
+        {
+            const int p = 2 * tid, pu = p >> 6, pv = (p >> 3) & 7, pw = p & 7;
+            uint4 d0[8], d1[8];
+            const int u = u0 + pu, v = v0 + pv, w = w0 + pw;
+            const bool in0 = u < R && v < R && w < R, in1 = u < R && v < R && w + 1 < R;
+            const uint16_t* r0 = dyb + (((size_t)u * R + v) * R + w) * Cout;
+#pragma unroll
+            for (int q = 0; q < 8; q++) {
+                d0[q] = in0 ? *(const uint4*)(r0 + 8 * q) : make_uint4(0, 0, 0, 0);
+                d1[q] = in1 ? *(const uint4*)(r0 + Cout + 8 * q) : make_uint4(0, 0, 0, 0);
+            }
+#pragma unroll
+            for (int q = 0; q < 8; q++) {
+                const uint32_t a[4] = {d0[q].x, d0[q].y, d0[q].z, d0[q].w};
+                const uint32_t c[4] = {d1[q].x, d1[q].y, d1[q].z, d1[q].w};
+#pragma unroll
+                for (int e = 0; e < 4; e++) {
+                    const int o = 8 * q + 2 * e;
+                    *(uint32_t*)(ldy + o * kDyPitch + p * 2) = (a[e] & 0xffffu) | (c[e] << 16);
+                    *(uint32_t*)(ldy + (o + 1) * kDyPitch + p * 2) = (a[e] >> 16) | (c[e] & 0xffff0000u);
+                }
+            }
+        }
+        // x of the halo: items (s, hu, hv, w-pair), voxels hw = 2 wp + s and + 1
+        for (int item = tid; item < 3 * 10 * 10 * 4; item += 256) {
+            const int wp = item & 3, hv = (item >> 2) % 10, hu = (item / 40) % 10, sc = item / 400;
+            const int u = u0 + hu - 1, v = v0 + hv - 1, w = w0 + 2 * wp + sc - 1;
+            const bool uv = u >= 0 && u < R && v >= 0 && v < R;
+            const bool in0 = uv && w >= 0 && w < R, in1 = uv && w + 1 >= 0 && w + 1 < R;
+            const uint16_t* r0 = xb + (((size_t)(uv ? u : 0) * R + (uv ? v : 0)) * R) * Cin;
+            uint4 x0[2], x1[2];
+#pragma unroll
+            for (int h = 0; h < 2; h++) {
+                x0[h] = in0 ? *(const uint4*)(r0 + (size_t)w * Cin + 8 * h) : make_uint4(0, 0, 0, 0);
+                x1[h] = in1 ? *(const uint4*)(r0 + (size_t)(w + 1) * Cin + 8 * h)
+                            : make_uint4(0, 0, 0, 0);
+            }
+#pragma unroll
+            for (int h = 0; h < 2; h++) {
+                const uint32_t a[4] = {x0[h].x, x0[h].y, x0[h].z, x0[h].w};
+                const uint32_t c[4] = {x1[h].x, x1[h].y, x1[h].z, x1[h].w};
+#pragma unroll
+                for (int e = 0; e < 4; e++) {
+                    const int i = 8 * h + 2 * e;
+                    const int base = (((sc * 16 + i) * 10 + hu) * 10 + hv) * 8 + 2 * wp;
+                    *(uint32_t*)(lxt + base * 2) = (a[e] & 0xffffu) | (c[e] << 16);
+                    *(uint32_t*)(lxt + (base + 800) * 2) = (a[e] >> 16) | (c[e] & 0xffff0000u);
+                }
+            }
+        }
+        __syncthreads();
+        // 32 k-steps of 16 voxels (two w-rows): this lane's row r = 2 ks + khalf
+        for (int ks = 0; ks < 32; ks++) {
+            const int r = 2 * ks + khalf, pu = r >> 3, pv = r & 7;
+            pv_bf16x8 a[2], bfr[4];
+#pragma unroll
+            for (int ob = 0; ob < 2; ob++)
+                a[ob] = *(const pv_bf16x8*)(ldy + (ob * 32 + r32) * kDyPitch + r * 16);
+#pragma unroll
+            for (int qi = 0; qi < 4; qi++) {
+                if (boff[qi] >= 0)
+                    bfr[qi] = *(const pv_bf16x8*)(lxt + boff[qi] + (pu * 10 + pv) * 16);
+                else
+                    bfr[qi] = pv_bf16x8{0, 0, 0, 0, 0, 0, 0, 0};
+            }
+#pragma unroll
+            for (int ob = 0; ob < 2; ob++)
+#pragma unroll
+                for (int qi = 0; qi < 4; qi++)
+                    if (wave + 4 * qi < kWgPairs)
+                        acc[ob][qi] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ob], bfr[qi],
+                                                                             acc[ob][qi], 0, 0, 0);
+        }
+        __syncthreads();
+    }
+    // partial sums: rows o = 8 j + 4 khalf + e of each 32-channel block, column r32
+    float* dst = part + (size_t)split * Cout * 27 * Cin;
+#pragma unroll
+    for (int qi = 0; qi < 4; qi++) {
+        if (boff[qi] < 0) continue;
+        const int tap = 2 * (wave + 4 * qi) + (r32 >> 4), i = i0 + (r32 & 15);
+#pragma unroll
+        for (int ob = 0; ob < 2; ob++)
+#pragma unroll
+            for (int j = 0; j < 16; j++) {
+                const int o = o0 + ob * 32 + 8 * (j >> 2) + 4 * khalf + (j & 3);
+                dst[((size_t)o * 27 + tap) * Cin + i] = acc[ob][qi][j];
+            }
+    }
+}
+
+// dW[j] = the sum of the splits' partials for element j, in split order.
+__global__ __launch_bounds__(256) void pv_wgrad_reduce_kernel(const float* __restrict__ part,
+                                                              float* __restrict__ dw, size_t n,
+                                                              int nsplit) {
+    for (size_t j = (size_t)blockIdx.x * 256 + threadIdx.x; j < n; j += (size_t)gridDim.x * 256) {
+        float sum = 0.f;
+        for (int s = 0; s < nsplit; s++) sum += part[(size_t)s * n + j];
+        dw[j] = sum;
+    }
+}
+
+// Splits of the voxel sum: enough workgroups for every CU, whole bricks each.
+int wgrad_splits(int B, int R, int Cin, int Cout) {
+    const int nbr = (R + 7) / 8;
+    const int nbricks = B * nbr * nbr * nbr;
+    const int tiles = (Cout / kWgO) * (Cin / 16);
+    const int want = (256 + tiles - 1) / tiles;
+    return std::max(1, std::min(nbricks, want));
+}
+
 unsigned blocks_for(size_t items) { return (unsigned)((items + 255) / 256); }
 
 unsigned fill_blocks(size_t n) {
@@ -336,5 +516,30 @@ pvconv_status pv_launch_act_bn_backward(const float* dy, const void* y, bool y_b
     } else {
         if (v4) go(float{}, std::true_type{}); else go(float{}, std::false_type{});
     }
+    return pv_launch_status();
+}
+
+size_t pv_conv3d_wgrad_ws_bytes(int B, int R, int Cin, int Cout) {
+    return (size_t)wgrad_splits(B, R, Cin, Cout) * Cout * 27 * Cin * sizeof(float);
+}
+
+pvconv_status pv_launch_conv3d_backward_weight(const void* dy, const void* x, int B, int R,
+                                               int Cin, int Cout, float* dw, void* ws,
+                                               hipStream_t s) {
+    const size_t n = (size_t)Cout * 27 * Cin;
+    if (B == 0) {
+        hipLaunchKernelGGL(pv_fill_zero_kernel, dim3(fill_blocks(n)), dim3(256), 0, s, dw, n);
+        return pv_launch_status();
+    }
+    const int nbr = (R + 7) / 8, nbricks = B * nbr * nbr * nbr;
+    const int nsplit = wgrad_splits(B, R, Cin, Cout);
+    const int per = (nbricks + nsplit - 1) / nsplit;
+    const int used = (nbricks + per - 1) / per;  // splits that hold at least one brick
+    float* part = (float*)ws;
+    hipLaunchKernelGGL(pv_conv3d_wgrad_kernel, dim3(used, Cout / kWgO, Cin / 16), dim3(256), 0, s,
+                       (const uint16_t*)dy, (const uint16_t*)x, part, R, Cin, Cout, nbr, nbricks,
+                       per);
+    const unsigned blocks = (unsigned)std::min<size_t>((n + 255) / 256, 2048);
+    hipLaunchKernelGGL(pv_wgrad_reduce_kernel, dim3(blocks), dim3(256), 0, s, part, dw, n, used);
     return pv_launch_status();
 }

@@ -142,6 +142,10 @@ pvconv_status pv_launch_devoxelize_backward(const float* dout, int B, int N, int
 pvconv_status pv_launch_conv3d_backward_data(const void* dy, int B, int R, int Cin, int Cout,
                                              const void* w, bool bf16, void* dx, bool dx_bf16,
                                              void* ws, hipStream_t s);
+size_t pv_conv3d_wgrad_ws_bytes(int B, int R, int Cin, int Cout);
+pvconv_status pv_launch_conv3d_backward_weight(const void* dy, const void* x, int B, int R,
+                                               int Cin, int Cout, float* dw, void* ws,
+                                               hipStream_t s);
 pvconv_status pv_launch_act_bn_backward(const float* dy, const void* y, bool y_bf16, size_t M,
                                         int C, const PvBnFold& bn, int act, float slope,
                                         float* dz, hipStream_t s);

@@ -30,7 +30,7 @@ def declared_functions():
 
 def test_library_exports_every_declared_symbol():
     names = declared_functions()
-    assert len(names) == 19
+    assert len(names) == 21
     out = subprocess.run(["nm", "-D", "--defined-only", b.LIB_PATH], capture_output=True,
                          text=True, check=True).stdout
     exported = set(re.findall(r"\bT (pvconv_\w+)", out))
@@ -273,6 +273,21 @@ def test_backward_entry_points_reject(call, status):
     if status is None:      # valid arguments: would launch, so only check the others
         return
     assert call() == status
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dt=0), ENOTSUP), (dict(Cout=96), ENOTSUP), (dict(Cin=8), ENOTSUP),
+    (dict(dt=4), EINVAL), (dict(R=0), EINVAL), (dict(B=-1), EINVAL), (dict(dw=None), EINVAL),
+    (dict(dy=None), EINVAL), (dict(x=ctypes.c_void_p(0x100008)), EINVAL),
+    (dict(ws=None), EWS), (dict(wsb=64), EWS),
+])
+def test_conv3d_backward_weight_rejects(kw, status):
+    a = dict(dy=FAKE, x=FAKE2, dt=1, B=2, R=8, Cin=64, Cout=128, dw=ctypes.c_void_p(0x300000),
+             ws=ctypes.c_void_p(0x400000), wsb=1 << 40, s=None)
+    a.update(kw)
+    assert L.pvconv_conv3d_backward_weight(a["dy"], a["x"], a["dt"], a["B"], a["R"], a["Cin"],
+                                           a["Cout"], a["dw"], a["ws"], a["wsb"],
+                                           a["s"]) == status
 
 
 def test_backward_workspace_query():

@@ -118,6 +118,42 @@ def test_conv3d_backward_data_is_the_adjoint_of_the_forward_on_gpu():
     assert abs(lhs - rhs) <= 1e-5 * scale, (lhs, rhs, scale)
 
 
+@pytest.mark.parametrize("B,R,Cin,Cout", [
+    (2, 32, 64, 128),    # the part-seg layer's first conv (batch reduced)
+    (1, 16, 128, 128),
+    (1, 13, 32, 64),     # ragged bricks
+    (3, 8, 16, 64),      # one brick per cloud
+    (1, 1, 16, 64),      # a single voxel: only the centre tap sees data
+])
+def test_conv3d_backward_weight_matches_oracle(B, R, Cin, Cout):
+    rng = np.random.default_rng(R * 3 + Cin + Cout)
+    dy = bf16_round(rng.normal(size=(B, R ** 3, Cout)) * (rng.random((B, R ** 3, 1)) < 0.5))
+    x = bf16_round(rng.normal(size=(B, R ** 3, Cin)) * (rng.random((B, R ** 3, 1)) < 0.3))
+    ref = oracle.conv3d_backward_weight(dy, x, R)
+    mag = oracle.conv3d_backward_weight(np.abs(dy), np.abs(x), R)
+    got = host(pv.pvconv_conv3d_backward_weight(dev(dy, torch.bfloat16), dev(x, torch.bfloat16),
+                                                R))
+    assert_dot_f32(got, ref, mag, "conv weight gradient")
+
+
+def test_conv3d_backward_weight_is_deterministic_and_the_adjoint_on_gpu():
+    # <dW, W> = <dy, conv(x, W)> with both sides from the GPU kernels
+    rng = np.random.default_rng(12)
+    R, Cin, Cout = 16, 32, 64
+    x = bf16_round(rng.normal(size=(2, R ** 3, Cin)))
+    dy = bf16_round(rng.normal(size=(2, R ** 3, Cout)))
+    w = synth.kaiming_normal(rng, (Cout, 3, 3, 3, Cin), 27 * Cin, bf16=True)
+    dyd, xd = dev(dy, torch.bfloat16), dev(x, torch.bfloat16)
+    dw1 = host(pv.pvconv_conv3d_backward_weight(dyd, xd, R))
+    dw2 = host(pv.pvconv_conv3d_backward_weight(dyd, xd, R))
+    assert np.array_equal(dw1, dw2)
+    y = host(pv.pvconv_conv3d(xd, dev(w, torch.bfloat16), R, act="none",
+                              out_dtype=torch.float32))
+    lhs, rhs = float(np.sum(dy * y)), float(np.sum(dw1 * w))
+    scale = max(float(np.sum(np.abs(dy * y))), float(np.sum(np.abs(dw1 * w))))
+    assert abs(lhs - rhs) <= 1e-5 * scale, (lhs, rhs, scale)
+
+
 @pytest.mark.parametrize("ydt,act,with_bn", [
     ("f32", "leaky", True), ("bf16", "leaky", True), ("f32", "relu", True),
     ("bf16", "none", False), ("f32", "leaky", False),
