@@ -253,16 +253,113 @@ __global__ __launch_bounds__(256) void pv_act_bn_backward_kernel(
 //    [s][16 i][10][10][8] for s = 0, 1, 2: copy s holds the halo's w-window
 //    s .. s+7, so the B fragment of a tap with w-offset dw (a w-row of 8
 //    voxels shifted by dw) is one aligned 16-byte read of copy dw + 1.
+// A brick's global loads are issued together into registers while the
+// previous brick's MFMAs run, then written to LDS.
 // The GEMM's columns pair the taps: column n of tap pair q is tap 2q + n/16,
-// input channel n % 16 (tap 27 of the last pair is padding, zero). Every wave
-// owns both 32-channel blocks of the 64 and tap pairs w, w+4, w+8, w+12 (<14).
+// input channel n % 16 (taps 27 .. 31 are padding: computed, never written).
+// Every wave owns both 32-channel blocks of the 64 and tap pairs w, w+4, w+8,
+// w+12.
 // Voxels outside the grid (ragged bricks, the halo's border) read as zero.
 constexpr int kWgO = 64;                              // output channels per workgroup
-constexpr int kWgPairs = 14;                          // tap pairs, 27 taps + 1 padding
 constexpr int kDyPitch = 512 * 2 + 16;                // bytes per transposed dy row
 constexpr int kDyBytes = kWgO * kDyPitch;             // 66560
-constexpr int kXtBytes = 3 * 16 * 10 * 10 * 8 * 2;    // 76800
-constexpr int kWgradLds = kDyBytes + kXtBytes;        // 143360
+// one (copy s, channel i) block of the halo: 10 x 10 w-windows of 8, padded
+// by 16 bytes so that the B reads of the 16 channels start in distinct banks
+constexpr int kXtBlock = 10 * 10 * 8 * 2 + 16;        // 1616
+constexpr int kXtBytes = 3 * 16 * kXtBlock;           // 77568
+constexpr int kWgradLds = kDyBytes + kXtBytes;        // 144128
+constexpr int kXtItems = 3 * 10 * 10 * 4;             // (s, hu, hv, w-pair)
+constexpr int kXtPer = (kXtItems + 255) / 256;        // 5 items per thread
+
+// A brick's operands in registers, between their global loads and their
+// transposing LDS writes: dy of voxels 2 tid, 2 tid + 1 (64 channels each)
+// and x of the thread's halo items (two voxels, 16 channels each).
+struct WgradRegs {
+    uint4 d0[8], d1[8];
+    uint4 x0[kXtPer][2], x1[kXtPer][2];
+};
+
+__device__ __forceinline__ void wgrad_load(WgradRegs& g, const uint16_t* __restrict__ dy,
+                                           const uint16_t* __restrict__ x, int brick, int nbr,
+                                           int R, int Cin, int Cout, int o0, int i0) {
+    const int tid = threadIdx.x;
+    int rest = brick;
+    const int bw = rest % nbr;
+    rest /= nbr;
+    const int bv = rest % nbr;
+    rest /= nbr;
+    const int bu = rest % nbr;
+    const int b = rest / nbr;
+    const int u0 = bu * 8, v0 = bv * 8, w0 = bw * 8;
+    const size_t V = (size_t)R * R * R;
+    const uint4 z = make_uint4(0, 0, 0, 0);
+    // every load reads a voxel clamped into the grid; outside voxels are then
+    // replaced by zero (no branches around the loads)
+    auto cl = [R](int a) { return min(max(a, 0), R - 1); };
+    auto sel = [&z](bool in, uint4 v) { return in ? v : z; };
+    {
+        const int p = 2 * tid, u = u0 + (p >> 6), v = v0 + ((p >> 3) & 7), w = w0 + (p & 7);
+        const bool in0 = u < R && v < R && w < R, in1 = in0 && w + 1 < R;
+        const uint16_t* dyb = dy + (size_t)b * V * Cout + o0;
+        const uint16_t* r0 = dyb + (((size_t)cl(u) * R + cl(v)) * R + cl(w)) * Cout;
+        const uint16_t* r1 = dyb + (((size_t)cl(u) * R + cl(v)) * R + cl(w + 1)) * Cout;
+#pragma unroll
+        for (int q = 0; q < 8; q++) {
+            g.d0[q] = sel(in0, *(const uint4*)(r0 + 8 * q));
+            g.d1[q] = sel(in1, *(const uint4*)(r1 + 8 * q));
+        }
+    }
+    const uint16_t* xb = x + (size_t)b * V * Cin + i0;
+#pragma unroll
+    for (int k = 0; k < kXtPer; k++) {
+        const int item = tid + 256 * k;
+        const int wp = item & 3, hv = (item >> 2) % 10, hu = (item / 40) % 10, sc = item / 400;
+        const int u = u0 + hu - 1, v = v0 + hv - 1, w = w0 + 2 * wp + sc - 1;
+        const bool uv = item < kXtItems && u >= 0 && u < R && v >= 0 && v < R;
+        const bool in0 = uv && w >= 0 && w < R, in1 = uv && w + 1 >= 0 && w + 1 < R;
+        const uint16_t* r0 = xb + (((size_t)cl(u) * R + cl(v)) * R + cl(w)) * Cin;
+        const uint16_t* r1 = xb + (((size_t)cl(u) * R + cl(v)) * R + cl(w + 1)) * Cin;
+#pragma unroll
+        for (int h = 0; h < 2; h++) {
+            g.x0[k][h] = sel(in0, *(const uint4*)(r0 + 8 * h));
+            g.x1[k][h] = sel(in1, *(const uint4*)(r1 + 8 * h));
+        }
+    }
+}
+
+__device__ __forceinline__ void wgrad_store(const WgradRegs& g, char* ldy, char* lxt) {
+    const int tid = threadIdx.x, p = 2 * tid;
+#pragma unroll
+    for (int q = 0; q < 8; q++) {
+        const uint32_t a[4] = {g.d0[q].x, g.d0[q].y, g.d0[q].z, g.d0[q].w};
+        const uint32_t c[4] = {g.d1[q].x, g.d1[q].y, g.d1[q].z, g.d1[q].w};
+#pragma unroll
+        for (int e = 0; e < 4; e++) {
+            const int o = 8 * q + 2 * e;
+            *(uint32_t*)(ldy + o * kDyPitch + p * 2) = (a[e] & 0xffffu) | (c[e] << 16);
+            *(uint32_t*)(ldy + (o + 1) * kDyPitch + p * 2) = (a[e] >> 16) | (c[e] & 0xffff0000u);
+        }
+    }
+#pragma unroll
+    for (int k = 0; k < kXtPer; k++) {
+        const int item = tid + 256 * k;
+        if (item >= kXtItems) continue;
+        const int wp = item & 3, hv = (item >> 2) % 10, hu = (item / 40) % 10, sc = item / 400;
+        const int pos = ((hu * 10 + hv) * 8 + 2 * wp) * 2;  // bytes within a block
+#pragma unroll
+        for (int h = 0; h < 2; h++) {
+            const uint32_t a[4] = {g.x0[k][h].x, g.x0[k][h].y, g.x0[k][h].z, g.x0[k][h].w};
+            const uint32_t c[4] = {g.x1[k][h].x, g.x1[k][h].y, g.x1[k][h].z, g.x1[k][h].w};
+#pragma unroll
+            for (int e = 0; e < 4; e++) {
+                const int i = 8 * h + 2 * e;
+                char* blk = lxt + (sc * 16 + i) * kXtBlock + pos;
+                *(uint32_t*)blk = (a[e] & 0xffffu) | (c[e] << 16);
+                *(uint32_t*)(blk + kXtBlock) = (a[e] >> 16) | (c[e] & 0xffff0000u);
+            }
+        }
+    }
+}
 
 __global__ __launch_bounds__(256, 1) void pv_conv3d_wgrad_kernel(
     const uint16_t* __restrict__ dy, const uint16_t* __restrict__ x, float* __restrict__ part,
@@ -274,7 +371,6 @@ __global__ __launch_bounds__(256, 1) void pv_conv3d_wgrad_kernel(
     const int r32 = lane & 31, khalf = lane >> 5;
     const int split = blockIdx.x, o0 = blockIdx.y * kWgO, i0 = blockIdx.z * 16;
     const int b0 = split * per_split, b1 = min(nbricks, b0 + per_split);
-    const size_t V = (size_t)R * R * R;
 
     pv_f32x16 acc[2][4];
 #pragma unroll
@@ -283,103 +379,48 @@ __global__ __launch_bounds__(256, 1) void pv_conv3d_wgrad_kernel(
         for (int qi = 0; qi < 4; qi++)
 #pragma unroll
             for (int j = 0; j < 16; j++) acc[ob][qi][j] = 0.f;
-    // this lane's columns: tap pair q = wave + 4 qi, tap 2q + (r32 >> 4), channel r32 & 15
-    int boff[4];   // LDS byte offset of the B fragment at (pu, pv) = (0, 0), or -1
+    // this lane's columns: tap pair q = wave + 4 qi, tap 2q + (r32 >> 4),
+    // channel r32 & 15; boff = LDS byte offset of its B fragment at
+    // (pu, pv) = (0, 0). Padding columns (tap >= 27) read tap 26's fragment
+    // and are never written out.
+    int boff[4];
 #pragma unroll
     for (int qi = 0; qi < 4; qi++) {
-        const int q = wave + 4 * qi, tap = 2 * q + (r32 >> 4);
-        if (q >= kWgPairs || tap >= 27) {
-            boff[qi] = -1;
-            continue;
-        }
+        const int tap = min(26, 2 * (wave + 4 * qi) + (r32 >> 4));
         const int du = tap / 9 - 1, dv = (tap / 3) % 3 - 1, dw = tap % 3 - 1;
-        boff[qi] = (((((dw + 1) * 16 + (r32 & 15)) * 10 + (du + 1)) * 10 + (dv + 1)) * 8) * 2;
+        boff[qi] = ((dw + 1) * 16 + (r32 & 15)) * kXtBlock + ((du + 1) * 10 + (dv + 1)) * 16;
     }
 
+    // the next brick's operands load during the current brick's MFMAs
+    WgradRegs g;
+    if (b0 < b1) wgrad_load(g, dy, x, b0, nbr, R, Cin, Cout, o0, i0);
     for (int brick = b0; brick < b1; brick++) {
-        int rest = brick;
-        const int bw = rest % nbr;
-        rest /= nbr;
-        const int bv = rest % nbr;
-        rest /= nbr;
-        const int bu = rest % nbr;
-        const int b = rest / nbr;
-        const int u0 = bu * 8, v0 = bv * 8, w0 = bw * 8;
-        const uint16_t* dyb = dy + (size_t)b * V * Cout + o0;
-        const uint16_t* xb = x + (size_t)b * V * Cin + i0;
-        // dy of voxels p = 2 tid, 2 tid + 1 (one w-row pair), all 64 channels
-        {
-            const int p = 2 * tid, pu = p >> 6, pv = (p >> 3) & 7, pw = p & 7;
-            uint4 d0[8], d1[8];
-            const int u = u0 + pu, v = v0 + pv, w = w0 + pw;
-            const bool in0 = u < R && v < R && w < R, in1 = u < R && v < R && w + 1 < R;
-            const uint16_t* r0 = dyb + (((size_t)u * R + v) * R + w) * Cout;
-#pragma unroll
-            for (int q = 0; q < 8; q++) {
-                d0[q] = in0 ? *(const uint4*)(r0 + 8 * q) : make_uint4(0, 0, 0, 0);
-                d1[q] = in1 ? *(const uint4*)(r0 + Cout + 8 * q) : make_uint4(0, 0, 0, 0);
-            }
-#pragma unroll
-            for (int q = 0; q < 8; q++) {
-                const uint32_t a[4] = {d0[q].x, d0[q].y, d0[q].z, d0[q].w};
-                const uint32_t c[4] = {d1[q].x, d1[q].y, d1[q].z, d1[q].w};
-#pragma unroll
-                for (int e = 0; e < 4; e++) {
-                    const int o = 8 * q + 2 * e;
-                    *(uint32_t*)(ldy + o * kDyPitch + p * 2) = (a[e] & 0xffffu) | (c[e] << 16);
-                    *(uint32_t*)(ldy + (o + 1) * kDyPitch + p * 2) = (a[e] >> 16) | (c[e] & 0xffff0000u);
-                }
-            }
-        }
-        // x of the halo: items (s, hu, hv, w-pair), voxels hw = 2 wp + s and + 1
-        for (int item = tid; item < 3 * 10 * 10 * 4; item += 256) {
-            const int wp = item & 3, hv = (item >> 2) % 10, hu = (item / 40) % 10, sc = item / 400;
-            const int u = u0 + hu - 1, v = v0 + hv - 1, w = w0 + 2 * wp + sc - 1;
-            const bool uv = u >= 0 && u < R && v >= 0 && v < R;
-            const bool in0 = uv && w >= 0 && w < R, in1 = uv && w + 1 >= 0 && w + 1 < R;
-            const uint16_t* r0 = xb + (((size_t)(uv ? u : 0) * R + (uv ? v : 0)) * R) * Cin;
-            uint4 x0[2], x1[2];
-#pragma unroll
-            for (int h = 0; h < 2; h++) {
-                x0[h] = in0 ? *(const uint4*)(r0 + (size_t)w * Cin + 8 * h) : make_uint4(0, 0, 0, 0);
-                x1[h] = in1 ? *(const uint4*)(r0 + (size_t)(w + 1) * Cin + 8 * h)
-                            : make_uint4(0, 0, 0, 0);
-            }
-#pragma unroll
-            for (int h = 0; h < 2; h++) {
-                const uint32_t a[4] = {x0[h].x, x0[h].y, x0[h].z, x0[h].w};
-                const uint32_t c[4] = {x1[h].x, x1[h].y, x1[h].z, x1[h].w};
-#pragma unroll
-                for (int e = 0; e < 4; e++) {
-                    const int i = 8 * h + 2 * e;
-                    const int base = (((sc * 16 + i) * 10 + hu) * 10 + hv) * 8 + 2 * wp;
-                    *(uint32_t*)(lxt + base * 2) = (a[e] & 0xffffu) | (c[e] << 16);
-                    *(uint32_t*)(lxt + (base + 800) * 2) = (a[e] >> 16) | (c[e] & 0xffff0000u);
-                }
-            }
-        }
+        wgrad_store(g, ldy, lxt);
         __syncthreads();
-        // 32 k-steps of 16 voxels (two w-rows): this lane's row r = 2 ks + khalf
-        for (int ks = 0; ks < 32; ks++) {
+        if (brick + 1 < b1) wgrad_load(g, dy, x, brick + 1, nbr, R, Cin, Cout, o0, i0);
+        // 32 k-steps of 16 voxels (two w-rows): this lane's row r = 2 ks + khalf;
+        // the fragments of step ks + 1 are read during the MFMAs of step ks
+        pv_bf16x8 a[2][2], bfr[2][4];
+        auto frags = [&](int ks, int buf) {
             const int r = 2 * ks + khalf, pu = r >> 3, pv = r & 7;
-            pv_bf16x8 a[2], bfr[4];
 #pragma unroll
             for (int ob = 0; ob < 2; ob++)
-                a[ob] = *(const pv_bf16x8*)(ldy + (ob * 32 + r32) * kDyPitch + r * 16);
+                a[buf][ob] = *(const pv_bf16x8*)(ldy + (ob * 32 + r32) * kDyPitch + r * 16);
 #pragma unroll
-            for (int qi = 0; qi < 4; qi++) {
-                if (boff[qi] >= 0)
-                    bfr[qi] = *(const pv_bf16x8*)(lxt + boff[qi] + (pu * 10 + pv) * 16);
-                else
-                    bfr[qi] = pv_bf16x8{0, 0, 0, 0, 0, 0, 0, 0};
-            }
+            for (int qi = 0; qi < 4; qi++)
+                bfr[buf][qi] = *(const pv_bf16x8*)(lxt + boff[qi] + (pu * 10 + pv) * 16);
+        };
+        frags(0, 0);
+#pragma unroll
+        for (int ks = 0; ks < 32; ks++) {
+            const int cur = ks & 1;
+            if (ks + 1 < 32) frags(ks + 1, cur ^ 1);
 #pragma unroll
             for (int ob = 0; ob < 2; ob++)
 #pragma unroll
                 for (int qi = 0; qi < 4; qi++)
-                    if (wave + 4 * qi < kWgPairs)
-                        acc[ob][qi] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ob], bfr[qi],
-                                                                             acc[ob][qi], 0, 0, 0);
+                    acc[ob][qi] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                        a[cur][ob], bfr[cur][qi], acc[ob][qi], 0, 0, 0);
         }
         __syncthreads();
     }
@@ -387,8 +428,8 @@ __global__ __launch_bounds__(256, 1) void pv_conv3d_wgrad_kernel(
     float* dst = part + (size_t)split * Cout * 27 * Cin;
 #pragma unroll
     for (int qi = 0; qi < 4; qi++) {
-        if (boff[qi] < 0) continue;
         const int tap = 2 * (wave + 4 * qi) + (r32 >> 4), i = i0 + (r32 & 15);
+        if (tap >= 27) continue;
 #pragma unroll
         for (int ob = 0; ob < 2; ob++)
 #pragma unroll
