@@ -1,12 +1,14 @@
 /*
- * pvconv.h -- C ABI of the MI355X (gfx950) Point-Voxel Convolution forward.
+ * pvconv.h -- C ABI of the MI355X (gfx950) Point-Voxel Convolution.
  *
  * Implements the PVConv layer of Liu, Tang, Lin, Han, "Point-Voxel CNN for
  * Efficient 3D Deep Learning" (NeurIPS 2019), Section 4: a voxel branch
  * (normalise -> voxelise -> 3x3x3 convolutions with batch normalisation and a
- * leaky rectifier -> trilinear devoxelise) and a point branch (a shared
- * per-point MLP), fused by addition. Every step runs as a HIP kernel on the
- * GPU; nothing here computes on the host.
+ * leaky rectifier -> trilinear or nearest-neighbour devoxelise) and a point
+ * branch (a shared per-point MLP), fused by addition; the per-cloud max-pool
+ * of the segmentation networks (Section 5.1); and the backward of the voxel
+ * branch's steps (the gradients at the end of this file). Every step runs as
+ * a HIP kernel on the GPU; nothing here computes on the host.
  *
  * Conventions shared by every entry point
  *  - Array pointers are DEVICE pointers owned by the caller. The library keeps
