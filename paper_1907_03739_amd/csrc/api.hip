@@ -283,20 +283,23 @@ pvconv_status pvconv_forward_ex(const float* coords, const void* feats, pvconv_d
 
     int32_t* ids = vox_id ? vox_id : w.ids;
     const float* pnorm = norm_coords ? norm_coords : w.pnorm;
-    st = ids_given ? pv_launch_voxelize_from_ids(ids, feats, feat_dt == PVCONV_BF16, feat_ld, B,
-                                                 N, L->cin, R, w.grid_a, bf, w.counts, w.vox_ws,
-                                                 s)
-                   : pv_launch_voxelize(coords, feats, feat_dt == PVCONV_BF16, feat_ld, B, N,
-                                        L->cin, R, w.grid_a, bf, w.counts, ids,
-                                        norm_coords ? norm_coords : w.pnorm, w.vox_ws, s);
-    if (st != PVCONV_OK) return st;
-    // bf16: the weights of all the convolutions repacked in one launch
-    if (bf) {
-        PvPackJobs jobs{};
+    // bf16: the weights of all the convolutions repacked by extra workgroups
+    // of the normalisation launch (or in a launch of their own when the
+    // normalisation is skipped)
+    PvPackJobs jobs{};
+    if (bf)
         for (int i = 0; i < L->n_convs; i++)
             pv_pack_job(jobs, L->conv_w[i], i ? L->cout : L->cin, L->cout, w.conv_ws[i]);
+    if (ids_given) {
         pv_launch_pack_conv_weights(jobs, s);
+        st = pv_launch_voxelize_from_ids(ids, feats, feat_dt == PVCONV_BF16, feat_ld, B, N,
+                                         L->cin, R, w.grid_a, bf, w.counts, w.vox_ws, s);
+    } else {
+        st = pv_launch_voxelize(coords, feats, feat_dt == PVCONV_BF16, feat_ld, B, N, L->cin, R,
+                                w.grid_a, bf, w.counts, ids,
+                                norm_coords ? norm_coords : w.pnorm, w.vox_ws, s, &jobs);
     }
+    if (st != PVCONV_OK) return st;
     void* src = w.grid_a;
     void* dst = w.grid_b;
     int cin = L->cin;

@@ -405,30 +405,10 @@ __global__ __launch_bounds__(256 * WCH, SB ? 2 : 1) void pv_conv3d_bf16_kernel(
 // (zero past Cin), G = Cout/32. One thread per element; one launch packs the
 // weights of all the convolutions of a layer (the blocks of job q follow those of
 // jobs 0 .. q-1).
+static_assert(kKC == kPvPackKC && kTaps == kPvPackTaps, "the packing matches the kernel");
+
 __global__ __launch_bounds__(256) void pv_pack_conv_weights_kernel(PvPackJobs jobs) {
-    int blk = blockIdx.x, q = 0;
-    while (q + 1 < jobs.n && blk >= jobs.job[q].blocks) blk -= jobs.job[q++].blocks;
-    const PvPackJob& J = jobs.job[q];
-    const int i = blk * 256 + threadIdx.x;
-    if (i >= J.total) return;
-    const int G = J.Cout / 32;
-    const int lane = i & 63;
-    int r = i >> 6;
-    const int g = r % G;
-    r /= G;
-    const int t = r % kTaps;
-    const int c = r / kTaps;
-    const int n = g * 32 + (lane & 31);
-    const int k = c * kKC + (lane >> 5) * 8;
-    const uint16_t* src = J.w + ((size_t)n * kTaps + t) * J.Cin;
-    if (J.vec) {  // Cin % 8 == 0 and 16-byte aligned rows: one load
-        J.packed[i] = k < J.Cin ? *(const uint4*)(src + k) : make_uint4(0u, 0u, 0u, 0u);
-        return;
-    }
-    uint16_t e[8];
-#pragma unroll
-    for (int j = 0; j < 8; j++) e[j] = k + j < J.Cin ? src[k + j] : (uint16_t)0;
-    J.packed[i] = pack8(e);
+    pv_pack_role(jobs, blockIdx.x);
 }
 
 // fp32 path: four consecutive lanes per output (voxel, channel), each
@@ -522,8 +502,7 @@ void pv_pack_job(PvPackJobs& jobs, const void* w, int Cin, int Cout, void* packe
 }
 
 void pv_launch_pack_conv_weights(const PvPackJobs& jobs, hipStream_t s) {
-    int blocks = 0;
-    for (int q = 0; q < jobs.n; q++) blocks += jobs.job[q].blocks;
+    const int blocks = pv_pack_blocks(jobs);
     if (blocks > 0)
         hipLaunchKernelGGL(pv_pack_conv_weights_kernel, dim3(blocks), dim3(256), 0, s, jobs);
 }

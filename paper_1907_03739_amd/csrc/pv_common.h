@@ -88,21 +88,8 @@ static inline bool pv_aligned16(const void* p) { return ((uintptr_t)p & 15u) == 
 
 static inline size_t pv_align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// ---- internal launchers (arguments already validated) ---------------------
-size_t pv_voxelize_ws_bytes(int B, int N, int R);
-pvconv_status pv_launch_voxelize(const float* coords, const void* feats, bool feat_bf16,
-                                 int feat_ld, int B, int N, int C, int R, void* grid,
-                                 bool grid_bf16, int32_t* counts, int32_t* vox_id,
-                                 float* norm_coords, void* ws, hipStream_t s);
-// the same with the voxel indices given (no normalisation)
-pvconv_status pv_launch_voxelize_from_ids(const int32_t* ids, const void* feats, bool feat_bf16,
-                                          int feat_ld, int B, int N, int C, int R, void* grid,
-                                          bool grid_bf16, int32_t* counts, void* ws,
-                                          hipStream_t s);
-size_t pv_conv3d_ws_bytes(int Cin, int Cout, bool bf16);
-// bf16 conv weights [Cout][27][Cin] repacked into the MFMA fragment order
-// (into a workspace of pv_conv3d_ws_bytes), the convolutions of a layer in one
-// launch
+// bf16 conv weights [Cout][27][Cin] repacked into the MFMA fragment order;
+// up to PVCONV_MAX_CONVS jobs per launch
 struct PvPackJob {
     const uint16_t* w;
     uint4* packed;
@@ -112,8 +99,65 @@ struct PvPackJobs {
     PvPackJob job[PVCONV_MAX_CONVS];
     int n;
 };
+
+// ---- internal launchers (arguments already validated) ---------------------
+size_t pv_voxelize_ws_bytes(int B, int N, int R);
+// pack (optional): weight-packing jobs run by extra workgroups of the
+// normalisation launch, which leaves most CUs idle (nullptr: none)
+pvconv_status pv_launch_voxelize(const float* coords, const void* feats, bool feat_bf16,
+                                 int feat_ld, int B, int N, int C, int R, void* grid,
+                                 bool grid_bf16, int32_t* counts, int32_t* vox_id,
+                                 float* norm_coords, void* ws, hipStream_t s,
+                                 const PvPackJobs* pack = nullptr);
+// the same with the voxel indices given (no normalisation)
+pvconv_status pv_launch_voxelize_from_ids(const int32_t* ids, const void* feats, bool feat_bf16,
+                                          int feat_ld, int B, int N, int C, int R, void* grid,
+                                          bool grid_bf16, int32_t* counts, void* ws,
+                                          hipStream_t s);
+size_t pv_conv3d_ws_bytes(int Cin, int Cout, bool bf16);
+// bf16 conv weights [Cout][27][Cin] repacked into the MFMA fragment order
+// (into a workspace of pv_conv3d_ws_bytes), the convolutions of a layer in one
+// launch
 void pv_pack_job(PvPackJobs& jobs, const void* w, int Cin, int Cout, void* packed);
 void pv_launch_pack_conv_weights(const PvPackJobs& jobs, hipStream_t s);
+static inline int pv_pack_blocks(const PvPackJobs& jobs) {
+    int blocks = 0;
+    for (int q = 0; q < jobs.n; q++) blocks += jobs.job[q].blocks;
+    return blocks;
+}
+// The packed layout: the convolution's MFMA A fragments in load order, for
+// input-channel chunks of kPvPackKC and the 27 taps. Workgroup blk (of
+// pv_pack_blocks) of a packing launch, 256 threads, one 16-byte piece each.
+constexpr int kPvPackKC = 16;
+constexpr int kPvPackTaps = 27;
+__device__ __forceinline__ void pv_pack_role(const PvPackJobs& jobs, int blk) {
+    int q = 0;
+    while (q + 1 < jobs.n && blk >= jobs.job[q].blocks) blk -= jobs.job[q++].blocks;
+    const PvPackJob& J = jobs.job[q];
+    const int i = blk * 256 + threadIdx.x;
+    if (i >= J.total) return;
+    const int G = J.Cout / 32;
+    const int lane = i & 63;
+    int r = i >> 6;
+    const int g = r % G;
+    r /= G;
+    const int t = r % kPvPackTaps;
+    const int c = r / kPvPackTaps;
+    const int n = g * 32 + (lane & 31);
+    const int k = c * kPvPackKC + (lane >> 5) * 8;
+    const uint16_t* src = J.w + ((size_t)n * kPvPackTaps + t) * J.Cin;
+    if (J.vec) {  // Cin % 8 == 0 and 16-byte aligned rows: one load
+        J.packed[i] = k < J.Cin ? *(const uint4*)(src + k) : make_uint4(0u, 0u, 0u, 0u);
+        return;
+    }
+    uint16_t e[8];
+#pragma unroll
+    for (int j = 0; j < 8; j++) e[j] = k + j < J.Cin ? src[k + j] : (uint16_t)0;
+    J.packed[i] = make_uint4((uint32_t)e[0] | ((uint32_t)e[1] << 16),
+                             (uint32_t)e[2] | ((uint32_t)e[3] << 16),
+                             (uint32_t)e[4] | ((uint32_t)e[5] << 16),
+                             (uint32_t)e[6] | ((uint32_t)e[7] << 16));
+}
 // packed: the bf16 weights are already repacked in ws (w is then unused)
 pvconv_status pv_launch_conv3d(const void* x, int B, int R, int Cin, int Cout, const void* w,
                                const PvBnFold& bn, int act, float slope, bool bf16, void* y,

@@ -257,17 +257,24 @@ __device__ void ids_role(const float* __restrict__ coords, int N, int R, int sli
     }
 }
 
-// One launch, two roles: the first B * slices workgroups normalise (slice
-// blockIdx % slices of cloud blockIdx / slices), the rest zero the grid.
+// One launch, three roles: the first B * slices workgroups normalise (slice
+// blockIdx % slices of cloud blockIdx / slices), the next npack repack conv
+// weights (a layer's convolutions, independent work that fills CUs the
+// normalisation leaves idle), the rest zero the grid.
 template <int PPT>
 __global__ __launch_bounds__(256) void pv_voxel_ids_kernel(const float* __restrict__ coords,
                                                            int N, int R, int slices, int nid,
                                                            int32_t* __restrict__ vox_id,
                                                            float* __restrict__ norm_coords,
-                                                           uint4* __restrict__ grid16, size_t n16) {
+                                                           uint4* __restrict__ grid16, size_t n16,
+                                                           PvPackJobs pack, int npack) {
     const int bid = blockIdx.x;
+    if (bid >= nid + npack) {
+        zero_fill_role(grid16, n16, bid - nid - npack, gridDim.x - nid - npack);
+        return;
+    }
     if (bid >= nid) {
-        zero_fill_role(grid16, n16, bid - nid, gridDim.x - nid);
+        pv_pack_role(pack, bid - nid);
         return;
     }
     ids_role<PPT>(coords, N, R, bid % slices, bid / slices, vox_id, norm_coords);
@@ -322,15 +329,20 @@ __device__ void combine_centroid(const SplitWs& ws, int b, int N, float* redf, l
     for (int a = 0; a < 3; a++) c[a] = centroid_from_sum(q[a], fixed_scale(A[a], N), A[a], N);
 }
 
-// Grid (G * B + zero workgroups): the first G * B compute abs-max partials,
-// the rest zero the grid.
+// Grid (G * B + npack + zero workgroups): the first G * B compute abs-max
+// partials, the next npack repack conv weights, the rest zero the grid.
 __global__ __launch_bounds__(kNormThreads) void pv_norm_absmax_kernel(const float* coords, int N,
                                                                       SplitWs ws, int B,
-                                                                      uint4* grid16, size_t n16) {
+                                                                      uint4* grid16, size_t n16,
+                                                                      PvPackJobs pack, int npack) {
     __shared__ float redf[3 * kNormThreads / 64];
     const int nid = ws.G * B;
+    if ((int)blockIdx.x >= nid + npack) {
+        zero_fill_role(grid16, n16, blockIdx.x - nid - npack, gridDim.x - nid - npack);
+        return;
+    }
     if ((int)blockIdx.x >= nid) {
-        zero_fill_role(grid16, n16, blockIdx.x - nid, gridDim.x - nid);
+        pv_pack_role(pack, blockIdx.x - nid);
         return;
     }
     if (blockIdx.x == 0) {  // the tile counters start at zero (used two launches later)
@@ -1400,8 +1412,14 @@ pvconv_status voxelize_fill(const int32_t* ids, const void* feats, bool feat_bf1
 pvconv_status pv_launch_voxelize(const float* coords, const void* feats, bool feat_bf16,
                                  int feat_ld, int B, int N, int C, int R, void* grid,
                                  bool grid_bf16, int32_t* counts, int32_t* vox_id,
-                                 float* norm_coords, void* ws, hipStream_t s) {
-    if (B == 0) return PVCONV_OK;
+                                 float* norm_coords, void* ws, hipStream_t s,
+                                 const PvPackJobs* pack) {
+    const PvPackJobs jobs = pack ? *pack : PvPackJobs{};
+    const int npack = pv_pack_blocks(jobs);
+    if (B == 0) {
+        pv_launch_pack_conv_weights(jobs, s);
+        return pv_launch_status();
+    }
     VoxWs w = carve_ws(ws, B, N, R, nullptr);
     int32_t* ids = vox_id ? vox_id : w.ids;
     float* pn = norm_coords ? norm_coords : w.pnorm;
@@ -1416,23 +1434,23 @@ pvconv_status pv_launch_voxelize(const float* coords, const void* feats, bool fe
     if (N <= kSmallMaxN) {
         const int slices = (N + 255) / 256;
         const int nid = slices * B;
-        if (nid + zb > 0) {
-            const dim3 gi(nid + zb);
+        if (nid + npack + zb > 0) {
+            const dim3 gi(nid + npack + zb);
             if (N <= 1024)
                 hipLaunchKernelGGL(pv_voxel_ids_kernel<4>, gi, dim3(256), 0, s, coords, N, R,
-                                   slices, nid, ids, pn, grid16, n16);
+                                   slices, nid, ids, pn, grid16, n16, jobs, npack);
             else if (N <= 2048)
                 hipLaunchKernelGGL(pv_voxel_ids_kernel<8>, gi, dim3(256), 0, s, coords, N, R,
-                                   slices, nid, ids, pn, grid16, n16);
+                                   slices, nid, ids, pn, grid16, n16, jobs, npack);
             else
                 hipLaunchKernelGGL(pv_voxel_ids_kernel<16>, gi, dim3(256), 0, s, coords, N, R,
-                                   slices, nid, ids, pn, grid16, n16);
+                                   slices, nid, ids, pn, grid16, n16, jobs, npack);
         }
     } else {
         const int nid = w.split.G * B;
         dim3 g(w.split.G, B);
-        hipLaunchKernelGGL(pv_norm_absmax_kernel, dim3(nid + zb), dim3(kNormThreads), 0, s,
-                           coords, N, w.split, B, grid16, n16);
+        hipLaunchKernelGGL(pv_norm_absmax_kernel, dim3(nid + npack + zb), dim3(kNormThreads), 0,
+                           s, coords, N, w.split, B, grid16, n16, jobs, npack);
         hipLaunchKernelGGL(pv_norm_sum_kernel, g, dim3(kNormThreads), 0, s, coords, N, w.split);
         hipLaunchKernelGGL(pv_norm_radius_kernel, g, dim3(kNormThreads), 0, s, coords, N, w.split);
         hipLaunchKernelGGL(pv_norm_points_kernel, g, dim3(kNormThreads),
