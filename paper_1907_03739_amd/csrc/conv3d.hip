@@ -15,15 +15,16 @@
 //    inputs; WCH = 2 (eight waves, two per SIMD, so that one wave's waits
 //    overlap the other's MFMAs) for 64-channel tiles of narrow inputs on
 //    small grids. Inputs of up to 128 channels on grids with enough tiles
-//    take 64-channel tiles single-buffered (SB): 72 KB of LDS and at most
-//    128 accumulator registers per wave, so two workgroups share a CU and
-//    one's prologue and epilogue overlap the other's MFMAs.
+//    take 64-channel tiles with compact halos (SB): 72 KB of LDS and at
+//    most 128 accumulator registers per wave, so two workgroups share a CU
+//    and one's prologue and epilogue overlap the other's MFMAs.
 //  * The input is consumed in chunks of 16 channels (one MFMA k step). A
 //    chunk's 10x10x10 halo (zero outside the grid) sits in LDS at 48 bytes per
 //    voxel (32 bytes of data) and 640 bytes per 10-voxel row: with that
-//    padding the 16-byte fragment reads of every tap hit distinct banks. The
-//    next chunk's halo is fetched into the other of two buffers during the
-//    first taps of the current chunk.
+//    padding the 16-byte fragment reads of every tap hit distinct banks (SB:
+//    32 bytes per voxel, the two halves swapped where bit 2 of w is set, the
+//    same effect). The next chunk's halo is fetched into the other of two
+//    buffers during the first taps of the current chunk.
 //  * The 27 taps of a chunk are unrolled, so every LDS fragment address is a
 //    per-lane base plus an immediate. Weights come pre-packed in fragment
 //    order (pv_pack_conv_weights_kernel): each fragment load is one coalesced
@@ -54,11 +55,18 @@ constexpr int kOOB = 0x40000000;                   // byte offset always out of 
 constexpr int kStageRow = 256 + 16;
 constexpr int kStageBytes = kBrick * kBrick * kBrick * kStageRow;  // 139264
 constexpr int kLdsBytes = kStageBytes > 2 * kHaloBytes ? kStageBytes : 2 * kHaloBytes;
-// Single-buffered variant (two workgroups per CU): one halo buffer; the
-// epilogue stages the 64-channel tile through LDS in one pass (bf16: whole
-// 128-byte halves of the output rows) or two (fp32).
+// Two-workgroups-per-CU variant (SB): the epilogue stages the 64-channel
+// tile through LDS in one pass (bf16: whole 128-byte halves of the output
+// rows) or two (fp32). Its two halo buffers are compact: 32 bytes per voxel, 320 per row, and the
+// two 16-byte halves of a voxel swap places where bit 2 of its w is set, so
+// that the eight consecutive voxels of one fragment read still hit distinct
+// banks.
 constexpr int kStageRowSB = 128 + 16;
-constexpr int kLdsBytesSB = 512 * kStageRowSB > kHaloBytes ? 512 * kStageRowSB : kHaloBytes;
+constexpr int kVoxPitchSB = 32;
+constexpr int kRowPitchSB = kHalo * kVoxPitchSB;                 // 320
+constexpr int kHaloBytesSB = kHalo * kHalo * kRowPitchSB;        // 32000 per buffer
+constexpr int kLdsBytesSB =
+    512 * kStageRowSB > 2 * kHaloBytesSB ? 512 * kStageRowSB : 2 * kHaloBytesSB;
 
 __device__ __forceinline__ uint4 pack8(const uint16_t* e) {
     return make_uint4((uint32_t)e[0] | ((uint32_t)e[1] << 16), (uint32_t)e[2] | ((uint32_t)e[3] << 16),
@@ -97,10 +105,9 @@ __device__ __forceinline__ uint4 bload8_elems(__amdgpu_buffer_rsrc_t r, int voff
 }
 
 // WCH channel groups of waves: 1 (four waves, 256 threads) or 2 (eight
-// waves, two per SIMD). SB: one halo buffer (the next chunk's halo waits in
-// registers until the current chunk is done) and at most 128 accumulator
-// registers, so that two workgroups share a CU and one's prologue and
-// epilogue overlap the other's MFMAs.
+// waves, two per SIMD). SB: compact halo buffers and at most 128
+// accumulator registers, so that two workgroups share a CU and one's
+// prologue and epilogue overlap the other's MFMAs.
 template <int NB, int WCH, bool VEC, bool SB = false>
 __global__ __launch_bounds__(256 * WCH, SB ? 2 : 1) void pv_conv3d_bf16_kernel(
     const uint16_t* __restrict__ x, const uint16_t* __restrict__ wpk, PvBnFold bn, int act,
@@ -138,12 +145,25 @@ __global__ __launch_bounds__(256 * WCH, SB ? 2 : 1) void pv_conv3d_bf16_kernel(
     // LDS byte address of this lane's B fragment (voxel column r32 of block
     // mb, channels khalf*8 .. +7) at tap offset (0,0,0) in buffer 0: block mb
     // covers u = 2*wave + mb/2 and v rows (mb&1)*4 .. +3, eight w each.
-    int bbase[4];
+    // SB: one base per w shift of the taps (the half swap depends on w).
+    constexpr int RP = SB ? kRowPitchSB : kRowPitch, HB = SB ? kHaloBytesSB : kHaloBytes;
+    auto half_off = [](int hw, int h) { return SB ? (h ^ ((hw >> 2) & 1)) * 16 : h * 16; };
+    int bbase[4], bsw[4][3];
 #pragma unroll
     for (int mb = 0; mb < 4; mb++) {
         const int ul = 2 * wv + (mb >> 1), vl = (mb & 1) * 4 + (r32 >> 3), wl = r32 & 7;
         bbase[mb] = (ul * kHalo + vl) * kRowPitch + wl * kVoxPitch + khalf * 16;
+#pragma unroll
+        for (int tw = 0; tw < 3; tw++)
+            bsw[mb][tw] = (ul * kHalo + vl) * kRowPitchSB + (wl + tw) * kVoxPitchSB +
+                          half_off(wl + tw, khalf);
     }
+    // LDS byte address (in buffer 0) of block mb's B fragment at tap tn
+    auto frag_addr = [&](int mb, int tn) {
+        const int tu = tn / 9, tv = (tn / 3) % 3, tw = tn % 3;
+        if constexpr (SB) return bsw[mb][tw] + (tu * kHalo + tv) * RP;
+        return bbase[mb] + (tu * kHalo + tv) * kRowPitch + tw * kVoxPitch;
+    };
 
     // Halo pieces of this thread: piece p = set*NTH + tid is voxel p/2 (as
     // (hu,hv,hw) of the 10x10x10 halo), channels (p%2)*8 .. +7 of the chunk.
@@ -163,7 +183,8 @@ __global__ __launch_bounds__(256 * WCH, SB ? 2 : 1) void pv_conv3d_bf16_kernel(
         const int gu = u0 + hu - 1, gv = v0 + hv - 1, gw = w0 + hw - 1;
         const bool in = gu >= 0 && gu < R && gv >= 0 && gv < R && gw >= 0 && gw < R;
         goff[set] = in ? ((((gu - ulo) * R + gv) * R + gw) * Cin + pq * 8) * 2 : kOOB;
-        loff[set] = (hu * kHalo + hv) * kRowPitch + hw * kVoxPitch + pq * 16;
+        loff[set] = SB ? (hu * kHalo + hv) * kRowPitchSB + hw * kVoxPitchSB + half_off(hw, pq)
+                       : (hu * kHalo + hv) * kRowPitch + hw * kVoxPitch + pq * 16;
     }
     // Piece of set `set` for the chunk starting at channel cc: pieces whose
     // channels lie past Cin read as zero.
@@ -215,59 +236,17 @@ __global__ __launch_bounds__(256 * WCH, SB ? 2 : 1) void pv_conv3d_bf16_kernel(
     // other LDS buffer at tap s+4. One loop body for every chunk keeps the
     // accumulators in the same registers throughout.
     constexpr int kHaloLag = 4;
-    if constexpr (SB) {
-        // One buffer: piece set s of the next chunk's halo is loaded at tap s
-        // into hr[s] and stored once every wave is done with the chunk.
-        uint4 hr[kSets];
-        for (int c = 0; c < nch; c++) {
-            const bool more = c + 1 < nch;
-            const int cn = (more ? c + 1 : c) * kKC;
-            pv_bf16x8 bf[2][4];
-#pragma unroll
-            for (int mb = 0; mb < 4; mb++) bf[0][mb] = *(const pv_bf16x8*)(lds + bbase[mb]);
-#pragma unroll
-            for (int t = 0; t < kTaps; t++) {
-                const int cur = t & 1, nxt = cur ^ 1;
-                if (t + 2 < kTaps)
-                    load_w(c, t + 2, wf[(t + 2) % 3]);
-                else
-                    load_w(c + 1, t + 2 - kTaps, wf[(t + 2) % 3]);
-                if (t < kSets && more) hr[t] = halo_load(t, cn);
-                if (t + 1 < kTaps) {
-                    const int tn = t + 1;
-                    const int toff = (tn / 9) * kHalo * kRowPitch + ((tn / 3) % 3) * kRowPitch +
-                                     (tn % 3) * kVoxPitch;
-#pragma unroll
-                    for (int mb = 0; mb < 4; mb++)
-                        bf[nxt][mb] = *(const pv_bf16x8*)(lds + bbase[mb] + toff);
-                }
-#pragma unroll
-                for (int mb = 0; mb < 4; mb++)
-#pragma unroll
-                    for (int nb = 0; nb < NBW; nb++)
-                        acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                            wf[t % 3][nb], bf[cur][mb], acc[mb][nb], 0, 0, 0);
-                __builtin_amdgcn_sched_barrier(0);
-            }
-            pv_lds_barrier();  // every wave is done reading the chunk
-            if (more) {
-#pragma unroll
-                for (int set = 0; set < kSets; set++) *(uint4*)(lds + loff[set]) = hr[set];
-                pv_lds_barrier();  // the next chunk's halo is in place (its loads are
-                                   // done: the stores above used them)
-            }
-        }
-    }
-    for (int c = 0; !SB && c < nch; c++) {
-        const int cur_off = (c & 1) * kHaloBytes, nxt_off = kHaloBytes - cur_off;
-        int rb[4];
-#pragma unroll
-        for (int mb = 0; mb < 4; mb++) rb[mb] = bbase[mb] + cur_off;
-        const int cn = (c + 1 < nch ? c + 1 : c) * kKC;  // last chunk reloads itself
+    for (int c = 0; c < nch; c++) {
+        const int cur_off = (c & 1) * HB, nxt_off = HB - cur_off;
+        // SB skips the last chunk's halo prefetch; the double-buffered
+        // variant reloads the last chunk into the idle buffer
+        const bool fetch = !SB || c + 1 < nch;
+        const int cn = (c + 1 < nch ? c + 1 : c) * kKC;
         pv_bf16x8 bf[2][4];
         uint4 hr[kHaloLag];
 #pragma unroll
-        for (int mb = 0; mb < 4; mb++) bf[0][mb] = *(const pv_bf16x8*)(lds + rb[mb]);
+        for (int mb = 0; mb < 4; mb++)
+            bf[0][mb] = *(const pv_bf16x8*)(lds + frag_addr(mb, 0) + cur_off);
 #pragma unroll
         for (int t = 0; t < kTaps; t++) {
             const int cur = t & 1, nxt = cur ^ 1;
@@ -275,16 +254,13 @@ __global__ __launch_bounds__(256 * WCH, SB ? 2 : 1) void pv_conv3d_bf16_kernel(
                 load_w(c, t + 2, wf[(t + 2) % 3]);
             else
                 load_w(c + 1, t + 2 - kTaps, wf[(t + 2) % 3]);
-            if (t >= kHaloLag && t < kSets + kHaloLag)
+            if (fetch && t >= kHaloLag && t < kSets + kHaloLag)
                 *(uint4*)(lds + loff[t - kHaloLag] + nxt_off) = hr[(t - kHaloLag) % kHaloLag];
-            if (t < kSets) hr[t % kHaloLag] = halo_load(t, cn);
+            if (fetch && t < kSets) hr[t % kHaloLag] = halo_load(t, cn);
             if (t + 1 < kTaps) {
-                const int tn = t + 1;
-                const int toff = (tn / 9) * kHalo * kRowPitch + ((tn / 3) % 3) * kRowPitch +
-                                 (tn % 3) * kVoxPitch;
 #pragma unroll
                 for (int mb = 0; mb < 4; mb++)
-                    bf[nxt][mb] = *(const pv_bf16x8*)(lds + rb[mb] + toff);
+                    bf[nxt][mb] = *(const pv_bf16x8*)(lds + frag_addr(mb, t + 1) + cur_off);
             }
 #pragma unroll
             for (int mb = 0; mb < 4; mb++)
@@ -294,7 +270,11 @@ __global__ __launch_bounds__(256 * WCH, SB ? 2 : 1) void pv_conv3d_bf16_kernel(
                         wf[t % 3][nb], bf[cur][mb], acc[mb][nb], 0, 0, 0);
             __builtin_amdgcn_sched_barrier(0);
         }
-        __syncthreads();  // chunk done: next halo complete, this buffer free
+        // chunk done: the next halo is complete and this buffer is free
+        if constexpr (SB)
+            pv_lds_barrier();  // LDS only: the weight prefetch stays in flight
+        else
+            __syncthreads();
     }
 
     // Epilogue. Block (mb, nb) holds D[n][voxel]: lane has voxel column r32
@@ -524,7 +504,7 @@ pvconv_status pv_launch_conv3d(const void* x, int B, int R, int Cin, int Cout, c
         const int nbr = (R + kBrick - 1) / kBrick;
         const long bricks = (long)B * nbr * nbr * nbr;
         // Inputs of up to 128 channels with enough tiles for two workgroups
-        // per CU: 64-channel tiles, single-buffered, two per CU (one's
+        // per CU: 64-channel tiles with compact halos, two per CU (one's
         // prologue and epilogue overlap the other's MFMAs: 11 % faster at
         // 64->128 and 64->64, 2.5 % at 128->128, than one 128-channel
         // workgroup per CU). Otherwise four waves (one per SIMD, 128 channels
