@@ -57,14 +57,16 @@ constexpr int kStageBytes = kBrick * kBrick * kBrick * kStageRow;  // 139264
 constexpr int kLdsBytes = kStageBytes > 2 * kHaloBytes ? kStageBytes : 2 * kHaloBytes;
 // Two-workgroups-per-CU variant (SB): the epilogue stages the 64-channel
 // tile through LDS in one pass (bf16: whole 128-byte halves of the output
-// rows) or two (fp32). Its two halo buffers are compact: 32 bytes per voxel, 320 per row, and the
-// two 16-byte halves of a voxel swap places where bit 2 of its w is set, so
-// that the eight consecutive voxels of one fragment read still hit distinct
-// banks.
+// rows) or two (fp32). Its two halo buffers are compact: 32 bytes per
+// voxel, 384 per 10-voxel row (64 bytes of padding: consecutive rows start
+// half a 256-byte bank window apart), and the two 16-byte halves of a voxel
+// swap places where bit 2 of its w is set, so that the 16 lanes of a
+// fragment read that are served together (8 consecutive voxels of two
+// consecutive rows) hit distinct banks.
 constexpr int kStageRowSB = 128 + 16;
 constexpr int kVoxPitchSB = 32;
-constexpr int kRowPitchSB = kHalo * kVoxPitchSB;                 // 320
-constexpr int kHaloBytesSB = kHalo * kHalo * kRowPitchSB;        // 32000 per buffer
+constexpr int kRowPitchSB = kHalo * kVoxPitchSB + 64;            // 384
+constexpr int kHaloBytesSB = kHalo * kHalo * kRowPitchSB;        // 38400 per buffer
 constexpr int kLdsBytesSB =
     512 * kStageRowSB > 2 * kHaloBytesSB ? 512 * kStageRowSB : 2 * kHaloBytesSB;
 
