@@ -313,6 +313,15 @@ pvconv_status pvconv_forward_ex(const float* coords, const void* feats, pvconv_d
         dst = t;
         cin = L->cout;
     }
+    // bf16 trilinear: the devoxelisation runs inside the point-MLP kernel
+    if (bf && L->devox == PVCONV_DEVOX_TRILINEAR) {
+        st = pv_launch_devox_point_mlp(PvDevoxIn{(const uint16_t*)src, pnorm, N, R}, feats,
+                                       feat_dt == PVCONV_BF16, feat_ld, B * N, L->cin, L->cout,
+                                       L->mlp_w, pv_make_fold(&L->mlp_bn, L->mlp_b),
+                                       PVCONV_ACT_RELU, 0.f, out, out_dt == PVCONV_BF16, out_ld,
+                                       s);
+        if (st != PVCONV_ENOTSUP) return st;
+    }
     st = L->devox == PVCONV_DEVOX_NEAREST
              ? pv_launch_devoxelize_nearest(src, B, R, L->cout, bf, ids, N, w.devox, s)
              : pv_launch_devoxelize(src, B, R, L->cout, bf, pnorm, N, w.devox, s);

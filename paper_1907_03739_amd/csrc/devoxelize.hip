@@ -10,46 +10,9 @@
 // (i + 1/2) / R, border cells replicated). Each XCD takes a contiguous range
 // of points (a few clouds), so that its L2 holds the rows those clouds touch.
 #include "pv_common.h"
+#include "pv_trilinear.h"
 
 namespace {
-
-// Cell indices and weights along one axis. The cell coordinate and the
-// weights are formed in fp64 (this kernel is bound by memory, not ALU), so the
-// only fp32 rounding left is the weighted sum itself.
-struct Axis {
-    int i0, i1;
-    double w0, w1;
-};
-
-__device__ __forceinline__ Axis trilinear_axis(float x, int R) {
-    double t = (double)x * (double)R - 0.5;
-    t = fmin(fmax(t, 0.0), (double)(R - 1));  // also maps NaN to 0
-    const double f = floor(t);
-    Axis a;
-    a.i0 = (int)f;
-    a.i1 = min(a.i0 + 1, R - 1);
-    a.w1 = t - f;
-    a.w0 = 1.0 - a.w1;
-    return a;
-}
-
-template <typename GT>
-__device__ __forceinline__ void fma8(const GT* src, float wt, float* acc);
-template <>
-__device__ __forceinline__ void fma8<float>(const float* src, float wt, float* acc) {
-    const float4 a = *(const float4*)src, b = *(const float4*)(src + 4);
-    acc[0] += wt * a.x; acc[1] += wt * a.y; acc[2] += wt * a.z; acc[3] += wt * a.w;
-    acc[4] += wt * b.x; acc[5] += wt * b.y; acc[6] += wt * b.z; acc[7] += wt * b.w;
-}
-template <>
-__device__ __forceinline__ void fma8<uint16_t>(const uint16_t* src, float wt, float* acc) {
-    const uint4 a = *(const uint4*)src;
-    const uint32_t w[4] = {a.x, a.y, a.z, a.w};
-    for (int i = 0; i < 4; i++) {
-        acc[2 * i] += wt * pv_bf16_to_f32((uint16_t)(w[i] & 0xffffu));
-        acc[2 * i + 1] += wt * pv_bf16_to_f32((uint16_t)(w[i] >> 16));
-    }
-}
 
 template <typename GT>
 __device__ __forceinline__ float load1(const GT* p);
@@ -77,24 +40,12 @@ __global__ __launch_bounds__(256) void pv_devoxelize_kernel(const GT* __restrict
     const size_t b = point / N;
     const size_t V = (size_t)R * R * R;
     const float* p = pn + point * 3;
-    const Axis ax = trilinear_axis(p[0], R), ay = trilinear_axis(p[1], R),
-               az = trilinear_axis(p[2], R);
+    const PvAxis ax = pv_trilinear_axis(p[0], R), ay = pv_trilinear_axis(p[1], R),
+                 az = pv_trilinear_axis(p[2], R);
     const GT* base = grid + b * V * C;
     if (VEC) {
-        float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-        for (int a = 0; a < 2; a++) {
-            const int iu = a ? ax.i1 : ax.i0;
-            const double wu = a ? ax.w1 : ax.w0;
-            for (int e = 0; e < 2; e++) {
-                const int iv = e ? ay.i1 : ay.i0;
-                const double wv = e ? ay.w1 : ay.w0;
-                for (int f = 0; f < 2; f++) {
-                    const int iw = f ? az.i1 : az.i0;
-                    const float wt = (float)((wu * wv) * (f ? az.w1 : az.w0));
-                    fma8<GT>(base + (((size_t)iu * R + iv) * R + iw) * C + g * 8, wt, acc);
-                }
-            }
-        }
+        float acc[8];
+        pv_trilinear8<GT>(base + g * 8, C, R, ax, ay, az, acc);
         float* o = out + point * C + g * 8;
         *(float4*)o = make_float4(acc[0], acc[1], acc[2], acc[3]);
         *(float4*)(o + 4) = make_float4(acc[4], acc[5], acc[6], acc[7]);

@@ -15,6 +15,7 @@
 // (ragged or unaligned C_in) or read and write channel by channel (ragged
 // C_out or unaligned rows).
 #include "pv_common.h"
+#include "pv_trilinear.h"
 
 namespace {
 
@@ -94,14 +95,31 @@ struct RawOf<uint16_t> {
 // past Cin. C4 (checked by the launcher): Cout % 4 == 0, residual / cloud
 // rows 16-byte aligned, output rows 16-byte (fp32) or 8-byte (bf16) aligned;
 // else the epilogue reads and writes channel by channel.
-template <int NB, typename XT, bool VEC, bool C4>
+//
+// DV: the residual is the trilinear devoxelisation of a bf16 grid (Section
+// 4.1), gathered by this kernel instead of read as rows of a separate
+// launch's output: the workgroup's 128 points x (32*NB) channels are summed
+// into LDS (fp32, the same arithmetic and order as the devoxelisation kernel,
+// so the result is the same bits) by all four waves before the GEMM. (Four
+// more waves gathering while the GEMM waves load and multiply measured
+// slower: two waves per SIMD leave room for only two items' loads in flight.)
+// Requires C4, Cout % 8 == 0 and a 16-byte aligned grid.
+template <int NB, typename XT, bool VEC, bool C4, bool DV = false>
 __global__ __launch_bounds__(kWaves * 64) void pv_point_mlp_tile_kernel(
     const XT* __restrict__ x, int x_ld, int M, int Cin, int Cout, const uint16_t* __restrict__ w,
     PvBnFold bn, int act, float slope, const float* __restrict__ cloud_bias, int ppc,
     const float* __restrict__ residual, int res_ld, void* __restrict__ out, int out_bf16,
-    int out_ld) {
+    int out_ld, PvDevoxIn dvin) {
     __shared__ float4 tab[2][NB * 8];  // folded scale / shift, 4 channels per entry
+    // DV: the devoxelised rows of the workgroup's points, padded by 4 floats
+    // so that the 32 rows read by one instruction start in different banks
+    constexpr int kDvLd = NB * 32 + 4;
+    __shared__ __attribute__((aligned(16))) float dvrow[DV ? kWaves * 32 : 1][DV ? kDvLd : 1];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    // DV: each XCD takes a contiguous range of points (a few clouds), so that
+    // the corner rows nearby points share are fetched into one L2
+    int bx = blockIdx.x;
+    if (DV && (gridDim.x & 7) == 0) bx = (bx & 7) * (gridDim.x >> 3) + (bx >> 3);
     const int n0 = blockIdx.y * (NB * 32);
     const int ncols = min(NB * 32, Cout - n0);
     if (threadIdx.x < NB * 32) {
@@ -111,8 +129,43 @@ __global__ __launch_bounds__(kWaves * 64) void pv_point_mlp_tile_kernel(
         ((float*)tab[0])[threadIdx.x] = sc;
         ((float*)tab[1])[threadIdx.x] = sh;
     }
+    if constexpr (DV) {
+        // Items (point, 8-channel group): consecutive lanes take consecutive
+        // groups of one point, so each corner row is read contiguously. NB*2
+        // items per thread (fewer valid ones in a ragged last channel block),
+        // in rounds of up to four whose 32 corner loads are all in flight
+        // together: one workgroup per CU has to cover the memory latency.
+        const int tid = threadIdx.x;
+        const int G = ncols >> 3, items = kWaves * 32 * G;
+        const size_t V = (size_t)dvin.R * dvin.R * dvin.R;
+        constexpr int kIPT = NB * 2, kRound = kIPT < 4 ? kIPT : 4;
+#pragma unroll
+        for (int r = 0; r < kIPT; r += kRound) {
+            float a[kRound][8];
+#pragma unroll
+            for (int u = 0; u < kRound; u++) {
+                const int i = min(tid + (r + u) * kWaves * 64, items - 1);
+                const int pl = i / G, g = i - pl * G;
+                const int m = min(bx * kWaves * 32 + pl, M - 1);
+                const float* p = dvin.pn + (size_t)m * 3;
+                const PvAxis ax = pv_trilinear_axis(p[0], dvin.R),
+                             ay = pv_trilinear_axis(p[1], dvin.R),
+                             az = pv_trilinear_axis(p[2], dvin.R);
+                pv_trilinear8<uint16_t>(dvin.grid + (size_t)(m / dvin.N) * V * Cout + n0 + g * 8,
+                                        Cout, dvin.R, ax, ay, az, a[u]);
+            }
+#pragma unroll
+            for (int u = 0; u < kRound; u++) {
+                const int i = tid + (r + u) * kWaves * 64;
+                if (i >= items) continue;
+                const int pl = i / G, g = i - pl * G;
+                *(float4*)&dvrow[pl][g * 8] = make_float4(a[u][0], a[u][1], a[u][2], a[u][3]);
+                *(float4*)&dvrow[pl][g * 8 + 4] = make_float4(a[u][4], a[u][5], a[u][6], a[u][7]);
+            }
+        }
+    }
     __syncthreads();
-    const int m0 = (blockIdx.x * kWaves + wave) * 32;
+    const int m0 = (bx * kWaves + wave) * 32;
     if (m0 >= M) return;
     const int r32 = lane & 31, h = lane >> 5;
     // Rows past M are clamped onto the last row: they compute values that are
@@ -144,7 +197,13 @@ __global__ __launch_bounds__(kWaves * 64) void pv_point_mlp_tile_kernel(
 
     // The residual rows go in flight first: they are consumed last.
     float4 res[NB][4];
-    if (residual) {
+    if constexpr (DV) {
+#pragma unroll
+        for (int nb = 0; nb < NB; nb++)
+#pragma unroll
+            for (int g = 0; g < 4; g++)
+                res[nb][g] = *(const float4*)&dvrow[wave * 32 + r32][coff[nb][g] - n0];
+    } else if (residual) {
         const float* rr = residual + (size_t)m * res_ld;
 #pragma unroll
         for (int nb = 0; nb < NB; nb++)
@@ -518,7 +577,7 @@ void launch_mfma(const void* x, int x_ld, int M, int Cin, int Cout, const void* 
 #define PV_TILE(V, C)                                                                         \
     hipLaunchKernelGGL((pv_point_mlp_tile_kernel<NB, XT, V, C>), g, dim3(kWaves * 64), 0, s, \
                        (const XT*)x, x_ld, M, Cin, Cout, (const uint16_t*)w, bn, act, slope,   \
-                       cb, ppc, res, res_ld, out, (int)out_bf16, out_ld)
+                       cb, ppc, res, res_ld, out, (int)out_bf16, out_ld, PvDevoxIn{})
     if (vec) {
         if (c4) PV_TILE(true, true); else PV_TILE(true, false);
     } else {
@@ -796,6 +855,32 @@ pvconv_status pv_launch_point_mlp(const void* x, bool x_bf16, int x_ld, int M, i
                                (const float*)x, x_ld, M, Cin, Cout, (const float*)w, bn, act,
                                slope, cb, ppc, res, res_ld, out, (int)out_bf16, out_ld);
     }
+    return pv_launch_status();
+}
+
+pvconv_status pv_launch_devox_point_mlp(const PvDevoxIn& dv, const void* x, bool x_bf16,
+                                        int x_ld, int M, int Cin, int Cout, const void* w,
+                                        const PvBnFold& bn, int act, float slope, void* out,
+                                        bool out_bf16, int out_ld, hipStream_t s) {
+    const size_t esz = x_bf16 ? 2 : 4;
+    // the shapes the unfused path runs on the tile kernel with vector access
+    const bool ok = M >= kWaves * 32 && Cin % 8 == 0 && pv_aligned16(x) && pv_aligned16(w) &&
+                    ((size_t)x_ld * esz) % 16 == 0 && Cout % 8 == 0 && out_ld % 4 == 0 &&
+                    ((uintptr_t)out & (out_bf16 ? 7u : 15u)) == 0 && pv_aligned16(dv.grid) &&
+                    !(Cin >= 128 && Cout >= 128) && dv.N > 0 && M % dv.N == 0;
+    if (!ok) return PVCONV_ENOTSUP;
+#define PV_DV(NB, XT)                                                                         \
+    hipLaunchKernelGGL((pv_point_mlp_tile_kernel<NB, XT, true, true, true>),                  \
+                       dim3((M + kWaves * 32 - 1) / (kWaves * 32), (Cout + NB * 32 - 1) / (NB * 32)), \
+                       dim3(kWaves * 64), 0, s, (const XT*)x, x_ld, M, Cin, Cout,              \
+                       (const uint16_t*)w, bn, act, slope, nullptr, 1, nullptr, 0, out,         \
+                       (int)out_bf16, out_ld, dv)
+    if (x_bf16) {
+        if (Cout > 64) PV_DV(4, uint16_t); else PV_DV(2, uint16_t);
+    } else {
+        if (Cout > 64) PV_DV(4, float); else PV_DV(2, float);
+    }
+#undef PV_DV
     return pv_launch_status();
 }
 

@@ -167,6 +167,22 @@ pvconv_status pv_launch_devoxelize(const void* grid, int B, int R, int C, bool g
 pvconv_status pv_launch_devoxelize_nearest(const void* grid, int B, int R, int C, bool grid_bf16,
                                            const int32_t* ids, int N, float* out,
                                            hipStream_t s);
+// The voxel branch of a PVConv layer as the point MLP's residual: a bf16 grid
+// [B][R^3][Cout] devoxelised trilinearly at the normalised coordinates pn
+// [B*N][3] (N points per cloud).
+struct PvDevoxIn {
+    const uint16_t* grid;
+    const float* pn;
+    int N, R;
+};
+// Point MLP whose residual is that devoxelisation, gathered inside the GEMM
+// kernel (one launch instead of two, no fp32 intermediate). Returns
+// PVCONV_ENOTSUP for shapes it does not take; the caller then runs the
+// devoxelisation and the point MLP separately.
+pvconv_status pv_launch_devox_point_mlp(const PvDevoxIn& dv, const void* x, bool x_bf16,
+                                        int x_ld, int M, int Cin, int Cout, const void* w,
+                                        const PvBnFold& bn, int act, float slope, void* out,
+                                        bool out_bf16, int out_ld, hipStream_t s);
 pvconv_status pv_launch_point_mlp(const void* x, bool x_bf16, int x_ld, int M, int Cin,
                                   int Cout, const void* w, bool bf16, const PvBnFold& bn,
                                   int act, float slope, const float* cloud_bias, int ppc,

@@ -577,6 +577,21 @@ def test_forward_layer_variants(R, n_convs, width, devox):
     assert_bf16_chain(got, ref, f"layer R{R} x{n_convs} {cin}->{cout} {devox}")
 
 
+@pytest.mark.parametrize("N,cin,cout", [(1000, 16, 32), (777, 64, 96), (300, 12, 64)])
+def test_forward_ragged_points_and_channels(N, cin, cout):
+    # point counts that leave the last 128-point tile of the point MLP (which
+    # gathers the trilinear voxel branch itself) partly empty, an output width
+    # (96) that fills its 128-channel block only partly, and an input width
+    # (12) that the fused kernel does not take (separate devoxelisation)
+    wl = synth.make_workload(2, B=3, N=N)
+    L = synth.draw_pvconv(np.random.default_rng(N), cin, cout, 16, 1, bf16=True)
+    feats = np.ascontiguousarray(wl.feats[..., :cin])
+    ref = oracle.pvconv_forward(wl.coords, feats, L)
+    layer = pv.DeviceLayer(L, "cuda", torch.bfloat16)
+    got = host(pv.pvconv_forward(dev(wl.coords), dev(feats), layer))
+    assert_bf16_chain(got, ref, f"layer N{N} {cin}->{cout}")
+
+
 def test_forward_scene_first_block_nine_channels():
     wl = synth.make_workload(4, B=2)
     L = wl.layers[0]
