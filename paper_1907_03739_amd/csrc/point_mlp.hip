@@ -13,7 +13,10 @@
 // LDS) and the activation, adds the residual and writes 16-byte (8-byte for
 // bf16) vectors. Shapes that rule out vector access load value by value
 // (ragged or unaligned C_in) or read and write channel by channel (ragged
-// C_out or unaligned rows).
+// C_out or unaligned rows). Inside a whole PVConv layer the residual is the
+// trilinear devoxelisation of the bf16 grid, which the kernel's DV variant
+// gathers itself (pv_launch_devox_point_mlp): one launch fewer and no fp32
+// intermediate rows in HBM.
 #include "pv_common.h"
 #include "pv_trilinear.h"
 
