@@ -872,17 +872,16 @@ pvconv_status pv_launch_devox_point_mlp(const PvDevoxIn& dv, const void* x, bool
                     ((uintptr_t)out & (out_bf16 ? 7u : 15u)) == 0 && pv_aligned16(dv.grid) &&
                     !(Cin >= 128 && Cout >= 128) && dv.N > 0 && M % dv.N == 0;
     if (!ok) return PVCONV_ENOTSUP;
+    // 64-channel tiles also for wider layers: twice the workgroups (two per
+    // CU at the part-seg shape) to cover the gather's latency, 1 % faster on
+    // that layer than 128-channel tiles, though the point rows are read twice
 #define PV_DV(NB, XT)                                                                         \
     hipLaunchKernelGGL((pv_point_mlp_tile_kernel<NB, XT, true, true, true>),                  \
                        dim3((M + kWaves * 32 - 1) / (kWaves * 32), (Cout + NB * 32 - 1) / (NB * 32)), \
                        dim3(kWaves * 64), 0, s, (const XT*)x, x_ld, M, Cin, Cout,              \
                        (const uint16_t*)w, bn, act, slope, nullptr, 1, nullptr, 0, out,         \
                        (int)out_bf16, out_ld, dv)
-    if (x_bf16) {
-        if (Cout > 64) PV_DV(4, uint16_t); else PV_DV(2, uint16_t);
-    } else {
-        if (Cout > 64) PV_DV(4, float); else PV_DV(2, float);
-    }
+    if (x_bf16) PV_DV(2, uint16_t); else PV_DV(2, float);
 #undef PV_DV
     return pv_launch_status();
 }
