@@ -201,7 +201,9 @@ pvconv_status pvconv_devoxelize_nearest(const void* grid, int B, int R, int C,
 /*  residual    [M][Cout] fp32 (row stride residual_ld) or NULL; added after */
 /*              the activation                                               */
 /*  out         out [M][Cout] (out_dt), row stride out_ld                    */
-/* 1 <= Cin, Cout <= 16384. out must not overlap x.                          */
+/* 1 <= Cin, Cout <= 16384. out must not share any byte with x (else         */
+/* PVCONV_EINVAL): other workgroups may still read rows that are stored.     */
+/* Disjoint column ranges of one wider array (equal row strides) are fine.  */
 /* ------------------------------------------------------------------------- */
 pvconv_status pvconv_point_mlp(const void* x, pvconv_dtype x_dt, int x_ld, int M, int Cin,
                                int Cout, const void* weight, pvconv_dtype compute_dt,
@@ -232,7 +234,9 @@ typedef enum { PVCONV_DEVOX_TRILINEAR = 0, PVCONV_DEVOX_NEAREST = 1 } pvconv_dev
 /* PVCONV_DEVOX_NEAREST, nearest neighbour (pvconv_devoxelize_nearest). A     */
 /* zero-initialised struct selects trilinear.                                */
 /* All weights are in compute_dt (BF16 or F32); grids are kept in            */
-/* compute_dt. out is [B][N][cout] (out_dt) with row stride out_ld.          */
+/* compute_dt. out is [B][N][cout] (out_dt) with row stride out_ld; it must  */
+/* not share any byte with feats (else PVCONV_EINVAL): in-place layers race. */
+/* Disjoint column ranges of one wider array (equal row strides) are fine.  */
 /* ------------------------------------------------------------------------- */
 typedef struct {
     int cin, cout, R, n_convs;                 /* 1 <= n_convs <= PVCONV_MAX_CONVS */

@@ -18,6 +18,23 @@ inline hipStream_t as_stream(void* s) { return (hipStream_t)s; }
 // Elements must fit the int32 voxel ids and list offsets the kernels use.
 inline bool sizes_fit(long long B, long long N) { return B * N <= (1LL << 30); }
 
+// Two row-major arrays of `rows` rows share at least one byte: array a has
+// rows of ca elements of dtype ta at a stride of lda elements, b likewise.
+// Column slices of one wider array (the same row pitch, disjoint column
+// ranges, as the segmentation networks use them) do not overlap.
+inline bool overlap(const void* a, long long rows, int ca, int lda, pvconv_dtype ta,
+                    const void* b, int cb, int ldb, pvconv_dtype tb) {
+    if (rows <= 0) return false;
+    const long long pa = (long long)lda * esize(ta), pb = (long long)ldb * esize(tb);
+    const long long wa = (long long)ca * esize(ta), wb = (long long)cb * esize(tb);
+    const long long a0 = (long long)(uintptr_t)a, b0 = (long long)(uintptr_t)b;
+    if (a0 + (rows - 1) * pa + wa <= b0 || b0 + (rows - 1) * pb + wb <= a0) return false;
+    if (pa != pb) return true;
+    // the same pitch: b's rows start e bytes into a's rows (or a's into b's)
+    const long long e = ((b0 - a0) % pa + pa) % pa;
+    return !(e >= wa && e + wb <= pa);
+}
+
 struct ForwardWs {
     void* conv_ws[PVCONV_MAX_CONVS];
     void* vox_ws;
@@ -221,7 +238,9 @@ pvconv_status pvconv_point_mlp(const void* x, pvconv_dtype x_dt, int x_ld, int M
         ((uintptr_t)out & (esize(out_dt) - 1)) || ((uintptr_t)bias & 3) ||
         ((uintptr_t)cloud_bias & 3) || ((uintptr_t)residual & 3))
         return PVCONV_EINVAL;
-    if (x == out) return PVCONV_EINVAL;
+    // an output row can be stored before another workgroup has read the
+    // input row it overlaps
+    if (overlap(x, M, Cin, x_ld, x_dt, out, Cout, out_ld, out_dt)) return PVCONV_EINVAL;
     return pv_launch_point_mlp(x, x_dt == PVCONV_BF16, x_ld, M, Cin, Cout, weight,
                                compute_dt == PVCONV_BF16, pv_make_fold(bn, bias), act, slope,
                                cloud_bias, cloud_bias ? points_per_cloud : 1, residual,
@@ -272,6 +291,10 @@ pvconv_status pvconv_forward_ex(const float* coords, const void* feats, pvconv_d
     if (((uintptr_t)coords & 3) || ((uintptr_t)feats & (esize(feat_dt) - 1)) ||
         ((uintptr_t)out & (esize(out_dt) - 1)) || ((uintptr_t)vox_id & 3) ||
         ((uintptr_t)norm_coords & 3))
+        return PVCONV_EINVAL;
+    // several workgroups read each feature row while others store output
+    // rows: the two must not share memory
+    if (overlap(feats, (long long)B * N, L->cin, feat_ld, feat_dt, out, L->cout, out_ld, out_dt))
         return PVCONV_EINVAL;
     const size_t need = carve_forward(nullptr, B, N, L).total;
     if (!workspace || ((uintptr_t)workspace & 255) || workspace_bytes < need)

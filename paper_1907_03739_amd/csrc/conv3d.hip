@@ -10,11 +10,9 @@
 //    32*NB/WCH channels with v_mfma_f32_32x32x16_bf16: A = weights (rows =
 //    output channels), B = voxels (columns), 4 x NB/WCH accumulator blocks,
 //    so every voxel fragment feeds NB/WCH MFMAs and every weight fragment
-//    four. WCH = 1 (four waves, one per SIMD, all 256 accumulator registers
-//    for a 128-channel tile) measures fastest for 128-channel tiles of wide
-//    inputs; WCH = 2 (eight waves, two per SIMD, so that one wave's waits
-//    overlap the other's MFMAs) for 64-channel tiles of narrow inputs on
-//    small grids. Inputs of up to 128 channels on grids with enough tiles
+//    four. WCH = 1: four waves, one per SIMD; WCH = 2 (eight waves, two per
+//    SIMD, so that one wave's waits overlap the other's MFMAs) for
+//    64-channel tiles of narrow inputs on small grids. Inputs of up to 128 channels on grids with enough tiles
 //    take 64-channel tiles with compact halos (SB): 72 KB of LDS and at
 //    most 128 accumulator registers per wave, so two workgroups share a CU
 //    and one's prologue and epilogue overlap the other's MFMAs.
@@ -509,14 +507,13 @@ pvconv_status pv_launch_conv3d(const void* x, int B, int R, int Cin, int Cout, c
         // per CU: 64-channel tiles with compact halos, two per CU (one's
         // prologue and epilogue overlap the other's MFMAs: 11 % faster at
         // 64->128 and 64->64, 2.5 % at 128->128, than one 128-channel
-        // workgroup per CU). Otherwise four waves (one per SIMD, 128 channels
-        // each) for 128-channel tiles; eight (two channel groups) for
-        // 64-channel tiles of narrow inputs.
+        // workgroup per CU). Otherwise 64-channel tiles, one workgroup per
+        // CU: eight waves (two channel groups) for narrow inputs, four for
+        // wide ones (a 128-channel tile of four waves would hold all 256
+        // accumulator registers and spill in its epilogue).
         const bool two = Cin <= 64;
         if (Cin <= 128 && Cout % 64 == 0 && bricks * (Cout / 64) >= 512) {
             launch_bf16<2, 1, true>(x, B, R, Cin, Cout, w, bn, act, slope, y, out_bf16, vec, s);
-        } else if (Cout % 128 == 0 && bricks * (Cout / 128) >= 256) {
-            launch_bf16<4, 1>(x, B, R, Cin, Cout, w, bn, act, slope, y, out_bf16, vec, s);
         } else if (Cout % 64 == 0 && bricks * (Cout / 64) >= 256) {
             if (two)
                 launch_bf16<2, 2>(x, B, R, Cin, Cout, w, bn, act, slope, y, out_bf16, vec, s);

@@ -471,24 +471,25 @@ __global__ __launch_bounds__(64 * WN * WM, 1) void pv_point_mlp_lds_kernel(
 
     // Epilogue, one (32-point block mb, 32-channel block nb) at a time.
     // acc[mb][nb][4g + j] is channel wn*NB*32 + nb*32 + 8g + 4*khalf + j of
-    // the tile at point wm*MB*32 + mb*32 + r32. The per-cloud and residual
-    // rows of the next block are loaded before this block is stored: one
-    // counter tracks loads and stores alike, so a load issued after a store
-    // would wait for it.
+    // the tile at point wm*MB*32 + mb*32 + r32. A block's values are finished
+    // first, then the per-cloud and residual rows of the next block are
+    // loaded into the same registers, then the block is stored: one counter
+    // tracks loads and stores alike, so a load issued after a store would
+    // wait for it.
     const float neg = act == PVCONV_ACT_LEAKY ? slope : (act == PVCONV_ACT_RELU ? 0.f : 1.f);
-    float4 ext[2][2][4];   // [set][cloud row, residual][g]
-    auto load_ext = [&](int mb, int nb, float4 (&e)[2][4]) {
+    float4 ext[2][4];   // [cloud row, residual][g] of the block being finished
+    auto load_ext = [&](int mb, int nb) {
         const int m = min(m0 + wm * MB * 32 + mb * 32 + r32, M - 1);
         const float* cbr = EXT && cloud_bias ? cloud_bias + (size_t)(m / ppc) * Cout : nullptr;
         const float* rr = EXT && residual ? residual + (size_t)m * res_ld : nullptr;
 #pragma unroll
         for (int g = 0; g < 4; g++) {
             const int n = min(n0 + wn * NB * 32 + nb * 32 + g * 8 + 4 * khalf, Cout - 4);
-            e[0][g] = cbr ? *(const float4*)(cbr + n) : float4{0.f, 0.f, 0.f, 0.f};
-            e[1][g] = rr ? *(const float4*)(rr + n) : float4{0.f, 0.f, 0.f, 0.f};
+            ext[0][g] = cbr ? *(const float4*)(cbr + n) : float4{0.f, 0.f, 0.f, 0.f};
+            ext[1][g] = rr ? *(const float4*)(rr + n) : float4{0.f, 0.f, 0.f, 0.f};
         }
     };
-    load_ext(0, 0, ext[0]);
+    load_ext(0, 0);
 #pragma unroll
     for (int mb = 0; mb < MB; mb++) {
         const int m = m0 + wm * MB * 32 + mb * 32 + r32;
@@ -496,28 +497,30 @@ __global__ __launch_bounds__(64 * WN * WM, 1) void pv_point_mlp_lds_kernel(
 #pragma unroll
         for (int nb = 0; nb < NB; nb++) {
             const int blk = mb * NB + nb;
-            if (blk + 1 < MB * NB) load_ext((blk + 1) / NB, (blk + 1) % NB, ext[(blk + 1) & 1]);
+            float4 val[4];
 #pragma unroll
             for (int g = 0; g < 4; g++) {
                 const int nl = wn * NB * 32 + nb * 32 + g * 8 + 4 * khalf;
                 const float4 sc = tab[0][nl >> 2], sh = tab[1][nl >> 2];
-                const float4 cb = ext[blk & 1][0][g], rs = ext[blk & 1][1][g];
+                const float4 cb = ext[0][g], rs = ext[1][g];
                 float v[4] = {(acc[mb][nb][4 * g] + cb.x) * sc.x + sh.x,
                               (acc[mb][nb][4 * g + 1] + cb.y) * sc.y + sh.y,
                               (acc[mb][nb][4 * g + 2] + cb.z) * sc.z + sh.z,
                               (acc[mb][nb][4 * g + 3] + cb.w) * sc.w + sh.w};
 #pragma unroll
                 for (int j = 0; j < 4; j++) v[j] = v[j] >= 0.f ? v[j] : v[j] * neg;
-                v[0] += rs.x;
-                v[1] += rs.y;
-                v[2] += rs.z;
-                v[3] += rs.w;
+                val[g] = float4{v[0] + rs.x, v[1] + rs.y, v[2] + rs.z, v[3] + rs.w};
+            }
+            if (blk + 1 < MB * NB) load_ext((blk + 1) / NB, (blk + 1) % NB);
+#pragma unroll
+            for (int g = 0; g < 4; g++) {
+                const int nl = wn * NB * 32 + nb * 32 + g * 8 + 4 * khalf;
                 if (m >= M || n0 + nl >= Cout) continue;
                 if (out_bf16)
                     *(uint2*)((uint16_t*)out + orow + n0 + nl) =
-                        uint2{pv_pack_bf16x2(v[0], v[1]), pv_pack_bf16x2(v[2], v[3])};
+                        uint2{pv_pack_bf16x2(val[g].x, val[g].y), pv_pack_bf16x2(val[g].z, val[g].w)};
                 else
-                    *(float4*)((float*)out + orow + n0 + nl) = float4{v[0], v[1], v[2], v[3]};
+                    *(float4*)((float*)out + orow + n0 + nl) = val[g];
             }
         }
     }

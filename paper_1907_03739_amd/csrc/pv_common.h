@@ -130,11 +130,13 @@ static inline int pv_pack_blocks(const PvPackJobs& jobs) {
 // pv_pack_blocks) of a packing launch, 256 threads, one 16-byte piece each.
 constexpr int kPvPackKC = 16;
 constexpr int kPvPackTaps = 27;
-__device__ __forceinline__ void pv_pack_role(const PvPackJobs& jobs, int blk) {
+// tid: the thread's index within its 256-thread share of the workgroup.
+__device__ __forceinline__ void pv_pack_role(const PvPackJobs& jobs, int blk,
+                                             int tid = threadIdx.x) {
     int q = 0;
     while (q + 1 < jobs.n && blk >= jobs.job[q].blocks) blk -= jobs.job[q++].blocks;
     const PvPackJob& J = jobs.job[q];
-    const int i = blk * 256 + threadIdx.x;
+    const int i = blk * 256 + tid;
     if (i >= J.total) return;
     const int G = J.Cout / 32;
     const int lane = i & 63;

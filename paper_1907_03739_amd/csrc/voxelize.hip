@@ -1,24 +1,25 @@
 // Normalisation and voxelisation (Section 4.1 "Normalization", "Voxelization",
 // Eq. 2) for gfx950.
 //
-// Data flow for one call (B clouds, N points, grid R^3, C channels):
-//   1. normalise: per-cloud centroid (int64 fixed point, order-free), largest
-//      centred norm, then every point's normalised coordinates and voxel id.
-//      Clouds of up to 4096 points: one kernel, whose 256-point slices each
-//      recompute the cloud's parameters from registers. Larger clouds: four
-//      short kernels (abs-max, fixed-point sum, radius, points) that pass
-//      per-workgroup partial results through the workspace.
-//   2. tile fill: one workgroup per (cloud, tile of TV voxels) collects the
-//      points that fall in its tile, counting-sorts them by voxel in LDS,
-//      writes the tile's counts, zero rows for its empty voxels and, for the
-//      occupied ones, the mean of their features (fp64 sums). Voxels holding
-//      many points are summed by a whole wave with the points split across
-//      lanes, so a heavily collided cloud costs a few extra rounds of loads.
-//      Barriers order LDS only, so the grid rows stream out while the
-//      workgroup works on.
-// No global atomics; with 16-byte grid rows every grid element is written
-// once. Otherwise the normalisation launch first zeroes the grid (extra
-// workgroups) and the tile fill overwrites the occupied rows.
+// Clouds of up to 4096 points (kSmallMaxN): one launch, pv_voxel_slab_kernel
+// (described where it is defined). Each workgroup owns a slab of one cloud's
+// grid: it recomputes the cloud's normalisation (order-free, so every
+// workgroup gets the same bits), sorts the slab's points by voxel stably and
+// averages them in point order, while its writer waves stream the zero rows
+// of the empty voxels. Within a voxel the features are summed in point order
+// from zero (voxels of up to 16 points, as the oracle sums them; heavier
+// ones in a fixed order of subsets), so the grid is the same bits on every
+// run.
+//
+// Larger clouds: the normalisation in four short kernels (abs-max,
+// fixed-point sum, radius, points) that pass per-workgroup partial results
+// through the workspace, the points bucketed by tile, then one workgroup per
+// (cloud, tile of TV voxels) that counting-sorts its bucket by voxel in LDS,
+// writes the tile's counts, zero rows for its empty voxels and, for the
+// occupied ones, the mean of their features (fp64 sums); voxels of more than
+// kExport points go to the heavy-voxel kernels, which spread them over the
+// chip in chunks.
+// No global float atomics.
 #include <algorithm>
 #include <mutex>
 #include <unordered_map>
@@ -35,7 +36,6 @@ constexpr int kExport = 32;         // large clouds: voxels with more points go 
 constexpr int kChunk = 256;         // points per work item of the heavy-voxel kernel
 constexpr int kHeavyMaxC = 128;     // ... for up to this many channels (its sums' workspace)
 constexpr int kMaxCap = 4096;       // tile points kept in LDS at once
-constexpr int kCUs = 256;           // compute units of an MI355X
 
 // ---------------------------------------------------------------------------
 // Normalisation arithmetic. IEEE fp64, round to nearest even, no contraction,
@@ -78,18 +78,22 @@ __device__ __forceinline__ int voxel_axis(double x, int R) {
     return (int)f;
 }
 
+// One axis of a point's normalised coordinates, and its voxel coordinate.
+__device__ __forceinline__ int normalise_axis(float p, double c, double M2, double m, int R,
+                                              float& pn) {
+#pragma clang fp contract(off)
+    const double d = (double)p - c;
+    const double unit = (M2 == 0.0) ? 0.0 : d / m;
+    const double x = unit * 0.5 + 0.5;
+    pn = (float)x;
+    return voxel_axis(x, R);
+}
+
 // Normalised coordinates of one point and its voxel id.
 __device__ __forceinline__ int normalise_point(const float* p, const double* c, double M2,
                                                double m, int R, float* pn_out) {
-#pragma clang fp contract(off)
     int uvw[3];
-    for (int a = 0; a < 3; a++) {
-        double d = (double)p[a] - c[a];
-        double unit = (M2 == 0.0) ? 0.0 : d / m;
-        double x = unit * 0.5 + 0.5;
-        pn_out[a] = (float)x;
-        uvw[a] = voxel_axis(x, R);
-    }
+    for (int a = 0; a < 3; a++) uvw[a] = normalise_axis(p[a], c[a], M2, m, R, pn_out[a]);
     return (uvw[0] * R + uvw[1]) * R + uvw[2];
 }
 
@@ -118,10 +122,62 @@ __device__ __forceinline__ void lds_barrier() {
 // ---------------------------------------------------------------------------
 // Workgroup reductions and scans (wave64).
 // ---------------------------------------------------------------------------
+// Moves of a 32- or 64-bit value across lanes by DPP (row_mask ROWS; rows
+// left out keep 0).
+template <int CTRL, int ROWS>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t v) {
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, ROWS, 0xf, false);
+}
+template <int CTRL, int ROWS, typename T>
+__device__ __forceinline__ T dpp_move(T v) {
+    static_assert(sizeof(T) == 4 || sizeof(T) == 8, "32- or 64-bit lanes");
+    T r;
+    if constexpr (sizeof(T) == 4) {
+        uint32_t u;
+        __builtin_memcpy(&u, &v, 4);
+        u = dpp_u32<CTRL, ROWS>(u);
+        __builtin_memcpy(&r, &u, 4);
+    } else {
+        uint64_t u;
+        __builtin_memcpy(&u, &v, 8);
+        const uint64_t lo = dpp_u32<CTRL, ROWS>((uint32_t)u);
+        const uint64_t hi = dpp_u32<CTRL, ROWS>((uint32_t)(u >> 32));
+        u = lo | (hi << 32);
+        __builtin_memcpy(&r, &u, 8);
+    }
+    return r;
+}
+template <typename T>
+__device__ __forceinline__ T read_lane63(T v) {
+    T r;
+    if constexpr (sizeof(T) == 4) {
+        int u;
+        __builtin_memcpy(&u, &v, 4);
+        u = __builtin_amdgcn_readlane(u, 63);
+        __builtin_memcpy(&r, &u, 4);
+    } else {
+        int u[2];
+        __builtin_memcpy(u, &v, 8);
+        u[0] = __builtin_amdgcn_readlane(u[0], 63);
+        u[1] = __builtin_amdgcn_readlane(u[1], 63);
+        __builtin_memcpy(&r, u, 8);
+    }
+    return r;
+}
+
+// Reduction over the wave (every lane gets the result) by DPP moves: quad
+// swaps, half-row and row mirrors, then the row broadcasts into lane 63.
+// The moves fill lanes they leave out with 0, so op must have 0 as its
+// identity: sums, or maxima of non-negative values (every use here).
 template <typename T, typename Op>
 __device__ __forceinline__ T wave_reduce(T v, Op op) {
-    for (int o = 32; o > 0; o >>= 1) v = op(v, __shfl_xor(v, o, 64));
-    return v;
+    v = op(v, dpp_move<0xB1, 0xf>(v));   // quad_perm [1,0,3,2]
+    v = op(v, dpp_move<0x4E, 0xf>(v));   // quad_perm [2,3,0,1]
+    v = op(v, dpp_move<0x141, 0xf>(v));  // row_half_mirror
+    v = op(v, dpp_move<0x140, 0xf>(v));  // row_mirror
+    v = op(v, dpp_move<0x142, 0xa>(v));  // row_bcast:15 into rows 1 and 3
+    v = op(v, dpp_move<0x143, 0xc>(v));  // row_bcast:31 into rows 2 and 3
+    return read_lane63(v);
 }
 
 struct MaxF { __device__ float operator()(float a, float b) const { return fmaxf(a, b); } };
@@ -132,36 +188,73 @@ struct AddL {
 
 // K values reduced together over an NT-thread workgroup; every thread gets
 // the results. lds holds K * NT/64 entries.
-template <int NT, int K, typename T, typename Op>
-__device__ void block_reduce_k(T (&v)[K], Op op, T* lds) {
+// The workgroup's barrier (LDS data only), as a functor.
+struct HwSync {
+    __device__ void operator()() const { lds_barrier(); }
+};
+
+// A barrier among the first NW waves of the workgroup only, on a counter in
+// LDS, so that the workgroup's other waves never have to reach it (they may
+// be stalled issuing stores). Each arrival adds one; the g-th barrier opens
+// when the counter reaches g * NW. The wait is bounded (well under a
+// second): a wave that never arrives would be a bug, and the others then go
+// on rather than hang.
+template <int NW>
+struct WaveGroupSync {
+    int* ctr;
+    int gen;
+    __device__ void operator()() {
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+        gen++;
+        if ((threadIdx.x & 63) == 0) atomicAdd(ctr, 1);
+        for (int spin = 0; spin < (1 << 24); spin++)
+            if (__hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) >= gen * NW)
+                break;
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+    }
+};
+
+// trailing: a barrier after the reads too, so that lds may be reused at
+// once (not needed when each reduction has LDS of its own)
+template <int NT, int K, typename T, typename Op, typename Sync = HwSync>
+__device__ void block_reduce_k(T (&v)[K], Op op, T* lds, Sync&& sync = Sync{},
+                               bool trailing = true) {
 #pragma unroll
     for (int i = 0; i < K; i++) v[i] = wave_reduce(v[i], op);
     const int w = threadIdx.x >> 6;
     if ((threadIdx.x & 63) == 0)
 #pragma unroll
         for (int i = 0; i < K; i++) lds[i * (NT / 64) + w] = v[i];
-    lds_barrier();
+    sync();
 #pragma unroll
     for (int i = 0; i < K; i++) {
         T r = lds[i * (NT / 64)];
         for (int j = 1; j < NT / 64; j++) r = op(r, lds[i * (NT / 64) + j]);
         v[i] = r;
     }
-    lds_barrier();
+    if (trailing) sync();
+}
+
+// Inclusive prefix sum over the wave by DPP moves (shifts within rows of 16
+// lanes, then the row broadcasts), without cross-lane LDS instructions.
+__device__ __forceinline__ int wave_inclusive_scan(int v) {
+    v += (int)dpp_u32<0x111, 0xf>((uint32_t)v);  // row_shr:1
+    v += (int)dpp_u32<0x112, 0xf>((uint32_t)v);  // row_shr:2
+    v += (int)dpp_u32<0x114, 0xf>((uint32_t)v);  // row_shr:4
+    v += (int)dpp_u32<0x118, 0xf>((uint32_t)v);  // row_shr:8
+    v += (int)dpp_u32<0x142, 0xa>((uint32_t)v);  // row_bcast:15 into rows 1 and 3
+    v += (int)dpp_u32<0x143, 0xc>((uint32_t)v);  // row_bcast:31 into rows 2 and 3
+    return v;
 }
 
 // Exclusive scan of one int per thread over the workgroup; also returns the total.
-template <int NT>
-__device__ int block_exclusive_scan(int v, int* lds /* NT/64 */, int& total) {
+template <int NT, typename Sync = HwSync>
+__device__ int block_exclusive_scan(int v, int* lds /* NT/64 */, int& total, Sync&& sync = Sync{}) {
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    int incl = v;
-    for (int o = 1; o < 64; o <<= 1) {
-        int t = __shfl_up(incl, o, 64);
-        if (lane >= o) incl += t;
-    }
-    lds_barrier();
+    const int incl = wave_inclusive_scan(v);
+    sync();
     if (lane == 63) lds[w] = incl;
-    lds_barrier();
+    sync();
     int before = 0;
     total = 0;
     for (int i = 0; i < NT / 64; i++) {
@@ -169,17 +262,10 @@ __device__ int block_exclusive_scan(int v, int* lds /* NT/64 */, int& total) {
         if (i < w) before += s;
         total += s;
     }
-    lds_barrier();
+    sync();
     return before + incl - v;
 }
 
-// ---------------------------------------------------------------------------
-// Normalisation, clouds of up to kSmallMaxN points: grid (slices, clouds) of
-// 256-thread workgroups. Every workgroup holds its cloud's points in
-// registers (PPT per thread), computes the normalisation parameters with
-// three workgroup reductions (the three axes reduced together) and writes
-// the voxel id and normalised coordinates of its own slice of 256 points.
-// The parameters are order-free, so all slices of a cloud agree bit for bit.
 // ---------------------------------------------------------------------------
 // Zero fill of the whole grid (16-byte stores, grid-stride over `zero_blocks`
 // workgroups). The tile kernel then writes the rows of occupied voxels.
@@ -192,10 +278,10 @@ __device__ __forceinline__ void zero_fill_role(uint4* grid16, size_t n16, int zb
 // norm M2, m = sqrt(M2)) from its N points, held PPT per thread (point
 // threadIdx.x + i*NT in x[i]) by an NT-thread workgroup. Every reduction is
 // order-free, so every workgroup that calls this for a cloud gets the same
-// bits.
-template <int PPT, int NT>
+// bits. Each reduction has LDS of its own, so no barrier follows its reads.
+template <int PPT, int NT, typename Sync = HwSync>
 __device__ void cloud_params(const float (&x)[PPT][3], int N, double (&c)[3], double& M2,
-                             double& m) {
+                             double& m, Sync&& sync = Sync{}) {
     __shared__ float redf[3 * NT / 64];
     __shared__ long long redl[3 * NT / 64];
     __shared__ double redd[NT / 64];
@@ -204,7 +290,7 @@ __device__ void cloud_params(const float (&x)[PPT][3], int N, double (&c)[3], do
     for (int i = 0; i < PPT; i++)
 #pragma unroll
         for (int a = 0; a < 3; a++) A[a] = fmaxf(A[a], fabsf(x[i][a]));
-    block_reduce_k<NT>(A, MaxF(), redf);
+    block_reduce_k<NT>(A, MaxF(), redf, sync, false);
     int S[3];
     long long q[3] = {0, 0, 0};
 #pragma unroll
@@ -214,14 +300,14 @@ __device__ void cloud_params(const float (&x)[PPT][3], int N, double (&c)[3], do
         for (int i = 0; i < PPT; i++)
             if (A[a] > 0.f && threadIdx.x + i * NT < N) q[a] += fixed_term(x[i][a], S[a]);
     }
-    block_reduce_k<NT>(q, AddL(), redl);
+    block_reduce_k<NT>(q, AddL(), redl, sync, false);
 #pragma unroll
     for (int a = 0; a < 3; a++) c[a] = centroid_from_sum(q[a], S[a], A[a], N);
     double mx[1] = {0.0};
 #pragma unroll
     for (int i = 0; i < PPT; i++)
         if (threadIdx.x + i * NT < N) mx[0] = fmax(mx[0], sq_dist(x[i], c));
-    block_reduce_k<NT>(mx, MaxD(), redd);
+    block_reduce_k<NT>(mx, MaxD(), redd, sync, false);
     M2 = mx[0];
     m = sqrt(M2);
 }
@@ -236,48 +322,6 @@ __device__ __forceinline__ void load_cloud(const float* __restrict__ p, int N,
 #pragma unroll
         for (int a = 0; a < 3; a++) x[i][a] = k < N ? p[3 * k + a] : 0.f;
     }
-}
-
-template <int PPT>
-__device__ void ids_role(const float* __restrict__ coords, int N, int R, int slice, int b,
-                         int32_t* __restrict__ vox_id, float* __restrict__ norm_coords) {
-    constexpr int NT = 256;
-    float x[PPT][3];
-    load_cloud<PPT, NT>(coords + (size_t)b * N * 3, N, x);
-    double c[3], M2, m;
-    cloud_params<PPT, NT>(x, N, c, M2, m);
-    // this workgroup's slice: points slice*256 + tid, i.e. register row `slice`
-#pragma unroll
-    for (int i = 0; i < PPT; i++) {
-        const int k = threadIdx.x + i * NT;
-        if (i != slice || k >= N) continue;
-        float pn[3];
-        const int id = normalise_point(x[i], c, M2, m, R, pn);
-        write_point(vox_id, norm_coords, (size_t)b * N + k, id, pn);
-    }
-}
-
-// One launch, three roles: the first B * slices workgroups normalise (slice
-// blockIdx % slices of cloud blockIdx / slices), the next npack repack conv
-// weights (a layer's convolutions, independent work that fills CUs the
-// normalisation leaves idle), the rest zero the grid.
-template <int PPT>
-__global__ __launch_bounds__(256) void pv_voxel_ids_kernel(const float* __restrict__ coords,
-                                                           int N, int R, int slices, int nid,
-                                                           int32_t* __restrict__ vox_id,
-                                                           float* __restrict__ norm_coords,
-                                                           uint4* __restrict__ grid16, size_t n16,
-                                                           PvPackJobs pack, int npack) {
-    const int bid = blockIdx.x;
-    if (bid >= nid + npack) {
-        zero_fill_role(grid16, n16, bid - nid - npack, gridDim.x - nid - npack);
-        return;
-    }
-    if (bid >= nid) {
-        pv_pack_role(pack, bid - nid);
-        return;
-    }
-    ids_role<PPT>(coords, N, R, bid % slices, bid / slices, vox_id, norm_coords);
 }
 
 // ---------------------------------------------------------------------------
@@ -588,6 +632,656 @@ __device__ __forceinline__ void sum8(const FT* fb, int feat_ld, int col, const i
 }
 
 // ---------------------------------------------------------------------------
+// Slab fill, clouds of up to kSmallMaxN points: the whole voxelisation in one
+// launch. Workgroup (s, b) owns the contiguous voxel range [v0, v0 + nv) of
+// cloud b (a slab of the grid, v0 = s * nvs). Its waves take two roles.
+//  * Compute waves (threads 0 .. kSlabNC-1) recompute the cloud's
+//    normalisation from the coordinates (order-free, so every workgroup of
+//    the cloud gets the same bits) or read given voxel indices, count the
+//    slab's points per voxel and list them in point-index order (ballots
+//    and per-wave counts), counting-sort them by voxel stably (one wave, 64
+//    points per step), then gather the features of the sorted points into
+//    LDS in segments (one round of loads per segment, all in flight) and
+//    average each occupied voxel's rows in sorted order in fp64: within a
+//    voxel the points are summed in point order from zero, as Eq. 2's
+//    oracle sums them, and the grid is the same bits on every run. A voxel
+//    with more points than the stage holds is summed from global memory by
+//    a whole wave, its points split into subsets whose sums are added in
+//    subset order.
+//  * A loader wave (threads kSlabLoader ..) streams the slab's feature rows
+//    into the LDS stage (global_load_lds, no registers) as soon as the
+//    points are listed, while the compute waves sort them, and raises a
+//    flag in LDS when they have landed.
+//  * Writer waves (the others) store zeros over the rows of the slab's empty
+//    voxels and write the slab's counts. Rows that no point can reach go
+//    out from the first cycle: a normalised point lies within 1/2 of the
+//    cube's centre, so a voxel whose cell is further away stays empty. The
+//    other empty rows follow once the counts are known. Compute and writer
+//    waves never write the same bytes.
+// While the writes stream, issuing a store can stall for microseconds (the
+// memory system pushes back), so the two roles share no barrier after the
+// first: the compute waves synchronise among themselves on a counter in LDS
+// (WaveGroupSync) and the writers wait for the counts on a flag in LDS.
+// ---------------------------------------------------------------------------
+constexpr int kSlabNC = 512;             // compute threads (eight waves)
+constexpr int kSortWaves = 4;            // compute waves that rank the points
+constexpr int kSlabLoader = kSlabNC;     // first thread of the loader waves
+constexpr int kLoaders = 2;              // loader waves
+constexpr int kSplit = 16;               // staged voxels with more points: summed by a whole wave
+// threads: kSlabLoader + 64 * kLoaders .. NT-1 write zeros. 1024 (six writer
+// waves) for clouds of up to 2048 points, whose compute waves fit in 128
+// registers, else 768 (two writer waves)
+constexpr int kSlabNT = 1024;
+constexpr int kSlabNTSmall = 768;
+constexpr int kSlabWGs = 256;            // slabs per launch (one workgroup per CU)
+constexpr int kSlabMinVox = 64;          // fewest voxels per slab
+constexpr int kSlabMaxVox = 2048;        // most voxels per slab (bounds its LDS)
+
+struct SlabShape {
+    int S, nvs;  // slabs per cloud, voxels per slab
+};
+// The kernel's dynamic LDS is about 17 bytes per slab voxel and 10 per point
+// of the cloud; with the static stage it has to fit a CU's 160 KB.
+constexpr int kSlabDynBudget = 62 * 1024;
+SlabShape slab_shape(int B, int V, int N) {
+    const int max_vox =
+        std::max(kSlabMinVox, std::min(kSlabMaxVox, (kSlabDynBudget - 10 * std::max(N, 1)) / 17));
+    int S = std::max(1, kSlabWGs / std::max(B, 1));
+    S = std::min(S, std::max(1, V / kSlabMinVox));
+    S = std::max(S, (V + max_vox - 1) / max_vox);
+    const int nvs = (V + S - 1) / S;
+    return SlabShape{(V + nvs - 1) / nvs, nvs};
+}
+
+// LDS of a slab workgroup (byte offsets; 16-bit entries where the values
+// fit: N <= 4096 points, nvs <= 2048 voxels):
+//  hist[nvs] int, start[nvs + 1], occ[nvs] (occupied voxels in voxel order),
+//  sortj[N], sortk[N] (the slab's points sorted by voxel: their position in
+//  kbuf, their index), far[nvs] bytes (no point can reach the voxel);
+//  then the sort's working set: kbuf[N] (the slab's points in point order),
+//  rbuf[N] int (their voxel in the slab, later with their rank),
+//  wc[kSortWaves][nvs] (per-wave cursors). All of this is the kernel's
+//  dynamic LDS. The feature stage is a static array of its own (kStageBytes, plus 1 KB of slack: the
+//  last load of a wave may run past the rows), so that the compiler sees
+//  that the loads streaming into it touch none of the tables: raw feature
+//  rows go into it straight from global memory, in kbuf order during the
+//  sort when the whole slab fits ("pre"), else in segments of the sorted
+//  order after it.
+struct SlabLayout {
+    int hist, start, occ, sortj, sortk, far, kbuf, rbuf, wc, pre;
+};
+__host__ __device__ inline SlabLayout slab_layout(int nvs, int N) {
+    const int N1 = N > 1 ? N : 1;
+    auto al = [](int x) { return (x + 15) & ~15; };
+    SlabLayout L;
+    int o = 0;
+    L.hist = o;
+    o += 4 * nvs;
+    L.start = o;
+    o += 2 * (nvs + 1);
+    L.occ = o;
+    o += 2 * nvs;
+    L.sortj = o;
+    o += 2 * N1;
+    L.sortk = o;
+    o += 2 * N1;
+    L.far = o;
+    o = al(o + nvs);
+    L.kbuf = o;
+    o += al(2 * N1);
+    L.rbuf = o;
+    o += al(4 * N1);
+    L.wc = o;
+    o += al(2 * kSortWaves * nvs);
+    L.pre = o;
+    return L;
+}
+constexpr int kStageSlack = 1024;
+constexpr int kStageBytes = 96 * 1024;
+
+// No normalised point reaches voxel `vox`: its cell lies further than 1/2
+// from the cube's centre. Exact integer test in units of 1/(2R): the cell
+// spans [2u, 2u + 2] per axis, the centre is at R, the radius R.
+__device__ __forceinline__ bool outside_ball(int vox, int R) {
+    const int w = vox % R, v = (vox / R) % R, u = vox / (R * R);
+    auto gap = [R](int i) { return max(max(2 * i - R, R - 2 * i - 2), 0); };
+    const long long du = gap(u), dv = gap(v), dw = gap(w);
+    return du * du + dv * dv + dw * dw > (long long)R * R;
+}
+
+__device__ __forceinline__ unsigned long long lanes_below() {
+    const int lane = threadIdx.x & 63;
+    return lane ? (~0ull >> (64 - lane)) : 0ull;
+}
+
+// Sum of 8 channels over the points list[j], list[j + step], ... (< j1) in
+// that order, fp64, in rounds of U points whose loads are all in flight
+// (indices past the end repeat the round's last point and are not added).
+template <typename FT, int U, typename IT>
+__device__ __forceinline__ void round_sum8(const FT* fb, int feat_ld, int col, const IT* list,
+                                           int j, int j1, int step, double* acc) {
+    for (; j < j1; j += U * step) {
+        const int n = min(U, (j1 - j + step - 1) / step);
+        float f[U][8];
+#pragma unroll
+        for (int u = 0; u < U; u++)
+            load8f<FT>(fb + (size_t)list[j + min(u, n - 1) * step] * feat_ld + col, f[u]);
+#pragma unroll
+        for (int u = 0; u < U; u++)
+            if (u < n)
+#pragma unroll
+                for (int i = 0; i < 8; i++) acc[i] += (double)f[u][i];
+    }
+}
+
+// A voxel too heavy for the feature stage, by one wave, channel groups cg0 ..
+// cg0+ng-1: lane = sub * ng + (cg - cg0) sums points j0 + sub, j0 + sub + S,
+// ... (S = 64 / ng subsets); lane cl < ng gets the total of its channel
+// group, the S partial sums added in subset order.
+template <typename FT, typename IT>
+__device__ __forceinline__ void wave_sum8(const FT* fb, int feat_ld, const IT* list, int j0,
+                                          int nk, int cg0, int ng, double* tot) {
+    const int lane = threadIdx.x & 63;
+    const int S = 64 / ng, sub = lane / ng, cl = lane % ng;
+    double acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    if (sub < S) round_sum8<FT, 4>(fb, feat_ld, (cg0 + cl) * 8, list, j0 + sub, j0 + nk, S, acc);
+#pragma unroll
+    for (int i = 0; i < 8; i++) tot[i] = __shfl(acc[i], cl, 64);
+    for (int s2 = 1; s2 < S; s2++)
+#pragma unroll
+        for (int i = 0; i < 8; i++) tot[i] += __shfl(acc[i], s2 * ng + cl, 64);
+}
+
+// Raw feature rows of FT into the LDS stage at dst, straight from global
+// memory (global_load_lds, 16 bytes a lane, the lane's bytes at dst + 16 *
+// lane): rows [0, nrows), row r holding the features of point pt(r). Wave
+// `wave` of the NC/64 taking part issues every (NC/64)-th 64-piece block;
+// the last block's lanes past the end re-load the last piece into the slack.
+template <int NC, typename FT, typename PointOf>
+__device__ __forceinline__ void dma_rows(char* dst, int nrows, int C, const FT* fb, int feat_ld,
+                                         PointOf pt, int wave) {
+    const int lane = threadIdx.x & 63;
+    const int ppr = C * (int)sizeof(FT) / 16;  // 16-byte pieces per row
+    const int npiece = nrows * ppr;
+    const bool pow2 = (ppr & (ppr - 1)) == 0;
+    const int sh = __ffs(ppr) - 1;
+    for (int p0 = wave * 64; p0 < npiece; p0 += NC) {
+        const int pc = min(p0 + lane, npiece - 1);
+        const int r = pow2 ? pc >> sh : pc / ppr, q = pc - r * ppr;
+        const FT* src = fb + (size_t)pt(r) * feat_ld + q * (16 / (int)sizeof(FT));
+        __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)src,
+                                         (void __attribute__((address_space(3)))*)(dst + p0 * 16),
+                                         16, 0, 0);
+    }
+}
+
+// 8 channels of a raw feature row in LDS as fp32.
+__device__ __forceinline__ void stage8(const float* p, float* v) {
+    const float4 a = *(const float4*)p, b = *(const float4*)(p + 4);
+    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+    v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+}
+__device__ __forceinline__ void stage8(const uint16_t* p, float* v) {
+    const uint4 a = *(const uint4*)p;
+    const uint32_t w[4] = {a.x, a.y, a.z, a.w};
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+        v[2 * i] = pv_bf16_to_f32((uint16_t)(w[i] & 0xffffu));
+        v[2 * i + 1] = pv_bf16_to_f32((uint16_t)(w[i] >> 16));
+    }
+}
+__device__ __forceinline__ float stage1(const float* p) { return *p; }
+__device__ __forceinline__ float stage1(const uint16_t* p) { return pv_bf16_to_f32(*p); }
+
+// VEC: C % 8 == 0 and 16-byte feature rows and grid rows (8 channels at a
+// time); else channel by channel. GVEC: grid rows are whole 16-byte pieces
+// (the writers' zero stores), else element stores.
+template <int PPT, int NT, typename FT, typename GT, bool VEC, bool GVEC>
+__global__ __launch_bounds__(NT) void pv_voxel_slab_kernel(
+    const float* __restrict__ coords, const int32_t* __restrict__ ids_in,
+    const FT* __restrict__ feats, int feat_ld, int N, int C, int R, int nvs, int nslab,
+    int cap_pre, GT* __restrict__ grid, int32_t* __restrict__ counts,
+    int32_t* __restrict__ vox_id, float* __restrict__ norm_coords, PvPackJobs pack, int npack) {
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    __shared__ __attribute__((aligned(16))) char s_stage[kStageBytes + kStageSlack];
+    // compute waves' barrier counter; counts complete; the slab's point count
+    // + 1 once listed; loader waves whose rows have landed
+    __shared__ int s_ctr, s_counted, s_listed, s_rows_in;
+    __shared__ int wcnt[PPT][kSlabNC / 64];
+    const int bid = blockIdx.x;
+    if (bid >= (int)gridDim.x - npack) {  // extra workgroups: conv weight packing
+        const int pb = bid - ((int)gridDim.x - npack);
+        if (threadIdx.x < 512) pv_pack_role(pack, 2 * pb + (threadIdx.x >= 256), threadIdx.x & 255);
+        return;
+    }
+    constexpr int NC = kSlabNC, NW = NT - kSlabLoader - 64 * kLoaders;
+    const int s = bid % nslab, b = bid / nslab;
+    const int V = R * R * R;
+    const int v0 = s * nvs, nv = min(nvs, V - v0);
+    GT* out = grid + ((size_t)b * V + v0) * C;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const SlabLayout LY = slab_layout(nvs, N);
+    int* hist = (int*)(smem + LY.hist);
+    uint16_t* start = (uint16_t*)(smem + LY.start);
+    uint16_t* occ = (uint16_t*)(smem + LY.occ);
+    uint16_t* sortj = (uint16_t*)(smem + LY.sortj);
+    uint16_t* sortk = (uint16_t*)(smem + LY.sortk);
+    unsigned char* far = (unsigned char*)(smem + LY.far);
+    uint16_t* kbuf = (uint16_t*)(smem + LY.kbuf);
+    int* rbuf = (int*)(smem + LY.rbuf);
+    uint16_t* wc = (uint16_t*)(smem + LY.wc);
+    for (int i = tid; i < nvs; i += NT) {
+        hist[i] = 0;
+        far[i] = !ids_in && i < nv && outside_ball(v0 + i, R);
+    }
+    if (tid == 0) {
+        s_ctr = 0;
+        s_counted = 0;
+        s_listed = 0;
+        s_rows_in = 0;
+    }
+    lds_barrier();  // the only barrier of the whole workgroup
+
+    // zero stores of the writer waves over the rows of voxels vi with
+    // want(vi): 16-byte pieces when the rows are made of them, else elements.
+    // Each thread keeps one piece (or element) column q of rows r0, r0 + rs,
+    // ..., so that the loop divides nothing, four rows a round (their table
+    // reads together); consecutive threads still write consecutive bytes.
+    constexpr int W0 = kSlabLoader + 64 * kLoaders;  // first writer thread
+    auto zero_rows = [&](auto want) {
+        const int wt = tid - W0;
+        const int pr = GVEC ? C * (int)sizeof(GT) / 16 : C;  // pieces per row
+        const int rs = NW / pr;                              // rows per round
+        if (rs > 0) {
+            const int q = wt % pr, r0 = wt / pr;
+            if (r0 >= rs) return;
+            for (int r = r0; r < nv; r += 4 * rs) {
+                bool z[4];
+#pragma unroll
+                for (int u = 0; u < 4; u++) z[u] = r + u * rs < nv && want(r + u * rs);
+#pragma unroll
+                for (int u = 0; u < 4; u++) {
+                    if (!z[u]) continue;
+                    const size_t i = (size_t)(r + u * rs) * pr + q;
+                    if (GVEC)
+                        ((uint4*)out)[i] = make_uint4(0u, 0u, 0u, 0u);
+                    else
+                        out[i] = (GT)0;
+                }
+            }
+            return;
+        }
+        for (int i = wt; i < nv * pr; i += NW) {  // rows wider than NW pieces
+            if (!want(i / pr)) continue;
+            if (GVEC)
+                ((uint4*)out)[i] = make_uint4(0u, 0u, 0u, 0u);
+            else
+                out[i] = (GT)0;
+        }
+    };
+    if (tid >= W0) {
+        // writers, before the counts exist: the rows no point can reach
+        // (normalised points only; given indices may name any voxel)
+        if (!ids_in) zero_rows([&](int vi) { return far[vi] != 0; });
+        // wait (bounded, well under a second) until the compute waves have counted
+        for (int spin = 0; spin < (1 << 23); spin++) {
+            if (__hip_atomic_load(&s_counted, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP))
+                break;
+            __builtin_amdgcn_s_sleep(2);
+        }
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+        // the other empty rows, then the counts
+        zero_rows([&](int vi) { return hist[vi] == 0 && !far[vi]; });
+        for (int v = tid - W0; v < nv; v += NW) counts[(size_t)b * V + v0 + v] = hist[v];
+        return;
+    }
+    // bounded wait (well under a second) for a flag in LDS
+    auto wait_flag = [](int* f) {
+        for (int spin = 0; spin < (1 << 23); spin++) {
+            if (__hip_atomic_load(f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP)) break;
+            __builtin_amdgcn_s_sleep(1);
+        }
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+    };
+    const FT* fb = feats + (size_t)b * N * feat_ld;
+    if (tid >= kSlabLoader) {
+        // the loader: once the points are listed, the whole slab's rows
+        // (when they fit the stage) in point order
+        wait_flag(&s_listed);
+        const int ns = s_listed - 1;
+        if (VEC && ns <= cap_pre)
+            dma_rows<64 * kLoaders, FT>(s_stage, ns, C, fb, feat_ld,
+                                        [&](int r) { return (int)kbuf[r]; }, wave - NC / 64);
+        __builtin_amdgcn_s_waitcnt(0);  // this wave's rows have landed
+        if (lane == 0) atomicAdd(&s_rows_in, 1);
+        return;
+    }
+
+    // ---- compute waves ----------------------------------------------------
+    WaveGroupSync<NC / 64> sync{&s_ctr, 0};
+    // 1. the cloud's points and the voxel ids of those in the slab
+    float x[PPT][3];
+    int id[PPT];
+    if (ids_in) {
+#pragma unroll
+        for (int i = 0; i < PPT; i++) {
+            const int k = tid + i * NC;
+            id[i] = k < N ? ids_in[(size_t)b * N + k] : -1;
+        }
+    } else {
+        load_cloud<PPT, NC>(coords + (size_t)b * N * 3, N, x);
+        double c[3], M2, m;
+        cloud_params<PPT, NC>(x, N, c, M2, m, sync);
+        // The slab spans voxel coordinates u in [ulo, uhi]. A point's u is
+        // first estimated with d * (1/m) for d / m (within a few units in the
+        // last place of the exact quotient, so the estimate's cell is the
+        // exact one unless it lies within 1e-9 of a cell face, where the
+        // exact division decides). The candidates, the points in the u range,
+        // are packed per wave into LDS (the stage, unused until the points
+        // are listed) and get their exact normalised coordinates and voxel id
+        // there, a full wave at a time; each lane then reads back its own.
+        const int ulo = v0 / (R * R), uhi = (v0 + nv - 1) / (R * R);
+        const double minv = M2 == 0.0 ? 0.0 : 1.0 / m;
+        float4* cbuf = (float4*)s_stage + wave * (PPT * 64);
+        const unsigned long long lt = lanes_below();
+        int ncand = 0, cpos[PPT];
+#pragma unroll
+        for (int i = 0; i < PPT; i++) {
+            id[i] = -1;
+            bool cand = false;
+            if (tid + i * NC < N) {
+#pragma clang fp contract(off)
+                const double xs = (((double)x[i][0] - c[0]) * minv * 0.5 + 0.5) * (double)R;
+                const double f = floor(xs);
+                int u;
+                float pnx;
+                if (xs - f < 1e-9 || f + 1.0 - xs < 1e-9)
+                    u = normalise_axis(x[i][0], c[0], M2, m, R, pnx);
+                else
+                    u = (int)fmin(fmax(f, 0.0), (double)(R - 1));
+                cand = u >= ulo && u <= uhi;
+            }
+            const unsigned long long cm = __ballot(cand);
+            cpos[i] = cand ? ncand + __popcll(cm & lt) : -1;
+            if (cand) cbuf[cpos[i]] = make_float4(x[i][0], x[i][1], x[i][2], 0.f);
+            ncand += __popcll(cm);
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
+        for (int j = lane; j < ((ncand + 63) & ~63); j += 64) {
+            if (j >= ncand) continue;
+            const float4 p = cbuf[j];
+            float pn[3];
+            const int u = normalise_axis(p.x, c[0], M2, m, R, pn[0]);
+            const int v = normalise_axis(p.y, c[1], M2, m, R, pn[1]);
+            const int w = normalise_axis(p.z, c[2], M2, m, R, pn[2]);
+            cbuf[j] = make_float4(pn[0], pn[1], pn[2], __int_as_float((u * R + v) * R + w));
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
+        // each lane's own candidates; the slab's points get their index and
+        // normalised coordinates written now (the compute waves issue no
+        // global loads that these stores could hold up)
+#pragma unroll
+        for (int i = 0; i < PPT; i++) {
+            if (cpos[i] < 0) continue;
+            const float4 r = cbuf[cpos[i]];
+            id[i] = __float_as_int(r.w);
+            if (id[i] >= v0 && id[i] < v0 + nv) {
+                const float pn[3] = {r.x, r.y, r.z};
+                write_point(vox_id, norm_coords, (size_t)b * N + tid + i * NC, id[i], pn);
+            }
+        }
+    }
+    // the slab's points in point-index order: register row i of the threads
+    // is points [i * NC, (i + 1) * NC); counts per (row, wave), per voxel
+    unsigned long long bal[PPT];
+#pragma unroll
+    for (int i = 0; i < PPT; i++) {
+        const int k = tid + i * NC;
+        const bool in = k < N && id[i] >= v0 && id[i] < v0 + nv;
+        bal[i] = __ballot(in);
+        if (lane == 0) wcnt[i][wave] = __popcll(bal[i]);
+        if (in) atomicAdd(&hist[id[i] - v0], 1);
+    }
+    sync();
+    if (tid == 0) __hip_atomic_store(&s_counted, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+    int ns = 0;
+    {
+        const unsigned long long lt = lanes_below();
+#pragma unroll
+        for (int i = 0; i < PPT; i++) {
+            int before = ns;
+            for (int w = 0; w < NC / 64; w++) {
+                const int cw = wcnt[i][w];
+                if (w < wave) before += cw;
+                ns += cw;
+            }
+            if ((bal[i] >> lane) & 1ull) {
+                const int pos = before + __popcll(bal[i] & lt);
+                kbuf[pos] = (uint16_t)(tid + i * NC);
+                rbuf[pos] = id[i] - v0;
+            }
+        }
+        for (int i = tid; i < kSortWaves * nvs; i += NC) wc[i] = 0;
+    }
+    sync();
+    // 2. the loader streams the slab's feature rows into LDS while the
+    // points are sorted (when they fit the stage)
+    if (tid == 0)
+        __hip_atomic_store(&s_listed, ns + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+    const bool pre = VEC && ns <= cap_pre;
+
+    // 3. exclusive prefix over the slab's voxels of (points, occupied): hi
+    // 16 bits count points (ns <= 4096), lo 16 bits voxels
+    int n_occ;
+    {
+        const int seg = (nv + NC - 1) / NC;
+        const int s0 = min(nv, tid * seg), s1 = min(nv, s0 + seg);
+        int local = 0;
+        for (int i = s0; i < s1; i++) local += (hist[i] << 16) + (hist[i] > 0);
+        int total;
+        int run = block_exclusive_scan<NC>(local, (int*)wcnt, total, sync);
+        for (int i = s0; i < s1; i++) {
+            const int h = hist[i];
+            start[i] = (uint16_t)(run >> 16);
+            if (h > 0) occ[run & 0xffff] = (uint16_t)i;
+            run += (h << 16) + (h > 0);
+        }
+        n_occ = total & 0xffff;
+    }
+    sync();
+    // 4. stable counting sort by voxel. Sort wave w (of kSortWaves) takes the
+    // w-th part of the point-ordered list, 64 entries at a time, and ranks
+    // each entry among the equal voxels before it in its part (within 64
+    // entries: lanes with the same voxel, found by ballots over the voxel's
+    // bits; across steps: a cursor per voxel, wc[w]); the rank goes into
+    // rbuf's upper bits. Then position = start + the equal voxels of the
+    // earlier parts + rank.
+    {
+        const int quarter = (ns + kSortWaves - 1) / kSortWaves;
+        const int j0w = wave < kSortWaves ? wave * quarter : ns;
+        const int j1w = min(ns, j0w + quarter);
+        int nbits = 0;
+        while ((1 << nbits) < nv) nbits++;
+        const unsigned long long lt = lanes_below();
+        uint16_t* cw = wc + wave * nvs;
+        for (int j0 = j0w; j0 < j1w; j0 += 64) {
+            const int j = j0 + lane;
+            const bool valid = j < j1w;
+            const int r = valid ? rbuf[j] : 0;
+            unsigned long long same = __ballot(valid);
+            for (int bit = 0; bit < nbits; bit++) {
+                const unsigned long long ones = __ballot((r >> bit) & 1);
+                same &= ((r >> bit) & 1) ? ones : ~ones;
+            }
+            const int rank = __popcll(same & lt), cnt = __popcll(same);
+            const int at = valid ? cw[r] : 0;
+            if (valid) rbuf[j] = ((at + rank) << 12) | r;
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
+            if (valid && rank == cnt - 1) cw[r] = (uint16_t)(at + cnt);
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
+        }
+        sync();
+        for (int j = tid; j < ns; j += NC) {
+            const int e = rbuf[j], r = e & 0xfff;
+            int pos = start[r] + (e >> 12);
+            for (int w2 = 0; (w2 + 1) * quarter <= j; w2++) pos += wc[w2 * nvs + r];
+            sortj[pos] = (uint16_t)j;
+            sortk[pos] = kbuf[j];
+        }
+    }
+    sync();
+    if (pre)  // both loader waves' rows have landed (bounded wait)
+        for (int spin = 0; spin < (1 << 23); spin++) {
+            if (__hip_atomic_load(&s_rows_in, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) >=
+                kLoaders)
+                break;
+            __builtin_amdgcn_s_sleep(1);
+        }
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+
+    // 5. means, over the occupied voxels in voxel order. pre: one pass over
+    // the prefetched rows (a voxel's rows through sortj). Else in segments
+    // whose points (a contiguous run of the sorted list) fit the stage; a
+    // voxel with more points than that is summed from global memory by
+    // wave 0.
+    const int gpv = VEC ? C / 8 : C;  // columns: 8-channel groups, or channels
+    // items (o, q): thread tid keeps column q = tid % gpv of voxels o0 + r0,
+    // o0 + r0 + rs, ... (rs = NC / gpv; when a row has more columns than
+    // there are threads, columns are strided instead)
+    const int rs = max(1, NC / gpv);
+    const int q0 = gpv <= NC ? tid % gpv : tid, r0 = gpv <= NC ? tid / gpv : 0;
+    const bool col_ok = gpv <= NC ? r0 < rs : true;
+    const int qstep = gpv <= NC ? gpv : NC;
+    // the mean of voxel occ[o] over column q, its rows in the stage at
+    // row_of(sorted position): the rows in sorted order (point order), fp64
+    auto mean_item = [&](int o, int q, const FT* stage, auto row_of) {
+        const int v = occ[o], nk = hist[v], p0 = start[v];
+        if (VEC) {
+            double acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+            for (int j = 0; j < nk; j++) {
+                float f[8];
+                stage8(stage + (size_t)row_of(p0 + j) * C + q * 8, f);
+#pragma unroll
+                for (int i = 0; i < 8; i++) acc[i] += (double)f[i];
+            }
+            float mean[8];
+#pragma unroll
+            for (int i = 0; i < 8; i++) mean[i] = (float)(acc[i] / (double)nk);
+            store8<GT>(out + (size_t)v * C + q * 8, mean);
+        } else {
+            double acc = 0.0;
+            for (int j = 0; j < nk; j++) acc += (double)stage1(stage + (size_t)row_of(p0 + j) * C + q);
+            store1<GT>(out + (size_t)v * C + q, (float)(acc / (double)nk));
+        }
+    };
+    // The staged voxels of occ[oa .. ob): those of up to kSplit points one
+    // item (o, q) a thread; heavier ones (VEC) one voxel a wave, taken in
+    // turn, lane sub * ng + cl summing rows sub, sub + S, ... of column group
+    // cg0 + cl (S = 64 / ng subsets), the S sums added in subset order.
+    auto staged_means = [&](int oa, int ob, const FT* stage, auto row_of) {
+        for (int q = q0; col_ok && q < gpv; q += qstep)
+            for (int o = oa + r0; o < ob; o += rs)
+                if (!VEC || hist[occ[o]] <= kSplit) mean_item(o, q, stage, row_of);
+        if (!VEC) return;
+        int nheavy = 0;
+        for (int o0 = oa; o0 < ob; o0 += 64) {
+            const int o = o0 + lane;
+            unsigned long long hm = __ballot(o < ob && hist[occ[min(o, ob - 1)]] > kSplit);
+            while (hm) {
+                const int oh = o0 + __ffsll((long long)hm) - 1;
+                hm &= hm - 1;
+                if (nheavy++ % (NC / 64) != wave) continue;
+                const int v = occ[oh], nk = hist[v], p0 = start[v];
+                for (int cg0 = 0; cg0 < gpv; cg0 += 64) {
+                    const int ng = min(64, gpv - cg0);
+                    const int S = 64 / ng, sub = lane / ng, cl = lane % ng;
+                    double acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+                    if (sub < S)
+                        for (int j = sub; j < nk; j += S) {
+                            float f[8];
+                            stage8(stage + (size_t)row_of(p0 + j) * C + (cg0 + cl) * 8, f);
+#pragma unroll
+                            for (int i = 0; i < 8; i++) acc[i] += (double)f[i];
+                        }
+                    double tot[8];
+#pragma unroll
+                    for (int i = 0; i < 8; i++) tot[i] = __shfl(acc[i], cl, 64);
+                    for (int s2 = 1; s2 < S; s2++)
+#pragma unroll
+                        for (int i = 0; i < 8; i++) tot[i] += __shfl(acc[i], s2 * ng + cl, 64);
+                    if (lane < ng) {
+                        float mean[8];
+#pragma unroll
+                        for (int i = 0; i < 8; i++) mean[i] = (float)(tot[i] / (double)nk);
+                        store8<GT>(out + (size_t)v * C + (cg0 + lane) * 8, mean);
+                    }
+                }
+            }
+        }
+    };
+    if (pre) {
+        staged_means(0, n_occ, (const FT*)s_stage, [&](int p) { return (int)sortj[p]; });
+    } else {
+        auto seg_end = [&](int o) { return o < n_occ ? (int)start[occ[o]] : ns; };
+        int oa = 0;
+        while (oa < n_occ) {
+            const int pa = start[occ[oa]];
+            // the last ob with seg_end(ob) - pa <= cap_pre (binary search)
+            int lo = oa, hi = n_occ;
+            while (lo < hi) {
+                const int mid = (lo + hi + 1) >> 1;
+                if (seg_end(mid) - pa <= cap_pre) lo = mid; else hi = mid - 1;
+            }
+            const int ob = lo;
+            if (ob == oa) {
+                // one voxel beyond the stage: wave 0 sums it from global memory
+                const int v = occ[oa], nk = hist[v];
+                if (wave == 0) {
+                    for (int cg0 = 0; cg0 < gpv; cg0 += 64) {
+                        const int ng = min(64, gpv - cg0);
+                        if (VEC) {
+                            double tot[8];
+                            wave_sum8<FT>(fb, feat_ld, sortk, pa, nk, cg0, ng, tot);
+                            if (lane < ng) {
+                                float mean[8];
+#pragma unroll
+                                for (int i = 0; i < 8; i++) mean[i] = (float)(tot[i] / (double)nk);
+                                store8<GT>(out + (size_t)v * C + (cg0 + lane) * 8, mean);
+                            }
+                        } else if (lane < ng) {
+                            double acc = 0.0;
+                            for (int j = pa; j < pa + nk; j++)
+                                acc += (double)load1<FT>(fb + (size_t)sortk[j] * feat_ld + cg0 + lane);
+                            store1<GT>(out + (size_t)v * C + cg0 + lane, (float)(acc / (double)nk));
+                        }
+                    }
+                }
+                oa++;
+                continue;
+            }
+            const int np = seg_end(ob) - pa;
+            if (VEC) {
+                dma_rows<NC, FT>(s_stage, np, C, fb, feat_ld,
+                                 [&](int r) { return (int)sortk[pa + r]; }, wave);
+                __builtin_amdgcn_s_waitcnt(0);
+            } else {
+                // channel by channel: column q of rows r0, r0 + rs, ...
+                FT* st = (FT*)s_stage;
+                for (int q = q0; col_ok && q < gpv; q += qstep)
+                    for (int r = r0; r < np; r += rs)
+                        st[(size_t)r * C + q] = fb[(size_t)sortk[pa + r] * feat_ld + q];
+            }
+            sync();
+            staged_means(oa, ob, (const FT*)s_stage, [&](int p) { return p - pa; });
+            sync();  // the stage is free again
+            oa = ob;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
 // Tile fill: one workgroup per (tile t of TV voxels, cloud b).
 //
 // Dynamic LDS: hist[TV] points per voxel, start[TV+1] exclusive prefix,
@@ -864,9 +1558,8 @@ __device__ void tile_fill_range(const TileLds& L, int lo, int hi, int base, cons
     if (!last) lds_barrier();
 }
 
-// The tile's points among ids[0 .. N): count per voxel and keep (index,
-// voxel) while they fit. Reads 16 ids per thread per round when the array
-// is 16-byte aligned.
+// One of the tile's points (index k, voxel r in the tile): count it per
+// voxel and keep (index, voxel) while they fit.
 __device__ __forceinline__ void tile_collect_one(const TileLds& L, int k, int r, int nv, int CAP,
                                                  int* s_ntile) {
     if (r >= 0 && r < nv) {
@@ -882,8 +1575,8 @@ __device__ __forceinline__ void tile_collect_one(const TileLds& L, int k, int r,
 // The rest of a tile once its points are collected (L.hist, L.kbuf/rbuf):
 // counts out, prefix over the voxels, counting sort, zero rows (zero_rows),
 // means. each_point(fn) calls fn(point, voxel - v0) for every point of the
-// cloud that may lie in the tile (for the segmented passes, when the tile
-// holds more than CAP points).
+// tile's bucket (for the segmented passes, when the tile holds more than
+// CAP points).
 template <int NT, typename FT, typename GT, bool VEC, typename EachPoint>
 __device__ void tile_finish(const TileLds& L, int TV, int nv, int CAP, int32_t* cnt, GT* out,
                             const FT* fb, int feat_ld, int C, bool zero_rows, int stage_bytes,
@@ -974,151 +1667,94 @@ __device__ void tile_finish(const TileLds& L, int TV, int nv, int CAP, int32_t* 
     }
 }
 
+// Tile fill of a large cloud whose points are bucketed by tile: one
+// workgroup per (tile t, cloud b) reads its bucket.
 template <int NT, typename FT, typename GT, bool VEC>
 __global__ __launch_bounds__(NT) void pv_voxel_tile_kernel(
-    const int32_t* __restrict__ vox_id, const FT* __restrict__ feats, int feat_ld, int N, int C,
-    int R, int TV, int CAP, int stage_bytes, int zero_rows, GT* __restrict__ grid,
-    int32_t* __restrict__ counts, int* bk, const int* __restrict__ br,
-    const int* __restrict__ tcount, const int* __restrict__ tstart, int T, int* hq) {
+    const FT* __restrict__ feats, int feat_ld, int N, int C, int R, int TV, int CAP,
+    int stage_bytes, int zero_rows, GT* __restrict__ grid, int32_t* __restrict__ counts,
+    int* bk, const int* __restrict__ br, const int* __restrict__ tcount,
+    const int* __restrict__ tstart, int T, int* hq) {
     extern __shared__ __attribute__((aligned(16))) char smem[];
     __shared__ int scan_lds[NT / 64];
     __shared__ int s_ntile, s_nheavy;
     const TileLds L = tile_lds(smem, TV, CAP);
 
     const int t = blockIdx.x, b = blockIdx.y;
-    const bool bucketed = bk != nullptr;
-    const int bstart = bucketed ? tstart[(size_t)b * T + t] : 0;
-    const int btotal = bucketed ? tcount[(size_t)b * T + t] : 0;
+    const int bstart = tstart[(size_t)b * T + t];
+    const int btotal = tcount[(size_t)b * T + t];
     const int V = R * R * R;
     const int v0 = t * TV, nv = min(TV, V - v0);
-    const int32_t* ids = vox_id + (size_t)b * N;
     const FT* fb = feats + (size_t)b * N * feat_ld;
     GT* out = grid + ((size_t)b * V + v0) * C;
 
     for (int i = threadIdx.x; i < TV; i += NT) L.hist[i] = 0;
     if (threadIdx.x == 0) s_ntile = 0;
     lds_barrier();
-    // 1. the tile's points: its bucket when the points were bucketed by tile
-    // (large clouds), else a scan of all the cloud's ids
-    const int* kb = bucketed ? bk + (size_t)b * N + bstart : nullptr;
-    const int* rb = bucketed ? br + (size_t)b * N + bstart : nullptr;
-    // every point of the tile (bucketed) or of the cloud, as (index, voxel - v0)
+    // 1. the tile's points: its bucket, as (index, voxel - v0)
+    const int* kb = bk + (size_t)b * N + bstart;
+    const int* rb = br + (size_t)b * N + bstart;
     auto each_point = [&](auto fn) {
-        if (bucketed)
-            for (int j = threadIdx.x; j < btotal; j += NT) fn(kb[j], rb[j]);
-        else
-            for (int k = threadIdx.x; k < N; k += NT) fn(k, ids[k] - v0);
+        for (int j = threadIdx.x; j < btotal; j += NT) fn(kb[j], rb[j]);
     };
-    if (bucketed) {
-        for (int j0 = threadIdx.x; j0 < btotal; j0 += 4 * NT) {
-            int kk[4], rr[4];
+    for (int j0 = threadIdx.x; j0 < btotal; j0 += 4 * NT) {
+        int kk[4], rr[4];
 #pragma unroll
-            for (int u = 0; u < 4; u++) {
-                const int j = j0 + u * NT;
-                kk[u] = j < btotal ? kb[j] : 0;
-                rr[u] = j < btotal ? rb[j] : -1;
-            }
-#pragma unroll
-            for (int u = 0; u < 4; u++) tile_collect_one(L, kk[u], rr[u], nv, CAP, &s_ntile);
+        for (int u = 0; u < 4; u++) {
+            const int j = j0 + u * NT;
+            kk[u] = j < btotal ? kb[j] : 0;
+            rr[u] = j < btotal ? rb[j] : -1;
         }
-    } else {
-        int k0 = 0;
-        if (((uintptr_t)ids & 15) == 0) {
-            const int n16 = N / 16 * 16;  // rounds of 4 int4 loads per thread
-            for (int kq = threadIdx.x * 4; kq < n16; kq += NT * 16) {
-                int4 q[4];
 #pragma unroll
-                for (int u = 0; u < 4; u++) {
-                    const int k = kq + u * NT * 4;
-                    q[u] = k < n16 ? *(const int4*)(ids + k) : make_int4(-1 - v0, 0, 0, 0);
-                }
-#pragma unroll
-                for (int u = 0; u < 4; u++) {
-                    const int k = kq + u * NT * 4;
-                    if (k < n16) {
-                        tile_collect_one(L, k, q[u].x - v0, nv, CAP, &s_ntile);
-                        tile_collect_one(L, k + 1, q[u].y - v0, nv, CAP, &s_ntile);
-                        tile_collect_one(L, k + 2, q[u].z - v0, nv, CAP, &s_ntile);
-                        tile_collect_one(L, k + 3, q[u].w - v0, nv, CAP, &s_ntile);
-                    }
-                }
-            }
-            k0 = n16;
-        }
-        for (int k = k0 + threadIdx.x; k < N; k += NT)
-            tile_collect_one(L, k, ids[k] - v0, nv, CAP, &s_ntile);
+        for (int u = 0; u < 4; u++) tile_collect_one(L, kk[u], rr[u], nv, CAP, &s_ntile);
     }
     lds_barrier();
-    const HeavyOut ho{bucketed ? hq : nullptr, bucketed ? bk + (size_t)b * N + bstart : nullptr, b,
-                      v0, bstart};
+    const HeavyOut ho{hq, bk + (size_t)b * N + bstart, b, v0, bstart};
     tile_finish<NT, FT, GT, VEC>(L, TV, nv, CAP, counts + (size_t)b * V + v0, out, fb, feat_ld, C,
                                  zero_rows != 0, stage_bytes, scan_lds, &s_nheavy, each_point, ho);
 }
 
-// Tile shape. Small clouds (every tile scans all N ids, cheap): about 2048
-// tiles of 128 threads, about 18 KB of LDS, so that eight workgroups fit per
-// CU and every tile is resident at once; coarse grids go down to 32 voxels
-// per tile to get there. Large clouds (points bucketed by tile beforehand):
-// about 1024 tiles of 256 threads, so that a dense cluster spreads over
-// several workgroups.
-struct TileShape {
-    int nt, tv;
-};
-TileShape tile_shape(int B, int V, int N) {
-    const bool small_cloud = N <= kSmallMaxN;
-    const long long want = small_cloud ? 2048 : 1024;
-    int tv = 1024;
-    while (tv > 32 && (long long)B * ((V + tv - 1) / tv) < want) tv >>= 1;
-    return TileShape{small_cloud ? 128 : 256, tv};
-}
-
-
-// LDS budget of the tile kernel: no feature stage (each (voxel, channel
-// group) sums straight from memory) and room for the tile's points, tiles
-// with more points taking the segmented path. Large clouds: kMaxCap points.
-// Small clouds: as many as keep every tile of the grid resident at once (the
-// 160 KB of a CU shared by its tiles, less 2 KB of slack), at least 256, at
-// most kMaxCap (coarse grids, with many points per tile, have few tiles).
-// Dynamic LDS beyond 64 KB has to be granted per kernel; when that fails the
-// capacity shrinks to what 64 KB holds.
-template <typename K>
-void tile_budget(K kernel, int NT, int TV, int N, long tiles, int& cap, int& stage) {
-    const bool small_cloud = N <= kSmallMaxN;
-    int want = kMaxCap;
-    if (small_cloud) {
-        const long per_cu = std::max(1L, (tiles + kCUs - 1) / kCUs);
-        const long budget = std::min<long>(65536, 160 * 1024 / per_cu - 2048);
-        const long fit = (budget - (long)tile_lds_bytes(NT, TV, 0, 0)) / 12;
-        want = (int)std::max(256L, std::min<long>(kMaxCap, fit));
-    }
-    cap = N < want ? (N > 0 ? N : 1) : want;
-    stage = 0;
-    const size_t small = 65536;
-    const size_t want_bytes = tile_lds_bytes(NT, TV, cap, stage);
-    if (want_bytes <= small) return;
-    // the grant is per kernel and lasts for the process: ask once per kernel
-    // and size (a launch being captured into a graph then makes no other call)
+// Dynamic LDS beyond 64 KB is granted per kernel (once per kernel and size:
+// a launch being captured into a graph then makes no other call).
+bool grant_lds(const void* kernel, size_t bytes) {
+    if (bytes <= 65536) return true;
     static std::mutex mu;
     static std::unordered_map<const void*, size_t> granted;
-    {
-        std::lock_guard<std::mutex> lock(mu);
-        auto it = granted.find((const void*)kernel);
-        if (it != granted.end() && want_bytes <= it->second) return;
+    std::lock_guard<std::mutex> lock(mu);
+    auto it = granted.find(kernel);
+    if (it != granted.end() && bytes <= it->second) return true;
+    if (hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes) !=
+        hipSuccess) {
+        (void)hipGetLastError();
+        return false;
     }
-    if (hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)want_bytes) == hipSuccess) {
-        std::lock_guard<std::mutex> lock(mu);
-        size_t& g = granted[(const void*)kernel];
-        g = std::max(g, want_bytes);
-        return;
-    }
-    (void)hipGetLastError();
-    stage = 0;
-    while (cap > 1 && tile_lds_bytes(NT, TV, cap, stage) > small) cap >>= 1;
+    granted[kernel] = std::max(granted[kernel], bytes);
+    return true;
 }
 
-// Tiles' point sources: the points bucketed by tile (large clouds) or none
-// (each tile scans all ids).
+// Tile shape of a large cloud (points bucketed by tile beforehand): about
+// 1024 tiles of 256 threads, so that a dense cluster spreads over several
+// workgroups.
+constexpr int kTileNT = 256;
+int tile_voxels(int B, int V) {
+    int tv = 1024;
+    while (tv > 32 && (long long)B * ((V + tv - 1) / tv) < 1024) tv >>= 1;
+    return tv;
+}
+
+// LDS of the tile kernel: no feature stage (each (voxel, channel group) sums
+// straight from memory) and room for kMaxCap of the tile's points, tiles
+// with more points taking the segmented path. Dynamic LDS beyond 64 KB is
+// granted per kernel; when that fails the capacity shrinks to what 64 KB
+// holds.
+template <typename K>
+void tile_budget(K kernel, int NT, int TV, int N, int& cap) {
+    cap = N < kMaxCap ? (N > 0 ? N : 1) : kMaxCap;
+    if (grant_lds((const void*)kernel, tile_lds_bytes(NT, TV, cap, 0))) return;
+    while (cap > 1 && tile_lds_bytes(NT, TV, cap, 0) > 65536) cap >>= 1;
+}
+
+// The points bucketed by tile.
 struct Buckets {
     int* bk;
     const int* br;
@@ -1128,23 +1764,22 @@ struct Buckets {
     int* hq;  // heavy-voxel queue (nullptr: none)
 };
 
-template <int NT, typename FT, typename GT>
-void launch_tiles_nt(const int32_t* ids, const void* feats, int feat_ld, int B, int N, int C,
-                     int R, int TV, void* grid, int32_t* counts, bool vec, bool zero_rows,
-                     const Buckets& bu, hipStream_t s) {
-    const int V = R * R * R;
+template <typename FT, typename GT>
+void launch_tiles(const void* feats, int feat_ld, int B, int N, int C, int R, void* grid,
+                  int32_t* counts, bool vec, const Buckets& bu, hipStream_t s) {
+    const int V = R * R * R, TV = tile_voxels(B, V);
     dim3 g((V + TV - 1) / TV, B);
-    int cap, stage;
+    int cap;
     if (vec) {
-        auto k = pv_voxel_tile_kernel<NT, FT, GT, true>;
-        tile_budget(k, NT, TV, N, (long)g.x * g.y, cap, stage);
-        hipLaunchKernelGGL(k, g, dim3(NT), tile_lds_bytes(NT, TV, cap, stage), s, ids,
-                           (const FT*)feats, feat_ld, N, C, R, TV, cap, stage, (int)zero_rows,
-                           (GT*)grid, counts, bu.bk, bu.br, bu.tcount, bu.tstart, bu.T, bu.hq);
+        auto k = pv_voxel_tile_kernel<kTileNT, FT, GT, true>;
+        tile_budget(k, kTileNT, TV, N, cap);
+        hipLaunchKernelGGL(k, g, dim3(kTileNT), tile_lds_bytes(kTileNT, TV, cap, 0), s,
+                           (const FT*)feats, feat_ld, N, C, R, TV, cap, 0, 1, (GT*)grid, counts,
+                           bu.bk, bu.br, bu.tcount, bu.tstart, bu.T, bu.hq);
     } else {
-        auto k = pv_voxel_tile_kernel<NT, FT, GT, false>;
-        tile_budget(k, NT, TV, N, (long)g.x * g.y, cap, stage);
-        hipLaunchKernelGGL(k, g, dim3(NT), tile_lds_bytes(NT, TV, cap, stage), s, ids,
+        auto k = pv_voxel_tile_kernel<kTileNT, FT, GT, false>;
+        tile_budget(k, kTileNT, TV, N, cap);
+        hipLaunchKernelGGL(k, g, dim3(kTileNT), tile_lds_bytes(kTileNT, TV, cap, 0), s,
                            (const FT*)feats, feat_ld, N, C, R, TV, cap, 0, 0, (GT*)grid, counts,
                            bu.bk, bu.br, bu.tcount, bu.tstart, bu.T, bu.hq);
     }
@@ -1259,18 +1894,6 @@ __global__ __launch_bounds__(256) void pv_voxel_heavy_mean_kernel(int C, int R,
     }
 }
 
-template <typename FT, typename GT>
-void launch_tiles(const int32_t* ids, const void* feats, int feat_ld, int B, int N, int C, int R,
-                  void* grid, int32_t* counts, bool vec, bool zero_rows, const Buckets& bu,
-                  hipStream_t s) {
-    const TileShape t = tile_shape(B, R * R * R, N);
-    if (t.nt == 128)
-        launch_tiles_nt<128, FT, GT>(ids, feats, feat_ld, B, N, C, R, t.tv, grid, counts, vec,
-                                     zero_rows, bu, s);
-    else
-        launch_tiles_nt<256, FT, GT>(ids, feats, feat_ld, B, N, C, R, t.tv, grid, counts, vec,
-                                     zero_rows, bu, s);
-}
 
 // Zero fill byte by byte, for grids the 16-byte path cannot cover.
 __global__ __launch_bounds__(256) void pv_zero_elems_kernel(char* __restrict__ p, size_t n) {
@@ -1289,8 +1912,8 @@ struct VoxWs {
 VoxWs carve_ws(void* ws, int B, int N, int R, size_t* bytes) {
     const int G = (N + kNormPts - 1) / kNormPts;
     const int V = R * R * R;
-    const TileShape ts = tile_shape(B, V, N);
     const bool large = N > kSmallMaxN;
+    const int TV = tile_voxels(B, V);
     size_t off = 0;
     VoxWs w;
     auto take = [&](size_t n) {
@@ -1304,8 +1927,8 @@ VoxWs carve_ws(void* ws, int B, int N, int R, size_t* bytes) {
     w.split.pA = (float*)take((size_t)B * G * 3 * sizeof(float));
     w.split.pQ = (long long*)take((size_t)B * G * 3 * sizeof(long long));
     w.split.pM = (double*)take((size_t)B * G * sizeof(double));
-    w.split.TV = ts.tv;
-    w.split.T = large ? (V + ts.tv - 1) / ts.tv : 0;
+    w.split.TV = TV;
+    w.split.T = large ? (V + TV - 1) / TV : 0;
     const size_t nt = (size_t)B * w.split.T;
     w.split.tcount = (int*)take(nt * sizeof(int));
     w.split.tcursor = (int*)take(nt * sizeof(int));
@@ -1355,27 +1978,25 @@ GridPlan grid_plan(const void* feats, bool feat_bf16, int feat_ld, int B, int C,
     return g;
 }
 
-// Everything after the voxel indices (and, for large clouds, the tile
-// buckets) are known: the tile kernel, then the heavy-voxel kernels.
-pvconv_status voxelize_fill(const int32_t* ids, const void* feats, bool feat_bf16, int feat_ld,
-                            int B, int N, int C, int R, void* grid, bool grid_bf16,
-                            int32_t* counts, const VoxWs& w, const GridPlan& gp,
-                            hipStream_t s) {
+// A large cloud once its voxel indices and tile buckets are known: the tile
+// kernel, then the heavy-voxel kernels.
+pvconv_status voxelize_fill(const void* feats, bool feat_bf16, int feat_ld, int B, int N, int C,
+                            int R, void* grid, bool grid_bf16, int32_t* counts, const VoxWs& w,
+                            const GridPlan& gp, hipStream_t s) {
     const bool vec = gp.vec;
-    const Buckets bu = N > kSmallMaxN
-                           ? Buckets{w.split.bk, w.split.br, w.split.tcount, w.split.tstart,
-                                     w.split.T, vec && C <= kHeavyMaxC ? w.split.hq : nullptr}
-                           : Buckets{nullptr, nullptr, nullptr, nullptr, 0, nullptr};
+    const Buckets bu{w.split.bk, w.split.br, w.split.tcount, w.split.tstart, w.split.T,
+                     vec && C <= kHeavyMaxC ? w.split.hq : nullptr};
     if (!gp.grid_ok) {
         // a grid that 16-byte stores cannot cover: the plain element kernel
         hipLaunchKernelGGL(pv_zero_elems_kernel, dim3(1024), dim3(256), 0, s, (char*)grid,
                            gp.gbytes);
     }
-    // heavy voxels queued by the tiles (large clouds, 16-byte rows)
+    // heavy voxels queued by the tiles (16-byte rows)
     const int hgrid = std::min(256, w.split.hmax);
-    auto heavy = [&](auto ft, auto gt) {
+    auto run = [&](auto ft, auto gt) {
         typedef decltype(ft) FT;
         typedef decltype(gt) GT;
+        launch_tiles<FT, GT>(feats, feat_ld, B, N, C, R, grid, counts, vec, bu, s);
         if (bu.hq && hgrid > 0) {
             hipLaunchKernelGGL((pv_voxel_heavy_kernel<FT>), dim3(hgrid), dim3(256), 0, s,
                                (const FT*)feats, feat_ld, N, C, w.split.bk, w.split.hq,
@@ -1385,26 +2006,78 @@ pvconv_status voxelize_fill(const int32_t* ids, const void* feats, bool feat_bf1
         }
     };
     if (feat_bf16) {
-        if (grid_bf16)
-            launch_tiles<uint16_t, uint16_t>(ids, feats, feat_ld, B, N, C, R, grid, counts, vec,
-                                             vec, bu, s);
-        else
-            launch_tiles<uint16_t, float>(ids, feats, feat_ld, B, N, C, R, grid, counts, vec, vec,
-                                          bu, s);
+        if (grid_bf16) run(uint16_t{}, uint16_t{}); else run(uint16_t{}, float{});
     } else {
-        if (grid_bf16)
-            launch_tiles<float, uint16_t>(ids, feats, feat_ld, B, N, C, R, grid, counts, vec, vec,
-                                          bu, s);
-        else
-            launch_tiles<float, float>(ids, feats, feat_ld, B, N, C, R, grid, counts, vec, vec, bu,
-                                       s);
-    }
-    if (feat_bf16) {
-        if (grid_bf16) heavy(uint16_t{}, uint16_t{}); else heavy(uint16_t{}, float{});
-    } else {
-        if (grid_bf16) heavy(float{}, uint16_t{}); else heavy(float{}, float{});
+        if (grid_bf16) run(float{}, uint16_t{}); else run(float{}, float{});
     }
     return pv_launch_status();
+}
+
+}  // namespace
+
+namespace {
+
+
+// Clouds of up to kSmallMaxN points: the slab kernel does the whole
+// voxelisation (ids_in given: from those voxel indices, no normalisation).
+// Its LDS holds the slab's points and per-voxel tables, then as many staged
+// mean rows as fit in a CU's 160 KB.
+template <typename FT, typename GT, bool VEC, bool GVEC>
+pvconv_status launch_slab_t(const float* coords, const int32_t* ids_in, const void* feats,
+                            int feat_ld, int B, int N, int C, int R, void* grid, int32_t* counts,
+                            int32_t* vox_id, float* pn, const PvPackJobs& jobs, hipStream_t s) {
+    const int V = R * R * R;
+    const SlabShape sh = slab_shape(B, V, N);
+    const int npack = (pv_pack_blocks(jobs) + 1) / 2;
+    // dynamic LDS: the tables and the sort's working set (at most ~57 KB for
+    // nvs <= 2048, N <= 4096, next to the kernel's 97 KB static stage); the
+    // stage holds cap_pre raw feature rows
+    const SlabLayout LY = slab_layout(sh.nvs, N);
+    const size_t row = (size_t)C * sizeof(FT);
+    const int cap_pre = (int)std::min((size_t)kStageBytes / row, (size_t)std::max(N, 1));
+    const size_t bytes = (size_t)LY.pre;
+    const dim3 g((unsigned)((size_t)B * sh.S + npack));
+    auto go = [&](auto kernel, int nt) {
+        if (!grant_lds((const void*)kernel, bytes)) return PVCONV_EHIP;
+        hipLaunchKernelGGL(kernel, g, dim3(nt), bytes, s, coords, ids_in, (const FT*)feats,
+                           feat_ld, N, C, R, sh.nvs, sh.S, cap_pre, (GT*)grid, counts, vox_id,
+                           pn, jobs, npack);
+        return pv_launch_status();
+    };
+    // points per compute thread: the cloud over kSlabNC threads
+    static_assert(kSlabNC == 512, "points per compute thread below assume 512 threads");
+    if (N <= 1024) return go(pv_voxel_slab_kernel<2, kSlabNT, FT, GT, VEC, GVEC>, kSlabNT);
+    if (N <= 2048) return go(pv_voxel_slab_kernel<4, kSlabNT, FT, GT, VEC, GVEC>, kSlabNT);
+    return go(pv_voxel_slab_kernel<8, kSlabNTSmall, FT, GT, VEC, GVEC>, kSlabNTSmall);
+}
+
+pvconv_status launch_slab(const float* coords, const int32_t* ids_in, const void* feats,
+                          bool feat_bf16, int feat_ld, int B, int N, int C, int R, void* grid,
+                          bool grid_bf16, int32_t* counts, int32_t* vox_id, float* pn, bool vec,
+                          const PvPackJobs& jobs, hipStream_t s) {
+    // zero stores of whole 16-byte pieces need 16-byte grid rows
+    const bool gvec = pv_aligned16(grid) && (C * (grid_bf16 ? 2 : 4)) % 16 == 0;
+    // (vec implies 16-byte grid rows)
+#define PV_SLAB(FT, GT)                                                                        \
+    if (vec)                                                                                   \
+        return launch_slab_t<FT, GT, true, true>(coords, ids_in, feats, feat_ld, B, N, C, R,   \
+                                                 grid, counts, vox_id, pn, jobs, s);           \
+    if (gvec)                                                                                  \
+        return launch_slab_t<FT, GT, false, true>(coords, ids_in, feats, feat_ld, B, N, C, R,  \
+                                                  grid, counts, vox_id, pn, jobs, s);          \
+    return launch_slab_t<FT, GT, false, false>(coords, ids_in, feats, feat_ld, B, N, C, R,     \
+                                               grid, counts, vox_id, pn, jobs, s)
+    if (feat_bf16) {
+        if (grid_bf16) {
+            PV_SLAB(uint16_t, uint16_t);
+        }
+        PV_SLAB(uint16_t, float);
+    }
+    if (grid_bf16) {
+        PV_SLAB(float, uint16_t);
+    }
+    PV_SLAB(float, float);
+#undef PV_SLAB
 }
 
 }  // namespace
@@ -1428,25 +2101,13 @@ pvconv_status pv_launch_voxelize(const float* coords, const void* feats, bool fe
     // grid is zeroed first, alongside the normalisation, and the tile kernel
     // overwrites the occupied rows.
     const GridPlan gp = grid_plan(feats, feat_bf16, feat_ld, B, C, R, grid, grid_bf16);
+    if (N <= kSmallMaxN)
+        return launch_slab(coords, nullptr, feats, feat_bf16, feat_ld, B, N, C, R, grid,
+                           grid_bf16, counts, ids, pn, gp.vec, jobs, s);
     const int zb = gp.zb;
     const size_t n16 = gp.n16;
     uint4* grid16 = (uint4*)grid;
-    if (N <= kSmallMaxN) {
-        const int slices = (N + 255) / 256;
-        const int nid = slices * B;
-        if (nid + npack + zb > 0) {
-            const dim3 gi(nid + npack + zb);
-            if (N <= 1024)
-                hipLaunchKernelGGL(pv_voxel_ids_kernel<4>, gi, dim3(256), 0, s, coords, N, R,
-                                   slices, nid, ids, pn, grid16, n16, jobs, npack);
-            else if (N <= 2048)
-                hipLaunchKernelGGL(pv_voxel_ids_kernel<8>, gi, dim3(256), 0, s, coords, N, R,
-                                   slices, nid, ids, pn, grid16, n16, jobs, npack);
-            else
-                hipLaunchKernelGGL(pv_voxel_ids_kernel<16>, gi, dim3(256), 0, s, coords, N, R,
-                                   slices, nid, ids, pn, grid16, n16, jobs, npack);
-        }
-    } else {
+    {
         const int nid = w.split.G * B;
         dim3 g(w.split.G, B);
         hipLaunchKernelGGL(pv_norm_absmax_kernel, dim3(nid + npack + zb), dim3(kNormThreads), 0,
@@ -1458,8 +2119,7 @@ pvconv_status pv_launch_voxelize(const float* coords, const void* feats, bool fe
         hipLaunchKernelGGL(pv_bucket_kernel, g, dim3(kNormThreads),
                            (size_t)2 * w.split.T * sizeof(int), s, ids, N, w.split);
     }
-    return voxelize_fill(ids, feats, feat_bf16, feat_ld, B, N, C, R, grid, grid_bf16, counts, w,
-                         gp, s);
+    return voxelize_fill(feats, feat_bf16, feat_ld, B, N, C, R, grid, grid_bf16, counts, w, gp, s);
 }
 
 pvconv_status pv_launch_voxelize_from_ids(const int32_t* ids, const void* feats, bool feat_bf16,
@@ -1470,13 +2130,10 @@ pvconv_status pv_launch_voxelize_from_ids(const int32_t* ids, const void* feats,
     VoxWs w = carve_ws(ws, B, N, R, nullptr);
     const GridPlan gp = grid_plan(feats, feat_bf16, feat_ld, B, C, R, grid, grid_bf16);
     uint4* grid16 = (uint4*)grid;
-    if (N <= kSmallMaxN) {
-        // the tiles scan the indices themselves; only a grid without 16-byte
-        // rows needs zeroing first
-        if (gp.zb > 0)
-            hipLaunchKernelGGL(pv_tile_reset_kernel, dim3(1 + gp.zb), dim3(kNormThreads), 0, s,
-                               w.split, 0, grid16, gp.n16);
-    } else {
+    if (N <= kSmallMaxN)
+        return launch_slab(nullptr, ids, feats, feat_bf16, feat_ld, B, N, C, R, grid, grid_bf16,
+                           counts, nullptr, nullptr, gp.vec, PvPackJobs{}, s);
+    {
         dim3 g(w.split.G, B);
         hipLaunchKernelGGL(pv_tile_reset_kernel, dim3(1 + gp.zb), dim3(kNormThreads), 0, s,
                            w.split, B, grid16, gp.n16);
@@ -1485,6 +2142,5 @@ pvconv_status pv_launch_voxelize_from_ids(const int32_t* ids, const void* feats,
         hipLaunchKernelGGL(pv_bucket_kernel, g, dim3(kNormThreads),
                            (size_t)2 * w.split.T * sizeof(int), s, ids, N, w.split);
     }
-    return voxelize_fill(ids, feats, feat_bf16, feat_ld, B, N, C, R, grid, grid_bf16, counts, w,
-                         gp, s);
+    return voxelize_fill(feats, feat_bf16, feat_ld, B, N, C, R, grid, grid_bf16, counts, w, gp, s);
 }

@@ -1,6 +1,6 @@
 """PVCNN segmentation network on the library's kernels (Section 5.1 "Models":
 PointNet with its per-point MLP layers replaced by PVConv; the part- and
-scene-segmentation networks of Sections 5.1 and 5.3).
+scene-segmentation networks of Sections 5.1 and 5.2).
 
 Every arithmetic step runs in libpvconv through the C-ABI calls of the
 binding; this module only lays out device buffers and orders the calls.

@@ -186,6 +186,9 @@ def _mlp(**kw):
     (dict(res=FAKE, res_ld=5), EINVAL), (dict(cb=FAKE, ppc=0), EINVAL), (dict(x=None), EINVAL),
     (dict(w=None), EINVAL), (dict(out=None), EINVAL), (dict(x_dt=5), EINVAL),
     (dict(act=-1), EINVAL), (dict(out=FAKE), EINVAL), (dict(x=FAKE_ODD), EINVAL),
+    # out shares bytes with x (100 rows of 64 fp32 = 25600 bytes from FAKE)
+    (dict(out=ctypes.c_void_p(0x100000 + 25600 - 16)), EINVAL),
+    (dict(x=ctypes.c_void_p(0x200000 + 51200 - 16)), EINVAL),
     (dict(M=0), OK),
 ])
 def test_point_mlp_rejects(kw, status):
@@ -215,7 +218,7 @@ def _layer():
 
 
 def _fwd(lay, **kw):
-    a = dict(coords=FAKE, feats=FAKE, fdt=0, fld=0, B=2, N=100, out=FAKE, odt=0, old=0, ws=FAKE,
+    a = dict(coords=FAKE, feats=FAKE, fdt=0, fld=0, B=2, N=100, out=FAKE2, odt=0, old=0, ws=FAKE,
              wsb=1 << 40, s=None)
     a.update(kw)
     return L.pvconv_forward(a["coords"], a["feats"], a["fdt"], a["fld"], a["B"], a["N"],
@@ -225,7 +228,7 @@ def _fwd(lay, **kw):
 
 def _fwd_ex(lay, **kw):
     a = dict(coords=FAKE, feats=FAKE, fdt=0, fld=0, B=2, N=100, ids=FAKE, norm=FAKE, given=1,
-             out=FAKE, odt=0, old=0, ws=FAKE, wsb=1 << 40, s=None)
+             out=FAKE2, odt=0, old=0, ws=FAKE, wsb=1 << 40, s=None)
     a.update(kw)
     return L.pvconv_forward_ex(a["coords"], a["feats"], a["fdt"], a["fld"], a["B"], a["N"],
                                ctypes.byref(lay), a["ids"], a["norm"], a["given"], a["out"],
@@ -317,6 +320,16 @@ def test_forward_rejects():
     assert _fwd(lay, coords=None) == EINVAL
     assert _fwd(lay, fld=3) == EINVAL
     assert _fwd(lay, B=0) == OK
+    # out must not share bytes with feats (an in-place layer would race):
+    # feats are 200 rows of 64 fp32 from FAKE
+    assert _fwd(lay, out=FAKE) == EINVAL
+    assert _fwd(lay, out=ctypes.c_void_p(0x100000 + 200 * 64 * 4 - 4)) == EINVAL
+    assert _fwd(lay, out=ctypes.c_void_p(0x100000 + 200 * 64 * 4), ws=None) == EWS
+    # column slices of one wider fp32 array (row stride 320): disjoint ranges pass
+    # validation, overlapping ones do not
+    assert _fwd(lay, fld=320, out=ctypes.c_void_p(0x100000 + 64 * 4), old=320, ws=None) == EWS
+    assert _fwd(lay, fld=320, out=ctypes.c_void_p(0x100000 + 60 * 4), old=320) == EINVAL
+    assert _fwd(lay, fld=320, out=ctypes.c_void_p(0x100000 + 200 * 4), old=320) == EINVAL
     for field, val, status in [("n_convs", 0, EINVAL), ("n_convs", 5, EINVAL), ("R", 0, EINVAL),
                                ("cout", 48, ENOTSUP), ("compute_dt", 4, EINVAL),
                                ("cin", 0, EINVAL), ("devox", 2, EINVAL), ("devox", -1, EINVAL)]:

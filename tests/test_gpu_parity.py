@@ -256,6 +256,32 @@ def test_voxelize_empty_clouds_give_zero_grids():
     assert g.numel() == 0
 
 
+@pytest.mark.parametrize("wl_idx,B,N,R,C", [(2, 4, 2048, 32, 64), (4, 2, 4096, 16, 64),
+                                         (1, 1, 1024, 8, 16), (3, 2, 2048, 16, 24)],
+                         ids=["partseg", "scene_R16", "fp32_layer", "C24"])
+def test_voxelize_small_clouds_sum_in_point_order(wl_idx, B, N, R, C):
+    # Clouds of up to 4096 points: within a voxel of up to 16 points the
+    # features are summed in point order from zero in fp64, as the oracle
+    # sums them, so those rows equal the oracle's, rounded to fp32, bit for
+    # bit; heavier voxels (subset sums added in a fixed order) are within
+    # the fp32 bound. Two runs give the same bits.
+    coords, feats = _cloud(wl_idx, B, N, C, seed=11)
+    pn, ids, grid, counts = _oracle_vox(coords, feats, R)
+    g1, c1, i1, p1 = pv.pvconv_voxelize(dev(coords), dev(feats), R, grid_dtype=torch.float32)
+    g2, c2, i2, p2 = pv.pvconv_voxelize(dev(coords), dev(feats), R, grid_dtype=torch.float32)
+    assert torch.equal(g1, g2) and torch.equal(c1, c2) and torch.equal(i1, i2)
+    assert np.array_equal(c1.cpu().numpy(), counts)
+    got = g1.cpu().numpy()
+    light = (counts >= 1) & (counts <= 16)
+    assert light.sum() > 0
+    assert np.array_equal(got[light], grid[light].astype(np.float32))
+    assert_rel(got, grid, 1e-5, "small-cloud grid fp32")
+    # bf16 grids: the same fp32 means, rounded once more
+    gb, _, _, _ = pv.pvconv_voxelize(dev(coords), dev(feats), R, grid_dtype=torch.bfloat16)
+    want = torch.as_tensor(grid[light].astype(np.float32)).to(torch.bfloat16)
+    assert torch.equal(gb.cpu()[torch.as_tensor(light)], want)
+
+
 def test_voxelize_is_deterministic_and_permutation_equivariant():
     coords, feats = _cloud(5, 1, 65536, 64)
     g1, c1, i1, p1 = pv.pvconv_voxelize(dev(coords), dev(feats), 64)
