@@ -8,6 +8,7 @@ from __future__ import annotations
 import concurrent.futures
 import glob
 import os
+import re
 import subprocess
 import sys
 
@@ -36,16 +37,45 @@ def peak_sources():
     return sorted(glob.glob(os.path.join(CSRC, "peak", "*.hip")))
 
 
+# Every kernel's resource usage is reported by the compiler; a kernel with
+# scratch (private memory, i.e. register spills or stack arrays) fails the
+# build, since scratch traffic goes to HBM and no kernel here is designed to
+# use it.
+RESOURCE_REMARKS = "-Rpass-analysis=kernel-resource-usage"
+_FN = re.compile(r"remark: Function Name: (\S+)")
+_SCRATCH = re.compile(r"remark:\s+ScratchSize \[bytes/lane\]: (\d+)")
+
+
+def scratch_kernels(remarks: str):
+    """(kernel, bytes per lane) for every function the remarks give scratch."""
+    bad, fn = [], None
+    for line in remarks.splitlines():
+        m = _FN.search(line)
+        if m:
+            fn = m.group(1)
+            continue
+        m = _SCRATCH.search(line)
+        if m and int(m.group(1)) > 0:
+            bad.append((fn, int(m.group(1))))
+    return bad
+
+
 def _compile(src, verbose):
     obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-    cmd = [HIPCC, *FLAGS, "-c", src, "-o", obj]
+    cmd = [HIPCC, *FLAGS, RESOURCE_REMARKS, "-c", src, "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
-    out = "\n".join(l for l in (r.stdout + r.stderr).splitlines()
-                    if "packed-fp32-ops" not in l and "is not a recognized feature" not in l)
+    lines = (r.stdout + r.stderr).splitlines()
+    out = "\n".join(l for l in lines
+                    if "packed-fp32-ops" not in l and "is not a recognized feature" not in l
+                    and "kernel-resource-usage" not in l)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{out}")
+    bad = scratch_kernels("\n".join(lines))
+    if bad:
+        listing = "\n".join(f"  {fn}: {n} bytes/lane" for fn, n in bad)
+        raise RuntimeError(f"kernels in {src} use scratch memory:\n{listing}")
     if verbose and out.strip():
         print(out)
     return obj
