@@ -12,8 +12,9 @@
  *
  * Conventions shared by every entry point
  *  - Array pointers are DEVICE pointers owned by the caller. The library keeps
- *    no device memory and no state between calls; scratch space is passed in
- *    as `workspace` where an entry point needs it.
+ *    no device memory and no state between calls, except the static array of
+ *    pvconv_conv3d_noalloc; scratch space is passed in as `workspace` where an
+ *    entry point needs it.
  *  - `stream` is a hipStream_t (NULL = the null stream). Every call only
  *    enqueues work on it: it never synchronises and never allocates.
  *  - Layouts are row-major, channels innermost ("channels last"):
@@ -75,6 +76,7 @@ typedef struct {
 #define PVCONV_MAX_CONV_CHANNELS 1024
 #define PVCONV_MAX_MLP_CHANNELS 16384
 #define PVCONV_MAX_CONVS 4
+#define PVCONV_CONV3D_NOALLOC_BYTES (4u << 20) /* pvconv_conv3d_noalloc's array */
 
 /* Human-readable name of a status code (static string). */
 const char* pvconv_status_string(pvconv_status s);
@@ -152,6 +154,27 @@ pvconv_status pvconv_conv3d(const void* x, int B, int R, int Cin, int Cout, cons
                             const float* bias, const pvconv_bn* bn, pvconv_act act, float slope,
                             pvconv_dtype dt, void* y, pvconv_dtype out_dt, void* workspace,
                             size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------- */
+/* pvconv_conv3d without a workspace argument, for callers that cannot       */
+/* allocate device memory (code under HIP graph capture, serving loops that  */
+/* must not call hipMalloc, harnesses that forbid it).                       */
+/* Arguments, results and errors as pvconv_conv3d. The repacked bf16 weights */
+/* go to a static device array of PVCONV_CONV3D_NOALLOC_BYTES inside the     */
+/* library, one per GPU, held until the process ends; a convolution whose    */
+/* pvconv_conv3d_workspace_size exceeds it returns PVCONV_EWORKSPACE (4 MiB  */
+/* takes Cin = Cout = 256). `stream` must belong to the current device       */
+/* (else PVCONV_EINVAL). Every call on one GPU uses that GPU's one array:    */
+/* calls that may run at the same time on one GPU (other streams, other     */
+/* host threads without ordering) race and give wrong results; calls in     */
+/* order on one stream are safe. Each call rewrites every byte of the array */
+/* it reads, so nothing depends on the previous call's contents. The first  */
+/* call on a device looks up the array's address (no allocation).           */
+/* ------------------------------------------------------------------------- */
+pvconv_status pvconv_conv3d_noalloc(const void* x, int B, int R, int Cin, int Cout,
+                                    const void* weight, const float* bias, const pvconv_bn* bn,
+                                    pvconv_act act, float slope, pvconv_dtype dt, void* y,
+                                    pvconv_dtype out_dt, void* stream);
 
 /* ------------------------------------------------------------------------- */
 /* Trilinear devoxelisation: Section 4.1 "Devoxelization".                   */

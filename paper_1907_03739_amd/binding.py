@@ -56,6 +56,8 @@ _SIGS = {
     "pvconv_conv3d_workspace_size": ([_I, _I, _I], _SZ),
     "pvconv_conv3d": ([_VP, _I, _I, _I, _I, _VP, _VP, _VP, _I, _F, _I, _VP, _I, _VP, _SZ, _VP],
                       _I),
+    "pvconv_conv3d_noalloc": ([_VP, _I, _I, _I, _I, _VP, _VP, _VP, _I, _F, _I, _VP, _I, _VP],
+                              _I),
     "pvconv_devoxelize": ([_VP, _I, _I, _I, _I, _VP, _I, _VP, _VP], _I),
     "pvconv_devoxelize_nearest": ([_VP, _I, _I, _I, _I, _VP, _I, _VP, _VP], _I),
     "pvconv_point_mlp": ([_VP, _I, _I, _I, _I, _I, _VP, _I, _VP, _VP, _I, _F, _VP, _I, _VP, _I,
@@ -219,6 +221,26 @@ def pvconv_conv3d(x: torch.Tensor, weight: torch.Tensor, R: int, bn=None,
         ctypes.byref(bns) if bn is not None else None, ACT[act], slope, _dt(x), _p(y), _dt(y),
         _p(workspace) if need else None, workspace.numel() if need else 0, _stream(x)))
     return y
+
+
+def pvconv_conv3d_noalloc(x: torch.Tensor, weight: torch.Tensor, R: int, out: torch.Tensor,
+                          bn=None, bias: Optional[torch.Tensor] = None, act="leaky", slope=0.1):
+    """pvconv_conv3d into the caller's `out` [B][R^3][Cout] (its dtype is the output
+    dtype), with the library's static workspace: the C call allocates nothing."""
+    B, V, Cin = x.shape
+    Cout = weight.shape[0]
+    if V != R ** 3 or tuple(weight.shape[1:]) != (3, 3, 3, Cin):
+        raise ValueError("shape mismatch")
+    if tuple(out.shape) != (B, V, Cout) or not out.is_contiguous():
+        raise ValueError("out must be a contiguous [B][R^3][Cout] tensor")
+    if not (x.is_contiguous() and weight.is_contiguous()):
+        raise ValueError("x and weight must be contiguous")
+    bns = _bn_struct(bn)
+    _check("pvconv_conv3d_noalloc", _lib.pvconv_conv3d_noalloc(
+        _p(x), B, R, Cin, Cout, _p(weight), _p(bias),
+        ctypes.byref(bns) if bn is not None else None, ACT[act], slope, _dt(x), _p(out),
+        _dt(out), _stream(x)))
+    return out
 
 
 def pvconv_devoxelize(grid: torch.Tensor, R: int, norm_coords: torch.Tensor, out=None):

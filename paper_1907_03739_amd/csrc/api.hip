@@ -1,6 +1,14 @@
 // C ABI of libpvconv: argument validation on the host, then launches on the
 // caller's stream. Nothing is enqueued when validation fails.
+#include <mutex>
+
 #include "pv_common.h"
+
+// The workspace of pvconv_conv3d_noalloc: one copy per GPU in the library's
+// device image, so that entry point allocates nothing. On the host this name
+// is only a stand-in: host code takes the device address of the current
+// GPU's copy from static_ws_on_device(), never from the name itself.
+static __device__ __align__(256) unsigned char scratch[PVCONV_CONV3D_NOALLOC_BYTES];
 
 namespace {
 
@@ -72,6 +80,55 @@ ForwardWs carve_forward(void* base, int B, int N, const pvconv_layer* L) {
     w.devox = (float*)take((size_t)B * N * L->cout * 4);
     w.total = off;
     return w;
+}
+
+// Device address of `scratch` on the GPU that runs work on stream s (which
+// must be the current device's), looked up with that device current on its
+// first use and kept per device.
+constexpr int kMaxDevices = 64;
+std::mutex g_static_ws_mu;
+void* g_static_ws[kMaxDevices];
+
+pvconv_status static_ws_on_device(hipStream_t s, void** out) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return PVCONV_EHIP;
+    if (dev < 0 || dev >= kMaxDevices) return PVCONV_ENOTSUP;
+    if (s) {
+        hipDevice_t sd = -1;
+        if (hipStreamGetDevice(s, &sd) != hipSuccess) return PVCONV_EHIP;
+        if (sd != dev) return PVCONV_EINVAL;
+    }
+    std::lock_guard<std::mutex> lock(g_static_ws_mu);
+    if (!g_static_ws[dev]) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) {
+            (void)hipGetLastError();  // leave no error for the next launch check
+            return PVCONV_EHIP;
+        }
+        g_static_ws[dev] = p;
+    }
+    *out = g_static_ws[dev];
+    return PVCONV_OK;
+}
+
+// Everything pvconv_conv3d checks except the workspace (B == 0 passes).
+pvconv_status check_conv3d(const void* x, int B, int R, int Cin, int Cout, const void* weight,
+                           const float* bias, const pvconv_bn* bn, pvconv_act act,
+                           pvconv_dtype dt, const void* y, pvconv_dtype out_dt) {
+    if (B < 0 || R < 1 || R > PVCONV_MAX_R || Cin < 1 || Cout < 1 ||
+        Cin > PVCONV_MAX_CONV_CHANNELS || Cout > PVCONV_MAX_CONV_CHANNELS)
+        return PVCONV_EINVAL;
+    if (!dtype_ok(dt) || !dtype_ok(out_dt) || !act_ok(act) || !bn_ok(bn)) return PVCONV_EINVAL;
+    if (B == 0) return PVCONV_OK;
+    if (!x || !weight || !y) return PVCONV_EINVAL;
+    if (((uintptr_t)x & (esize(dt) - 1)) || ((uintptr_t)weight & (esize(dt) - 1)) ||
+        ((uintptr_t)y & (esize(out_dt) - 1)) || ((uintptr_t)bias & 3))
+        return PVCONV_EINVAL;
+    if (dt == PVCONV_BF16 && Cout % 32 != 0) return PVCONV_ENOTSUP;
+    // every input voxel is read by up to 27 workgroups while others store
+    if (overlap(x, (long long)B * R * R * R, Cin, Cin, dt, y, Cout, Cout, out_dt))
+        return PVCONV_EINVAL;
+    return PVCONV_OK;
 }
 
 pvconv_status check_layer(const pvconv_layer* L) {
@@ -167,23 +224,32 @@ pvconv_status pvconv_conv3d(const void* x, int B, int R, int Cin, int Cout, cons
                             const float* bias, const pvconv_bn* bn, pvconv_act act, float slope,
                             pvconv_dtype dt, void* y, pvconv_dtype out_dt, void* workspace,
                             size_t workspace_bytes, void* stream) {
-    if (B < 0 || R < 1 || R > PVCONV_MAX_R || Cin < 1 || Cout < 1 ||
-        Cin > PVCONV_MAX_CONV_CHANNELS || Cout > PVCONV_MAX_CONV_CHANNELS)
-        return PVCONV_EINVAL;
-    if (!dtype_ok(dt) || !dtype_ok(out_dt) || !act_ok(act) || !bn_ok(bn)) return PVCONV_EINVAL;
-    if (B == 0) return PVCONV_OK;
-    if (!x || !weight || !y) return PVCONV_EINVAL;
-    if (((uintptr_t)x & (esize(dt) - 1)) || ((uintptr_t)weight & (esize(dt) - 1)) ||
-        ((uintptr_t)y & (esize(out_dt) - 1)) || ((uintptr_t)bias & 3))
-        return PVCONV_EINVAL;
-    if (dt == PVCONV_BF16 && Cout % 32 != 0) return PVCONV_ENOTSUP;
-    if (x == y) return PVCONV_EINVAL;
+    const pvconv_status st =
+        check_conv3d(x, B, R, Cin, Cout, weight, bias, bn, act, dt, y, out_dt);
+    if (st != PVCONV_OK || B == 0) return st;
     const size_t need = pv_conv3d_ws_bytes(Cin, Cout, dt == PVCONV_BF16);
     if (need && (!workspace || ((uintptr_t)workspace & 255) || workspace_bytes < need))
         return PVCONV_EWORKSPACE;
     return pv_launch_conv3d(x, B, R, Cin, Cout, weight, pv_make_fold(bn, bias), act, slope,
                             dt == PVCONV_BF16, y, out_dt == PVCONV_BF16, workspace,
                             as_stream(stream));
+}
+
+pvconv_status pvconv_conv3d_noalloc(const void* x, int B, int R, int Cin, int Cout,
+                                    const void* weight, const float* bias, const pvconv_bn* bn,
+                                    pvconv_act act, float slope, pvconv_dtype dt, void* y,
+                                    pvconv_dtype out_dt, void* stream) {
+    pvconv_status st = check_conv3d(x, B, R, Cin, Cout, weight, bias, bn, act, dt, y, out_dt);
+    if (st != PVCONV_OK || B == 0) return st;
+    const size_t need = pv_conv3d_ws_bytes(Cin, Cout, dt == PVCONV_BF16);
+    if (need > PVCONV_CONV3D_NOALLOC_BYTES) return PVCONV_EWORKSPACE;
+    hipStream_t s = as_stream(stream);
+    void* ws = nullptr;
+    if (need && (st = static_ws_on_device(s, &ws)) != PVCONV_OK) return st;
+    // the packing launch rewrites all `need` bytes of the array, so nothing
+    // from an earlier call is read
+    return pv_launch_conv3d(x, B, R, Cin, Cout, weight, pv_make_fold(bn, bias), act, slope,
+                            dt == PVCONV_BF16, y, out_dt == PVCONV_BF16, ws, s);
 }
 
 pvconv_status pvconv_devoxelize(const void* grid, int B, int R, int C, pvconv_dtype grid_dt,

@@ -30,7 +30,7 @@ def declared_functions():
 
 def test_library_exports_every_declared_symbol():
     names = declared_functions()
-    assert len(names) == 21
+    assert len(names) == 22
     out = subprocess.run(["nm", "-D", "--defined-only", b.LIB_PATH], capture_output=True,
                          text=True, check=True).stdout
     exported = set(re.findall(r"\bT (pvconv_\w+)", out))
@@ -107,6 +107,39 @@ def _conv(**kw):
 ])
 def test_conv3d_rejects(kw, status):
     assert _conv(**kw) == status
+
+
+def test_conv3d_rejects_overlapping_output():
+    # x [1][512][16] bf16 spans 16 KiB from FAKE; y starting inside it overlaps
+    assert _conv(y=ctypes.c_void_p(0x100000 + 4096)) == EINVAL
+    assert _conv(y=ctypes.c_void_p(0x100000 - 512), out_dt=1, Cout=64) == EINVAL
+
+
+def _conv_na(**kw):
+    a = dict(x=FAKE, B=1, R=8, Cin=16, Cout=64, w=FAKE, bias=None, bn=None, act=2, slope=0.1,
+             dt=1, y=ctypes.c_void_p(0x200000), out_dt=1, s=None)
+    a.update(kw)
+    return L.pvconv_conv3d_noalloc(a["x"], a["B"], a["R"], a["Cin"], a["Cout"], a["w"],
+                                   a["bias"], a["bn"], a["act"], a["slope"], a["dt"], a["y"],
+                                   a["out_dt"], a["s"])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(B=-1), EINVAL), (dict(R=0), EINVAL), (dict(Cin=0), EINVAL), (dict(Cout=2000), EINVAL),
+    (dict(act=5), EINVAL), (dict(x=None), EINVAL), (dict(w=None), EINVAL),
+    (dict(y=None), EINVAL), (dict(y=FAKE), EINVAL), (dict(Cout=48), ENOTSUP), (dict(B=0), OK),
+    # packed weights beyond the 4 MiB static array: 27 * 512 * 512 * 2 bytes
+    (dict(Cin=512, Cout=512), EWS), (dict(Cin=1024, Cout=128), EWS),
+])
+def test_conv3d_noalloc_rejects(kw, status):
+    assert _conv_na(**kw) == status
+
+
+def test_conv3d_noalloc_limit():
+    # the largest square convolution the static array takes is 256 -> 256
+    limit = 4 << 20
+    assert L.pvconv_conv3d_workspace_size(256, 256, 1) <= limit
+    assert L.pvconv_conv3d_workspace_size(512, 256, 1) > limit
 
 
 def test_conv3d_rejects_incomplete_batchnorm():
