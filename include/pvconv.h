@@ -156,6 +156,28 @@ pvconv_status pvconv_conv3d(const void* x, int B, int R, int Cin, int Cout, cons
                             size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------- */
+/* The same convolution in two parts, for weights used by many calls (a      */
+/* network's fixed weights): the bf16 weights repacked once into the MFMA    */
+/* fragment order, then any number of convolutions on the packed copy.       */
+/* pvconv_conv3d(...) equals pvconv_conv3d_pack_weights then                */
+/* pvconv_conv3d_packed on the same stream, bit for bit.                     */
+/*  weight  [Cout][3][3][3][Cin] bf16 (the MFMA path: Cout % 32 == 0, else   */
+/*          PVCONV_ENOTSUP)                                                  */
+/*  packed  out: >= pvconv_conv3d_workspace_size(Cin, Cout, PVCONV_BF16)     */
+/*          bytes, 256-byte aligned, owned by the caller; every byte of that */
+/*          size is written. Its layout is internal to the library.          */
+/* pvconv_conv3d_packed takes the arguments of pvconv_conv3d with dt = BF16, */
+/* and `packed` (as written by the pack call for the same Cin, Cout) in     */
+/* place of weight and workspace; errors as pvconv_conv3d.                   */
+/* ------------------------------------------------------------------------- */
+pvconv_status pvconv_conv3d_pack_weights(const void* weight, int Cin, int Cout, void* packed,
+                                         size_t packed_bytes, void* stream);
+pvconv_status pvconv_conv3d_packed(const void* x, int B, int R, int Cin, int Cout,
+                                   const void* packed, size_t packed_bytes, const float* bias,
+                                   const pvconv_bn* bn, pvconv_act act, float slope, void* y,
+                                   pvconv_dtype out_dt, void* stream);
+
+/* ------------------------------------------------------------------------- */
 /* pvconv_conv3d without a workspace argument, for callers that cannot       */
 /* allocate device memory (code under HIP graph capture, serving loops that  */
 /* must not call hipMalloc, harnesses that forbid it).                       */
@@ -234,6 +256,34 @@ pvconv_status pvconv_point_mlp(const void* x, pvconv_dtype x_dt, int x_ld, int M
                                float slope, const float* cloud_bias, int points_per_cloud,
                                const float* residual, int residual_ld, void* out,
                                pvconv_dtype out_dt, int out_ld, void* stream);
+
+/* ------------------------------------------------------------------------- */
+/* The end of a PVConv layer in one kernel: the point MLP of Section 4.2     */
+/* whose epilogue adds the trilinear devoxelisation of Section 4.1 (fusion   */
+/* by addition, Section 4.3), gathered from the grid inside the same kernel, */
+/* without an fp32 intermediate. The same result as pvconv_devoxelize into a */
+/* buffer r, then pvconv_point_mlp(..., residual = r, ...):                  */
+/*  out[b,k,o] = act( BN_o( sum_i W[o][i] x[b,k,i] + bias_o ) )              */
+/*               + trilinear(grid[b], norm_coords[b][k])[o]                  */
+/*  grid         [B][R^3][Cout] bf16 (a layer's last convolution output)     */
+/*  norm_coords  [B][N][3] fp32 (as written by pvconv_voxelize)              */
+/*  x            [B][N][Cin] (x_dt), row stride x_ld (0: Cin)                */
+/*  weight       [Cout][Cin] bf16 (MFMA, fp32 accumulation)                  */
+/*  bias, bn, act, slope as pvconv_point_mlp                                 */
+/*  out          out [B][N][Cout] (out_dt), row stride out_ld (0: Cout)      */
+/* Shapes the fused kernel takes: Cin % 8 == 0, Cout % 8 == 0, not both of   */
+/* Cin and Cout >= 128, B*N >= 128, 16-byte aligned x, weight and grid rows, */
+/* x rows a multiple of 16 bytes, out_ld % 4 == 0 and out aligned to 16     */
+/* bytes (8 for bf16). Others return PVCONV_ENOTSUP (pvconv_forward then     */
+/* runs the two steps separately). out must not overlap x, grid or          */
+/* norm_coords (PVCONV_EINVAL).                                              */
+/* ------------------------------------------------------------------------- */
+pvconv_status pvconv_devoxelize_point_mlp(const void* grid, int R, const float* norm_coords,
+                                          int B, int N, const void* x, pvconv_dtype x_dt,
+                                          int x_ld, int Cin, int Cout, const void* weight,
+                                          const float* bias, const pvconv_bn* bn,
+                                          pvconv_act act, float slope, void* out,
+                                          pvconv_dtype out_dt, int out_ld, void* stream);
 
 /* ------------------------------------------------------------------------- */
 /* Per-cloud max over the points (the PointNet global feature that PVCNN     */

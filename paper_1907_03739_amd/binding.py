@@ -56,6 +56,11 @@ _SIGS = {
     "pvconv_conv3d_workspace_size": ([_I, _I, _I], _SZ),
     "pvconv_conv3d": ([_VP, _I, _I, _I, _I, _VP, _VP, _VP, _I, _F, _I, _VP, _I, _VP, _SZ, _VP],
                       _I),
+    "pvconv_conv3d_pack_weights": ([_VP, _I, _I, _VP, _SZ, _VP], _I),
+    "pvconv_conv3d_packed": ([_VP, _I, _I, _I, _I, _VP, _SZ, _VP, _VP, _I, _F, _VP, _I, _VP],
+                             _I),
+    "pvconv_devoxelize_point_mlp": ([_VP, _I, _VP, _I, _I, _VP, _I, _I, _I, _I, _VP, _VP, _VP,
+                                     _I, _F, _VP, _I, _I, _VP], _I),
     "pvconv_conv3d_noalloc": ([_VP, _I, _I, _I, _I, _VP, _VP, _VP, _I, _F, _I, _VP, _I, _VP],
                               _I),
     "pvconv_devoxelize": ([_VP, _I, _I, _I, _I, _VP, _I, _VP, _VP], _I),
@@ -221,6 +226,60 @@ def pvconv_conv3d(x: torch.Tensor, weight: torch.Tensor, R: int, bn=None,
         ctypes.byref(bns) if bn is not None else None, ACT[act], slope, _dt(x), _p(y), _dt(y),
         _p(workspace) if need else None, workspace.numel() if need else 0, _stream(x)))
     return y
+
+
+def pvconv_conv3d_pack_weights(weight: torch.Tensor, out: Optional[torch.Tensor] = None):
+    """bf16 weight [Cout][3][3][3][Cin] -> its MFMA-order copy (uint8 bytes) for
+    pvconv_conv3d_packed."""
+    Cout, Cin = weight.shape[0], weight.shape[-1]
+    if tuple(weight.shape[1:]) != (3, 3, 3, Cin) or weight.dtype != torch.bfloat16:
+        raise ValueError("weight must be [Cout][3][3][3][Cin] bf16")
+    need = _lib.pvconv_conv3d_workspace_size(Cin, Cout, BF16)
+    if out is None:
+        out = torch.empty(max(need, 256), dtype=torch.uint8, device=weight.device)
+    _check("pvconv_conv3d_pack_weights", _lib.pvconv_conv3d_pack_weights(
+        _p(weight.contiguous()), Cin, Cout, _p(out), out.numel(), _stream(weight)))
+    return out
+
+
+def pvconv_conv3d_packed(x: torch.Tensor, packed: torch.Tensor, Cout: int, R: int, bn=None,
+                         bias: Optional[torch.Tensor] = None, act="leaky", slope=0.1,
+                         out_dtype=None, out: Optional[torch.Tensor] = None):
+    """x [B][R^3][Cin] bf16 with pre-packed weights -> y [B][R^3][Cout]."""
+    B, V, Cin = x.shape
+    if V != R ** 3:
+        raise ValueError("shape mismatch")
+    y = out if out is not None else torch.empty(
+        (B, V, Cout), dtype=_torch_dt(out_dtype or x.dtype), device=x.device)
+    bns = _bn_struct(bn)
+    _check("pvconv_conv3d_packed", _lib.pvconv_conv3d_packed(
+        _p(x.contiguous()), B, R, Cin, Cout, _p(packed), packed.numel(), _p(bias),
+        ctypes.byref(bns) if bn is not None else None, ACT[act], slope, _p(y), _dt(y),
+        _stream(x)))
+    return y
+
+
+def pvconv_devoxelize_point_mlp(grid: torch.Tensor, R: int, norm_coords: torch.Tensor,
+                                x: torch.Tensor, weight: torch.Tensor, bias=None, bn=None,
+                                act="relu", slope=0.0, out: Optional[torch.Tensor] = None,
+                                out_dtype=torch.float32):
+    """grid [B][R^3][Cout] bf16, norm_coords [B][N][3], x [B][N][Cin] (rows evenly
+    strided), weight [Cout][Cin] bf16 -> act(BN(W x + b)) + devoxelised grid."""
+    B, N, Cin = x.shape
+    Cout = weight.shape[0]
+    if tuple(grid.shape) != (B, R ** 3, Cout) or tuple(norm_coords.shape) != (B, N, 3):
+        raise ValueError("shape mismatch")
+    x_ld = _rows(x, N, Cin)
+    if out is None:
+        out = torch.empty((B, N, Cout), dtype=_torch_dt(out_dtype), device=x.device)
+    out_ld = _rows(out, N, Cout)
+    bns = _bn_struct(bn)
+    _check("pvconv_devoxelize_point_mlp", _lib.pvconv_devoxelize_point_mlp(
+        _p(grid.contiguous()), R, _p(norm_coords.contiguous()), B, N, _p(x), _dt(x), x_ld,
+        Cin, Cout, _p(weight.contiguous()), _p(bias),
+        ctypes.byref(bns) if bn is not None else None, ACT[act], slope, _p(out), _dt(out),
+        out_ld, _stream(x)))
+    return out
 
 
 def pvconv_conv3d_noalloc(x: torch.Tensor, weight: torch.Tensor, R: int, out: torch.Tensor,

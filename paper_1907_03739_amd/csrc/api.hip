@@ -43,6 +43,12 @@ inline bool overlap(const void* a, long long rows, int ca, int lda, pvconv_dtype
     return !(e >= wa && e + wb <= pa);
 }
 
+// Two byte ranges [a, a + na) and [b, b + nb) intersect.
+inline bool bytes_overlap(const void* a, size_t na, const void* b, size_t nb) {
+    const uintptr_t a0 = (uintptr_t)a, b0 = (uintptr_t)b;
+    return na && nb && a0 < b0 + nb && b0 < a0 + na;
+}
+
 struct ForwardWs {
     void* conv_ws[PVCONV_MAX_CONVS];
     void* vox_ws;
@@ -235,6 +241,38 @@ pvconv_status pvconv_conv3d(const void* x, int B, int R, int Cin, int Cout, cons
                             as_stream(stream));
 }
 
+pvconv_status pvconv_conv3d_pack_weights(const void* weight, int Cin, int Cout, void* packed,
+                                         size_t packed_bytes, void* stream) {
+    if (Cin < 1 || Cout < 1 || Cin > PVCONV_MAX_CONV_CHANNELS || Cout > PVCONV_MAX_CONV_CHANNELS)
+        return PVCONV_EINVAL;
+    if (Cout % 32 != 0) return PVCONV_ENOTSUP;
+    if (!weight || ((uintptr_t)weight & 1)) return PVCONV_EINVAL;
+    const size_t need = pv_conv3d_ws_bytes(Cin, Cout, true);
+    if (!packed || ((uintptr_t)packed & 255) || packed_bytes < need) return PVCONV_EWORKSPACE;
+    if (bytes_overlap(weight, (size_t)Cout * 27 * Cin * 2, packed, need)) return PVCONV_EINVAL;
+    PvPackJobs jobs{};
+    pv_pack_job(jobs, weight, Cin, Cout, packed);
+    pv_launch_pack_conv_weights(jobs, as_stream(stream));
+    return pv_launch_status();
+}
+
+pvconv_status pvconv_conv3d_packed(const void* x, int B, int R, int Cin, int Cout,
+                                   const void* packed, size_t packed_bytes, const float* bias,
+                                   const pvconv_bn* bn, pvconv_act act, float slope, void* y,
+                                   pvconv_dtype out_dt, void* stream) {
+    // the packed copy stands in for the weights in the common checks
+    const pvconv_status st = check_conv3d(x, B, R, Cin, Cout, packed, bias, bn, act,
+                                          PVCONV_BF16, y, out_dt);
+    if (st != PVCONV_OK || B == 0) return st;
+    const size_t need = pv_conv3d_ws_bytes(Cin, Cout, true);
+    if (((uintptr_t)packed & 255) || packed_bytes < need) return PVCONV_EWORKSPACE;
+    if (bytes_overlap(y, (size_t)B * R * R * R * Cout * esize(out_dt), packed, need))
+        return PVCONV_EINVAL;
+    return pv_launch_conv3d(x, B, R, Cin, Cout, nullptr, pv_make_fold(bn, bias), act, slope,
+                            true, y, out_dt == PVCONV_BF16, const_cast<void*>(packed),
+                            as_stream(stream), /*packed=*/true);
+}
+
 pvconv_status pvconv_conv3d_noalloc(const void* x, int B, int R, int Cin, int Cout,
                                     const void* weight, const float* bias, const pvconv_bn* bn,
                                     pvconv_act act, float slope, pvconv_dtype dt, void* y,
@@ -312,6 +350,37 @@ pvconv_status pvconv_point_mlp(const void* x, pvconv_dtype x_dt, int x_ld, int M
                                cloud_bias, cloud_bias ? points_per_cloud : 1, residual,
                                residual_ld, out, out_dt == PVCONV_BF16, out_ld,
                                as_stream(stream));
+}
+
+pvconv_status pvconv_devoxelize_point_mlp(const void* grid, int R, const float* norm_coords,
+                                          int B, int N, const void* x, pvconv_dtype x_dt,
+                                          int x_ld, int Cin, int Cout, const void* weight,
+                                          const float* bias, const pvconv_bn* bn,
+                                          pvconv_act act, float slope, void* out,
+                                          pvconv_dtype out_dt, int out_ld, void* stream) {
+    if (B < 0 || N < 0 || !sizes_fit(B, N) || R < 1 || R > PVCONV_MAX_R || Cin < 1 ||
+        Cout < 1 || Cin > PVCONV_MAX_MLP_CHANNELS || Cout > PVCONV_MAX_MLP_CHANNELS)
+        return PVCONV_EINVAL;
+    if (!dtype_ok(x_dt) || !dtype_ok(out_dt) || !act_ok(act) || !bn_ok(bn)) return PVCONV_EINVAL;
+    if (x_ld == 0) x_ld = Cin;
+    if (out_ld == 0) out_ld = Cout;
+    if (x_ld < Cin || out_ld < Cout) return PVCONV_EINVAL;
+    if (B == 0 || N == 0) return PVCONV_OK;
+    if (!grid || !norm_coords || !x || !weight || !out) return PVCONV_EINVAL;
+    if (((uintptr_t)grid & 1) || ((uintptr_t)norm_coords & 3) ||
+        ((uintptr_t)x & (esize(x_dt) - 1)) || ((uintptr_t)weight & 1) ||
+        ((uintptr_t)out & (esize(out_dt) - 1)) || ((uintptr_t)bias & 3))
+        return PVCONV_EINVAL;
+    const long long M = (long long)B * N;
+    const size_t out_bytes = (size_t)((M - 1) * out_ld + Cout) * esize(out_dt);
+    if (overlap(x, M, Cin, x_ld, x_dt, out, Cout, out_ld, out_dt) ||
+        bytes_overlap(out, out_bytes, grid, (size_t)B * R * R * R * Cout * 2) ||
+        bytes_overlap(out, out_bytes, norm_coords, (size_t)M * 12))
+        return PVCONV_EINVAL;
+    return pv_launch_devox_point_mlp(PvDevoxIn{(const uint16_t*)grid, norm_coords, N, R}, x,
+                                     x_dt == PVCONV_BF16, x_ld, (int)M, Cin, Cout, weight,
+                                     pv_make_fold(bn, bias), act, slope, out,
+                                     out_dt == PVCONV_BF16, out_ld, as_stream(stream));
 }
 
 pvconv_status pvconv_maxpool(const void* x, pvconv_dtype dt, int x_ld, int B, int N, int C,

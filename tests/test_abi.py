@@ -30,7 +30,7 @@ def declared_functions():
 
 def test_library_exports_every_declared_symbol():
     names = declared_functions()
-    assert len(names) == 22
+    assert len(names) == 25
     out = subprocess.run(["nm", "-D", "--defined-only", b.LIB_PATH], capture_output=True,
                          text=True, check=True).stdout
     exported = set(re.findall(r"\bT (pvconv_\w+)", out))
@@ -140,6 +140,64 @@ def test_conv3d_noalloc_limit():
     limit = 4 << 20
     assert L.pvconv_conv3d_workspace_size(256, 256, 1) <= limit
     assert L.pvconv_conv3d_workspace_size(512, 256, 1) > limit
+
+
+@pytest.mark.parametrize("args,status", [
+    (dict(Cin=0), EINVAL), (dict(Cout=2048), EINVAL), (dict(Cout=48), ENOTSUP),
+    (dict(w=None), EINVAL), (dict(w=FAKE_ODD), EINVAL), (dict(packed=None), EWS),
+    (dict(packed=ctypes.c_void_p(0x400010)), EWS), (dict(nbytes=100), EWS),
+    # the packed copy written over the weights themselves
+    (dict(packed=FAKE), EINVAL),
+])
+def test_conv3d_pack_weights_rejects(args, status):
+    a = dict(w=FAKE, Cin=16, Cout=64, packed=ctypes.c_void_p(0x400000), nbytes=1 << 30)
+    a.update(args)
+    assert L.pvconv_conv3d_pack_weights(a["w"], a["Cin"], a["Cout"], a["packed"], a["nbytes"],
+                                        None) == status
+
+
+@pytest.mark.parametrize("args,status", [
+    (dict(B=-1), EINVAL), (dict(R=0), EINVAL), (dict(Cout=48), ENOTSUP), (dict(B=0), OK),
+    (dict(x=None), EINVAL), (dict(packed=None), EINVAL), (dict(y=FAKE), EINVAL),
+    (dict(packed=ctypes.c_void_p(0x400010)), EWS), (dict(nbytes=100), EWS),
+    # the output written over the packed weights
+    (dict(packed=ctypes.c_void_p(0x200000)), EINVAL),
+])
+def test_conv3d_packed_rejects(args, status):
+    a = dict(x=FAKE, B=1, R=8, Cin=16, Cout=64, packed=ctypes.c_void_p(0x800000),
+             nbytes=1 << 30, y=ctypes.c_void_p(0x200000), out_dt=1)
+    a.update(args)
+    assert L.pvconv_conv3d_packed(a["x"], a["B"], a["R"], a["Cin"], a["Cout"], a["packed"],
+                                  a["nbytes"], None, None, 2, 0.1, a["y"], a["out_dt"],
+                                  None) == status
+
+
+def _dvmlp(**kw):
+    a = dict(grid=ctypes.c_void_p(0x1000000), R=8, pn=ctypes.c_void_p(0x2000000), B=2, N=100,
+             x=FAKE, x_dt=0, x_ld=0, Cin=16, Cout=64, w=ctypes.c_void_p(0x3000000), bias=None,
+             bn=None, act=1, slope=0.0, out=ctypes.c_void_p(0x4000000), out_dt=0, out_ld=0)
+    a.update(kw)
+    return L.pvconv_devoxelize_point_mlp(a["grid"], a["R"], a["pn"], a["B"], a["N"], a["x"],
+                                         a["x_dt"], a["x_ld"], a["Cin"], a["Cout"], a["w"],
+                                         a["bias"], a["bn"], a["act"], a["slope"], a["out"],
+                                         a["out_dt"], a["out_ld"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(B=-1), EINVAL), (dict(R=0), EINVAL), (dict(Cin=0), EINVAL), (dict(x_ld=8), EINVAL),
+    (dict(out_ld=32), EINVAL), (dict(act=7), EINVAL), (dict(B=0), OK), (dict(N=0), OK),
+    (dict(grid=None), EINVAL), (dict(pn=None), EINVAL), (dict(w=None), EINVAL),
+    (dict(grid=ctypes.c_void_p(0x1000001)), EINVAL), (dict(x=FAKE_ODD), EINVAL),
+    # out over x, over the grid, over the coordinates
+    (dict(out=ctypes.c_void_p(0x100000 + 64)), EINVAL),
+    (dict(out=ctypes.c_void_p(0x1000000 + 4096)), EINVAL),
+    (dict(out=ctypes.c_void_p(0x2000000 - 1024)), EINVAL),
+    # shapes the fused kernel does not take: checked after validation, before
+    # anything is enqueued
+    (dict(Cin=12), ENOTSUP), (dict(Cin=128, Cout=128), ENOTSUP), (dict(B=1, N=100), ENOTSUP),
+])
+def test_devoxelize_point_mlp_rejects(kw, status):
+    assert _dvmlp(**kw) == status
 
 
 def test_conv3d_rejects_incomplete_batchnorm():
