@@ -74,8 +74,23 @@ def _load():
     lib.ref_leaky_relu.restype = None
     lib.ref_relu.argtypes = [_P, _I64]
     lib.ref_relu.restype = None
+    # the OpenMP runtime the library links (thread count of its loops)
+    lib.omp_set_num_threads.argtypes = [ctypes.c_int]
+    lib.omp_set_num_threads.restype = None
+    lib.omp_get_max_threads.argtypes = []
+    lib.omp_get_max_threads.restype = ctypes.c_int
     _lib = lib
     return lib
+
+
+def set_threads(n: int) -> None:
+    """Number of threads the oracle's parallel loops use from now on."""
+    _load().omp_set_num_threads(int(n))
+
+
+def threads() -> int:
+    """Number of threads the oracle's parallel loops use."""
+    return int(_load().omp_get_max_threads())
 
 
 def _f64(a) -> np.ndarray:
@@ -335,19 +350,31 @@ def maxpool(x: np.ndarray) -> np.ndarray:
 # ----------------------------------------------------------------------------
 # composition: one PVConv layer (Figure "overview", Sections 4.1-4.3)
 # ----------------------------------------------------------------------------
-def voxel_branch(coords, feats, layer):
+def _storage(stage_dtype):
+    if stage_dtype not in ("f64", "bf16"):
+        raise ValueError("stage_dtype must be 'f64' or 'bf16'")
+    return round_bf16 if stage_dtype == "bf16" else (lambda v: v)
+
+
+def voxel_branch(coords, feats, layer, stage_dtype="f64"):
     """Normalise, voxelise, n_convs x (conv + BN + leaky ReLU), devoxelise
     (trilinear, or nearest neighbour when layer.devox == "nearest").
 
+    stage_dtype "bf16" stores the voxel grid and each convolution's output in
+    bf16 (round_bf16) before the next step reads it, as a layer with bf16
+    grids does; "f64" keeps every value in fp64.
+
     Returns a dict with every intermediate: centroid, radius, pnorm, ids, grid,
     counts, conv outputs (list, post-activation) and devox [B][N][Cout]."""
+    store = _storage(stage_dtype)
     c, m, pn = normalize(coords)
     ids = voxel_ids(pn, layer.R)
     grid, counts = voxelize(ids, feats, layer.R)
+    grid = store(grid)
     h = grid
     convs = []
     for w, bn in zip(layer.conv_w, layer.conv_bn):
-        h = leaky_relu(batchnorm(conv3d(h, w, layer.R), bn), layer.slope)
+        h = store(leaky_relu(batchnorm(conv3d(h, w, layer.R), bn), layer.slope))
         convs.append(h)
     if getattr(layer, "devox", "trilinear") == "nearest":
         dv = devoxelize_nearest(h, layer.R, ids)
@@ -357,15 +384,20 @@ def voxel_branch(coords, feats, layer):
                 convs=convs, devox=dv)
 
 
-def point_branch(feats, layer):
-    """Section 4.2: h = ReLU(BN(W f (+ b)))."""
-    return relu(batchnorm(linear(feats, layer.mlp_w, layer.mlp_b), layer.mlp_bn))
+def point_branch(feats, layer, stage_dtype="f64"):
+    """Section 4.2: h = ReLU(BN(W f (+ b))). stage_dtype "bf16" rounds the
+    features to bf16 before the product (the operand precision of a bf16
+    layer)."""
+    f = _storage(stage_dtype)(feats)
+    return relu(batchnorm(linear(f, layer.mlp_w, layer.mlp_b), layer.mlp_bn))
 
 
-def pvconv_forward(coords, feats, layer, return_parts=False):
-    """Section 4.3: the two branches fused by addition (no activation after it)."""
-    vb = voxel_branch(coords, feats, layer)
-    pb = point_branch(feats, layer)
+def pvconv_forward(coords, feats, layer, return_parts=False, stage_dtype="f64"):
+    """Section 4.3: the two branches fused by addition (no activation after
+    it). stage_dtype as in voxel_branch and point_branch; the output itself
+    is never rounded."""
+    vb = voxel_branch(coords, feats, layer, stage_dtype)
+    pb = point_branch(feats, layer, stage_dtype)
     out = vb["devox"] + pb
     if return_parts:
         vb["point"] = pb

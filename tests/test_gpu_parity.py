@@ -17,7 +17,7 @@ import oracle
 import synth
 from paper_1907_03739_amd import binding as pv
 from _helpers import (assert_bf16_chain, assert_bf16_step, assert_dot_f32, assert_rel,
-                            bf16_round, bn_scale, dev, dev_bn, host)
+                      bf16_round, bn_scale, dev, dev_bn, host)
 
 pytestmark = pytest.mark.gpu
 
@@ -335,6 +335,24 @@ def test_conv3d_bf16_matches_oracle(case):
     assert_bf16_step(host(y), ref, f"conv {case}")
 
 
+@pytest.mark.parametrize("case", CONV_CASES[:5], ids=lambda c: "B{}_R{}_{}to{}_{}".format(*c))
+def test_conv3d_packed_weights_give_the_same_bits(case):
+    # packing once and convolving on the packed copy is the same computation
+    # as the one-call convolution, which packs internally
+    B, R, Cin, Cout, odt = case
+    rng = np.random.default_rng(R * 1000 + Cin + 1)
+    x = dev(_sparse_grid(rng, B, R, Cin), torch.bfloat16)
+    w = dev(synth.kaiming_normal(rng, (Cout, 3, 3, 3, Cin), 27 * Cin, bf16=True), torch.bfloat16)
+    bn = dev_bn(synth.draw_bn(rng, Cout))
+    odt = torch.bfloat16 if odt == "bf16" else torch.float32
+    ref = pv.pvconv_conv3d(x, w, R, bn=bn, out_dtype=odt)
+    packed = pv.pvconv_conv3d_pack_weights(w)
+    got = pv.pvconv_conv3d_packed(x, packed, Cout, R, bn=bn, out_dtype=odt)
+    assert torch.equal(ref, got)
+    # a second convolution on the same packed copy
+    assert torch.equal(ref, pv.pvconv_conv3d_packed(x, packed, Cout, R, bn=bn, out_dtype=odt))
+
+
 def test_conv3d_bias_and_activations():
     rng = np.random.default_rng(7)
     B, R, Cin, Cout = 1, 16, 32, 64
@@ -522,6 +540,46 @@ def test_point_mlp_f32_matches_oracle(M, Cin, Cout):
     assert_dot_f32(host(out), ref, mag, "mlp fp32")
 
 
+@pytest.mark.parametrize("B,N,R,cin,cout,xdt,odt", [
+    (2, 2048, 32, 64, 128, "f32", "f32"),    # part-seg layer's end, two clouds
+    (3, 777, 16, 64, 96, "bf16", "f32"),     # ragged last tile, 96 = 1.5 channel blocks
+    (2, 1000, 24, 16, 32, "f32", "bf16"),    # narrow layer, bf16 output
+])
+def test_devoxelize_point_mlp_matches_oracle_and_the_two_steps(B, N, R, cin, cout, xdt, odt):
+    rng = np.random.default_rng(N + cout)
+    wl = synth.make_workload(2, B=B, N=N)
+    pn = oracle.normalize(wl.coords)[2]
+    grid = bf16_round(rng.normal(size=(B, R ** 3, cout)))
+    x = wl.feats[..., :cin]
+    if xdt == "bf16":
+        x = bf16_round(x)
+    w = synth.kaiming_normal(rng, (cout, cin), cin, bf16=True)
+    bias = rng.uniform(-0.1, 0.1, size=cout).astype(np.float32)
+    bn = synth.draw_bn(rng, cout)
+    ref = oracle.devoxelize(grid, R, pn) + oracle.relu(
+        oracle.batchnorm(oracle.linear(bf16_round(x), w, bias), bn))
+    tdt = torch.bfloat16 if odt == "bf16" else torch.float32
+    g_grid, g_pn = dev(grid, torch.bfloat16), dev(pn)
+    g_x = dev(x, torch.bfloat16 if xdt == "bf16" else torch.float32)
+    g_w, g_b, g_bn = dev(w, torch.bfloat16), dev(bias), dev_bn(bn)
+    got = pv.pvconv_devoxelize_point_mlp(g_grid, R, g_pn, g_x, g_w, bias=g_b, bn=g_bn,
+                                         out_dtype=tdt)
+    what = f"fused devox + MLP B{B} N{N} R{R} {cin}->{cout}"
+    if odt == "bf16":
+        assert_bf16_step(host(got), ref, what)
+    else:
+        # fp32 sums of bf16 products and of eight weighted corners
+        mag = oracle.devoxelize(np.abs(grid), R, pn) + oracle.linear(
+            np.abs(bf16_round(x)), np.abs(w), np.abs(bias)) * bn_scale(bn)
+        assert_dot_f32(host(got), ref, mag, what)
+    # the same arithmetic as the devoxelisation into a buffer followed by the
+    # point MLP with that buffer as its residual
+    dv = pv.pvconv_devoxelize(g_grid, R, g_pn)
+    two = pv.pvconv_point_mlp(g_x, g_w, bias=g_b, bn=g_bn, act="relu", residual=dv,
+                              out_dtype=tdt)
+    assert torch.equal(got, two), what
+
+
 @pytest.mark.parametrize("dt,off,C,N,shift", [
     ("f32", 300, 2048, 2048, 0.0),    # 16-byte rows: vector path
     ("bf16", 304, 2048, 2048, 0.0),
@@ -672,6 +730,57 @@ def test_forward_part_seg_full_size_sampled():
     sub = np.stack([got[b, k] for b, k in pts])
     # the chain tolerance's RMS floor uses the whole sampled block
     assert_bf16_chain(sub, ref, "part-seg layer, sampled points")
+
+
+def test_forward_part_seg_full_size_every_element():
+    # all 16 clouds x 2048 points x 128 channels of the part-segmentation
+    # layer, in the launch configuration the benchmark times
+    wl = synth.make_workload(2)
+    L = wl.layers[0]
+    got = _run_layer(wl, L, torch.bfloat16)
+    # against the fp64 layer: the chain bound
+    assert_bf16_chain(got, oracle.pvconv_forward(wl.coords, wl.feats, L),
+                      "part-seg layer, every element")
+    # against the layer that stores its grid and convolution outputs in bf16
+    # as the GPU does: the single-step bound. What is left is the fp32
+    # accumulation and the values whose fp32 and fp64 sums round to
+    # neighbouring bf16 numbers (each at most 2^-7 |h|, few, and spread over
+    # the trilinear weights)
+    ref16 = oracle.pvconv_forward(wl.coords, wl.feats, L, stage_dtype="bf16")
+    d = np.abs(got - ref16)
+    print(f"[bf16-stage layer] max |d| = {d.max():.3g}, "
+          f"max |d| / (1e-3 + 2e-2 |ref|) = {np.max(d / (1e-3 + 2e-2 * np.abs(ref16))):.3g}",
+          flush=True)
+    assert_bf16_step(got, ref16, "part-seg layer vs bf16-stage oracle")
+
+
+def test_composed_entry_points_give_the_forward_bits():
+    # the layer as separate C-ABI calls (voxelise, two convolutions on packed
+    # weights, the fused devoxelisation + point MLP) is the forward's own
+    # sequence of kernels: the same bits at full size
+    wl = synth.make_workload(2)
+    L = wl.layers[0]
+    layer = pv.DeviceLayer(L, "cuda", torch.bfloat16)
+    coords, feats = dev(wl.coords), dev(wl.feats)
+    want = pv.pvconv_forward(coords, feats, layer)
+    grid, _, _, pn = pv.pvconv_voxelize(coords, feats, L.R, grid_dtype=torch.bfloat16)
+    h = grid
+    for i in range(L.n_convs):
+        packed = pv.pvconv_conv3d_pack_weights(layer.conv_w[i])
+        h = pv.pvconv_conv3d_packed(h, packed, L.cout, L.R, bn=layer.conv_bn[i], act="leaky",
+                                    slope=L.slope, out_dtype=torch.bfloat16)
+    got = pv.pvconv_devoxelize_point_mlp(h, L.R, pn, feats, layer.mlp_w, bias=layer.mlp_b,
+                                         bn=layer.mlp_bn, act="relu")
+    assert torch.equal(got, want)
+    # and with the one-call convolutions, which pack internally
+    h = grid
+    for i in range(L.n_convs):
+        h = pv.pvconv_conv3d(h, layer.conv_w[i], L.R, bn=layer.conv_bn[i], act="leaky",
+                             slope=L.slope, out_dtype=torch.bfloat16)
+    dv = pv.pvconv_devoxelize(h, L.R, pn)
+    got2 = pv.pvconv_point_mlp(feats, layer.mlp_w, bias=layer.mlp_b, bn=layer.mlp_bn,
+                               act="relu", residual=dv)
+    assert torch.equal(got2, want)
 
 
 def test_forward_on_a_side_stream_and_repeatable():

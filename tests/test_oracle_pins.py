@@ -661,3 +661,57 @@ def test_network_bf16_storage_rounds_every_stage():
     assert np.max(np.abs(out16 - out64)) > 0.0
     with pytest.raises(ValueError):
         oracle.network_forward(wl, stage_dtype="f16")
+
+
+def _identity_layer(C, R):
+    """A layer whose convolutions copy the grid (centre tap = identity, all
+    other taps zero), with identity batch norms and no point branch weight."""
+    one = synth.BNParams(gamma=np.ones(C, np.float32), beta=np.zeros(C, np.float32),
+                         mean=np.zeros(C, np.float32), var=np.ones(C, np.float32), eps=0.0)
+    w = np.zeros((C, 3, 3, 3, C), np.float32)
+    w[:, 1, 1, 1, :] = np.eye(C, dtype=np.float32)
+    return synth.PVConvParams(cin=C, cout=C, R=R, conv_w=[w, w.copy()], conv_bn=[one, one],
+                              mlp_w=np.zeros((C, C), np.float32), mlp_bn=one)
+
+
+def test_layer_bf16_storage_is_lossless_on_bf16_values_and_rounds_others():
+    # a 4 x 4 x 4 lattice, one point per voxel of an R = 16 grid: the grid is
+    # the features themselves and the identity convolutions copy it exactly
+    R, C = 16, 8
+    cells = np.array([(u, v, w) for u in range(4) for v in range(4) for w in range(4)])
+    coords = ((cells + 0.5) / 4.0)[None] * 2.0 - 1.0
+    rng = np.random.default_rng(3)
+    feats = rng.integers(1, 200, size=(1, len(cells), C)).astype(np.float64)
+    L = _identity_layer(C, R)
+    parts = oracle.pvconv_forward(coords, feats, L, return_parts=True)
+    assert parts["counts"].max() == 1
+    # small positive integers are bf16 values: storage changes nothing
+    np.testing.assert_array_equal(
+        oracle.pvconv_forward(coords, feats, L, stage_dtype="bf16"), parts["out"])
+    # features of thirds are not: every stored stage is rounded, and as every
+    # step before the devoxelisation is exact, storing in bf16 is the same as
+    # rounding the features once and computing in fp64
+    thirds = feats / 3.0
+    p16 = oracle.pvconv_forward(coords, thirds, L, return_parts=True, stage_dtype="bf16")
+    for stage in [p16["grid"]] + p16["convs"]:
+        np.testing.assert_array_equal(oracle.round_bf16(stage), stage)
+    np.testing.assert_array_equal(
+        p16["out"], oracle.pvconv_forward(coords, oracle.round_bf16(thirds), L))
+    assert np.max(np.abs(p16["out"] - oracle.pvconv_forward(coords, thirds, L))) > 0.0
+
+
+def test_layer_bf16_storage_stays_within_a_bf16_ulp_chain():
+    wl = synth.make_workload(2, B=1, N=256)
+    L = wl.layers[0]
+    p16 = oracle.pvconv_forward(wl.coords, wl.feats, L, return_parts=True, stage_dtype="bf16")
+    p64 = oracle.pvconv_forward(wl.coords, wl.feats, L, return_parts=True)
+    for stage in [p16["grid"]] + p16["convs"]:
+        np.testing.assert_array_equal(oracle.round_bf16(stage), stage)
+    # the grid is rounded once: within half a bf16 spacing, at most 2^-8 |x|
+    g64 = p64["grid"]
+    assert np.all(np.abs(p16["grid"] - g64) <= np.abs(g64) * 2.0 ** -8)
+    rms = np.sqrt(np.mean(p64["out"] ** 2))
+    d = np.abs(p16["out"] - p64["out"])
+    assert 0.0 < np.max(d) < 0.05 * rms
+    with pytest.raises(ValueError):
+        oracle.pvconv_forward(wl.coords, wl.feats, L, stage_dtype="f16")
