@@ -14,16 +14,23 @@ Default workload: the part-segmentation-scale layer, 16 clouds x 2048 points,
 64 -> 128 channels, R = 32, bf16 operands with fp32 accumulation.
 
 Printed: ONE JSON line with the headline throughput (points/s), ms per layer,
-the roofline of the dominant kernel (the convolution, MFMA-bound), per-step
-timings of the same chain (back to back, and cold: after a 512 MiB write that
-evicts the caches), the device's measured peaks (a dense bf16 MFMA loop and a
-16-byte copy) as a second denominator next to the published ones, and the CPU
-oracle timed on a bounded sample of the same workload (which also checks the
-GPU output on that sample).
+the roofline of the dominant kernel (the convolution, MFMA-bound, timed on
+weights packed beforehand as the forward runs it), per-step timings of the
+same chain (back to back, and cold: after a 512 MiB write that evicts the
+caches), including the fused devoxelisation + point MLP kernel the forward
+runs, the peak device memory of one forward, the device's measured peaks (a
+dense bf16 MFMA loop and a 16-byte copy) as a second denominator next to the
+published ones, the CPU oracle timed on a bounded sample of the same workload
+(which also checks the GPU output on that sample), and for the default
+workload a compact `workloads` summary of the four others.
+
+The per-step breakdown runs before the headline's warmup and timed steps, so
+that those run at the clock the GPU settles to under load.
 """
 from __future__ import annotations
 
 import argparse
+import gc
 import json
 import os
 import statistics
@@ -52,6 +59,10 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="lower bound of CPU work for the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-workloads", action="store_true",
+                    help="headline workload only (no `workloads` summary of the others)")
+    ap.add_argument("--workload-cpu-seconds", type=float, default=2.0,
+                    help="lower bound of CPU work for each other workload's oracle sample")
     ap.add_argument("--no-peaks", action="store_true",
                     help="skip the measured-peak probes (MFMA loop, copy)")
     ap.add_argument("--variants", action="store_true",
@@ -184,30 +195,31 @@ def distinct_corners(pn, R):
 
 
 def cpu_baseline(wl, gpu_out, seconds):
-    """The oracle on the first clouds of the same workload, one at a time,
-    until at least `seconds` of CPU work; also compares the GPU output on
-    those clouds against it (the bf16 chain bound of the parity tests)."""
+    """The oracle on the workload's clouds, one per call, in order (again from
+    the first once all are done) until at least `seconds` of CPU work; also
+    compares the GPU output on those clouds against it (the bf16 chain bound
+    of the parity tests)."""
     import numpy as np
     import oracle
     L = wl.layers[0]
     oracle.pvconv_forward(wl.coords[:1, :8], wl.feats[:1, :8], L)  # load the library
-    cores = int(os.environ.get("OMP_NUM_THREADS") or len(os.sched_getaffinity(0)))
     done, worst, t_total = 0, 0.0, 0.0
-    for b in range(wl.B):
+    while t_total < seconds:
+        b = done % wl.B
         t0 = time.perf_counter()
         ref = oracle.pvconv_forward(wl.coords[b:b + 1], wl.feats[b:b + 1], L)[0]
         t_total += time.perf_counter() - t0
-        rms = float(np.sqrt(np.mean(ref ** 2)))
-        worst = max(worst, float(np.max(np.abs(gpu_out[b] - ref) / (np.abs(ref) + rms))))
+        if done < wl.B:
+            rms = float(np.sqrt(np.mean(ref ** 2)))
+            worst = max(worst, float(np.max(np.abs(gpu_out[b] - ref) / (np.abs(ref) + rms))))
         done += 1
-        if t_total >= seconds:
-            break
+    checked = min(done, wl.B)
     tol = 2e-2 if wl.dtype == "bf16" else 1e-5
-    return ({"value": done * wl.N / t_total, "unit": "points/s", "cores": cores,
+    return ({"value": done * wl.N / t_total, "unit": "points/s", "cores": oracle.threads(),
              "kind": "oracle",
-             "sample": f"first {done} of {wl.B} clouds ({done * wl.N} points), one cloud per "
-                       f"oracle call, fp64, {t_total:.1f} s"},
-            {"clouds": done, "max_err": worst, "bound": tol, "ok": worst <= tol})
+             "sample": f"{done} oracle calls of one cloud ({done * wl.N} points) over the "
+                       f"{wl.B} clouds in order, fp64, {t_total:.1f} s"},
+            {"clouds": checked, "max_err": worst, "bound": tol, "ok": worst <= tol})
 
 
 def network_flops(wl):
@@ -230,36 +242,33 @@ def network_flops(wl):
     return fl
 
 
-def bench_network(args, wl, dev):
+def bench_network(args, wl, dev, peaks=True, cpu_seconds=None):
     """A step is one whole segmentation-network forward (PVConv blocks, point
-    MLPs, max-pool, head) on the batch."""
+    MLPs, max-pool, head) on the batch. Returns the JSON line (a dict)."""
     import numpy as np
     import torch
     from paper_1907_03739_amd.network import DeviceNetwork
 
     B, N = wl.B, wl.N
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    torch.cuda.reset_peak_memory_stats(dev)
+    base = torch.cuda.memory_allocated(dev)
     net = DeviceNetwork(wl.layers, wl.mlps, wl.head, B, N, dev)
     coords = torch.as_tensor(wl.coords).to(dev)
     feats = torch.as_tensor(wl.feats).to(dev)
+    net.forward(coords, feats)
+    torch.cuda.synchronize()
+    memory = {"peak_bytes": int(torch.cuda.max_memory_allocated(dev) - base),
+              "how": "torch.cuda.max_memory_allocated over building the network (weights, "
+                     "activation and workspace buffers), the inputs and one forward"}
     stream = torch.cuda.current_stream(dev)
-    for _ in range(args.warmup):
-        net.forward(coords, feats)
-    torch.cuda.synchronize()
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
-    t0 = time.perf_counter()
-    ev[0].record(stream)
-    for i in range(args.steps):
-        net.forward(coords, feats)
-        ev[i + 1].record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    step_ms = [ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)]
-    ms_per_step = wall * 1e3 / args.steps
-    gpu_out = net.logits.double().cpu().numpy()
 
+    # per-step breakdown first (events between the steps of whole forwards),
+    # so that the headline's steps run at the settled clock
     names = net.steps()
     per = {n: [] for n in names}
-    for _ in range(args.steps):
+    for _ in range(max(args.steps, 10)):
         marks = []
 
         def mark(name, marks=marks):
@@ -271,6 +280,24 @@ def bench_network(args, wl, dev):
         torch.cuda.synchronize()
         for j, n in enumerate(names):
             per[n].append(marks[j].elapsed_time(marks[j + 1]))
+
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    quiet_host()
+    for _ in range(args.warmup):
+        net.forward(coords, feats)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev[0].record(stream)
+    for i in range(args.steps):
+        net.forward(coords, feats)
+        ev[i + 1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    gc.enable()
+    step_ms = [ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)]
+    ms_per_step = wall * 1e3 / args.steps
+    gpu_out = net.logits.double().cpu().numpy()
+
     fl = network_flops(wl)
     kernels = {}
     for n in names:
@@ -284,10 +311,10 @@ def bench_network(args, wl, dev):
                 "unit": "TFLOP/s", "frac": kernels[dom]["frac"], "traffic": None,
                 "kernel": f"network step {dom}", "flop_per_launch": fl[dom],
                 "avg_launch_ms": kernels[dom]["ms"]}
-    peaks = None if args.no_peaks else measured_peaks(stream)
-    if peaks:
+    pk = measured_peaks(stream) if peaks else None
+    if pk:
         roofline["frac_measured_peak"] = round(kernels[dom]["achieved"] /
-                                               peaks["mfma_bf16_tflops"], 4)
+                                               pk["mfma_bf16_tflops"], 4)
     total_fl = sum(fl.values())
     line = {
         "metric": METRIC, "value": round(B * N / (ms_per_step * 1e-3), 1), "unit": "points/s",
@@ -303,25 +330,25 @@ def bench_network(args, wl, dev):
         "network_tflops": round(total_fl / (ms_per_step * 1e-3) / 1e12, 2),
         "roofline": roofline,
         "kernels": kernels,
-        "peaks_measured": peaks,
+        "memory": memory,
+        "peaks_measured": pk,
         "inputs_sha256": wl.sha256(),
     }
-    if not args.no_cpu_baseline:
+    if cpu_seconds:
         import oracle
-        cores = int(os.environ.get("OMP_NUM_THREADS") or len(os.sched_getaffinity(0)))
         done, worst, t_total = 0, 0.0, 0.0
-        for b in range(B):
-            one = synth_one(wl, b)
+        while t_total < cpu_seconds and done < B:
+            one = synth_one(wl, done)
             t1 = time.perf_counter()
             ref = oracle.network_forward(one, stage_dtype="bf16")[0]
             t_total += time.perf_counter() - t1
             rms = float(np.sqrt(np.mean(ref ** 2)))
-            worst = max(worst, float(np.max(np.abs(gpu_out[b] - ref) / (np.abs(ref) + rms))))
+            worst = max(worst, float(np.max(np.abs(gpu_out[done] - ref) /
+                                            (np.abs(ref) + rms))))
             done += 1
-            if t_total >= args.cpu_seconds:
-                break
         line["cpu_baseline"] = {
-            "value": done * N / t_total, "unit": "points/s", "cores": cores, "kind": "oracle",
+            "value": done * N / t_total, "unit": "points/s", "cores": oracle.threads(),
+            "kind": "oracle",
             "sample": f"first {done} of {B} clouds ({done * N} points), one cloud per oracle "
                       f"call, fp64 with bf16 stage storage, {t_total:.1f} s"}
         # end-to-end bound of the network parity tests: sqrt(S) x the chain bound
@@ -329,7 +356,7 @@ def bench_network(args, wl, dev):
         bound = 2e-2 * stages ** 0.5
         line["parity_sample"] = {"clouds": done, "max_err": worst, "bound": round(bound, 4),
                                  "ok": worst <= bound}
-    print(json.dumps(line), flush=True)
+    return line
 
 
 # Layer variants on the default workload's clouds (16 x 2048 points): the
@@ -499,6 +526,320 @@ def synth_one(wl, b):
     return one
 
 
+def cpu_model():
+    """The host CPU's model name and the cores this process may use."""
+    name = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    name = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"model": name, "cores_available": len(os.sched_getaffinity(0))}
+
+
+def quiet_host():
+    """Before a timed region: collect the garbage the breakdown left (graphs
+    among it, whose destruction can block the host) and keep the collector
+    off until the region ends (the caller enables it again)."""
+    import torch
+    gc.collect()
+    torch.cuda.synchronize()
+    gc.disable()
+
+
+# The per-step breakdown: each step captured BREAKDOWN_REPS times back to back
+# in one graph, replayed BREAKDOWN_ROUNDS times (independent of --steps: it is
+# diagnostics around the headline, not the headline).
+BREAKDOWN_REPS = 10
+BREAKDOWN_ROUNDS = 10
+
+
+def captured(fn, stream, reps, rounds):
+    """The graph of `reps` back-to-back calls of fn (so that host submission
+    cannot leave the GPU idle between them) and its ms per call over
+    `rounds` replays, all enqueued before one synchronisation, between HIP
+    events on the stream the kernels run on."""
+    import torch
+    fn()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for _ in range(reps):
+            fn()
+    g.replay()
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(max(1, rounds) + 1)]
+    ev[0].record(stream)
+    for i in range(max(1, rounds)):
+        g.replay()
+        ev[i + 1].record(stream)
+    torch.cuda.synchronize()
+    return g, [ev[i].elapsed_time(ev[i + 1]) / reps for i in range(max(1, rounds))]
+
+
+def graph_times(fn, stream, reps, rounds):
+    """ms per call of fn, as captured() measures it (the graph is freed)."""
+    g, times = captured(fn, stream, reps, rounds)
+    del g
+    return times
+
+
+def cold_times(fn, stream, reps, rounds, dev):
+    """ms per call from cold caches: a graph of `reps` (flush, call) pairs
+    against a graph of `reps` flushes alone, where a flush is a 512 MiB write
+    that evicts the L2s and the 256 MB Infinity Cache."""
+    import torch
+    scratch = torch.empty(512 << 18, dtype=torch.float32, device=dev)
+
+    def flush():
+        scratch.fill_(1.0)
+
+    def both():
+        flush()
+        fn()
+
+    t_flush = graph_times(flush, stream, reps, rounds)
+    t_both = graph_times(both, stream, reps, rounds)
+    del scratch
+    return [b - f for b, f in zip(t_both, t_flush)]
+
+
+def bench_layer(args, wl, dev, cold=True, peaks=True, cpu_seconds=None):
+    """A step is one pvconv_forward call on the whole batch. Returns the JSON
+    line (a dict) and the output of the last timed step."""
+    import numpy as np
+    import torch
+
+    from paper_1907_03739_amd import binding as pv
+
+    L = wl.layers[0]
+    bf16 = wl.dtype == "bf16"
+    cdt = torch.bfloat16 if bf16 else torch.float32
+    B, N, R, cin, cout = wl.B, wl.N, L.R, L.cin, L.cout
+    V = R ** 3
+    stream = torch.cuda.current_stream(dev)
+
+    # ---- device memory of one layer forward: inputs, weights, workspace,
+    # output (the library allocates nothing itself) ------------------------
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    torch.cuda.reset_peak_memory_stats(dev)
+    base = torch.cuda.memory_allocated(dev)
+    layer = pv.DeviceLayer(L, dev, cdt)
+    coords = torch.as_tensor(wl.coords).to(dev)
+    feats = torch.as_tensor(wl.feats).to(dev)
+    out = torch.empty((B, N, cout), dtype=torch.float32, device=dev)
+    ws = torch.empty(max(pv.pvconv_forward_workspace_size(B, N, layer), 256), dtype=torch.uint8,
+                     device=dev)
+    pv.pvconv_forward(coords, feats, layer, out=out, workspace=ws)
+    torch.cuda.synchronize()
+    memory = {"peak_bytes": int(torch.cuda.max_memory_allocated(dev) - base),
+              "workspace_bytes": int(ws.numel()),
+              "how": "torch.cuda.max_memory_allocated over allocating the inputs, weights, "
+                     "output and workspace and one forward"}
+
+    # ---- per-step breakdown, run before the headline so that the headline's
+    # steps run at the settled clock: the forward's kernels called one C-ABI
+    # step at a time on the same data. Convolutions run on weights packed
+    # beforehand (the forward packs them inside the voxelisation launch). ---
+    grid = torch.empty((B, V, cin), dtype=cdt, device=dev)
+    counts = torch.empty((B, V), dtype=torch.int32, device=dev)
+    ids = torch.empty((B, N), dtype=torch.int32, device=dev)
+    pn = torch.empty((B, N, 3), dtype=torch.float32, device=dev)
+    vws = torch.empty(max(pv._lib.pvconv_voxelize_workspace_size(B, N, R), 256),
+                      dtype=torch.uint8, device=dev)
+    hs = [torch.empty((B, V, cout), dtype=cdt, device=dev) for _ in range(L.n_convs)]
+    packed = [pv.pvconv_conv3d_pack_weights(w) for w in layer.conv_w] if bf16 else None
+    dv = torch.empty((B, N, cout), dtype=torch.float32, device=dev)
+    out2 = torch.empty_like(out)
+    fused = bf16 and L.devox == "trilinear"
+    steps = ["voxelize"] + [f"conv{i + 1}" for i in range(L.n_convs)]
+    steps += ["devox_point_mlp", "devoxelize", "point_mlp"] if fused else ["devoxelize",
+                                                                           "point_mlp"]
+
+    def step_fn(name):
+        if name == "voxelize":
+            return lambda: pv.pvconv_voxelize(coords, feats, R, grid_dtype=cdt, grid=grid,
+                                              counts=counts, ids=ids, norm=pn, workspace=vws)
+        if name.startswith("conv"):
+            i = int(name[4:]) - 1
+            src = grid if i == 0 else hs[i - 1]
+            if bf16:
+                return lambda: pv.pvconv_conv3d_packed(src, packed[i], cout, R,
+                                                       bn=layer.conv_bn[i], act="leaky",
+                                                       slope=L.slope, out=hs[i])
+            return lambda: pv.pvconv_conv3d(src, layer.conv_w[i], R, bn=layer.conv_bn[i],
+                                            act="leaky", slope=L.slope, out=hs[i])
+        if name == "devox_point_mlp":
+            return lambda: pv.pvconv_devoxelize_point_mlp(hs[-1], R, pn, feats, layer.mlp_w,
+                                                          bias=layer.mlp_b, bn=layer.mlp_bn,
+                                                          act="relu", out=out2)
+        if name == "devoxelize":
+            return lambda: pv.pvconv_devoxelize(hs[-1], R, pn, out=dv)
+        return lambda: pv.pvconv_point_mlp(feats, layer.mlp_w, bias=layer.mlp_b, bn=layer.mlp_bn,
+                                           act="relu", residual=dv, out=out2)
+
+    for n in steps:  # one eager pass fills every intermediate
+        step_fn(n)()
+    torch.cuda.synchronize()
+    per = {n: graph_times(step_fn(n), stream, BREAKDOWN_REPS, BREAKDOWN_ROUNDS) for n in steps}
+    cold_ms = {n: cold_times(step_fn(n), stream, BREAKDOWN_REPS, BREAKDOWN_ROUNDS, dev)
+               for n in steps} if cold else None
+    pn_host = pn.cpu().numpy()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    quiet_host()
+    # the whole forward, BREAKDOWN_REPS steps per graph (no host launch cost
+    # between kernels), last in the breakdown: about 50 ms of back-to-back
+    # steps, followed by the headline without a pause (the GPU's clock drops
+    # within milliseconds of idling and takes tens of milliseconds of load to
+    # come back). The graph is freed after the headline.
+    fwd = lambda: pv.pvconv_forward(coords, feats, layer, out=out, workspace=ws)
+    fwd_graph, graph_ms = captured(fwd, stream, BREAKDOWN_REPS, BREAKDOWN_ROUNDS)
+
+    # ---- headline: W untimed steps, then exactly K timed steps -------------
+    for _ in range(args.warmup):
+        pv.pvconv_forward(coords, feats, layer, out=out, workspace=ws)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev[0].record(stream)
+    for i in range(args.steps):
+        pv.pvconv_forward(coords, feats, layer, out=out, workspace=ws)
+        ev[i + 1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    del fwd_graph
+    gc.enable()
+    step_ms = [ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)]
+    ms_per_step = wall * 1e3 / args.steps
+    gpu_out = out.double().cpu().numpy()
+
+    pk = measured_peaks(stream) if peaks else None
+
+    # ---- algorithmic work per step ---------------------------------------
+    s_g = 2 if bf16 else 4
+    corners = distinct_corners(pn_host, R)
+    work = {
+        "voxelize": ("GB/s", B * N * (12 + 4 * cin + 4) + B * V * (cin * s_g + 4)),
+        "devoxelize": ("GB/s", B * N * (12 + 4 * cout) + corners * cout * s_g),
+        "point_mlp": ("GB/s", B * N * (4 * cin + 8 * cout)),
+        # read: coordinates, features, the grid rows the points touch, the
+        # weights; write: the output
+        "devox_point_mlp": ("GB/s", B * N * (12 + 4 * cin + 4 * cout) + corners * cout * 2 +
+                            cout * cin * 2),
+    }
+    c = cin
+    for i in range(L.n_convs):
+        work[f"conv{i + 1}"] = ("TFLOP/s", conv_flops(B, R, c, cout))
+        c = cout
+    kernels = {}
+    for n in steps:
+        unit, amount = work[n]
+        ms = statistics.mean(per[n])
+        if unit == "GB/s":
+            rate, peak = amount / (ms * 1e-3) / 1e9, PEAK_HBM_GBS
+        else:
+            rate = amount / (ms * 1e-3) / 1e12
+            peak = PEAK_BF16_TFLOPS if bf16 else PEAK_F32_TFLOPS
+        k = {"ms": round(ms, 4), "ms_min": round(min(per[n]), 4), "achieved": round(rate, 2),
+             "unit": unit, "frac": round(rate / peak, 4), "algorithmic": amount,
+             "in_forward": not (fused and n in ("devoxelize", "point_mlp"))}
+        if cold_ms:
+            ms_cold = statistics.median(cold_ms[n])
+            rate_cold = amount / (ms_cold * 1e-3) / (1e9 if unit == "GB/s" else 1e12)
+            k.update({"ms_cold": round(ms_cold, 4), "achieved_cold": round(rate_cold, 2),
+                      "frac_cold": round(rate_cold / peak, 4)})
+        if pk:
+            mp = pk["hbm_copy_gbs"] if unit == "GB/s" else (
+                pk["mfma_bf16_tflops"] if bf16 else None)
+            if mp:
+                k["frac_measured_peak"] = round(rate / mp, 4)
+        kernels[n] = k
+
+    # dominant kernel: the convolution (one kernel, L.n_convs launches per step)
+    conv_names = [f"conv{i + 1}" for i in range(L.n_convs)]
+    conv_ms = statistics.mean([kernels[n]["ms"] for n in conv_names])
+    conv_work = statistics.mean([work[n][1] for n in conv_names])
+    conv_peak = PEAK_BF16_TFLOPS if bf16 else PEAK_F32_TFLOPS
+    achieved = conv_work / (conv_ms * 1e-3) / 1e12
+    roofline = {"bound": "mfma" if bf16 else "alu", "achieved": round(achieved, 2),
+                "peak": conv_peak, "unit": "TFLOP/s", "frac": round(achieved / conv_peak, 4),
+                "traffic": measured_traffic() if (bf16 and wl.index == 2) else None,
+                "kernel": "pv_conv3d_bf16_kernel" if bf16 else "pv_conv3d_f32_kernel",
+                "flop_per_launch": conv_work, "avg_launch_ms": round(conv_ms, 4),
+                "timed": "pvconv_conv3d_packed (weights packed beforehand)" if bf16 else
+                         "pvconv_conv3d"}
+    if pk and bf16:
+        roofline["frac_measured_peak"] = round(achieved / pk["mfma_bf16_tflops"], 4)
+
+    line = {
+        "metric": METRIC, "value": round(B * N / (ms_per_step * 1e-3), 1), "unit": "points/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16" if bf16 else "f32", "data": "synthetic",
+        "config": {"workload": wl.name, "B": B, "N": N, "R": R, "cin": cin, "cout": cout,
+                   "n_convs": L.n_convs, "points_per_step": B * N},
+        "ms_per_layer": round(ms_per_step, 4),
+        "ms_per_step_events": {"median": round(statistics.median(step_ms), 4),
+                               "min": round(min(step_ms), 4)},
+        "ms_per_step_graph": {"median": round(statistics.median(graph_ms), 4),
+                              "min": round(min(graph_ms), 4),
+                              "how": f"the forward captured {BREAKDOWN_REPS} times in one HIP "
+                                     f"graph, replayed {BREAKDOWN_ROUNDS} times"},
+        "roofline": roofline,
+        "kernels": kernels,
+        "memory": memory,
+        "peaks_measured": pk,
+        "inputs_sha256": wl.sha256(),
+    }
+    if cpu_seconds:
+        cb, parity = cpu_baseline(wl, gpu_out, cpu_seconds)
+        line["cpu_baseline"] = cb
+        line["parity_sample"] = parity
+    return line
+
+
+def compact(line):
+    """The summary of one workload's line kept in the headline's `workloads`."""
+    ks = {n: k for n, k in line["kernels"].items() if k.get("in_forward", True)}
+    dom = max(ks, key=lambda n: ks[n]["ms"])
+    out = {"workload": line["config"]["workload"], "dtype": line["dtype"],
+           "points_per_step": line["config"]["points_per_step"],
+           "ms_per_step": line["ms_per_step"], "points_per_s": line["value"],
+           "dominant": {"step": dom, "ms": ks[dom]["ms"], "achieved": ks[dom]["achieved"],
+                        "unit": ks[dom]["unit"], "frac": ks[dom]["frac"]},
+           "steps": {n: {"ms": k["ms"], "frac": k["frac"], "unit": k["unit"]}
+                     for n, k in ks.items()},
+           "memory_peak_bytes": line["memory"]["peak_bytes"]}
+    if "cpu_baseline" in line:
+        out["cpu_oracle"] = line["cpu_baseline"]
+        out["parity_sample"] = line["parity_sample"]
+    return out
+
+
+def oracle_one_thread(wl, seconds):
+    """The oracle on the workload's first cloud with one thread, repeated for
+    at least `seconds`."""
+    import oracle
+    before = oracle.threads()
+    oracle.set_threads(1)
+    try:
+        L = wl.layers[0]
+        done, t_total = 0, 0.0
+        while t_total < seconds:
+            t0 = time.perf_counter()
+            oracle.pvconv_forward(wl.coords[:1], wl.feats[:1], L)
+            t_total += time.perf_counter() - t0
+            done += 1
+    finally:
+        oracle.set_threads(before)
+    return {"value": round(done * wl.N / t_total, 1), "unit": "points/s", "cores": 1,
+            "kind": "oracle", "sample": f"cloud 0 ({wl.N} points) {done} times, fp64, "
+                                        f"one thread, {t_total:.2f} s"}
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -511,11 +852,9 @@ def main():
     if args.copy_probe:
         return copy_probe(args.copy_probe)
 
-    import numpy as np
     import torch
 
     import synth
-    from paper_1907_03739_amd import binding as pv
 
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
@@ -528,205 +867,30 @@ def main():
     if args.backward:
         return bench_backward(args, dev)
     wl = synth.make_workload(args.workload)
+    cpu_s = None if args.no_cpu_baseline else args.cpu_seconds
     if wl.is_network:
-        return bench_network(args, wl, dev)
-    L = wl.layers[0]
-    bf16 = wl.dtype == "bf16"
-    cdt = torch.bfloat16 if bf16 else torch.float32
-    B, N, R, cin, cout = wl.B, wl.N, L.R, L.cin, L.cout
-    layer = pv.DeviceLayer(L, dev, cdt)
-    coords = torch.as_tensor(wl.coords).to(dev)
-    feats = torch.as_tensor(wl.feats).to(dev)
-    out = torch.empty((B, N, cout), dtype=torch.float32, device=dev)
-    ws = torch.empty(max(pv.pvconv_forward_workspace_size(B, N, layer), 256), dtype=torch.uint8,
-                     device=dev)
-    stream = torch.cuda.current_stream(dev)
-
-    # ---- headline: K whole-layer steps -----------------------------------
-    for _ in range(args.warmup):
-        pv.pvconv_forward(coords, feats, layer, out=out, workspace=ws)
-    torch.cuda.synchronize()
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
-    t0 = time.perf_counter()
-    ev[0].record(stream)
-    for i in range(args.steps):
-        pv.pvconv_forward(coords, feats, layer, out=out, workspace=ws)
-        ev[i + 1].record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    step_ms = [ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)]
-    ms_per_step = wall * 1e3 / args.steps
-    gpu_out = out.double().cpu().numpy()
-
-    # ---- per-step breakdown: the same chain as separate C-ABI calls. Each
-    # call is timed as the average of REPS back-to-back launches captured in a
-    # HIP graph (so that host submission cannot leave the GPU idle between
-    # them), replayed `steps // REPS` times between HIP events on the stream
-    # the kernels run on. Buffers are allocated once, outside the timing. -----
-    names = ["voxelize"] + [f"conv{i + 1}" for i in range(L.n_convs)] + ["devoxelize",
-                                                                         "point_mlp"]
-    V = R ** 3
-    grid = torch.empty((B, V, cin), dtype=cdt, device=dev)
-    counts = torch.empty((B, V), dtype=torch.int32, device=dev)
-    ids = torch.empty((B, N), dtype=torch.int32, device=dev)
-    pn = torch.empty((B, N, 3), dtype=torch.float32, device=dev)
-    vws = torch.empty(max(pv._lib.pvconv_voxelize_workspace_size(B, N, R), 256),
-                      dtype=torch.uint8, device=dev)
-    hs = [torch.empty((B, V, cout), dtype=cdt, device=dev) for _ in range(L.n_convs)]
-    cws = torch.empty(max(pv._lib.pvconv_conv3d_workspace_size(max(cin, cout), cout,
-                                                               1 if bf16 else 0), 256),
-                      dtype=torch.uint8, device=dev)
-    dv = torch.empty((B, N, cout), dtype=torch.float32, device=dev)
-
-    def step_fn(name):
-        if name == "voxelize":
-            return lambda: pv.pvconv_voxelize(coords, feats, R, grid_dtype=cdt, grid=grid,
-                                              counts=counts, ids=ids, norm=pn, workspace=vws)
-        if name.startswith("conv"):
-            i = int(name[4:]) - 1
-            src = grid if i == 0 else hs[i - 1]
-            return lambda: pv.pvconv_conv3d(src, layer.conv_w[i], R, bn=layer.conv_bn[i],
-                                            act="leaky", slope=L.slope, out=hs[i],
-                                            workspace=cws)
-        if name == "devoxelize":
-            return lambda: pv.pvconv_devoxelize(hs[-1], R, pn, out=dv)
-        return lambda: pv.pvconv_point_mlp(feats, layer.mlp_w, bias=layer.mlp_b, bn=layer.mlp_bn,
-                                           act="relu", residual=dv, out=out)
-
-    for n in names:  # one eager pass fills every intermediate
-        step_fn(n)()
-    torch.cuda.synchronize()
-    REPS = 10
-    per = {}
-    for n in names:
-        fn = step_fn(n)
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g):
-            for _ in range(REPS):
-                fn()
-        g.replay()
-        torch.cuda.synchronize()
-        times = []
-        for _ in range(max(1, args.steps // REPS)):
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record(stream)
-            g.replay()
-            e1.record(stream)
-            torch.cuda.synchronize()
-            times.append(e0.elapsed_time(e1) / REPS)
-        per[n] = times
-        del g
-
-    # ---- the same calls cold: each after a 512 MiB write that evicts the
-    # L2s and the 256 MB Infinity Cache. A graph of REPS (flush, call) pairs
-    # against a graph of REPS flushes alone; the difference per pair is the
-    # call's time from cold caches. ---------------------------------------
-    scratch = torch.empty(512 << 18, dtype=torch.float32, device=dev)
-    COLD = 10
-
-    def timed(graph):
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        graph.replay()
-        e1.record(stream)
-        torch.cuda.synchronize()
-        return e0.elapsed_time(e1)
-
-    g0 = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(g0):
-        for _ in range(COLD):
-            scratch.fill_(1.0)
-    g0.replay()
-    torch.cuda.synchronize()
-    cold = {}
-    for n in names:
-        fn = step_fn(n)
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g):
-            for _ in range(COLD):
-                scratch.fill_(1.0)
-                fn()
-        g.replay()
-        torch.cuda.synchronize()
-        diffs = []
-        for _ in range(max(1, args.steps // COLD)):
-            t_flush = timed(g0)
-            t_both = timed(g)
-            diffs.append((t_both - t_flush) / COLD)
-        cold[n] = diffs
-        del g
-    del g0, scratch
-    pn_host = pn.cpu().numpy()
-
-    peaks = None if args.no_peaks else measured_peaks(stream)
-
-    # ---- algorithmic work per step ---------------------------------------
-    s_g = 2 if bf16 else 4
-    work = {
-        "voxelize": ("GB/s", B * N * (12 + 4 * cin + 4) + B * V * (cin * s_g + 4)),
-        "devoxelize": ("GB/s", B * N * (12 + 4 * cout) + distinct_corners(pn_host, R) * cout * s_g),
-        "point_mlp": ("GB/s", B * N * (4 * cin + 8 * cout)),
-    }
-    c = cin
-    for i in range(L.n_convs):
-        work[f"conv{i + 1}"] = ("TFLOP/s", conv_flops(B, R, c, cout))
-        c = cout
-    kernels = {}
-    for n in names:
-        unit, amount = work[n]
-        ms = statistics.mean(per[n])
-        if unit == "GB/s":
-            rate, peak = amount / (ms * 1e-3) / 1e9, PEAK_HBM_GBS
-        else:
-            rate = amount / (ms * 1e-3) / 1e12
-            peak = PEAK_BF16_TFLOPS if bf16 else PEAK_F32_TFLOPS
-        ms_cold = statistics.median(cold[n])
-        rate_cold = amount / (ms_cold * 1e-3) / (1e9 if unit == "GB/s" else 1e12)
-        kernels[n] = {"ms": round(ms, 4), "ms_min": round(min(per[n]), 4),
-                      "achieved": round(rate, 2), "unit": unit, "frac": round(rate / peak, 4),
-                      "ms_cold": round(ms_cold, 4), "achieved_cold": round(rate_cold, 2),
-                      "frac_cold": round(rate_cold / peak, 4), "algorithmic": amount}
-        if peaks:
-            mp = peaks["hbm_copy_gbs"] if unit == "GB/s" else (
-                peaks["mfma_bf16_tflops"] if bf16 else None)
-            if mp:
-                kernels[n]["frac_measured_peak"] = round(rate / mp, 4)
-                kernels[n]["frac_cold_measured_peak"] = round(rate_cold / mp, 4)
-
-    # dominant kernel: the convolution (one kernel, L.n_convs launches per step)
-    conv_names = [f"conv{i + 1}" for i in range(L.n_convs)]
-    conv_ms = statistics.mean([kernels[n]["ms"] for n in conv_names])
-    conv_work = statistics.mean([work[n][1] for n in conv_names])
-    conv_peak = PEAK_BF16_TFLOPS if bf16 else PEAK_F32_TFLOPS
-    achieved = conv_work / (conv_ms * 1e-3) / 1e12
-    roofline = {"bound": "mfma" if bf16 else "alu", "achieved": round(achieved, 2),
-                "peak": conv_peak, "unit": "TFLOP/s", "frac": round(achieved / conv_peak, 4),
-                "traffic": measured_traffic() if (bf16 and args.workload == 2) else None,
-                "kernel": "pv_conv3d_bf16_kernel" if bf16 else
-                "pv_conv3d_f32_kernel", "flop_per_launch": conv_work,
-                "avg_launch_ms": round(conv_ms, 4)}
-    if peaks and bf16:
-        roofline["frac_measured_peak"] = round(achieved / peaks["mfma_bf16_tflops"], 4)
-
-    line = {
-        "metric": METRIC, "value": round(B * N / (ms_per_step * 1e-3), 1), "unit": "points/s",
-        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-        "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": "bf16" if bf16 else "f32", "data": "synthetic",
-        "config": {"workload": wl.name, "B": B, "N": N, "R": R, "cin": cin, "cout": cout,
-                   "n_convs": L.n_convs, "points_per_step": B * N},
-        "ms_per_layer": round(ms_per_step, 4),
-        "ms_per_step_events": {"median": round(statistics.median(step_ms), 4),
-                               "min": round(min(step_ms), 4)},
-        "roofline": roofline,
-        "kernels": kernels,
-        "peaks_measured": peaks,
-        "inputs_sha256": wl.sha256(),
-    }
-    if not args.no_cpu_baseline:
-        cb, parity = cpu_baseline(wl, gpu_out, args.cpu_seconds)
-        line["cpu_baseline"] = cb
-        line["parity_sample"] = parity
+        line = bench_network(args, wl, dev, peaks=not args.no_peaks, cpu_seconds=cpu_s)
+    else:
+        line = bench_layer(args, wl, dev, peaks=not args.no_peaks, cpu_seconds=cpu_s)
+    if "cpu_baseline" in line:
+        line["cpu_baseline"]["cpu"] = cpu_model()
+    if args.workload == 2 and not args.no_workloads:
+        # the other workloads, each a compact summary: the same step timing
+        # (W warmup, K timed steps), per-step breakdown, memory and a bounded
+        # oracle sample with its parity check
+        wls = {}
+        for idx in (1, 3, 4, 5):
+            w = synth.make_workload(idx)
+            ws_cpu = None if args.no_cpu_baseline else args.workload_cpu_seconds
+            if w.is_network:
+                one = bench_network(args, w, dev, peaks=False, cpu_seconds=ws_cpu)
+            else:
+                one = bench_layer(args, w, dev, cold=False, peaks=False, cpu_seconds=ws_cpu)
+            summary = compact(one)
+            if idx == 1 and not args.no_cpu_baseline:
+                summary["cpu_oracle_one_thread"] = oracle_one_thread(w, 1.0)
+            wls[str(idx)] = summary
+        line["workloads"] = wls
     print(json.dumps(line), flush=True)
 
 
