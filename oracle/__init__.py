@@ -65,6 +65,11 @@ def _load():
         "ref_conv3d_backward_weight": [_P, _P, _I64, ctypes.c_int, _I64, _I64, _P],
         "ref_linear": [_P, _I64, _I64, _I64, _P, _P, _P],
         "ref_maxpool": [_P, _I64, _I64, _I64, _P],
+        "ref_fps": [_P, _I64, _I64, _I64, _P],
+        "ref_ball_query": [_P, _I64, _I64, _P, _I64, ctypes.c_float, _I64, _P],
+        "ref_group": [_P, _P, _I64, _I64, _I64, _P, _I64, _P, _I64, _P],
+        "ref_three_nn": [_P, _I64, _I64, _P, _I64, _P, _P],
+        "ref_three_interpolate": [_P, _I64, _I64, _I64, _P, _P, _I64, _P],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -344,6 +349,92 @@ def maxpool(x: np.ndarray) -> np.ndarray:
     B, N, C = x.shape
     out = np.empty((B, C))
     _check(lib.ref_maxpool(_ptr(x), B, N, C, _ptr(out)), "maxpool")
+    return out
+
+
+# ----------------------------------------------------------------------------
+# PointNet++ primitives of PVCNN++ (Section 5.2 "Models": PointNet++ extended
+# with PVConv), as PointNet++ defines them. The choices of an index (farthest
+# point, ball membership, nearest neighbours) compare fp32 squared distances
+# formed as the kernels form them.
+# ----------------------------------------------------------------------------
+def _f32(a) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.float32)
+
+
+def fps(xyz: np.ndarray, npoint: int) -> np.ndarray:
+    """Iterative farthest point sampling: xyz [B][N][3] -> indices [B][npoint]
+    (the first is point 0; each next maximises the distance to the samples
+    taken so far, the lowest index among equals)."""
+    lib = _load()
+    xyz = _f32(xyz)
+    B, N, _ = xyz.shape
+    idx = np.empty((B, npoint), np.int32)
+    _check(lib.ref_fps(_ptr(xyz), B, N, npoint, _ptr(idx)), "fps")
+    return idx
+
+
+def gather_points(xyz: np.ndarray, idx: np.ndarray) -> np.ndarray:
+    """xyz [B][N][D], idx [B][M] -> [B][M][D] (the sampled points)."""
+    return np.stack([xyz[b][idx[b]] for b in range(xyz.shape[0])])
+
+
+def ball_query(xyz: np.ndarray, centers: np.ndarray, radius: float, nsample: int) -> np.ndarray:
+    """For each centre, the first nsample points in index order within the
+    radius (squared distance below radius^2), short lists completed with
+    their first entry: xyz [B][N][3], centers [B][M][3] -> [B][M][nsample]."""
+    lib = _load()
+    xyz, centers = _f32(xyz), _f32(centers)
+    B, N, _ = xyz.shape
+    M = centers.shape[1]
+    idx = np.empty((B, M, nsample), np.int32)
+    _check(lib.ref_ball_query(_ptr(xyz), B, N, _ptr(centers), M, float(radius), nsample,
+                              _ptr(idx)), "ball_query")
+    return idx
+
+
+def group(xyz: np.ndarray, feats: np.ndarray, centers: np.ndarray, idx: np.ndarray) -> np.ndarray:
+    """Rows (x_j - c_i, f_j) for each centre i and each of its neighbours j:
+    -> [B][M][nsample][3 + C]."""
+    lib = _load()
+    xyz, centers = _f32(xyz), _f32(centers)
+    feats = _f64(feats)
+    idx = np.ascontiguousarray(idx, np.int32)
+    B, N, _ = xyz.shape
+    C = feats.shape[2]
+    M, S = idx.shape[1], idx.shape[2]
+    out = np.empty((B, M, S, 3 + C))
+    _check(lib.ref_group(_ptr(xyz), _ptr(feats), B, N, C, _ptr(centers), M, _ptr(idx), S,
+                         _ptr(out)), "group")
+    return out
+
+
+def three_nn(unknown: np.ndarray, known: np.ndarray):
+    """The three nearest known points of each unknown point and their
+    normalised inverse-distance weights: -> idx [B][n][3], weight [B][n][3]."""
+    lib = _load()
+    unknown, known = _f32(unknown), _f32(known)
+    B, n, _ = unknown.shape
+    m = known.shape[1]
+    idx = np.empty((B, n, 3), np.int32)
+    w = np.empty((B, n, 3))
+    _check(lib.ref_three_nn(_ptr(unknown), B, n, _ptr(known), m, _ptr(idx), _ptr(w)),
+           "three_nn")
+    return idx, w
+
+
+def three_interpolate(feats: np.ndarray, idx: np.ndarray, weight: np.ndarray) -> np.ndarray:
+    """out[b][i] = sum_k weight[b][i][k] * feats[b][idx[b][i][k]]: feats
+    [B][m][C] -> [B][n][C]."""
+    lib = _load()
+    feats = _f64(feats)
+    idx = np.ascontiguousarray(idx, np.int32)
+    weight = _f64(weight)
+    B, m, C = feats.shape
+    n = idx.shape[1]
+    out = np.empty((B, n, C))
+    _check(lib.ref_three_interpolate(_ptr(feats), B, m, C, _ptr(idx), _ptr(weight), n,
+                                     _ptr(out)), "three_interpolate")
     return out
 
 

@@ -31,6 +31,13 @@
  *                      nearest); each is the adjoint of the linear map the
  *                      forward step applies
  *   ref_maxpool        Section 5.1 "Models" (PointNet backbone global feature)
+ *   ref_fps, ref_ball_query, ref_group, ref_three_nn, ref_three_interpolate
+ *                      the PointNet++ primitives that PVCNN++ keeps around its
+ *                      PVConv layers (Section 5.2 "Models": PointNet++
+ *                      extended with PVConv), as PointNet++ (Qi et al., 2017)
+ *                      defines them: iterative farthest point sampling, ball
+ *                      query grouping, and inverse-distance interpolation
+ *                      over the three nearest neighbours
  * Fusion by addition (Section 4.3) and the composition of the steps live in
  * oracle/__init__.py.
  *
@@ -47,7 +54,11 @@
  *  - grid layout [B][R][R][R][C] with x -> u (slowest), z -> w, C innermost.
  *
  * All arithmetic is IEEE fp64 with round-to-nearest-even and no contraction
- * (built with -ffp-contract=off).
+ * (built with -ffp-contract=off), except where a floating-point comparison
+ * decides an index (the farthest point, ball membership, the three nearest
+ * neighbours): there the squared distance is computed in fp32 as
+ * (dx*dx + dy*dy) + dz*dz with dx = x_j - x_c, the precision and order the GPU
+ * kernels use, so that both sides make the same choices.
  */
 #include <math.h>
 #include <stdint.h>
@@ -504,5 +515,160 @@ int ref_conv3d_backward_weight(const double* dy, const double* x, int64_t B, int
                             for (int64_t i = 0; i < Cin; i++) out[i] += g * xin[i];
                         }
         }
+    return PV_ORACLE_OK;
+}
+
+/* ------------------------------------------------------------------------- */
+/* PointNet++ primitives (PVCNN++, Section 5.2 "Models")                     */
+/* ------------------------------------------------------------------------- */
+
+/* Squared distance between two points of fp32 coordinates, in fp32, in the
+ * order the kernels use. */
+static float sqdist_f32(const float* a, const float* b) {
+    const float dx = a[0] - b[0];
+    const float dy = a[1] - b[1];
+    const float dz = a[2] - b[2];
+    const float xx = dx * dx;
+    const float yy = dy * dy;
+    const float zz = dz * dz;
+    return (xx + yy) + zz;
+}
+
+/* Iterative farthest point sampling. The first sample is point 0; each next
+ * one is the point whose distance to the samples taken so far (the minimum
+ * over them) is largest, the lowest index among equals. xyz [B][N][3],
+ * idx out [B][npoint]. 1 <= npoint <= N. */
+int ref_fps(const float* xyz, int64_t B, int64_t N, int64_t npoint, int32_t* idx) {
+    if (B < 0 || N < 1 || npoint < 1 || npoint > N) return PV_ORACLE_EINVAL;
+    float* dmin = (float*)malloc((size_t)N * sizeof(float));
+    if (!dmin) return PV_ORACLE_EINVAL;
+    for (int64_t b = 0; b < B; b++) {
+        const float* p = xyz + b * N * 3;
+        int32_t* out = idx + b * npoint;
+        for (int64_t j = 0; j < N; j++) dmin[j] = INFINITY;
+        int64_t last = 0;
+        out[0] = 0;
+        for (int64_t s = 1; s < npoint; s++) {
+            int64_t best = 0;
+            float bestd = -1.0f;
+            for (int64_t j = 0; j < N; j++) {
+                const float d = sqdist_f32(p + j * 3, p + last * 3);
+                if (d < dmin[j]) dmin[j] = d;
+                if (dmin[j] > bestd) {
+                    bestd = dmin[j];
+                    best = j;
+                }
+            }
+            out[s] = (int32_t)best;
+            last = best;
+        }
+    }
+    free(dmin);
+    return PV_ORACLE_OK;
+}
+
+/* Ball query: for each centre, the first nsample points (in index order)
+ * whose squared distance to it is below radius^2 (radius^2 formed in fp32);
+ * a centre with fewer repeats its first neighbour in the remaining slots, and
+ * one with none gets point 0 in every slot. xyz [B][N][3], centers
+ * [B][npoint][3], idx out [B][npoint][nsample]. */
+int ref_ball_query(const float* xyz, int64_t B, int64_t N, const float* centers,
+                   int64_t npoint, float radius, int64_t nsample, int32_t* idx) {
+    if (B < 0 || N < 1 || npoint < 0 || nsample < 1 || !(radius >= 0.0f))
+        return PV_ORACLE_EINVAL;
+    const float r2 = radius * radius;
+    for (int64_t b = 0; b < B; b++)
+        for (int64_t i = 0; i < npoint; i++) {
+            const float* c = centers + (b * npoint + i) * 3;
+            int32_t* out = idx + (b * npoint + i) * nsample;
+            int64_t cnt = 0;
+            for (int64_t j = 0; j < N && cnt < nsample; j++)
+                if (sqdist_f32(xyz + (b * N + j) * 3, c) < r2) out[cnt++] = (int32_t)j;
+            const int32_t fill = cnt > 0 ? out[0] : 0;
+            for (int64_t k = cnt; k < nsample; k++) out[k] = fill;
+        }
+    return PV_ORACLE_OK;
+}
+
+/* Grouping: for centre i and slot k with neighbour j = idx[b][i][k], the row
+ * (x_j - c_i, feats_j): the neighbour's coordinates relative to the centre,
+ * then its C features. out [B][npoint][nsample][3 + C]. */
+int ref_group(const float* xyz, const double* feats, int64_t B, int64_t N, int64_t C,
+              const float* centers, int64_t npoint, const int32_t* idx, int64_t nsample,
+              double* out) {
+    if (B < 0 || N < 1 || C < 0 || npoint < 0 || nsample < 1) return PV_ORACLE_EINVAL;
+    for (int64_t b = 0; b < B; b++)
+        for (int64_t i = 0; i < npoint; i++) {
+            const float* cf = centers + (b * npoint + i) * 3;
+            for (int64_t k = 0; k < nsample; k++) {
+                const int64_t j = idx[(b * npoint + i) * nsample + k];
+                if (j < 0 || j >= N) return PV_ORACLE_EINVAL;
+                double* o = out + ((b * npoint + i) * nsample + k) * (3 + C);
+                const float* p = xyz + (b * N + j) * 3;
+                for (int a = 0; a < 3; a++) o[a] = (double)p[a] - (double)cf[a];
+                for (int64_t ch = 0; ch < C; ch++) o[3 + ch] = feats[(b * N + j) * C + ch];
+            }
+        }
+    return PV_ORACLE_OK;
+}
+
+/* Three nearest neighbours: for each of the n unknown points, the three known
+ * points (of m >= 3) with the smallest squared distance, nearest first, the
+ * lower index first among equals; and the inverse-distance weights
+ * w_k = (1 / (d_k + 1e-8)) / sum_l (1 / (d_l + 1e-8)) with d the Euclidean
+ * distance. unknown [B][n][3], known [B][m][3]; idx out [B][n][3], weight out
+ * [B][n][3]. */
+int ref_three_nn(const float* unknown, int64_t B, int64_t n, const float* known, int64_t m,
+                 int32_t* idx, double* weight) {
+    if (B < 0 || n < 0 || m < 3) return PV_ORACLE_EINVAL;
+    for (int64_t b = 0; b < B; b++)
+        for (int64_t i = 0; i < n; i++) {
+            const float* u = unknown + (b * n + i) * 3;
+            float bd[3] = {INFINITY, INFINITY, INFINITY};
+            int64_t bi[3] = {0, 0, 0};
+            for (int64_t j = 0; j < m; j++) {
+                const float d = sqdist_f32(known + (b * m + j) * 3, u);
+                /* strictly smaller moves ahead: among equals the earlier
+                 * (lower) index stays in front */
+                if (d < bd[0]) {
+                    bd[2] = bd[1]; bi[2] = bi[1];
+                    bd[1] = bd[0]; bi[1] = bi[0];
+                    bd[0] = d; bi[0] = j;
+                } else if (d < bd[1]) {
+                    bd[2] = bd[1]; bi[2] = bi[1];
+                    bd[1] = d; bi[1] = j;
+                } else if (d < bd[2]) {
+                    bd[2] = d; bi[2] = j;
+                }
+            }
+            double inv[3], sum = 0.0;
+            for (int k = 0; k < 3; k++) {
+                inv[k] = 1.0 / (sqrt((double)bd[k]) + 1e-8);
+                sum += inv[k];
+            }
+            for (int k = 0; k < 3; k++) {
+                idx[(b * n + i) * 3 + k] = (int32_t)bi[k];
+                weight[(b * n + i) * 3 + k] = inv[k] / sum;
+            }
+        }
+    return PV_ORACLE_OK;
+}
+
+/* Inverse-distance interpolation: out[b][i][c] = sum_k weight[b][i][k] *
+ * feats[b][idx[b][i][k]][c]. feats [B][m][C], out [B][n][C]. */
+int ref_three_interpolate(const double* feats, int64_t B, int64_t m, int64_t C,
+                          const int32_t* idx, const double* weight, int64_t n, double* out) {
+    if (B < 0 || m < 1 || C < 1 || n < 0) return PV_ORACLE_EINVAL;
+    for (int64_t b = 0; b < B; b++)
+        for (int64_t i = 0; i < n; i++)
+            for (int64_t c = 0; c < C; c++) {
+                double acc = 0.0;
+                for (int k = 0; k < 3; k++) {
+                    const int64_t j = idx[(b * n + i) * 3 + k];
+                    if (j < 0 || j >= m) return PV_ORACLE_EINVAL;
+                    acc += weight[(b * n + i) * 3 + k] * feats[(b * m + j) * C + c];
+                }
+                out[(b * n + i) * C + c] = acc;
+            }
     return PV_ORACLE_OK;
 }

@@ -715,3 +715,114 @@ def test_layer_bf16_storage_stays_within_a_bf16_ulp_chain():
     assert 0.0 < np.max(d) < 0.05 * rms
     with pytest.raises(ValueError):
         oracle.pvconv_forward(wl.coords, wl.feats, L, stage_dtype="f16")
+
+
+# ----------------------------------------------------------------------------
+# PointNet++ primitives of PVCNN++ (Section 5.2 "Models")
+# ----------------------------------------------------------------------------
+def test_fps_on_a_line_follows_the_halving_order():
+    # nine points at x = 0..8: after 0 the farthest is 8, then 4, then 2 and
+    # 6 (equal: the lower index first), then 1, 3, 5, 7
+    xyz = np.zeros((1, 9, 3), np.float32)
+    xyz[0, :, 0] = np.arange(9)
+    assert oracle.fps(xyz, 9)[0].tolist() == [0, 8, 4, 2, 6, 1, 3, 5, 7]
+    assert oracle.fps(xyz, 3)[0].tolist() == [0, 8, 4]
+
+
+def test_fps_each_pick_is_the_farthest_from_the_picks_before_it():
+    from scipy.spatial.distance import cdist
+    rng = np.random.default_rng(11)
+    xyz = rng.random((2, 300, 3)).astype(np.float32)
+    idx = oracle.fps(xyz, 40)
+    for b in range(2):
+        pts = xyz[b].astype(np.float64)
+        picks = idx[b].tolist()
+        assert picks[0] == 0 and len(set(picks)) == len(picks)
+        for s in range(1, len(picks)):
+            dmin = cdist(pts, pts[picks[:s]]).min(axis=1)
+            assert picks[s] == int(np.argmax(dmin)), (b, s)
+
+
+def _lattice(rng, B, N, step=1.0 / 8):
+    """Points on a lattice of spacing 1/8 in [0, 2): every coordinate
+    difference and squared distance is exact in fp32 and fp64."""
+    return (rng.integers(0, 16, size=(B, N, 3)) * step).astype(np.float32)
+
+
+def test_ball_query_matches_a_kd_tree():
+    from scipy.spatial import cKDTree
+    rng = np.random.default_rng(12)
+    xyz = _lattice(rng, 2, 400)
+    centers = _lattice(rng, 2, 30)
+    # radius^2 = 0.1 is no multiple of 1/64: no point lies on a sphere
+    radius, nsample = np.float32(np.sqrt(0.1)), 16
+    idx = oracle.ball_query(xyz, centers, radius, nsample)
+    for b in range(2):
+        tree = cKDTree(xyz[b].astype(np.float64))
+        for i in range(30):
+            near = sorted(tree.query_ball_point(centers[b, i].astype(np.float64),
+                                                float(radius)))[:nsample]
+            want = near + [near[0] if near else 0] * (nsample - len(near))
+            assert idx[b, i].tolist() == want, (b, i)
+
+
+def test_ball_query_with_no_neighbour_fills_point_zero():
+    xyz = np.zeros((1, 5, 3), np.float32)
+    centers = np.full((1, 1, 3), 5.0, np.float32)
+    assert oracle.ball_query(xyz, centers, 1.0, 4)[0, 0].tolist() == [0, 0, 0, 0]
+
+
+def test_group_rows_are_relative_coordinates_then_features():
+    rng = np.random.default_rng(13)
+    xyz = _lattice(rng, 2, 64)
+    feats = rng.normal(size=(2, 64, 5))
+    cidx = oracle.fps(xyz, 8)
+    centers = oracle.gather_points(xyz, cidx)
+    idx = oracle.ball_query(xyz, centers, 0.5, 6)
+    g = oracle.group(xyz, feats, centers, idx)
+    assert g.shape == (2, 8, 6, 8)
+    for b in range(2):
+        nb = xyz[b][idx[b]]
+        np.testing.assert_array_equal(g[b, ..., :3] + centers[b][:, None, :], nb)
+        np.testing.assert_array_equal(g[b, ..., 3:], feats[b][idx[b]])
+    # wherever a centre appears among its own neighbours, its row is (0, 0, 0, f_c)
+    own = idx == cidx[:, :, None]
+    assert own.any()
+    assert np.all(g[own][:, :3] == 0.0)
+
+
+def test_three_nn_matches_a_kd_tree_and_weights_sum_to_one():
+    from scipy.spatial import cKDTree
+    rng = np.random.default_rng(14)
+    known = rng.random((2, 50, 3)).astype(np.float32)
+    unknown = rng.random((2, 200, 3)).astype(np.float32)
+    idx, w = oracle.three_nn(unknown, known)
+    for b in range(2):
+        d, j = cKDTree(known[b].astype(np.float64)).query(unknown[b].astype(np.float64), k=3)
+        np.testing.assert_array_equal(idx[b], j)
+        inv = 1.0 / (d + 1e-8)
+        np.testing.assert_allclose(w[b], inv / inv.sum(axis=1, keepdims=True), rtol=1e-6)
+    np.testing.assert_allclose(w.sum(axis=2), 1.0, rtol=1e-12)
+    # an unknown point on a known one takes (nearly) all its weight from it
+    idx2, w2 = oracle.three_nn(known[:, :5], known)
+    assert np.array_equal(idx2[:, :, 0], np.tile(np.arange(5), (2, 1)))
+    assert np.all(w2[:, :, 0] > 1.0 - 1e-6)
+
+
+def test_three_interpolate_is_linear_and_keeps_constants():
+    rng = np.random.default_rng(15)
+    known = rng.random((1, 20, 3)).astype(np.float32)
+    unknown = rng.random((1, 70, 3)).astype(np.float32)
+    idx, w = oracle.three_nn(unknown, known)
+    F, G = rng.normal(size=(1, 20, 4)), rng.normal(size=(1, 20, 4))
+    np.testing.assert_allclose(oracle.three_interpolate(2.5 * F + G, idx, w),
+                               2.5 * oracle.three_interpolate(F, idx, w) +
+                               oracle.three_interpolate(G, idx, w), rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(oracle.three_interpolate(np.full((1, 20, 3), 7.0), idx, w), 7.0,
+                               rtol=1e-12)
+    # one-hot features give back each neighbour's weight
+    onehot = np.eye(20)[None]
+    out = oracle.three_interpolate(onehot, idx, w)
+    for i in range(70):
+        for k in range(3):
+            assert out[0, i, idx[0, i, k]] == pytest.approx(w[0, i, k], rel=1e-12)
