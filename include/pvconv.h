@@ -295,6 +295,69 @@ pvconv_status pvconv_devoxelize_point_mlp(const void* grid, int R, const float* 
 pvconv_status pvconv_maxpool(const void* x, pvconv_dtype dt, int x_ld, int B, int N, int C,
                              float* out, void* stream);
 
+/* ========================================================================= */
+/* PVCNN++ (Section 5.2 "Models": PointNet++ extended with PVConv): the      */
+/* PointNet++ primitives around the PVConv layers, as PointNet++ (Qi et al., */
+/* 2017) defines them. Set abstraction samples centres by farthest point     */
+/* sampling, gathers each centre's neighbours by ball query, groups their    */
+/* relative coordinates and features for a shared MLP (pvconv_point_mlp) and */
+/* takes the maximum over the neighbours (pvconv_maxpool); feature           */
+/* propagation interpolates features back to the denser level from the three */
+/* nearest neighbours. Every choice of an index compares fp32 squared        */
+/* distances (dx*dx + dy*dy) + dz*dz, dx = x_j - x_c, without contraction,   */
+/* with ties to the lower index, so results are the same on every run.       */
+/* Coordinates are [B][*][3] fp32; indices are within the cloud.             */
+/* ========================================================================= */
+
+/* Farthest point sampling: idx[b][0] = 0; idx[b][s] is the point whose      */
+/* distance to points idx[b][0..s-1] (the minimum over them) is largest.     */
+/*  xyz      [B][N][3], 1 <= N <= 16384 (larger: PVCONV_ENOTSUP)             */
+/*  idx      out [B][npoint] int32, 1 <= npoint <= N                         */
+/*  new_xyz  out [B][npoint][3] (the sampled points' coordinates) or NULL    */
+/* One workgroup per cloud: the npoint steps are sequential.                 */
+pvconv_status pvconv_furthest_point_sample(const float* xyz, int B, int N, int npoint,
+                                           int32_t* idx, float* new_xyz, void* stream);
+
+/* Ball query: idx[b][i][0..] = the first nsample points, in index order,    */
+/* whose squared distance to centre i is below radius*radius (formed in     */
+/* fp32); a centre with fewer repeats its first neighbour in the remaining   */
+/* slots, one with none gets 0 in every slot.                                */
+/*  xyz [B][N][3], centers [B][M][3], idx out [B][M][nsample] int32.         */
+/*  N >= 1, nsample >= 1, radius >= 0.                                       */
+pvconv_status pvconv_ball_query(const float* xyz, int B, int N, const float* centers, int M,
+                                float radius, int nsample, int32_t* idx, void* stream);
+
+/* Grouping: row (b, i, k) of out = (x_j - c_i, feats_j) with j =            */
+/* idx[b][i][k]: 3 relative coordinates, then the C features.                */
+/*  xyz [B][N][3]; feats [B][N][C] (feat_dt, row stride feat_ld, 0: C; C may */
+/*  be 0 and feats NULL); centers [B][M][3]; idx [B][M][nsample] (entries    */
+/*  outside [0, N) are clamped: memory-safe, result unspecified);            */
+/*  out [B][M][nsample][3 + C] (out_dt, row stride out_ld, 0: 3 + C).        */
+pvconv_status pvconv_group_points(const float* xyz, const void* feats, pvconv_dtype feat_dt,
+                                  int feat_ld, int B, int N, int C, const float* centers, int M,
+                                  const int32_t* idx, int nsample, void* out,
+                                  pvconv_dtype out_dt, int out_ld, void* stream);
+
+/* Three nearest neighbours: for each unknown point the three known points   */
+/* with the smallest squared distance, nearest first, and the weights        */
+/* w_k = (1 / (d_k + 1e-8)) / sum_l (1 / (d_l + 1e-8)), d the Euclidean      */
+/* distance, in fp32.                                                        */
+/*  unknown [B][n][3], known [B][m][3] with m >= 3;                          */
+/*  idx out [B][n][3] int32, weight out [B][n][3] fp32.                      */
+pvconv_status pvconv_three_nn(const float* unknown, int B, int n, const float* known, int m,
+                              int32_t* idx, float* weight, void* stream);
+
+/* Inverse-distance interpolation: out[b][i][c] = sum_k weight[b][i][k] *    */
+/* feats[b][idx[b][i][k]][c], fp32 sums.                                     */
+/*  feats [B][m][C] (feat_dt, row stride feat_ld, 0: C); idx, weight as      */
+/*  pvconv_three_nn writes them (indices clamped into [0, m));               */
+/*  out [B][n][C] (out_dt, row stride out_ld, 0: C), e.g. a column slice of  */
+/*  the feature-propagation input that also holds the skip features.         */
+pvconv_status pvconv_three_interpolate(const void* feats, pvconv_dtype feat_dt, int feat_ld,
+                                       int B, int m, int C, const int32_t* idx,
+                                       const float* weight, int n, void* out,
+                                       pvconv_dtype out_dt, int out_ld, void* stream);
+
 /* Devoxelisation of a layer (Section 4.1 "Devoxelization"). */
 typedef enum { PVCONV_DEVOX_TRILINEAR = 0, PVCONV_DEVOX_NEAREST = 1 } pvconv_devox;
 

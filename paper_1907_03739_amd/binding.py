@@ -61,6 +61,12 @@ _SIGS = {
                              _I),
     "pvconv_devoxelize_point_mlp": ([_VP, _I, _VP, _I, _I, _VP, _I, _I, _I, _I, _VP, _VP, _VP,
                                      _I, _F, _VP, _I, _I, _VP], _I),
+    "pvconv_furthest_point_sample": ([_VP, _I, _I, _I, _VP, _VP, _VP], _I),
+    "pvconv_ball_query": ([_VP, _I, _I, _VP, _I, _F, _I, _VP, _VP], _I),
+    "pvconv_group_points": ([_VP, _VP, _I, _I, _I, _I, _I, _VP, _I, _VP, _I, _VP, _I, _I, _VP],
+                            _I),
+    "pvconv_three_nn": ([_VP, _I, _I, _VP, _I, _VP, _VP, _VP], _I),
+    "pvconv_three_interpolate": ([_VP, _I, _I, _I, _I, _I, _VP, _VP, _I, _VP, _I, _I, _VP], _I),
     "pvconv_conv3d_noalloc": ([_VP, _I, _I, _I, _I, _VP, _VP, _VP, _I, _F, _I, _VP, _I, _VP],
                               _I),
     "pvconv_devoxelize": ([_VP, _I, _I, _I, _I, _VP, _I, _VP, _VP], _I),
@@ -279,6 +285,85 @@ def pvconv_devoxelize_point_mlp(grid: torch.Tensor, R: int, norm_coords: torch.T
         Cin, Cout, _p(weight.contiguous()), _p(bias),
         ctypes.byref(bns) if bn is not None else None, ACT[act], slope, _p(out), _dt(out),
         out_ld, _stream(x)))
+    return out
+
+
+def _xyz(t: torch.Tensor, what: str):
+    if t.dim() != 3 or t.shape[2] != 3 or t.dtype != torch.float32 or not t.is_contiguous():
+        raise ValueError(f"{what} must be a contiguous [B][N][3] float32 tensor")
+    return t
+
+
+def pvconv_furthest_point_sample(xyz: torch.Tensor, npoint: int, idx=None, new_xyz=None,
+                                 want_xyz=True):
+    """xyz [B][N][3] f32 -> idx [B][npoint] int32 (and the sampled points
+    [B][npoint][3] f32 unless want_xyz is False)."""
+    B, N, _ = _xyz(xyz, "xyz").shape
+    idx = _out(idx, (B, npoint), torch.int32, xyz.device, "idx")
+    if want_xyz:
+        new_xyz = _out(new_xyz, (B, npoint, 3), torch.float32, xyz.device, "new_xyz")
+    _check("pvconv_furthest_point_sample", _lib.pvconv_furthest_point_sample(
+        _p(xyz), B, N, npoint, _p(idx), _p(new_xyz) if want_xyz else None, _stream(xyz)))
+    return (idx, new_xyz) if want_xyz else idx
+
+
+def pvconv_ball_query(xyz: torch.Tensor, centers: torch.Tensor, radius: float, nsample: int,
+                      idx=None):
+    """-> idx [B][M][nsample] int32: the first nsample points within radius."""
+    B, N, _ = _xyz(xyz, "xyz").shape
+    M = _xyz(centers, "centers").shape[1]
+    idx = _out(idx, (B, M, nsample), torch.int32, xyz.device, "idx")
+    _check("pvconv_ball_query", _lib.pvconv_ball_query(
+        _p(xyz), B, N, _p(centers), M, float(radius), nsample, _p(idx), _stream(xyz)))
+    return idx
+
+
+def pvconv_group_points(xyz: torch.Tensor, feats: Optional[torch.Tensor], centers: torch.Tensor,
+                        idx: torch.Tensor, out: Optional[torch.Tensor] = None,
+                        out_dtype=torch.bfloat16):
+    """-> [B][M][nsample][3 + C]: neighbour coordinates relative to the centre,
+    then the neighbour's features (feats [B][N][C], rows evenly strided, or None)."""
+    B, N, _ = _xyz(xyz, "xyz").shape
+    M, S = idx.shape[1], idx.shape[2]
+    C = 0 if feats is None else feats.shape[2]
+    fld = 0 if feats is None else _rows(feats, N, C)
+    if out is None:
+        out = torch.empty((B, M, S, 3 + C), dtype=_torch_dt(out_dtype), device=xyz.device)
+    # a contiguous [B][M][nsample][3 + C] tensor, or [B*M*nsample][3 + C] rows
+    # (possibly a column slice of a wider array)
+    flat = out.view(B * M * S, out.shape[-1]) if out.dim() == 4 else out
+    old = _rows(flat, B * M * S, 3 + C)
+    _check("pvconv_group_points", _lib.pvconv_group_points(
+        _p(xyz), _p(feats), _dt(feats) if feats is not None else F32, fld, B, N, C,
+        _p(centers.contiguous()), M, _p(idx.contiguous()), S, _p(out), _dt(out), old,
+        _stream(xyz)))
+    return out
+
+
+def pvconv_three_nn(unknown: torch.Tensor, known: torch.Tensor, idx=None, weight=None):
+    """-> idx [B][n][3] int32, weight [B][n][3] f32."""
+    B, n, _ = _xyz(unknown, "unknown").shape
+    m = _xyz(known, "known").shape[1]
+    idx = _out(idx, (B, n, 3), torch.int32, unknown.device, "idx")
+    weight = _out(weight, (B, n, 3), torch.float32, unknown.device, "weight")
+    _check("pvconv_three_nn", _lib.pvconv_three_nn(_p(unknown), B, n, _p(known), m, _p(idx),
+                                                   _p(weight), _stream(unknown)))
+    return idx, weight
+
+
+def pvconv_three_interpolate(feats: torch.Tensor, idx: torch.Tensor, weight: torch.Tensor,
+                             out: Optional[torch.Tensor] = None, out_dtype=torch.float32):
+    """feats [B][m][C] (rows evenly strided) -> [B][n][C]; out may be a column
+    slice of a wider [B][n][*] tensor."""
+    B, m, C = feats.shape
+    n = idx.shape[1]
+    fld = _rows(feats, m, C)
+    if out is None:
+        out = torch.empty((B, n, C), dtype=_torch_dt(out_dtype), device=feats.device)
+    old = _rows(out, n, C)
+    _check("pvconv_three_interpolate", _lib.pvconv_three_interpolate(
+        _p(feats), _dt(feats), fld, B, m, C, _p(idx.contiguous()), _p(weight.contiguous()), n,
+        _p(out), _dt(out), old, _stream(feats)))
     return out
 
 

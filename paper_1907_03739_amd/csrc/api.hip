@@ -394,6 +394,107 @@ pvconv_status pvconv_maxpool(const void* x, pvconv_dtype dt, int x_ld, int B, in
     return pv_launch_maxpool(x, dt == PVCONV_BF16, x_ld, B, N, C, out, as_stream(stream));
 }
 
+pvconv_status pvconv_furthest_point_sample(const float* xyz, int B, int N, int npoint,
+                                           int32_t* idx, float* new_xyz, void* stream) {
+    if (B < 0 || N < 1 || npoint < 1 || npoint > N || !sizes_fit(B, N)) return PVCONV_EINVAL;
+    if (B == 0) return PVCONV_OK;
+    if (!xyz || !idx || ((uintptr_t)xyz & 3) || ((uintptr_t)idx & 3) || ((uintptr_t)new_xyz & 3))
+        return PVCONV_EINVAL;
+    if (N > kPvFpsMaxN) return PVCONV_ENOTSUP;
+    if (bytes_overlap(idx, (size_t)B * npoint * 4, xyz, (size_t)B * N * 12) ||
+        (new_xyz && (bytes_overlap(new_xyz, (size_t)B * npoint * 12, xyz, (size_t)B * N * 12) ||
+                     bytes_overlap(new_xyz, (size_t)B * npoint * 12, idx, (size_t)B * npoint * 4))))
+        return PVCONV_EINVAL;
+    return pv_launch_fps(xyz, B, N, npoint, idx, new_xyz, as_stream(stream));
+}
+
+pvconv_status pvconv_ball_query(const float* xyz, int B, int N, const float* centers, int M,
+                                float radius, int nsample, int32_t* idx, void* stream) {
+    if (B < 0 || N < 1 || M < 0 || nsample < 1 || !(radius >= 0.f) || !sizes_fit(B, N) ||
+        !sizes_fit(B, M) || (long long)B * M * nsample > (1LL << 30))
+        return PVCONV_EINVAL;
+    if (B == 0 || M == 0) return PVCONV_OK;
+    if (!xyz || !centers || !idx || ((uintptr_t)xyz & 3) || ((uintptr_t)centers & 3) ||
+        ((uintptr_t)idx & 3))
+        return PVCONV_EINVAL;
+    const size_t ib = (size_t)B * M * nsample * 4;
+    if (bytes_overlap(idx, ib, xyz, (size_t)B * N * 12) ||
+        bytes_overlap(idx, ib, centers, (size_t)B * M * 12))
+        return PVCONV_EINVAL;
+    return pv_launch_ball_query(xyz, B, N, centers, M, radius, nsample, idx, as_stream(stream));
+}
+
+pvconv_status pvconv_group_points(const float* xyz, const void* feats, pvconv_dtype feat_dt,
+                                  int feat_ld, int B, int N, int C, const float* centers, int M,
+                                  const int32_t* idx, int nsample, void* out,
+                                  pvconv_dtype out_dt, int out_ld, void* stream) {
+    if (B < 0 || N < 1 || C < 0 || C > PVCONV_MAX_MLP_CHANNELS - 3 || M < 0 || nsample < 1 ||
+        !sizes_fit(B, N) || (long long)B * M * nsample > (1LL << 30))
+        return PVCONV_EINVAL;
+    if (!dtype_ok(feat_dt) || !dtype_ok(out_dt)) return PVCONV_EINVAL;
+    if (feat_ld == 0) feat_ld = C;
+    if (out_ld == 0) out_ld = 3 + C;
+    if (feat_ld < C || out_ld < 3 + C) return PVCONV_EINVAL;
+    if (B == 0 || M == 0) return PVCONV_OK;
+    if (!xyz || !centers || !idx || !out || (C > 0 && !feats)) return PVCONV_EINVAL;
+    if (((uintptr_t)xyz & 3) || ((uintptr_t)centers & 3) || ((uintptr_t)idx & 3) ||
+        ((uintptr_t)feats & (esize(feat_dt) - 1)) || ((uintptr_t)out & (esize(out_dt) - 1)))
+        return PVCONV_EINVAL;
+    const long long rows = (long long)B * M * nsample;
+    const size_t ob = (size_t)((rows - 1) * out_ld + 3 + C) * esize(out_dt);
+    if (bytes_overlap(out, ob, xyz, (size_t)B * N * 12) ||
+        bytes_overlap(out, ob, centers, (size_t)B * M * 12) ||
+        bytes_overlap(out, ob, idx, (size_t)rows * 4) ||
+        (C > 0 && bytes_overlap(out, ob, feats,
+                                (size_t)(((long long)B * N - 1) * feat_ld + C) * esize(feat_dt))))
+        return PVCONV_EINVAL;
+    return pv_launch_group(xyz, feats, feat_dt == PVCONV_BF16, feat_ld, B, N, C, centers, M, idx,
+                           nsample, out, out_dt == PVCONV_BF16, out_ld, as_stream(stream));
+}
+
+pvconv_status pvconv_three_nn(const float* unknown, int B, int n, const float* known, int m,
+                              int32_t* idx, float* weight, void* stream) {
+    if (B < 0 || n < 0 || m < 3 || !sizes_fit(B, n) || !sizes_fit(B, m)) return PVCONV_EINVAL;
+    if (B == 0 || n == 0) return PVCONV_OK;
+    if (!unknown || !known || !idx || !weight || ((uintptr_t)unknown & 3) ||
+        ((uintptr_t)known & 3) || ((uintptr_t)idx & 3) || ((uintptr_t)weight & 3))
+        return PVCONV_EINVAL;
+    const size_t ob = (size_t)B * n * 12;
+    if (bytes_overlap(idx, ob, weight, ob) || bytes_overlap(idx, ob, unknown, ob) ||
+        bytes_overlap(weight, ob, unknown, ob) ||
+        bytes_overlap(idx, ob, known, (size_t)B * m * 12) ||
+        bytes_overlap(weight, ob, known, (size_t)B * m * 12))
+        return PVCONV_EINVAL;
+    return pv_launch_three_nn(unknown, B, n, known, m, idx, weight, as_stream(stream));
+}
+
+pvconv_status pvconv_three_interpolate(const void* feats, pvconv_dtype feat_dt, int feat_ld,
+                                       int B, int m, int C, const int32_t* idx,
+                                       const float* weight, int n, void* out,
+                                       pvconv_dtype out_dt, int out_ld, void* stream) {
+    if (B < 0 || m < 1 || C < 1 || n < 0 || C > PVCONV_MAX_MLP_CHANNELS || !sizes_fit(B, n) ||
+        !sizes_fit(B, m))
+        return PVCONV_EINVAL;
+    if (!dtype_ok(feat_dt) || !dtype_ok(out_dt)) return PVCONV_EINVAL;
+    if (feat_ld == 0) feat_ld = C;
+    if (out_ld == 0) out_ld = C;
+    if (feat_ld < C || out_ld < C) return PVCONV_EINVAL;
+    if (B == 0 || n == 0) return PVCONV_OK;
+    if (!feats || !idx || !weight || !out || ((uintptr_t)feats & (esize(feat_dt) - 1)) ||
+        ((uintptr_t)idx & 3) || ((uintptr_t)weight & 3) || ((uintptr_t)out & (esize(out_dt) - 1)))
+        return PVCONV_EINVAL;
+    const long long rows = (long long)B * n;
+    const size_t ob = (size_t)((rows - 1) * out_ld + C) * esize(out_dt);
+    if (bytes_overlap(out, ob, feats,
+                      (size_t)(((long long)B * m - 1) * feat_ld + C) * esize(feat_dt)) ||
+        bytes_overlap(out, ob, idx, (size_t)rows * 12) ||
+        bytes_overlap(out, ob, weight, (size_t)rows * 12))
+        return PVCONV_EINVAL;
+    return pv_launch_three_interpolate(feats, feat_dt == PVCONV_BF16, feat_ld, B, m, C, idx,
+                                       weight, n, out, out_dt == PVCONV_BF16, out_ld,
+                                       as_stream(stream));
+}
+
 size_t pvconv_forward_workspace_size(int B, int N, const pvconv_layer* L) {
     if (B < 0 || N < 0 || check_layer(L) != PVCONV_OK) return 0;
     return carve_forward(nullptr, B, N, L).total;

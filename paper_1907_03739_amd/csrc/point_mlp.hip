@@ -137,7 +137,11 @@ __global__ __launch_bounds__(kWaves * 64) void pv_point_mlp_tile_kernel(
         // groups of one point, so each corner row is read contiguously. NB*2
         // items per thread (fewer valid ones in a ragged last channel block),
         // in rounds of up to four whose 32 corner loads are all in flight
-        // together: one workgroup per CU has to cover the memory latency.
+        // together. The launcher takes NB = 2 (64-channel column blocks):
+        // one round of four items, and at the part-segmentation layer 512
+        // workgroups, two per CU, all resident at once. The kernel reads
+        // nothing from HBM twice, so the latency of this gather and of the
+        // feature loads that follow it is what bounds it.
         const int tid = threadIdx.x;
         const int G = ncols >> 3, items = kWaves * 32 * G;
         const size_t V = (size_t)dvin.R * dvin.R * dvin.R;

@@ -192,6 +192,22 @@ pvconv_status pv_launch_point_mlp(const void* x, bool x_bf16, int x_ld, int M, i
                                   int out_ld, hipStream_t s);
 pvconv_status pv_launch_maxpool(const void* x, bool bf16, int x_ld, int B, int N, int C,
                                 float* out, hipStream_t s);
+// PointNet++ primitives of PVCNN++ (pointnet2.hip)
+constexpr int kPvFpsMaxN = 16384;  // points per cloud farthest point sampling takes
+pvconv_status pv_launch_fps(const float* xyz, int B, int N, int npoint, int32_t* idx,
+                            float* new_xyz, hipStream_t s);
+pvconv_status pv_launch_ball_query(const float* xyz, int B, int N, const float* centers, int M,
+                                   float radius, int nsample, int32_t* idx, hipStream_t s);
+pvconv_status pv_launch_group(const float* xyz, const void* feats, bool feat_bf16, int feat_ld,
+                              int B, int N, int C, const float* centers, int M,
+                              const int32_t* idx, int nsample, void* out, bool out_bf16,
+                              int out_ld, hipStream_t s);
+pvconv_status pv_launch_three_nn(const float* unknown, int B, int n, const float* known, int m,
+                                 int32_t* idx, float* weight, hipStream_t s);
+pvconv_status pv_launch_three_interpolate(const void* feats, bool feat_bf16, int feat_ld, int B,
+                                          int m, int C, const int32_t* idx, const float* weight,
+                                          int n, void* out, bool out_bf16, int out_ld,
+                                          hipStream_t s);
 // backward (backward.hip)
 size_t pv_conv3d_bwd_data_ws_bytes(int Cin, int Cout, bool bf16);
 pvconv_status pv_launch_voxelize_backward(const void* dgrid, bool bf16, int B, int N, int C,

@@ -30,7 +30,7 @@ def declared_functions():
 
 def test_library_exports_every_declared_symbol():
     names = declared_functions()
-    assert len(names) == 25
+    assert len(names) == 30
     out = subprocess.run(["nm", "-D", "--defined-only", b.LIB_PATH], capture_output=True,
                          text=True, check=True).stdout
     exported = set(re.findall(r"\bT (pvconv_\w+)", out))
@@ -453,3 +453,79 @@ def test_peak_probe_library():
     assert lib.pv_peak_mfma(0, 10, FAKE, None) != 0          # rejected before any launch
     assert lib.pv_peak_copy(FAKE_ODD, FAKE, 4, None) != 0    # misaligned
     assert lib.pv_peak_copy(FAKE, FAKE, 0, None) == 0         # nothing to do
+
+
+# ---- PointNet++ primitives ---------------------------------------------------
+@pytest.mark.parametrize("args,status", [
+    (dict(B=-1), EINVAL), (dict(N=0), EINVAL), (dict(npoint=0), EINVAL),
+    (dict(npoint=101), EINVAL), (dict(B=0), OK), (dict(xyz=None), EINVAL),
+    (dict(idx=None), EINVAL), (dict(xyz=FAKE_ODD), EINVAL),
+    (dict(N=20000, npoint=10), ENOTSUP),
+    (dict(idx=ctypes.c_void_p(0x100000 + 64)), EINVAL),        # over xyz
+    (dict(new_xyz=ctypes.c_void_p(0x400000 + 8)), EINVAL),     # over idx
+])
+def test_furthest_point_sample_rejects(args, status):
+    a = dict(xyz=FAKE, B=2, N=100, npoint=10, idx=ctypes.c_void_p(0x400000), new_xyz=None)
+    a.update(args)
+    assert L.pvconv_furthest_point_sample(a["xyz"], a["B"], a["N"], a["npoint"], a["idx"],
+                                          a["new_xyz"], None) == status
+
+
+@pytest.mark.parametrize("args,status", [
+    (dict(B=-1), EINVAL), (dict(N=0), EINVAL), (dict(M=-1), EINVAL), (dict(nsample=0), EINVAL),
+    (dict(radius=-1.0), EINVAL), (dict(radius=float("nan")), EINVAL), (dict(B=0), OK),
+    (dict(M=0), OK), (dict(xyz=None), EINVAL), (dict(centers=None), EINVAL),
+    (dict(idx=None), EINVAL), (dict(idx=ctypes.c_void_p(0x200000 + 4)), EINVAL),
+])
+def test_ball_query_rejects(args, status):
+    a = dict(xyz=FAKE, B=2, N=100, centers=ctypes.c_void_p(0x200000), M=10, radius=0.2,
+             nsample=16, idx=ctypes.c_void_p(0x400000))
+    a.update(args)
+    assert L.pvconv_ball_query(a["xyz"], a["B"], a["N"], a["centers"], a["M"], a["radius"],
+                               a["nsample"], a["idx"], None) == status
+
+
+@pytest.mark.parametrize("args,status", [
+    (dict(B=-1), EINVAL), (dict(N=0), EINVAL), (dict(C=-1), EINVAL), (dict(nsample=0), EINVAL),
+    (dict(fdt=5), EINVAL), (dict(fld=4), EINVAL), (dict(old=7), EINVAL), (dict(B=0), OK),
+    (dict(feats=None), EINVAL), (dict(out=None), EINVAL), (dict(idx=None), EINVAL),
+    (dict(out=ctypes.c_void_p(0x300000 + 8)), EINVAL),      # over idx
+    (dict(out=ctypes.c_void_p(0x500000 + 2)), EINVAL),      # over feats
+])
+def test_group_points_rejects(args, status):
+    a = dict(xyz=FAKE, feats=ctypes.c_void_p(0x500000), fdt=1, fld=0, B=2, N=100, C=8,
+             centers=ctypes.c_void_p(0x200000), M=10, idx=ctypes.c_void_p(0x300000), nsample=16,
+             out=ctypes.c_void_p(0x1000000), odt=1, old=0)
+    a.update(args)
+    assert L.pvconv_group_points(a["xyz"], a["feats"], a["fdt"], a["fld"], a["B"], a["N"],
+                                 a["C"], a["centers"], a["M"], a["idx"], a["nsample"], a["out"],
+                                 a["odt"], a["old"], None) == status
+
+
+@pytest.mark.parametrize("args,status", [
+    (dict(B=-1), EINVAL), (dict(n=-1), EINVAL), (dict(m=2), EINVAL), (dict(B=0), OK),
+    (dict(n=0), OK), (dict(unknown=None), EINVAL), (dict(idx=None), EINVAL),
+    (dict(weight=ctypes.c_void_p(0x300000 + 12)), EINVAL),   # over idx
+])
+def test_three_nn_rejects(args, status):
+    a = dict(unknown=FAKE, B=2, n=100, known=ctypes.c_void_p(0x200000), m=10,
+             idx=ctypes.c_void_p(0x300000), weight=ctypes.c_void_p(0x400000))
+    a.update(args)
+    assert L.pvconv_three_nn(a["unknown"], a["B"], a["n"], a["known"], a["m"], a["idx"],
+                             a["weight"], None) == status
+
+
+@pytest.mark.parametrize("args,status", [
+    (dict(B=-1), EINVAL), (dict(m=0), EINVAL), (dict(C=0), EINVAL), (dict(fld=3), EINVAL),
+    (dict(old=3), EINVAL), (dict(fdt=9), EINVAL), (dict(B=0), OK), (dict(n=0), OK),
+    (dict(feats=None), EINVAL), (dict(out=None), EINVAL),
+    (dict(out=ctypes.c_void_p(0x300000 + 16)), EINVAL),      # over idx
+])
+def test_three_interpolate_rejects(args, status):
+    a = dict(feats=FAKE, fdt=1, fld=0, B=2, m=10, C=8, idx=ctypes.c_void_p(0x300000),
+             weight=ctypes.c_void_p(0x400000), n=100, out=ctypes.c_void_p(0x1000000), odt=0,
+             old=0)
+    a.update(args)
+    assert L.pvconv_three_interpolate(a["feats"], a["fdt"], a["fld"], a["B"], a["m"], a["C"],
+                                      a["idx"], a["weight"], a["n"], a["out"], a["odt"],
+                                      a["old"], None) == status
