@@ -6,7 +6,9 @@ batch: normalisation and voxelisation, the 3x3x3 convolutions with batch norm
 and leaky ReLU, trilinear devoxelisation and the point-branch MLP whose
 epilogue adds the two branches (Section 4 of the PVCNN paper).
 Network workloads (3, 4): a step is one forward of the PVCNN segmentation
-network (Section 5.1): PVConv blocks, point MLPs, max-pool, head.
+network (Section 5.1): PVConv blocks, point MLPs, max-pool, head. Workload 6:
+one forward of PVCNN++ (Section 5.2: PointNet++'s set abstraction and feature
+propagation levels around PVConv layers) on 4 x 8192 room points.
 Inputs (coordinates, features, weights) are resident in device memory before
 the timed region starts.
 
@@ -53,9 +55,10 @@ def parse():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=100,
                     help="untimed steps first (the clock settles under load within ~50 ms)")
-    ap.add_argument("--workload", type=int, default=2, choices=(1, 2, 3, 4, 5),
+    ap.add_argument("--workload", type=int, default=2, choices=(1, 2, 3, 4, 5, 6),
                     help="1 fp32 layer R=8, 2 part-seg layer R=32, 3 part-seg network, "
-                         "4 scene-seg network, 5 stress layer R=64")
+                         "4 scene-seg network, 5 stress layer R=64, 6 PVCNN++ scene-seg "
+                         "network")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="lower bound of CPU work for the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -242,19 +245,61 @@ def network_flops(wl):
     return fl
 
 
+def pvcnn2_work(wl):
+    """Work of each step of the PVCNN++ forward: MFMA flops of the PVConv
+    layers, the shared MLPs and the head (bf16), and for the sampling steps
+    the fp32 operations of farthest point sampling and ball query (about 9
+    per distance: three differences, three products, two sums and a
+    comparison), which run as sequential steps per cloud."""
+    B = wl.B
+    npts = [wl.N] + [lev.npoint for lev in wl.sa]
+    work = {}
+    c = wl.feats.shape[2]
+    c_feat = []
+    for l, lev in enumerate(wl.sa):
+        if lev.pvconvs:
+            f = 0.0
+            for L in lev.pvconvs:
+                ci = L.cin
+                for _ in range(L.n_convs):
+                    f += conv_flops(B, L.R, ci, L.cout)
+                    ci = L.cout
+                f += 2.0 * B * npts[l] * L.cin * L.cout
+            work[f"pvconv{l + 1}"] = ("TFLOP/s", f)
+            c = lev.pvconvs[-1].cout
+        c_feat.append(c)
+        work[f"sample{l + 1}"] = ("fp32 TFLOP/s", 9.0 * B * npts[l] * (lev.npoint + lev.npoint))
+        rows = B * lev.npoint * lev.nsample
+        work[f"group_mlp{l + 1}"] = ("TFLOP/s", sum(2.0 * rows * m.w.shape[0] * m.w.shape[1]
+                                                   for m in lev.mlps))
+        c = lev.mlps[-1].w.shape[0]
+    for k, lev in enumerate(wl.fp):
+        l = len(wl.sa) - 1 - k
+        work[f"fp{k + 1}"] = ("TFLOP/s", sum(2.0 * B * npts[l] * m.w.shape[0] * m.w.shape[1]
+                                            for m in lev.mlps))
+    work["head"] = ("TFLOP/s", sum(2.0 * B * wl.N * m.w.shape[0] * m.w.shape[1]
+                                   for m in wl.head))
+    return work
+
+
 def bench_network(args, wl, dev, peaks=True, cpu_seconds=None):
-    """A step is one whole segmentation-network forward (PVConv blocks, point
-    MLPs, max-pool, head) on the batch. Returns the JSON line (a dict)."""
+    """A step is one whole segmentation-network forward on the batch: PVCNN
+    (PVConv blocks, point MLPs, max-pool, head) or PVCNN++ (set abstraction
+    and feature propagation levels around PVConv layers, head). Returns the
+    JSON line (a dict)."""
     import numpy as np
     import torch
-    from paper_1907_03739_amd.network import DeviceNetwork
+    from paper_1907_03739_amd.network import DeviceNetwork, DevicePVCNN2
 
     B, N = wl.B, wl.N
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
     torch.cuda.reset_peak_memory_stats(dev)
     base = torch.cuda.memory_allocated(dev)
-    net = DeviceNetwork(wl.layers, wl.mlps, wl.head, B, N, dev)
+    if wl.is_pvcnn2:
+        net = DevicePVCNN2(wl.sa, wl.fp, wl.head, B, N, wl.feats.shape[2], dev)
+    else:
+        net = DeviceNetwork(wl.layers, wl.mlps, wl.head, B, N, dev)
     coords = torch.as_tensor(wl.coords).to(dev)
     feats = torch.as_tensor(wl.feats).to(dev)
     net.forward(coords, feats)
@@ -298,33 +343,48 @@ def bench_network(args, wl, dev, peaks=True, cpu_seconds=None):
     ms_per_step = wall * 1e3 / args.steps
     gpu_out = net.logits.double().cpu().numpy()
 
-    fl = network_flops(wl)
+    work = pvcnn2_work(wl) if wl.is_pvcnn2 else {n: ("TFLOP/s", f)
+                                                 for n, f in network_flops(wl).items()}
     kernels = {}
     for n in names:
+        unit, amount = work[n]
+        peak = PEAK_F32_TFLOPS if unit.startswith("fp32") else PEAK_BF16_TFLOPS
         ms = statistics.mean(per[n])
-        rate = fl[n] / (ms * 1e-3) / 1e12
+        rate = amount / (ms * 1e-3) / 1e12
         kernels[n] = {"ms": round(ms, 4), "ms_min": round(min(per[n]), 4),
                       "achieved": round(rate, 2), "unit": "TFLOP/s",
-                      "frac": round(rate / PEAK_BF16_TFLOPS, 4), "algorithmic": fl[n]}
+                      "frac": round(rate / peak, 4), "algorithmic": amount}
+        if unit.startswith("fp32"):
+            kernels[n]["bound"] = "alu (sequential per cloud)"
     dom = max(names, key=lambda n: kernels[n]["ms"])
-    roofline = {"bound": "mfma", "achieved": kernels[dom]["achieved"], "peak": PEAK_BF16_TFLOPS,
+    dom_f32 = work[dom][0].startswith("fp32")
+    roofline = {"bound": "alu" if dom_f32 else "mfma", "achieved": kernels[dom]["achieved"],
+                "peak": PEAK_F32_TFLOPS if dom_f32 else PEAK_BF16_TFLOPS,
                 "unit": "TFLOP/s", "frac": kernels[dom]["frac"], "traffic": None,
-                "kernel": f"network step {dom}", "flop_per_launch": fl[dom],
+                "kernel": f"network step {dom}", "flop_per_launch": work[dom][1],
                 "avg_launch_ms": kernels[dom]["ms"]}
     pk = measured_peaks(stream) if peaks else None
-    if pk:
+    if pk and not dom_f32:
         roofline["frac_measured_peak"] = round(kernels[dom]["achieved"] /
                                                pk["mfma_bf16_tflops"], 4)
-    total_fl = sum(fl.values())
+    total_fl = sum(a for u, a in work.values() if not u.startswith("fp32"))
     line = {
         "metric": METRIC, "value": round(B * N / (ms_per_step * 1e-3), 1), "unit": "points/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": wl.name, "B": B, "N": N,
-                   "blocks": [[L.cin, L.cout, L.R] for L in wl.layers],
-                   "mlps": [int(m.w.shape[0]) for m in wl.mlps],
-                   "head": [int(h.w.shape[0]) for h in wl.head], "points_per_step": B * N},
+        "config": ({"workload": wl.name, "B": B, "N": N,
+                    "sa": [{"pvconv": [[L.cin, L.cout, L.R] for L in lev.pvconvs],
+                            "npoint": lev.npoint, "radius": lev.radius,
+                            "nsample": lev.nsample, "mlp": [int(m.w.shape[0]) for m in lev.mlps]}
+                           for lev in wl.sa],
+                    "fp": [[int(m.w.shape[0]) for m in lev.mlps] for lev in wl.fp],
+                    "head": [int(h.w.shape[0]) for h in wl.head], "points_per_step": B * N}
+                   if wl.is_pvcnn2 else
+                   {"workload": wl.name, "B": B, "N": N,
+                    "blocks": [[L.cin, L.cout, L.R] for L in wl.layers],
+                    "mlps": [int(m.w.shape[0]) for m in wl.mlps],
+                    "head": [int(h.w.shape[0]) for h in wl.head], "points_per_step": B * N}),
         "ms_per_step_events": {"median": round(statistics.median(step_ms), 4),
                                "min": round(min(step_ms), 4)},
         "network_tflops": round(total_fl / (ms_per_step * 1e-3) / 1e12, 2),
@@ -340,7 +400,8 @@ def bench_network(args, wl, dev, peaks=True, cpu_seconds=None):
         while t_total < cpu_seconds and done < B:
             one = synth_one(wl, done)
             t1 = time.perf_counter()
-            ref = oracle.network_forward(one, stage_dtype="bf16")[0]
+            ref = (oracle.pvcnn2_forward(one, stage_dtype="bf16") if wl.is_pvcnn2 else
+                   oracle.network_forward(one, stage_dtype="bf16"))[0]
             t_total += time.perf_counter() - t1
             rms = float(np.sqrt(np.mean(ref ** 2)))
             worst = max(worst, float(np.max(np.abs(gpu_out[done] - ref) /
@@ -352,7 +413,11 @@ def bench_network(args, wl, dev, peaks=True, cpu_seconds=None):
             "sample": f"first {done} of {B} clouds ({done * N} points), one cloud per oracle "
                       f"call, fp64 with bf16 stage storage, {t_total:.1f} s"}
         # end-to-end bound of the network parity tests: sqrt(S) x the chain bound
-        stages = len(wl.layers) + len(wl.mlps) + len(wl.head) - 1
+        if wl.is_pvcnn2:
+            stages = sum(len(lev.pvconvs) + 1 + len(lev.mlps) for lev in wl.sa) + sum(
+                1 + len(lev.mlps) for lev in wl.fp) + len(wl.head) - 1
+        else:
+            stages = len(wl.layers) + len(wl.mlps) + len(wl.head) - 1
         bound = 2e-2 * stages ** 0.5
         line["parity_sample"] = {"clouds": done, "max_err": worst, "bound": round(bound, 4),
                                  "ok": worst <= bound}
@@ -879,7 +944,7 @@ def main():
         # (W warmup, K timed steps), per-step breakdown, memory and a bounded
         # oracle sample with its parity check
         wls = {}
-        for idx in (1, 3, 4, 5):
+        for idx in (1, 3, 4, 5, 6):
             w = synth.make_workload(idx)
             ws_cpu = None if args.no_cpu_baseline else args.workload_cpu_seconds
             if w.is_network:

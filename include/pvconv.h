@@ -338,6 +338,15 @@ pvconv_status pvconv_group_points(const float* xyz, const void* feats, pvconv_dt
                                   const int32_t* idx, int nsample, void* out,
                                   pvconv_dtype out_dt, int out_ld, void* stream);
 
+/* Maximum over each centre's neighbours (the set abstraction's pooling):    */
+/* out[g][c] = max_k x[g*nsample + k][c], exact.                             */
+/*  x    [G*nsample][C] (dt, row stride x_ld, 0: C), e.g. the shared MLP's   */
+/*       output on the grouped rows (G = B*M centres)                        */
+/*  out  [G][C] (out_dt, row stride out_ld, 0: C), e.g. a column slice of a  */
+/*       feature-propagation input. NaN inputs: result unspecified.          */
+pvconv_status pvconv_group_max(const void* x, pvconv_dtype dt, int x_ld, int G, int nsample,
+                               int C, void* out, pvconv_dtype out_dt, int out_ld, void* stream);
+
 /* Three nearest neighbours: for each unknown point the three known points   */
 /* with the smallest squared distance, nearest first, and the weights        */
 /* w_k = (1 / (d_k + 1e-8)) / sum_l (1 / (d_l + 1e-8)), d the Euclidean      */

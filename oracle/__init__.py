@@ -579,3 +579,55 @@ def network_forward(wl, return_stages=False, stage_dtype="f64"):
     if return_stages:
         return h, stages, g
     return h
+
+
+def pvcnn2_forward(wl, stage_dtype="f64", return_levels=False):
+    """PVCNN++ segmentation forward (Section 5.2 "Models": PointNet++ extended
+    with PVConv).
+
+    Set abstraction, per level: the level's PVConv layers on its points
+    (features of the same points), then npoint centres by farthest point
+    sampling, the first nsample points within the radius of each centre, the
+    grouped rows (relative coordinates, then features) through the shared
+    MLP, and the maximum over each centre's neighbours: the next level's
+    points and features. Feature propagation, from the coarsest level down:
+    the coarser features interpolated onto the level's points from the three
+    nearest coarser points, concatenated with the features that level's set
+    abstraction consumed (its skip link), through a shared MLP. Then the
+    head on the original points.
+
+    stage_dtype "bf16" stores every step's output in bf16 (round_bf16) before
+    the next step reads it, the storage of the bf16 network; the logits are
+    never rounded. Returns logits [B][N][classes] (and with return_levels the
+    level coordinates, the skip features and the propagated features)."""
+    store = _storage(stage_dtype)
+    xyz = [_f32(wl.coords)]
+    x = _f64(wl.feats)
+    skips = []
+    for lev in wl.sa:
+        for L in lev.pvconvs:
+            x = store(pvconv_forward(xyz[-1], x, L, stage_dtype=stage_dtype))
+        skips.append(x)
+        centers = gather_points(xyz[-1], fps(xyz[-1], lev.npoint))
+        nb = ball_query(xyz[-1], centers, lev.radius, lev.nsample)
+        h = store(group(xyz[-1], x, centers, nb))
+        for lp in lev.mlps:
+            h = store(shared_mlp(h, lp))
+        x = h.max(axis=2)
+        xyz.append(centers)
+    props = []
+    for k, lev in enumerate(wl.fp):
+        lvl = len(wl.sa) - 1 - k
+        idx, w = three_nn(xyz[lvl], xyz[lvl + 1])
+        h = np.concatenate([store(three_interpolate(x, idx, w)), skips[lvl]], axis=2)
+        for lp in lev.mlps:
+            h = store(shared_mlp(h, lp))
+        x = h
+        props.append(x)
+    for k, lp in enumerate(wl.head):
+        x = shared_mlp(x, lp)
+        if k + 1 < len(wl.head):
+            x = store(x)
+    if return_levels:
+        return x, dict(xyz=xyz, skips=skips, props=props)
+    return x

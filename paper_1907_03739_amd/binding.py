@@ -65,6 +65,7 @@ _SIGS = {
     "pvconv_ball_query": ([_VP, _I, _I, _VP, _I, _F, _I, _VP, _VP], _I),
     "pvconv_group_points": ([_VP, _VP, _I, _I, _I, _I, _I, _VP, _I, _VP, _I, _VP, _I, _I, _VP],
                             _I),
+    "pvconv_group_max": ([_VP, _I, _I, _I, _I, _I, _VP, _I, _I, _VP], _I),
     "pvconv_three_nn": ([_VP, _I, _I, _VP, _I, _VP, _VP, _VP], _I),
     "pvconv_three_interpolate": ([_VP, _I, _I, _I, _I, _I, _VP, _VP, _I, _VP, _I, _I, _VP], _I),
     "pvconv_conv3d_noalloc": ([_VP, _I, _I, _I, _I, _VP, _VP, _VP, _I, _F, _I, _VP, _I, _VP],
@@ -337,6 +338,23 @@ def pvconv_group_points(xyz: torch.Tensor, feats: Optional[torch.Tensor], center
         _p(xyz), _p(feats), _dt(feats) if feats is not None else F32, fld, B, N, C,
         _p(centers.contiguous()), M, _p(idx.contiguous()), S, _p(out), _dt(out), old,
         _stream(xyz)))
+    return out
+
+
+def pvconv_group_max(x: torch.Tensor, nsample: int, out: Optional[torch.Tensor] = None,
+                     out_dtype=torch.float32):
+    """x [G*nsample][C] (rows evenly strided) -> [G][C]: the maximum over each
+    group of nsample rows; out may be a column slice of a wider [G][*] tensor."""
+    rows, C = x.shape
+    if rows % nsample:
+        raise ValueError("rows must be a multiple of nsample")
+    G = rows // nsample
+    xld = _rows(x, rows, C)
+    if out is None:
+        out = torch.empty((G, C), dtype=_torch_dt(out_dtype), device=x.device)
+    old = _rows(out, G, C)
+    _check("pvconv_group_max", _lib.pvconv_group_max(_p(x), _dt(x), xld, G, nsample, C, _p(out),
+                                                     _dt(out), old, _stream(x)))
     return out
 
 

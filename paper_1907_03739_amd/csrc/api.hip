@@ -452,6 +452,25 @@ pvconv_status pvconv_group_points(const float* xyz, const void* feats, pvconv_dt
                            nsample, out, out_dt == PVCONV_BF16, out_ld, as_stream(stream));
 }
 
+pvconv_status pvconv_group_max(const void* x, pvconv_dtype dt, int x_ld, int G, int nsample,
+                               int C, void* out, pvconv_dtype out_dt, int out_ld, void* stream) {
+    if (G < 0 || nsample < 1 || C < 1 || C > PVCONV_MAX_MLP_CHANNELS ||
+        (long long)G * nsample > (1LL << 30))
+        return PVCONV_EINVAL;
+    if (!dtype_ok(dt) || !dtype_ok(out_dt)) return PVCONV_EINVAL;
+    if (x_ld == 0) x_ld = C;
+    if (out_ld == 0) out_ld = C;
+    if (x_ld < C || out_ld < C) return PVCONV_EINVAL;
+    if (G == 0) return PVCONV_OK;
+    if (!x || !out || ((uintptr_t)x & (esize(dt) - 1)) || ((uintptr_t)out & (esize(out_dt) - 1)))
+        return PVCONV_EINVAL;
+    if (bytes_overlap(out, (size_t)(((long long)G - 1) * out_ld + C) * esize(out_dt), x,
+                      (size_t)(((long long)G * nsample - 1) * x_ld + C) * esize(dt)))
+        return PVCONV_EINVAL;
+    return pv_launch_group_max(x, dt == PVCONV_BF16, x_ld, G, nsample, C, out,
+                               out_dt == PVCONV_BF16, out_ld, as_stream(stream));
+}
+
 pvconv_status pvconv_three_nn(const float* unknown, int B, int n, const float* known, int m,
                               int32_t* idx, float* weight, void* stream) {
     if (B < 0 || n < 0 || m < 3 || !sizes_fit(B, n) || !sizes_fit(B, m)) return PVCONV_EINVAL;

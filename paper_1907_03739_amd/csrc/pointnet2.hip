@@ -296,6 +296,36 @@ __global__ __launch_bounds__(256) void pv_three_interpolate_kernel(
     }
 }
 
+// ---------------------------------------------------------------------------
+// Maximum over each group's S rows (a centre's neighbours after the shared
+// MLP): out[g][c] = max_k x[g*S + k][c]. One thread per output element,
+// channels fastest; exact, so the order of the comparisons does not matter.
+// ---------------------------------------------------------------------------
+template <typename XT, typename OT>
+__global__ __launch_bounds__(256) void pv_group_max_kernel(const XT* __restrict__ x, int x_ld,
+                                                           int S, int C, OT* __restrict__ out,
+                                                           int out_ld, size_t total) {
+    for (size_t e = (size_t)blockIdx.x * 256 + threadIdx.x; e < total;
+         e += (size_t)gridDim.x * 256) {
+        const size_t g = e / C;
+        const int c = (int)(e - g * C);
+        const XT* r = x + g * S * (size_t)x_ld + c;
+        float m = -INFINITY;
+        for (int k = 0; k < S; k++) {
+            float v;
+            if constexpr (sizeof(XT) == 2)
+                v = pv_bf16_to_f32(r[(size_t)k * x_ld]);
+            else
+                v = r[(size_t)k * x_ld];
+            m = fmaxf(m, v);
+        }
+        if constexpr (sizeof(OT) == 2)
+            out[g * out_ld + c] = pv_f32_to_bf16(m);
+        else
+            out[g * out_ld + c] = m;
+    }
+}
+
 unsigned grid_for(size_t total) {
     const size_t blocks = (total + 255) / 256;
     return (unsigned)(blocks < 65536 ? blocks : 65536);
@@ -370,5 +400,20 @@ pvconv_status pv_launch_three_interpolate(const void* feats, bool feat_bf16, int
     else if (out_bf16) PV_INTERP(float, uint16_t);
     else PV_INTERP(float, float);
 #undef PV_INTERP
+    return pv_launch_status();
+}
+
+pvconv_status pv_launch_group_max(const void* x, bool x_bf16, int x_ld, int G, int S, int C,
+                                  void* out, bool out_bf16, int out_ld, hipStream_t s) {
+    const size_t total = (size_t)G * C;
+    if (total == 0) return PVCONV_OK;
+#define PV_GMAX(XT, OT)                                                                     \
+    hipLaunchKernelGGL((pv_group_max_kernel<XT, OT>), dim3(grid_for(total)), dim3(256), 0, s, \
+                       (const XT*)x, x_ld, S, C, (OT*)out, out_ld, total)
+    if (x_bf16 && out_bf16) PV_GMAX(uint16_t, uint16_t);
+    else if (x_bf16) PV_GMAX(uint16_t, float);
+    else if (out_bf16) PV_GMAX(float, uint16_t);
+    else PV_GMAX(float, float);
+#undef PV_GMAX
     return pv_launch_status();
 }

@@ -208,6 +208,8 @@ pvconv_status pv_launch_three_interpolate(const void* feats, bool feat_bf16, int
                                           int m, int C, const int32_t* idx, const float* weight,
                                           int n, void* out, bool out_bf16, int out_ld,
                                           hipStream_t s);
+pvconv_status pv_launch_group_max(const void* x, bool x_bf16, int x_ld, int G, int S, int C,
+                                  void* out, bool out_bf16, int out_ld, hipStream_t s);
 // backward (backward.hip)
 size_t pv_conv3d_bwd_data_ws_bytes(int Cin, int Cout, bool bf16);
 pvconv_status pv_launch_voxelize_backward(const void* dgrid, bool bf16, int B, int N, int C,

@@ -279,8 +279,70 @@ def draw_linear(rng, cin, cout, bf16, final=False) -> LinearParams:
     return LinearParams(w=w, b=None, bn=draw_bn(rng, cout), relu=True)
 
 
+@dataclasses.dataclass
+class SAParams:
+    """One set-abstraction level of PVCNN++: PVConv layers on the level's
+    points (possibly none), then npoint centres by farthest point sampling,
+    nsample neighbours within radius, a shared MLP on the grouped rows
+    (relative coordinates, then features) and the maximum over the
+    neighbours."""
+    pvconvs: List[PVConvParams]
+    npoint: int
+    radius: float
+    nsample: int
+    mlps: List[LinearParams]
+
+
+@dataclasses.dataclass
+class FPParams:
+    """One feature-propagation level: the coarser level's features
+    interpolated onto this level's points (three nearest neighbours),
+    concatenated with this level's features, then a shared MLP."""
+    mlps: List[LinearParams]
+
+
+def draw_pvcnn2(rng, cin, width=1.0):
+    """PVCNN++ for scene segmentation: PointNet++'s four set-abstraction and
+    four feature-propagation levels, with a PVConv layer (two convolutions)
+    on the points of each of the first three levels, then the head. Channel
+    counts scale by `width` (the compact models' channel multiplier).
+
+    Returns (sa levels, fp levels, head)."""
+    w = lambda c: max(1, int(round(c * width)))
+    sa_cfg = [  # npoint, radius (m), PVConv (cout, R) or None, MLP widths
+        (1024, 0.2, (32, 32), [32, 32, 64]),
+        (256, 0.4, (64, 16), [64, 64, 128]),
+        (64, 0.8, (128, 8), [128, 128, 256]),
+        (16, 1.6, None, [256, 256, 512]),
+    ]
+    sa, feat_widths, c = [], [], cin
+    for npoint, radius, pvc, mlp in sa_cfg:
+        pvconvs = []
+        if pvc:
+            pvconvs.append(draw_pvconv(rng, c, w(pvc[0]), pvc[1], 2, bf16=True))
+            c = w(pvc[0])
+        feat_widths.append(c)  # the level's features: the skip link of its FP level
+        layers, ci = [], 3 + c
+        for co in mlp:
+            layers.append(draw_linear(rng, ci, w(co), True))
+            ci = w(co)
+        sa.append(SAParams(pvconvs, npoint, radius, 32, layers))
+        c = ci
+    fp = []
+    for widths, skip in zip([[256, 256], [256, 256], [256, 128], [128, 128, 128]],
+                            reversed(feat_widths)):
+        layers, ci = [], c + skip
+        for co in widths:
+            layers.append(draw_linear(rng, ci, w(co), True))
+            ci = w(co)
+        fp.append(FPParams(layers))
+        c = ci
+    head = [draw_linear(rng, c, w(128), True), draw_linear(rng, w(128), 13, True, final=True)]
+    return sa, fp, head
+
+
 # ----------------------------------------------------------------------------
-# the five workloads
+# the workloads
 # ----------------------------------------------------------------------------
 @dataclasses.dataclass
 class Workload:
@@ -295,6 +357,12 @@ class Workload:
     mlps: List[LinearParams] = dataclasses.field(default_factory=list)   # point-only MLPs
     head: List[LinearParams] = dataclasses.field(default_factory=list)   # seg head
     n_classes: int = 0
+    sa: List[SAParams] = dataclasses.field(default_factory=list)         # PVCNN++ levels
+    fp: List[FPParams] = dataclasses.field(default_factory=list)
+
+    @property
+    def is_pvcnn2(self):
+        return bool(self.sa)
 
     @property
     def is_network(self):
@@ -310,6 +378,16 @@ class Workload:
             h.update(L.mlp_w.tobytes())
         for L in self.mlps + self.head:
             h.update(L.w.tobytes())
+        for lev in self.sa:
+            for L in lev.pvconvs:
+                for w in L.conv_w:
+                    h.update(w.tobytes())
+                h.update(L.mlp_w.tobytes())
+            for L in lev.mlps:
+                h.update(L.w.tobytes())
+        for lev in self.fp:
+            for L in lev.mlps:
+                h.update(L.w.tobytes())
         return h.hexdigest()
 
 
@@ -319,12 +397,13 @@ WORKLOAD_NAMES = {
     3: "pvcnn_partseg_bf16_B8_N2048",
     4: "pvcnn_sceneseg_bf16_B8_N4096",
     5: "pvconv_layer_bf16_B1_N65536_C64to64_R64_clustered",
+    6: "pvcnn2_sceneseg_bf16_B4_N8192",
 }
 
 
 def make_workload(index: int, seed: Optional[int] = None, B: Optional[int] = None,
                   N: Optional[int] = None) -> Workload:
-    """Build workload `index` (1..5) from seed 1000 + index unless given.
+    """Build workload `index` (1..6) from seed 1000 + index unless given.
 
     B and N may be overridden to make reduced-size variants of the same shape
     family (the parity tests use that to keep the oracle within seconds)."""
@@ -372,4 +451,12 @@ def make_workload(index: int, seed: Optional[int] = None, B: Optional[int] = Non
         feats = rng.normal(size=(B_, N_, 64)).astype(np.float32)
         layers = [draw_pvconv(rng, 64, 64, 64, 2, bf16=True)]
         return Workload(5, WORKLOAD_NAMES[5], B_, N_, "bf16", coords, feats, layers)
+    if index == 6:
+        # PVCNN++ on indoor scenes: 4 x 8192 points (the batch the paper times
+        # its scene-segmentation models on), 9 input channels, 13 classes
+        B_, N_ = B or 4, N or 8192
+        coords, feats = rooms(rng, B_, N_)
+        sa, fp, head = draw_pvcnn2(rng, 9)
+        return Workload(6, WORKLOAD_NAMES[6], B_, N_, "bf16", coords, feats, [], [], head, 13,
+                        sa, fp)
     raise ValueError(f"unknown workload {index}")

@@ -30,7 +30,7 @@ def declared_functions():
 
 def test_library_exports_every_declared_symbol():
     names = declared_functions()
-    assert len(names) == 30
+    assert len(names) == 31
     out = subprocess.run(["nm", "-D", "--defined-only", b.LIB_PATH], capture_output=True,
                          text=True, check=True).stdout
     exported = set(re.findall(r"\bT (pvconv_\w+)", out))
@@ -529,3 +529,15 @@ def test_three_interpolate_rejects(args, status):
     assert L.pvconv_three_interpolate(a["feats"], a["fdt"], a["fld"], a["B"], a["m"], a["C"],
                                       a["idx"], a["weight"], a["n"], a["out"], a["odt"],
                                       a["old"], None) == status
+
+
+@pytest.mark.parametrize("args,status", [
+    (dict(G=-1), EINVAL), (dict(S=0), EINVAL), (dict(C=0), EINVAL), (dict(xld=3), EINVAL),
+    (dict(old=3), EINVAL), (dict(dt=4), EINVAL), (dict(G=0), OK), (dict(x=None), EINVAL),
+    (dict(out=None), EINVAL), (dict(out=ctypes.c_void_p(0x100000 + 64)), EINVAL),
+])
+def test_group_max_rejects(args, status):
+    a = dict(x=FAKE, dt=1, xld=0, G=10, S=32, C=8, out=ctypes.c_void_p(0x400000), odt=1, old=0)
+    a.update(args)
+    assert L.pvconv_group_max(a["x"], a["dt"], a["xld"], a["G"], a["S"], a["C"], a["out"],
+                              a["odt"], a["old"], None) == status

@@ -138,3 +138,68 @@ def test_network_rejects_a_head_of_the_wrong_width():
     bad[0] = synth.LinearParams(w=wl.head[0].w[:, :100], b=None, bn=wl.head[0].bn, relu=True)
     with pytest.raises(ValueError):
         DeviceNetwork(wl.layers, wl.mlps, bad, wl.B, wl.N)
+
+
+# ----------------------------------------------------------------------------
+# PVCNN++ (Section 5.2 "Models": PointNet++ extended with PVConv)
+# ----------------------------------------------------------------------------
+def _pvcnn2_stages(wl):
+    """bf16-stored stages on the longest path: PVConv layers, grouped rows
+    and MLP layers of the set abstraction, interpolations and MLP layers of
+    the feature propagation, the hidden head layer."""
+    s = sum(len(lev.pvconvs) + 1 + len(lev.mlps) for lev in wl.sa)
+    s += sum(1 + len(lev.mlps) for lev in wl.fp)
+    return s + len(wl.head) - 1
+
+
+def test_pvcnn2_full_size_two_clouds():
+    from paper_1907_03739_amd.network import DevicePVCNN2
+    wl = synth.make_workload(6)
+    net = DevicePVCNN2(wl.sa, wl.fp, wl.head, wl.B, wl.N, wl.feats.shape[2])
+    logits = host(net.forward(dev(wl.coords), dev(wl.feats)))
+    S = _pvcnn2_stages(wl)
+    for b in (0, wl.B - 1):
+        one = synth.make_workload(6)
+        one.B, one.coords, one.feats = 1, wl.coords[b:b + 1], wl.feats[b:b + 1]
+        ref, lv = oracle.pvcnn2_forward(one, "bf16", return_levels=True)
+        # the sampled points of every level: the same choices, bit for bit
+        for l in range(1, len(lv["xyz"])):
+            np.testing.assert_array_equal(net.xyz[l][b].cpu().numpy(), lv["xyz"][l][0])
+        # level-0 features after the last propagation, then the logits
+        got0 = host(net.props[0][b:b + 1])
+        ref0 = lv["props"][-1]
+        for got, want, what in ((got0, ref0, "features"), (logits[b:b + 1], ref, "logits")):
+            d = np.abs(got - want)
+            rms = float(np.sqrt(np.mean(want ** 2)))
+            ratio = float(np.max(d / (np.abs(want) + rms)))
+            print(f"[pvcnn2 cloud {b} {what}] max |d|/(|ref|+rms) = {ratio:.3g} (S = {S})",
+                  flush=True)
+            assert ratio <= 2e-2 * np.sqrt(S), f"cloud {b} {what}: {ratio:.3g}"
+
+
+def test_pvcnn2_indices_of_every_level():
+    from paper_1907_03739_amd.network import DevicePVCNN2
+    wl = synth.make_workload(6, B=2, N=4096)
+    net = DevicePVCNN2(wl.sa, wl.fp, wl.head, wl.B, wl.N, wl.feats.shape[2])
+    net.forward(dev(wl.coords), dev(wl.feats))
+    torch.cuda.synchronize()
+    xyz = wl.coords
+    for l, lev in enumerate(wl.sa):
+        idx = oracle.fps(xyz, lev.npoint)
+        np.testing.assert_array_equal(net.fps_idx[l].cpu().numpy(), idx)
+        centers = oracle.gather_points(xyz, idx)
+        np.testing.assert_array_equal(net.ball[l].cpu().numpy(),
+                                      oracle.ball_query(xyz, centers, lev.radius, lev.nsample))
+        nn_i, _ = oracle.three_nn(xyz, centers)
+        np.testing.assert_array_equal(net.nn_idx[l].cpu().numpy(), nn_i)
+        xyz = centers
+
+
+def test_pvcnn2_forward_is_repeatable():
+    from paper_1907_03739_amd.network import DevicePVCNN2
+    wl = synth.make_workload(6, B=2, N=2048)
+    net = DevicePVCNN2(wl.sa, wl.fp, wl.head, wl.B, wl.N, wl.feats.shape[2])
+    c, f = dev(wl.coords), dev(wl.feats)
+    a = net.forward(c, f).clone()
+    b = net.forward(c, f)
+    assert torch.equal(a, b)

@@ -826,3 +826,30 @@ def test_three_interpolate_is_linear_and_keeps_constants():
     for i in range(70):
         for k in range(3):
             assert out[0, i, idx[0, i, k]] == pytest.approx(w[0, i, k], rel=1e-12)
+
+
+def test_pvcnn2_concat_puts_the_interpolation_first_and_stores_bf16():
+    import copy
+    wl = synth.make_workload(6, B=1, N=2048)
+    out16, lv = oracle.pvcnn2_forward(wl, "bf16", return_levels=True)
+    for s in lv["skips"] + lv["props"]:
+        np.testing.assert_array_equal(oracle.round_bf16(s), s)
+    out64 = oracle.pvcnn2_forward(wl)
+    rms = np.sqrt(np.mean(out64 ** 2))
+    assert 0.0 < np.max(np.abs(out16 - out64)) < 0.1 * rms
+    # the last propagation level's first layer sees [interpolated | skip]:
+    # with zero weights on the interpolated columns, the coarse levels (here
+    # perturbed through the deepest MLP's weights) no longer matter
+    wl2 = copy.deepcopy(wl)
+    lp = wl2.fp[-1].mlps[0]
+    c_interp = lp.w.shape[1] - lv["skips"][0].shape[2]
+    lp.w[:, :c_interp] = 0.0
+    a = oracle.pvcnn2_forward(wl2)
+    wl2.sa[-1].mlps[-1].w *= 3.0
+    np.testing.assert_array_equal(oracle.pvcnn2_forward(wl2), a)
+    # ... while with the skip columns zeroed instead, they do
+    wl3 = copy.deepcopy(wl)
+    wl3.fp[-1].mlps[0].w[:, c_interp:] = 0.0
+    b3 = oracle.pvcnn2_forward(wl3)
+    wl3.sa[-1].mlps[-1].w *= 3.0
+    assert np.max(np.abs(oracle.pvcnn2_forward(wl3) - b3)) > 0.0
