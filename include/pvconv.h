@@ -304,8 +304,9 @@ pvconv_status pvconv_maxpool(const void* x, pvconv_dtype dt, int x_ld, int B, in
 /* takes the maximum over the neighbours (pvconv_maxpool); feature           */
 /* propagation interpolates features back to the denser level from the three */
 /* nearest neighbours. Every choice of an index compares fp32 squared        */
-/* distances (dx*dx + dy*dy) + dz*dz, dx = x_j - x_c, without contraction,   */
-/* with ties to the lower index, so results are the same on every run.       */
+/* distances fma(dz, dz, fma(dy, dy, dx*dx)), dx = x_j - x_c (each fused     */
+/* multiply-add rounded once), with ties to the lower index, so results are  */
+/* the same on every run.                                                    */
 /* Coordinates are [B][*][3] fp32; indices are within the cloud.             */
 /* ========================================================================= */
 

@@ -356,7 +356,7 @@ def maxpool(x: np.ndarray) -> np.ndarray:
 # PointNet++ primitives of PVCNN++ (Section 5.2 "Models": PointNet++ extended
 # with PVConv), as PointNet++ defines them. The choices of an index (farthest
 # point, ball membership, nearest neighbours) compare fp32 squared distances
-# formed as the kernels form them.
+# formed as the kernels form them: fma(dz, dz, fma(dy, dy, dx * dx)).
 # ----------------------------------------------------------------------------
 def _f32(a) -> np.ndarray:
     return np.ascontiguousarray(a, dtype=np.float32)

@@ -57,8 +57,9 @@
  * (built with -ffp-contract=off), except where a floating-point comparison
  * decides an index (the farthest point, ball membership, the three nearest
  * neighbours): there the squared distance is computed in fp32 as
- * (dx*dx + dy*dy) + dz*dz with dx = x_j - x_c, the precision and order the GPU
- * kernels use, so that both sides make the same choices.
+ * fma(dz, dz, fma(dy, dy, dx*dx)) with dx = x_j - x_c (fmaf rounds once), the
+ * precision and order the GPU kernels use, so that both sides make the same
+ * choices.
  */
 #include <math.h>
 #include <stdint.h>
@@ -523,15 +524,12 @@ int ref_conv3d_backward_weight(const double* dy, const double* x, int64_t B, int
 /* ------------------------------------------------------------------------- */
 
 /* Squared distance between two points of fp32 coordinates, in fp32, in the
- * order the kernels use. */
+ * form the kernels use: fused multiply-adds, each rounded once. */
 static float sqdist_f32(const float* a, const float* b) {
     const float dx = a[0] - b[0];
     const float dy = a[1] - b[1];
     const float dz = a[2] - b[2];
-    const float xx = dx * dx;
-    const float yy = dy * dy;
-    const float zz = dz * dz;
-    return (xx + yy) + zz;
+    return fmaf(dz, dz, fmaf(dy, dy, dx * dx));
 }
 
 /* Iterative farthest point sampling. The first sample is point 0; each next

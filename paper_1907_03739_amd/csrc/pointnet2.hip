@@ -6,9 +6,9 @@
 //
 // Every choice of an index (the farthest point, ball membership, the three
 // nearest neighbours) compares fp32 squared distances formed as
-// (dx*dx + dy*dy) + dz*dz, dx = x_j - x_c, without contraction, with ties
-// going to the lower index: the same choices on every run and in every
-// launch configuration.
+// fma(dz, dz, fma(dy, dy, dx * dx)), dx = x_j - x_c, with ties going to the
+// lower index: the same choices on every run and in every launch
+// configuration.
 #include "pv_common.h"
 #include "pv_wave.h"
 
@@ -18,34 +18,41 @@ __device__ __forceinline__ float sqdist(float ax, float ay, float az, float bx, 
                                         float bz) {
 #pragma clang fp contract(off)
     const float dx = ax - bx, dy = ay - by, dz = az - bz;
-    const float xx = dx * dx, yy = dy * dy, zz = dz * dz;
-    return (xx + yy) + zz;
+    return __builtin_fmaf(dz, dz, __builtin_fmaf(dy, dy, dx * dx));
 }
 
-struct MaxU64 {
-    __device__ uint64_t operator()(uint64_t a, uint64_t b) const { return a > b ? a : b; }
+struct MaxU32 {
+    __device__ uint32_t operator()(uint32_t a, uint32_t b) const { return a > b ? a : b; }
 };
 
 // ---------------------------------------------------------------------------
 // Farthest point sampling, one workgroup of NT threads per cloud. Thread t
 // keeps points t, t + NT, ... (PPT of them) and their distance to the samples
 // taken so far in registers. Each step: update those distances with the last
-// sample, take the thread's farthest point, then the wave's (a maximum over
-// the 64-bit key (distance bits << 32) | ~index: the larger distance, the
-// lower index among equals; distances are >= 0, so their bits order as their
-// values), then the workgroup's through one LDS slot per wave. The winner's
-// coordinates travel with its key, so nothing is read back from memory. The
-// slots alternate between two buffers so that one barrier per step suffices:
-// step s+2 writes the buffer step s read only after every wave has passed the
-// barrier of step s+1, which follows those reads.
+// sample and take the thread's farthest point (the lowest index among equals:
+// the thread's points come in index order and only a strictly larger distance
+// replaces); then the wave's: the maximum distance over the wave, the lanes
+// holding it by ballot, and among several such lanes the lowest index (rare:
+// a second reduction over the indices); then the workgroup's through one LDS
+// slot per wave. TAB (clouds of up to kFpsTab points): the cloud's
+// coordinates sit in an LDS table, and the winner's are read from it by
+// index; otherwise each thread also carries its farthest point's coordinates
+// and the winning lane writes them to its slot. The slots alternate between
+// two buffers so that one barrier per step suffices: step s+2 writes the
+// buffer step s read only after every wave has passed the barrier of step
+// s+1, which follows those reads.
 // ---------------------------------------------------------------------------
-template <int PPT, int NT>
+constexpr int kFpsTab = 8192;
+
+template <int PPT, int NT, bool TAB>
 __global__ __launch_bounds__(NT) void pv_fps_kernel(const float* __restrict__ xyz, int N,
                                                     int npoint, int32_t* __restrict__ idx,
                                                     float* __restrict__ new_xyz) {
     constexpr int NW = NT / 64;
-    __shared__ uint64_t s_key[2][NW];
+    __shared__ float s_d[2][NW];
+    __shared__ int s_j[2][NW];
     __shared__ float s_pt[2][NW][4];
+    __shared__ float s_tab[TAB ? 3 * kFpsTab : 1];
     const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const float* p = xyz + (size_t)b * N * 3;
     float px[PPT], py[PPT], pz[PPT], dmin[PPT];
@@ -58,6 +65,11 @@ __global__ __launch_bounds__(NT) void pv_fps_kernel(const float* __restrict__ xy
         py[k] = q[1];
         pz[k] = q[2];
         dmin[k] = ok ? INFINITY : -1.f;  // -1: never the farthest
+        if (TAB && ok) {  // the table is only read for TAB
+            s_tab[j] = px[k];
+            s_tab[kFpsTab + j] = py[k];
+            s_tab[2 * kFpsTab + j] = pz[k];
+        }
     }
     float lx = p[0], ly = p[1], lz = p[2];
     int32_t* out = idx + (size_t)b * npoint;
@@ -70,6 +82,7 @@ __global__ __launch_bounds__(NT) void pv_fps_kernel(const float* __restrict__ xy
             oxyz[2] = lz;
         }
     }
+    if (TAB) pv_lds_barrier();
     for (int s = 1; s < npoint; s++) {
         float bestd = -1.f, bx = 0.f, by = 0.f, bz = 0.f;
         int bestj = 0;
@@ -79,39 +92,66 @@ __global__ __launch_bounds__(NT) void pv_fps_kernel(const float* __restrict__ xy
             const bool better = dmin[k] > bestd;  // strict: the lower index stays
             bestd = better ? dmin[k] : bestd;
             bestj = better ? tid + k * NT : bestj;
-            bx = better ? px[k] : bx;
-            by = better ? py[k] : by;
-            bz = better ? pz[k] : bz;
+            if constexpr (!TAB) {
+                bx = better ? px[k] : bx;
+                by = better ? py[k] : by;
+                bz = better ? pz[k] : bz;
+            }
         }
-        const uint64_t key = bestd >= 0.f ? ((uint64_t)__float_as_uint(bestd) << 32) |
-                                                (uint64_t)(0xffffffffu - (uint32_t)bestj)
-                                          : 0ull;
-        const uint64_t wkey = wave_reduce(key, MaxU64{});
+        // the wave's farthest point: a maximum over the distances' bits
+        // (distances are >= 0, so their bits order as their values), offset
+        // by one so that 0 means "no point" (the reduction fills lanes it
+        // leaves out with 0); then the lanes holding it by ballot
+        const uint32_t key = bestd >= 0.f ? __float_as_uint(bestd) + 1u : 0u;
+        const uint32_t wkey = wave_reduce(key, MaxU32{});
+        const uint64_t hold = __ballot(key != 0u && key == wkey);
+        int wj = 0x7fffffff;
+        float wd = -1.f;
+        if (hold != 0ull) {
+            wd = __uint_as_float(wkey - 1u);
+            if ((hold & (hold - 1ull)) == 0ull) {  // one lane
+                wj = __builtin_amdgcn_readlane(bestj, __ffsll((long long)hold) - 1);
+            } else {  // equal distances in several lanes: the lowest index
+                const uint32_t jk = (hold >> lane) & 1ull ? 0xffffffffu - (uint32_t)bestj : 0u;
+                wj = (int)(0xffffffffu - wave_reduce(jk, MaxU32{}));
+            }
+        }
         const int buf = s & 1;
-        if (wkey == 0ull) {
-            if (lane == 0) s_key[buf][w] = 0ull;
-        } else if (key == wkey) {  // exactly one lane: indices are distinct
-            s_key[buf][w] = key;
-            s_pt[buf][w][0] = bx;
-            s_pt[buf][w][1] = by;
-            s_pt[buf][w][2] = bz;
+        if (lane == 0) {
+            s_d[buf][w] = wd;
+            s_j[buf][w] = wj;
+        }
+        if constexpr (!TAB) {
+            if (bestj == wj && wd >= 0.f) {  // the one lane that holds it
+                s_pt[buf][w][0] = bx;
+                s_pt[buf][w][1] = by;
+                s_pt[buf][w][2] = bz;
+            }
         }
         pv_lds_barrier();
-        uint64_t best = s_key[buf][0];
-        int bw = 0;
+        float best = s_d[buf][0];
+        int bj = s_j[buf][0], bw = 0;
 #pragma unroll
         for (int i = 1; i < NW; i++) {
-            const uint64_t k2 = s_key[buf][i];
-            if (k2 > best) {
-                best = k2;
+            const float d = s_d[buf][i];
+            const int j = s_j[buf][i];
+            if (d > best || (d == best && j < bj)) {
+                best = d;
+                bj = j;
                 bw = i;
             }
         }
-        lx = s_pt[buf][bw][0];
-        ly = s_pt[buf][bw][1];
-        lz = s_pt[buf][bw][2];
+        if constexpr (TAB) {
+            lx = s_tab[bj];
+            ly = s_tab[kFpsTab + bj];
+            lz = s_tab[2 * kFpsTab + bj];
+        } else {
+            lx = s_pt[buf][bw][0];
+            ly = s_pt[buf][bw][1];
+            lz = s_pt[buf][bw][2];
+        }
         if (tid == 0) {
-            out[s] = (int32_t)(0xffffffffu - (uint32_t)best);
+            out[s] = bj;
             if (oxyz) {
                 oxyz[(size_t)s * 3] = lx;
                 oxyz[(size_t)s * 3 + 1] = ly;
@@ -336,14 +376,17 @@ unsigned grid_for(size_t total) {
 pvconv_status pv_launch_fps(const float* xyz, int B, int N, int npoint, int32_t* idx,
                             float* new_xyz, hipStream_t s) {
     if (B == 0) return PVCONV_OK;
-#define PV_FPS(PPT, NT) \
-    hipLaunchKernelGGL((pv_fps_kernel<PPT, NT>), dim3(B), dim3(NT), 0, s, xyz, N, npoint, idx, new_xyz)
-    if (N <= 64) PV_FPS(1, 64);
-    else if (N <= 256) PV_FPS(1, 256);
-    else if (N <= 1024) PV_FPS(4, 256);
-    else if (N <= 4096) PV_FPS(8, 512);
-    else if (N <= 8192) PV_FPS(8, 1024);
-    else if (N <= kPvFpsMaxN) PV_FPS(16, 1024);
+    // four waves (one per SIMD), so that each step's wave reductions are
+    // paid four times, not sixteen; the clouds' points in registers
+#define PV_FPS(PPT, NT, TAB)                                                              \
+    hipLaunchKernelGGL((pv_fps_kernel<PPT, NT, TAB>), dim3(B), dim3(NT), 0, s, xyz, N, npoint, \
+                       idx, new_xyz)
+    if (N <= 256) PV_FPS(4, 64, true);
+    else if (N <= 1024) PV_FPS(4, 256, true);
+    else if (N <= 2048) PV_FPS(8, 256, true);
+    else if (N <= 4096) PV_FPS(16, 256, true);
+    else if (N <= kFpsTab) PV_FPS(32, 256, true);
+    else if (N <= kPvFpsMaxN) PV_FPS(16, 1024, false);
     else return PVCONV_ENOTSUP;
 #undef PV_FPS
     return pv_launch_status();
