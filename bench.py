@@ -427,8 +427,8 @@ def bench_network(args, wl, dev, peaks=True, cpu_seconds=None):
 # Layer variants on the default workload's clouds (16 x 2048 points): the
 # resolution sweep of the resolution table (R = 16, 24, 32), the number of
 # convolutions per PVConv of the ablation table (1, 2, 3), narrower layers
-# (the width multipliers of the scene-segmentation table; bf16 MFMA needs
-# C_out % 32 == 0, so 0.25 x (64 -> 128) is the narrowest) and the
+# (the width multipliers of the scene-segmentation table, down to 0.125 x C:
+# 8 -> 16 channels, a convolution tile half of zero weights) and the
 # nearest-neighbour devoxelisation the ablation compares with trilinear.
 VARIANTS = [
     # name, R, n_convs, width, devox
@@ -439,8 +439,10 @@ VARIANTS = [
     ("convs3", 32, 3, 1.0, "trilinear"),
     ("width0.5", 32, 2, 0.5, "trilinear"),
     ("width0.25", 32, 2, 0.25, "trilinear"),
+    ("width0.125", 32, 2, 0.125, "trilinear"),
     ("nearest", 32, 2, 1.0, "nearest"),
     ("R16_width0.25", 16, 2, 0.25, "trilinear"),
+    ("R16_width0.125", 16, 2, 0.125, "trilinear"),
 ]
 
 

@@ -143,7 +143,9 @@ pvconv_status pvconv_voxelize_from_ids(const int32_t* vox_id, const void* feats,
 /*  bias    [Cout] fp32 or NULL; bn may be NULL                              */
 /*  act     NONE / RELU / LEAKY (negative slope `slope`)                     */
 /*  y       out [B][R^3][Cout], dtype out_dt                                 */
-/* dt = BF16: MFMA implicit GEMM, bf16 x bf16 -> fp32; needs Cout % 32 == 0. */
+/* dt = BF16: MFMA implicit GEMM, bf16 x bf16 -> fp32, output channels in   */
+/* tiles of 32 (a Cout that is no multiple of 32 pads its last tile with     */
+/* zero weights; only the Cout channels are stored).                         */
 /* It first repacks the weights into the MFMA fragment order inside          */
 /* `workspace` (>= pvconv_conv3d_workspace_size bytes, 256-byte aligned;     */
 /* contents on entry ignored). dt = F32: fp32 FMA, no workspace (may be      */
@@ -161,8 +163,7 @@ pvconv_status pvconv_conv3d(const void* x, int B, int R, int Cin, int Cout, cons
 /* fragment order, then any number of convolutions on the packed copy.       */
 /* pvconv_conv3d(...) equals pvconv_conv3d_pack_weights then                */
 /* pvconv_conv3d_packed on the same stream, bit for bit.                     */
-/*  weight  [Cout][3][3][3][Cin] bf16 (the MFMA path: Cout % 32 == 0, else   */
-/*          PVCONV_ENOTSUP)                                                  */
+/*  weight  [Cout][3][3][3][Cin] bf16 (the MFMA path)                        */
 /*  packed  out: >= pvconv_conv3d_workspace_size(Cin, Cout, PVCONV_BF16)     */
 /*          bytes, 256-byte aligned, owned by the caller; every byte of that */
 /*          size is written. Its layout is internal to the library.          */

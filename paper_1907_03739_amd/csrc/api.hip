@@ -130,7 +130,6 @@ pvconv_status check_conv3d(const void* x, int B, int R, int Cin, int Cout, const
     if (((uintptr_t)x & (esize(dt) - 1)) || ((uintptr_t)weight & (esize(dt) - 1)) ||
         ((uintptr_t)y & (esize(out_dt) - 1)) || ((uintptr_t)bias & 3))
         return PVCONV_EINVAL;
-    if (dt == PVCONV_BF16 && Cout % 32 != 0) return PVCONV_ENOTSUP;
     // every input voxel is read by up to 27 workgroups while others store
     if (overlap(x, (long long)B * R * R * R, Cin, Cin, dt, y, Cout, Cout, out_dt))
         return PVCONV_EINVAL;
@@ -144,7 +143,6 @@ pvconv_status check_layer(const pvconv_layer* L) {
         L->n_convs < 1 || L->n_convs > PVCONV_MAX_CONVS)
         return PVCONV_EINVAL;
     if (!dtype_ok(L->compute_dt)) return PVCONV_EINVAL;
-    if (L->compute_dt == PVCONV_BF16 && L->cout % 32 != 0) return PVCONV_ENOTSUP;
     for (int i = 0; i < L->n_convs; i++)
         if (!L->conv_w[i] || !bn_ok(&L->conv_bn[i])) return PVCONV_EINVAL;
     if (!L->mlp_w || !bn_ok(&L->mlp_bn)) return PVCONV_EINVAL;
@@ -245,7 +243,6 @@ pvconv_status pvconv_conv3d_pack_weights(const void* weight, int Cin, int Cout, 
                                          size_t packed_bytes, void* stream) {
     if (Cin < 1 || Cout < 1 || Cin > PVCONV_MAX_CONV_CHANNELS || Cout > PVCONV_MAX_CONV_CHANNELS)
         return PVCONV_EINVAL;
-    if (Cout % 32 != 0) return PVCONV_ENOTSUP;
     if (!weight || ((uintptr_t)weight & 1)) return PVCONV_EINVAL;
     const size_t need = pv_conv3d_ws_bytes(Cin, Cout, true);
     if (!packed || ((uintptr_t)packed & 255) || packed_bytes < need) return PVCONV_EWORKSPACE;

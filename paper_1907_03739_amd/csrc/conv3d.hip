@@ -128,7 +128,7 @@ __global__ __launch_bounds__(256 * WCH, SB ? 2 : 1) void pv_conv3d_bf16_kernel(
     constexpr int NTH = 256 * WCH, NBW = NB / WCH;
     constexpr int kSets = (kPieces + NTH - 1) / NTH;  // halo pieces per thread
     const int wv = wave / WCH, wc = wave % WCH;
-    const int ntiles = Cout / NT;
+    const int ntiles = (Cout + NT - 1) / NT;  // the last tile may be partly past Cout
     const int nt = bid % ntiles;
     bid /= ntiles;
     const int bw = bid % nbr;
@@ -194,8 +194,9 @@ __global__ __launch_bounds__(256 * WCH, SB ? 2 : 1) void pv_conv3d_bf16_kernel(
     };
 
     // Packed weights: for chunk c, tap t and 32-channel output group g the 64
-    // lanes' fragments are 1 KB at ((c*27 + t)*G + g)*1024.
-    const int G = Cout / 32;
+    // lanes' fragments are 1 KB at ((c*27 + t)*G + g)*1024 (output channels
+    // past Cout packed as zeros).
+    const int G = (Cout + 31) / 32;
     const __amdgpu_buffer_rsrc_t wr = make_rsrc(wpk, (uint32_t)((size_t)nch * kTaps * G * 1024));
     const int wlane = lane * 16;
     auto load_w = [&](int c, int tap, pv_bf16x8 (&wf)[NBW]) {
@@ -214,9 +215,9 @@ __global__ __launch_bounds__(256 * WCH, SB ? 2 : 1) void pv_conv3d_bf16_kernel(
 #pragma unroll
             for (int e = 0; e < 16; e++) acc[i][j][e] = 0.f;
 
-    if (tid < NT) {
+    if (tid < NT) {  // channels past Cout take the last one's (never stored)
         float sc, sh;
-        pv_bn_coeffs(bn, n0 + tid, sc, sh);
+        pv_bn_coeffs(bn, min(n0 + tid, Cout - 1), sc, sh);
         bn_tab[0][tid] = sc;
         bn_tab[1][tid] = sh;
     }
@@ -325,9 +326,15 @@ __global__ __launch_bounds__(256 * WCH, SB ? 2 : 1) void pv_conv3d_bf16_kernel(
                 }
             }
             pv_lds_barrier();
-            // copy out: piece k of voxel vox (k < pieces)
+            // copy out: piece k of voxel vox (k < pieces); a pass partly past
+            // Cout copies its first ncols channels (whole pieces, then the
+            // elements of a last partial one)
             const size_t col = ((size_t)n0 + pass * PW) * esz;
-            if (vec_out && u0 + kBrick <= R && v0 + kBrick <= R && w0 + kBrick <= R) {
+            const int ncols = min(PW, Cout - n0 - pass * PW);
+            if (ncols <= 0) continue;  // uniform: the whole pass lies past Cout
+            const int vbytes = ncols * esz;
+            if (ncols == PW && vec_out && u0 + kBrick <= R && v0 + kBrick <= R &&
+                w0 + kBrick <= R) {
                 // the whole brick inside the grid: batches of UC pieces per
                 // thread, every LDS read of a batch issued before its stores
                 constexpr int kIt = 512 * pieces / NTH, UC = kIt < 4 ? kIt : 4;
@@ -355,14 +362,15 @@ __global__ __launch_bounds__(256 * WCH, SB ? 2 : 1) void pv_conv3d_bf16_kernel(
             for (int i = tid; i < 512 * pieces; i += NTH) {
                 const int vox = i / pieces, k = i % pieces;
                 const int u = u0 + (vox >> 6), v = v0 + ((vox >> 3) & 7), ww = w0 + (vox & 7);
-                if (u >= R || v >= R || ww >= R) continue;
+                if (u >= R || v >= R || ww >= R || k * 16 >= vbytes) continue;
                 const uint4 val = *(const uint4*)(lds + vox * kRow + k * 16);
                 char* dst = (char*)y + (cloud + ((size_t)u * R + v) * R + ww) * yrow + col + k * 16;
-                if (vec_out) {
+                const int nel = min(16, vbytes - k * 16) / esz;  // elements of this piece
+                if (vec_out && nel * esz == 16) {
                     *(uint4*)dst = val;
                 } else {
                     const uint32_t q[4] = {val.x, val.y, val.z, val.w};
-                    for (int e = 0; e < 16 / esz; e++) {
+                    for (int e = 0; e < nel; e++) {
                         if constexpr (OBF)
                             ((uint16_t*)dst)[e] = (uint16_t)(q[e >> 1] >> ((e & 1) * 16));
                         else
@@ -382,7 +390,8 @@ __global__ __launch_bounds__(256 * WCH, SB ? 2 : 1) void pv_conv3d_bf16_kernel(
 // Repack bf16 weights [Cout][27][Cin] into the fragment order the MFMA conv
 // reads: 16-byte element ((c*27 + t)*G + g)*64 + lane holds the 8 channels
 // k = c*16 + (lane/32)*8 .. +7 of output channel g*32 + lane%32 at tap t
-// (zero past Cin), G = Cout/32. One thread per element; one launch packs the
+// (zero past Cin and past Cout), G = ceil(Cout/32). One thread per element;
+// one launch packs the
 // weights of all the convolutions of a layer (the blocks of job q follow those of
 // jobs 0 .. q-1).
 static_assert(kKC == kPvPackKC && kTaps == kPvPackTaps, "the packing matches the kernel");
@@ -448,8 +457,9 @@ void launch_bf16(const void* x, int B, int R, int Cin, int Cout, const void* w,
                  const PvBnFold& bn, int act, float slope, void* y, bool out_bf16, bool vec,
                  hipStream_t s) {
     const int nbr = (R + kBrick - 1) / kBrick;
-    const size_t blocks = (size_t)B * nbr * nbr * nbr * (Cout / (NB * 32));
-    const bool vec_out = pv_aligned16(y);
+    const size_t blocks = (size_t)B * nbr * nbr * nbr * ((Cout + NB * 32 - 1) / (NB * 32));
+    // 16-byte stores: aligned output with rows of whole 16-byte pieces
+    const bool vec_out = pv_aligned16(y) && ((size_t)Cout * (out_bf16 ? 2 : 4)) % 16 == 0;
     if (vec)
         hipLaunchKernelGGL((pv_conv3d_bf16_kernel<NB, WCH, true, SB>), dim3((unsigned)blocks),
                            dim3(256 * WCH), 0, s, (const uint16_t*)x, (const uint16_t*)w, bn,
@@ -467,7 +477,7 @@ void launch_bf16(const void* x, int B, int R, int Cin, int Cout, const void* w,
 size_t pv_conv3d_ws_bytes(int Cin, int Cout, bool bf16) {
     if (!bf16) return 0;
     const size_t nch = (size_t)(Cin + kKC - 1) / kKC;
-    return nch * kKC * kTaps * (size_t)Cout * 2;
+    return nch * kKC * kTaps * (size_t)((Cout + 31) / 32 * 32) * 2;  // Cout padded to 32
 }
 
 void pv_pack_job(PvPackJobs& jobs, const void* w, int Cin, int Cout, void* packed) {

@@ -138,7 +138,7 @@ __device__ __forceinline__ void pv_pack_role(const PvPackJobs& jobs, int blk,
     const PvPackJob& J = jobs.job[q];
     const int i = blk * 256 + tid;
     if (i >= J.total) return;
-    const int G = J.Cout / 32;
+    const int G = (J.Cout + 31) / 32;  // output channels padded to 32 with zeros
     const int lane = i & 63;
     int r = i >> 6;
     const int g = r % G;
@@ -147,6 +147,10 @@ __device__ __forceinline__ void pv_pack_role(const PvPackJobs& jobs, int blk,
     const int c = r / kPvPackTaps;
     const int n = g * 32 + (lane & 31);
     const int k = c * kPvPackKC + (lane >> 5) * 8;
+    if (n >= J.Cout) {
+        J.packed[i] = make_uint4(0u, 0u, 0u, 0u);
+        return;
+    }
     const uint16_t* src = J.w + ((size_t)n * kPvPackTaps + t) * J.Cin;
     if (J.vec) {  // Cin % 8 == 0 and 16-byte aligned rows: one load
         J.packed[i] = k < J.Cin ? *(const uint4*)(src + k) : make_uint4(0u, 0u, 0u, 0u);

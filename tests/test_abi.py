@@ -45,9 +45,12 @@ def test_status_strings():
 
 
 def test_conv_workspace_query():
-    # bf16: the packed weights, channels padded to 16; fp32 needs none
+    # bf16: the packed weights, input channels padded to 16 and output
+    # channels to 32; fp32 needs none
     assert L.pvconv_conv3d_workspace_size(128, 128, 1) == 128 * 27 * 128 * 2
     assert L.pvconv_conv3d_workspace_size(3, 64, 1) == 64 * 27 * 16 * 2
+    assert L.pvconv_conv3d_workspace_size(8, 16, 1) == 32 * 27 * 16 * 2
+    assert L.pvconv_conv3d_workspace_size(64, 40, 1) == 64 * 27 * 64 * 2
     assert L.pvconv_conv3d_workspace_size(16, 32, 0) == 0
     assert L.pvconv_conv3d_workspace_size(0, 32, 1) == 0
 
@@ -102,8 +105,11 @@ def _conv(**kw):
     (dict(B=-1), EINVAL), (dict(R=0), EINVAL), (dict(R=200), EINVAL), (dict(Cin=0), EINVAL),
     (dict(Cout=2000), EINVAL), (dict(act=5), EINVAL), (dict(dt=3), EINVAL), (dict(x=None), EINVAL),
     (dict(w=None), EINVAL), (dict(y=None), EINVAL), (dict(x=FAKE_ODD), EINVAL),
-    (dict(y=FAKE), EINVAL), (dict(Cout=48), ENOTSUP), (dict(B=0), OK),
+    (dict(y=FAKE), EINVAL), (dict(B=0), OK),
     (dict(ws=None), EWS), (dict(wsb=100), EWS), (dict(ws=ctypes.c_void_p(0x400010)), EWS),
+    # 48 output channels (two 32-channel tiles, the second half zeros): the
+    # workspace is that of 64
+    (dict(Cout=48, wsb=16 * 27 * 48 * 2), EWS),
 ])
 def test_conv3d_rejects(kw, status):
     assert _conv(**kw) == status
@@ -127,7 +133,7 @@ def _conv_na(**kw):
 @pytest.mark.parametrize("kw,status", [
     (dict(B=-1), EINVAL), (dict(R=0), EINVAL), (dict(Cin=0), EINVAL), (dict(Cout=2000), EINVAL),
     (dict(act=5), EINVAL), (dict(x=None), EINVAL), (dict(w=None), EINVAL),
-    (dict(y=None), EINVAL), (dict(y=FAKE), EINVAL), (dict(Cout=48), ENOTSUP), (dict(B=0), OK),
+    (dict(y=None), EINVAL), (dict(y=FAKE), EINVAL), (dict(B=0), OK),
     # packed weights beyond the 4 MiB static array: 27 * 512 * 512 * 2 bytes
     (dict(Cin=512, Cout=512), EWS), (dict(Cin=1024, Cout=128), EWS),
 ])
@@ -143,7 +149,8 @@ def test_conv3d_noalloc_limit():
 
 
 @pytest.mark.parametrize("args,status", [
-    (dict(Cin=0), EINVAL), (dict(Cout=2048), EINVAL), (dict(Cout=48), ENOTSUP),
+    (dict(Cin=0), EINVAL), (dict(Cout=2048), EINVAL),
+    (dict(Cout=48, nbytes=16 * 27 * 48 * 2), EWS),
     (dict(w=None), EINVAL), (dict(w=FAKE_ODD), EINVAL), (dict(packed=None), EWS),
     (dict(packed=ctypes.c_void_p(0x400010)), EWS), (dict(nbytes=100), EWS),
     # the packed copy written over the weights themselves
@@ -157,7 +164,8 @@ def test_conv3d_pack_weights_rejects(args, status):
 
 
 @pytest.mark.parametrize("args,status", [
-    (dict(B=-1), EINVAL), (dict(R=0), EINVAL), (dict(Cout=48), ENOTSUP), (dict(B=0), OK),
+    (dict(B=-1), EINVAL), (dict(R=0), EINVAL), (dict(B=0), OK),
+    (dict(Cout=48, nbytes=16 * 27 * 48 * 2), EWS),
     (dict(x=None), EINVAL), (dict(packed=None), EINVAL), (dict(y=FAKE), EINVAL),
     (dict(packed=ctypes.c_void_p(0x400010)), EWS), (dict(nbytes=100), EWS),
     # the output written over the packed weights
@@ -422,7 +430,7 @@ def test_forward_rejects():
     assert _fwd(lay, fld=320, out=ctypes.c_void_p(0x100000 + 60 * 4), old=320) == EINVAL
     assert _fwd(lay, fld=320, out=ctypes.c_void_p(0x100000 + 200 * 4), old=320) == EINVAL
     for field, val, status in [("n_convs", 0, EINVAL), ("n_convs", 5, EINVAL), ("R", 0, EINVAL),
-                               ("cout", 48, ENOTSUP), ("compute_dt", 4, EINVAL),
+                               ("cout", 0, EINVAL), ("compute_dt", 4, EINVAL),
                                ("cin", 0, EINVAL), ("devox", 2, EINVAL), ("devox", -1, EINVAL)]:
         lay = _layer()
         setattr(lay, field, val)

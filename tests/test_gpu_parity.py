@@ -319,6 +319,10 @@ CONV_CASES = [
     (1, 13, 32, 32, "bf16"),       # ragged R, 32-channel tiles
     (1, 7, 40, 96, "f32"),         # Cin not a multiple of 32, Cout = 3 x 32
     (3, 1, 16, 64, "bf16"),        # R = 1
+    (2, 32, 8, 16, "bf16"),        # 0.125 x C: 16 output channels, half a tile
+    (2, 16, 8, 8, "bf16"),         # 8 output channels
+    (1, 8, 16, 12, "bf16"),        # 12 channels: rows of 24 bytes, element stores
+    (1, 13, 24, 40, "f32"),        # a second tile of 8 channels
 ]
 
 
@@ -644,6 +648,7 @@ def test_forward_nearest_devox_layer(wl_idx, B):
 @pytest.mark.parametrize("R,n_convs,width,devox", [
     (24, 2, 1.0, "trilinear"), (32, 1, 1.0, "trilinear"), (32, 3, 1.0, "trilinear"),
     (32, 2, 0.25, "trilinear"), (16, 3, 0.5, "nearest"), (24, 2, 0.5, "nearest"),
+    (32, 2, 0.125, "trilinear"), (16, 2, 0.125, "nearest"),
 ])
 def test_forward_layer_variants(R, n_convs, width, devox):
     # the variants the paper's resolution and ablation tables vary: R (24 is
