@@ -30,24 +30,35 @@ _P = ctypes.c_void_p
 _I64 = ctypes.c_int64
 
 
-def build(verbose: bool = False) -> str:
-    """Compile the oracle with gcc (fp64, no FMA contraction, OpenMP)."""
+# A build of the same source with AddressSanitizer and UndefinedBehaviorSanitizer
+# (host code only), for the test that runs the oracle under them.
+SANITIZED_LIB_PATH = os.path.join(_HERE, "libpvconv_oracle_san.so")
+
+
+def build(verbose: bool = False, sanitize: bool = False) -> str:
+    """Compile the oracle with gcc (fp64, no FMA contraction, OpenMP);
+    sanitize: the ASan + UBSan build at SANITIZED_LIB_PATH instead."""
+    out = SANITIZED_LIB_PATH if sanitize else _LIB_PATH
+    extra = ["-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
+             "-fno-sanitize-recover=undefined"] if sanitize else []
     cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fopenmp", "-ffp-contract=off",
-           "-Wall", "-Wextra", "-o", _LIB_PATH + ".tmp", _SRC, "-lm"]
+           "-Wall", "-Wextra", *extra, "-o", out + ".tmp", _SRC, "-lm"]
     if verbose:
         print(" ".join(cmd))
     subprocess.run(cmd, check=True)
-    os.replace(_LIB_PATH + ".tmp", _LIB_PATH)
-    return _LIB_PATH
+    os.replace(out + ".tmp", out)
+    return out
 
 
 def _load():
     global _lib
     if _lib is not None:
         return _lib
-    if not os.path.exists(_LIB_PATH) or os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC):
+    path = os.environ.get("PV_ORACLE_LIB", _LIB_PATH)
+    if path == _LIB_PATH and (not os.path.exists(_LIB_PATH) or
+                              os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC)):
         build()
-    lib = ctypes.CDLL(_LIB_PATH)
+    lib = ctypes.CDLL(path)
     sig = {
         "ref_normalize": [_P, _I64, _I64, _P, _P, _P],
         "ref_voxel_ids": [_P, _I64, _I64, ctypes.c_int, _P],
