@@ -58,6 +58,7 @@ struct ForwardWs {
     void* grid_a;
     void* grid_b;
     float* devox;
+    float* split;  // fp32 partial sums of split convolutions (small grids), or NULL
     size_t total;
 };
 
@@ -84,6 +85,13 @@ ForwardWs carve_forward(void* base, int B, int N, const pvconv_layer* L) {
     w.grid_a = take((size_t)B * V * cmax * es);
     w.grid_b = take((size_t)B * V * L->cout * es);
     w.devox = (float*)take((size_t)B * N * L->cout * 4);
+    size_t split = 0;
+    if (L->compute_dt == PVCONV_BF16)
+        for (int i = 0; i < L->n_convs; i++) {
+            const size_t b = pv_conv3d_split_ws_bytes(B, L->R, i ? L->cout : L->cin, L->cout);
+            split = b > split ? b : split;
+        }
+    w.split = split ? (float*)take(split) : nullptr;
     w.total = off;
     return w;
 }
@@ -581,7 +589,8 @@ pvconv_status pvconv_forward_ex(const float* coords, const void* feats, pvconv_d
     for (int i = 0; i < L->n_convs; i++) {
         st = pv_launch_conv3d(src, B, R, cin, L->cout, L->conv_w[i],
                               pv_make_fold(&L->conv_bn[i], nullptr), PVCONV_ACT_LEAKY,
-                              L->conv_slope, bf, dst, bf, w.conv_ws[i], s, /*packed=*/bf);
+                              L->conv_slope, bf, dst, bf, w.conv_ws[i], s, /*packed=*/bf,
+                              w.split);
         if (st != PVCONV_OK) return st;
         void* t = src;
         src = dst;

@@ -33,6 +33,8 @@
 //    LDS so that every store instruction writes whole contiguous rows.
 //
 // fp32 path: four lanes per (voxel, output channel), plain FMA loops.
+#include <algorithm>
+
 #include "pv_common.h"
 
 namespace {
@@ -108,11 +110,16 @@ __device__ __forceinline__ uint4 bload8_elems(__amdgpu_buffer_rsrc_t r, int voff
 // waves, two per SIMD). SB: compact halo buffers and at most 128
 // accumulator registers, so that two workgroups share a CU and one's
 // prologue and epilogue overlap the other's MFMAs.
+// Split-K (ksplit > 1): the input channels' chunks are divided among ksplit
+// groups of workgroups (cps chunks each); split s reads channels from
+// s*cps*16 (rows of x_ld elements), and writes its fp32 partial sums, without
+// batch norm or activation, to y + s*B*R^3*Cout (the caller passes an
+// identity fold and no activation); pv_conv_split_reduce_kernel adds them.
 template <int NB, int WCH, bool VEC, bool SB = false>
 __global__ __launch_bounds__(256 * WCH, SB ? 2 : 1) void pv_conv3d_bf16_kernel(
     const uint16_t* __restrict__ x, const uint16_t* __restrict__ wpk, PvBnFold bn, int act,
     float slope, void* __restrict__ y, int out_bf16, int vec_out, int R, int Cin, int Cout,
-    int nbr, int nblocks) {
+    int nbr, int nblocks, int x_ld, int ksplit, int cps, int B) {
     __shared__ __attribute__((aligned(16))) char lds[SB ? kLdsBytesSB : kLdsBytes];
     __shared__ float bn_tab[2][NB * 32];  // folded scale and shift per output channel
 
@@ -121,6 +128,15 @@ __global__ __launch_bounds__(256 * WCH, SB ? 2 : 1) void pv_conv3d_bf16_kernel(
     // contiguous range of bricks so that neighbouring halos share its L2.
     int bid = blockIdx.x;
     if ((nblocks & 7) == 0) bid = (bid & 7) * (nblocks >> 3) + (bid >> 3);
+    if (ksplit > 1) {  // this workgroup's share of the input channels
+        const int split = bid % ksplit;
+        bid /= ksplit;
+        const int c_lo = split * cps * kKC;
+        x += c_lo;
+        wpk += (size_t)split * cps * kTaps * ((Cout + 31) / 32) * 512;
+        Cin = min(Cin - c_lo, cps * kKC);
+        y = (float*)y + (size_t)split * B * R * R * R * Cout;
+    }
     constexpr int NT = NB * 32;
     // Waves = 4 voxel groups x WCH channel groups: each wave owns two u-slices
     // of the brick (4 blocks of 32 voxels) and NBW blocks of 32 channels.
@@ -171,9 +187,11 @@ __global__ __launch_bounds__(256 * WCH, SB ? 2 : 1) void pv_conv3d_bf16_kernel(
     // goff: byte offset into the input resource (kOOB outside the grid);
     // loff: LDS byte offset in buffer 0.
     const int ulo = max(u0 - 1, 0), uhi = min(u0 + kBrick + 1, R);
-    const size_t slab = (size_t)R * R * Cin;  // elements per u-slab
-    const __amdgpu_buffer_rsrc_t xr =
-        make_rsrc(x + cloud * Cin + ulo * slab, (uint32_t)((uhi - ulo) * slab * 2));
+    // rows of x_ld elements, of which the first Cin are this conv's (or this
+    // split's) channels; the range ends with the last row's channels
+    const size_t slab = (size_t)R * R * x_ld;  // elements per u-slab
+    const __amdgpu_buffer_rsrc_t xr = make_rsrc(
+        x + cloud * x_ld + ulo * slab, (uint32_t)(((uhi - ulo) * slab - (x_ld - Cin)) * 2));
     const int pq = tid & 1;
     int goff[kSets], loff[kSets];
 #pragma unroll
@@ -182,7 +200,7 @@ __global__ __launch_bounds__(256 * WCH, SB ? 2 : 1) void pv_conv3d_bf16_kernel(
         const int hu = h / (kHalo * kHalo), hv = (h / kHalo) % kHalo, hw = h % kHalo;
         const int gu = u0 + hu - 1, gv = v0 + hv - 1, gw = w0 + hw - 1;
         const bool in = gu >= 0 && gu < R && gv >= 0 && gv < R && gw >= 0 && gw < R;
-        goff[set] = in ? ((((gu - ulo) * R + gv) * R + gw) * Cin + pq * 8) * 2 : kOOB;
+        goff[set] = in ? ((((gu - ulo) * R + gv) * R + gw) * x_ld + pq * 8) * 2 : kOOB;
         loff[set] = SB ? (hu * kHalo + hv) * kRowPitchSB + hw * kVoxPitchSB + half_off(hw, pq)
                        : (hu * kHalo + hv) * kRowPitch + hw * kVoxPitch + pq * 16;
     }
@@ -452,24 +470,75 @@ __global__ __launch_bounds__(256) void pv_conv3d_f32_kernel(const float* __restr
         ((float*)y)[i] = val;
 }
 
+// y = act(BN(sum of the ksplit partial sums)), the partials added in split
+// order. Four channels per thread (C_out % 4 == 0 and 16-byte aligned rows),
+// else one.
+template <bool V4>
+__global__ __launch_bounds__(256) void pv_conv_split_reduce_kernel(
+    const float* __restrict__ part, int ksplit, size_t n, int Cout, PvBnFold bn, int act,
+    float slope, void* __restrict__ y, int out_bf16) {
+    const size_t i0 = ((size_t)blockIdx.x * 256 + threadIdx.x) * (V4 ? 4 : 1);
+    if (i0 >= n) return;
+    const int c0 = (int)(i0 % Cout);
+    float v[V4 ? 4 : 1];
+    if constexpr (V4) {
+        float4 a = *(const float4*)(part + i0);
+        for (int s = 1; s < ksplit; s++) {
+            const float4 b = *(const float4*)(part + (size_t)s * n + i0);
+            a.x += b.x;
+            a.y += b.y;
+            a.z += b.z;
+            a.w += b.w;
+        }
+        v[0] = a.x;
+        v[1] = a.y;
+        v[2] = a.z;
+        v[3] = a.w;
+    } else {
+        float a = part[i0];
+        for (int s = 1; s < ksplit; s++) a += part[(size_t)s * n + i0];
+        v[0] = a;
+    }
+#pragma unroll
+    for (int e = 0; e < (V4 ? 4 : 1); e++) {
+        float sc, sh;
+        pv_bn_coeffs(bn, c0 + e, sc, sh);
+        v[e] = pv_activate(v[e] * sc + sh, act, slope);
+    }
+    if (out_bf16) {
+        uint16_t* o = (uint16_t*)y + i0;
+        if constexpr (V4)
+            *(uint2*)o = make_uint2(pv_pack_bf16x2(v[0], v[1]), pv_pack_bf16x2(v[2], v[3]));
+        else
+            o[0] = pv_f32_to_bf16(v[0]);
+    } else {
+        float* o = (float*)y + i0;
+        if constexpr (V4)
+            *(float4*)o = make_float4(v[0], v[1], v[2], v[3]);
+        else
+            o[0] = v[0];
+    }
+}
+
 template <int NB, int WCH, bool SB = false>
 void launch_bf16(const void* x, int B, int R, int Cin, int Cout, const void* w,
                  const PvBnFold& bn, int act, float slope, void* y, bool out_bf16, bool vec,
-                 hipStream_t s) {
+                 hipStream_t s, int ksplit = 1, int cps = 0) {
     const int nbr = (R + kBrick - 1) / kBrick;
-    const size_t blocks = (size_t)B * nbr * nbr * nbr * ((Cout + NB * 32 - 1) / (NB * 32));
+    const size_t blocks =
+        (size_t)B * nbr * nbr * nbr * ((Cout + NB * 32 - 1) / (NB * 32)) * ksplit;
     // 16-byte stores: aligned output with rows of whole 16-byte pieces
     const bool vec_out = pv_aligned16(y) && ((size_t)Cout * (out_bf16 ? 2 : 4)) % 16 == 0;
+#define PV_CONV(V)                                                                          \
+    hipLaunchKernelGGL((pv_conv3d_bf16_kernel<NB, WCH, V, SB>), dim3((unsigned)blocks),     \
+                       dim3(256 * WCH), 0, s, (const uint16_t*)x, (const uint16_t*)w, bn, act, \
+                       slope, y, (int)out_bf16, (int)vec_out, R, Cin, Cout, nbr, (int)blocks, \
+                       Cin, ksplit, cps, B)
     if (vec)
-        hipLaunchKernelGGL((pv_conv3d_bf16_kernel<NB, WCH, true, SB>), dim3((unsigned)blocks),
-                           dim3(256 * WCH), 0, s, (const uint16_t*)x, (const uint16_t*)w, bn,
-                           act, slope, y, (int)out_bf16, (int)vec_out, R, Cin, Cout, nbr,
-                           (int)blocks);
+        PV_CONV(true);
     else
-        hipLaunchKernelGGL((pv_conv3d_bf16_kernel<NB, WCH, false, SB>), dim3((unsigned)blocks),
-                           dim3(256 * WCH), 0, s, (const uint16_t*)x, (const uint16_t*)w, bn,
-                           act, slope, y, (int)out_bf16, (int)vec_out, R, Cin, Cout, nbr,
-                           (int)blocks);
+        PV_CONV(false);
+#undef PV_CONV
 }
 
 }  // namespace
@@ -497,9 +566,33 @@ void pv_launch_pack_conv_weights(const PvPackJobs& jobs, hipStream_t s) {
         hipLaunchKernelGGL(pv_pack_conv_weights_kernel, dim3(blocks), dim3(256), 0, s, jobs);
 }
 
+int pv_conv3d_splits(int B, int R, int Cin, int Cout) {
+    // Grids so small that the unsplit launch (32-channel tiles) leaves most
+    // CUs idle, fewer than 64 workgroups (PVCNN++'s R = 8 level: 16), divide
+    // the input channels among more workgroups of the two-per-CU variant.
+    // At 64 and more (the R = 16 blocks) the split's extra prologues, fp32
+    // partials and reduction cost more than the occupancy gains (measured).
+    const int nbr = (R + kBrick - 1) / kBrick;
+    const long bricks = (long)B * nbr * nbr * nbr;
+    const long tiles = bricks * (Cout / 64);
+    const int nch = (Cin + kKC - 1) / kKC;
+    if (Cout % 64 != 0 || Cin % kKC != 0 || bricks * ((Cout + 31) / 32) >= 64 || nch < 2 ||
+        tiles == 0)
+        return 1;
+    const int want = (int)((512 + tiles - 1) / tiles);
+    const int cps = (nch + std::min(want, nch) - 1) / std::min(want, nch);
+    return (nch + cps - 1) / cps;
+}
+
+size_t pv_conv3d_split_ws_bytes(int B, int R, int Cin, int Cout) {
+    const int S = pv_conv3d_splits(B, R, Cin, Cout);
+    return S > 1 ? (size_t)S * B * R * R * R * Cout * 4 : 0;
+}
+
 pvconv_status pv_launch_conv3d(const void* x, int B, int R, int Cin, int Cout, const void* w,
                                const PvBnFold& bn, int act, float slope, bool bf16, void* y,
-                               bool out_bf16, void* ws, hipStream_t s, bool packed) {
+                               bool out_bf16, void* ws, hipStream_t s, bool packed,
+                               float* split_ws) {
     if (B == 0) return PVCONV_OK;
     if (bf16) {
         if (!packed) {
@@ -509,6 +602,25 @@ pvconv_status pv_launch_conv3d(const void* x, int B, int R, int Cin, int Cout, c
         }
         w = ws;
         const bool vec = (Cin % 8 == 0) && pv_aligned16(x);
+        const int S = split_ws ? pv_conv3d_splits(B, R, Cin, Cout) : 1;
+        if (S > 1) {
+            // fp32 partial sums per split (identity fold, no activation),
+            // then their fixed-order sum with the batch norm and activation
+            const int nch = (Cin + kKC - 1) / kKC, cps = (nch + S - 1) / S;
+            launch_bf16<2, 1, true>(x, B, R, Cin, Cout, w, PvBnFold{}, PVCONV_ACT_NONE, 0.f,
+                                    split_ws, false, vec, s, S, cps);
+            const size_t n = (size_t)B * R * R * R * Cout;
+            const bool v4 = Cout % 4 == 0 && pv_aligned16(y) && pv_aligned16(split_ws);
+            const size_t threads = v4 ? n / 4 : n;
+            const unsigned blocks = (unsigned)((threads + 255) / 256);
+            if (v4)
+                hipLaunchKernelGGL(pv_conv_split_reduce_kernel<true>, dim3(blocks), dim3(256), 0,
+                                   s, split_ws, S, n, Cout, bn, act, slope, y, (int)out_bf16);
+            else
+                hipLaunchKernelGGL(pv_conv_split_reduce_kernel<false>, dim3(blocks), dim3(256),
+                                   0, s, split_ws, S, n, Cout, bn, act, slope, y, (int)out_bf16);
+            return pv_launch_status();
+        }
         // Channel tile: the widest (most reuse of each halo) that still gives
         // about one workgroup per CU; small grids (R = 16) take narrow tiles.
         const int nbr = (R + kBrick - 1) / kBrick;

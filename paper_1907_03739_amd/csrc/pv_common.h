@@ -164,10 +164,16 @@ __device__ __forceinline__ void pv_pack_role(const PvPackJobs& jobs, int blk,
                              (uint32_t)e[4] | ((uint32_t)e[5] << 16),
                              (uint32_t)e[6] | ((uint32_t)e[7] << 16));
 }
-// packed: the bf16 weights are already repacked in ws (w is then unused)
+// packed: the bf16 weights are already repacked in ws (w is then unused).
+// split_ws: fp32 room for pv_conv3d_split_ws_bytes, or nullptr: grids too
+// small to fill the chip then split the input channels across workgroups
+// (fixed-order sum of the partials), else they run unsplit.
 pvconv_status pv_launch_conv3d(const void* x, int B, int R, int Cin, int Cout, const void* w,
                                const PvBnFold& bn, int act, float slope, bool bf16, void* y,
-                               bool out_bf16, void* ws, hipStream_t s, bool packed = false);
+                               bool out_bf16, void* ws, hipStream_t s, bool packed = false,
+                               float* split_ws = nullptr);
+int pv_conv3d_splits(int B, int R, int Cin, int Cout);
+size_t pv_conv3d_split_ws_bytes(int B, int R, int Cin, int Cout);
 pvconv_status pv_launch_devoxelize(const void* grid, int B, int R, int C, bool grid_bf16,
                                    const float* pn, int N, float* out, hipStream_t s);
 pvconv_status pv_launch_devoxelize_nearest(const void* grid, int B, int R, int C, bool grid_bf16,

@@ -649,6 +649,7 @@ def test_forward_nearest_devox_layer(wl_idx, B):
     (24, 2, 1.0, "trilinear"), (32, 1, 1.0, "trilinear"), (32, 3, 1.0, "trilinear"),
     (32, 2, 0.25, "trilinear"), (16, 3, 0.5, "nearest"), (24, 2, 0.5, "nearest"),
     (32, 2, 0.125, "trilinear"), (16, 2, 0.125, "nearest"),
+    (8, 2, 1.0, "trilinear"),   # a grid of 2 x 1 bricks: the convs split their input channels
 ])
 def test_forward_layer_variants(R, n_convs, width, devox):
     # the variants the paper's resolution and ablation tables vary: R (24 is
