@@ -573,14 +573,18 @@ pvconv_status pvconv_forward_ex(const float* coords, const void* feats, pvconv_d
     if (bf)
         for (int i = 0; i < L->n_convs; i++)
             pv_pack_job(jobs, L->conv_w[i], i ? L->cout : L->cin, L->cout, w.conv_ws[i]);
+    // bf16 small clouds: the grid holds only its occupied rows (most voxels
+    // are empty: their rows are neither written nor read); the first
+    // convolution reads the counts and takes empty voxels as zero
+    const bool sparse = bf && pv_voxelize_sparse_ok(N);
     if (ids_given) {
         pv_launch_pack_conv_weights(jobs, s);
         st = pv_launch_voxelize_from_ids(ids, feats, feat_dt == PVCONV_BF16, feat_ld, B, N,
-                                         L->cin, R, w.grid_a, bf, w.counts, w.vox_ws, s);
+                                         L->cin, R, w.grid_a, bf, w.counts, w.vox_ws, s, sparse);
     } else {
         st = pv_launch_voxelize(coords, feats, feat_dt == PVCONV_BF16, feat_ld, B, N, L->cin, R,
                                 w.grid_a, bf, w.counts, ids,
-                                norm_coords ? norm_coords : w.pnorm, w.vox_ws, s, &jobs);
+                                norm_coords ? norm_coords : w.pnorm, w.vox_ws, s, &jobs, sparse);
     }
     if (st != PVCONV_OK) return st;
     void* src = w.grid_a;
@@ -590,7 +594,7 @@ pvconv_status pvconv_forward_ex(const float* coords, const void* feats, pvconv_d
         st = pv_launch_conv3d(src, B, R, cin, L->cout, L->conv_w[i],
                               pv_make_fold(&L->conv_bn[i], nullptr), PVCONV_ACT_LEAKY,
                               L->conv_slope, bf, dst, bf, w.conv_ws[i], s, /*packed=*/bf,
-                              w.split);
+                              w.split, i == 0 && sparse ? w.counts : nullptr);
         if (st != PVCONV_OK) return st;
         void* t = src;
         src = dst;

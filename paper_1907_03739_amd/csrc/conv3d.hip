@@ -119,7 +119,7 @@ template <int NB, int WCH, bool VEC, bool SB = false>
 __global__ __launch_bounds__(256 * WCH, SB ? 2 : 1) void pv_conv3d_bf16_kernel(
     const uint16_t* __restrict__ x, const uint16_t* __restrict__ wpk, PvBnFold bn, int act,
     float slope, void* __restrict__ y, int out_bf16, int vec_out, int R, int Cin, int Cout,
-    int nbr, int nblocks, int x_ld, int ksplit, int cps, int B) {
+    int nbr, int nblocks, int x_ld, int ksplit, int cps, int B, const int32_t* __restrict__ occ) {
     __shared__ __attribute__((aligned(16))) char lds[SB ? kLdsBytesSB : kLdsBytes];
     __shared__ float bn_tab[2][NB * 32];  // folded scale and shift per output channel
 
@@ -199,7 +199,10 @@ __global__ __launch_bounds__(256 * WCH, SB ? 2 : 1) void pv_conv3d_bf16_kernel(
         const int h = min(set * (NTH / 2) + (tid >> 1), kHaloVox - 1);
         const int hu = h / (kHalo * kHalo), hv = (h / kHalo) % kHalo, hw = h % kHalo;
         const int gu = u0 + hu - 1, gv = v0 + hv - 1, gw = w0 + hw - 1;
-        const bool in = gu >= 0 && gu < R && gv >= 0 && gv < R && gw >= 0 && gw < R;
+        bool in = gu >= 0 && gu < R && gv >= 0 && gv < R && gw >= 0 && gw < R;
+        // a sparse input grid: empty voxels read as zero (their rows were
+        // never written), through the out-of-range offset
+        if (occ && in) in = occ[cloud + ((size_t)gu * R + gv) * R + gw] > 0;
         goff[set] = in ? ((((gu - ulo) * R + gv) * R + gw) * x_ld + pq * 8) * 2 : kOOB;
         loff[set] = SB ? (hu * kHalo + hv) * kRowPitchSB + hw * kVoxPitchSB + half_off(hw, pq)
                        : (hu * kHalo + hv) * kRowPitch + hw * kVoxPitch + pq * 16;
@@ -523,7 +526,7 @@ __global__ __launch_bounds__(256) void pv_conv_split_reduce_kernel(
 template <int NB, int WCH, bool SB = false>
 void launch_bf16(const void* x, int B, int R, int Cin, int Cout, const void* w,
                  const PvBnFold& bn, int act, float slope, void* y, bool out_bf16, bool vec,
-                 hipStream_t s, int ksplit = 1, int cps = 0) {
+                 hipStream_t s, int ksplit = 1, int cps = 0, const int32_t* occ = nullptr) {
     const int nbr = (R + kBrick - 1) / kBrick;
     const size_t blocks =
         (size_t)B * nbr * nbr * nbr * ((Cout + NB * 32 - 1) / (NB * 32)) * ksplit;
@@ -533,7 +536,7 @@ void launch_bf16(const void* x, int B, int R, int Cin, int Cout, const void* w,
     hipLaunchKernelGGL((pv_conv3d_bf16_kernel<NB, WCH, V, SB>), dim3((unsigned)blocks),     \
                        dim3(256 * WCH), 0, s, (const uint16_t*)x, (const uint16_t*)w, bn, act, \
                        slope, y, (int)out_bf16, (int)vec_out, R, Cin, Cout, nbr, (int)blocks, \
-                       Cin, ksplit, cps, B)
+                       Cin, ksplit, cps, B, occ)
     if (vec)
         PV_CONV(true);
     else
@@ -592,7 +595,7 @@ size_t pv_conv3d_split_ws_bytes(int B, int R, int Cin, int Cout) {
 pvconv_status pv_launch_conv3d(const void* x, int B, int R, int Cin, int Cout, const void* w,
                                const PvBnFold& bn, int act, float slope, bool bf16, void* y,
                                bool out_bf16, void* ws, hipStream_t s, bool packed,
-                               float* split_ws) {
+                               float* split_ws, const int32_t* occ) {
     if (B == 0) return PVCONV_OK;
     if (bf16) {
         if (!packed) {
@@ -608,7 +611,7 @@ pvconv_status pv_launch_conv3d(const void* x, int B, int R, int Cin, int Cout, c
             // then their fixed-order sum with the batch norm and activation
             const int nch = (Cin + kKC - 1) / kKC, cps = (nch + S - 1) / S;
             launch_bf16<2, 1, true>(x, B, R, Cin, Cout, w, PvBnFold{}, PVCONV_ACT_NONE, 0.f,
-                                    split_ws, false, vec, s, S, cps);
+                                    split_ws, false, vec, s, S, cps, occ);
             const size_t n = (size_t)B * R * R * R * Cout;
             const bool v4 = Cout % 4 == 0 && pv_aligned16(y) && pv_aligned16(split_ws);
             const size_t threads = v4 ? n / 4 : n;
@@ -635,14 +638,14 @@ pvconv_status pv_launch_conv3d(const void* x, int B, int R, int Cin, int Cout, c
         // accumulator registers and spill in its epilogue).
         const bool two = Cin <= 64;
         if (Cin <= 128 && Cout % 64 == 0 && bricks * (Cout / 64) >= 512) {
-            launch_bf16<2, 1, true>(x, B, R, Cin, Cout, w, bn, act, slope, y, out_bf16, vec, s);
+            launch_bf16<2, 1, true>(x, B, R, Cin, Cout, w, bn, act, slope, y, out_bf16, vec, s, 1, 0, occ);
         } else if (Cout % 64 == 0 && bricks * (Cout / 64) >= 256) {
             if (two)
-                launch_bf16<2, 2>(x, B, R, Cin, Cout, w, bn, act, slope, y, out_bf16, vec, s);
+                launch_bf16<2, 2>(x, B, R, Cin, Cout, w, bn, act, slope, y, out_bf16, vec, s, 1, 0, occ);
             else
-                launch_bf16<2, 1>(x, B, R, Cin, Cout, w, bn, act, slope, y, out_bf16, vec, s);
+                launch_bf16<2, 1>(x, B, R, Cin, Cout, w, bn, act, slope, y, out_bf16, vec, s, 1, 0, occ);
         } else {
-            launch_bf16<1, 1>(x, B, R, Cin, Cout, w, bn, act, slope, y, out_bf16, vec, s);
+            launch_bf16<1, 1>(x, B, R, Cin, Cout, w, bn, act, slope, y, out_bf16, vec, s, 1, 0, occ);
         }
     } else {
         const size_t total = (size_t)B * R * R * R * Cout;

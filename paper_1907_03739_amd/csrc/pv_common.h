@@ -103,17 +103,20 @@ struct PvPackJobs {
 // ---- internal launchers (arguments already validated) ---------------------
 size_t pv_voxelize_ws_bytes(int B, int N, int R);
 // pack (optional): weight-packing jobs run by extra workgroups of the
-// normalisation launch, which leaves most CUs idle (nullptr: none)
+// voxelisation launch (nullptr: none). sparse: the caller reads the grid only
+// at voxels whose count is positive, so the rows of empty voxels are not
+// written (honoured where pv_voxelize_sparse_ok(N), else the grid is whole).
 pvconv_status pv_launch_voxelize(const float* coords, const void* feats, bool feat_bf16,
                                  int feat_ld, int B, int N, int C, int R, void* grid,
                                  bool grid_bf16, int32_t* counts, int32_t* vox_id,
                                  float* norm_coords, void* ws, hipStream_t s,
-                                 const PvPackJobs* pack = nullptr);
+                                 const PvPackJobs* pack = nullptr, bool sparse = false);
 // the same with the voxel indices given (no normalisation)
 pvconv_status pv_launch_voxelize_from_ids(const int32_t* ids, const void* feats, bool feat_bf16,
                                           int feat_ld, int B, int N, int C, int R, void* grid,
                                           bool grid_bf16, int32_t* counts, void* ws,
-                                          hipStream_t s);
+                                          hipStream_t s, bool sparse = false);
+bool pv_voxelize_sparse_ok(int N);
 size_t pv_conv3d_ws_bytes(int Cin, int Cout, bool bf16);
 // bf16 conv weights [Cout][27][Cin] repacked into the MFMA fragment order
 // (into a workspace of pv_conv3d_ws_bytes), the convolutions of a layer in one
@@ -167,11 +170,13 @@ __device__ __forceinline__ void pv_pack_role(const PvPackJobs& jobs, int blk,
 // packed: the bf16 weights are already repacked in ws (w is then unused).
 // split_ws: fp32 room for pv_conv3d_split_ws_bytes, or nullptr: grids too
 // small to fill the chip then split the input channels across workgroups
-// (fixed-order sum of the partials), else they run unsplit.
+// (fixed-order sum of the partials), else they run unsplit. occ: per-voxel
+// counts of the input grid [B][R^3] or nullptr; with it, input voxels of
+// count 0 read as zero and their rows are never read (a sparse grid).
 pvconv_status pv_launch_conv3d(const void* x, int B, int R, int Cin, int Cout, const void* w,
                                const PvBnFold& bn, int act, float slope, bool bf16, void* y,
                                bool out_bf16, void* ws, hipStream_t s, bool packed = false,
-                               float* split_ws = nullptr);
+                               float* split_ws = nullptr, const int32_t* occ = nullptr);
 int pv_conv3d_splits(int B, int R, int Cin, int Cout);
 size_t pv_conv3d_split_ws_bytes(int B, int R, int Cin, int Cout);
 pvconv_status pv_launch_devoxelize(const void* grid, int B, int R, int C, bool grid_bf16,

@@ -784,7 +784,8 @@ __global__ __launch_bounds__(NT) void pv_voxel_slab_kernel(
     const float* __restrict__ coords, const int32_t* __restrict__ ids_in,
     const FT* __restrict__ feats, int feat_ld, int N, int C, int R, int nvs, int nslab,
     int cap_pre, GT* __restrict__ grid, int32_t* __restrict__ counts,
-    int32_t* __restrict__ vox_id, float* __restrict__ norm_coords, PvPackJobs pack, int npack) {
+    int32_t* __restrict__ vox_id, float* __restrict__ norm_coords, PvPackJobs pack, int npack,
+    int sparse) {
     extern __shared__ __attribute__((aligned(16))) char smem[];
     __shared__ __attribute__((aligned(16))) char s_stage[kStageBytes + kStageSlack];
     // compute waves' barrier counter; counts complete; the slab's point count
@@ -865,7 +866,7 @@ __global__ __launch_bounds__(NT) void pv_voxel_slab_kernel(
     if (tid >= W0) {
         // writers, before the counts exist: the rows no point can reach
         // (normalised points only; given indices may name any voxel)
-        if (!ids_in) zero_rows([&](int vi) { return far[vi] != 0; });
+        if (!ids_in && !sparse) zero_rows([&](int vi) { return far[vi] != 0; });
         // wait (bounded, well under a second) until the compute waves have counted
         for (int spin = 0; spin < (1 << 23); spin++) {
             if (__hip_atomic_load(&s_counted, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP))
@@ -873,8 +874,8 @@ __global__ __launch_bounds__(NT) void pv_voxel_slab_kernel(
             __builtin_amdgcn_s_sleep(2);
         }
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-        // the other empty rows, then the counts
-        zero_rows([&](int vi) { return hist[vi] == 0 && !far[vi]; });
+        // the other empty rows (sparse: none), then the counts
+        if (!sparse) zero_rows([&](int vi) { return hist[vi] == 0 && !far[vi]; });
         for (int v = tid - W0; v < nv; v += NW) counts[(size_t)b * V + v0 + v] = hist[v];
         return;
     }
@@ -1968,7 +1969,8 @@ namespace {
 template <typename FT, typename GT, bool VEC, bool GVEC>
 pvconv_status launch_slab_t(const float* coords, const int32_t* ids_in, const void* feats,
                             int feat_ld, int B, int N, int C, int R, void* grid, int32_t* counts,
-                            int32_t* vox_id, float* pn, const PvPackJobs& jobs, hipStream_t s) {
+                            int32_t* vox_id, float* pn, const PvPackJobs& jobs, bool sparse,
+                            hipStream_t s) {
     const int V = R * R * R;
     const SlabShape sh = slab_shape(B, V, N);
     const int npack = (pv_pack_blocks(jobs) + 1) / 2;
@@ -1984,7 +1986,7 @@ pvconv_status launch_slab_t(const float* coords, const int32_t* ids_in, const vo
         if (!grant_lds((const void*)kernel, bytes)) return PVCONV_EHIP;
         hipLaunchKernelGGL(kernel, g, dim3(nt), bytes, s, coords, ids_in, (const FT*)feats,
                            feat_ld, N, C, R, sh.nvs, sh.S, cap_pre, (GT*)grid, counts, vox_id,
-                           pn, jobs, npack);
+                           pn, jobs, npack, (int)sparse);
         return pv_launch_status();
     };
     // points per compute thread: the cloud over kSlabNC threads
@@ -1997,19 +1999,19 @@ pvconv_status launch_slab_t(const float* coords, const int32_t* ids_in, const vo
 pvconv_status launch_slab(const float* coords, const int32_t* ids_in, const void* feats,
                           bool feat_bf16, int feat_ld, int B, int N, int C, int R, void* grid,
                           bool grid_bf16, int32_t* counts, int32_t* vox_id, float* pn, bool vec,
-                          const PvPackJobs& jobs, hipStream_t s) {
+                          const PvPackJobs& jobs, bool sparse, hipStream_t s) {
     // zero stores of whole 16-byte pieces need 16-byte grid rows
     const bool gvec = pv_aligned16(grid) && (C * (grid_bf16 ? 2 : 4)) % 16 == 0;
     // (vec implies 16-byte grid rows)
 #define PV_SLAB(FT, GT)                                                                        \
     if (vec)                                                                                   \
         return launch_slab_t<FT, GT, true, true>(coords, ids_in, feats, feat_ld, B, N, C, R,   \
-                                                 grid, counts, vox_id, pn, jobs, s);           \
+                                                 grid, counts, vox_id, pn, jobs, sparse, s);   \
     if (gvec)                                                                                  \
         return launch_slab_t<FT, GT, false, true>(coords, ids_in, feats, feat_ld, B, N, C, R,  \
-                                                  grid, counts, vox_id, pn, jobs, s);          \
+                                                  grid, counts, vox_id, pn, jobs, sparse, s);  \
     return launch_slab_t<FT, GT, false, false>(coords, ids_in, feats, feat_ld, B, N, C, R,     \
-                                               grid, counts, vox_id, pn, jobs, s)
+                                               grid, counts, vox_id, pn, jobs, sparse, s)
     if (feat_bf16) {
         if (grid_bf16) {
             PV_SLAB(uint16_t, uint16_t);
@@ -2029,7 +2031,7 @@ pvconv_status pv_launch_voxelize(const float* coords, const void* feats, bool fe
                                  int feat_ld, int B, int N, int C, int R, void* grid,
                                  bool grid_bf16, int32_t* counts, int32_t* vox_id,
                                  float* norm_coords, void* ws, hipStream_t s,
-                                 const PvPackJobs* pack) {
+                                 const PvPackJobs* pack, bool sparse) {
     const PvPackJobs jobs = pack ? *pack : PvPackJobs{};
     const int npack = pv_pack_blocks(jobs);
     if (B == 0) {
@@ -2046,7 +2048,7 @@ pvconv_status pv_launch_voxelize(const float* coords, const void* feats, bool fe
     const GridPlan gp = grid_plan(feats, feat_bf16, feat_ld, B, C, R, grid, grid_bf16);
     if (N <= kSmallMaxN)
         return launch_slab(coords, nullptr, feats, feat_bf16, feat_ld, B, N, C, R, grid,
-                           grid_bf16, counts, ids, pn, gp.vec, jobs, s);
+                           grid_bf16, counts, ids, pn, gp.vec, jobs, sparse, s);
     const int zb = gp.zb;
     const size_t n16 = gp.n16;
     uint4* grid16 = (uint4*)grid;
@@ -2068,14 +2070,14 @@ pvconv_status pv_launch_voxelize(const float* coords, const void* feats, bool fe
 pvconv_status pv_launch_voxelize_from_ids(const int32_t* ids, const void* feats, bool feat_bf16,
                                           int feat_ld, int B, int N, int C, int R, void* grid,
                                           bool grid_bf16, int32_t* counts, void* ws,
-                                          hipStream_t s) {
+                                          hipStream_t s, bool sparse) {
     if (B == 0) return PVCONV_OK;
     VoxWs w = carve_ws(ws, B, N, R, nullptr);
     const GridPlan gp = grid_plan(feats, feat_bf16, feat_ld, B, C, R, grid, grid_bf16);
     uint4* grid16 = (uint4*)grid;
     if (N <= kSmallMaxN)
         return launch_slab(nullptr, ids, feats, feat_bf16, feat_ld, B, N, C, R, grid, grid_bf16,
-                           counts, nullptr, nullptr, gp.vec, PvPackJobs{}, s);
+                           counts, nullptr, nullptr, gp.vec, PvPackJobs{}, sparse, s);
     {
         dim3 g(w.split.G, B);
         hipLaunchKernelGGL(pv_tile_reset_kernel, dim3(1 + gp.zb), dim3(kNormThreads), 0, s,
@@ -2087,3 +2089,5 @@ pvconv_status pv_launch_voxelize_from_ids(const int32_t* ids, const void* feats,
     }
     return voxelize_fill(feats, feat_bf16, feat_ld, B, N, C, R, grid, grid_bf16, counts, w, gp, s);
 }
+
+bool pv_voxelize_sparse_ok(int N) { return N <= kSmallMaxN; }
