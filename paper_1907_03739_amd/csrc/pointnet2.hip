@@ -242,63 +242,91 @@ __global__ __launch_bounds__(256) void pv_group_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Three nearest neighbours: one thread per unknown point; the cloud's known
-// points pass through LDS in tiles that every thread scans in index order,
-// keeping the three smallest squared distances (a strictly smaller one moves
-// ahead, so among equals the lower index stays in front). Then the
-// normalised inverse-distance weights, in fp32.
+// Three nearest neighbours: kNnLanes lanes per unknown point, each scanning
+// every kNnLanes-th known point (the cloud's known points pass through LDS
+// in tiles) and keeping its three nearest in (distance, index) order: a
+// strictly smaller distance moves ahead, and the lane's candidates come in
+// index order, so among equals the lower index stays in front. The lanes'
+// lists are then merged pairwise by shuffles in the same (distance, index)
+// order. Then the normalised inverse-distance weights, in fp32.
 // ---------------------------------------------------------------------------
 constexpr int kNnThreads = 256;
+constexpr int kNnLanes = 4;
+constexpr int kNnPoints = kNnThreads / kNnLanes;  // unknown points per workgroup
 constexpr int kNnTile = 1024;
+
+struct Near3 {
+    float d[3];
+    int i[3];
+};
+// (d, i) lexicographic order
+__device__ __forceinline__ bool nn_less(float da, int ia, float db, int ib) {
+    return da < db || (da == db && ia < ib);
+}
+__device__ __forceinline__ void nn_insert(Near3& n, float d, int i) {
+    if (nn_less(d, i, n.d[2], n.i[2])) {
+        if (nn_less(d, i, n.d[1], n.i[1])) {
+            n.d[2] = n.d[1];
+            n.i[2] = n.i[1];
+            if (nn_less(d, i, n.d[0], n.i[0])) {
+                n.d[1] = n.d[0];
+                n.i[1] = n.i[0];
+                n.d[0] = d;
+                n.i[0] = i;
+            } else {
+                n.d[1] = d;
+                n.i[1] = i;
+            }
+        } else {
+            n.d[2] = d;
+            n.i[2] = i;
+        }
+    }
+}
 
 __global__ __launch_bounds__(kNnThreads) void pv_three_nn_kernel(
     const float* __restrict__ unknown, int n, const float* __restrict__ known, int m,
     int32_t* __restrict__ idx, float* __restrict__ weight) {
     __shared__ float s_k[kNnTile * 3];
     const int b = blockIdx.y;
-    const int i = blockIdx.x * kNnThreads + threadIdx.x;
+    const int q = threadIdx.x % kNnLanes;  // this lane's share of the candidates
+    const int i = blockIdx.x * kNnPoints + threadIdx.x / kNnLanes;
     const bool active = i < n;
     const float* u = unknown + ((size_t)b * n + (active ? i : 0)) * 3;
     const float ux = u[0], uy = u[1], uz = u[2];
     const float* kp = known + (size_t)b * m * 3;
-    float d0 = INFINITY, d1 = INFINITY, d2 = INFINITY;
-    int i0 = 0, i1 = 0, i2 = 0;
+    Near3 nn{{INFINITY, INFINITY, INFINITY}, {0x7fffffff, 0x7fffffff, 0x7fffffff}};
     for (int t0 = 0; t0 < m; t0 += kNnTile) {
         const int cnt = min(kNnTile, m - t0);
         pv_lds_barrier();  // the previous tile's reads are done
         for (int e = threadIdx.x; e < cnt * 3; e += kNnThreads) s_k[e] = kp[(size_t)t0 * 3 + e];
         pv_lds_barrier();
-        for (int j = 0; j < cnt; j++) {
+        for (int j = q; j < cnt; j += kNnLanes) {
             const float d = sqdist(s_k[j * 3], s_k[j * 3 + 1], s_k[j * 3 + 2], ux, uy, uz);
-            const int jj = t0 + j;
-            if (d < d2) {
-                if (d < d1) {
-                    d2 = d1;
-                    i2 = i1;
-                    if (d < d0) {
-                        d1 = d0;
-                        i1 = i0;
-                        d0 = d;
-                        i0 = jj;
-                    } else {
-                        d1 = d;
-                        i1 = jj;
-                    }
-                } else {
-                    d2 = d;
-                    i2 = jj;
-                }
-            }
+            if (d < nn.d[2]) nn_insert(nn, d, t0 + j);  // a strict < keeps the earlier index
         }
     }
-    if (!active) return;
-    const float a0 = 1.f / (sqrtf(d0) + 1e-8f), a1 = 1.f / (sqrtf(d1) + 1e-8f),
-                a2 = 1.f / (sqrtf(d2) + 1e-8f);
+    // merge with the other lanes of this point (xor 1, then xor 2)
+#pragma unroll
+    for (int off = 1; off < kNnLanes; off <<= 1) {
+        float od[3];
+        int oi[3];
+#pragma unroll
+        for (int k = 0; k < 3; k++) {
+            od[k] = __shfl_xor(nn.d[k], off, 64);
+            oi[k] = __shfl_xor(nn.i[k], off, 64);
+        }
+#pragma unroll
+        for (int k = 0; k < 3; k++) nn_insert(nn, od[k], oi[k]);
+    }
+    if (!active || q != 0) return;
+    const float a0 = 1.f / (sqrtf(nn.d[0]) + 1e-8f), a1 = 1.f / (sqrtf(nn.d[1]) + 1e-8f),
+                a2 = 1.f / (sqrtf(nn.d[2]) + 1e-8f);
     const float sum = (a0 + a1) + a2;
     const size_t o = ((size_t)b * n + i) * 3;
-    idx[o] = i0;
-    idx[o + 1] = i1;
-    idx[o + 2] = i2;
+    idx[o] = nn.i[0];
+    idx[o + 1] = nn.i[1];
+    idx[o + 2] = nn.i[2];
     weight[o] = a0 / sum;
     weight[o + 1] = a1 / sum;
     weight[o + 2] = a2 / sum;
@@ -423,7 +451,7 @@ pvconv_status pv_launch_group(const float* xyz, const void* feats, bool feat_bf1
 pvconv_status pv_launch_three_nn(const float* unknown, int B, int n, const float* known, int m,
                                  int32_t* idx, float* weight, hipStream_t s) {
     if (B == 0 || n == 0) return PVCONV_OK;
-    hipLaunchKernelGGL(pv_three_nn_kernel, dim3((n + kNnThreads - 1) / kNnThreads, B),
+    hipLaunchKernelGGL(pv_three_nn_kernel, dim3((n + kNnPoints - 1) / kNnPoints, B),
                        dim3(kNnThreads), 0, s, unknown, n, known, m, idx, weight);
     return pv_launch_status();
 }
