@@ -36,22 +36,42 @@ def _duplicates(B, N, seed):
     return (rng.integers(0, 5, size=(B, N, 3)) * 0.25).astype(np.float32)
 
 
+def _cloud(kind, B, N, seed):
+    if kind == "rooms":
+        return _rooms(B, N, seed)[0]
+    if kind == "duplicates":
+        return _duplicates(B, N, seed)
+    if kind == "flat":  # a floor: no extent along z
+        xyz = _rooms(B, N, seed)[0]
+        xyz[..., 2] = 0.5
+        return xyz
+    assert kind == "identical"  # one place: no extent at all
+    return np.full((B, N, 3), -0.25, np.float32)
+
+
 FPS_CASES = [
-    # B, N, npoint, cloud (one per launch configuration of the kernel)
+    # B, N, npoint, cloud (every launch configuration of the kernel, ragged
+    # sizes, and clouds whose distances tie: duplicates, a flat floor, one
+    # point repeated)
     (3, 64, 16, "rooms"),
     (2, 200, 50, "rooms"),
     (2, 1000, 250, "rooms"),
+    (2, 1025, 1025, "rooms"),        # every point
     (2, 3000, 700, "rooms"),
     (4, 8192, 1024, "rooms"),
+    (1, 8191, 2048, "rooms"),
     (1, 12000, 300, "rooms"),
     (2, 300, 300, "duplicates"),     # every point, past the distinct ones
+    (1, 5000, 1500, "duplicates"),
+    (2, 4096, 512, "flat"),
+    (1, 2000, 40, "identical"),
     (1, 16384, 64, "duplicates"),
 ]
 
 
 @pytest.mark.parametrize("B,N,npoint,cloud", FPS_CASES)
 def test_fps_matches_oracle(B, N, npoint, cloud):
-    xyz = _rooms(B, N, N)[0] if cloud == "rooms" else _duplicates(B, N, N)
+    xyz = _cloud(cloud, B, N, N)
     want = oracle.fps(xyz, npoint)
     idx, new_xyz = pv.pvconv_furthest_point_sample(dev(xyz), npoint)
     got = idx.cpu().numpy()
