@@ -533,10 +533,13 @@ def bench_backward(args, dev):
     dw2 = torch.empty((cout, 3, 3, 3, cout), dtype=torch.float32, device=dev)
     wws = torch.empty(max(pv._lib.pvconv_conv3d_backward_weight_workspace_size(B, R, c, cout)
                           for c in (cin, cout)), dtype=torch.uint8, device=dev)
+    dws = torch.empty(pv._lib.pvconv_devoxelize_backward_workspace_size(B, N, cout, R),
+                      dtype=torch.uint8, device=dev)
     s_g = 2
     steps = [
         # name, call, unit, algorithmic amount per call
-        ("devoxelize_backward", lambda: pv.pvconv_devoxelize_backward(dout, R, pn, out=dgrid),
+        ("devoxelize_backward", lambda: pv.pvconv_devoxelize_backward(dout, R, pn, out=dgrid,
+                                                                      workspace=dws),
          "GB/s", B * N * (12 + 4 * cout) + B * V * cout * 4),
         ("act_bn_backward", lambda: pv.pvconv_act_bn_backward(dgrid, y, bn=bn2, out=dz),
          "GB/s", B * V * cout * (4 + s_g + 4)),

@@ -439,15 +439,24 @@ pvconv_status pvconv_voxelize_backward(const void* dgrid, pvconv_dtype dt, int B
 /*  dgrid[b][cell][c] = sum over points k of w(k, cell) * dout[b][k][c], with */
 /*  the 8 cells and weights of pvconv_devoxelize. dout [B][N][C] fp32,        */
 /*  norm_coords [B][N][3]; dgrid out [B][R^3][C] fp32, every element written  */
-/*  (cleared, then accumulated with fp32 atomic adds: the order of the adds,  */
-/*  and so the last bits, may differ between runs).                          */
+/*  once. Computed as a gather: the points sorted stably by the cell of their */
+/*  lower trilinear corner, each cell sums its points' weighted gradients in  */
+/*  a fixed order (candidate cells in index order, their points in index      */
+/*  order, fp32), so the result is the same bits on every run. workspace >=   */
+/*  pvconv_devoxelize_backward_workspace_size(B, N, C, R) bytes, 256-byte     */
+/*  aligned (may be NULL when N == 0), else PVCONV_EWORKSPACE.                */
+size_t pvconv_devoxelize_backward_workspace_size(int B, int N, int C, int R);
 pvconv_status pvconv_devoxelize_backward(const float* dout, int B, int N, int C, int R,
-                                         const float* norm_coords, float* dgrid, void* stream);
+                                         const float* norm_coords, float* dgrid, void* workspace,
+                                         size_t workspace_bytes, void* stream);
 
 /* Nearest-neighbour devoxelisation: dgrid[b][cell] = sum of dout[b][k] over  */
-/* the points k with vox_id[b][k] = cell (as above otherwise).               */
+/* the points k with vox_id[b][k] = cell, in point order (as above           */
+/* otherwise; the same workspace). An index outside the grid is invalid      */
+/* input (clamped: memory-safe, result unspecified).                         */
 pvconv_status pvconv_devoxelize_nearest_backward(const float* dout, int B, int N, int C, int R,
                                                  const int32_t* vox_id, float* dgrid,
+                                                 void* workspace, size_t workspace_bytes,
                                                  void* stream);
 
 /* Convolution (Section 4.1 "Feature Aggregation"), gradient with respect to */

@@ -82,8 +82,9 @@ _SIGS = {
                            _I, _I, _VP, _SZ, _VP], _I),
     "pvconv_status_string": ([_I], ctypes.c_char_p),
     "pvconv_voxelize_backward": ([_VP, _I, _I, _I, _I, _I, _VP, _VP, _VP, _VP], _I),
-    "pvconv_devoxelize_backward": ([_VP, _I, _I, _I, _I, _VP, _VP, _VP], _I),
-    "pvconv_devoxelize_nearest_backward": ([_VP, _I, _I, _I, _I, _VP, _VP, _VP], _I),
+    "pvconv_devoxelize_backward_workspace_size": ([_I, _I, _I, _I], _SZ),
+    "pvconv_devoxelize_backward": ([_VP, _I, _I, _I, _I, _VP, _VP, _VP, _SZ, _VP], _I),
+    "pvconv_devoxelize_nearest_backward": ([_VP, _I, _I, _I, _I, _VP, _VP, _VP, _SZ, _VP], _I),
     "pvconv_conv3d_backward_data_workspace_size": ([_I, _I, _I], _SZ),
     "pvconv_conv3d_backward_data": ([_VP, _I, _I, _I, _I, _VP, _I, _VP, _I, _VP, _SZ, _VP],
                                     _I),
@@ -481,23 +482,34 @@ def pvconv_voxelize_backward(dgrid: torch.Tensor, R: int, vox_id: torch.Tensor,
     return out
 
 
-def pvconv_devoxelize_backward(dout: torch.Tensor, R: int, norm_coords: torch.Tensor, out=None):
+def _devox_bwd_ws(B: int, N: int, C: int, R: int, device, workspace):
+    wsb = _lib.pvconv_devoxelize_backward_workspace_size(B, N, C, R)
+    if workspace is not None and workspace.numel() >= wsb:
+        return workspace, wsb
+    return torch.empty(max(wsb, 256), dtype=torch.uint8, device=device), wsb
+
+
+def pvconv_devoxelize_backward(dout: torch.Tensor, R: int, norm_coords: torch.Tensor, out=None,
+                               workspace=None):
     """dout [B][N][C] f32 -> dgrid [B][R^3][C] f32 (trilinear weights, transposed)."""
     B, N, C = dout.shape
     out = _out(out, (B, R ** 3, C), torch.float32, dout.device, "out")
+    ws, wsb = _devox_bwd_ws(B, N, C, R, dout.device, workspace)
     _check("pvconv_devoxelize_backward", _lib.pvconv_devoxelize_backward(
-        _p(dout.contiguous()), B, N, C, R, _p(norm_coords.contiguous()), _p(out),
+        _p(dout.contiguous()), B, N, C, R, _p(norm_coords.contiguous()), _p(out), _p(ws), wsb,
         _stream(dout)))
     return out
 
 
 def pvconv_devoxelize_nearest_backward(dout: torch.Tensor, R: int, vox_id: torch.Tensor,
-                                       out=None):
+                                       out=None, workspace=None):
     """dout [B][N][C] f32 -> dgrid [B][R^3][C] f32 (each point's gradient to its cell)."""
     B, N, C = dout.shape
     out = _out(out, (B, R ** 3, C), torch.float32, dout.device, "out")
+    ws, wsb = _devox_bwd_ws(B, N, C, R, dout.device, workspace)
     _check("pvconv_devoxelize_nearest_backward", _lib.pvconv_devoxelize_nearest_backward(
-        _p(dout.contiguous()), B, N, C, R, _p(vox_id.contiguous()), _p(out), _stream(dout)))
+        _p(dout.contiguous()), B, N, C, R, _p(vox_id.contiguous()), _p(out), _p(ws), wsb,
+        _stream(dout)))
     return out
 
 

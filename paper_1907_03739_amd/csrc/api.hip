@@ -635,9 +635,14 @@ pvconv_status pvconv_voxelize_backward(const void* dgrid, pvconv_dtype dt, int B
                                        dfeats, as_stream(stream));
 }
 
+size_t pvconv_devoxelize_backward_workspace_size(int B, int N, int C, int R) {
+    if (B < 0 || N < 0 || C < 1 || R < 1 || R > PVCONV_MAX_R || !sizes_fit(B, N)) return 0;
+    return pv_devox_bwd_ws_bytes(B, N, C, R);
+}
+
 static pvconv_status devox_backward(const float* dout, int B, int N, int C, int R,
                                     const float* pn, const int32_t* ids, float* dgrid,
-                                    void* stream) {
+                                    void* workspace, size_t workspace_bytes, void* stream) {
     if (B < 0 || N < 0 || C < 1 || R < 1 || R > PVCONV_MAX_R || !sizes_fit(B, N))
         return PVCONV_EINVAL;
     if (B == 0) return PVCONV_OK;
@@ -645,20 +650,28 @@ static pvconv_status devox_backward(const float* dout, int B, int N, int C, int 
     if (((uintptr_t)dout & 3) || ((uintptr_t)pn & 3) || ((uintptr_t)ids & 3) ||
         ((uintptr_t)dgrid & 3))
         return PVCONV_EINVAL;
-    return pv_launch_devoxelize_backward(dout, B, N, C, R, pn, ids, dgrid, as_stream(stream));
+    if (N > 0 && (!workspace || ((uintptr_t)workspace & 255) ||
+                  workspace_bytes < pv_devox_bwd_ws_bytes(B, N, C, R)))
+        return PVCONV_EWORKSPACE;
+    return pv_launch_devoxelize_backward(dout, B, N, C, R, pn, ids, dgrid, workspace,
+                                         as_stream(stream));
 }
 
 pvconv_status pvconv_devoxelize_backward(const float* dout, int B, int N, int C, int R,
-                                         const float* norm_coords, float* dgrid, void* stream) {
+                                         const float* norm_coords, float* dgrid, void* workspace,
+                                         size_t workspace_bytes, void* stream) {
     if (B > 0 && N > 0 && !norm_coords) return PVCONV_EINVAL;
-    return devox_backward(dout, B, N, C, R, norm_coords, nullptr, dgrid, stream);
+    return devox_backward(dout, B, N, C, R, norm_coords, nullptr, dgrid, workspace,
+                          workspace_bytes, stream);
 }
 
 pvconv_status pvconv_devoxelize_nearest_backward(const float* dout, int B, int N, int C, int R,
                                                  const int32_t* vox_id, float* dgrid,
+                                                 void* workspace, size_t workspace_bytes,
                                                  void* stream) {
     if (B > 0 && N > 0 && !vox_id) return PVCONV_EINVAL;
-    return devox_backward(dout, B, N, C, R, nullptr, vox_id, dgrid, stream);
+    return devox_backward(dout, B, N, C, R, nullptr, vox_id, dgrid, workspace, workspace_bytes,
+                          stream);
 }
 
 size_t pvconv_conv3d_backward_data_workspace_size(int Cin, int Cout, pvconv_dtype dt) {

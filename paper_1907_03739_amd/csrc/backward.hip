@@ -7,11 +7,13 @@
 //  * voxelise backward is a gather: each point reads its voxel's gradient row
 //    and divides by the voxel's count (one item per point and 8 channels, as
 //    in the devoxelise gather);
-//  * devoxelise backward is a scatter-add onto the grid: the gradient grid is
-//    cleared by a fill kernel, then every (point, corner, channel) adds its
-//    weighted gradient with a hardware fp32 atomic (global_atomic_add_f32),
-//    one channel per lane. The order of the adds, and so the last bits of the
-//    sums, vary between runs;
+//  * devoxelise backward, the adjoint of a gather, is computed as a gather
+//    too, so that every grid row is written once and its sum is taken in a
+//    fixed order: the points are sorted stably by the cell of their base
+//    corner (the lower of the two trilinear cells on every axis; nearest:
+//    their voxel) with a radix sort, each cell's range of the sorted list is
+//    recorded, and each cell then sums the weighted gradients of the points
+//    whose base corner is the cell or its lower neighbour on some axes;
 //  * the convolution's input gradient is the forward convolution of the
 //    output gradient with the kernel mirrored through its centre and its
 //    channel axes swapped, W'[i][t][o] = W[o][26 - t][i]: a transform kernel
@@ -121,56 +123,305 @@ __device__ __forceinline__ Axis trilinear_axis(float x, int R) {
     return a;
 }
 
-// Scatter kernels: one (point, channel) item per lane, consecutive lanes on
-// consecutive channels of a point, so that every atomic instruction adds to
-// 64 consecutive floats of a cell row (6.5x faster than 8 channels per lane,
-// whose atomics touch 8 floats 32 bytes apart).
+// ---------------------------------------------------------------------------
+// Devoxelisation backward as a gather. A point's trilinear cells are, on
+// every axis, its base cell i0 and i1 = min(i0 + 1, R - 1), so the points
+// that reach cell (u, v, w) have base cells in {u-1, u} x {v-1, v} x
+// {w-1, w}. The points are sorted stably by (cloud, base cell) with an LSD
+// radix sort on 8-bit digits (one pass per digit of the cell index; the
+// clouds' entries stay in their own ranges); each cell's range in the
+// sorted list is recorded with, per sorted point, its eight corner weights
+// (as pv_devoxelize forms them: fp64 products rounded once) and its
+// gradient row (copied into sorted order), and the cells that some point
+// reaches are marked (a byte per cell). One workgroup per 64 consecutive
+// cells then writes their rows: zeros for unmarked cells, and for marked
+// ones the sum, over the cell's eight candidate base cells in a fixed order
+// and their points in index order, of the point's weight at this cell times
+// its gradient. The sum's order is fixed by the data, so the grid is the
+// same bits on every run. Nearest neighbour: the key is the voxel, one range
+// per cell, weight one.
+// ---------------------------------------------------------------------------
+constexpr int kSortChunk = 256;  // entries per sort workgroup (one wave)
 
-// dG[cell] += w(point, cell) * dout[point] over the point's 8 cells.
-__global__ __launch_bounds__(256) void pv_devoxelize_backward_kernel(
-    const float* __restrict__ dout, const float* __restrict__ pn, float* __restrict__ dgrid,
-    int N, int R, int C, size_t items) {
-    const size_t item = xcd_item(gridDim.x);
-    if (item >= items) return;
-    const size_t point = item / C;
-    const int c = (int)(item - point * C);
-    const size_t b = point / N;
-    const size_t V = (size_t)R * R * R;
-    const float* p = pn + point * 3;
-    const Axis ax = trilinear_axis(p[0], R), ay = trilinear_axis(p[1], R),
-               az = trilinear_axis(p[2], R);
-    const float v = dout[point * C + c];
-    float* base = dgrid + b * V * C + c;
+// Sort keys: the point's base cell (or voxel, clamped: an index outside the
+// grid is invalid input) and its entry index b*N + i; the cell ranges and
+// the reached-cell marks cleared.
+__global__ __launch_bounds__(256) void pv_devox_bwd_keys_kernel(
+    const float* __restrict__ pn, const int32_t* __restrict__ ids, int R, size_t E,
+    size_t ncells, uint32_t* __restrict__ key, int32_t* __restrict__ val,
+    int2* __restrict__ bounds, uint32_t* __restrict__ act) {
+    const size_t stride = (size_t)gridDim.x * 256;
+    const size_t t0 = (size_t)blockIdx.x * 256 + threadIdx.x;
+    for (size_t i = t0; i < E; i += stride) {
+        int cell;
+        if (ids) {
+            cell = min(max(ids[i], 0), R * R * R - 1);
+        } else {
+            const float* p = pn + i * 3;
+            cell = (trilinear_axis(p[0], R).i0 * R + trilinear_axis(p[1], R).i0) * R +
+                   trilinear_axis(p[2], R).i0;
+        }
+        key[i] = (uint32_t)cell;
+        val[i] = (int32_t)i;
+    }
+    for (size_t k = t0; k < ncells; k += stride) bounds[k] = make_int2(0, 0);
+    for (size_t k = t0; k < (ncells + 3) / 4; k += stride) act[k] = 0u;
+}
+
+// Radix pass, 1/3: each chunk's histogram of the digit (key >> shift) & 255,
+// stored digit-major per cloud: hist[b][digit][chunk]. Workgroup b*nch + j
+// takes chunk j of cloud b (so do the scatter's).
+__global__ __launch_bounds__(64) void pv_radix_hist_kernel(const uint32_t* __restrict__ key,
+                                                           int N, int nch, int shift,
+                                                           uint32_t* __restrict__ hist) {
+    __shared__ uint32_t h[256];
+    const int j = (int)(blockIdx.x % nch), b = (int)(blockIdx.x / nch), lane = threadIdx.x;
+    for (int d = lane; d < 256; d += 64) h[d] = 0u;
+    __syncthreads();
+    const uint32_t* kb = key + (size_t)b * N;
+    const int i1 = min(N, (j + 1) * kSortChunk);
+    for (int i = j * kSortChunk + lane; i < i1; i += 64) atomicAdd(&h[(kb[i] >> shift) & 255u], 1u);
+    __syncthreads();
+    for (int d = lane; d < 256; d += 64) hist[((size_t)b * 256 + d) * nch + j] = h[d];
+}
+
+// Radix pass, 2/3: per cloud, the exclusive prefix of hist in (digit,
+// chunk) order, plus the cloud's first entry: where each chunk's entries of
+// each digit start in the output.
+__global__ __launch_bounds__(256) void pv_radix_scan_kernel(uint32_t* __restrict__ hist, int N,
+                                                            int nch) {
+    __shared__ uint32_t s[256];
+    const int b = blockIdx.x, d = threadIdx.x;
+    uint32_t* row = hist + ((size_t)b * 256 + d) * nch;
+    uint32_t t = 0;
+    for (int j = 0; j < nch; j++) t += row[j];
+    s[d] = t;
+    __syncthreads();
+    for (int off = 1; off < 256; off <<= 1) {  // inclusive prefix over the digits
+        const uint32_t v = d >= off ? s[d - off] : 0u;
+        __syncthreads();
+        s[d] += v;
+        __syncthreads();
+    }
+    uint32_t run = s[d] - t + (uint32_t)((size_t)b * N);
+    for (int j = 0; j < nch; j++) {
+        const uint32_t c = row[j];
+        row[j] = run;
+        run += c;
+    }
+}
+
+// Radix pass, 3/3: each chunk moves its entries, in order, to their digit's
+// place: the lanes of a round that share a digit (found with one ballot per
+// digit bit) take consecutive places in lane order after the chunk's earlier
+// entries of that digit. Stable, so after the last pass the entries of a
+// cell are in index order.
+__global__ __launch_bounds__(64) void pv_radix_scatter_kernel(
+    const uint32_t* __restrict__ kin, const int32_t* __restrict__ vin,
+    uint32_t* __restrict__ kout, int32_t* __restrict__ vout, const uint32_t* __restrict__ hist,
+    int N, int nch, int shift) {
+    __shared__ uint32_t run[256];
+    const int j = (int)(blockIdx.x % nch), b = (int)(blockIdx.x / nch), lane = threadIdx.x;
+    for (int d = lane; d < 256; d += 64) run[d] = hist[((size_t)b * 256 + d) * nch + j];
+    __syncthreads();
+    const size_t cb = (size_t)b * N;
+    const uint64_t below = (1ull << lane) - 1ull;
+    const int i1 = min(N, (j + 1) * kSortChunk);
+    for (int r = j * kSortChunk; r < i1; r += 64) {
+        const int i = r + lane;
+        const bool ok = i < i1;
+        const uint32_t k = ok ? kin[cb + i] : 0u;
+        const int32_t v = ok ? vin[cb + i] : 0;
+        const uint32_t d = (k >> shift) & 255u;
+        uint64_t peers = __ballot(ok);
 #pragma unroll
-    for (int a = 0; a < 2; a++) {
-        const int iu = a ? ax.i1 : ax.i0;
-        const double wu = a ? ax.w1 : ax.w0;
+        for (int bit = 0; bit < 8; bit++) {
+            const uint64_t m = __ballot((d >> bit) & 1u);
+            peers &= ((d >> bit) & 1u) ? m : ~m;
+        }
+        if (ok) {
+            const uint32_t pos = run[d] + (uint32_t)__popcll(peers & below);
+            kout[pos] = k;
+            vout[pos] = v;
+        }
+        __syncthreads();  // every lane has read its digit's place
+        if (ok && (peers & below) == 0ull) run[d] += (uint32_t)__popcll(peers);
+        __syncthreads();
+    }
+}
+
+// Each cell's range [first, last + 1) in the sorted list (cells without
+// points keep the cleared [0, 0)), the cells the points reach, marked, and
+// (trilinear) per sorted entry its eight corner weights as pv_devoxelize
+// forms them, corner (a, b, c) = offsets (0/1) from the base cell at
+// 4a + 2b + c: fp64 products, rounded once. Where both corners of an axis are the grid's last
+// cell, the upper one's weight is 0.
+__global__ __launch_bounds__(256) void pv_devox_bwd_bounds_kernel(
+    const uint32_t* __restrict__ key, const int32_t* __restrict__ val,
+    const float* __restrict__ pn, int N, size_t E, int R, int2* __restrict__ bounds,
+    float4* __restrict__ rec_w, uint8_t* __restrict__ act) {
+    const size_t stride = (size_t)gridDim.x * 256;
+    const int V = R * R * R;
+    for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < E; i += stride) {
+        const size_t b = i / N;
+        const int in = (int)(i - b * N);
+        const uint32_t k = key[i];
+        int2* bd = bounds + b * V + k;
+        if (in == 0 || key[i - 1] != k) bd->x = (int)i;
+        if (in == N - 1 || key[i + 1] != k) bd->y = (int)(i + 1);
+        const int e = val[i];
+        // the cells this point reaches, marked (every writer stores 1)
+        const int ku = (int)(k / (uint32_t)(R * R)), kv = (int)(k / (uint32_t)R) % R,
+                  kw = (int)(k % (uint32_t)R);
+        for (int c = 0; c < (pn ? 8 : 1); c++) {
+            const int cu = min(ku + (c >> 2), R - 1), cv = min(kv + ((c >> 1) & 1), R - 1),
+                      cw = min(kw + (c & 1), R - 1);
+            act[b * V + ((size_t)cu * R + cv) * R + cw] = 1;
+        }
+        if (pn) {
+            const float* p = pn + (size_t)e * 3;
+            const Axis ax = trilinear_axis(p[0], R), ay = trilinear_axis(p[1], R),
+                       az = trilinear_axis(p[2], R);
+            float wt[8];
 #pragma unroll
-        for (int e = 0; e < 2; e++) {
-            const int iv = e ? ay.i1 : ay.i0;
-            const double wv = e ? ay.w1 : ay.w0;
-#pragma unroll
-            for (int f = 0; f < 2; f++) {
-                const int iw = f ? az.i1 : az.i0;
-                const float wt = (float)((wu * wv) * (f ? az.w1 : az.w0));
-                unsafeAtomicAdd(base + (((size_t)iu * R + iv) * R + iw) * C, wt * v);
-            }
+            for (int c = 0; c < 8; c++)
+                wt[c] = (float)(((c & 4 ? ax.w1 : ax.w0) * (c & 2 ? ay.w1 : ay.w0)) *
+                                (c & 1 ? az.w1 : az.w0));
+            rec_w[2 * i] = make_float4(wt[0], wt[1], wt[2], wt[3]);
+            rec_w[2 * i + 1] = make_float4(wt[4], wt[5], wt[6], wt[7]);
         }
     }
 }
 
-// dG[id_k] += dout[k]. An index outside the grid is clamped (invalid input).
-__global__ __launch_bounds__(256) void pv_devoxelize_nearest_backward_kernel(
-    const float* __restrict__ dout, const int32_t* __restrict__ ids, float* __restrict__ dgrid,
-    int N, int R, int C, size_t items) {
-    const size_t item = xcd_item(gridDim.x);
-    if (item >= items) return;
-    const size_t point = item / C;
-    const int c = (int)(item - point * C);
-    const size_t b = point / N;
-    const int V = R * R * R;
-    const int id = min(max(ids[point], 0), V - 1);
-    unsafeAtomicAdd(dgrid + (b * V + id) * C + c, dout[point * C + c]);
+// The gradient rows in sorted order: srow[i] = dout[val[i]], VW floats per
+// item.
+template <int VW>
+__global__ __launch_bounds__(256) void pv_devox_bwd_rows_kernel(const float* __restrict__ dout,
+                                                                const int32_t* __restrict__ val,
+                                                                int C, size_t items,
+                                                                float* __restrict__ srow) {
+    const int per = C / VW;
+    const size_t stride = (size_t)gridDim.x * 256;
+    for (size_t it = (size_t)blockIdx.x * 256 + threadIdx.x; it < items; it += stride) {
+        const size_t i = it / per;
+        const int q = (int)(it - i * per);
+        const float* src = dout + (size_t)val[i] * C + q * VW;
+        float* dst = srow + i * C + q * VW;
+        if constexpr (VW == 4)
+            *(float4*)dst = *(const float4*)src;
+        else
+            *dst = *src;
+    }
+}
+
+// x / d for 0 <= x < 2^24 and d >= 1, with inv = 1/d in fp32: the product's
+// floor is the quotient or one off it, corrected with the remainder.
+__device__ __forceinline__ int pv_div_small(int x, int d, float inv, int* rem) {
+    int q = (int)((float)x * inv);
+    int r = x - q * d;
+    if (r < 0) {
+        q--;
+        r += d;
+    } else if (r >= d) {
+        q++;
+        r -= d;
+    }
+    *rem = r;
+    return q;
+}
+
+// dG rows: workgroup x takes cells x*64 .. x*64 + 63 (of all clouds' cells
+// in order); every wave reads their marks, so all know which are reached.
+// Items (cell j, channel group q) = threadIdx.x, + 256, ... (walked by
+// constant steps, no divisions): unmarked cells' rows are written as
+// zeros, marked ones as their sums.
+template <int VW, bool NEAREST>
+__global__ __launch_bounds__(256) void pv_devox_bwd_gather_kernel(
+    const float* __restrict__ srow, const float* __restrict__ rec_w,
+    const int2* __restrict__ bounds, const uint8_t* __restrict__ act, size_t ncells, int R,
+    int C, float* __restrict__ dgrid) {
+    const int per = C / VW;
+    const int V = R * R * R, RR = R * R;
+    const float invR = 1.f / (float)R, invRR = 1.f / (float)RR;
+    const int lane = threadIdx.x & 63;
+    const int j0 = (int)threadIdx.x / per, q0 = (int)threadIdx.x - j0 * per;
+    const int dj = 256 / per, dq = 256 - dj * per;
+    for (size_t c0 = (size_t)blockIdx.x * 64; c0 < ncells; c0 += (size_t)gridDim.x * 64) {
+        const uint64_t marked = __ballot(c0 + lane < ncells && act[c0 + lane] != 0);
+        const int nc = (int)std::min<size_t>(64, ncells - c0);
+        const size_t b0 = c0 / (size_t)V;  // the chunk's first cell: cloud and index
+        const int cell0 = (int)(c0 - b0 * V);
+        int j = j0, q = q0;
+        while (j < nc) {
+            const size_t cg = c0 + j;
+            float acc[VW];
+#pragma unroll
+            for (int k = 0; k < VW; k++) acc[k] = 0.f;
+            if ((marked >> j) & 1ull) {
+                int cell = cell0 + j;
+                size_t b = b0;
+                while (cell >= V) {  // the chunk runs into the next cloud
+                    cell -= V;
+                    b++;
+                }
+                if (NEAREST) {
+                    const int2 rg = bounds[cg];
+#pragma unroll 2
+                    for (int sidx = rg.x; sidx < rg.y; sidx++) {
+                        const float* src = srow + (size_t)sidx * C + q * VW;
+                        if constexpr (VW == 4) {
+                            const float4 x = *(const float4*)src;
+                            acc[0] += x.x; acc[1] += x.y; acc[2] += x.z; acc[3] += x.w;
+                        } else {
+                            acc[0] += *src;
+                        }
+                    }
+                } else {
+                    int rr, w;
+                    const int u = pv_div_small(cell, RR, invRR, &rr);
+                    const int v = pv_div_small(rr, R, invR, &w);
+                    // the base cells (u - 1 .. u, v - 1 .. v, w - 1 .. w) in
+                    // index order, whose points reach this cell through their
+                    // corner 7 - t; their ranges loaded together
+                    const int2* bc = bounds + b * V + ((u - 1) * R + (v - 1)) * R + (w - 1);
+                    int2 rgs[8];
+#pragma unroll
+                    for (int t = 0; t < 8; t++) {
+                        const bool in =
+                            ((t & 4) || u > 0) && ((t & 2) || v > 0) && ((t & 1) || w > 0);
+                        rgs[t] = in ? bc[(t >> 2) * RR + ((t >> 1) & 1) * R + (t & 1)]
+                                    : make_int2(0, 0);
+                    }
+#pragma unroll
+                    for (int t = 0; t < 8; t++) {
+#pragma unroll 2
+                        for (int sidx = rgs[t].x; sidx < rgs[t].y; sidx++) {
+                            const float wt = rec_w[(size_t)sidx * 8 + (7 - t)];
+                            const float* src = srow + (size_t)sidx * C + q * VW;
+                            if constexpr (VW == 4) {
+                                const float4 x = *(const float4*)src;
+                                acc[0] += wt * x.x; acc[1] += wt * x.y;
+                                acc[2] += wt * x.z; acc[3] += wt * x.w;
+                            } else {
+                                acc[0] += wt * *src;
+                            }
+                        }
+                    }
+                }
+            }
+            float* dst = dgrid + cg * C + q * VW;
+            if constexpr (VW == 4)
+                *(float4*)dst = make_float4(acc[0], acc[1], acc[2], acc[3]);
+            else
+                dst[0] = acc[0];
+            j += dj;
+            q += dq;
+            if (q >= per) {
+                q -= per;
+                j++;
+            }
+        }
+    }
 }
 
 // W'[i][t][o] = W[o][26 - t][i]: the kernel mirrored through its centre
@@ -498,20 +749,97 @@ pvconv_status pv_launch_voxelize_backward(const void* dgrid, bool bf16, int B, i
     return pv_launch_status();
 }
 
+namespace {
+struct DevoxBwdWs {
+    uint32_t* key[2];
+    int32_t* val[2];
+    uint32_t* hist;  // [B][256][chunks per cloud]
+    int2* bounds;    // [B * R^3]
+    float4* rec_w;   // [B * N][2] their corner weights (trilinear)
+    uint8_t* act;    // [B * R^3] cells some point reaches (rounded up to 4 bytes)
+    float* srow;     // [B * N][C] gradient rows in sorted order
+};
+
+size_t devox_bwd_layout(int B, int N, int C, int R, char* base, DevoxBwdWs* ws) {
+    const size_t E = (size_t)B * N, V = (size_t)R * R * R;
+    const size_t nch = ((size_t)N + kSortChunk - 1) / kSortChunk;
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        char* p = base ? base + off : nullptr;
+        off += pv_align256(bytes);
+        return p;
+    };
+    for (int i = 0; i < 2; i++) {
+        ws->key[i] = (uint32_t*)take(E * 4);
+        ws->val[i] = (int32_t*)take(E * 4);
+    }
+    ws->hist = (uint32_t*)take((size_t)B * 256 * nch * 4);
+    ws->bounds = (int2*)take((size_t)B * V * sizeof(int2));
+    ws->rec_w = (float4*)take(E * 2 * sizeof(float4));
+    ws->act = (uint8_t*)take(((size_t)B * V + 3) / 4 * 4);
+    ws->srow = (float*)take(E * (size_t)C * 4);
+
+    return off;
+}
+}  // namespace
+
+size_t pv_devox_bwd_ws_bytes(int B, int N, int C, int R) {
+    DevoxBwdWs ws;
+    return devox_bwd_layout(B, N, C, R, nullptr, &ws);
+}
+
 pvconv_status pv_launch_devoxelize_backward(const float* dout, int B, int N, int C, int R,
                                             const float* pn, const int32_t* ids, float* dgrid,
-                                            hipStream_t s) {
+                                            void* workspace, hipStream_t s) {
     if (B == 0) return PVCONV_OK;
-    const size_t gn = (size_t)B * R * R * R * C;
-    hipLaunchKernelGGL(pv_fill_zero_kernel, dim3(fill_blocks(gn)), dim3(256), 0, s, dgrid, gn);
-    if (N == 0) return pv_launch_status();
-    const size_t items = (size_t)B * N * C;
-    if (ids)
-        hipLaunchKernelGGL(pv_devoxelize_nearest_backward_kernel, dim3(blocks_for(items)),
-                           dim3(256), 0, s, dout, ids, dgrid, N, R, C, items);
+    const size_t V = (size_t)R * R * R;
+    const size_t gn = (size_t)B * V * C;
+    if (N == 0) {
+        hipLaunchKernelGGL(pv_fill_zero_kernel, dim3(fill_blocks(gn)), dim3(256), 0, s, dgrid, gn);
+        return pv_launch_status();
+    }
+    DevoxBwdWs ws;
+    devox_bwd_layout(B, N, C, R, (char*)workspace, &ws);
+    const size_t E = (size_t)B * N;
+    const int nch = (N + kSortChunk - 1) / kSortChunk;
+    const size_t ncells = (size_t)B * V;
+    const unsigned kb = (unsigned)std::min<size_t>((std::max(E, ncells) + 255) / 256, 4096);
+    hipLaunchKernelGGL(pv_devox_bwd_keys_kernel, dim3(kb), dim3(256), 0, s, pn, ids, R, E, ncells,
+                       ws.key[0], ws.val[0], ws.bounds, (uint32_t*)ws.act);
+    // one pass per 8-bit digit of the largest cell index
+    int cur = 0;
+    for (int shift = 0; shift == 0 || ((V - 1) >> shift) != 0; shift += 8) {
+        hipLaunchKernelGGL(pv_radix_hist_kernel, dim3(B * nch), dim3(64), 0, s, ws.key[cur], N, nch,
+                           shift, ws.hist);
+        hipLaunchKernelGGL(pv_radix_scan_kernel, dim3(B), dim3(256), 0, s, ws.hist, N, nch);
+        hipLaunchKernelGGL(pv_radix_scatter_kernel, dim3(B * nch), dim3(64), 0, s, ws.key[cur],
+                           ws.val[cur], ws.key[cur ^ 1], ws.val[cur ^ 1], ws.hist, N, nch, shift);
+        cur ^= 1;
+    }
+    hipLaunchKernelGGL(pv_devox_bwd_bounds_kernel, dim3(std::min<size_t>(blocks_for(E), 4096)),
+                       dim3(256), 0, s, ws.key[cur], ws.val[cur], ids ? nullptr : pn, N, E, R,
+                       ws.bounds, ws.rec_w, ws.act);
+    const bool vec = C % 4 == 0 && ((uintptr_t)dout & 15) == 0 && ((uintptr_t)dgrid & 15) == 0;
+    const size_t rows = E * (size_t)(vec ? C / 4 : C);
+    const unsigned rb = (unsigned)std::min<size_t>((rows + 255) / 256, 8192);
+    if (vec)
+        hipLaunchKernelGGL(pv_devox_bwd_rows_kernel<4>, dim3(rb), dim3(256), 0, s, dout,
+                           ws.val[cur], C, rows, ws.srow);
     else
-        hipLaunchKernelGGL(pv_devoxelize_backward_kernel, dim3(blocks_for(items)), dim3(256), 0,
-                           s, dout, pn, dgrid, N, R, C, items);
+        hipLaunchKernelGGL(pv_devox_bwd_rows_kernel<1>, dim3(rb), dim3(256), 0, s, dout,
+                           ws.val[cur], C, rows, ws.srow);
+    const unsigned gb = (unsigned)std::min<size_t>((ncells + 63) / 64, (size_t)1 << 20);
+#define PV_DEVOX_BWD(VW, NEAR)                                                                   \
+    hipLaunchKernelGGL((pv_devox_bwd_gather_kernel<VW, NEAR>), dim3(gb), dim3(256), 0, s, ws.srow, \
+                       (const float*)ws.rec_w, ws.bounds, ws.act, ncells, R, C, dgrid)
+    if (vec) {
+        if (ids) PV_DEVOX_BWD(4, true);
+        else PV_DEVOX_BWD(4, false);
+    } else {
+        if (ids) PV_DEVOX_BWD(1, true);
+        else PV_DEVOX_BWD(1, false);
+    }
+#undef PV_DEVOX_BWD
     return pv_launch_status();
 }
 

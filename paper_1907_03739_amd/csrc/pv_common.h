@@ -230,10 +230,12 @@ size_t pv_conv3d_bwd_data_ws_bytes(int Cin, int Cout, bool bf16);
 pvconv_status pv_launch_voxelize_backward(const void* dgrid, bool bf16, int B, int N, int C,
                                           int R, const int32_t* ids, const int32_t* counts,
                                           float* dfeats, hipStream_t s);
-// ids != NULL: nearest neighbour (pn unused), else trilinear
+// ids != NULL: nearest neighbour (pn unused), else trilinear; workspace of
+// pv_devox_bwd_ws_bytes (256-byte aligned; unused when N == 0)
+size_t pv_devox_bwd_ws_bytes(int B, int N, int C, int R);
 pvconv_status pv_launch_devoxelize_backward(const float* dout, int B, int N, int C, int R,
                                             const float* pn, const int32_t* ids, float* dgrid,
-                                            hipStream_t s);
+                                            void* workspace, hipStream_t s);
 pvconv_status pv_launch_conv3d_backward_data(const void* dy, int B, int R, int Cin, int Cout,
                                              const void* w, bool bf16, void* dx, bool dx_bf16,
                                              void* ws, hipStream_t s);

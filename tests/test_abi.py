@@ -30,7 +30,7 @@ def declared_functions():
 
 def test_library_exports_every_declared_symbol():
     names = declared_functions()
-    assert len(names) == 31
+    assert len(names) == 32
     out = subprocess.run(["nm", "-D", "--defined-only", b.LIB_PATH], capture_output=True,
                          text=True, check=True).stdout
     exported = set(re.findall(r"\bT (pvconv_\w+)", out))
@@ -62,6 +62,12 @@ def test_workspace_queries():
     assert L.pvconv_voxelize_workspace_size(-1, 10, 8) == 0
     assert L.pvconv_voxelize_workspace_size(1, 10, 0) == 0
     assert L.pvconv_voxelize_workspace_size(1, 10, 129) == 0
+    # the devoxelisation backward's sort: keys and entries twice, the cell ranges
+    assert L.pvconv_devoxelize_backward_workspace_size(16, 2048, 128, 32) >= \
+        16 * 2048 * (16 + 128 * 4) + 16 * 32 ** 3 * 8
+    assert L.pvconv_devoxelize_backward_workspace_size(-1, 10, 8, 8) == 0
+    assert L.pvconv_devoxelize_backward_workspace_size(1, 10, 0, 8) == 0
+    assert L.pvconv_devoxelize_backward_workspace_size(1, 10, 8, 129) == 0
     lay = _layer()
     need = L.pvconv_forward_workspace_size(16, 2048, ctypes.byref(lay))
     # at least: two bf16 grids of 128 channels + the fp32 devox buffer
@@ -343,15 +349,27 @@ def _fwd_ex(lay, **kw):
     (lambda: L.pvconv_voxelize_backward(FAKE, 1, 2, 10, 16, 8, FAKE, FAKE, FAKE_ODD, None),
      EINVAL),
     (lambda: L.pvconv_voxelize_backward(FAKE, 1, 0, 10, 16, 8, FAKE, FAKE, FAKE, None), OK),
-    (lambda: L.pvconv_devoxelize_backward(FAKE, 2, 10, 16, 129, FAKE, FAKE, None), EINVAL),
-    (lambda: L.pvconv_devoxelize_backward(FAKE, 2, 10, 16, 8, None, FAKE, None), EINVAL),
-    (lambda: L.pvconv_devoxelize_backward(FAKE, 2, 10, 16, 8, FAKE, None, None), EINVAL),
-    (lambda: L.pvconv_devoxelize_backward(FAKE_ODD, 2, 10, 16, 8, FAKE, FAKE, None), EINVAL),
-    (lambda: L.pvconv_devoxelize_backward(FAKE, 0, 10, 16, 8, FAKE, FAKE, None), OK),
-    (lambda: L.pvconv_devoxelize_nearest_backward(FAKE, 2, 10, 16, 8, None, FAKE, None),
+    (lambda: L.pvconv_devoxelize_backward(FAKE, 2, 10, 16, 129, FAKE, FAKE, FAKE, 1 << 40,
+                                          None), EINVAL),
+    (lambda: L.pvconv_devoxelize_backward(FAKE, 2, 10, 16, 8, None, FAKE, FAKE, 1 << 40, None),
      EINVAL),
-    (lambda: L.pvconv_devoxelize_nearest_backward(FAKE, 2, -1, 16, 8, FAKE, FAKE, None),
+    (lambda: L.pvconv_devoxelize_backward(FAKE, 2, 10, 16, 8, FAKE, None, FAKE, 1 << 40, None),
      EINVAL),
+    (lambda: L.pvconv_devoxelize_backward(FAKE_ODD, 2, 10, 16, 8, FAKE, FAKE, FAKE, 1 << 40,
+                                          None), EINVAL),
+    (lambda: L.pvconv_devoxelize_backward(FAKE, 2, 10, 16, 8, FAKE, FAKE, None, 1 << 40, None),
+     EWS),
+    (lambda: L.pvconv_devoxelize_backward(FAKE, 2, 10, 16, 8, FAKE, FAKE, FAKE_ODD, 1 << 40,
+                                          None), EWS),
+    (lambda: L.pvconv_devoxelize_backward(FAKE, 2, 10, 16, 8, FAKE, FAKE, FAKE, 256, None),
+     EWS),
+    (lambda: L.pvconv_devoxelize_backward(FAKE, 0, 10, 16, 8, FAKE, FAKE, None, 0, None), OK),
+    (lambda: L.pvconv_devoxelize_nearest_backward(FAKE, 2, 10, 16, 8, None, FAKE, FAKE, 1 << 40,
+                                                  None), EINVAL),
+    (lambda: L.pvconv_devoxelize_nearest_backward(FAKE, 2, -1, 16, 8, FAKE, FAKE, FAKE, 1 << 40,
+                                                  None), EINVAL),
+    (lambda: L.pvconv_devoxelize_nearest_backward(FAKE, 2, 10, 16, 8, FAKE, FAKE, None, 0,
+                                                  None), EWS),
     (lambda: L.pvconv_conv3d_backward_data(FAKE, 2, 8, 48, 64, FAKE, 1, FAKE, 0, FAKE, 1 << 40,
                                            None), ENOTSUP),
     (lambda: L.pvconv_conv3d_backward_data(FAKE, 2, 8, 64, 64, FAKE, 1, FAKE2, 0, None, 0, None),

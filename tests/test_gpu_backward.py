@@ -62,7 +62,7 @@ def test_devoxelize_backward_matches_oracle(wl_idx, B, N, R, C):
     pn32 = pn.astype(np.float32)
     rng = np.random.default_rng(3 * R + C)
     dout = rng.normal(size=(B, N, C)).astype(np.float32).astype(np.float64)
-    # trilinear: atomics in any order, fp32 sums
+    # trilinear: fp32 sums in the kernel's fixed order
     ref = oracle.devoxelize_backward(dout, R, pn32)
     mag = oracle.devoxelize_backward(np.abs(dout), R, pn32)
     dirty = torch.full((B, R ** 3, C), float("nan"), device="cuda")
@@ -73,6 +73,73 @@ def test_devoxelize_backward_matches_oracle(wl_idx, B, N, R, C):
     mag = oracle.devoxelize_nearest_backward(np.abs(dout), R, ids)
     got = pv.pvconv_devoxelize_nearest_backward(dev(dout), R, _i32(ids), out=dirty)
     assert_dot_f32(host(got), ref, mag, "nearest devoxelize backward")
+
+
+DEVOX_BWD_EDGES = [
+    # B, N, R, C, cloud: a one-cell grid (every corner clamped onto it), points
+    # on the grid's faces and corners (both corners of an axis clamped to one
+    # cell), clouds spanning several sort chunks with ragged ends, three radix
+    # passes (R = 64), channel rows of 1 and 3 floats
+    (2, 300, 1, 4, "uniform"),
+    (3, 700, 5, 3, "faces"),
+    (2, 2500, 16, 8, "uniform"),
+    (1, 3000, 64, 1, "faces"),
+    (4, 1025, 7, 12, "uniform"),
+]
+
+
+def _cloud(kind, B, N, seed):
+    rng = np.random.default_rng(seed)
+    pn = rng.uniform(0.0, 1.0, size=(B, N, 3))
+    if kind == "faces":  # a third of the coordinates exactly on 0 or 1
+        m = rng.uniform(size=pn.shape) < 0.33
+        pn[m] = rng.integers(0, 2, size=int(m.sum()))
+    return pn.astype(np.float32)
+
+
+@pytest.mark.parametrize("B,N,R,C,kind", DEVOX_BWD_EDGES)
+def test_devoxelize_backward_edges_and_repeatability(B, N, R, C, kind):
+    pn = _cloud(kind, B, N, N + R)
+    ids = np.clip(np.floor(pn.astype(np.float64) * R), 0, R - 1).astype(np.int64)
+    ids = ((ids[..., 0] * R + ids[..., 1]) * R + ids[..., 2]).astype(np.int32)
+    dout = np.random.default_rng(C).normal(size=(B, N, C)).astype(np.float32)
+    ws = torch.empty(pv._lib.pvconv_devoxelize_backward_workspace_size(B, N, C, R),
+                     dtype=torch.uint8, device="cuda")
+    for nearest in (False, True):
+        call = (lambda w: pv.pvconv_devoxelize_nearest_backward(dev(dout), R, _i32(ids),
+                                                                workspace=w)) if nearest else \
+               (lambda w: pv.pvconv_devoxelize_backward(dev(dout), R, dev(pn), workspace=w))
+        ws.fill_(0x5A)
+        first = call(ws)
+        ws.fill_(0xA7)  # the result does not depend on what the workspace held
+        again = call(ws)
+        assert torch.equal(first, again), "devoxelize backward is not repeatable"
+        d64 = dout.astype(np.float64)
+        ref = (oracle.devoxelize_nearest_backward(d64, R, ids) if nearest
+               else oracle.devoxelize_backward(d64, R, pn))
+        mag = (oracle.devoxelize_nearest_backward(np.abs(d64), R, ids) if nearest
+               else oracle.devoxelize_backward(np.abs(d64), R, pn))
+        assert_dot_f32(host(first), ref, mag, f"devoxelize backward (nearest={nearest})")
+
+
+def test_devoxelize_backward_unaligned_rows_and_no_points():
+    B, N, R, C = 2, 400, 6, 8
+    pn = _cloud("uniform", B, N, 5)
+    dout = np.random.default_rng(6).normal(size=(B, N, C)).astype(np.float32)
+    # rows that start 4 bytes past a 16-byte boundary take the channel-by-channel items
+    buf = torch.zeros(B * N * C + 1, dtype=torch.float32, device="cuda")
+    shifted = buf[1:].view(B, N, C)
+    shifted.copy_(dev(dout))
+    got = pv.pvconv_devoxelize_backward(shifted, R, dev(pn))
+    d64 = dout.astype(np.float64)
+    assert_dot_f32(host(got), oracle.devoxelize_backward(d64, R, pn),
+                   oracle.devoxelize_backward(np.abs(d64), R, pn), "unaligned rows")
+    assert torch.equal(got, pv.pvconv_devoxelize_backward(dev(dout), R, dev(pn)))
+    # no points: the whole gradient grid is zero
+    dirty = torch.full((B, R ** 3, C), float("nan"), device="cuda")
+    empty = pv.pvconv_devoxelize_backward(torch.zeros((B, 0, C), device="cuda"), R,
+                                          torch.zeros((B, 0, 3), device="cuda"), out=dirty)
+    assert torch.count_nonzero(empty).item() == 0 and not torch.isnan(empty).any()
 
 
 @pytest.mark.parametrize("B,R,Cin,Cout,dt", [
