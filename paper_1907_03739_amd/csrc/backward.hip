@@ -497,37 +497,43 @@ __global__ __launch_bounds__(256) void pv_act_bn_backward_kernel(
 // K = voxels. A workgroup (four waves) owns 64 output channels x one chunk of
 // 16 input channels x all 27 taps for a contiguous range of 8x8x8 bricks (a
 // split of the voxel sum); each split writes its partial sums, and a second
-// kernel adds the splits in split order. Per brick:
-//  * dy of the brick, transposed in LDS to [64 o][512 p]: an A fragment (8
-//    consecutive voxels, one w-row, of one channel) is one 16-byte read;
-//  * x of the brick's 10x10x10 halo for the 16 channels, transposed to
-//    [s][16 i][10][10][8] for s = 0, 1, 2: copy s holds the halo's w-window
-//    s .. s+7, so the B fragment of a tap with w-offset dw (a w-row of 8
-//    voxels shifted by dw) is one aligned 16-byte read of copy dw + 1.
-// A brick's global loads are issued together into registers while the
-// previous brick's MFMAs run, then written to LDS.
+// kernel adds the splits in split order. Per brick, both operands sit in LDS
+// as they lie in memory, voxel-major with channels fastest:
+//  * dy of the brick, [512 p][64 o] (128-byte rows; 64-byte halves swapped
+//    where bit 1 of p is set, so that the four consecutive rows one
+//    fragment read touches fall in distinct banks);
+//  * x of the brick's 10x10x10 halo for the 16 channels, [1000][16 i].
+// The MFMA fragments need the transposes (8 consecutive voxels of one
+// channel per lane). gfx950's transposing LDS read does that: each group of
+// 16 lanes names 16 pieces of 4 channels (4 voxels x 4 pieces), and lane
+// 4a + c receives channel 4a + c of the 4 voxels. Two such reads (voxels
+// k0 .. k0+3, k0+4 .. k0+7) make one 8-voxel fragment, for A (dy) and for B
+// (the halo shifted by the tap). A brick's global loads are issued together
+// into registers while the previous brick's MFMAs run, then written to LDS
+// with 16-byte stores.
 // The GEMM's columns pair the taps: column n of tap pair q is tap 2q + n/16,
 // input channel n % 16 (taps 27 .. 31 are padding: computed, never written).
 // Every wave owns both 32-channel blocks of the 64 and tap pairs w, w+4, w+8,
 // w+12.
 // Voxels outside the grid (ragged bricks, the halo's border) read as zero.
 constexpr int kWgO = 64;                              // output channels per workgroup
-constexpr int kDyPitch = 512 * 2 + 16;                // bytes per transposed dy row
-constexpr int kDyBytes = kWgO * kDyPitch;             // 66560
-// one (copy s, channel i) block of the halo: 10 x 10 w-windows of 8, padded
-// by 16 bytes so that the B reads of the 16 channels start in distinct banks
-constexpr int kXtBlock = 10 * 10 * 8 * 2 + 16;        // 1616
-constexpr int kXtBytes = 3 * 16 * kXtBlock;           // 77568
-constexpr int kWgradLds = kDyBytes + kXtBytes;        // 144128
-constexpr int kXtItems = 3 * 10 * 10 * 4;             // (s, hu, hv, w-pair)
-constexpr int kXtPer = (kXtItems + 255) / 256;        // 5 items per thread
+constexpr int kDyBytes = 512 * kWgO * 2;              // 65536
+constexpr int kXtBytes = 1000 * 16 * 2;               // 32000
+constexpr int kWgradLds = kDyBytes + kXtBytes;        // 97536
+constexpr int kXtPer = (1000 * 2 + 255) / 256;        // halo pieces (16 bytes) per thread: 8
 
-// A brick's operands in registers, between their global loads and their
-// transposing LDS writes: dy of voxels 2 tid, 2 tid + 1 (64 channels each)
-// and x of the thread's halo items (two voxels, 16 channels each).
+typedef short pv_i16x4 __attribute__((ext_vector_type(4)));
+
+// byte offset of channels [c, c + 8) of voxel p in the dy tile (c % 8 == 0,
+// or any channel offset within such a piece)
+__device__ __forceinline__ int wg_dy_off(int p, int cbyte) { return p * 128 + (cbyte ^ ((p & 2) << 5)); }
+
+// A brick's operands in registers, between their global loads and their LDS
+// stores: dy of voxels 2 tid, 2 tid + 1 (64 channels each), and halo pieces
+// tid + 256 k (piece = voxel * 2 + half of its 16 channels).
 struct WgradRegs {
     uint4 d0[8], d1[8];
-    uint4 x0[kXtPer][2], x1[kXtPer][2];
+    uint4 x[kXtPer];
 };
 
 __device__ __forceinline__ void wgrad_load(WgradRegs& g, const uint16_t* __restrict__ dy,
@@ -563,18 +569,12 @@ __device__ __forceinline__ void wgrad_load(WgradRegs& g, const uint16_t* __restr
     const uint16_t* xb = x + (size_t)b * V * Cin + i0;
 #pragma unroll
     for (int k = 0; k < kXtPer; k++) {
-        const int item = tid + 256 * k;
-        const int wp = item & 3, hv = (item >> 2) % 10, hu = (item / 40) % 10, sc = item / 400;
-        const int u = u0 + hu - 1, v = v0 + hv - 1, w = w0 + 2 * wp + sc - 1;
-        const bool uv = item < kXtItems && u >= 0 && u < R && v >= 0 && v < R;
-        const bool in0 = uv && w >= 0 && w < R, in1 = uv && w + 1 >= 0 && w + 1 < R;
-        const uint16_t* r0 = xb + (((size_t)cl(u) * R + cl(v)) * R + cl(w)) * Cin;
-        const uint16_t* r1 = xb + (((size_t)cl(u) * R + cl(v)) * R + cl(w + 1)) * Cin;
-#pragma unroll
-        for (int h = 0; h < 2; h++) {
-            g.x0[k][h] = sel(in0, *(const uint4*)(r0 + 8 * h));
-            g.x1[k][h] = sel(in1, *(const uint4*)(r1 + 8 * h));
-        }
+        const int piece = tid + 256 * k, h = piece >> 1, half = piece & 1;
+        const int hw = h % 10, hv = (h / 10) % 10, hu = h / 100;
+        const int u = u0 + hu - 1, v = v0 + hv - 1, w = w0 + hw - 1;
+        const bool in = piece < 2000 && u >= 0 && u < R && v >= 0 && v < R && w >= 0 && w < R;
+        g.x[k] = sel(in, *(const uint4*)(xb + (((size_t)cl(u) * R + cl(v)) * R + cl(w)) * Cin +
+                                         8 * half));
     }
 }
 
@@ -582,34 +582,25 @@ __device__ __forceinline__ void wgrad_store(const WgradRegs& g, char* ldy, char*
     const int tid = threadIdx.x, p = 2 * tid;
 #pragma unroll
     for (int q = 0; q < 8; q++) {
-        const uint32_t a[4] = {g.d0[q].x, g.d0[q].y, g.d0[q].z, g.d0[q].w};
-        const uint32_t c[4] = {g.d1[q].x, g.d1[q].y, g.d1[q].z, g.d1[q].w};
-#pragma unroll
-        for (int e = 0; e < 4; e++) {
-            const int o = 8 * q + 2 * e;
-            *(uint32_t*)(ldy + o * kDyPitch + p * 2) = (a[e] & 0xffffu) | (c[e] << 16);
-            *(uint32_t*)(ldy + (o + 1) * kDyPitch + p * 2) = (a[e] >> 16) | (c[e] & 0xffff0000u);
-        }
+        *(uint4*)(ldy + wg_dy_off(p, 16 * q)) = g.d0[q];
+        *(uint4*)(ldy + wg_dy_off(p + 1, 16 * q)) = g.d1[q];
     }
 #pragma unroll
     for (int k = 0; k < kXtPer; k++) {
-        const int item = tid + 256 * k;
-        if (item >= kXtItems) continue;
-        const int wp = item & 3, hv = (item >> 2) % 10, hu = (item / 40) % 10, sc = item / 400;
-        const int pos = ((hu * 10 + hv) * 8 + 2 * wp) * 2;  // bytes within a block
-#pragma unroll
-        for (int h = 0; h < 2; h++) {
-            const uint32_t a[4] = {g.x0[k][h].x, g.x0[k][h].y, g.x0[k][h].z, g.x0[k][h].w};
-            const uint32_t c[4] = {g.x1[k][h].x, g.x1[k][h].y, g.x1[k][h].z, g.x1[k][h].w};
-#pragma unroll
-            for (int e = 0; e < 4; e++) {
-                const int i = 8 * h + 2 * e;
-                char* blk = lxt + (sc * 16 + i) * kXtBlock + pos;
-                *(uint32_t*)blk = (a[e] & 0xffffu) | (c[e] << 16);
-                *(uint32_t*)(blk + kXtBlock) = (a[e] >> 16) | (c[e] & 0xffff0000u);
-            }
-        }
+        const int piece = tid + 256 * k;
+        if (piece < 2000) *(uint4*)(lxt + piece * 16) = g.x[k];
     }
+}
+
+__device__ __forceinline__ pv_bf16x8 wg_frag(const char* lo, const char* hi) {
+    const pv_i16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (pv_i16x4 __attribute__((address_space(3)))*)lo);
+    const pv_i16x4 c = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (pv_i16x4 __attribute__((address_space(3)))*)hi);
+    pv_bf16x8 r;
+    r[0] = a[0]; r[1] = a[1]; r[2] = a[2]; r[3] = a[3];
+    r[4] = c[0]; r[5] = c[1]; r[6] = c[2]; r[7] = c[3];
+    return r;
 }
 
 __global__ __launch_bounds__(256, 1) void pv_conv3d_wgrad_kernel(
@@ -630,17 +621,22 @@ __global__ __launch_bounds__(256, 1) void pv_conv3d_wgrad_kernel(
         for (int qi = 0; qi < 4; qi++)
 #pragma unroll
             for (int j = 0; j < 16; j++) acc[ob][qi][j] = 0.f;
-    // this lane's columns: tap pair q = wave + 4 qi, tap 2q + (r32 >> 4),
-    // channel r32 & 15; boff = LDS byte offset of its B fragment at
-    // (pu, pv) = (0, 0). Padding columns (tap >= 27) read tap 26's fragment
-    // and are never written out.
+    // As a source of the transposing reads, lane l names piece a = l % 4 of
+    // voxel j = (l % 16) / 4 of its group g = l / 16: group g serves rows (A:
+    // output channels 16 (g % 2) .. +15; B: tap 2q + g % 2) and k-half g / 2.
+    const int grp = lane >> 4, sj = (lane >> 2) & 3, sa = lane & 3;
+    const int gh = grp >> 1;  // k-half this lane serves as a source
+    // B: the halo voxel offset of this lane's source voxel at (pu, pv, pw) =
+    // (0, 0, sj), per tap pair: (du + 1, dv + 1, dw + 1) shifted; padding
+    // columns (tap >= 27) read tap 26
     int boff[4];
 #pragma unroll
     for (int qi = 0; qi < 4; qi++) {
-        const int tap = min(26, 2 * (wave + 4 * qi) + (r32 >> 4));
+        const int tap = min(26, 2 * (wave + 4 * qi) + (grp & 1));
         const int du = tap / 9 - 1, dv = (tap / 3) % 3 - 1, dw = tap % 3 - 1;
-        boff[qi] = ((dw + 1) * 16 + (r32 & 15)) * kXtBlock + ((du + 1) * 10 + (dv + 1)) * 16;
+        boff[qi] = (((du + 1) * 10 + (dv + 1)) * 10 + (dw + 1 + sj)) * 32 + sa * 8;
     }
+    const int acol = (grp & 1) * 32 + sa * 8;  // A: byte offset of its 4 channels in a dy row
 
     // the next brick's operands load during the current brick's MFMAs
     WgradRegs g;
@@ -649,17 +645,21 @@ __global__ __launch_bounds__(256, 1) void pv_conv3d_wgrad_kernel(
         wgrad_store(g, ldy, lxt);
         __syncthreads();
         if (brick + 1 < b1) wgrad_load(g, dy, x, brick + 1, nbr, R, Cin, Cout, o0, i0);
-        // 32 k-steps of 16 voxels (two w-rows): this lane's row r = 2 ks + khalf;
-        // the fragments of step ks + 1 are read during the MFMAs of step ks
+        // 32 k-steps of 16 voxels (two w-rows): k-half h is row r = 2 ks + h
+        // (pu, pv) = (r >> 3, r & 7); the fragments of step ks + 1 are read
+        // during the MFMAs of step ks
         pv_bf16x8 a[2][2], bfr[2][4];
         auto frags = [&](int ks, int buf) {
-            const int r = 2 * ks + khalf, pu = r >> 3, pv = r & 7;
+            const int r = 2 * ks + gh, pu = r >> 3, pv = r & 7;
+            const int p0 = r * 8 + sj;  // voxel of the first read (pw = sj), then + 4
 #pragma unroll
             for (int ob = 0; ob < 2; ob++)
-                a[buf][ob] = *(const pv_bf16x8*)(ldy + (ob * 32 + r32) * kDyPitch + r * 16);
+                a[buf][ob] = wg_frag(ldy + wg_dy_off(p0, ob * 64 + acol),
+                                     ldy + wg_dy_off(p0 + 4, ob * 64 + acol));
+            const int hoff = (pu * 10 + pv) * 10 * 32;
 #pragma unroll
             for (int qi = 0; qi < 4; qi++)
-                bfr[buf][qi] = *(const pv_bf16x8*)(lxt + boff[qi] + (pu * 10 + pv) * 16);
+                bfr[buf][qi] = wg_frag(lxt + boff[qi] + hoff, lxt + boff[qi] + hoff + 4 * 32);
         };
         frags(0, 0);
 #pragma unroll
