@@ -495,14 +495,15 @@ __global__ __launch_bounds__(256) void pv_act_bn_backward_kernel(
 //   dW[o][t][i] = sum over clouds b and output voxels p of dy[b][p][o] * x[b][p + d_t][i]
 // an implicit GEMM with M = output channels, N = (tap, input channel) and
 // K = voxels. A workgroup (four waves) owns 64 output channels x one chunk of
-// 16 input channels x all 27 taps for a contiguous range of 8x8x8 bricks (a
-// split of the voxel sum); each split writes its partial sums, and a second
-// kernel adds the splits in split order. Per brick, both operands sit in LDS
-// as they lie in memory, voxel-major with channels fastest:
+// CI (32, else 16) input channels x all 27 taps for a contiguous range of
+// 8x8x8 bricks (a split of the voxel sum); each split writes its partial
+// sums, and a second kernel adds the splits in split order. Per brick, both
+// operands sit in LDS as they lie in memory, voxel-major with channels
+// fastest:
 //  * dy of the brick, [512 p][64 o] (128-byte rows; 64-byte halves swapped
 //    where bit 1 of p is set, so that the four consecutive rows one
 //    fragment read touches fall in distinct banks);
-//  * x of the brick's 10x10x10 halo for the 16 channels, [1000][16 i].
+//  * x of the brick's 10x10x10 halo for the CI channels, [1000][CI i].
 // The MFMA fragments need the transposes (8 consecutive voxels of one
 // channel per lane). gfx950's transposing LDS read does that: each group of
 // 16 lanes names 16 pieces of 4 channels (4 voxels x 4 pieces), and lane
@@ -511,16 +512,24 @@ __global__ __launch_bounds__(256) void pv_act_bn_backward_kernel(
 // (the halo shifted by the tap). A brick's global loads are issued together
 // into registers while the previous brick's MFMAs run, then written to LDS
 // with 16-byte stores.
-// The GEMM's columns pair the taps: column n of tap pair q is tap 2q + n/16,
-// input channel n % 16 (taps 27 .. 31 are padding: computed, never written).
-// Every wave owns both 32-channel blocks of the 64 and tap pairs w, w+4, w+8,
-// w+12.
+// The GEMM's columns come in blocks of 32: block q holds TPB = 32 / CI taps,
+// column n tap TPB q + n / CI, input channel n % CI (taps past 26 are
+// padding: computed, never written). Every wave owns both 32-channel blocks
+// of the 64 output channels and column blocks w, w + 4, w + 8, ... (CI 32:
+// 7 blocks a wave, one padding tap in all; CI 16: 4 tap pairs, five).
 // Voxels outside the grid (ragged bricks, the halo's border) read as zero.
 constexpr int kWgO = 64;                              // output channels per workgroup
 constexpr int kDyBytes = 512 * kWgO * 2;              // 65536
-constexpr int kXtBytes = 1000 * 16 * 2;               // 32000
-constexpr int kWgradLds = kDyBytes + kXtBytes;        // 97536
-constexpr int kXtPer = (1000 * 2 + 255) / 256;        // halo pieces (16 bytes) per thread: 8
+template <int CI>
+struct WgShape {
+    static constexpr int kXtBytes = 1000 * CI * 2;                // 32000 or 64000
+    static constexpr int kLds = kDyBytes + kXtBytes;
+    static constexpr int kPieces = 1000 * CI / 8;                 // 16-byte halo pieces
+    static constexpr int kXtPer = (kPieces + 255) / 256;          // per thread: 8 or 16
+    static constexpr int kTpb = 32 / CI;                          // taps per column block
+    static constexpr int kBlocks = (27 + kTpb - 1) / kTpb;        // 14 or 27
+    static constexpr int kQb = (kBlocks + 3) / 4;                 // per wave: 4 or 7
+};
 
 typedef short pv_i16x4 __attribute__((ext_vector_type(4)));
 
@@ -530,13 +539,15 @@ __device__ __forceinline__ int wg_dy_off(int p, int cbyte) { return p * 128 + (c
 
 // A brick's operands in registers, between their global loads and their LDS
 // stores: dy of voxels 2 tid, 2 tid + 1 (64 channels each), and halo pieces
-// tid + 256 k (piece = voxel * 2 + half of its 16 channels).
+// tid + 256 k (piece = voxel * CI / 8 + which 8 of its CI channels).
+template <int CI>
 struct WgradRegs {
     uint4 d0[8], d1[8];
-    uint4 x[kXtPer];
+    uint4 x[WgShape<CI>::kXtPer];
 };
 
-__device__ __forceinline__ void wgrad_load(WgradRegs& g, const uint16_t* __restrict__ dy,
+template <int CI>
+__device__ __forceinline__ void wgrad_load(WgradRegs<CI>& g, const uint16_t* __restrict__ dy,
                                            const uint16_t* __restrict__ x, int brick, int nbr,
                                            int R, int Cin, int Cout, int o0, int i0) {
     const int tid = threadIdx.x;
@@ -567,18 +578,21 @@ __device__ __forceinline__ void wgrad_load(WgradRegs& g, const uint16_t* __restr
         }
     }
     const uint16_t* xb = x + (size_t)b * V * Cin + i0;
+    constexpr int PPV = CI / 8;  // pieces per halo voxel
 #pragma unroll
-    for (int k = 0; k < kXtPer; k++) {
-        const int piece = tid + 256 * k, h = piece >> 1, half = piece & 1;
+    for (int k = 0; k < WgShape<CI>::kXtPer; k++) {
+        const int piece = tid + 256 * k, h = piece / PPV, part = piece % PPV;
         const int hw = h % 10, hv = (h / 10) % 10, hu = h / 100;
         const int u = u0 + hu - 1, v = v0 + hv - 1, w = w0 + hw - 1;
-        const bool in = piece < 2000 && u >= 0 && u < R && v >= 0 && v < R && w >= 0 && w < R;
+        const bool in = piece < WgShape<CI>::kPieces && u >= 0 && u < R && v >= 0 && v < R &&
+                        w >= 0 && w < R;
         g.x[k] = sel(in, *(const uint4*)(xb + (((size_t)cl(u) * R + cl(v)) * R + cl(w)) * Cin +
-                                         8 * half));
+                                         8 * part));
     }
 }
 
-__device__ __forceinline__ void wgrad_store(const WgradRegs& g, char* ldy, char* lxt) {
+template <int CI>
+__device__ __forceinline__ void wgrad_store(const WgradRegs<CI>& g, char* ldy, char* lxt) {
     const int tid = threadIdx.x, p = 2 * tid;
 #pragma unroll
     for (int q = 0; q < 8; q++) {
@@ -586,9 +600,9 @@ __device__ __forceinline__ void wgrad_store(const WgradRegs& g, char* ldy, char*
         *(uint4*)(ldy + wg_dy_off(p + 1, 16 * q)) = g.d1[q];
     }
 #pragma unroll
-    for (int k = 0; k < kXtPer; k++) {
+    for (int k = 0; k < WgShape<CI>::kXtPer; k++) {
         const int piece = tid + 256 * k;
-        if (piece < 2000) *(uint4*)(lxt + piece * 16) = g.x[k];
+        if (piece < WgShape<CI>::kPieces) *(uint4*)(lxt + piece * 16) = g.x[k];
     }
 }
 
@@ -603,52 +617,58 @@ __device__ __forceinline__ pv_bf16x8 wg_frag(const char* lo, const char* hi) {
     return r;
 }
 
+template <int CI>
 __global__ __launch_bounds__(256, 1) void pv_conv3d_wgrad_kernel(
     const uint16_t* __restrict__ dy, const uint16_t* __restrict__ x, float* __restrict__ part,
     int R, int Cin, int Cout, int nbr, int nbricks, int per_split) {
-    __shared__ __attribute__((aligned(16))) char lds[kWgradLds];
+    using S = WgShape<CI>;
+    constexpr int QB = S::kQb, TPB = S::kTpb;
+    __shared__ __attribute__((aligned(16))) char lds[S::kLds];
     char* ldy = lds;
     char* lxt = lds + kDyBytes;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int r32 = lane & 31, khalf = lane >> 5;
-    const int split = blockIdx.x, o0 = blockIdx.y * kWgO, i0 = blockIdx.z * 16;
+    const int split = blockIdx.x, o0 = blockIdx.y * kWgO, i0 = blockIdx.z * CI;
     const int b0 = split * per_split, b1 = min(nbricks, b0 + per_split);
 
-    pv_f32x16 acc[2][4];
+    pv_f32x16 acc[2][QB];
 #pragma unroll
     for (int ob = 0; ob < 2; ob++)
 #pragma unroll
-        for (int qi = 0; qi < 4; qi++)
+        for (int qi = 0; qi < QB; qi++)
 #pragma unroll
             for (int j = 0; j < 16; j++) acc[ob][qi][j] = 0.f;
     // As a source of the transposing reads, lane l names piece a = l % 4 of
-    // voxel j = (l % 16) / 4 of its group g = l / 16: group g serves rows (A:
-    // output channels 16 (g % 2) .. +15; B: tap 2q + g % 2) and k-half g / 2.
+    // voxel j = (l % 16) / 4 of its group g = l / 16: group g serves k-half
+    // g / 2 and columns 16 (g % 2) .. +15 of its block (A: output channels;
+    // B: CI 16, tap TPB q + g % 2, CI 32, channels 16 (g % 2) ..).
     const int grp = lane >> 4, sj = (lane >> 2) & 3, sa = lane & 3;
     const int gh = grp >> 1;  // k-half this lane serves as a source
-    // B: the halo voxel offset of this lane's source voxel at (pu, pv, pw) =
-    // (0, 0, sj), per tap pair: (du + 1, dv + 1, dw + 1) shifted; padding
-    // columns (tap >= 27) read tap 26
-    int boff[4];
+    constexpr int XROW = CI * 2;  // bytes per halo voxel
+    // B: the halo offset of this lane's source piece at (pu, pv, pw) =
+    // (0, 0, sj), per column block: the tap's (du + 1, dv + 1, dw + 1)
+    // shift; padding columns (tap >= 27) read tap 26
+    int boff[QB];
 #pragma unroll
-    for (int qi = 0; qi < 4; qi++) {
-        const int tap = min(26, 2 * (wave + 4 * qi) + (grp & 1));
+    for (int qi = 0; qi < QB; qi++) {
+        const int tap = min(26, TPB * (wave + 4 * qi) + (CI == 16 ? (grp & 1) : 0));
         const int du = tap / 9 - 1, dv = (tap / 3) % 3 - 1, dw = tap % 3 - 1;
-        boff[qi] = (((du + 1) * 10 + (dv + 1)) * 10 + (dw + 1 + sj)) * 32 + sa * 8;
+        boff[qi] = (((du + 1) * 10 + (dv + 1)) * 10 + (dw + 1 + sj)) * XROW +
+                   (CI == 16 ? 0 : (grp & 1) * 32) + sa * 8;
     }
     const int acol = (grp & 1) * 32 + sa * 8;  // A: byte offset of its 4 channels in a dy row
 
     // the next brick's operands load during the current brick's MFMAs
-    WgradRegs g;
-    if (b0 < b1) wgrad_load(g, dy, x, b0, nbr, R, Cin, Cout, o0, i0);
+    WgradRegs<CI> g;
+    if (b0 < b1) wgrad_load<CI>(g, dy, x, b0, nbr, R, Cin, Cout, o0, i0);
     for (int brick = b0; brick < b1; brick++) {
-        wgrad_store(g, ldy, lxt);
+        wgrad_store<CI>(g, ldy, lxt);
         __syncthreads();
-        if (brick + 1 < b1) wgrad_load(g, dy, x, brick + 1, nbr, R, Cin, Cout, o0, i0);
+        if (brick + 1 < b1) wgrad_load<CI>(g, dy, x, brick + 1, nbr, R, Cin, Cout, o0, i0);
         // 32 k-steps of 16 voxels (two w-rows): k-half h is row r = 2 ks + h
         // (pu, pv) = (r >> 3, r & 7); the fragments of step ks + 1 are read
         // during the MFMAs of step ks
-        pv_bf16x8 a[2][2], bfr[2][4];
+        pv_bf16x8 a[2][2], bfr[2][QB];
         auto frags = [&](int ks, int buf) {
             const int r = 2 * ks + gh, pu = r >> 3, pv = r & 7;
             const int p0 = r * 8 + sj;  // voxel of the first read (pw = sj), then + 4
@@ -656,10 +676,10 @@ __global__ __launch_bounds__(256, 1) void pv_conv3d_wgrad_kernel(
             for (int ob = 0; ob < 2; ob++)
                 a[buf][ob] = wg_frag(ldy + wg_dy_off(p0, ob * 64 + acol),
                                      ldy + wg_dy_off(p0 + 4, ob * 64 + acol));
-            const int hoff = (pu * 10 + pv) * 10 * 32;
+            const int hoff = (pu * 10 + pv) * 10 * XROW;
 #pragma unroll
-            for (int qi = 0; qi < 4; qi++)
-                bfr[buf][qi] = wg_frag(lxt + boff[qi] + hoff, lxt + boff[qi] + hoff + 4 * 32);
+            for (int qi = 0; qi < QB; qi++)
+                bfr[buf][qi] = wg_frag(lxt + boff[qi] + hoff, lxt + boff[qi] + hoff + 4 * XROW);
         };
         frags(0, 0);
 #pragma unroll
@@ -669,7 +689,7 @@ __global__ __launch_bounds__(256, 1) void pv_conv3d_wgrad_kernel(
 #pragma unroll
             for (int ob = 0; ob < 2; ob++)
 #pragma unroll
-                for (int qi = 0; qi < 4; qi++)
+                for (int qi = 0; qi < QB; qi++)
                     acc[ob][qi] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
                         a[cur][ob], bfr[cur][qi], acc[ob][qi], 0, 0, 0);
         }
@@ -678,8 +698,8 @@ __global__ __launch_bounds__(256, 1) void pv_conv3d_wgrad_kernel(
     // partial sums: rows o = 8 j + 4 khalf + e of each 32-channel block, column r32
     float* dst = part + (size_t)split * Cout * 27 * Cin;
 #pragma unroll
-    for (int qi = 0; qi < 4; qi++) {
-        const int tap = 2 * (wave + 4 * qi) + (r32 >> 4), i = i0 + (r32 & 15);
+    for (int qi = 0; qi < QB; qi++) {
+        const int tap = TPB * (wave + 4 * qi) + r32 / CI, i = i0 + r32 % CI;
         if (tap >= 27) continue;
 #pragma unroll
         for (int ob = 0; ob < 2; ob++)
@@ -706,7 +726,7 @@ __global__ __launch_bounds__(256) void pv_wgrad_reduce_kernel(const float* __res
 int wgrad_splits(int B, int R, int Cin, int Cout) {
     const int nbr = (R + 7) / 8;
     const int nbricks = B * nbr * nbr * nbr;
-    const int tiles = (Cout / kWgO) * (Cin / 16);
+    const int tiles = (Cout / kWgO) * (Cin % 32 == 0 ? Cin / 32 : Cin / 16);
     const int want = (256 + tiles - 1) / tiles;
     return std::max(1, std::min(nbricks, want));
 }
@@ -905,9 +925,14 @@ pvconv_status pv_launch_conv3d_backward_weight(const void* dy, const void* x, in
     const int per = (nbricks + nsplit - 1) / nsplit;
     const int used = (nbricks + per - 1) / per;  // splits that hold at least one brick
     float* part = (float*)ws;
-    hipLaunchKernelGGL(pv_conv3d_wgrad_kernel, dim3(used, Cout / kWgO, Cin / 16), dim3(256), 0, s,
-                       (const uint16_t*)dy, (const uint16_t*)x, part, R, Cin, Cout, nbr, nbricks,
-                       per);
+    if (Cin % 32 == 0)
+        hipLaunchKernelGGL(pv_conv3d_wgrad_kernel<32>, dim3(used, Cout / kWgO, Cin / 32), dim3(256),
+                           0, s, (const uint16_t*)dy, (const uint16_t*)x, part, R, Cin, Cout, nbr,
+                           nbricks, per);
+    else
+        hipLaunchKernelGGL(pv_conv3d_wgrad_kernel<16>, dim3(used, Cout / kWgO, Cin / 16), dim3(256),
+                           0, s, (const uint16_t*)dy, (const uint16_t*)x, part, R, Cin, Cout, nbr,
+                           nbricks, per);
     const unsigned blocks = (unsigned)std::min<size_t>((n + 255) / 256, 2048);
     hipLaunchKernelGGL(pv_wgrad_reduce_kernel, dim3(blocks), dim3(256), 0, s, part, dw, n, used);
     return pv_launch_status();

@@ -190,6 +190,7 @@ def test_conv3d_backward_data_is_the_adjoint_of_the_forward_on_gpu():
     (1, 16, 128, 128),
     (1, 13, 32, 64),     # ragged bricks
     (3, 8, 16, 64),      # one brick per cloud
+    (1, 9, 48, 64),      # 16-channel chunks (48 is no multiple of 32), ragged bricks
     (1, 1, 16, 64),      # a single voxel: only the centre tap sees data
 ])
 def test_conv3d_backward_weight_matches_oracle(B, R, Cin, Cout):
