@@ -538,8 +538,9 @@ typedef short pv_i16x4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ int wg_dy_off(int p, int cbyte) { return p * 128 + (cbyte ^ ((p & 2) << 5)); }
 
 // A brick's operands in registers, between their global loads and their LDS
-// stores: dy of voxels 2 tid, 2 tid + 1 (64 channels each), and halo pieces
-// tid + 256 k (piece = voxel * CI / 8 + which 8 of its CI channels).
+// stores: dy of voxels tid and tid + 256 (64 channels each: consecutive
+// lanes store consecutive rows), and halo pieces tid + 256 k (piece = voxel
+// * CI / 8 + which 8 of its CI channels).
 template <int CI>
 struct WgradRegs {
     uint4 d0[8], d1[8];
@@ -566,11 +567,12 @@ __device__ __forceinline__ void wgrad_load(WgradRegs<CI>& g, const uint16_t* __r
     auto cl = [R](int a) { return min(max(a, 0), R - 1); };
     auto sel = [&z](bool in, uint4 v) { return in ? v : z; };
     {
-        const int p = 2 * tid, u = u0 + (p >> 6), v = v0 + ((p >> 3) & 7), w = w0 + (p & 7);
-        const bool in0 = u < R && v < R && w < R, in1 = in0 && w + 1 < R;
+        // voxels p = tid and p + 256 = the same (v, w), u + 4
+        const int p = tid, u = u0 + (p >> 6), v = v0 + ((p >> 3) & 7), w = w0 + (p & 7);
+        const bool in0 = u < R && v < R && w < R, in1 = v < R && w < R && u + 4 < R;
         const uint16_t* dyb = dy + (size_t)b * V * Cout + o0;
         const uint16_t* r0 = dyb + (((size_t)cl(u) * R + cl(v)) * R + cl(w)) * Cout;
-        const uint16_t* r1 = dyb + (((size_t)cl(u) * R + cl(v)) * R + cl(w + 1)) * Cout;
+        const uint16_t* r1 = dyb + (((size_t)cl(u + 4) * R + cl(v)) * R + cl(w)) * Cout;
 #pragma unroll
         for (int q = 0; q < 8; q++) {
             g.d0[q] = sel(in0, *(const uint4*)(r0 + 8 * q));
@@ -593,11 +595,11 @@ __device__ __forceinline__ void wgrad_load(WgradRegs<CI>& g, const uint16_t* __r
 
 template <int CI>
 __device__ __forceinline__ void wgrad_store(const WgradRegs<CI>& g, char* ldy, char* lxt) {
-    const int tid = threadIdx.x, p = 2 * tid;
+    const int tid = threadIdx.x;
 #pragma unroll
     for (int q = 0; q < 8; q++) {
-        *(uint4*)(ldy + wg_dy_off(p, 16 * q)) = g.d0[q];
-        *(uint4*)(ldy + wg_dy_off(p + 1, 16 * q)) = g.d1[q];
+        *(uint4*)(ldy + wg_dy_off(tid, 16 * q)) = g.d0[q];
+        *(uint4*)(ldy + wg_dy_off(tid + 256, 16 * q)) = g.d1[q];
     }
 #pragma unroll
     for (int k = 0; k < WgShape<CI>::kXtPer; k++) {
