@@ -278,6 +278,11 @@ class DevicePVCNN2:
             for layer in lev:
                 ws = max(ws, pv.pvconv_forward_workspace_size(B, self.npts[l], layer))
         self.workspace = torch.empty(ws, dtype=torch.uint8, device=device)
+        # forward(): the coordinate-only steps (sampling, ball queries, three
+        # nearest neighbours) on a second stream, at the default priority
+        self.side = torch.cuda.Stream(device=device)
+        self.sampled = [torch.cuda.Event() for _ in range(L)]
+        self.nn_ready = torch.cuda.Event()
 
     def _hidden(self, bufs, k, rows, c):
         return bufs[k % 2][:rows * c].view(rows, c)
@@ -332,10 +337,17 @@ class DevicePVCNN2:
         pv.pvconv_group_max(x, lev.nsample, out=target.view(-1, target.shape[2]))
         return target
 
-    def run_fp(self, k: int, coarse: torch.Tensor) -> torch.Tensor:
-        """Feature propagation k (to level L-1-k) from the coarser features."""
+    def run_three_nn(self, k: int):
+        """The three nearest level-(l+1) points of each level-l point, l = L-1-k."""
         l = self.L - 1 - k
         pv.pvconv_three_nn(self.xyz[l], self.xyz[l + 1], idx=self.nn_idx[l], weight=self.nn_w[l])
+
+    def run_fp(self, k: int, coarse: torch.Tensor, nn_done: bool = False) -> torch.Tensor:
+        """Feature propagation k (to level L-1-k) from the coarser features
+        (the three nearest neighbours found here unless nn_done)."""
+        l = self.L - 1 - k
+        if not nn_done:
+            self.run_three_nn(k)
         pv.pvconv_three_interpolate(coarse, self.nn_idx[l], self.nn_w[l],
                                     out=self.cat[l][:, :, :self.c_interp[l]])
         x = self.cat[l]
@@ -387,5 +399,36 @@ class DevicePVCNN2:
 
     def forward(self, coords: torch.Tensor, feats: torch.Tensor) -> torch.Tensor:
         """coords [B][N][3] f32, feats [B][N][C_in] (f32 or bf16) -> logits
-        [B][N][13] f32 (a view of a buffer reused by the next call)."""
-        return self.forward_timed(coords, feats, lambda name: None)
+        [B][N][13] f32 (a view of a buffer reused by the next call).
+
+        The same steps as forward_timed, on two streams: the sampling of
+        every level and the nearest neighbours of the propagation, which
+        depend on the coordinates alone, run on the side stream while the
+        main stream runs the PVConv layers (farthest point sampling of a
+        large cloud keeps one CU per cloud busy for a long sequential
+        chain); the main stream waits for level l's sampling before level
+        l's grouping, and for the neighbours before the propagation. The
+        side stream first waits for the main stream's earlier work, so
+        the buffers the previous forward still reads are not overwritten."""
+        main = torch.cuda.current_stream(coords.device)
+        self.xyz[0] = coords  # level 0 is the caller's points
+        self.side.wait_stream(main)
+        with torch.cuda.stream(self.side):
+            xyz = coords
+            for l in range(self.L):
+                xyz, _ = self.run_sample(l, xyz)
+                self.sampled[l].record(self.side)
+            for k in range(self.L):
+                self.run_three_nn(k)
+            self.nn_ready.record(self.side)
+        xyz, x = coords, feats
+        for l, lev in enumerate(self.sa):
+            if lev.pvconvs:
+                x = self.run_pvconv(l, xyz, x)
+            main.wait_event(self.sampled[l])
+            x = self.run_group_mlp(l, xyz, x, self.xyz[l + 1], self.ball[l])
+            xyz = self.xyz[l + 1]
+        main.wait_event(self.nn_ready)
+        for k in range(self.L):
+            x = self.run_fp(k, x, nn_done=True)
+        return self.run_head(x)
