@@ -326,7 +326,9 @@ def bench_network(args, wl, dev, peaks=True, cpu_seconds=None):
         for j, n in enumerate(names):
             per[n].append(marks[j].elapsed_time(marks[j + 1]))
 
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    # two events around the K steps only: an event recorded between steps
+    # leaves the GPU idle for a few microseconds
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
     quiet_host()
     for _ in range(args.warmup):
         net.forward(coords, feats)
@@ -335,11 +337,11 @@ def bench_network(args, wl, dev, peaks=True, cpu_seconds=None):
     ev[0].record(stream)
     for i in range(args.steps):
         net.forward(coords, feats)
-        ev[i + 1].record(stream)
+    ev[1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     gc.enable()
-    step_ms = [ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)]
+    ev_ms = ev[0].elapsed_time(ev[1]) / args.steps
     ms_per_step = wall * 1e3 / args.steps
     gpu_out = net.logits.double().cpu().numpy()
 
@@ -385,8 +387,7 @@ def bench_network(args, wl, dev, peaks=True, cpu_seconds=None):
                     "blocks": [[L.cin, L.cout, L.R] for L in wl.layers],
                     "mlps": [int(m.w.shape[0]) for m in wl.mlps],
                     "head": [int(h.w.shape[0]) for h in wl.head], "points_per_step": B * N}),
-        "ms_per_step_events": {"median": round(statistics.median(step_ms), 4),
-                               "min": round(min(step_ms), 4)},
+        "ms_per_step_events": round(ev_ms, 4),
         "network_tflops": round(total_fl / (ms_per_step * 1e-3) / 1e12, 2),
         "roofline": roofline,
         "kernels": kernels,
@@ -762,7 +763,9 @@ def bench_layer(args, wl, dev, cold=True, peaks=True, cpu_seconds=None):
     cold_ms = {n: cold_times(step_fn(n), stream, BREAKDOWN_REPS, BREAKDOWN_ROUNDS, dev)
                for n in steps} if cold else None
     pn_host = pn.cpu().numpy()
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    # two events around the K steps only: an event recorded between steps
+    # leaves the GPU idle for a few microseconds
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
     quiet_host()
     # the whole forward, BREAKDOWN_REPS steps per graph (no host launch cost
     # between kernels), last in the breakdown: about 50 ms of back-to-back
@@ -780,12 +783,12 @@ def bench_layer(args, wl, dev, cold=True, peaks=True, cpu_seconds=None):
     ev[0].record(stream)
     for i in range(args.steps):
         pv.pvconv_forward(coords, feats, layer, out=out, workspace=ws)
-        ev[i + 1].record(stream)
+    ev[1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     del fwd_graph
     gc.enable()
-    step_ms = [ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)]
+    ev_ms = ev[0].elapsed_time(ev[1]) / args.steps
     ms_per_step = wall * 1e3 / args.steps
     gpu_out = out.double().cpu().numpy()
 
@@ -860,8 +863,7 @@ def bench_layer(args, wl, dev, cold=True, peaks=True, cpu_seconds=None):
         "config": {"workload": wl.name, "B": B, "N": N, "R": R, "cin": cin, "cout": cout,
                    "n_convs": L.n_convs, "points_per_step": B * N},
         "ms_per_layer": round(ms_per_step, 4),
-        "ms_per_step_events": {"median": round(statistics.median(step_ms), 4),
-                               "min": round(min(step_ms), 4)},
+        "ms_per_step_events": round(ev_ms, 4),
         "ms_per_step_graph": {"median": round(statistics.median(graph_ms), 4),
                               "min": round(min(graph_ms), 4),
                               "how": f"the forward captured {BREAKDOWN_REPS} times in one HIP "
