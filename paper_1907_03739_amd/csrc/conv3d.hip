@@ -242,61 +242,74 @@ __global__ __launch_bounds__(256 * WCH, SB ? 2 : 1) void pv_conv3d_bf16_kernel(
         bn_tab[0][tid] = sc;
         bn_tab[1][tid] = sh;
     }
-    // Chunk 0's halo, the weights of taps 0 and 1.
+    // A sparse input (occ) whose halo holds no occupied voxel: every product
+    // is zero, so the accumulators stay zero and the epilogue writes
+    // act(BN(0)), the same bits as the full loop would. The reduction is also
+    // the barrier before the epilogue reads bn_tab.
+    bool live = true;
+    if (occ) {
+        bool any = false;
 #pragma unroll
-    for (int set = 0; set < kSets; set++) *(uint4*)(lds + loff[set]) = halo_load(set, 0);
-    pv_bf16x8 wf[3][NBW];
-    load_w(0, 0, wf[0]);
-    load_w(0, 1, wf[1]);
-    __syncthreads();
+        for (int set = 0; set < kSets; set++) any |= goff[set] != kOOB;
+        live = __syncthreads_or(any);
+    }
+    if (live) {
+        // Chunk 0's halo, the weights of taps 0 and 1.
+#pragma unroll
+        for (int set = 0; set < kSets; set++) *(uint4*)(lds + loff[set]) = halo_load(set, 0);
+        pv_bf16x8 wf[3][NBW];
+        load_w(0, 0, wf[0]);
+        load_w(0, 1, wf[1]);
+        __syncthreads();
 
-    // Chunk c sits in LDS buffer c%2: 27 taps, unrolled. Tap t computes with
-    // weight set t%3 (27 = 9 x 3, so the ring realigns at every chunk) while
-    // tap t+2's weights load into set (t+2)%3, and with B fragments bf[t%2]
-    // while tap t+1's are read from LDS into the other set. Piece set s of the
-    // next chunk's halo is loaded at tap s into hr[s%4] and stored to the
-    // other LDS buffer at tap s+4. One loop body for every chunk keeps the
-    // accumulators in the same registers throughout.
-    constexpr int kHaloLag = 4;
-    for (int c = 0; c < nch; c++) {
-        const int cur_off = (c & 1) * HB, nxt_off = HB - cur_off;
-        // SB skips the last chunk's halo prefetch; the double-buffered
-        // variant reloads the last chunk into the idle buffer
-        const bool fetch = !SB || c + 1 < nch;
-        const int cn = (c + 1 < nch ? c + 1 : c) * kKC;
-        pv_bf16x8 bf[2][4];
-        uint4 hr[kHaloLag];
-#pragma unroll
-        for (int mb = 0; mb < 4; mb++)
-            bf[0][mb] = *(const pv_bf16x8*)(lds + frag_addr(mb, 0) + cur_off);
-#pragma unroll
-        for (int t = 0; t < kTaps; t++) {
-            const int cur = t & 1, nxt = cur ^ 1;
-            if (t + 2 < kTaps)
-                load_w(c, t + 2, wf[(t + 2) % 3]);
-            else
-                load_w(c + 1, t + 2 - kTaps, wf[(t + 2) % 3]);
-            if (fetch && t >= kHaloLag && t < kSets + kHaloLag)
-                *(uint4*)(lds + loff[t - kHaloLag] + nxt_off) = hr[(t - kHaloLag) % kHaloLag];
-            if (fetch && t < kSets) hr[t % kHaloLag] = halo_load(t, cn);
-            if (t + 1 < kTaps) {
-#pragma unroll
-                for (int mb = 0; mb < 4; mb++)
-                    bf[nxt][mb] = *(const pv_bf16x8*)(lds + frag_addr(mb, t + 1) + cur_off);
-            }
+        // Chunk c sits in LDS buffer c%2: 27 taps, unrolled. Tap t computes with
+        // weight set t%3 (27 = 9 x 3, so the ring realigns at every chunk) while
+        // tap t+2's weights load into set (t+2)%3, and with B fragments bf[t%2]
+        // while tap t+1's are read from LDS into the other set. Piece set s of the
+        // next chunk's halo is loaded at tap s into hr[s%4] and stored to the
+        // other LDS buffer at tap s+4. One loop body for every chunk keeps the
+        // accumulators in the same registers throughout.
+        constexpr int kHaloLag = 4;
+        for (int c = 0; c < nch; c++) {
+            const int cur_off = (c & 1) * HB, nxt_off = HB - cur_off;
+            // SB skips the last chunk's halo prefetch; the double-buffered
+            // variant reloads the last chunk into the idle buffer
+            const bool fetch = !SB || c + 1 < nch;
+            const int cn = (c + 1 < nch ? c + 1 : c) * kKC;
+            pv_bf16x8 bf[2][4];
+            uint4 hr[kHaloLag];
 #pragma unroll
             for (int mb = 0; mb < 4; mb++)
+                bf[0][mb] = *(const pv_bf16x8*)(lds + frag_addr(mb, 0) + cur_off);
 #pragma unroll
-                for (int nb = 0; nb < NBW; nb++)
-                    acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                        wf[t % 3][nb], bf[cur][mb], acc[mb][nb], 0, 0, 0);
-            __builtin_amdgcn_sched_barrier(0);
+            for (int t = 0; t < kTaps; t++) {
+                const int cur = t & 1, nxt = cur ^ 1;
+                if (t + 2 < kTaps)
+                    load_w(c, t + 2, wf[(t + 2) % 3]);
+                else
+                    load_w(c + 1, t + 2 - kTaps, wf[(t + 2) % 3]);
+                if (fetch && t >= kHaloLag && t < kSets + kHaloLag)
+                    *(uint4*)(lds + loff[t - kHaloLag] + nxt_off) = hr[(t - kHaloLag) % kHaloLag];
+                if (fetch && t < kSets) hr[t % kHaloLag] = halo_load(t, cn);
+                if (t + 1 < kTaps) {
+#pragma unroll
+                    for (int mb = 0; mb < 4; mb++)
+                        bf[nxt][mb] = *(const pv_bf16x8*)(lds + frag_addr(mb, t + 1) + cur_off);
+                }
+#pragma unroll
+                for (int mb = 0; mb < 4; mb++)
+#pragma unroll
+                    for (int nb = 0; nb < NBW; nb++)
+                        acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                            wf[t % 3][nb], bf[cur][mb], acc[mb][nb], 0, 0, 0);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            // chunk done: the next halo is complete and this buffer is free
+            if constexpr (SB)
+                pv_lds_barrier();  // LDS only: the weight prefetch stays in flight
+            else
+                __syncthreads();
         }
-        // chunk done: the next halo is complete and this buffer is free
-        if constexpr (SB)
-            pv_lds_barrier();  // LDS only: the weight prefetch stays in flight
-        else
-            __syncthreads();
     }
 
     // Epilogue. Block (mb, nb) holds D[n][voxel]: lane has voxel column r32
