@@ -254,28 +254,41 @@ __global__ __launch_bounds__(256 * WCH, SB ? 2 : 1) void pv_conv3d_bf16_kernel(
         live = __syncthreads_or(any);
     }
     if (live) {
-        // Chunk 0's halo, the weights of taps 0 and 1.
+        // Chunk 0's halo, the weights of the first kWD taps.
 #pragma unroll
         for (int set = 0; set < kSets; set++) *(uint4*)(lds + loff[set]) = halo_load(set, 0);
-        pv_bf16x8 wf[3][NBW];
-        load_w(0, 0, wf[0]);
-        load_w(0, 1, wf[1]);
+        // Weights load kWD taps ahead through a ring of kWD + 1 sets (a
+        // divisor of 27, so the ring realigns at every chunk). The 32-channel
+        // tiles (one wave per SIMD, four MFMAs per tap) look further ahead,
+        // and store each halo piece eight taps after its load (1.5-2 % on
+        // the small grids' convolutions).
+        constexpr int kWD = (!SB && NB == 1) ? 8 : 2, kWR = kWD + 1;
+        static_assert(kTaps % kWR == 0, "the weight ring realigns at every chunk");
+        pv_bf16x8 wf[kWR][NBW];
+#pragma unroll
+        for (int k = 0; k < kWD; k++) load_w(0, k, wf[k]);
         __syncthreads();
 
         // Chunk c sits in LDS buffer c%2: 27 taps, unrolled. Tap t computes with
-        // weight set t%3 (27 = 9 x 3, so the ring realigns at every chunk) while
-        // tap t+2's weights load into set (t+2)%3, and with B fragments bf[t%2]
-        // while tap t+1's are read from LDS into the other set. Piece set s of the
-        // next chunk's halo is loaded at tap s into hr[s%4] and stored to the
-        // other LDS buffer at tap s+4. One loop body for every chunk keeps the
-        // accumulators in the same registers throughout.
-        constexpr int kHaloLag = 4;
+        // weight set t%kWR while tap t+kWD's weights load, and with B fragments
+        // bf[t%2] while tap t+1's are read from LDS into the other set. Piece
+        // set s of the next chunk's halo is loaded at tap s into
+        // hr[s%kHaloLag] and stored to the other LDS buffer at tap
+        // s+kHaloLag. One loop body for every chunk keeps the accumulators in
+        // the same registers throughout.
+        constexpr int kHaloLag = (!SB && NB == 1) ? 8 : 4;
         for (int c = 0; c < nch; c++) {
             const int cur_off = (c & 1) * HB, nxt_off = HB - cur_off;
-            // SB skips the last chunk's halo prefetch; the double-buffered
-            // variant reloads the last chunk into the idle buffer
-            const bool fetch = !SB || c + 1 < nch;
-            const int cn = (c + 1 < nch ? c + 1 : c) * kKC;
+            // Next chunk's halo. Past the last chunk the double-buffered
+            // variant reloads the last chunk into the idle buffer, and SB
+            // loads out of range (zeros, no memory access) into it: with
+            // unconditional loads the compiler's wait counts stay exact (with
+            // a branch around them it must assume they were skipped, and each
+            // tap's weight wait then also waits for the next tap's weights).
+            // Element-wise loads (!VEC) keep the branch: unconditional, they
+            // spill registers.
+            const bool fetch = VEC || !SB || c + 1 < nch;
+            const int cn = c + 1 < nch ? (c + 1) * kKC : (SB ? Cin : c * kKC);
             pv_bf16x8 bf[2][4];
             uint4 hr[kHaloLag];
 #pragma unroll
@@ -284,10 +297,10 @@ __global__ __launch_bounds__(256 * WCH, SB ? 2 : 1) void pv_conv3d_bf16_kernel(
 #pragma unroll
             for (int t = 0; t < kTaps; t++) {
                 const int cur = t & 1, nxt = cur ^ 1;
-                if (t + 2 < kTaps)
-                    load_w(c, t + 2, wf[(t + 2) % 3]);
+                if (t + kWD < kTaps)
+                    load_w(c, t + kWD, wf[(t + kWD) % kWR]);
                 else
-                    load_w(c + 1, t + 2 - kTaps, wf[(t + 2) % 3]);
+                    load_w(c + 1, t + kWD - kTaps, wf[(t + kWD) % kWR]);
                 if (fetch && t >= kHaloLag && t < kSets + kHaloLag)
                     *(uint4*)(lds + loff[t - kHaloLag] + nxt_off) = hr[(t - kHaloLag) % kHaloLag];
                 if (fetch && t < kSets) hr[t % kHaloLag] = halo_load(t, cn);
@@ -301,7 +314,7 @@ __global__ __launch_bounds__(256 * WCH, SB ? 2 : 1) void pv_conv3d_bf16_kernel(
 #pragma unroll
                     for (int nb = 0; nb < NBW; nb++)
                         acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                            wf[t % 3][nb], bf[cur][mb], acc[mb][nb], 0, 0, 0);
+                            wf[t % kWR][nb], bf[cur][mb], acc[mb][nb], 0, 0, 0);
                 __builtin_amdgcn_sched_barrier(0);
             }
             // chunk done: the next halo is complete and this buffer is free
