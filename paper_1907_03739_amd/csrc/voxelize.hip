@@ -681,6 +681,9 @@ __host__ __device__ inline SlabLayout slab_layout(int nvs, int N) {
 }
 constexpr int kStageSlack = 1024;
 constexpr int kStageBytes = 96 * 1024;
+// A slab with more points than the stage holds, but no more than this many
+// beyond it, stages the rest after the sort in the sort's dead tables.
+constexpr int kExtRows = 128;
 
 // No normalised point reaches voxel `vox`: its cell lies further than 1/2
 // from the cube's centre. Exact integer test in units of 1/(2R): the cell
@@ -748,13 +751,25 @@ __device__ __forceinline__ void dma_rows(char* dst, int nrows, int C, const FT* 
     const int npiece = nrows * ppr;
     const bool pow2 = (ppr & (ppr - 1)) == 0;
     const int sh = __ffs(ppr) - 1;
-    for (int p0 = wave * 64; p0 < npiece; p0 += NC) {
-        const int pc = min(p0 + lane, npiece - 1);
-        const int r = pow2 ? pc >> sh : pc / ppr, q = pc - r * ppr;
-        const FT* src = fb + (size_t)pt(r) * feat_ld + q * (16 / (int)sizeof(FT));
-        __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)src,
-                                         (void __attribute__((address_space(3)))*)(dst + p0 * 16),
-                                         16, 0, 0);
+    // U wave-steps at a time: their row indices (LDS reads) first, then the
+    // DMAs, so that the index reads' latency is paid once per U steps
+    constexpr int U = 8;
+    for (int p00 = wave * 64; p00 < npiece; p00 += U * NC) {
+        const FT* src[U];
+#pragma unroll
+        for (int u = 0; u < U; u++) {
+            const int pc = min(p00 + u * NC + lane, npiece - 1);
+            const int r = pow2 ? pc >> sh : pc / ppr, q = pc - r * ppr;
+            src[u] = fb + (size_t)pt(r) * feat_ld + q * (16 / (int)sizeof(FT));
+        }
+#pragma unroll
+        for (int u = 0; u < U; u++) {
+            const int p0 = p00 + u * NC;
+            if (p0 < npiece)
+                __builtin_amdgcn_global_load_lds(
+                    (const void __attribute__((address_space(1)))*)src[u],
+                    (void __attribute__((address_space(3)))*)(dst + p0 * 16), 16, 0, 0);
+        }
     }
 }
 
@@ -792,6 +807,7 @@ __global__ __launch_bounds__(NT) void pv_voxel_slab_kernel(
     // + 1 once listed; loader waves whose rows have landed
     __shared__ int s_ctr, s_counted, s_listed, s_rows_in;
     __shared__ int wcnt[PPT][kSlabNC / 64];
+    __shared__ uint16_t s_extk[kExtRows];  // points of list positions cap_pre, cap_pre + 1, ...
     const int bid = blockIdx.x;
     if (bid >= (int)gridDim.x - npack) {  // extra workgroups: conv weight packing
         const int pb = bid - ((int)gridDim.x - npack);
@@ -814,6 +830,11 @@ __global__ __launch_bounds__(NT) void pv_voxel_slab_kernel(
     uint16_t* kbuf = (uint16_t*)(smem + LY.kbuf);
     int* rbuf = (int*)(smem + LY.rbuf);
     uint16_t* wc = (uint16_t*)(smem + LY.wc);
+    // Rows past the stage (slabs of cap_pre < ns <= cap_pre + cap_ext points)
+    // go to kbuf .. the end of the dynamic LDS once the sort is done with it,
+    // less the slack a wave's last DMA may write past its rows.
+    const int cap_ext =
+        VEC ? min(kExtRows, max(0, (LY.pre - LY.kbuf - kStageSlack) / (C * (int)sizeof(FT)))) : 0;
     for (int i = tid; i < nvs; i += NT) {
         hist[i] = 0;
         far[i] = !ids_in && i < nv && outside_ball(v0 + i, R);
@@ -893,8 +914,8 @@ __global__ __launch_bounds__(NT) void pv_voxel_slab_kernel(
         // (when they fit the stage) in point order
         wait_flag(&s_listed);
         const int ns = s_listed - 1;
-        if (VEC && ns <= cap_pre)
-            dma_rows<64 * kLoaders, FT>(s_stage, ns, C, fb, feat_ld,
+        if (VEC && ns <= cap_pre + cap_ext)
+            dma_rows<64 * kLoaders, FT>(s_stage, min(ns, cap_pre), C, fb, feat_ld,
                                         [&](int r) { return (int)kbuf[r]; }, wave - NC / 64);
         __builtin_amdgcn_s_waitcnt(0);  // this wave's rows have landed
         if (lane == 0) atomicAdd(&s_rows_in, 1);
@@ -1005,6 +1026,8 @@ __global__ __launch_bounds__(NT) void pv_voxel_slab_kernel(
                 const int pos = before + __popcll(bal[i] & lt);
                 kbuf[pos] = (uint16_t)(tid + i * NC);
                 rbuf[pos] = id[i] - v0;
+                if (pos >= cap_pre && pos < cap_pre + kExtRows)
+                    s_extk[pos - cap_pre] = (uint16_t)(tid + i * NC);
             }
         }
         for (int i = tid; i < kSortWaves * nvs; i += NC) wc[i] = 0;
@@ -1015,6 +1038,7 @@ __global__ __launch_bounds__(NT) void pv_voxel_slab_kernel(
     if (tid == 0)
         __hip_atomic_store(&s_listed, ns + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
     const bool pre = VEC && ns <= cap_pre;
+    const bool ext = VEC && !pre && ns <= cap_pre + cap_ext;
 
     // 3. exclusive prefix over the slab's voxels of (points, occupied): hi
     // 16 bits count points (ns <= 4096), lo 16 bits voxels
@@ -1076,7 +1100,7 @@ __global__ __launch_bounds__(NT) void pv_voxel_slab_kernel(
         }
     }
     sync();
-    if (pre)  // both loader waves' rows have landed (bounded wait)
+    if (pre || ext)  // both loader waves' rows have landed (bounded wait)
         for (int spin = 0; spin < (1 << 23); spin++) {
             if (__hip_atomic_load(&s_rows_in, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) >=
                 kLoaders)
@@ -1084,6 +1108,15 @@ __global__ __launch_bounds__(NT) void pv_voxel_slab_kernel(
             __builtin_amdgcn_s_sleep(1);
         }
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+    // ext: the loaders (which read kbuf for their addresses) are done and
+    // the sort's tables are dead, so the rest of the slab's rows go there
+    const FT* xstage = (const FT*)(smem + LY.kbuf);
+    if (ext) {
+        dma_rows<NC, FT>(smem + LY.kbuf, ns - cap_pre, C, fb, feat_ld,
+                         [&](int r) { return (int)s_extk[r]; }, wave);
+        __builtin_amdgcn_s_waitcnt(0);
+        sync();
+    }
 
     // 5. means, over the occupied voxels in voxel order. pre: one pass over
     // the prefetched rows (a voxel's rows through sortj). Else in segments
@@ -1100,13 +1133,13 @@ __global__ __launch_bounds__(NT) void pv_voxel_slab_kernel(
     const int qstep = gpv <= NC ? gpv : NC;
     // the mean of voxel occ[o] over column q, its rows in the stage at
     // row_of(sorted position): the rows in sorted order (point order), fp64
-    auto mean_item = [&](int o, int q, const FT* stage, auto row_of) {
+    auto mean_item = [&](int o, int q, auto rowp) {
         const int v = occ[o], nk = hist[v], p0 = start[v];
         if (VEC) {
             double acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
             for (int j = 0; j < nk; j++) {
                 float f[8];
-                stage8(stage + (size_t)row_of(p0 + j) * C + q * 8, f);
+                stage8(rowp(p0 + j) + q * 8, f);
 #pragma unroll
                 for (int i = 0; i < 8; i++) acc[i] += (double)f[i];
             }
@@ -1116,7 +1149,7 @@ __global__ __launch_bounds__(NT) void pv_voxel_slab_kernel(
             store8<GT>(out + (size_t)v * C + q * 8, mean);
         } else {
             double acc = 0.0;
-            for (int j = 0; j < nk; j++) acc += (double)stage1(stage + (size_t)row_of(p0 + j) * C + q);
+            for (int j = 0; j < nk; j++) acc += (double)stage1(rowp(p0 + j) + q);
             store1<GT>(out + (size_t)v * C + q, (float)(acc / (double)nk));
         }
     };
@@ -1124,10 +1157,10 @@ __global__ __launch_bounds__(NT) void pv_voxel_slab_kernel(
     // item (o, q) a thread; heavier ones (VEC) one voxel a wave, taken in
     // turn, lane sub * ng + cl summing rows sub, sub + S, ... of column group
     // cg0 + cl (S = 64 / ng subsets), the S sums added in subset order.
-    auto staged_means = [&](int oa, int ob, const FT* stage, auto row_of) {
+    auto staged_means = [&](int oa, int ob, auto rowp) {
         for (int q = q0; col_ok && q < gpv; q += qstep)
             for (int o = oa + r0; o < ob; o += rs)
-                if (!VEC || hist[occ[o]] <= kSplit) mean_item(o, q, stage, row_of);
+                if (!VEC || hist[occ[o]] <= kSplit) mean_item(o, q, rowp);
         if (!VEC) return;
         int nheavy = 0;
         for (int o0 = oa; o0 < ob; o0 += 64) {
@@ -1145,7 +1178,7 @@ __global__ __launch_bounds__(NT) void pv_voxel_slab_kernel(
                     if (sub < S)
                         for (int j = sub; j < nk; j += S) {
                             float f[8];
-                            stage8(stage + (size_t)row_of(p0 + j) * C + (cg0 + cl) * 8, f);
+                            stage8(rowp(p0 + j) + (cg0 + cl) * 8, f);
 #pragma unroll
                             for (int i = 0; i < 8; i++) acc[i] += (double)f[i];
                         }
@@ -1165,8 +1198,14 @@ __global__ __launch_bounds__(NT) void pv_voxel_slab_kernel(
             }
         }
     };
+    const FT* stage = (const FT*)s_stage;
     if (pre) {
-        staged_means(0, n_occ, (const FT*)s_stage, [&](int p) { return (int)sortj[p]; });
+        staged_means(0, n_occ, [&](int p) { return stage + (size_t)sortj[p] * C; });
+    } else if (ext) {
+        staged_means(0, n_occ, [&](int p) {
+            const int j = sortj[p];
+            return j < cap_pre ? stage + (size_t)j * C : xstage + (size_t)(j - cap_pre) * C;
+        });
     } else {
         auto seg_end = [&](int o) { return o < n_occ ? (int)start[occ[o]] : ns; };
         int oa = 0;
@@ -1218,7 +1257,7 @@ __global__ __launch_bounds__(NT) void pv_voxel_slab_kernel(
                         st[(size_t)r * C + q] = fb[(size_t)sortk[pa + r] * feat_ld + q];
             }
             sync();
-            staged_means(oa, ob, (const FT*)s_stage, [&](int p) { return p - pa; });
+            staged_means(oa, ob, [&](int p) { return stage + (size_t)(p - pa) * C; });
             sync();  // the stage is free again
             oa = ob;
         }
