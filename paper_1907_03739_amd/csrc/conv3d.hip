@@ -110,18 +110,24 @@ __device__ __forceinline__ uint4 bload8_elems(__amdgpu_buffer_rsrc_t r, int voff
 // waves, two per SIMD). SB: compact halo buffers and at most 128
 // accumulator registers, so that two workgroups share a CU and one's
 // prologue and epilogue overlap the other's MFMAs.
+// SP (with occ, the forward's first convolution on its sparse grid): an
+// MFMA whose 32 input voxels are all empty adds only zeros to accumulators
+// that started at +0, so it is skipped (same bits). A bitmap of the halo's
+// occupied voxels (one word per halo row) gives each wave, once per brick,
+// which of its blocks have an occupied input voxel at each tap.
 // Split-K (ksplit > 1): the input channels' chunks are divided among ksplit
 // groups of workgroups (cps chunks each); split s reads channels from
 // s*cps*16 (rows of x_ld elements), and writes its fp32 partial sums, without
 // batch norm or activation, to y + s*B*R^3*Cout (the caller passes an
 // identity fold and no activation); pv_conv_split_reduce_kernel adds them.
-template <int NB, int WCH, bool VEC, bool SB = false>
+template <int NB, int WCH, bool VEC, bool SB = false, bool SP = false>
 __global__ __launch_bounds__(256 * WCH, SB ? 2 : 1) void pv_conv3d_bf16_kernel(
     const uint16_t* __restrict__ x, const uint16_t* __restrict__ wpk, PvBnFold bn, int act,
     float slope, void* __restrict__ y, int out_bf16, int vec_out, int R, int Cin, int Cout,
     int nbr, int nblocks, int x_ld, int ksplit, int cps, int B, const int32_t* __restrict__ occ) {
     __shared__ __attribute__((aligned(16))) char lds[SB ? kLdsBytesSB : kLdsBytes];
     __shared__ float bn_tab[2][NB * 32];  // folded scale and shift per output channel
+    __shared__ uint32_t occ_row[SP ? kHalo * kHalo : 1];  // SP: occupied w of each halo row
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     // Blocks are dispatched round-robin over the 8 XCDs; give each XCD a
@@ -194,6 +200,10 @@ __global__ __launch_bounds__(256 * WCH, SB ? 2 : 1) void pv_conv3d_bf16_kernel(
         x + cloud * x_ld + ulo * slab, (uint32_t)(((uhi - ulo) * slab - (x_ld - Cin)) * 2));
     const int pq = tid & 1;
     int goff[kSets], loff[kSets];
+    if constexpr (SP) {
+        if (tid < kHalo * kHalo) occ_row[tid] = 0u;
+        __syncthreads();
+    }
 #pragma unroll
     for (int set = 0; set < kSets; set++) {
         const int h = min(set * (NTH / 2) + (tid >> 1), kHaloVox - 1);
@@ -203,6 +213,8 @@ __global__ __launch_bounds__(256 * WCH, SB ? 2 : 1) void pv_conv3d_bf16_kernel(
         // a sparse input grid: empty voxels read as zero (their rows were
         // never written), through the out-of-range offset
         if (occ && in) in = occ[cloud + ((size_t)gu * R + gv) * R + gw] > 0;
+        if constexpr (SP)
+            if (in && pq == 0) atomicOr(&occ_row[hu * kHalo + hv], 1u << hw);
         goff[set] = in ? ((((gu - ulo) * R + gv) * R + gw) * x_ld + pq * 8) * 2 : kOOB;
         loff[set] = SB ? (hu * kHalo + hv) * kRowPitchSB + hw * kVoxPitchSB + half_off(hw, pq)
                        : (hu * kHalo + hv) * kRowPitch + hw * kVoxPitch + pq * 16;
@@ -252,6 +264,27 @@ __global__ __launch_bounds__(256 * WCH, SB ? 2 : 1) void pv_conv3d_bf16_kernel(
 #pragma unroll
         for (int set = 0; set < kSets; set++) any |= goff[set] != kOOB;
         live = __syncthreads_or(any);
+    }
+    // SP: bit 10*tv + w of msk[mb][tu] is set when block mb's input row
+    // (tu, tv) holds an occupied voxel at halo w; the block's fragment at tap
+    // (tu, tv, tw) covers w = tw .. tw + 7 of four such rows.
+    uint32_t msk[4][3];
+    if constexpr (SP) {
+#pragma unroll
+        for (int mb = 0; mb < 4; mb++)
+#pragma unroll
+            for (int tu = 0; tu < 3; tu++) {
+                uint32_t m = 0u;
+#pragma unroll
+                for (int tv = 0; tv < 3; tv++) {
+                    uint32_t r = 0u;
+#pragma unroll
+                    for (int k = 0; k < 4; k++)
+                        r |= occ_row[(2 * wv + (mb >> 1) + tu) * kHalo + (mb & 1) * 4 + tv + k];
+                    m |= r << (10 * tv);
+                }
+                msk[mb][tu] = __builtin_amdgcn_readfirstlane(m);
+            }
     }
     if (live) {
         // Chunk 0's halo, the weights of the first kWD taps.
@@ -310,11 +343,20 @@ __global__ __launch_bounds__(256 * WCH, SB ? 2 : 1) void pv_conv3d_bf16_kernel(
                         bf[nxt][mb] = *(const pv_bf16x8*)(lds + frag_addr(mb, t + 1) + cur_off);
                 }
 #pragma unroll
-                for (int mb = 0; mb < 4; mb++)
+                for (int mb = 0; mb < 4; mb++) {
+                    if constexpr (SP) {
+                        // opaque here, so that the test stays a scalar shift,
+                        // mask and branch inside the loop (hoisted, the 108
+                        // tests of a chunk would not fit in scalar registers)
+                        uint32_t mm = msk[mb][t / 9];
+                        asm volatile("" : "+s"(mm));
+                        if (((mm >> (10 * ((t / 3) % 3) + t % 3)) & 0xffu) == 0u) continue;
+                    }
 #pragma unroll
                     for (int nb = 0; nb < NBW; nb++)
                         acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
                             wf[t % kWR][nb], bf[cur][mb], acc[mb][nb], 0, 0, 0);
+                }
                 __builtin_amdgcn_sched_barrier(0);
             }
             // chunk done: the next halo is complete and this buffer is free
@@ -558,15 +600,18 @@ void launch_bf16(const void* x, int B, int R, int Cin, int Cout, const void* w,
         (size_t)B * nbr * nbr * nbr * ((Cout + NB * 32 - 1) / (NB * 32)) * ksplit;
     // 16-byte stores: aligned output with rows of whole 16-byte pieces
     const bool vec_out = pv_aligned16(y) && ((size_t)Cout * (out_bf16 ? 2 : 4)) % 16 == 0;
-#define PV_CONV(V)                                                                          \
-    hipLaunchKernelGGL((pv_conv3d_bf16_kernel<NB, WCH, V, SB>), dim3((unsigned)blocks),     \
+#define PV_CONV(V, SPX)                                                                     \
+    hipLaunchKernelGGL((pv_conv3d_bf16_kernel<NB, WCH, V, SB, SPX>), dim3((unsigned)blocks),\
                        dim3(256 * WCH), 0, s, (const uint16_t*)x, (const uint16_t*)w, bn, act, \
                        slope, y, (int)out_bf16, (int)vec_out, R, Cin, Cout, nbr, (int)blocks, \
                        Cin, ksplit, cps, B, occ)
-    if (vec)
-        PV_CONV(true);
+    // a sparse input on the two-per-CU form skips its empty fragments' MFMAs
+    if (vec && SB && occ)
+        PV_CONV(true, SB);
+    else if (vec)
+        PV_CONV(true, false);
     else
-        PV_CONV(false);
+        PV_CONV(false, false);
 #undef PV_CONV
 }
 
