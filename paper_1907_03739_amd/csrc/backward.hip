@@ -461,32 +461,57 @@ __device__ __forceinline__ void load4<uint16_t>(const uint16_t* p, float* v) {
 }
 
 // dz may alias dy (each element is read, then written, by one thread).
-template <typename YT, bool V4>
+// TAB: the folded BN scale of each channel is formed once per workgroup into
+// LDS (pv_bn_coeffs, so the same bits as forming it per element); each
+// thread keeps U groups of E elements in flight.
+template <typename YT, bool V4, bool TAB>
 __global__ __launch_bounds__(256) void pv_act_bn_backward_kernel(
     const float* dy, const YT* __restrict__ y, PvBnFold bn, float neg, float* dz, int C,
     size_t n) {
-    const size_t stride = (size_t)gridDim.x * 256;
-    constexpr int E = V4 ? 4 : 1;
-    for (size_t j = ((size_t)blockIdx.x * 256 + threadIdx.x) * E; j < n; j += stride * E) {
-        const int c = (int)(j % C);
-        float yv[E], g[E];
-        if (V4) {
-            load4<YT>(y + j, yv);
-            load4<float>(dy + j, g);
-        } else {
-            yv[0] = load1<YT>(y + j);
-            g[0] = dy[j];
+    extern __shared__ float s_scale[];  // TAB: [C]
+    if constexpr (TAB) {
+        for (int c = threadIdx.x; c < C; c += 256) {
+            float scale, shift;
+            pv_bn_coeffs(bn, c, scale, shift);
+            s_scale[c] = scale;
+        }
+        __syncthreads();
+    }
+    constexpr int E = V4 ? 4 : 1, U = 4;
+    const size_t step = (size_t)gridDim.x * 256 * E;
+    for (size_t j0 = ((size_t)blockIdx.x * 256 + threadIdx.x) * E; j0 < n; j0 += step * U) {
+        float yv[U][E], g[U][E];
+#pragma unroll
+        for (int u = 0; u < U; u++) {
+            const size_t j = j0 + u * step;
+            if (j >= n) continue;
+            if (V4) {
+                load4<YT>(y + j, yv[u]);
+                load4<float>(dy + j, g[u]);
+            } else {
+                yv[u][0] = load1<YT>(y + j);
+                g[u][0] = dy[j];
+            }
         }
 #pragma unroll
-        for (int e = 0; e < E; e++) {
-            float scale, shift;
-            pv_bn_coeffs(bn, c + e, scale, shift);
-            g[e] = g[e] * (yv[e] > 0.f ? 1.f : neg) * scale;
+        for (int u = 0; u < U; u++) {
+            const size_t j = j0 + u * step;
+            if (j >= n) continue;
+            const int c = (int)(j % C);
+#pragma unroll
+            for (int e = 0; e < E; e++) {
+                float scale, shift;
+                if (TAB)
+                    scale = s_scale[c + e];
+                else
+                    pv_bn_coeffs(bn, c + e, scale, shift);
+                g[u][e] = g[u][e] * (yv[u][e] > 0.f ? 1.f : neg) * scale;
+            }
+            if (V4)
+                *(float4*)(dz + j) = make_float4(g[u][0], g[u][1], g[u][2], g[u][3]);
+            else
+                dz[j] = g[u][0];
         }
-        if (V4)
-            *(float4*)(dz + j) = make_float4(g[0], g[1], g[2], g[3]);
-        else
-            dz[j] = g[0];
     }
 }
 
@@ -897,10 +922,17 @@ pvconv_status pv_launch_act_bn_backward(const float* dy, const void* y, bool y_b
                     ((uintptr_t)y & (y_bf16 ? 7 : 15)) == 0;
     const size_t per = v4 ? 4 : 1;
     const unsigned blocks = (unsigned)std::min<size_t>((n / per + 255) / 256, 8192);
+    // the scale table takes C floats of LDS (up to 64 KB)
+    const bool tab = C <= 16384;
     auto go = [&](auto yt, auto v4t) {
         typedef decltype(yt) YT;
-        hipLaunchKernelGGL((pv_act_bn_backward_kernel<YT, decltype(v4t)::value>), dim3(blocks),
-                           dim3(256), 0, s, dy, (const YT*)y, bn, neg, dz, C, n);
+        if (tab)
+            hipLaunchKernelGGL((pv_act_bn_backward_kernel<YT, decltype(v4t)::value, true>),
+                               dim3(blocks), dim3(256), (size_t)C * sizeof(float), s, dy,
+                               (const YT*)y, bn, neg, dz, C, n);
+        else
+            hipLaunchKernelGGL((pv_act_bn_backward_kernel<YT, decltype(v4t)::value, false>),
+                               dim3(blocks), dim3(256), 0, s, dy, (const YT*)y, bn, neg, dz, C, n);
     };
     if (y_bf16) {
         if (v4) go(uint16_t{}, std::true_type{}); else go(uint16_t{}, std::false_type{});
