@@ -282,6 +282,31 @@ def test_voxelize_small_clouds_sum_in_point_order(wl_idx, B, N, R, C):
     assert torch.equal(gb.cpu()[torch.as_tensor(light)], want)
 
 
+def test_voxelize_dense_slabs_past_the_stage():
+    # Sixteen clouds of 2048 points at R = 32 give slabs of 2048 voxels. A
+    # slab's LDS stage holds 384 rows of 64 fp32 channels; cloud 0 packs
+    # ~460 points into one slab (the rest of its rows are staged after the
+    # sort in the sort's tables, up to 492), cloud 1 ~720 (beyond that:
+    # segments). Both must give the oracle's grid, light voxels bit for bit.
+    rng = np.random.default_rng(21)
+    B, N, R, C = 16, 2048, 32, 64
+    coords = rng.uniform(-1, 1, (B, N, 3)).astype(np.float32)
+    for b, k in ((0, 280), (1, 560)):  # a thin layer across x: one or two u-slices
+        coords[b, :k, 0] = rng.uniform(0.30, 0.32, k).astype(np.float32)
+    feats = rng.normal(size=(B, N, C)).astype(np.float32)
+    pn, ids, grid, counts = _oracle_vox(coords, feats, R)
+    dense = [int(np.bincount(ids[b] // 2048, minlength=16).max()) for b in range(3)]
+    assert 384 < dense[0] <= 492 < dense[1] and dense[2] <= 384, dense
+    g1, c1, _, _ = pv.pvconv_voxelize(dev(coords), dev(feats), R, grid_dtype=torch.float32)
+    g2, c2, _, _ = pv.pvconv_voxelize(dev(coords), dev(feats), R, grid_dtype=torch.float32)
+    assert torch.equal(g1, g2) and torch.equal(c1, c2)
+    assert np.array_equal(c1.cpu().numpy(), counts)
+    got = g1.cpu().numpy()
+    light = (counts >= 1) & (counts <= 16)
+    assert np.array_equal(got[light], grid[light].astype(np.float32))
+    assert_rel(got, grid, 1e-5, "dense-slab grid fp32")
+
+
 def test_voxelize_is_deterministic_and_permutation_equivariant():
     coords, feats = _cloud(5, 1, 65536, 64)
     g1, c1, i1, p1 = pv.pvconv_voxelize(dev(coords), dev(feats), 64)
