@@ -222,13 +222,17 @@ def test_conv3d_backward_weight_is_deterministic_and_the_adjoint_on_gpu():
     assert abs(lhs - rhs) <= 1e-5 * scale, (lhs, rhs, scale)
 
 
-@pytest.mark.parametrize("ydt,act,with_bn", [
-    ("f32", "leaky", True), ("bf16", "leaky", True), ("f32", "relu", True),
-    ("bf16", "none", False), ("f32", "leaky", False),
+@pytest.mark.parametrize("ydt,act,with_bn,M,C", [
+    ("f32", "leaky", True, 20000, 96), ("bf16", "leaky", True, 20000, 96),
+    ("f32", "relu", True, 20000, 96), ("bf16", "none", False, 20000, 96),
+    ("f32", "leaky", False, 20000, 96),
+    # a channel count that is no multiple of 4 (element by element); more
+    # channels than the per-channel scale table holds (scales per element)
+    ("bf16", "leaky", True, 3001, 13), ("f32", "leaky", True, 40, 16500),
+    ("bf16", "relu", True, 7, 16387),
 ])
-def test_act_bn_backward_matches_oracle(ydt, act, with_bn):
+def test_act_bn_backward_matches_oracle(ydt, act, with_bn, M, C):
     rng = np.random.default_rng(5)
-    M, C = 20000, 96
     bn = synth.draw_bn(rng, C) if with_bn else None
     y = rng.normal(size=(M, C)).astype(np.float32).astype(np.float64)
     if ydt == "bf16":
