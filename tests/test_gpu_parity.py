@@ -785,14 +785,26 @@ def test_forward_part_seg_full_size_every_element():
     assert_bf16_step(got, ref16, "part-seg layer vs bf16-stage oracle")
 
 
-def test_composed_entry_points_give_the_forward_bits():
+@pytest.mark.parametrize("cloud", ["workload", "uniform", "clustered"])
+def test_composed_entry_points_give_the_forward_bits(cloud):
     # the layer as separate C-ABI calls (voxelise, two convolutions on packed
     # weights, the fused devoxelisation + point MLP) is the forward's own
-    # sequence of kernels: the same bits at full size
+    # sequence of kernels: the same bits at full size. Inside the forward the
+    # first convolution runs on the sparse grid and skips the MFMAs of empty
+    # fragments; clouds of different occupancy (points spread through the
+    # cube, or packed into a few blobs) exercise that.
     wl = synth.make_workload(2)
     L = wl.layers[0]
     layer = pv.DeviceLayer(L, "cuda", torch.bfloat16)
-    coords, feats = dev(wl.coords), dev(wl.feats)
+    xyz = wl.coords
+    rng = np.random.default_rng(31)
+    if cloud == "uniform":
+        xyz = rng.uniform(-1, 1, xyz.shape).astype(np.float32)
+    elif cloud == "clustered":
+        centres = rng.uniform(-1, 1, (xyz.shape[0], 4, 1, 3))
+        blobs = centres + 0.03 * rng.normal(size=(xyz.shape[0], 4, xyz.shape[1] // 4, 3))
+        xyz = blobs.reshape(xyz.shape).astype(np.float32)
+    coords, feats = dev(xyz), dev(wl.feats)
     want = pv.pvconv_forward(coords, feats, layer)
     grid, _, _, pn = pv.pvconv_voxelize(coords, feats, L.R, grid_dtype=torch.bfloat16)
     h = grid
