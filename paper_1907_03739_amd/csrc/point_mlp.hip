@@ -805,7 +805,7 @@ pvconv_status pv_launch_point_mlp(const void* x, bool x_bf16, int x_ld, int M, i
         // wide layers: LDS-tiled GEMM, 256 x 256 (channels x points) tiles of
         // eight waves (two per SIMD, 128 x 64 each) when they still give a
         // workgroup per CU, else eight-wave 128 x 256 (128 x 32 each) or
-        // four-wave 128 x 128 tiles
+        // 128 x 128 tiles (eight waves of 64 x 32)
         const long big_tiles = (long)((Cout + 255) / 256) * ((M + 255) / 256);
         if (tile && Cin >= 128 && Cout >= 256 && big_tiles >= 256) {
             if (x_bf16)
@@ -817,14 +817,15 @@ pvconv_status pv_launch_point_mlp(const void* x, bool x_bf16, int x_ld, int M, i
             return pv_launch_status();
         }
         // 128 x 128 tiles where 128 x 256 would leave CUs idle (e.g. the head's
-        // 256-wide first layer: 34 % faster)
+        // 256-wide first layer: 34 % faster), of eight waves so that two share
+        // each SIMD (2 % on the part-segmentation network against four)
         const long mid_tiles = (long)((Cout + 127) / 128) * ((M + 255) / 256);
         if (tile && Cin >= 128 && Cout >= 128 && mid_tiles < 256) {
             if (x_bf16)
-                launch_lds<4, 1, 1, 4, uint16_t>(x, x_ld, M, Cin, Cout, w, bn, act, slope, cb, ppc,
+                launch_lds<2, 1, 2, 4, uint16_t>(x, x_ld, M, Cin, Cout, w, bn, act, slope, cb, ppc,
                                                  res, res_ld, out, out_bf16, out_ld, s);
             else
-                launch_lds<4, 1, 1, 4, float>(x, x_ld, M, Cin, Cout, w, bn, act, slope, cb, ppc,
+                launch_lds<2, 1, 2, 4, float>(x, x_ld, M, Cin, Cout, w, bn, act, slope, cb, ppc,
                                               res, res_ld, out, out_bf16, out_ld, s);
             return pv_launch_status();
         }
