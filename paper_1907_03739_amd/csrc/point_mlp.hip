@@ -17,6 +17,8 @@
 // trilinear devoxelisation of the bf16 grid, which the kernel's DV variant
 // gathers itself (pv_launch_devox_point_mlp): one launch fewer and no fp32
 // intermediate rows in HBM.
+#include <type_traits>
+
 #include "pv_common.h"
 #include "pv_trilinear.h"
 
@@ -409,8 +411,11 @@ __global__ __launch_bounds__(64 * WN * WM, 1) void pv_point_mlp_lds_kernel(
     // The columns past C_in are zeroed when the chunk is stored to LDS, not
     // when it is loaded: a select right after the load would make the wave
     // wait for the load there, before the MFMAs it is meant to overlap.
-    uint4 stage[S::PIECES];
-    auto stage_load = [&](int k0) {
+    // Two register sets (see kD below); past the last chunk the loads re-read
+    // column 0 (stored as zeros, never used), so that every load is
+    // unconditional and the wait counts stay exact.
+    uint4 stage[2][S::PIECES];
+    auto stage_load = [&](int set, int k0) {
         const bool ok = k0 + part * 8 < Cin;
         const int k = ok ? k0 : 0;
 #pragma unroll
@@ -421,15 +426,15 @@ __global__ __launch_bounds__(64 * WN * WM, 1) void pv_point_mlp_lds_kernel(
                 v = piece_bf16(wsrc + (size_t)min(n0 + row, Cout - 1) * Cin + k);
             else
                 v = piece_bf16(xsrc + (size_t)min(m0 + row - S::TN, M - 1) * x_ld + k);
-            stage[i] = v;
+            stage[set][i] = v;
         }
     };
-    auto stage_store = [&](int buf, int k0) {
+    auto stage_store = [&](int buf, int set, int k0) {
         const bool ok = k0 + part * 8 < Cin;
         char* base = lds + buf * (S::ROWS * kGPitch) + (tid >> 3) * kGPitch + part * 16;
 #pragma unroll
         for (int i = 0; i < S::PIECES; i++)
-            *(uint4*)(base + i * S::RSET * kGPitch) = ok ? stage[i] : uint4{0u, 0u, 0u, 0u};
+            *(uint4*)(base + i * S::RSET * kGPitch) = ok ? stage[set][i] : uint4{0u, 0u, 0u, 0u};
     };
 
     const int wn = wave % WN, wm = wave / WN;
@@ -446,12 +451,21 @@ __global__ __launch_bounds__(64 * WN * WM, 1) void pv_point_mlp_lds_kernel(
             for (int e = 0; e < 16; e++) acc[i][j][e] = 0.f;
 
     const int nch = (Cin + kGK - 1) / kGK;
-    stage_load(0);
-    stage_store(0, 0);
+    // Chunk j is staged through register set j % 2 and LDS buffer j % 2.
+    // Loads run kD chunks ahead: two, unless fp32 rows of eight pieces a
+    // thread make two sets too many registers.
+    constexpr int kD = std::is_same<XT, float>::value && S::PIECES >= 8 ? 1 : 2;
+    stage_load(0, 0);
+    if (kD == 2) stage_load(1, kGK);
+    stage_store(0, 0, 0);
     __syncthreads();
-    for (int c = 0; c < nch; c++) {
-        if (c + 1 < nch) stage_load((c + 1) * kGK);
-        const char* buf = lds + (c & 1) * (S::ROWS * kGPitch);
+    // chunk c (parity P = c % 2, a compile-time index into the register
+    // sets): chunk c + kD loads, the MFMAs read LDS buffer P, then chunk c + 1
+    // is stored from its set to buffer 1 - P
+    auto chunk = [&](int c, auto parity) {
+        constexpr int P = decltype(parity)::value;
+        stage_load(kD == 2 ? P : 1 - P, (c + kD) * kGK);
+        const char* buf = lds + P * (S::ROWS * kGPitch);
 #pragma unroll
         for (int ks = 0; ks < kGK / 16; ks++) {
             pv_bf16x8 a[NB], b[MB];
@@ -468,9 +482,12 @@ __global__ __launch_bounds__(64 * WN * WM, 1) void pv_point_mlp_lds_kernel(
                     acc[mb][nb] =
                         __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[nb], b[mb], acc[mb][nb], 0, 0, 0);
         }
-        if (c + 1 < nch) stage_store((c + 1) & 1, (c + 1) * kGK);
-
+        if (c + 1 < nch) stage_store(1 - P, 1 - P, (c + 1) * kGK);
         __syncthreads();
+    };
+    for (int c = 0; c < nch; c += 2) {
+        chunk(c, std::integral_constant<int, 0>{});
+        if (c + 1 < nch) chunk(c + 1, std::integral_constant<int, 1>{});
     }
 
     // Epilogue, one (32-point block mb, 32-channel block nb) at a time.
