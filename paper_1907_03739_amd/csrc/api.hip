@@ -590,11 +590,16 @@ pvconv_status pvconv_forward_ex(const float* coords, const void* feats, pvconv_d
     void* src = w.grid_a;
     void* dst = w.grid_b;
     int cin = L->cin;
+    // The last convolution's grid is read only by the devoxelisation, at
+    // its points' corners (trilinear) or voxels (nearest), all within one
+    // voxel of an occupied voxel: only those outputs are computed.
     for (int i = 0; i < L->n_convs; i++) {
+        const bool last = i == L->n_convs - 1;
         st = pv_launch_conv3d(src, B, R, cin, L->cout, L->conv_w[i],
                               pv_make_fold(&L->conv_bn[i], nullptr), PVCONV_ACT_LEAKY,
                               L->conv_slope, bf, dst, bf, w.conv_ws[i], s, /*packed=*/bf,
-                              w.split, i == 0 && sparse ? w.counts : nullptr);
+                              w.split, i == 0 && sparse ? w.counts : nullptr,
+                              last && bf && (i > 0 || sparse) ? w.counts : nullptr);
         if (st != PVCONV_OK) return st;
         void* t = src;
         src = dst;

@@ -115,19 +115,28 @@ __device__ __forceinline__ uint4 bload8_elems(__amdgpu_buffer_rsrc_t r, int voff
 // that started at +0, so it is skipped (same bits). A bitmap of the halo's
 // occupied voxels (one word per halo row) gives each wave, once per brick,
 // which of its blocks have an occupied input voxel at each tap.
+// OS (with need, the forward's last convolution, whose grid the
+// devoxelisation samples only at its points' trilinear corners, all within
+// one voxel of an occupied voxel): a block of 32 output voxels with no
+// occupied voxel within one voxel skips its MFMAs, a wave with no such block
+// also its fragment reads, and a workgroup with no such wave returns before
+// loading anything; the outputs they leave are not needed (their values are
+// unspecified, those of needed voxels the same bits as the full loop's).
 // Split-K (ksplit > 1): the input channels' chunks are divided among ksplit
 // groups of workgroups (cps chunks each); split s reads channels from
 // s*cps*16 (rows of x_ld elements), and writes its fp32 partial sums, without
 // batch norm or activation, to y + s*B*R^3*Cout (the caller passes an
 // identity fold and no activation); pv_conv_split_reduce_kernel adds them.
-template <int NB, int WCH, bool VEC, bool SB = false, bool SP = false>
+template <int NB, int WCH, bool VEC, bool SB = false, bool SP = false, bool OS = false>
 __global__ __launch_bounds__(256 * WCH, SB ? 2 : 1) void pv_conv3d_bf16_kernel(
     const uint16_t* __restrict__ x, const uint16_t* __restrict__ wpk, PvBnFold bn, int act,
     float slope, void* __restrict__ y, int out_bf16, int vec_out, int R, int Cin, int Cout,
-    int nbr, int nblocks, int x_ld, int ksplit, int cps, int B, const int32_t* __restrict__ occ) {
+    int nbr, int nblocks, int x_ld, int ksplit, int cps, int B, const int32_t* __restrict__ occ,
+    const int32_t* __restrict__ need) {
     __shared__ __attribute__((aligned(16))) char lds[SB ? kLdsBytesSB : kLdsBytes];
     __shared__ float bn_tab[2][NB * 32];  // folded scale and shift per output channel
-    __shared__ uint32_t occ_row[SP ? kHalo * kHalo : 1];  // SP: occupied w of each halo row
+    // SP, OS: occupied w of each halo row
+    __shared__ uint32_t occ_row[SP || OS ? kHalo * kHalo : 1];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     // Blocks are dispatched round-robin over the 8 XCDs; give each XCD a
@@ -200,7 +209,7 @@ __global__ __launch_bounds__(256 * WCH, SB ? 2 : 1) void pv_conv3d_bf16_kernel(
         x + cloud * x_ld + ulo * slab, (uint32_t)(((uhi - ulo) * slab - (x_ld - Cin)) * 2));
     const int pq = tid & 1;
     int goff[kSets], loff[kSets];
-    if constexpr (SP) {
+    if constexpr (SP || OS) {
         if (tid < kHalo * kHalo) occ_row[tid] = 0u;
         __syncthreads();
     }
@@ -215,6 +224,9 @@ __global__ __launch_bounds__(256 * WCH, SB ? 2 : 1) void pv_conv3d_bf16_kernel(
         if (occ && in) in = occ[cloud + ((size_t)gu * R + gv) * R + gw] > 0;
         if constexpr (SP)
             if (in && pq == 0) atomicOr(&occ_row[hu * kHalo + hv], 1u << hw);
+        if constexpr (OS && !SP)
+            if (in && pq == 0 && need[cloud + ((size_t)gu * R + gv) * R + gw] > 0)
+                atomicOr(&occ_row[hu * kHalo + hv], 1u << hw);
         goff[set] = in ? ((((gu - ulo) * R + gv) * R + gw) * x_ld + pq * 8) * 2 : kOOB;
         loff[set] = SB ? (hu * kHalo + hv) * kRowPitchSB + hw * kVoxPitchSB + half_off(hw, pq)
                        : (hu * kHalo + hv) * kRowPitch + hw * kVoxPitch + pq * 16;
@@ -264,6 +276,29 @@ __global__ __launch_bounds__(256 * WCH, SB ? 2 : 1) void pv_conv3d_bf16_kernel(
 #pragma unroll
         for (int set = 0; set < kSets; set++) any |= goff[set] != kOOB;
         live = __syncthreads_or(any);
+    }
+    // OS: block mb's outputs (u-slice 2wv + mb/2, v rows (mb&1)*4 .. +3) and
+    // their neighbours are halo rows 2wv + mb/2 .. +2 by (mb&1)*4 .. +5, all
+    // ten w; bit mb of blive is set when one of them holds an occupied voxel.
+    // A brick with no live block has nothing to compute or store.
+    bool wave_live = true;
+    uint32_t blive = 15u;
+    if constexpr (OS) {
+        if constexpr (!SP) __syncthreads();  // the bitmap is complete
+        uint32_t bm = 0u;
+#pragma unroll
+        for (int mb = 0; mb < 4; mb++) {
+            uint32_t m = 0u;
+#pragma unroll
+            for (int du = 0; du < 3; du++)
+#pragma unroll
+                for (int dv = 0; dv < 6; dv++)
+                    m |= occ_row[(2 * wv + (mb >> 1) + du) * kHalo + (mb & 1) * 4 + dv];
+            bm |= (m != 0u ? 1u : 0u) << mb;
+        }
+        blive = __builtin_amdgcn_readfirstlane(bm);
+        wave_live = blive != 0u;
+        if (!__syncthreads_or(wave_live)) return;
     }
     // SP: bit 10*tv + w of msk[mb][tu] is set when block mb's input row
     // (tu, tv) holds an occupied voxel at halo w; the block's fragment at tap
@@ -337,13 +372,18 @@ __global__ __launch_bounds__(256 * WCH, SB ? 2 : 1) void pv_conv3d_bf16_kernel(
                 if (fetch && t >= kHaloLag && t < kSets + kHaloLag)
                     *(uint4*)(lds + loff[t - kHaloLag] + nxt_off) = hr[(t - kHaloLag) % kHaloLag];
                 if (fetch && t < kSets) hr[t % kHaloLag] = halo_load(t, cn);
-                if (t + 1 < kTaps) {
+                if (t + 1 < kTaps && (!OS || wave_live)) {
 #pragma unroll
                     for (int mb = 0; mb < 4; mb++)
                         bf[nxt][mb] = *(const pv_bf16x8*)(lds + frag_addr(mb, t + 1) + cur_off);
                 }
 #pragma unroll
-                for (int mb = 0; mb < 4; mb++) {
+                for (int mb = 0; mb < 4 && (!OS || wave_live); mb++) {
+                    if constexpr (OS) {
+                        uint32_t bb = blive;
+                        asm volatile("" : "+s"(bb));
+                        if (((bb >> mb) & 1u) == 0u) continue;
+                    }
                     if constexpr (SP) {
                         // opaque here, so that the test stays a scalar shift,
                         // mask and branch inside the loop (hoisted, the 108
@@ -594,24 +634,32 @@ __global__ __launch_bounds__(256) void pv_conv_split_reduce_kernel(
 template <int NB, int WCH, bool SB = false>
 void launch_bf16(const void* x, int B, int R, int Cin, int Cout, const void* w,
                  const PvBnFold& bn, int act, float slope, void* y, bool out_bf16, bool vec,
-                 hipStream_t s, int ksplit = 1, int cps = 0, const int32_t* occ = nullptr) {
+                 hipStream_t s, int ksplit = 1, int cps = 0, const int32_t* occ = nullptr,
+                 const int32_t* need = nullptr) {
     const int nbr = (R + kBrick - 1) / kBrick;
     const size_t blocks =
         (size_t)B * nbr * nbr * nbr * ((Cout + NB * 32 - 1) / (NB * 32)) * ksplit;
     // 16-byte stores: aligned output with rows of whole 16-byte pieces
     const bool vec_out = pv_aligned16(y) && ((size_t)Cout * (out_bf16 ? 2 : 4)) % 16 == 0;
-#define PV_CONV(V, SPX)                                                                     \
-    hipLaunchKernelGGL((pv_conv3d_bf16_kernel<NB, WCH, V, SB, SPX>), dim3((unsigned)blocks),\
+#define PV_CONV(V, SPX, OSX)                                                                \
+    hipLaunchKernelGGL((pv_conv3d_bf16_kernel<NB, WCH, V, SB, SPX, OSX>),                   \
+                       dim3((unsigned)blocks),                                                 \
                        dim3(256 * WCH), 0, s, (const uint16_t*)x, (const uint16_t*)w, bn, act, \
                        slope, y, (int)out_bf16, (int)vec_out, R, Cin, Cout, nbr, (int)blocks, \
-                       Cin, ksplit, cps, B, occ)
-    // a sparse input on the two-per-CU form skips its empty fragments' MFMAs
-    if (vec && SB && occ)
-        PV_CONV(true, SB);
+                       Cin, ksplit, cps, B, occ, need)
+    // a sparse input on the two-per-CU form skips its empty fragments' MFMAs,
+    // a needed-output mask its unneeded blocks, waves and bricks (given
+    // together, the two are the same counts)
+    if (vec && SB && occ && need)
+        PV_CONV(true, SB, SB);
+    else if (vec && SB && occ)
+        PV_CONV(true, SB, false);
+    else if (vec && SB && need)
+        PV_CONV(true, false, SB);
     else if (vec)
-        PV_CONV(true, false);
+        PV_CONV(true, false, false);
     else
-        PV_CONV(false, false);
+        PV_CONV(false, false, false);
 #undef PV_CONV
 }
 
@@ -666,7 +714,7 @@ size_t pv_conv3d_split_ws_bytes(int B, int R, int Cin, int Cout) {
 pvconv_status pv_launch_conv3d(const void* x, int B, int R, int Cin, int Cout, const void* w,
                                const PvBnFold& bn, int act, float slope, bool bf16, void* y,
                                bool out_bf16, void* ws, hipStream_t s, bool packed,
-                               float* split_ws, const int32_t* occ) {
+                               float* split_ws, const int32_t* occ, const int32_t* need) {
     if (B == 0) return PVCONV_OK;
     if (bf16) {
         if (!packed) {
@@ -709,7 +757,8 @@ pvconv_status pv_launch_conv3d(const void* x, int B, int R, int Cin, int Cout, c
         // accumulator registers and spill in its epilogue).
         const bool two = Cin <= 64;
         if (Cin <= 128 && Cout % 64 == 0 && bricks * (Cout / 64) >= 512) {
-            launch_bf16<2, 1, true>(x, B, R, Cin, Cout, w, bn, act, slope, y, out_bf16, vec, s, 1, 0, occ);
+            launch_bf16<2, 1, true>(x, B, R, Cin, Cout, w, bn, act, slope, y, out_bf16, vec, s, 1, 0, occ,
+                                    need);
         } else if (Cout % 64 == 0 && bricks * (Cout / 64) >= 256) {
             if (two)
                 launch_bf16<2, 2>(x, B, R, Cin, Cout, w, bn, act, slope, y, out_bf16, vec, s, 1, 0, occ);

@@ -172,11 +172,16 @@ __device__ __forceinline__ void pv_pack_role(const PvPackJobs& jobs, int blk,
 // small to fill the chip then split the input channels across workgroups
 // (fixed-order sum of the partials), else they run unsplit. occ: per-voxel
 // counts of the input grid [B][R^3] or nullptr; with it, input voxels of
-// count 0 read as zero and their rows are never read (a sparse grid).
+// count 0 read as zero and their rows are never read (a sparse grid). need:
+// per-voxel counts of the layer's points [B][R^3] or nullptr; with it only
+// the outputs within one voxel of an occupied voxel are computed (those a
+// devoxelisation of the points reads), the others left unspecified (where
+// given together, occ and need are the same counts).
 pvconv_status pv_launch_conv3d(const void* x, int B, int R, int Cin, int Cout, const void* w,
                                const PvBnFold& bn, int act, float slope, bool bf16, void* y,
                                bool out_bf16, void* ws, hipStream_t s, bool packed = false,
-                               float* split_ws = nullptr, const int32_t* occ = nullptr);
+                               float* split_ws = nullptr, const int32_t* occ = nullptr,
+                               const int32_t* need = nullptr);
 int pv_conv3d_splits(int B, int R, int Cin, int Cout);
 size_t pv_conv3d_split_ws_bytes(int B, int R, int Cin, int Cout);
 pvconv_status pv_launch_devoxelize(const void* grid, int B, int R, int C, bool grid_bf16,

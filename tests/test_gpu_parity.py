@@ -826,6 +826,36 @@ def test_composed_entry_points_give_the_forward_bits(cloud):
     assert torch.equal(got2, want)
 
 
+@pytest.mark.parametrize("n_convs,devox", [
+    (2, "trilinear"), (2, "nearest"), (1, "trilinear"), (1, "nearest"), (3, "trilinear"),
+])
+def test_forward_computes_every_voxel_the_devoxelisation_reads(n_convs, devox):
+    # Inside the forward the last convolution computes only the outputs
+    # within one voxel of an occupied voxel (the devoxelisation reads nothing
+    # else) and leaves the rest of its grid as the workspace held it. With
+    # the workspace full of NaN bytes, the output must still be the bits of
+    # the separate calls, whose grids are complete: no unneeded voxel is read.
+    wl = synth.make_workload(2)
+    L = synth.draw_pvconv(np.random.default_rng(50 + n_convs), 64, 128, 32, n_convs, bf16=True)
+    L.devox = devox
+    layer = pv.DeviceLayer(L, "cuda", torch.bfloat16)
+    coords, feats = dev(wl.coords), dev(wl.feats)
+    size = pv.pvconv_forward_workspace_size(wl.B, wl.N, layer)
+    ws = torch.full((size,), 0xFF, dtype=torch.uint8, device="cuda")
+    want = pv.pvconv_forward(coords, feats, layer, workspace=ws)
+    grid, _, ids, pn = pv.pvconv_voxelize(coords, feats, L.R, grid_dtype=torch.bfloat16)
+    h = grid
+    for i in range(L.n_convs):
+        h = pv.pvconv_conv3d(h, layer.conv_w[i], L.R, bn=layer.conv_bn[i], act="leaky",
+                             slope=L.slope, out_dtype=torch.bfloat16)
+    dv = (pv.pvconv_devoxelize_nearest(h, L.R, ids) if devox == "nearest"
+          else pv.pvconv_devoxelize(h, L.R, pn))
+    got = pv.pvconv_point_mlp(feats, layer.mlp_w, bias=layer.mlp_b, bn=layer.mlp_bn,
+                              act="relu", residual=dv)
+    assert torch.isfinite(want).all()
+    assert torch.equal(got, want)
+
+
 def test_forward_on_a_side_stream_and_repeatable():
     wl = synth.make_workload(2, B=2)
     layer = pv.DeviceLayer(wl.layers[0], "cuda", torch.bfloat16)
