@@ -117,10 +117,10 @@ __device__ __forceinline__ uint4 bload8_elems(__amdgpu_buffer_rsrc_t r, int voff
 // which of its blocks have an occupied input voxel at each tap.
 // OS (with need, the forward's last convolution, whose grid the
 // devoxelisation samples only at its points' trilinear corners, all within
-// one voxel of an occupied voxel): a block of 32 output voxels with no
-// occupied voxel within one voxel skips its MFMAs, a wave with no such block
-// also its fragment reads, and a workgroup with no such wave returns before
-// loading anything; the outputs they leave are not needed (their values are
+// one voxel of an occupied voxel): only the blocks of 32 output voxels with
+// an occupied voxel within one voxel run their MFMAs, dealt evenly to the
+// waves; a wave with none skips its fragment reads too, and a workgroup with
+// none returns before loading anything; the outputs they leave are not needed (their values are
 // unspecified, those of needed voxels the same bits as the full loop's).
 // Split-K (ksplit > 1): the input channels' chunks are divided among ksplit
 // groups of workgroups (cps chunks each); split s reads channels from
@@ -179,16 +179,30 @@ __global__ __launch_bounds__(256 * WCH, SB ? 2 : 1) void pv_conv3d_bf16_kernel(
     // SB: one base per w shift of the taps (the half swap depends on w).
     constexpr int RP = SB ? kRowPitchSB : kRowPitch, HB = SB ? kHaloBytesSB : kHaloBytes;
     auto half_off = [](int hw, int h) { return SB ? (h ^ ((hw >> 2) & 1)) * 16 : h * 16; };
+    // Slot mb of the wave computes the block at u-slice blk_u(mb), v rows
+    // blk_v(mb)*4 .. +3: 2*wave + mb/2 and mb&1, unless OS deals the blocks
+    // out (then slot mb holds block g = bits 4mb .. 4mb+3 of gpack, u-slice
+    // g/2, v half g&1).
+    uint32_t gpack = 0u;
+    auto blk_u = [&](int mb) -> int {
+        if constexpr (OS) return (int)((gpack >> (4 * mb + 1)) & 7u);
+        return 2 * wv + (mb >> 1);
+    };
+    auto blk_v = [&](int mb) -> int {
+        if constexpr (OS) return (int)((gpack >> (4 * mb)) & 1u);
+        return mb & 1;
+    };
     int bbase[4], bsw[4][3];
-#pragma unroll
-    for (int mb = 0; mb < 4; mb++) {
-        const int ul = 2 * wv + (mb >> 1), vl = (mb & 1) * 4 + (r32 >> 3), wl = r32 & 7;
+    auto place = [&](int mb, int ul, int vh) {
+        const int vl = vh * 4 + (r32 >> 3), wl = r32 & 7;
         bbase[mb] = (ul * kHalo + vl) * kRowPitch + wl * kVoxPitch + khalf * 16;
 #pragma unroll
         for (int tw = 0; tw < 3; tw++)
             bsw[mb][tw] = (ul * kHalo + vl) * kRowPitchSB + (wl + tw) * kVoxPitchSB +
                           half_off(wl + tw, khalf);
-    }
+    };
+#pragma unroll
+    for (int mb = 0; mb < 4; mb++) place(mb, 2 * wv + (mb >> 1), mb & 1);
     // LDS byte address (in buffer 0) of block mb's B fragment at tap tn
     auto frag_addr = [&](int mb, int tn) {
         const int tu = tn / 9, tv = (tn / 3) % 3, tw = tn % 3;
@@ -277,28 +291,46 @@ __global__ __launch_bounds__(256 * WCH, SB ? 2 : 1) void pv_conv3d_bf16_kernel(
         for (int set = 0; set < kSets; set++) any |= goff[set] != kOOB;
         live = __syncthreads_or(any);
     }
-    // OS: block mb's outputs (u-slice 2wv + mb/2, v rows (mb&1)*4 .. +3) and
-    // their neighbours are halo rows 2wv + mb/2 .. +2 by (mb&1)*4 .. +5, all
-    // ten w; bit mb of blive is set when one of them holds an occupied voxel.
-    // A brick with no live block has nothing to compute or store.
+    // OS: block g's outputs (u-slice g/2, v rows (g&1)*4 .. +3) and their
+    // neighbours are halo rows g/2 .. +2 by (g&1)*4 .. +5, all ten w; the
+    // block is live when one of them holds an occupied voxel. A brick with no
+    // live block has nothing to compute or store. The live blocks are dealt
+    // to the waves in turn (slot k of wave w takes the (4k + w)-th), so that
+    // the brick's busiest wave has ceil(live / 4) of them; bit k of blive
+    // marks a slot that holds one.
     bool wave_live = true;
     uint32_t blive = 15u;
     if constexpr (OS) {
         if constexpr (!SP) __syncthreads();  // the bitmap is complete
-        uint32_t bm = 0u;
-#pragma unroll
-        for (int mb = 0; mb < 4; mb++) {
+        bool lv = false;
+        if (lane < 16) {  // lane g tests block g
             uint32_t m = 0u;
 #pragma unroll
             for (int du = 0; du < 3; du++)
 #pragma unroll
                 for (int dv = 0; dv < 6; dv++)
-                    m |= occ_row[(2 * wv + (mb >> 1) + du) * kHalo + (mb & 1) * 4 + dv];
-            bm |= (m != 0u ? 1u : 0u) << mb;
+                    m |= occ_row[((lane >> 1) + du) * kHalo + (lane & 1) * 4 + dv];
+            lv = m != 0u;
         }
-        blive = __builtin_amdgcn_readfirstlane(bm);
+        const uint32_t bl = (uint32_t)__builtin_amdgcn_ballot_w64(lv);
+        if (bl == 0u) return;  // every wave reads the same bitmap
+        uint32_t m = bl;
+        const int ws = __builtin_amdgcn_readfirstlane(wv);
+        for (int i = 0; i < ws; i++) m &= m - 1u;
+        uint32_t gp = 0u, bv = 0u;
+#pragma unroll
+        for (int k = 0; k < 4; k++) {
+            const uint32_t g = m ? (uint32_t)__builtin_ctz(m) : 0u;  // idle: valid addresses
+            bv |= (m ? 1u : 0u) << k;
+            gp |= g << (4 * k);
+#pragma unroll
+            for (int i = 0; i < 4; i++) m &= m - 1u;  // past the next four live blocks
+        }
+        gpack = __builtin_amdgcn_readfirstlane(gp);
+        blive = __builtin_amdgcn_readfirstlane(bv);
+#pragma unroll
+        for (int k = 0; k < 4; k++) place(k, blk_u(k), blk_v(k));
         wave_live = blive != 0u;
-        if (!__syncthreads_or(wave_live)) return;
     }
     // SP: bit 10*tv + w of msk[mb][tu] is set when block mb's input row
     // (tu, tv) holds an occupied voxel at halo w; the block's fragment at tap
@@ -315,7 +347,7 @@ __global__ __launch_bounds__(256 * WCH, SB ? 2 : 1) void pv_conv3d_bf16_kernel(
                     uint32_t r = 0u;
 #pragma unroll
                     for (int k = 0; k < 4; k++)
-                        r |= occ_row[(2 * wv + (mb >> 1) + tu) * kHalo + (mb & 1) * 4 + tv + k];
+                        r |= occ_row[(blk_u(mb) + tu) * kHalo + blk_v(mb) * 4 + tv + k];
                     m |= r << (10 * tv);
                 }
                 msk[mb][tu] = __builtin_amdgcn_readfirstlane(m);
@@ -436,8 +468,9 @@ __global__ __launch_bounds__(256 * WCH, SB ? 2 : 1) void pv_conv3d_bf16_kernel(
                     const int cb = (nl - pass * PW) * esz;  // byte offset in the row
 #pragma unroll
                     for (int mb = 0; mb < 4; mb++) {
-                        const int vox = (2 * wv + (mb >> 1)) * 64 +
-                                        ((mb & 1) * 4 + (r32 >> 3)) * 8 + (r32 & 7);
+                        if (OS && ((blive >> mb) & 1u) == 0u) continue;  // an idle slot
+                        const int vox = blk_u(mb) * 64 + (blk_v(mb) * 4 + (r32 >> 3)) * 8 +
+                                        (r32 & 7);
                         float r[4] = {acc[mb][nb][4 * j + 0] * sc.x + sh.x,
                                       acc[mb][nb][4 * j + 1] * sc.y + sh.y,
                                       acc[mb][nb][4 * j + 2] * sc.z + sh.z,
