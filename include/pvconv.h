@@ -410,7 +410,9 @@ pvconv_status pvconv_forward(const float* coords, const void* feats, pvconv_dtyp
 /*    outputs (each may be NULL), as pvconv_voxelize writes them;            */
 /*  ids_given = 1: both are inputs (non-NULL) from such a call with the same */
 /*    coordinates and the same R; the normalisation is skipped and coords    */
-/*    is not read (may be NULL).                                             */
+/*    is not read (may be NULL). Indices that are not those of the given     */
+/*    normalised coordinates leave the output unspecified (memory-safe): the */
+/*    last convolution computes only the voxels near occupied ones.          */
 /* pvconv_forward(...) is pvconv_forward_ex(..., NULL, NULL, 0, ...).         */
 pvconv_status pvconv_forward_ex(const float* coords, const void* feats, pvconv_dtype feat_dt,
                                 int feat_ld, int B, int N, const pvconv_layer* L,
