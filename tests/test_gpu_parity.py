@@ -826,17 +826,19 @@ def test_composed_entry_points_give_the_forward_bits(cloud):
     assert torch.equal(got2, want)
 
 
-@pytest.mark.parametrize("n_convs,devox", [
-    (2, "trilinear"), (2, "nearest"), (1, "trilinear"), (1, "nearest"), (3, "trilinear"),
+@pytest.mark.parametrize("n_convs,devox,R", [
+    (2, "trilinear", 32), (2, "nearest", 32), (1, "trilinear", 32), (1, "nearest", 32),
+    (3, "trilinear", 32),
+    (2, "trilinear", 20),   # bricks cut by the grid's faces
 ])
-def test_forward_computes_every_voxel_the_devoxelisation_reads(n_convs, devox):
+def test_forward_computes_every_voxel_the_devoxelisation_reads(n_convs, devox, R):
     # Inside the forward the last convolution computes only the outputs
     # within one voxel of an occupied voxel (the devoxelisation reads nothing
     # else) and leaves the rest of its grid as the workspace held it. With
     # the workspace full of NaN bytes, the output must still be the bits of
     # the separate calls, whose grids are complete: no unneeded voxel is read.
     wl = synth.make_workload(2)
-    L = synth.draw_pvconv(np.random.default_rng(50 + n_convs), 64, 128, 32, n_convs, bf16=True)
+    L = synth.draw_pvconv(np.random.default_rng(50 + n_convs), 64, 128, R, n_convs, bf16=True)
     L.devox = devox
     layer = pv.DeviceLayer(L, "cuda", torch.bfloat16)
     coords, feats = dev(wl.coords), dev(wl.feats)
