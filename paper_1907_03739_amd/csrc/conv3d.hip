@@ -141,8 +141,19 @@ __global__ __launch_bounds__(256 * WCH, SB ? 2 : 1) void pv_conv3d_bf16_kernel(
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     // Blocks are dispatched round-robin over the 8 XCDs; give each XCD a
     // contiguous range of bricks so that neighbouring halos share its L2.
+    // With SP or OS a brick's work depends on its cloud's occupancy: there
+    // each XCD takes an eighth of every cloud (whole clouds per XCD left the
+    // XCDs that drew the denser clouds running long after the others).
     int bid = blockIdx.x;
-    if ((nblocks & 7) == 0) bid = (bid & 7) * (nblocks >> 3) + (bid >> 3);
+    const int per = nblocks / max(B, 1);  // workgroups per cloud
+    if ((SP || OS) && (per & 7) == 0 && per * B == nblocks) {
+        // every XCD takes one contiguous eighth of every cloud, rotated by
+        // the cloud, so that clouds of different occupancy share the XCDs
+        const int x = bid & 7, k = bid >> 3, c = k / (per >> 3), j = k % (per >> 3);
+        bid = c * per + ((x + c) & 7) * (per >> 3) + j;
+    } else if ((nblocks & 7) == 0) {
+        bid = (bid & 7) * (nblocks >> 3) + (bid >> 3);
+    }
     if (ksplit > 1) {  // this workgroup's share of the input channels
         const int split = bid % ksplit;
         bid /= ksplit;
